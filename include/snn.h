@@ -1,0 +1,204 @@
+/*
+ * snn.h -- C ABI of libsnn.so: spiking-layer training on one MI355X (gfx950).
+ *
+ * The library computes one feed-forward spiking layer at a time, unrolled
+ * over T time steps, and its backpropagation-through-time (BPTT) backward:
+ *
+ *   synapse   I[t,b,:] = W x[t,b,:] + bias     the "w x_t" term of eqs. (4)/(5);
+ *             dense, or a 5x5 valid convolution followed by 2x2 max-pooling
+ *             of the currents (the 5C12-MP2 / 5C64-MP2 layers of Table I)
+ *   neuron    Leaky (eq. 4):  u_t = beta u_{t-1} + I_t - z_{t-1} thr
+ *             Synaptic (eqs. 5-6): i_t = alpha i_{t-1} + I_t,
+ *                                  u_t = beta u_{t-1} + i_t - z_{t-1} thr
+ *             spike (eq. 3): z_t = 1 if u_t > thr (strict), else 0;
+ *             initial state u = i = 0, no spike before the first step
+ *   backward  the spike's derivative is replaced by the fast-sigmoid
+ *             surrogate of eqs. (8)-(9) with slope k:
+ *                 s_t = 1 / (1 + k |u_t - thr|)^2
+ *             lam_t = g_t s_t + (beta - r thr s_t) lam_{t+1}  (r = 1 only for
+ *             SNN_RESET_SURROGATE); Synaptic adds lami_t = lam_t + alpha lami_{t+1}.
+ *             dL/dI_t = lam_t (Leaky) or lami_t (Synaptic), then
+ *             dW = dI^T x, dbias = sum dI, dx = dI W.
+ *   loss      on output spike counts c = sum_t z_t (rate-coded readout, the
+ *             class is the neuron with most spikes, Sec. V): cross-entropy
+ *             with c as logits (mean over the batch) or mean-squared error.
+ *
+ * Conventions for every entry point:
+ *   - Tensor pointers are DEVICE pointers unless stated otherwise, row-major
+ *     and contiguous, time-major [T, B, features] with features fastest.
+ *     Every device pointer must be 16-byte aligned (SNN_ERR_ALIGN otherwise).
+ *   - The caller owns and allocates every buffer, including `saved` and the
+ *     workspace `ws` sized by the *_bytes queries.  The library allocates
+ *     nothing, keeps no state between calls and is reentrant across streams.
+ *   - Calls only enqueue work on `stream` (a hipStream_t; NULL = the null
+ *     stream) and never synchronise the device.  Arguments are validated on
+ *     the host before anything is launched; on error nothing is launched and
+ *     outputs are untouched.  A failed launch returns SNN_ERR_HIP.
+ *   - Outputs are overwritten, never accumulated into.
+ *   - Arithmetic: contractions accumulate in fp32 (operands fp32, or fp16
+ *     for SNN_F16 weights); neuron state is fp32; loss reductions in fp64.
+ *   - T == 0 or B == 0 is valid: no compute is launched, and outputs that
+ *     are sums over an empty range (counts, grad_w, grad_b) are set to 0.
+ *     A loss over B == 0 or K == 0 is rejected (SNN_ERR_SHAPE).
+ */
+#ifndef SNN_H
+#define SNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SNN_ABI_VERSION 1
+
+typedef enum snn_status {
+    SNN_OK = 0,
+    SNN_ERR_NULL = 1,        /* a required pointer is NULL */
+    SNN_ERR_SHAPE = 2,       /* sizes negative, inconsistent or too large */
+    SNN_ERR_DTYPE = 3,       /* dtype / format combination not supported */
+    SNN_ERR_ALIGN = 4,       /* a device pointer is not 16-byte aligned */
+    SNN_ERR_UNSUPPORTED = 5, /* valid request this build does not implement */
+    SNN_ERR_WORKSPACE = 6,   /* ws_bytes smaller than the query returned */
+    SNN_ERR_HIP = 7          /* a kernel launch failed */
+} snn_status;
+
+/* element types */
+#define SNN_F32 0
+#define SNN_F16 1
+#define SNN_BF16 2
+#define SNN_U8 3 /* spikes stored as bytes 0 / 1 */
+
+/* neuron models */
+#define SNN_LEAKY 0    /* eq. (4) */
+#define SNN_SYNAPTIC 1 /* eqs. (5)-(6) */
+
+/* synapse kinds */
+#define SNN_SYN_DENSE 0       /* x [T,B,n_in], w [n_out, n_in] */
+#define SNN_SYN_CONV5_POOL2 1 /* x [T,B,c_in,h_in,w_in], w [c_out,c_in,5,5];
+                                 currents [T,B,c_out,(h_in-4)/2,(w_in-4)/2] */
+#define SNN_SYN_NONE 2        /* x already holds fp32 currents [T,B,n_out] */
+
+/* gradient through the reset term -z_{t-1} thr */
+#define SNN_RESET_DETACHED 0  /* reset treated as a constant in the backward */
+#define SNN_RESET_SURROGATE 1 /* reset differentiated with the surrogate */
+
+/* kinds of upstream gradient dL/dz for snn_layer_bwd / snn_neuron_bwd */
+#define SNN_GRAD_FULL 0  /* g [T,B,n_out] fp32 */
+#define SNN_GRAD_BCAST 1 /* g [B,n_out] fp32, the same for every t (a loss on
+                            counts summed over T) */
+
+/* losses on spike counts */
+#define SNN_LOSS_CE_COUNT 0  /* labels int32 [B] in [0,K) */
+#define SNN_LOSS_MSE_COUNT 1 /* targets fp32 [B,K] */
+
+typedef struct snn_layer_desc {
+    int32_t T, B;           /* time steps, batch */
+    int32_t synapse;        /* SNN_SYN_* */
+    int32_t neuron;         /* SNN_LEAKY | SNN_SYNAPTIC */
+    int32_t n_in, n_out;    /* features per (t,b) of x and of the output;
+                               conv: c_in*h_in*w_in and c_out*hp*wp;
+                               SNN_SYN_NONE: n_in == n_out */
+    int32_t c_in, h_in, w_in, c_out; /* conv geometry, else ignored */
+    int32_t in_dtype;       /* x: SNN_U8 spikes, SNN_F32 (also SYN_NONE), SNN_F16 */
+    int32_t w_dtype;        /* w: SNN_F32 | SNN_F16 */
+    int32_t out_dtype;      /* spikes written as SNN_U8 | SNN_F16 (0.0 / 1.0) */
+    int32_t grad_dtype;     /* dL/dI handed to the weight / input gradient
+                               contractions: SNN_F32 | SNN_BF16 | SNN_F16 */
+    int32_t reset_grad;     /* SNN_RESET_DETACHED | SNN_RESET_SURROGATE */
+    int32_t flags;          /* must be 0 */
+    float beta;             /* membrane decay, eqs. (4)/(6) */
+    float alpha;            /* synaptic decay, eq. (5); ignored for Leaky */
+    float threshold;        /* u_thr */
+    float slope;            /* surrogate slope k (k = 1 is eq. (9) as printed) */
+} snn_layer_desc;
+
+typedef struct snn_grad_in {
+    int32_t kind;       /* SNN_GRAD_FULL | SNN_GRAD_BCAST */
+    int32_t reserved;   /* must be 0 */
+    const float *g;     /* dL/dz of this layer's output spikes, fp32 */
+} snn_grad_in;
+
+int snn_abi_version(void);
+const char *snn_status_str(snn_status s);
+
+/* Bytes of the forward-to-backward state: the membrane u_t after each step
+ * (fp32 [T,B,n_out]) and, for conv layers, the 2x2 pool selection (one byte
+ * per pooled current).  The backward needs nothing else: the surrogate only
+ * depends on u_t. */
+size_t snn_layer_saved_bytes(const snn_layer_desc *d);
+
+/* Scratch bytes needed by snn_layer_fwd / snn_layer_bwd and the stage calls
+ * below (the maximum over all of them).  0 is a valid answer. */
+size_t snn_layer_workspace_bytes(const snn_layer_desc *d);
+
+/* Forward of one layer (synapse, then the neuron scan over all T).
+ *   x       [T,B,n_in] of d->in_dtype
+ *   w       weights of d->w_dtype (NULL iff SNN_SYN_NONE)
+ *   bias    fp32 [n_out] dense / [c_out] conv, or NULL for no bias
+ *   spk_out [T,B,n_out] spikes of d->out_dtype
+ *   saved   snn_layer_saved_bytes(d) bytes, kept for snn_layer_bwd
+ *   counts  fp32 [B,n_out] spike counts sum_t z_t, or NULL
+ *   ws      snn_layer_workspace_bytes(d) bytes (may be NULL if 0) */
+snn_status snn_layer_fwd(const snn_layer_desc *d, const void *x, const void *w,
+                         const float *bias, void *spk_out, void *saved, float *counts,
+                         void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Backward of one layer (reverse-time neuron scan, then the synapse).
+ *   grad    upstream dL/dz of this layer's spikes
+ *   x, w    the forward's inputs; saved: the forward's saved state
+ *   grad_w  dL/dw (layout of w, fp32), NULL to skip; must be NULL for SYN_NONE
+ *   grad_b  dL/dbias fp32, NULL to skip
+ *   grad_x  dL/dx fp32 [T,B,n_in] (the g of the layer below), NULL to skip;
+ *           for SNN_SYN_NONE this is dL/dI and is required */
+snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const void *x,
+                         const void *w, const void *saved, float *grad_w, float *grad_b,
+                         float *grad_x, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* Loss on spike counts [B,K] and its gradient dL/dc [B,K] (which is dL/dz_t
+ * for every t, since dc/dz_t = 1).  `loss` is a device fp32 scalar.
+ * CE: L = mean_b (logsumexp(c_b) - c_b[y_b]),  g = (softmax(c_b) - onehot)/B.
+ * MSE: L = mean (c - y)^2,                    g = 2 (c - y) / (B K). */
+size_t snn_loss_workspace_bytes(int32_t kind, int32_t B, int32_t K);
+snn_status snn_loss(int32_t kind, int32_t B, int32_t K, const float *counts,
+                    const int32_t *labels, const float *targets, float *loss,
+                    float *grad_counts, void *ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---- stage calls: the two halves of snn_layer_fwd / snn_layer_bwd -------
+ * snn_layer_fwd == snn_synapse_fwd(cur = saved) + snn_neuron_fwd(cur = saved,
+ * saved_u = saved); snn_layer_bwd == snn_neuron_bwd + snn_synapse_bwd.  They
+ * let a caller time the contraction and the scan separately (the paper's
+ * split of time between synaptic and neuron work, Sec. IV) and check each
+ * stage on its own. */
+
+/* Currents I [T,B,n_out] fp32.  pool_arg: conv only, u8 [T,B,n_out] pool
+ * selection 0..3 (row-major in the 2x2 window, first maximum wins). */
+snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w,
+                           const float *bias, float *cur, uint8_t *pool_arg, void *ws,
+                           size_t ws_bytes, hipStream_t stream);
+
+/* Neuron scan over T.  cur and saved_u may be the same pointer (in place);
+ * any other overlap is undefined. */
+snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, void *spk_out,
+                          float *saved_u, float *counts, hipStream_t stream);
+
+/* Reverse-time scan: dcur = dL/dI [T,B,n_out] of d->grad_dtype, and
+ * grad_b (nullable) = sum of dL/dI over t, b (and pooled positions). */
+snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad,
+                          const float *saved_u, void *dcur, float *grad_b, void *ws,
+                          size_t ws_bytes, hipStream_t stream);
+
+/* Synapse backward from dcur (of d->grad_dtype): grad_w and/or grad_x. */
+snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
+                           const uint8_t *pool_arg, const void *x, const void *w,
+                           float *grad_w, float *grad_x, void *ws, size_t ws_bytes,
+                           hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SNN_H */

@@ -1,0 +1,348 @@
+"""MI355X-native spiking-layer training: time-stepped forward and BPTT backward.
+
+Thin ctypes binding over ``libsnn.so`` (C ABI declared in ``include/snn.h``).
+The functions below have the ABI's names and only marshal arguments: torch
+tensors supply device pointers and the HIP stream, every step of the method
+runs in the library's HIP kernels.  There is no CPU fallback: if the library
+is missing, the first call raises.
+
+``Network`` chains the layer calls of a feed-forward spiking network (layers
+ascending in the forward pass, loss on the output spike counts, layers
+descending in the backward pass), the training step the paper times
+(Sec. IV "Baseline Throughput", without the optimizer update).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import workloads  # noqa: F401  (seeded inputs; no method arithmetic)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsnn.so")
+
+# element types, neuron models, synapses, gradient kinds, losses (snn.h)
+F32, F16, BF16, U8 = 0, 1, 2, 3
+LEAKY, SYNAPTIC = 0, 1
+SYN_DENSE, SYN_CONV5_POOL2, SYN_NONE = 0, 1, 2
+RESET_DETACHED, RESET_SURROGATE = 0, 1
+GRAD_FULL, GRAD_BCAST = 0, 1
+LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
+ABI_VERSION = 1
+
+STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
+          4: "SNN_ERR_ALIGN", 5: "SNN_ERR_UNSUPPORTED", 6: "SNN_ERR_WORKSPACE",
+          7: "SNN_ERR_HIP"}
+
+EXPORTS = ["snn_abi_version", "snn_status_str", "snn_layer_saved_bytes",
+           "snn_layer_workspace_bytes", "snn_layer_fwd", "snn_layer_bwd",
+           "snn_loss_workspace_bytes", "snn_loss", "snn_synapse_fwd", "snn_neuron_fwd",
+           "snn_neuron_bwd", "snn_synapse_bwd"]
+
+
+class LayerDesc(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("B", ctypes.c_int32),
+                ("synapse", ctypes.c_int32), ("neuron", ctypes.c_int32),
+                ("n_in", ctypes.c_int32), ("n_out", ctypes.c_int32),
+                ("c_in", ctypes.c_int32), ("h_in", ctypes.c_int32),
+                ("w_in", ctypes.c_int32), ("c_out", ctypes.c_int32),
+                ("in_dtype", ctypes.c_int32), ("w_dtype", ctypes.c_int32),
+                ("out_dtype", ctypes.c_int32), ("grad_dtype", ctypes.c_int32),
+                ("reset_grad", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("beta", ctypes.c_float), ("alpha", ctypes.c_float),
+                ("threshold", ctypes.c_float), ("slope", ctypes.c_float)]
+
+    def copy(self):
+        d = LayerDesc()
+        ctypes.pointer(d)[0] = self
+        return d
+
+
+class GradIn(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("g", ctypes.c_void_p)]
+
+
+class SNNError(RuntimeError):
+    def __init__(self, fn, status):
+        self.status = status
+        super().__init__(f"{fn} failed: {STATUS.get(status, status)} "
+                         f"({_lib.snn_status_str(status).decode() if _lib else ''})")
+
+
+_lib = None
+
+
+def lib():
+    """Load libsnn.so (built in-tree by ``build.build()``); raise if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"HIP library {LIB_PATH} is not built; run __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    P, S = ctypes.c_void_p, ctypes.c_size_t
+    D = ctypes.POINTER(LayerDesc)
+    G = ctypes.POINTER(GradIn)
+    i32 = ctypes.c_int32
+    sig = {
+        "snn_abi_version": ([], ctypes.c_int),
+        "snn_status_str": ([ctypes.c_int], ctypes.c_char_p),
+        "snn_layer_saved_bytes": ([D], S),
+        "snn_layer_workspace_bytes": ([D], S),
+        "snn_layer_fwd": ([D, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_layer_bwd": ([D, G, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_loss_workspace_bytes": ([i32, i32, i32], S),
+        "snn_loss": ([i32, i32, i32, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_synapse_fwd": ([D, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_neuron_fwd": ([D, P, P, P, P, P], ctypes.c_int),
+        "snn_neuron_bwd": ([D, G, P, P, P, P, S, P], ctypes.c_int),
+        "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    if L.snn_abi_version() != ABI_VERSION:
+        raise RuntimeError("libsnn.so ABI version mismatch")
+    _lib = L
+    return L
+
+
+# --------------------------------------------------------------------------
+# argument marshalling
+# --------------------------------------------------------------------------
+def _p(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(fn, st):
+    if st != 0:
+        raise SNNError(fn, st)
+
+
+def snn_layer_saved_bytes(desc: LayerDesc) -> int:
+    return int(lib().snn_layer_saved_bytes(ctypes.byref(desc)))
+
+
+def snn_layer_workspace_bytes(desc: LayerDesc) -> int:
+    return int(lib().snn_layer_workspace_bytes(ctypes.byref(desc)))
+
+
+def snn_loss_workspace_bytes(kind: int, B: int, K: int) -> int:
+    return int(lib().snn_loss_workspace_bytes(kind, B, K))
+
+
+def snn_layer_fwd(desc, x, w, bias, spk_out, saved, counts, ws, stream=None):
+    _check("snn_layer_fwd", lib().snn_layer_fwd(
+        ctypes.byref(desc), _p(x), _p(w), _p(bias), _p(spk_out), _p(saved), _p(counts),
+        _p(ws), _nbytes(ws), _stream(stream)))
+
+
+def snn_layer_bwd(desc, grad_kind, g, x, w, saved, grad_w, grad_b, grad_x, ws, stream=None):
+    gi = GradIn(grad_kind, 0, _p(g))
+    _check("snn_layer_bwd", lib().snn_layer_bwd(
+        ctypes.byref(desc), ctypes.byref(gi), _p(x), _p(w), _p(saved), _p(grad_w), _p(grad_b),
+        _p(grad_x), _p(ws), _nbytes(ws), _stream(stream)))
+
+
+def snn_loss(kind, B, K, counts, labels, targets, loss, grad_counts, ws, stream=None):
+    _check("snn_loss", lib().snn_loss(kind, B, K, _p(counts), _p(labels), _p(targets), _p(loss),
+                                      _p(grad_counts), _p(ws), _nbytes(ws), _stream(stream)))
+
+
+def snn_synapse_fwd(desc, x, w, bias, cur, pool_arg, ws, stream=None):
+    _check("snn_synapse_fwd", lib().snn_synapse_fwd(
+        ctypes.byref(desc), _p(x), _p(w), _p(bias), _p(cur), _p(pool_arg), _p(ws), _nbytes(ws),
+        _stream(stream)))
+
+
+def snn_neuron_fwd(desc, cur, spk_out, saved_u, counts, stream=None):
+    _check("snn_neuron_fwd", lib().snn_neuron_fwd(
+        ctypes.byref(desc), _p(cur), _p(spk_out), _p(saved_u), _p(counts), _stream(stream)))
+
+
+def snn_neuron_bwd(desc, grad_kind, g, saved_u, dcur, grad_b, ws, stream=None):
+    gi = GradIn(grad_kind, 0, _p(g))
+    _check("snn_neuron_bwd", lib().snn_neuron_bwd(
+        ctypes.byref(desc), ctypes.byref(gi), _p(saved_u), _p(dcur), _p(grad_b), _p(ws),
+        _nbytes(ws), _stream(stream)))
+
+
+def snn_synapse_bwd(desc, dcur, pool_arg, x, w, grad_w, grad_x, ws, stream=None):
+    _check("snn_synapse_bwd", lib().snn_synapse_bwd(
+        ctypes.byref(desc), _p(dcur), _p(pool_arg), _p(x), _p(w), _p(grad_w), _p(grad_x),
+        _p(ws), _nbytes(ws), _stream(stream)))
+
+
+# --------------------------------------------------------------------------
+# descriptors from plain layer specs
+# --------------------------------------------------------------------------
+_NEURON = {"leaky": LEAKY, "synaptic": SYNAPTIC}
+
+
+def layer_desc(spec: dict, T: int, B: int, in_dtype=U8, w_dtype=F32, out_dtype=U8,
+               grad_dtype=F32, slope=25.0, reset_grad=RESET_DETACHED) -> LayerDesc:
+    d = LayerDesc()
+    d.T, d.B = T, B
+    d.neuron = _NEURON[spec["neuron"]]
+    d.beta = spec["beta"]
+    d.alpha = spec.get("alpha", 0.0)
+    d.threshold = spec.get("thr", 1.0)
+    d.slope = slope
+    d.reset_grad = reset_grad
+    d.in_dtype, d.w_dtype, d.out_dtype, d.grad_dtype = in_dtype, w_dtype, out_dtype, grad_dtype
+    if spec["kind"] == "dense":
+        d.synapse = SYN_DENSE
+        d.n_in, d.n_out = spec["n_in"], spec["n_out"]
+    elif spec["kind"] == "conv":
+        d.synapse = SYN_CONV5_POOL2
+        d.c_in, d.h_in, d.w_in, d.c_out = spec["c_in"], spec["h"], spec["w"], spec["c_out"]
+        d.n_in = d.c_in * d.h_in * d.w_in
+        d.n_out = d.c_out * ((d.h_in - 4) // 2) * ((d.w_in - 4) // 2)
+    else:
+        d.synapse = SYN_NONE
+        d.n_in = d.n_out = spec["n"]
+        d.in_dtype = F32
+    return d
+
+
+class Network:
+    """Device buffers and the layer-call sequence of one training step.
+
+    All buffers are allocated once here (torch, device memory only); ``step``
+    then only enqueues library calls on the current stream."""
+
+    def __init__(self, wl, params, device="cuda", reset_grad=RESET_DETACHED):
+        import torch
+        self.torch = torch
+        self.wl = wl
+        self.device = device
+        T, B = wl.T, wl.B
+        half = wl.dtype == "f16"
+        self.descs = []
+        self.W, self.b = [], []
+        for li, spec in enumerate(wl.layers):
+            in_dt = F32 if spec["kind"] == "none" else U8
+            d = layer_desc(spec, T, B, in_dtype=in_dt, w_dtype=F16 if half else F32,
+                           out_dtype=U8, grad_dtype=F32, slope=wl.slope, reset_grad=reset_grad)
+            self.descs.append(d)
+            W, b = params[li]
+            if W is None:
+                self.W.append(None)
+                self.b.append(None)
+            else:
+                wdt = torch.float16 if half else torch.float32
+                self.W.append(torch.as_tensor(np.ascontiguousarray(W)).to(device=device, dtype=wdt))
+                self.b.append(torch.as_tensor(np.ascontiguousarray(b)).to(device=device,
+                                                                         dtype=torch.float32))
+        u8 = torch.uint8
+        self.spk = [torch.empty((T, B, d.n_out), dtype=u8, device=device) for d in self.descs]
+        self.saved = [torch.empty(snn_layer_saved_bytes(d), dtype=u8, device=device)
+                      for d in self.descs]
+        self.gW = [None if w is None else torch.empty(w.shape, dtype=torch.float32, device=device)
+                   for w in self.W]
+        self.gb = [None if b is None else torch.empty(b.shape, dtype=torch.float32, device=device)
+                   for b in self.b]
+        # dL/dx of layer l is the upstream gradient of layer l-1
+        self.gx = [None] + [torch.empty((T, B, d.n_in), dtype=torch.float32, device=device)
+                            for d in self.descs[1:]]
+        if self.descs[0].synapse == SYN_NONE:
+            self.gx[0] = torch.empty((T, B, self.descs[0].n_in), dtype=torch.float32, device=device)
+        K = self.descs[-1].n_out
+        self.K = K
+        self.counts = torch.empty((B, K), dtype=torch.float32, device=device)
+        self.loss = torch.empty(4, dtype=torch.float32, device=device)  # [0] is the loss
+        self.gcounts = torch.empty((B, K), dtype=torch.float32, device=device)
+        self.loss_kind = LOSS_CE_COUNT if wl.loss == "ce" else LOSS_MSE_COUNT
+        ws = max([snn_layer_workspace_bytes(d) for d in self.descs] +
+                 [snn_loss_workspace_bytes(self.loss_kind, B, K), 256])
+        self.ws = torch.empty(ws, dtype=u8, device=device)
+
+    def forward(self, x, stream=None):
+        h = x
+        n = len(self.descs)
+        for li, d in enumerate(self.descs):
+            snn_layer_fwd(d, h, self.W[li], self.b[li], self.spk[li], self.saved[li],
+                          self.counts if li == n - 1 else None, self.ws, stream)
+            h = self.spk[li]
+
+    def loss_and_grad(self, labels=None, targets=None, stream=None):
+        snn_loss(self.loss_kind, self.wl.B, self.K, self.counts, labels, targets, self.loss,
+                 self.gcounts, self.ws, stream)
+
+    def backward(self, x, stream=None):
+        n = len(self.descs)
+        kind, g = GRAD_BCAST, self.gcounts
+        for li in range(n - 1, -1, -1):
+            d = self.descs[li]
+            xin = x if li == 0 else self.spk[li - 1]
+            snn_layer_bwd(d, kind, g, xin, self.W[li], self.saved[li], self.gW[li], self.gb[li],
+                          self.gx[li], self.ws, stream)
+            kind, g = GRAD_FULL, self.gx[li]
+
+    def step(self, x, labels=None, targets=None, stream=None):
+        self.forward(x, stream)
+        self.loss_and_grad(labels, targets, stream)
+        self.backward(x, stream)
+
+    # the same work through the stage calls, with a hook between stages
+    def step_stages(self, x, labels=None, targets=None, stream=None, hook=None):
+        hook = hook or (lambda name, li: None)
+        n = len(self.descs)
+        h = x
+        for li, d in enumerate(self.descs):
+            cur = self.saved[li]
+            if d.synapse != SYN_NONE:
+                hook("synapse_fwd", li)
+                snn_synapse_fwd(d, h, self.W[li], self.b[li], cur, None, self.ws, stream)
+                hook("synapse_fwd_end", li)
+            else:
+                cur = h
+            hook("neuron_fwd", li)
+            snn_neuron_fwd(d, cur, self.spk[li], self.saved[li],
+                           self.counts if li == n - 1 else None, stream)
+            hook("neuron_fwd_end", li)
+            h = self.spk[li]
+        hook("loss", -1)
+        self.loss_and_grad(labels, targets, stream)
+        hook("loss_end", -1)
+        kind, g = GRAD_BCAST, self.gcounts
+        for li in range(n - 1, -1, -1):
+            d = self.descs[li]
+            xin = x if li == 0 else self.spk[li - 1]
+            if d.synapse == SYN_NONE:
+                hook("neuron_bwd", li)
+                snn_neuron_bwd(d, kind, g, self.saved[li], self.gx[li], None, None, stream)
+                hook("neuron_bwd_end", li)
+                continue
+            dcur_bytes = d.T * d.B * d.n_out * 4
+            dcur = self.ws[:dcur_bytes]
+            rest = self.ws[(dcur_bytes + 255) // 256 * 256:]
+            hook("neuron_bwd", li)
+            snn_neuron_bwd(d, kind, g, self.saved[li], dcur, self.gb[li], rest, stream)
+            hook("neuron_bwd_end", li)
+            hook("synapse_bwd", li)
+            snn_synapse_bwd(d, dcur, None, xin, self.W[li], self.gW[li], self.gx[li], rest,
+                            stream)
+            hook("synapse_bwd_end", li)
+            kind, g = GRAD_FULL, self.gx[li]

@@ -1,0 +1,333 @@
+// Host side of the C ABI (include/snn.h): argument validation, workspace
+// layout and the order of kernel launches for one layer.
+#include <math.h>
+#include <string.h>
+
+#include "snn_internal.hpp"
+
+using namespace snn;
+
+namespace {
+
+bool aligned16(const void *p) { return (((uintptr_t)p) & 15u) == 0; }
+
+bool finite(float x) { return isfinite(x) != 0; }
+
+// Validates a layer descriptor; nothing here touches the device.
+snn_status check_desc(const snn_layer_desc *d) {
+    if (!d) return SNN_ERR_NULL;
+    if (d->flags != 0) return SNN_ERR_UNSUPPORTED;
+    if (d->T < 0 || d->B < 0 || d->n_in < 0 || d->n_out < 0) return SNN_ERR_SHAPE;
+    if (d->neuron != SNN_LEAKY && d->neuron != SNN_SYNAPTIC) return SNN_ERR_UNSUPPORTED;
+    if (d->reset_grad != SNN_RESET_DETACHED && d->reset_grad != SNN_RESET_SURROGATE)
+        return SNN_ERR_UNSUPPORTED;
+    if (!finite(d->beta) || !finite(d->alpha) || !finite(d->threshold) || !finite(d->slope) ||
+        d->slope < 0.f)
+        return SNN_ERR_SHAPE;
+    if (d->out_dtype != SNN_U8 && d->out_dtype != SNN_F16) return SNN_ERR_DTYPE;
+    if (d->grad_dtype != SNN_F32 && d->grad_dtype != SNN_F16 && d->grad_dtype != SNN_BF16)
+        return SNN_ERR_DTYPE;
+    const int64_t TB = (int64_t)d->T * d->B;
+    if (TB > INT32_MAX) return SNN_ERR_SHAPE;
+    switch (d->synapse) {
+        case SNN_SYN_DENSE:
+            if (d->n_in < 1 || d->n_out < 1) return SNN_ERR_SHAPE;
+            if (d->in_dtype != SNN_U8 && d->in_dtype != SNN_F32 && d->in_dtype != SNN_F16)
+                return SNN_ERR_DTYPE;
+            if (d->w_dtype != SNN_F32 && d->w_dtype != SNN_F16) return SNN_ERR_DTYPE;
+            break;
+        case SNN_SYN_CONV5_POOL2: {
+            if (d->c_in < 1 || d->c_out < 1 || d->h_in < 6 || d->w_in < 6) return SNN_ERR_SHAPE;
+            const int64_t hp = (d->h_in - 4) / 2, wp = (d->w_in - 4) / 2;
+            if ((int64_t)d->c_in * d->h_in * d->w_in != d->n_in) return SNN_ERR_SHAPE;
+            if ((int64_t)d->c_out * hp * wp != d->n_out) return SNN_ERR_SHAPE;
+            if (d->in_dtype != SNN_U8 && d->in_dtype != SNN_F32) return SNN_ERR_DTYPE;
+            if (d->w_dtype != SNN_F32) return SNN_ERR_DTYPE;
+            return SNN_ERR_UNSUPPORTED;  // convolutional synapse not in this build yet
+        }
+        case SNN_SYN_NONE:
+            if (d->n_in != d->n_out || d->n_out < 1) return SNN_ERR_SHAPE;
+            if (d->in_dtype != SNN_F32) return SNN_ERR_DTYPE;
+            if (d->grad_dtype != SNN_F32) return SNN_ERR_DTYPE;
+            break;
+        default:
+            return SNN_ERR_UNSUPPORTED;
+    }
+    if (TB * (int64_t)(d->n_in > d->n_out ? d->n_in : d->n_out) > ((int64_t)1 << 40))
+        return SNN_ERR_SHAPE;
+    return SNN_OK;
+}
+
+int64_t rows(const snn_layer_desc *d) { return (int64_t)d->T * d->B; }
+
+// ---- workspace layout ------------------------------------------------------
+// forward:  [gemm split-K partials]
+// backward: [dcur (grad_dtype) T*B*n_out][colsum fp32 B*n_out][gemm partials]
+size_t fwd_ws(const snn_layer_desc *d) {
+    if (d->synapse != SNN_SYN_DENSE) return 0;
+    return gemm_workspace_bytes((int)rows(d), d->n_out, d->n_in, d->in_dtype, d->w_dtype);
+}
+size_t dcur_bytes(const snn_layer_desc *d) {
+    if (d->synapse == SNN_SYN_NONE) return 0;
+    return align_up((size_t)rows(d) * d->n_out * dtype_bytes(d->grad_dtype));
+}
+size_t colsum_bytes(const snn_layer_desc *d) {
+    return align_up((size_t)d->B * d->n_out * sizeof(float));
+}
+size_t bwd_gemm_ws(const snn_layer_desc *d) {
+    if (d->synapse != SNN_SYN_DENSE) return 0;
+    const int M = (int)rows(d);
+    const size_t dw = gemm_workspace_bytes(d->n_out, d->n_in, M, d->grad_dtype, d->in_dtype);
+    const size_t dx = gemm_workspace_bytes(M, d->n_in, d->n_out, d->grad_dtype, d->w_dtype);
+    return dw > dx ? dw : dx;
+}
+size_t bwd_ws(const snn_layer_desc *d) { return dcur_bytes(d) + colsum_bytes(d) + bwd_gemm_ws(d); }
+
+snn_status hip_status(hipError_t e) { return e == hipSuccess ? SNN_OK : SNN_ERR_HIP; }
+
+snn_status check_grad(const snn_layer_desc *d, const snn_grad_in *g) {
+    if (!g || !g->g) return SNN_ERR_NULL;
+    if (g->kind != SNN_GRAD_FULL && g->kind != SNN_GRAD_BCAST) return SNN_ERR_UNSUPPORTED;
+    if (g->reserved != 0) return SNN_ERR_UNSUPPORTED;
+    if (!aligned16(g->g)) return SNN_ERR_ALIGN;
+    (void)d;
+    return SNN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int snn_abi_version(void) { return SNN_ABI_VERSION; }
+
+const char *snn_status_str(snn_status s) {
+    switch (s) {
+        case SNN_OK: return "ok";
+        case SNN_ERR_NULL: return "required pointer is NULL";
+        case SNN_ERR_SHAPE: return "invalid or inconsistent sizes";
+        case SNN_ERR_DTYPE: return "unsupported dtype combination";
+        case SNN_ERR_ALIGN: return "device pointer not 16-byte aligned";
+        case SNN_ERR_UNSUPPORTED: return "not supported by this build";
+        case SNN_ERR_WORKSPACE: return "workspace too small";
+        case SNN_ERR_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+size_t snn_layer_saved_bytes(const snn_layer_desc *d) {
+    if (check_desc(d) != SNN_OK) return 0;
+    size_t b = align_up((size_t)rows(d) * d->n_out * sizeof(float));
+    if (d->synapse == SNN_SYN_CONV5_POOL2) b += align_up((size_t)rows(d) * d->n_out);
+    return b;
+}
+
+size_t snn_layer_workspace_bytes(const snn_layer_desc *d) {
+    if (check_desc(d) != SNN_OK) return 0;
+    const size_t f = fwd_ws(d), b = bwd_ws(d);
+    return f > b ? f : b;
+}
+
+snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w,
+                           const float *bias, float *cur, uint8_t *pool_arg, void *ws,
+                           size_t ws_bytes, hipStream_t stream) {
+    snn_status st = check_desc(d);
+    if (st != SNN_OK) return st;
+    if (d->synapse == SNN_SYN_NONE) return SNN_ERR_UNSUPPORTED;  // nothing to contract
+    if (!x || !w || !cur) return SNN_ERR_NULL;
+    if (!aligned16(x) || !aligned16(w) || !aligned16(cur) || (bias && !aligned16(bias)))
+        return SNN_ERR_ALIGN;
+    if (fwd_ws(d) > ws_bytes || (fwd_ws(d) > 0 && !ws)) return SNN_ERR_WORKSPACE;
+    (void)pool_arg;
+    if (rows(d) == 0) return SNN_OK;
+    (void)hipGetLastError();
+    GemmArgs g{};
+    g.M = (int)rows(d);
+    g.N = d->n_out;
+    g.K = d->n_in;
+    g.A = x; g.lda = d->n_in; g.a_dtype = d->in_dtype; g.a_kc = true;
+    g.B = w; g.ldb = d->n_in; g.b_dtype = d->w_dtype; g.b_kc = true;
+    g.C = cur; g.ldc = d->n_out; g.bias = bias;
+    return hip_status(launch_gemm(g, ws, ws_bytes, stream));
+}
+
+snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, void *spk_out,
+                          float *saved_u, float *counts, hipStream_t stream) {
+    snn_status st = check_desc(d);
+    if (st != SNN_OK) return st;
+    if (!cur || !spk_out || !saved_u) return SNN_ERR_NULL;
+    if (!aligned16(cur) || !aligned16(spk_out) || !aligned16(saved_u) ||
+        (counts && !aligned16(counts)))
+        return SNN_ERR_ALIGN;
+    (void)hipGetLastError();
+    if (rows(d) == 0) {
+        // counts over zero time steps are 0
+        if (counts) return hip_status(launch_fill_zero(counts, (int64_t)d->B * d->n_out, stream));
+        return SNN_OK;
+    }
+    const int64_t C = (int64_t)d->B * d->n_out;
+    return hip_status(launch_neuron_fwd(d->neuron, d->T, C, d->alpha, d->beta, d->threshold, cur,
+                                        spk_out, d->out_dtype, saved_u, counts, stream));
+}
+
+snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad,
+                          const float *saved_u, void *dcur, float *grad_b, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
+    snn_status st = check_desc(d);
+    if (st != SNN_OK) return st;
+    if ((st = check_grad(d, grad)) != SNN_OK) return st;
+    if (!saved_u || !dcur) return SNN_ERR_NULL;
+    if (!aligned16(saved_u) || !aligned16(dcur) || (grad_b && !aligned16(grad_b)))
+        return SNN_ERR_ALIGN;
+    if (grad_b && d->synapse == SNN_SYN_NONE) return SNN_ERR_SHAPE;  // no bias to differentiate
+    const size_t need = grad_b ? colsum_bytes(d) : 0;
+    if (need > ws_bytes || (need > 0 && !ws)) return SNN_ERR_WORKSPACE;
+    (void)hipGetLastError();
+    if (rows(d) == 0) {
+        if (grad_b) {
+            const int64_t nb = d->synapse == SNN_SYN_CONV5_POOL2 ? d->c_out : d->n_out;
+            return hip_status(launch_fill_zero(grad_b, nb, stream));
+        }
+        return SNN_OK;
+    }
+    const int64_t C = (int64_t)d->B * d->n_out;
+    float *colsum = grad_b ? reinterpret_cast<float *>(ws) : nullptr;
+    hipError_t e = launch_neuron_bwd(d->neuron, d->reset_grad, d->T, C, d->alpha, d->beta,
+                                     d->threshold, d->slope, saved_u, grad->g,
+                                     grad->kind == SNN_GRAD_BCAST, dcur, d->grad_dtype, colsum,
+                                     stream);
+    if (e != hipSuccess) return SNN_ERR_HIP;
+    if (grad_b) {
+        int F = d->n_out, P = 1;
+        if (d->synapse == SNN_SYN_CONV5_POOL2) {
+            F = d->c_out;
+            P = d->n_out / d->c_out;
+        }
+        e = launch_bias_reduce(d->B, F, P, colsum, grad_b, stream);
+    }
+    return hip_status(e);
+}
+
+snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
+                           const uint8_t *pool_arg, const void *x, const void *w,
+                           float *grad_w, float *grad_x, void *ws, size_t ws_bytes,
+                           hipStream_t stream) {
+    snn_status st = check_desc(d);
+    if (st != SNN_OK) return st;
+    if (d->synapse == SNN_SYN_NONE) return SNN_ERR_UNSUPPORTED;
+    if (!dcur) return SNN_ERR_NULL;
+    if ((grad_w && !x) || (grad_x && !w)) return SNN_ERR_NULL;
+    if (!aligned16(dcur) || (x && !aligned16(x)) || (w && !aligned16(w)) ||
+        (grad_w && !aligned16(grad_w)) || (grad_x && !aligned16(grad_x)))
+        return SNN_ERR_ALIGN;
+    const size_t need = bwd_gemm_ws(d);
+    if (need > ws_bytes || (need > 0 && !ws)) return SNN_ERR_WORKSPACE;
+    (void)pool_arg;
+    if (rows(d) == 0) {
+        // empty batch: the weight gradient is an empty sum
+        if (grad_w)
+            return hip_status(launch_fill_zero(grad_w, (int64_t)d->n_out * d->n_in, stream));
+        return SNN_OK;
+    }
+    (void)hipGetLastError();
+    const int M = (int)rows(d);
+    if (grad_w) {
+        // dW[o,i] = sum_m dI[m,o] x[m,i]: both operands stored with the output
+        // index contiguous, K = T*B.
+        GemmArgs g{};
+        g.M = d->n_out; g.N = d->n_in; g.K = M;
+        g.A = dcur; g.lda = d->n_out; g.a_dtype = d->grad_dtype; g.a_kc = false;
+        g.B = x; g.ldb = d->n_in; g.b_dtype = d->in_dtype; g.b_kc = false;
+        g.C = grad_w; g.ldc = d->n_in; g.bias = nullptr;
+        hipError_t e = launch_gemm(g, ws, ws_bytes, stream);
+        if (e != hipSuccess) return SNN_ERR_HIP;
+    }
+    if (grad_x) {
+        // dx[m,i] = sum_o dI[m,o] W[o,i]
+        GemmArgs g{};
+        g.M = M; g.N = d->n_in; g.K = d->n_out;
+        g.A = dcur; g.lda = d->n_out; g.a_dtype = d->grad_dtype; g.a_kc = true;
+        g.B = w; g.ldb = d->n_in; g.b_dtype = d->w_dtype; g.b_kc = false;
+        g.C = grad_x; g.ldc = d->n_in; g.bias = nullptr;
+        hipError_t e = launch_gemm(g, ws, ws_bytes, stream);
+        if (e != hipSuccess) return SNN_ERR_HIP;
+    }
+    return SNN_OK;
+}
+
+snn_status snn_layer_fwd(const snn_layer_desc *d, const void *x, const void *w,
+                         const float *bias, void *spk_out, void *saved, float *counts,
+                         void *ws, size_t ws_bytes, hipStream_t stream) {
+    snn_status st = check_desc(d);
+    if (st != SNN_OK) return st;
+    if (!x || !spk_out || !saved) return SNN_ERR_NULL;
+    if (d->synapse != SNN_SYN_NONE && !w) return SNN_ERR_NULL;
+    if (!aligned16(x) || !aligned16(spk_out) || !aligned16(saved) || (w && !aligned16(w)) ||
+        (bias && !aligned16(bias)) || (counts && !aligned16(counts)))
+        return SNN_ERR_ALIGN;
+    if (fwd_ws(d) > ws_bytes) return SNN_ERR_WORKSPACE;
+    float *u = reinterpret_cast<float *>(saved);
+    if (d->synapse == SNN_SYN_NONE)
+        return snn_neuron_fwd(d, reinterpret_cast<const float *>(x), spk_out, u, counts, stream);
+    uint8_t *arg = nullptr;
+    if (d->synapse == SNN_SYN_CONV5_POOL2)
+        arg = reinterpret_cast<uint8_t *>(saved) + align_up((size_t)rows(d) * d->n_out * sizeof(float));
+    st = snn_synapse_fwd(d, x, w, bias, u, arg, ws, ws_bytes, stream);
+    if (st != SNN_OK) return st;
+    return snn_neuron_fwd(d, u, spk_out, u, counts, stream);
+}
+
+snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const void *x,
+                         const void *w, const void *saved, float *grad_w, float *grad_b,
+                         float *grad_x, void *ws, size_t ws_bytes, hipStream_t stream) {
+    snn_status st = check_desc(d);
+    if (st != SNN_OK) return st;
+    if ((st = check_grad(d, grad)) != SNN_OK) return st;
+    if (!saved) return SNN_ERR_NULL;
+    if (!aligned16(saved)) return SNN_ERR_ALIGN;
+    const float *u = reinterpret_cast<const float *>(saved);
+    if (d->synapse == SNN_SYN_NONE) {
+        if (grad_w || grad_b) return SNN_ERR_SHAPE;
+        if (!grad_x) return SNN_ERR_NULL;
+        return snn_neuron_bwd(d, grad, u, grad_x, nullptr, nullptr, 0, stream);
+    }
+    if (grad_w && !x) return SNN_ERR_NULL;
+    if (grad_x && !w) return SNN_ERR_NULL;
+    if (bwd_ws(d) > ws_bytes || !ws) return SNN_ERR_WORKSPACE;
+    char *base = reinterpret_cast<char *>(ws);
+    void *dcur = base;
+    char *colsum = base + dcur_bytes(d);
+    char *gws = colsum + colsum_bytes(d);
+    st = snn_neuron_bwd(d, grad, u, dcur, grad_b, colsum, colsum_bytes(d), stream);
+    if (st != SNN_OK) return st;
+    if (!grad_w && !grad_x) return SNN_OK;
+    const uint8_t *arg = nullptr;
+    if (d->synapse == SNN_SYN_CONV5_POOL2)
+        arg = reinterpret_cast<const uint8_t *>(saved) +
+              align_up((size_t)rows(d) * d->n_out * sizeof(float));
+    return snn_synapse_bwd(d, dcur, arg, x, w, grad_w, grad_x, gws, bwd_gemm_ws(d), stream);
+}
+
+size_t snn_loss_workspace_bytes(int32_t kind, int32_t B, int32_t K) {
+    if (kind != SNN_LOSS_CE_COUNT && kind != SNN_LOSS_MSE_COUNT) return 0;
+    return loss_workspace_bytes(kind, B, K);
+}
+
+snn_status snn_loss(int32_t kind, int32_t B, int32_t K, const float *counts,
+                    const int32_t *labels, const float *targets, float *loss,
+                    float *grad_counts, void *ws, size_t ws_bytes, hipStream_t stream) {
+    if (kind != SNN_LOSS_CE_COUNT && kind != SNN_LOSS_MSE_COUNT) return SNN_ERR_UNSUPPORTED;
+    if (B < 1 || K < 1) return SNN_ERR_SHAPE;
+    if (!counts || !loss) return SNN_ERR_NULL;
+    if (kind == SNN_LOSS_CE_COUNT && !labels) return SNN_ERR_NULL;
+    if (kind == SNN_LOSS_MSE_COUNT && !targets) return SNN_ERR_NULL;
+    if (!aligned16(counts) || !aligned16(loss) || (labels && !aligned16(labels)) ||
+        (targets && !aligned16(targets)) || (grad_counts && !aligned16(grad_counts)))
+        return SNN_ERR_ALIGN;
+    const size_t need = loss_workspace_bytes(kind, B, K);
+    if (need > ws_bytes || (need > 0 && !ws)) return SNN_ERR_WORKSPACE;
+    (void)hipGetLastError();
+    return hip_status(launch_loss(kind, B, K, counts, labels, targets, loss, grad_counts, ws,
+                                  stream));
+}
+
+}  // extern "C"

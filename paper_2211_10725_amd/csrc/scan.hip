@@ -1,0 +1,323 @@
+// Neuron time scans for gfx950: forward (eqs. 3-6) and the BPTT reverse scan
+// with the fast-sigmoid surrogate (eqs. 8-9).
+//
+// Layout: every tensor is time-major [T, C] with C = B * n columns, column
+// fastest.  One lane owns VEC consecutive columns for all T steps and keeps
+// the neuron state in registers; a wave therefore streams 64*VEC contiguous
+// floats per step (1 KiB for VEC = 4), fully coalesced.  The inputs of the
+// next D steps do not depend on the state, so each lane keeps a ring of D
+// prefetched steps in registers to keep enough HBM requests in flight while
+// the sequential recurrence runs.
+#include "snn_internal.hpp"
+
+namespace snn {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kDepth = 8;  // time steps prefetched ahead per lane
+
+template <int VEC>
+struct Vec;
+template <>
+struct Vec<4> {
+    static __device__ inline void load(const float *p, float (&v)[4]) {
+        const float4 x = *reinterpret_cast<const float4 *>(p);
+        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
+    }
+    static __device__ inline void store(float *p, const float (&v)[4]) {
+        *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+};
+template <>
+struct Vec<1> {
+    static __device__ inline void load(const float *p, float (&v)[1]) { v[0] = *p; }
+    static __device__ inline void store(float *p, const float (&v)[1]) { *p = v[0]; }
+};
+
+// spikes as bytes 0/1
+template <int VEC>
+__device__ inline void store_spikes_u8(uint8_t *p, const float (&z)[VEC]) {
+    if constexpr (VEC == 4) {
+        const uint32_t w = (uint32_t)z[0] | ((uint32_t)z[1] << 8) | ((uint32_t)z[2] << 16) |
+                           ((uint32_t)z[3] << 24);
+        *reinterpret_cast<uint32_t *>(p) = w;
+    } else {
+        p[0] = (uint8_t)z[0];
+    }
+}
+
+// spikes as fp16 0.0 / 1.0 (0x3c00)
+template <int VEC>
+__device__ inline void store_spikes_f16(uint16_t *p, const float (&z)[VEC]) {
+    if constexpr (VEC == 4) {
+        const uint32_t lo = (z[0] != 0.f ? 0x3c00u : 0u) | (z[1] != 0.f ? 0x3c000000u : 0u);
+        const uint32_t hi = (z[2] != 0.f ? 0x3c00u : 0u) | (z[3] != 0.f ? 0x3c000000u : 0u);
+        *reinterpret_cast<uint2 *>(p) = make_uint2(lo, hi);
+    } else {
+        p[0] = z[0] != 0.f ? 0x3c00u : 0u;
+    }
+}
+
+// Forward scan.  `cur` and `u_out` may alias exactly: each lane reads step t
+// of its columns before it writes step t, and prefetches only later steps.
+template <int NEURON, int VEC, int OUT>
+__global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, float alpha,
+                                                              float beta, float thr,
+                                                              const float *cur, void *spk,
+                                                              float *u_out,
+                                                              float *__restrict__ counts) {
+    const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
+    if (col >= C) return;
+    float u[VEC], syn[VEC], zp[VEC], cnt[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) u[v] = syn[v] = zp[v] = cnt[v] = 0.f;
+
+    float in[kDepth][VEC], nx[kDepth][VEC];
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j)
+        if (j < T) Vec<VEC>::load(cur + (int64_t)j * C + col, in[j]);
+
+    for (int t0 = 0; t0 < T; t0 += kDepth) {
+#pragma unroll
+        for (int j = 0; j < kDepth; ++j)
+            if (t0 + kDepth + j < T) Vec<VEC>::load(cur + (int64_t)(t0 + kDepth + j) * C + col, nx[j]);
+#pragma unroll
+        for (int j = 0; j < kDepth; ++j) {
+            const int t = t0 + j;
+            if (t < T) {
+                float z[VEC];
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) {
+                    float uu;
+                    if constexpr (NEURON == SNN_SYNAPTIC) {
+                        syn[v] = __builtin_fmaf(alpha, syn[v], in[j][v]);
+                        uu = __builtin_fmaf(beta, u[v], syn[v]);
+                    } else {
+                        uu = __builtin_fmaf(beta, u[v], in[j][v]);
+                    }
+                    uu = (zp[v] != 0.f) ? uu - thr : uu;  // reset by subtraction
+                    u[v] = uu;
+                    z[v] = (uu > thr) ? 1.f : 0.f;       // eq. (3), strict
+                    zp[v] = z[v];
+                    cnt[v] += z[v];
+                }
+                const int64_t off = (int64_t)t * C + col;
+                Vec<VEC>::store(u_out + off, u);
+                if constexpr (OUT == SNN_U8)
+                    store_spikes_u8<VEC>(reinterpret_cast<uint8_t *>(spk) + off, z);
+                else
+                    store_spikes_f16<VEC>(reinterpret_cast<uint16_t *>(spk) + off, z);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kDepth; ++j)
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) in[j][v] = nx[j][v];
+    }
+    if (counts) Vec<VEC>::store(counts + col, cnt);
+}
+
+__device__ inline uint16_t f32_to_bf16_rne(float x) {
+    const uint32_t b = __float_as_uint(x);
+    return (uint16_t)((b + 0x7fffu + ((b >> 16) & 1u)) >> 16);
+}
+
+template <int GT, int VEC>
+__device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC]) {
+    if constexpr (GT == SNN_F32) {
+        Vec<VEC>::store(reinterpret_cast<float *>(base) + off, v);
+    } else {
+        uint16_t h[VEC];
+#pragma unroll
+        for (int i = 0; i < VEC; ++i) {
+            if constexpr (GT == SNN_F16) {
+                const _Float16 f = (_Float16)v[i];
+                h[i] = __builtin_bit_cast(uint16_t, f);
+            } else {
+                h[i] = f32_to_bf16_rne(v[i]);
+            }
+        }
+        uint16_t *p = reinterpret_cast<uint16_t *>(base) + off;
+        if constexpr (VEC == 4)
+            *reinterpret_cast<uint2 *>(p) =
+                make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+        else
+            p[0] = h[0];
+    }
+}
+
+// Reverse-time scan.  lam carries dL/du_{t+1} (and lami dL/di_{t+1}).
+template <int NEURON, int VEC, bool BCAST, bool RESET_SURR, int GT>
+__global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
+    int T, int64_t C, float alpha, float beta, float thr, float slope,
+    const float *__restrict__ u, const float *__restrict__ g, void *__restrict__ dcur,
+    float *__restrict__ colsum) {
+    const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
+    if (col >= C) return;
+    float lam[VEC], lami[VEC], acc[VEC], gb[VEC];
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) lam[v] = lami[v] = acc[v] = gb[v] = 0.f;
+    if constexpr (BCAST) Vec<VEC>::load(g + col, gb);
+
+    float uu[kDepth][VEC], nu[kDepth][VEC];
+    float gg[BCAST ? 1 : kDepth][VEC], ng[BCAST ? 1 : kDepth][VEC];
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j) {
+        const int t = T - 1 - j;
+        if (t >= 0) {
+            Vec<VEC>::load(u + (int64_t)t * C + col, uu[j]);
+            if constexpr (!BCAST) Vec<VEC>::load(g + (int64_t)t * C + col, gg[j]);
+        }
+    }
+    for (int t0 = T - 1; t0 >= 0; t0 -= kDepth) {
+#pragma unroll
+        for (int j = 0; j < kDepth; ++j) {
+            const int t = t0 - kDepth - j;
+            if (t >= 0) {
+                Vec<VEC>::load(u + (int64_t)t * C + col, nu[j]);
+                if constexpr (!BCAST) Vec<VEC>::load(g + (int64_t)t * C + col, ng[j]);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kDepth; ++j) {
+            const int t = t0 - j;
+            if (t >= 0) {
+                float d[VEC];
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) {
+                    const float e = 1.f + slope * __builtin_fabsf(uu[j][v] - thr);
+                    const float s = __builtin_amdgcn_rcpf(e * e);  // eq. (9) with slope
+                    float gt;
+                    if constexpr (BCAST) gt = gb[v]; else gt = gg[j][v];
+                    float carry = beta;
+                    if constexpr (RESET_SURR) carry = beta - thr * s;
+                    lam[v] = __builtin_fmaf(carry, lam[v], gt * s);
+                    if constexpr (NEURON == SNN_SYNAPTIC) {
+                        lami[v] = __builtin_fmaf(alpha, lami[v], lam[v]);
+                        d[v] = lami[v];
+                    } else {
+                        d[v] = lam[v];
+                    }
+                    acc[v] += d[v];
+                }
+                store_grad<GT, VEC>(dcur, (int64_t)t * C + col, d);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kDepth; ++j)
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                uu[j][v] = nu[j][v];
+                if constexpr (!BCAST) gg[j][v] = ng[j][v];
+            }
+    }
+    if (colsum) Vec<VEC>::store(colsum + col, acc);
+}
+
+__global__ __launch_bounds__(kThreads) void bias_reduce_kernel(int B, int F, int P,
+                                                               const float *__restrict__ colsum,
+                                                               float *__restrict__ db) {
+    const int f = blockIdx.x * kThreads + threadIdx.x;
+    if (f >= F) return;
+    const int64_t row = (int64_t)F * P;
+    double acc = 0.0;
+    for (int b = 0; b < B; ++b)
+        for (int p = 0; p < P; ++p) acc += (double)colsum[b * row + (int64_t)f * P + p];
+    db[f] = (float)acc;
+}
+
+__global__ __launch_bounds__(kThreads) void fill_zero_kernel(float *__restrict__ p, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < n) p[i] = 0.f;
+}
+
+template <int NEURON, int VEC, int OUT>
+void fwd_launch(int T, int64_t C, float alpha, float beta, float thr, const float *cur,
+                void *spk, float *u_out, float *counts, hipStream_t s) {
+    const int64_t lanes = (C + VEC - 1) / VEC;
+    const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
+    neuron_fwd_kernel<NEURON, VEC, OUT><<<grid, kThreads, 0, s>>>(T, C, alpha, beta, thr, cur,
+                                                                 spk, u_out, counts);
+}
+
+template <int NEURON, int VEC, bool BCAST, bool RS, int GT>
+void bwd_launch(int T, int64_t C, float alpha, float beta, float thr, float slope,
+                const float *u, const float *g, void *dcur, float *colsum, hipStream_t s) {
+    const int64_t lanes = (C + VEC - 1) / VEC;
+    const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
+    neuron_bwd_kernel<NEURON, VEC, BCAST, RS, GT><<<grid, kThreads, 0, s>>>(
+        T, C, alpha, beta, thr, slope, u, g, dcur, colsum);
+}
+
+template <int NEURON, int VEC, bool BCAST, bool RS>
+void bwd_dispatch_gt(int gt, int T, int64_t C, float alpha, float beta, float thr, float slope,
+                     const float *u, const float *g, void *dcur, float *colsum, hipStream_t s) {
+    if (gt == SNN_F32)
+        bwd_launch<NEURON, VEC, BCAST, RS, SNN_F32>(T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+    else if (gt == SNN_F16)
+        bwd_launch<NEURON, VEC, BCAST, RS, SNN_F16>(T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+    else
+        bwd_launch<NEURON, VEC, BCAST, RS, SNN_BF16>(T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+}
+
+template <int NEURON, int VEC>
+void bwd_dispatch(int rs, int bcast, int gt, int T, int64_t C, float alpha, float beta, float thr,
+                  float slope, const float *u, const float *g, void *dcur, float *colsum,
+                  hipStream_t s) {
+    if (bcast) {
+        if (rs) bwd_dispatch_gt<NEURON, VEC, true, true>(gt, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+        else bwd_dispatch_gt<NEURON, VEC, true, false>(gt, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+    } else {
+        if (rs) bwd_dispatch_gt<NEURON, VEC, false, true>(gt, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+        else bwd_dispatch_gt<NEURON, VEC, false, false>(gt, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, float alpha, float beta, float thr,
+                             const float *cur, void *spk, int out_dtype, float *u_out,
+                             float *counts, hipStream_t s) {
+    if (T <= 0 || C <= 0) return hipSuccess;
+    const bool v4 = (C % 4) == 0;
+#define SNN_FWD(N, V, O) fwd_launch<N, V, O>(T, C, alpha, beta, thr, cur, spk, u_out, counts, s)
+    if (neuron == SNN_SYNAPTIC) {
+        if (out_dtype == SNN_U8) { if (v4) SNN_FWD(SNN_SYNAPTIC, 4, SNN_U8); else SNN_FWD(SNN_SYNAPTIC, 1, SNN_U8); }
+        else { if (v4) SNN_FWD(SNN_SYNAPTIC, 4, SNN_F16); else SNN_FWD(SNN_SYNAPTIC, 1, SNN_F16); }
+    } else {
+        if (out_dtype == SNN_U8) { if (v4) SNN_FWD(SNN_LEAKY, 4, SNN_U8); else SNN_FWD(SNN_LEAKY, 1, SNN_U8); }
+        else { if (v4) SNN_FWD(SNN_LEAKY, 4, SNN_F16); else SNN_FWD(SNN_LEAKY, 1, SNN_F16); }
+    }
+#undef SNN_FWD
+    return hipGetLastError();
+}
+
+hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, float alpha,
+                             float beta, float thr, float slope, const float *u, const float *g,
+                             int g_bcast, void *dcur, int grad_dtype, float *colsum,
+                             hipStream_t s) {
+    if (T <= 0 || C <= 0) return hipSuccess;
+    const bool v4 = (C % 4) == 0;
+    if (neuron == SNN_SYNAPTIC) {
+        if (v4) bwd_dispatch<SNN_SYNAPTIC, 4>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+        else bwd_dispatch<SNN_SYNAPTIC, 1>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+    } else {
+        if (v4) bwd_dispatch<SNN_LEAKY, 4>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+        else bwd_dispatch<SNN_LEAKY, 1>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    fill_zero_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, s>>>(p, n);
+    return hipGetLastError();
+}
+
+hipError_t launch_bias_reduce(int B, int F, int P, const float *colsum, float *db, hipStream_t s) {
+    if (F <= 0) return hipSuccess;
+    bias_reduce_kernel<<<(F + kThreads - 1) / kThreads, kThreads, 0, s>>>(B, F, P, colsum, db);
+    return hipGetLastError();
+}
+
+}  // namespace snn

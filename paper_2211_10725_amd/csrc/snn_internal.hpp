@@ -1,0 +1,87 @@
+// Internal launch interface of libsnn.so (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "snn.h"
+
+namespace snn {
+
+constexpr size_t kAlign = 256;  // workspace sub-buffers start on 256-byte boundaries
+
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+inline size_t dtype_bytes(int dt) {
+    switch (dt) {
+        case SNN_F32: return 4;
+        case SNN_F16: return 2;
+        case SNN_BF16: return 2;
+        case SNN_U8: return 1;
+        default: return 0;
+    }
+}
+
+// ---- neuron scans (scan.hip) ---------------------------------------------
+// Forward: C = B * N independent columns, time-major [T, C].
+hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, float alpha, float beta, float thr,
+                             const float *cur, void *spk, int out_dtype, float *u_out,
+                             float *counts, hipStream_t s);
+
+// Backward: writes dcur [T, C] (grad_dtype) and colsum [C] = sum_t dcur (fp32,
+// may be NULL).
+hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, float alpha,
+                             float beta, float thr, float slope, const float *u, const float *g,
+                             int g_bcast, void *dcur, int grad_dtype, float *colsum,
+                             hipStream_t s);
+
+// p[0..n) = 0 with a kernel (safe inside captured graphs)
+hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
+
+// db[f] = sum_b sum_p colsum[b*F*P + f*P + p]  (fixed order)
+hipError_t launch_bias_reduce(int B, int F, int P, const float *colsum, float *db, hipStream_t s);
+
+// ---- GEMM (gemm.hip) -------------------------------------------------------
+// C[M,N] = sum_k A(m,k) * B(n,k) (+ bias[n]).  A(m,k) = A[m*lda + k] when a_kc
+// (K contiguous) else A[k*lda + m]; likewise B.  Element types SNN_F32, SNN_F16,
+// SNN_BF16 or SNN_U8; products accumulate in fp32.  Split-K partials go to ws.
+struct GemmArgs {
+    int M, N, K;
+    const void *A;
+    int64_t lda;
+    int a_dtype;
+    bool a_kc;
+    const void *B;
+    int64_t ldb;
+    int b_dtype;
+    bool b_kc;
+    float *C;
+    int64_t ldc;
+    const float *bias;  // [N] or NULL
+};
+size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype);
+hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
+
+// ---- losses (loss.hip) -----------------------------------------------------
+size_t loss_workspace_bytes(int kind, int B, int K);
+hipError_t launch_loss(int kind, int B, int K, const float *counts, const int32_t *labels,
+                       const float *targets, float *loss, float *grad, void *ws,
+                       hipStream_t s);
+
+// ---- convolution + pool (conv.hip) -------------------------------------------
+struct ConvGeom {
+    int NB;   // T * B images
+    int Ci, H, W, Co;
+    int Ho, Wo, Hp, Wp;  // conv output and pooled sizes
+};
+size_t conv_workspace_bytes(const ConvGeom &g, int in_dtype, int w_dtype, int grad_dtype);
+hipError_t launch_conv_pool_fwd(const ConvGeom &g, const void *x, int in_dtype, const void *w,
+                                int w_dtype, const float *bias, float *cur, uint8_t *arg,
+                                void *ws, size_t ws_bytes, hipStream_t s);
+hipError_t launch_conv_pool_bwd(const ConvGeom &g, const void *dcur, int grad_dtype,
+                                const uint8_t *arg, const void *x, int in_dtype, const void *w,
+                                int w_dtype, float *grad_w, float *grad_x, void *ws,
+                                size_t ws_bytes, hipStream_t s);
+
+}  // namespace snn

@@ -1,0 +1,105 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+include/snn.h declares, and validates arguments on the host (no launches)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2211_10725_amd as snn
+from tests.conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "snn.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(snn_[a-z_]+)\s*\(", src)))
+
+
+def test_header_and_binding_agree():
+    assert _declared() == sorted(snn.EXPORTS)
+
+
+def test_library_exports_every_symbol():
+    L = snn.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+    assert L.snn_abi_version() == snn.ABI_VERSION
+    for s in range(8):
+        assert isinstance(L.snn_status_str(s), bytes)
+
+
+def _dense(T=4, B=3, n_in=20, n_out=7):
+    return snn.layer_desc(dict(kind="dense", n_in=n_in, n_out=n_out, neuron="leaky", beta=0.9),
+                          T, B)
+
+
+def _fwd(desc, x=16, w=32, bias=None, spk=48, saved=64, counts=None, ws=None, wsb=0):
+    return snn.lib().snn_layer_fwd(ctypes.byref(desc) if desc is not None else None, x, w, bias,
+                                   spk, saved, counts, ws, wsb, None)
+
+
+def test_validation_errors_before_launch():
+    # fake, aligned, never dereferenced addresses: validation fails first
+    d = _dense()
+    assert _fwd(None) == 1                                     # NULL desc
+    assert _fwd(d, x=None) == 1                                # NULL x
+    assert _fwd(d, w=None) == 1                                # dense needs w
+    assert _fwd(d, x=17) == 4                                  # misaligned
+    bad = d.copy(); bad.T = -1
+    assert _fwd(bad) == 2
+    bad = d.copy(); bad.neuron = 7
+    assert _fwd(bad) == 5
+    bad = d.copy(); bad.in_dtype = 9
+    assert _fwd(bad) == 3
+    bad = d.copy(); bad.flags = 1
+    assert _fwd(bad) == 5
+    bad = d.copy(); bad.slope = float("nan")
+    assert _fwd(bad) == 2
+    none = snn.layer_desc(dict(kind="none", n=12, neuron="leaky", beta=0.9), 4, 3)
+    bad = none.copy(); bad.n_out = 13
+    assert _fwd(bad, w=None) == 2
+    conv = snn.layer_desc(dict(kind="conv", c_in=1, h=28, w=28, c_out=12, neuron="leaky",
+                               beta=0.5), 4, 3)
+    bad = conv.copy(); bad.n_out = 5
+    assert _fwd(bad) == 2
+
+
+def test_loss_validation():
+    L = snn.lib()
+    assert L.snn_loss(0, 0, 10, 16, 32, None, 48, 64, None, 0, None) == 2   # B = 0
+    assert L.snn_loss(0, 4, 10, 16, None, None, 48, 64, None, 0, None) == 1  # CE needs labels
+    assert L.snn_loss(1, 4, 10, 16, None, None, 48, 64, None, 0, None) == 1  # MSE needs targets
+    assert L.snn_loss(5, 4, 10, 16, 32, None, 48, 64, None, 0, None) == 5
+    need = L.snn_loss_workspace_bytes(1, 64, 65536)
+    assert need > 0
+    assert L.snn_loss(1, 64, 65536, 16, None, 32, 48, 64, 256, need - 1, None) == 6
+
+
+def test_sizes_queries():
+    d = _dense(T=25, B=32, n_in=784, n_out=1000)
+    assert snn.snn_layer_saved_bytes(d) >= 25 * 32 * 1000 * 4
+    ws = snn.snn_layer_workspace_bytes(d)
+    assert ws >= 25 * 32 * 1000 * 4          # holds dL/dI for the backward
+    bad = d.copy(); bad.n_in = 0
+    assert snn.snn_layer_saved_bytes(bad) == 0
+    none = snn.layer_desc(dict(kind="none", n=65536, neuron="leaky", beta=0.95), 1000, 64)
+    assert snn.snn_layer_saved_bytes(none) == 1000 * 64 * 65536 * 4
+
+
+def test_workspace_too_small_is_rejected():
+    d = _dense(T=25, B=32, n_in=784, n_out=1000)
+    gi = snn.GradIn(snn.GRAD_BCAST, 0, 16)
+    need = snn.snn_layer_workspace_bytes(d)
+    st = snn.lib().snn_layer_bwd(ctypes.byref(d), ctypes.byref(gi), 32, 48, 64, 80, 96, None,
+                                 256, need - 1, None)
+    assert st == 6
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(snn, "_lib", None)
+    monkeypatch.setattr(snn, "LIB_PATH", str(tmp_path / "libsnn.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        snn.lib()

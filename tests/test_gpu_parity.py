@@ -1,0 +1,340 @@
+"""GPU path vs CPU oracle, through the C ABI, on identical seeded inputs.
+
+Stage tests feed the oracle the GPU's own inputs to that stage (teacher
+forcing), so that a legal spike flip in one stage cannot cascade into the
+next.  Scans given identical fp32 currents must be bit-identical.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2211_10725_amd as snn
+from paper_2211_10725_amd import workloads as wls
+from tests.parity import assert_close, assert_spikes, spike_flips
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+def _t(a, dtype=None):
+    t = torch.as_tensor(np.ascontiguousarray(a))
+    if dtype is not None:
+        t = t.to(dtype)
+    return t.to(DEV)
+
+
+def _np(t):
+    torch.cuda.synchronize()
+    return t.detach().cpu().numpy()
+
+
+def _none_desc(T, B, N, neuron="leaky", beta=0.9, alpha=0.0, thr=1.0, slope=25.0,
+               reset=snn.RESET_DETACHED):
+    spec = dict(kind="none", n=N, neuron=neuron, beta=beta, alpha=alpha, thr=thr)
+    return snn.layer_desc(spec, T, B, slope=slope, reset_grad=reset), spec
+
+
+def _assert_fp32_sum(a, terms_abs, K, what):
+    """A priori bound of an fp32 sum of K products, any order:
+    |fl(sum) - sum| <= (K + 1) u sum|terms|, u = 2^-24 (plus one rounding)."""
+    bound = (K + 2) * 2.0 ** -24 * terms_abs
+    err = np.abs(np.asarray(a, np.float64))
+    assert (err <= bound).all(), f"{what}: error above the fp32 summation bound"
+
+
+def _ws(nbytes):
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=DEV)
+
+
+# ---------------------------------------------------------------------------
+# neuron scans
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("neuron,alpha,beta", [("leaky", 0.0, 0.95), ("synaptic", 0.9, 0.8)])
+@pytest.mark.parametrize("T,B,N", [(1, 2, 8), (7, 3, 101), (33, 4, 256), (50, 5, 1001)])
+def test_scan_fwd_bit_exact(neuron, alpha, beta, T, B, N):
+    rng = np.random.default_rng(T * 1000 + N)
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    d, spec = _none_desc(T, B, N, neuron, beta, alpha)
+    x = _t(I)
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    counts = torch.empty((B, N), dtype=torch.float32, device=DEV)
+    snn.snn_neuron_fwd(d, x, spk, saved, counts)
+    z, u, c = oracle.scan_fwd(I, neuron, beta, 1.0, alpha)
+    np.testing.assert_array_equal(_np(spk), z)
+    np.testing.assert_array_equal(_np(saved), u)
+    np.testing.assert_array_equal(_np(counts), c)
+
+
+def test_scan_fwd_in_place_and_f16_spikes():
+    T, B, N = 20, 3, 64
+    rng = np.random.default_rng(11)
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    d, _ = _none_desc(T, B, N, "synaptic", 0.8, 0.6)
+    d.out_dtype = snn.F16
+    buf = _t(I)
+    spk = torch.empty((T, B, N), dtype=torch.float16, device=DEV)
+    snn.snn_neuron_fwd(d, buf, spk, buf, None)        # currents overwritten by u
+    z, u, _ = oracle.scan_fwd(I, "synaptic", 0.8, 1.0, 0.6)
+    np.testing.assert_array_equal(_np(buf), u)
+    np.testing.assert_array_equal(_np(spk).astype(np.uint8), z)
+
+
+@pytest.mark.parametrize("neuron,alpha,beta", [("leaky", 0.0, 0.95), ("synaptic", 0.9, 0.8)])
+@pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
+@pytest.mark.parametrize("bcast", [True, False])
+@pytest.mark.parametrize("T,B,N", [(1, 2, 8), (9, 3, 37), (40, 4, 512)])
+def test_scan_bwd(neuron, alpha, beta, reset, bcast, T, B, N):
+    rng = np.random.default_rng(7 * T + N)
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    d, spec = _none_desc(T, B, N, neuron, beta, alpha, reset=reset)
+    x = _t(I)
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    snn.snn_neuron_fwd(d, x, spk, saved, None)
+    g = rng.normal(0, 1, (B, N) if bcast else (T, B, N)).astype(np.float32)
+    dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST if bcast else snn.GRAD_FULL, _t(g), saved, dI, None, None)
+    ref = oracle.scan_bwd(_np(saved), g, neuron, beta, 1.0, 25.0, alpha, reset == snn.RESET_SURROGATE)
+    assert_close(_np(dI), ref, 1e-3, what="dL/dI")
+
+
+@pytest.mark.parametrize("gdt,tdt", [(snn.F16, torch.float16), (snn.BF16, torch.bfloat16)])
+def test_scan_bwd_half_gradient_operand(gdt, tdt):
+    T, B, N = 30, 4, 96
+    rng = np.random.default_rng(5)
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    spec = dict(kind="dense", n_in=8, n_out=N, neuron="leaky", beta=0.9)
+    d = snn.layer_desc(spec, T, B, grad_dtype=gdt)
+    dn, _ = _none_desc(T, B, N, "leaky", 0.9)
+    saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    snn.snn_neuron_fwd(dn, _t(I), spk, saved, None)
+    g = rng.normal(0, 0.01, (B, N)).astype(np.float32)
+    dI = torch.empty((T, B, N), dtype=tdt, device=DEV)
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, _t(g), saved, dI, None, None)
+    ref = oracle.scan_bwd(_np(saved), g, "leaky", 0.9, 1.0, 25.0)
+    assert_close(_np(dI.float()), ref, 2e-2, what="half dL/dI")
+
+
+# ---------------------------------------------------------------------------
+# synaptic contractions
+# ---------------------------------------------------------------------------
+GEMM_SHAPES = [(37, 29, 53), (800, 1000, 784), (128, 10, 1000), (300, 7, 33), (64, 130, 1),
+               (5, 300, 17)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("wdt", ["f32", "f16"])
+def test_synapse_fwd(M, N, K, wdt):
+    rng = np.random.default_rng(M + N + K)
+    x = (rng.random((M, K)) < 0.5).astype(np.uint8)
+    W = rng.uniform(-1, 1, (N, K)).astype(np.float32)
+    if wdt == "f16":
+        W = W.astype(np.float16).astype(np.float32)
+    b = rng.uniform(-1, 1, N).astype(np.float32)
+    spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
+    d = snn.layer_desc(spec, 1, M, w_dtype=snn.F16 if wdt == "f16" else snn.F32)
+    cur = torch.empty((M, N), dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    Wt = _t(W, torch.float16 if wdt == "f16" else torch.float32)
+    snn.snn_synapse_fwd(d, _t(x), Wt, _t(b), cur, None, ws)
+    ref = oracle.dense_fwd(x, W, b)
+    got = _np(cur)
+    assert_close(got, ref, 1e-3, what="currents")
+    _assert_fp32_sum(got - ref, x.astype(np.float64) @ np.abs(W).T.astype(np.float64) + np.abs(b),
+                     K, "currents")
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+def test_synapse_bwd(M, N, K):
+    """dW = dI^T x (split over K = T*B) and dx = dI W."""
+    rng = np.random.default_rng(3 * M + N)
+    x = (rng.random((M, K)) < 0.5).astype(np.uint8)
+    W = rng.uniform(-1, 1, (N, K)).astype(np.float32)
+    dI = rng.normal(0, 1, (M, N)).astype(np.float32)
+    spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
+    d = snn.layer_desc(spec, 1, M)
+    gW = torch.empty((N, K), dtype=torch.float32, device=DEV)
+    gx = torch.empty((M, K), dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    snn.snn_synapse_bwd(d, _t(dI), None, _t(x), _t(W), gW, gx, ws)
+    rW, _, rx = oracle.dense_bwd(dI, x, W)
+    gotW, gotx = _np(gW), _np(gx)
+    assert_close(gotW, rW, 1e-3, what="dW")
+    assert_close(gotx, rx, 1e-3, what="dx")
+    aI = np.abs(dI).astype(np.float64)
+    _assert_fp32_sum(gotW - rW, aI.T @ x.astype(np.float64), M, "dW")
+    _assert_fp32_sum(gotx - rx, aI @ np.abs(W).astype(np.float64), N, "dx")
+
+
+# ---------------------------------------------------------------------------
+# losses
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("B,K", [(1, 10), (32, 10), (513, 10), (7, 3)])
+def test_loss_ce(B, K):
+    rng = np.random.default_rng(B)
+    c = rng.integers(0, 26, (B, K)).astype(np.float32)
+    y = rng.integers(0, K, B).astype(np.int32)
+    loss = torch.empty(4, dtype=torch.float32, device=DEV)
+    g = torch.empty((B, K), dtype=torch.float32, device=DEV)
+    snn.snn_loss(snn.LOSS_CE_COUNT, B, K, _t(c), _t(y), None, loss, g, None)
+    L, rg = oracle.loss_ce(c, y)
+    assert abs(_np(loss)[0] - L) <= 1e-6 * max(1.0, abs(L))
+    assert_close(_np(g), rg, 1e-5, what="CE grad")
+
+
+@pytest.mark.parametrize("B,K", [(1, 1), (64, 1000), (64, 65536), (3, 7)])
+def test_loss_mse(B, K):
+    rng = np.random.default_rng(K)
+    c = rng.integers(0, 200, (B, K)).astype(np.float32)
+    y = rng.uniform(0, 50, (B, K)).astype(np.float32)
+    loss = torch.empty(4, dtype=torch.float32, device=DEV)
+    g = torch.empty((B, K), dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_loss_workspace_bytes(snn.LOSS_MSE_COUNT, B, K))
+    snn.snn_loss(snn.LOSS_MSE_COUNT, B, K, _t(c), None, _t(y), loss, g, ws)
+    L, rg = oracle.loss_mse(c, y)
+    assert abs(_np(loss)[0] - L) <= 1e-6 * abs(L)
+    assert_close(_np(g), rg, 1e-6, what="MSE grad")
+
+
+# ---------------------------------------------------------------------------
+# whole training steps
+# ---------------------------------------------------------------------------
+def _saved_u(net, li):
+    d = net.descs[li]
+    n = d.T * d.B * d.n_out
+    return _np(net.saved[li][: n * 4].view(torch.float32)).reshape(d.T, d.B, d.n_out)
+
+
+def _check_step_teacher_forced(wl, inp, net, tol=1e-3):
+    """Every stage of the GPU step against the oracle fed the GPU's inputs."""
+    T, B = wl.T, wl.B
+    n = len(wl.layers)
+    h = inp["x"]
+    xs = []
+    for li, spec in enumerate(wl.layers):
+        W, b = inp["params"][li]
+        xs.append(h)
+        z_gpu = _np(net.spk[li])
+        u_gpu = _saved_u(net, li)
+        if spec["kind"] == "dense":
+            xin = np.asarray(h, np.float64).reshape(T * B, -1)
+            I = oracle.dense_fwd(xin, W, b).astype(np.float32).reshape(T, B, -1)
+        else:
+            I = np.asarray(h, np.float32)
+        z, u, c = oracle.scan_fwd(I, spec["neuron"], spec["beta"], spec["thr"],
+                                  spec.get("alpha", 0.0))
+        assert_spikes(z_gpu, z, u, spec["thr"], what=f"L{li} spikes")
+        assert_close(u_gpu, u, tol, what=f"L{li} membrane")
+        h = z_gpu  # teacher-force the next layer on the GPU's spikes
+    L, gc = (oracle.loss_ce(_np(net.counts), inp["labels"]) if wl.loss == "ce"
+             else oracle.loss_mse(_np(net.counts), inp["targets"]))
+    assert abs(_np(net.loss)[0] - L) <= 1e-5 * max(1.0, abs(L))
+    assert_close(_np(net.gcounts), gc, 1e-5, what="dL/dcounts")
+    g = _np(net.gcounts)
+    for li in range(n - 1, -1, -1):
+        spec = wl.layers[li]
+        W = inp["params"][li][0]
+        u_gpu = _saved_u(net, li)
+        dI = oracle.scan_bwd(u_gpu, g, spec["neuron"], spec["beta"], spec["thr"], wl.slope,
+                             spec.get("alpha", 0.0))
+        if spec["kind"] == "none":
+            assert_close(_np(net.gx[li]), dI, tol, what="dL/dI")
+            break
+        xin = np.asarray(xs[li], np.float64).reshape(T * B, -1)
+        dW, db, dx = oracle.dense_bwd(dI.reshape(T * B, -1), xin, W, want_dx=li > 0)
+        assert_close(_np(net.gW[li]), dW, tol, what=f"L{li} dW")
+        assert_close(_np(net.gb[li]), db, tol, what=f"L{li} db")
+        if li > 0:
+            gx = _np(net.gx[li])
+            assert_close(gx.reshape(T * B, -1), dx, tol, what=f"L{li} dx")
+            g = gx  # teacher-force the layer below on the GPU's gradient
+
+
+@pytest.mark.parametrize("name", ["dsnn_leaky_t25_b32"])
+def test_step_full_size_teacher_forced(name):
+    wl = wls.get(name)
+    inp = wls.make_inputs(wl, seed=0)
+    net = snn.Network(wl, inp["params"], device=DEV)
+    net.step(_t(inp["x"]), labels=_t(inp["labels"]))
+    _check_step_teacher_forced(wl, inp, net)
+
+
+@pytest.mark.parametrize("name,T,B,width", [("dsnn_synaptic_t50_b256", 20, 16, 200),
+                                            ("dsnn_leaky_t25_b32", 25, 8, 300),
+                                            ("scan_wide_t1000_b64", 60, 4, 1000)])
+@pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
+def test_step_scaled_teacher_forced(name, T, B, width, reset):
+    wl = wls.scaled(wls.get(name), T=T, B=B, width=width)
+    inp = wls.make_inputs(wl, seed=1)
+    net = snn.Network(wl, inp["params"], device=DEV, reset_grad=reset)
+    lab = _t(inp["labels"]) if wl.loss == "ce" else None
+    tgt = _t(inp["targets"]) if wl.loss == "mse" else None
+    x = _t(inp["x"])
+    net.step(x, labels=lab, targets=tgt)
+    if reset == snn.RESET_DETACHED:
+        _check_step_teacher_forced(wl, inp, net)
+    # the stage calls give the same bytes as the layer calls
+    snap = [_np(t).copy() for t in net.gW if t is not None] + [_np(net.loss).copy()]
+    net.step_stages(x, labels=lab, targets=tgt)
+    snap2 = [_np(t) for t in net.gW if t is not None] + [_np(net.loss)]
+    for a, b in zip(snap, snap2):
+        np.testing.assert_array_equal(a, b)
+
+
+def test_step_end_to_end_unforced():
+    """The whole step, oracle run on its own; flips are counted, gradient
+    columns downstream of a flip are excluded."""
+    wl = wls.get("dsnn_leaky_t25_b32")
+    inp = wls.make_inputs(wl, seed=2)
+    net = snn.Network(wl, inp["params"], device=DEV)
+    net.step(_t(inp["x"]), labels=_t(inp["labels"]))
+    L, fwds, bwds = oracle.net_step(wl.layers, inp["params"], inp["x"].astype(np.float64), "ce",
+                                    labels=inp["labels"], slope=wl.slope)
+    roots = 0
+    for li, f in enumerate(fwds):
+        agree, r, illegal = spike_flips(_np(net.spk[li]), f["z"], f["u"], 1.0)
+        assert illegal == 0 and agree >= 0.9999
+        roots += r
+    if roots == 0:
+        assert abs(_np(net.loss)[0] - L) <= 1e-5 * abs(L)
+        for li in range(len(wl.layers)):
+            assert_close(_np(net.gW[li]), bwds[li]["dW"], 1e-3, what=f"L{li} dW")
+            assert_close(_np(net.gb[li]), bwds[li]["db"], 1e-3, what=f"L{li} db")
+
+
+def test_deterministic():
+    wl = wls.get("dsnn_synaptic_t50_b256")
+    wl = wls.scaled(wl, T=10, B=32)
+    inp = wls.make_inputs(wl, seed=3)
+    net = snn.Network(wl, inp["params"], device=DEV)
+    x, y = _t(inp["x"]), _t(inp["labels"])
+    net.step(x, labels=y)
+    a = [_np(t).copy() for t in net.gW + net.gb] + [_np(net.loss).copy()]
+    net.step(x, labels=y)
+    b = [_np(t) for t in net.gW + net.gb] + [_np(net.loss)]
+    for p, q in zip(a, b):
+        np.testing.assert_array_equal(p, q)
+
+
+def test_empty_time_and_batch():
+    for T, B in [(0, 4), (4, 0)]:
+        spec = dict(kind="dense", n_in=16, n_out=8, neuron="leaky", beta=0.9)
+        d = snn.layer_desc(spec, T, B)
+        x = torch.empty((max(T * B, 1), 16), dtype=torch.uint8, device=DEV)
+        W = torch.ones((8, 16), dtype=torch.float32, device=DEV)
+        spk = torch.empty(256, dtype=torch.uint8, device=DEV)
+        saved = torch.empty(256, dtype=torch.uint8, device=DEV)
+        counts = torch.full((max(B, 1), 8), 7.0, device=DEV)
+        snn.snn_layer_fwd(d, x, W, None, spk, saved, counts, _ws(256))
+        if B > 0:
+            assert (_np(counts) == 0).all()
+        gW = torch.full((8, 16), 3.0, device=DEV)
+        gb = torch.full((8,), 3.0, device=DEV)
+        g = torch.zeros(256, dtype=torch.float32, device=DEV)
+        snn.snn_layer_bwd(d, snn.GRAD_BCAST, g, x, W, saved, gW, gb, None,
+                          _ws(snn.snn_layer_workspace_bytes(d)))
+        assert (_np(gW) == 0).all() and (_np(gb) == 0).all()
