@@ -1,0 +1,290 @@
+#!/usr/bin/env python
+"""Training-step benchmark on one MI355X.
+
+A step is one forward + BPTT pass of the whole spiking network over one batch
+of synthetic rate-coded input (synapse and neuron scan per layer, loss on the
+output spike counts, then the reverse scan and weight/input gradients per
+layer), the quantity the paper times per minibatch (Sec. IV, "Baseline
+Throughput") minus the optimizer update.  Default workload: dense
+784-1000-10 with current-based neurons (eqs. 5-6), alpha 0.9, beta 0.8,
+T = 50, batch 256, fp32.
+
+Prints one JSON line: samples/s over the timed steps, the roofline of the
+dominant kernel (timed with HIP events on its own stream inside the timed
+region), the per-stage time split, and the CPU oracle timed on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "SNN training samples/sec (fwd+BPTT) at 1 GPU; scan HBM GB/s, GEMM MFMA %"
+PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
+PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
+PEAK_FP16_MFMA_TFLOPS = 2500.0
+
+
+def csrc_hash() -> str:
+    """Hash of the kernel sources, to tell whether a stored counter profile
+    still describes the kernels being timed."""
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2211_10725_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        with open(os.path.join(d, f), "rb") as fh:
+            h.update(f.encode() + fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(kernel_key: str):
+    """HBM bytes per launch of `kernel_key` from the committed counter
+    summary, if it was taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    m = re.search(r"csrc_hash:\s*([0-9a-f]+)", txt)
+    if not m or m.group(1) != csrc_hash():
+        return None
+    m = re.search(rf"^\|\s*{re.escape(kernel_key)}\s*\|[^|]*\|[^|]*\|[^|]*\|\s*([0-9.eE+]+)\s*\|",
+                  txt, re.M)
+    return float(m.group(1)) if m else None
+
+
+def stage_work(net, name, li):
+    """Algorithmic work of one stage launch: ('flop', F) for contractions,
+    ('byte', Bytes) for scans.  Per-unit figures:
+      contraction  2 M N K flops (one multiply and one add per MAC)
+      forward scan 4 B read current + 4 B write membrane + 1 B write spike per
+                   (t, b, n), + 4 B count per (b, n)
+      reverse scan 4 B read membrane + 4 B read dL/dz (full only) + 4 B write
+                   dL/dI per (t, b, n), + 4 B colsum per (b, n)."""
+    d = net.descs[li]
+    TB = d.T * d.B
+    if name == "synapse_fwd":
+        return "flop", 2.0 * TB * d.n_out * d.n_in
+    if name == "synapse_bwd":
+        f = 2.0 * TB * d.n_out * d.n_in  # dW
+        if li > 0:
+            f *= 2  # and dx
+        return "flop", f
+    el = TB * d.n_out
+    cols = d.B * d.n_out
+    if name == "neuron_fwd":
+        return "byte", 9.0 * el + 4.0 * cols
+    if name == "neuron_bwd":
+        full = li < len(net.descs) - 1
+        return "byte", (12.0 if full else 8.0) * el + 4.0 * cols
+    return None, 0.0
+
+
+def run_pmc_mode(net, x, y, tgt, steps):
+    """Kernels for counter collection: a 1 GiB device copy (calibration of
+    FETCH_SIZE / WRITE_SIZE against known bytes) and a few training steps."""
+    import torch
+    a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    for _ in range(3):
+        b.copy_(a)
+    for _ in range(steps):
+        net.step_stages(x, labels=y, targets=tgt)
+    torch.cuda.synchronize()
+    print(json.dumps({"pmc_mode": True, "copy_bytes": 2 * (1 << 30), "steps": steps,
+                      "csrc_hash": csrc_hash()}))
+
+
+def cpu_baseline(wl, inp, budget_s=30.0):
+    """The oracle as it stands, on this host's cores, over one full step of
+    the same workload (all B samples)."""
+    import oracle
+    t0 = time.perf_counter()
+    oracle.net_step(wl.layers, inp["params"], inp["x"], wl.loss, labels=inp.get("labels"),
+                    targets=inp.get("targets"), slope=wl.slope)
+    dt = time.perf_counter() - t0
+    return {"value": round(wl.B / dt, 3), "unit": "samples/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"one full fwd+BPTT step of {wl.name} (B={wl.B}, T={wl.T}) "
+                      f"in {dt:.2f} s, C oracle with OpenMP, fp64 contractions"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="dsnn_synaptic_t50_b256")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", choices=["bench", "pmc"], default="bench")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2211_10725_amd as snn
+    from paper_2211_10725_amd import workloads as wls
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    snn.lib()  # fail loudly before anything else if the HIP library is missing
+    torch.cuda.set_device(0)
+    wl = wls.get(args.workload)
+    inp = wls.make_inputs(wl, args.seed)
+    net = snn.Network(wl, inp["params"], device="cuda")
+    stream = torch.cuda.Stream()  # default priority
+    with torch.cuda.stream(stream):
+        x = torch.as_tensor(inp["x"]).to("cuda", non_blocking=False)
+        y = torch.as_tensor(inp["labels"]).cuda() if wl.loss == "ce" else None
+        tgt = torch.as_tensor(inp["targets"]).cuda() if wl.loss == "mse" else None
+    torch.cuda.synchronize()
+
+    if args.mode == "pmc":
+        with torch.cuda.stream(stream):
+            run_pmc_mode(net, x, y, tgt, max(1, args.steps))
+        return
+
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            net.step_stages(x, labels=y, targets=tgt)
+        torch.cuda.synchronize()
+
+        # per-stage split (one pass, outside the timed region): find the
+        # dominant single-kernel stage
+        evs = []
+
+        def rec(name, li):
+            e = torch.cuda.Event(enable_timing=True)
+            e.record(stream)
+            evs.append((name, li, e))
+
+        split_steps = 5
+        for _ in range(split_steps):
+            net.step_stages(x, labels=y, targets=tgt, hook=rec)
+        torch.cuda.synchronize()
+        split = {}
+        for (n0, l0, e0), (n1, l1, e1) in zip(evs, evs[1:]):
+            if n1 == n0 + "_end" and l1 == l0:
+                key = f"{n0}[L{l0}]" if l0 >= 0 else n0
+                split[key] = split.get(key, 0.0) + e0.elapsed_time(e1) / split_steps
+        # candidates: stages that launch exactly one kernel in this build
+        single = {k: v for k, v in split.items() if _single_kernel_stage(net, k)}
+        dom_key = max(single, key=single.get)
+        dom_name, dom_li = dom_key.split("[L")[0], int(dom_key.split("[L")[1].rstrip("]"))
+
+        # timed region: K steps, events around the dominant kernel's launch
+        kev = []
+
+        def rec_dom(name, li):
+            if li == dom_li and name in (dom_name, dom_name + "_end"):
+                e = torch.cuda.Event(enable_timing=True)
+                e.record(stream)
+                kev.append(e)
+
+        start = torch.cuda.Event(enable_timing=True)
+        end = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record(stream)
+        for _ in range(args.steps):
+            net.step_stages(x, labels=y, targets=tgt, hook=rec_dom)
+        end.record(stream)
+        torch.cuda.synchronize()
+        total_ms = start.elapsed_time(end)
+        kms = [kev[i].elapsed_time(kev[i + 1]) for i in range(0, len(kev), 2)]
+        k_avg_ms = sum(kms) / len(kms)
+
+    ms_per_step = total_ms / args.steps
+    value = wl.B * args.steps / (total_ms / 1000.0)
+    kind, work = stage_work(net, dom_name, dom_li)
+    if kind == "flop":
+        achieved = work / (k_avg_ms / 1000.0) / 1e12
+        peak = PEAK_FP16_MFMA_TFLOPS if wl.dtype == "f16" else PEAK_FP32_MFMA_TFLOPS
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s"}
+    else:
+        achieved = work / (k_avg_ms / 1000.0) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = round(achieved / roof["peak"], 4)
+    tr = stored_traffic(dom_key)
+    roof["traffic"] = tr
+    roof["kernel"] = dom_key
+    roof["avg_launch_ms"] = round(k_avg_ms, 5)
+    roof["algorithmic_per_launch"] = work
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f16" if wl.dtype == "f16" else "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.description, "T": wl.T,
+                   "batch": wl.B, "layers": [_layer_str(s) for s in wl.layers],
+                   "surrogate_slope": wl.slope, "input": "Bernoulli rate-coded spikes"
+                   if wl.input == "spikes" else "normal currents",
+                   "includes": "forward + loss + BPTT backward, no optimizer update"},
+        "roofline": roof,
+        "stage_ms": {k: round(v, 5) for k, v in split.items()},
+    }
+    syn = sum(v for k, v in split.items() if k.startswith("synapse"))
+    neu = sum(v for k, v in split.items() if k.startswith("neuron"))
+    out["spiking_vs_synaptic_ms"] = {"neuron_scans": round(neu, 5), "contractions": round(syn, 5)}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, inp)
+    print(json.dumps(out), flush=True)
+
+
+def _single_kernel_stage(net, key):
+    """Stages that launch exactly one kernel: a forward scan, or a forward
+    contraction that is not split over K."""
+    name, li = key.split("[L")[0], int(key.split("[L")[1].rstrip("]")) if "[L" in key else -1
+    if name == "neuron_fwd":
+        return True
+    if name == "synapse_fwd":
+        d = net.descs[li]
+        return _gemm_splits(d.T * d.B, d.n_out, d.n_in) == 1
+    return False
+
+
+def _gemm_splits(M, N, K):
+    """Mirror of the library's split-K choice (gemm.hip make_plan)."""
+    BK = 16
+    if N <= 16:
+        BM, BN = 64, 16
+    elif M <= 16:
+        BM, BN = 16, 64
+    else:
+        big = ((M + 127) // 128) * ((N + 127) // 128)
+        BM, BN = (128, 128) if big >= 192 else (64, 64)
+    tiles = ((M + BM - 1) // BM) * ((N + BN - 1) // BN)
+    ksteps = (K + BK - 1) // BK
+    S = 1
+    if tiles < 256:
+        S = (512 + tiles - 1) // tiles
+        S = min(S, max(1, ksteps // 8), 64)
+    k_chunk = ((ksteps + S - 1) // S) * BK
+    return (K + k_chunk - 1) // k_chunk
+
+
+def _layer_str(s):
+    if s["kind"] == "dense":
+        return f"dense {s['n_in']}->{s['n_out']} {s['neuron']}"
+    if s["kind"] == "conv":
+        return f"conv5 {s['c_in']}->{s['c_out']} pool2 {s['neuron']}"
+    return f"scan-only {s['n']} {s['neuron']}"
+
+
+if __name__ == "__main__":
+    main()
