@@ -35,8 +35,11 @@
  *     the host before anything is launched; on error nothing is launched and
  *     outputs are untouched.  A failed launch returns SNN_ERR_HIP.
  *   - Outputs are overwritten, never accumulated into.
- *   - Arithmetic: contractions accumulate in fp32 (operands fp32, or fp16
- *     for SNN_F16 weights); neuron state is fp32; loss reductions in fp64.
+ *   - Arithmetic: contractions accumulate in fp32 with exact products
+ *     (fp32 operands, fp16 weights, and spikes, which are exact in bf16: a
+ *     spike x fp32 contraction runs as three bf16 MFMA passes over the exact
+ *     split of the fp32 operand unless SNN_FLAG_FP32_MFMA is set); neuron
+ *     state is fp32; loss reductions in fp64.
  *   - T == 0 or B == 0 is valid: no compute is launched, and outputs that
  *     are sums over an empty range (counts, grad_w, grad_b) are set to 0.
  *     A loss over B == 0 or K == 0 is rejected (SNN_ERR_SHAPE).
@@ -91,6 +94,12 @@ typedef enum snn_status {
 #define SNN_GRAD_BCAST 1 /* g [B,n_out] fp32, the same for every t (a loss on
                             counts summed over T) */
 
+/* descriptor flags */
+#define SNN_FLAG_FP32_MFMA 1 /* contract spike x fp32 operands with fp32 MFMA
+                                instead of three exact bf16 MFMA passes (the
+                                fp32 operand split into hi + mid + lo bf16
+                                parts, every product exact, fp32 accumulate) */
+
 /* losses on spike counts */
 #define SNN_LOSS_CE_COUNT 0  /* labels int32 [B] in [0,K) */
 #define SNN_LOSS_MSE_COUNT 1 /* targets fp32 [B,K] */
@@ -109,7 +118,7 @@ typedef struct snn_layer_desc {
     int32_t grad_dtype;     /* dL/dI handed to the weight / input gradient
                                contractions: SNN_F32 | SNN_BF16 | SNN_F16 */
     int32_t reset_grad;     /* SNN_RESET_DETACHED | SNN_RESET_SURROGATE */
-    int32_t flags;          /* must be 0 */
+    int32_t flags;          /* 0 or SNN_FLAG_FP32_MFMA */
     float beta;             /* membrane decay, eqs. (4)/(6) */
     float alpha;            /* synaptic decay, eq. (5); ignored for Leaky */
     float threshold;        /* u_thr */

@@ -30,6 +30,7 @@ SYN_DENSE, SYN_CONV5_POOL2, SYN_NONE = 0, 1, 2
 RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST = 0, 1
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
+FLAG_FP32_MFMA = 1
 ABI_VERSION = 1
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
@@ -201,8 +202,9 @@ _NEURON = {"leaky": LEAKY, "synaptic": SYNAPTIC}
 
 
 def layer_desc(spec: dict, T: int, B: int, in_dtype=U8, w_dtype=F32, out_dtype=U8,
-               grad_dtype=F32, slope=25.0, reset_grad=RESET_DETACHED) -> LayerDesc:
+               grad_dtype=F32, slope=25.0, reset_grad=RESET_DETACHED, flags=0) -> LayerDesc:
     d = LayerDesc()
+    d.flags = flags
     d.T, d.B = T, B
     d.neuron = _NEURON[spec["neuron"]]
     d.beta = spec["beta"]
@@ -232,7 +234,7 @@ class Network:
     All buffers are allocated once here (torch, device memory only); ``step``
     then only enqueues library calls on the current stream."""
 
-    def __init__(self, wl, params, device="cuda", reset_grad=RESET_DETACHED):
+    def __init__(self, wl, params, device="cuda", reset_grad=RESET_DETACHED, flags=0):
         import torch
         self.torch = torch
         self.wl = wl
@@ -244,7 +246,8 @@ class Network:
         for li, spec in enumerate(wl.layers):
             in_dt = F32 if spec["kind"] == "none" else U8
             d = layer_desc(spec, T, B, in_dtype=in_dt, w_dtype=F16 if half else F32,
-                           out_dtype=U8, grad_dtype=F32, slope=wl.slope, reset_grad=reset_grad)
+                           out_dtype=U8, grad_dtype=F32, slope=wl.slope, reset_grad=reset_grad,
+                           flags=flags)
             self.descs.append(d)
             W, b = params[li]
             if W is None:

@@ -16,7 +16,7 @@ bool finite(float x) { return isfinite(x) != 0; }
 // Validates a layer descriptor; nothing here touches the device.
 snn_status check_desc(const snn_layer_desc *d) {
     if (!d) return SNN_ERR_NULL;
-    if (d->flags != 0) return SNN_ERR_UNSUPPORTED;
+    if (d->flags & ~SNN_FLAG_FP32_MFMA) return SNN_ERR_UNSUPPORTED;
     if (d->T < 0 || d->B < 0 || d->n_in < 0 || d->n_out < 0) return SNN_ERR_SHAPE;
     if (d->neuron != SNN_LEAKY && d->neuron != SNN_SYNAPTIC) return SNN_ERR_UNSUPPORTED;
     if (d->reset_grad != SNN_RESET_DETACHED && d->reset_grad != SNN_RESET_SURROGATE)
@@ -60,12 +60,16 @@ snn_status check_desc(const snn_layer_desc *d) {
 
 int64_t rows(const snn_layer_desc *d) { return (int64_t)d->T * d->B; }
 
+// spike x fp32 contractions may use the exact three-pass bf16 kernels
+bool split_ok(const snn_layer_desc *d) { return (d->flags & SNN_FLAG_FP32_MFMA) == 0; }
+
 // ---- workspace layout ------------------------------------------------------
 // forward:  [gemm split-K partials]
 // backward: [dcur (grad_dtype) T*B*n_out][colsum fp32 B*n_out][gemm partials]
 size_t fwd_ws(const snn_layer_desc *d) {
     if (d->synapse != SNN_SYN_DENSE) return 0;
-    return gemm_workspace_bytes((int)rows(d), d->n_out, d->n_in, d->in_dtype, d->w_dtype);
+    return gemm_workspace_bytes((int)rows(d), d->n_out, d->n_in, d->in_dtype, d->w_dtype, true,
+                                true, split_ok(d));
 }
 size_t dcur_bytes(const snn_layer_desc *d) {
     if (d->synapse == SNN_SYN_NONE) return 0;
@@ -77,8 +81,10 @@ size_t colsum_bytes(const snn_layer_desc *d) {
 size_t bwd_gemm_ws(const snn_layer_desc *d) {
     if (d->synapse != SNN_SYN_DENSE) return 0;
     const int M = (int)rows(d);
-    const size_t dw = gemm_workspace_bytes(d->n_out, d->n_in, M, d->grad_dtype, d->in_dtype);
-    const size_t dx = gemm_workspace_bytes(M, d->n_in, d->n_out, d->grad_dtype, d->w_dtype);
+    const size_t dw = gemm_workspace_bytes(d->n_out, d->n_in, M, d->grad_dtype, d->in_dtype,
+                                           false, false, split_ok(d));
+    const size_t dx = gemm_workspace_bytes(M, d->n_in, d->n_out, d->grad_dtype, d->w_dtype,
+                                           true, false, split_ok(d));
     return dw > dx ? dw : dx;
 }
 size_t bwd_ws(const snn_layer_desc *d) { return dcur_bytes(d) + colsum_bytes(d) + bwd_gemm_ws(d); }
@@ -146,7 +152,7 @@ snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w
     g.K = d->n_in;
     g.A = x; g.lda = d->n_in; g.a_dtype = d->in_dtype; g.a_kc = true;
     g.B = w; g.ldb = d->n_in; g.b_dtype = d->w_dtype; g.b_kc = true;
-    g.C = cur; g.ldc = d->n_out; g.bias = bias;
+    g.C = cur; g.ldc = d->n_out; g.bias = bias; g.allow_split = split_ok(d);
     return hip_status(launch_gemm(g, ws, ws_bytes, stream));
 }
 
@@ -237,7 +243,7 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
         g.M = d->n_out; g.N = d->n_in; g.K = M;
         g.A = dcur; g.lda = d->n_out; g.a_dtype = d->grad_dtype; g.a_kc = false;
         g.B = x; g.ldb = d->n_in; g.b_dtype = d->in_dtype; g.b_kc = false;
-        g.C = grad_w; g.ldc = d->n_in; g.bias = nullptr;
+        g.C = grad_w; g.ldc = d->n_in; g.bias = nullptr; g.allow_split = split_ok(d);
         hipError_t e = launch_gemm(g, ws, ws_bytes, stream);
         if (e != hipSuccess) return SNN_ERR_HIP;
     }
@@ -247,7 +253,7 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
         g.M = M; g.N = d->n_in; g.K = d->n_out;
         g.A = dcur; g.lda = d->n_out; g.a_dtype = d->grad_dtype; g.a_kc = true;
         g.B = w; g.ldb = d->n_in; g.b_dtype = d->w_dtype; g.b_kc = false;
-        g.C = grad_x; g.ldc = d->n_in; g.bias = nullptr;
+        g.C = grad_x; g.ldc = d->n_in; g.bias = nullptr; g.allow_split = split_ok(d);
         hipError_t e = launch_gemm(g, ws, ws_bytes, stream);
         if (e != hipSuccess) return SNN_ERR_HIP;
     }

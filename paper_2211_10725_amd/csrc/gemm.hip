@@ -137,10 +137,15 @@ __global__ __launch_bounds__(kThreads) void gemm_f32_kernel(
     __shared__ float As[BK * SA];
     __shared__ float Bs[BK * SB];
 
-    const int tile = blockIdx.x;
+    // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2);
+    // renumber them so that each XCD runs a contiguous range of work items,
+    // ordered (split, m-tile, n-tile): neighbours share an operand tile.
+    const int item = xcd_local_item();
+    const int tiles = gridDim.x;
+    const int zk = item / tiles, tile = item % tiles;
     const int tm = tile / tiles_n, tn = tile % tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
-    const int kbeg = blockIdx.z * k_chunk;
+    const int kbeg = zk * k_chunk;
     const int kend = min(K, kbeg + k_chunk);
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -189,7 +194,7 @@ __global__ __launch_bounds__(kThreads) void gemm_f32_kernel(
 
     // D layout of a 16x16 block: lane holds column (lane & 15), rows
     // 4*(lane >> 4) + r for the four accumulator registers r.
-    float *Cz = C + (int64_t)blockIdx.z * split_stride;
+    float *Cz = C + (int64_t)zk * split_stride;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -295,9 +300,18 @@ void launch_btype(const GemmArgs &g, const Plan &p, float *out, int64_t ldo, int
 
 }  // namespace
 
-size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype) {
-    (void)a_dtype; (void)b_dtype;
+size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype, bool a_kc, bool b_kc,
+                            bool allow_split) {
     if (M <= 0 || N <= 0 || K <= 0) return 0;
+    GemmArgs probe{};
+    probe.M = M;
+    probe.N = N;
+    probe.a_dtype = a_dtype;
+    probe.b_dtype = b_dtype;
+    if (allow_split && gemm_bf16_applies(probe)) {
+        const bool a_f32 = a_dtype == SNN_F32;
+        return gemm_bf16_workspace_bytes(M, N, K, a_f32, a_f32 ? a_kc : b_kc);
+    }
     const Plan p = make_plan(M, N, K);
     if (p.splits <= 1) return 0;
     return align_up((size_t)p.splits * M * N * sizeof(float));
@@ -309,6 +323,7 @@ hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t
         // empty contraction: C = bias (or 0)
         return hipErrorInvalidValue;
     }
+    if (g.allow_split && gemm_bf16_applies(g)) return launch_gemm_bf16(g, ws, ws_bytes, s);
     const Plan p = make_plan(g.M, g.N, g.K);
     float *out = g.C;
     int64_t ldo = g.ldc, ss = 0;
@@ -329,13 +344,16 @@ hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (p.splits > 1) {
-        const int64_t total = (int64_t)g.M * g.N;
-        splitk_reduce_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(
-            g.M, g.N, p.splits, out, g.C, g.ldc, g.bias);
-        e = hipGetLastError();
-    }
+    if (p.splits > 1) e = launch_splitk_reduce(g.M, g.N, p.splits, out, g.C, g.ldc, g.bias, s);
     return e;
+}
+
+hipError_t launch_splitk_reduce(int M, int N, int S, const float *P, float *C, int64_t ldc,
+                                const float *bias, hipStream_t s) {
+    const int64_t total = (int64_t)M * N;
+    splitk_reduce_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(
+        M, N, S, P, C, ldc, bias);
+    return hipGetLastError();
 }
 
 }  // namespace snn

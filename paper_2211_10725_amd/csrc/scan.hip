@@ -14,7 +14,10 @@ namespace snn {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kDepth = 8;  // time steps prefetched ahead per lane
+// Lanes own 4 columns and prefetch 8 steps when there are enough columns to
+// fill the chip; otherwise 1 column and 16 steps, which gives 4x the waves
+// and halves the number of exposed memory round trips of the serial scan.
+constexpr int kWideColumns = 4 * 64 * 2048;  // 2048 waves of 4-column lanes
 
 template <int VEC>
 struct Vec;
@@ -60,7 +63,7 @@ __device__ inline void store_spikes_f16(uint16_t *p, const float (&z)[VEC]) {
 
 // Forward scan.  `cur` and `u_out` may alias exactly: each lane reads step t
 // of its columns before it writes step t, and prefetches only later steps.
-template <int NEURON, int VEC, int OUT>
+template <int NEURON, int VEC, int OUT, int kDepth>
 __global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, float alpha,
                                                               float beta, float thr,
                                                               const float *cur, void *spk,
@@ -147,7 +150,7 @@ __device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC]
 }
 
 // Reverse-time scan.  lam carries dL/du_{t+1} (and lami dL/di_{t+1}).
-template <int NEURON, int VEC, bool BCAST, bool RESET_SURR, int GT>
+template <int NEURON, int VEC, bool BCAST, bool RESET_SURR, int GT, int kDepth>
 __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
     int T, int64_t C, float alpha, float beta, float thr, float slope,
     const float *__restrict__ u, const float *__restrict__ g, void *__restrict__ dcur,
@@ -214,16 +217,27 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
     if (colsum) Vec<VEC>::store(colsum + col, acc);
 }
 
+// Bias gradient: db[f] = sum over b (and pooled positions p) of the per-column
+// time sums.  A block owns 64 consecutive features (one per lane); its four
+// waves take every fourth batch row, each lane summing in fp64 in a fixed
+// order, and the four partial sums are added in wave order.
 __global__ __launch_bounds__(kThreads) void bias_reduce_kernel(int B, int F, int P,
                                                                const float *__restrict__ colsum,
                                                                float *__restrict__ db) {
-    const int f = blockIdx.x * kThreads + threadIdx.x;
-    if (f >= F) return;
+    __shared__ double part[4][64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int f = blockIdx.x * 64 + lane;
     const int64_t row = (int64_t)F * P;
     double acc = 0.0;
-    for (int b = 0; b < B; ++b)
-        for (int p = 0; p < P; ++p) acc += (double)colsum[b * row + (int64_t)f * P + p];
-    db[f] = (float)acc;
+    if (f < F) {
+        const float *base = colsum + (int64_t)f * P;
+#pragma unroll 8
+        for (int b = wave; b < B; b += 4)
+            for (int p = 0; p < P; ++p) acc += (double)base[b * row + p];
+    }
+    part[wave][lane] = acc;
+    __syncthreads();
+    if (wave == 0 && f < F) db[f] = (float)(((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane]);
 }
 
 __global__ __launch_bounds__(kThreads) void fill_zero_kernel(float *__restrict__ p, int64_t n) {
@@ -236,7 +250,7 @@ void fwd_launch(int T, int64_t C, float alpha, float beta, float thr, const floa
                 void *spk, float *u_out, float *counts, hipStream_t s) {
     const int64_t lanes = (C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_fwd_kernel<NEURON, VEC, OUT><<<grid, kThreads, 0, s>>>(T, C, alpha, beta, thr, cur,
+    neuron_fwd_kernel<NEURON, VEC, OUT, VEC == 4 ? 8 : 16><<<grid, kThreads, 0, s>>>(T, C, alpha, beta, thr, cur,
                                                                  spk, u_out, counts);
 }
 
@@ -245,7 +259,7 @@ void bwd_launch(int T, int64_t C, float alpha, float beta, float thr, float slop
                 const float *u, const float *g, void *dcur, float *colsum, hipStream_t s) {
     const int64_t lanes = (C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_bwd_kernel<NEURON, VEC, BCAST, RS, GT><<<grid, kThreads, 0, s>>>(
+    neuron_bwd_kernel<NEURON, VEC, BCAST, RS, GT, VEC == 4 ? 8 : 16><<<grid, kThreads, 0, s>>>(
         T, C, alpha, beta, thr, slope, u, g, dcur, colsum);
 }
 
@@ -279,7 +293,7 @@ hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, float alpha, float be
                              const float *cur, void *spk, int out_dtype, float *u_out,
                              float *counts, hipStream_t s) {
     if (T <= 0 || C <= 0) return hipSuccess;
-    const bool v4 = (C % 4) == 0;
+    const bool v4 = (C % 4) == 0 && C >= kWideColumns;
 #define SNN_FWD(N, V, O) fwd_launch<N, V, O>(T, C, alpha, beta, thr, cur, spk, u_out, counts, s)
     if (neuron == SNN_SYNAPTIC) {
         if (out_dtype == SNN_U8) { if (v4) SNN_FWD(SNN_SYNAPTIC, 4, SNN_U8); else SNN_FWD(SNN_SYNAPTIC, 1, SNN_U8); }
@@ -297,7 +311,7 @@ hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, 
                              int g_bcast, void *dcur, int grad_dtype, float *colsum,
                              hipStream_t s) {
     if (T <= 0 || C <= 0) return hipSuccess;
-    const bool v4 = (C % 4) == 0;
+    const bool v4 = (C % 4) == 0 && C >= kWideColumns;
     if (neuron == SNN_SYNAPTIC) {
         if (v4) bwd_dispatch<SNN_SYNAPTIC, 4>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
         else bwd_dispatch<SNN_SYNAPTIC, 1>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
@@ -316,7 +330,7 @@ hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s) {
 
 hipError_t launch_bias_reduce(int B, int F, int P, const float *colsum, float *db, hipStream_t s) {
     if (F <= 0) return hipSuccess;
-    bias_reduce_kernel<<<(F + kThreads - 1) / kThreads, kThreads, 0, s>>>(B, F, P, colsum, db);
+    bias_reduce_kernel<<<(F + 63) / 64, kThreads, 0, s>>>(B, F, P, colsum, db);
     return hipGetLastError();
 }
 

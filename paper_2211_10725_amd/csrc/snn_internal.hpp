@@ -13,6 +13,19 @@ constexpr size_t kAlign = 256;  // workspace sub-buffers start on 256-byte bound
 
 inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+constexpr int kXcds = 8;  // MI355X: 8 accelerator complex dies, one L2 each
+
+// Linear workgroup id renumbered so that the workgroups the dispatcher sends
+// to one XCD (ids congruent mod 8) cover one contiguous range of work items.
+// A bijection on [0, gridDim.x * gridDim.y * gridDim.z).
+__device__ inline int xcd_local_item() {
+    const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    const int total = gridDim.x * gridDim.y * gridDim.z;
+    const int xcd = lin % kXcds, idx = lin / kXcds;
+    const int per = total / kXcds, rem = total % kXcds;
+    return xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
+}
+
 inline size_t dtype_bytes(int dt) {
     switch (dt) {
         case SNN_F32: return 4;
@@ -59,9 +72,19 @@ struct GemmArgs {
     float *C;
     int64_t ldc;
     const float *bias;  // [N] or NULL
+    bool allow_split;   // spike x fp32 may run as three exact bf16 passes
 };
-size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype);
+size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype, bool a_kc,
+                            bool b_kc, bool allow_split);
 hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
+// C[m,n] = sum_{z<S} P[z][m][n] (+ bias[n]), fixed order
+hipError_t launch_splitk_reduce(int M, int N, int S, const float *P, float *C, int64_t ldc,
+                                const float *bias, hipStream_t s);
+
+// ---- spike x fp32 on bf16 matrix cores (gemm_bf16.hip) -----------------------
+bool gemm_bf16_applies(const GemmArgs &g);
+size_t gemm_bf16_workspace_bytes(int M, int N, int K, bool a_f32, bool f32_kc);
+hipError_t launch_gemm_bf16(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
 
 // ---- losses (loss.hip) -----------------------------------------------------
 size_t loss_workspace_bytes(int kind, int B, int K);

@@ -54,7 +54,7 @@ def test_validation_errors_before_launch():
     assert _fwd(bad) == 5
     bad = d.copy(); bad.in_dtype = 9
     assert _fwd(bad) == 3
-    bad = d.copy(); bad.flags = 1
+    bad = d.copy(); bad.flags = 2
     assert _fwd(bad) == 5
     bad = d.copy(); bad.slope = float("nan")
     assert _fwd(bad) == 2

@@ -52,7 +52,8 @@ def _ws(nbytes):
 # neuron scans
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("neuron,alpha,beta", [("leaky", 0.0, 0.95), ("synaptic", 0.9, 0.8)])
-@pytest.mark.parametrize("T,B,N", [(1, 2, 8), (7, 3, 101), (33, 4, 256), (50, 5, 1001)])
+@pytest.mark.parametrize("T,B,N", [(1, 2, 8), (7, 3, 101), (33, 4, 256), (50, 5, 1001),
+                                   (6, 8, 65536), (3, 9, 65537)])
 def test_scan_fwd_bit_exact(neuron, alpha, beta, T, B, N):
     rng = np.random.default_rng(T * 1000 + N)
     I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
@@ -85,7 +86,7 @@ def test_scan_fwd_in_place_and_f16_spikes():
 @pytest.mark.parametrize("neuron,alpha,beta", [("leaky", 0.0, 0.95), ("synaptic", 0.9, 0.8)])
 @pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
 @pytest.mark.parametrize("bcast", [True, False])
-@pytest.mark.parametrize("T,B,N", [(1, 2, 8), (9, 3, 37), (40, 4, 512)])
+@pytest.mark.parametrize("T,B,N", [(1, 2, 8), (9, 3, 37), (40, 4, 512), (5, 8, 65536)])
 def test_scan_bwd(neuron, alpha, beta, reset, bcast, T, B, N):
     rng = np.random.default_rng(7 * T + N)
     I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
@@ -126,9 +127,13 @@ GEMM_SHAPES = [(37, 29, 53), (800, 1000, 784), (128, 10, 1000), (300, 7, 33), (6
                (5, 300, 17)]
 
 
-@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+PATHS = {"split": 0, "fp32mfma": snn.FLAG_FP32_MFMA}
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784)])
 @pytest.mark.parametrize("wdt", ["f32", "f16"])
-def test_synapse_fwd(M, N, K, wdt):
+@pytest.mark.parametrize("path", list(PATHS))
+def test_synapse_fwd(M, N, K, wdt, path):
     rng = np.random.default_rng(M + N + K)
     x = (rng.random((M, K)) < 0.5).astype(np.uint8)
     W = rng.uniform(-1, 1, (N, K)).astype(np.float32)
@@ -136,7 +141,8 @@ def test_synapse_fwd(M, N, K, wdt):
         W = W.astype(np.float16).astype(np.float32)
     b = rng.uniform(-1, 1, N).astype(np.float32)
     spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
-    d = snn.layer_desc(spec, 1, M, w_dtype=snn.F16 if wdt == "f16" else snn.F32)
+    d = snn.layer_desc(spec, 1, M, w_dtype=snn.F16 if wdt == "f16" else snn.F32,
+                       flags=PATHS[path])
     cur = torch.empty((M, N), dtype=torch.float32, device=DEV)
     ws = _ws(snn.snn_layer_workspace_bytes(d))
     Wt = _t(W, torch.float16 if wdt == "f16" else torch.float32)
@@ -148,15 +154,16 @@ def test_synapse_fwd(M, N, K, wdt):
                      K, "currents")
 
 
-@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
-def test_synapse_bwd(M, N, K):
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784)])
+@pytest.mark.parametrize("path", list(PATHS))
+def test_synapse_bwd(M, N, K, path):
     """dW = dI^T x (split over K = T*B) and dx = dI W."""
     rng = np.random.default_rng(3 * M + N)
     x = (rng.random((M, K)) < 0.5).astype(np.uint8)
     W = rng.uniform(-1, 1, (N, K)).astype(np.float32)
     dI = rng.normal(0, 1, (M, N)).astype(np.float32)
     spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
-    d = snn.layer_desc(spec, 1, M)
+    d = snn.layer_desc(spec, 1, M, flags=PATHS[path])
     gW = torch.empty((N, K), dtype=torch.float32, device=DEV)
     gx = torch.empty((M, K), dtype=torch.float32, device=DEV)
     ws = _ws(snn.snn_layer_workspace_bytes(d))
@@ -209,8 +216,18 @@ def _saved_u(net, li):
     return _np(net.saved[li][: n * 4].view(torch.float32)).reshape(d.T, d.B, d.n_out)
 
 
-def _check_step_teacher_forced(wl, inp, net, tol=1e-3):
-    """Every stage of the GPU step against the oracle fed the GPU's inputs."""
+def _gpu_currents(net, li, xin):
+    """Currents of layer li recomputed by the stage call on the GPU's input."""
+    d = net.descs[li]
+    cur = torch.empty((d.T, d.B, d.n_out), dtype=torch.float32, device=DEV)
+    snn.snn_synapse_fwd(d, xin, net.W[li], net.b[li], cur, None, net.ws)
+    return _np(cur)
+
+
+def _check_step_teacher_forced(wl, inp, net, x_dev, tol=1e-3):
+    """Every stage of the GPU step against the oracle fed the GPU's inputs:
+    contraction vs oracle contraction on the same spikes; oracle scan on the
+    GPU's own currents must reproduce spikes, membrane and counts exactly."""
     T, B = wl.T, wl.B
     n = len(wl.layers)
     h = inp["x"]
@@ -222,13 +239,17 @@ def _check_step_teacher_forced(wl, inp, net, tol=1e-3):
         u_gpu = _saved_u(net, li)
         if spec["kind"] == "dense":
             xin = np.asarray(h, np.float64).reshape(T * B, -1)
-            I = oracle.dense_fwd(xin, W, b).astype(np.float32).reshape(T, B, -1)
+            I_orc = oracle.dense_fwd(xin, W, b).reshape(T, B, -1)
+            I = _gpu_currents(net, li, x_dev if li == 0 else net.spk[li - 1])
+            assert_close(I, I_orc, tol, what=f"L{li} currents")
         else:
             I = np.asarray(h, np.float32)
         z, u, c = oracle.scan_fwd(I, spec["neuron"], spec["beta"], spec["thr"],
                                   spec.get("alpha", 0.0))
-        assert_spikes(z_gpu, z, u, spec["thr"], what=f"L{li} spikes")
-        assert_close(u_gpu, u, tol, what=f"L{li} membrane")
+        np.testing.assert_array_equal(z_gpu, z, err_msg=f"L{li} spikes")
+        np.testing.assert_array_equal(u_gpu, u, err_msg=f"L{li} membrane")
+        if li == n - 1:
+            np.testing.assert_array_equal(_np(net.counts).reshape(c.shape), c)
         h = z_gpu  # teacher-force the next layer on the GPU's spikes
     L, gc = (oracle.loss_ce(_np(net.counts), inp["labels"]) if wl.loss == "ce"
              else oracle.loss_mse(_np(net.counts), inp["targets"]))
@@ -254,29 +275,32 @@ def _check_step_teacher_forced(wl, inp, net, tol=1e-3):
             g = gx  # teacher-force the layer below on the GPU's gradient
 
 
-@pytest.mark.parametrize("name", ["dsnn_leaky_t25_b32"])
-def test_step_full_size_teacher_forced(name):
+@pytest.mark.parametrize("name", ["dsnn_leaky_t25_b32", "dsnn_synaptic_t50_b256"])
+@pytest.mark.parametrize("path", list(PATHS))
+def test_step_full_size_teacher_forced(name, path):
     wl = wls.get(name)
     inp = wls.make_inputs(wl, seed=0)
-    net = snn.Network(wl, inp["params"], device=DEV)
-    net.step(_t(inp["x"]), labels=_t(inp["labels"]))
-    _check_step_teacher_forced(wl, inp, net)
+    net = snn.Network(wl, inp["params"], device=DEV, flags=PATHS[path])
+    x = _t(inp["x"])
+    net.step(x, labels=_t(inp["labels"]))
+    _check_step_teacher_forced(wl, inp, net, x)
 
 
 @pytest.mark.parametrize("name,T,B,width", [("dsnn_synaptic_t50_b256", 20, 16, 200),
                                             ("dsnn_leaky_t25_b32", 25, 8, 300),
                                             ("scan_wide_t1000_b64", 60, 4, 1000)])
 @pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
-def test_step_scaled_teacher_forced(name, T, B, width, reset):
+@pytest.mark.parametrize("path", list(PATHS))
+def test_step_scaled_teacher_forced(name, T, B, width, reset, path):
     wl = wls.scaled(wls.get(name), T=T, B=B, width=width)
     inp = wls.make_inputs(wl, seed=1)
-    net = snn.Network(wl, inp["params"], device=DEV, reset_grad=reset)
+    net = snn.Network(wl, inp["params"], device=DEV, reset_grad=reset, flags=PATHS[path])
     lab = _t(inp["labels"]) if wl.loss == "ce" else None
     tgt = _t(inp["targets"]) if wl.loss == "mse" else None
     x = _t(inp["x"])
     net.step(x, labels=lab, targets=tgt)
     if reset == snn.RESET_DETACHED:
-        _check_step_teacher_forced(wl, inp, net)
+        _check_step_teacher_forced(wl, inp, net, x)
     # the stage calls give the same bytes as the layer calls
     snap = [_np(t).copy() for t in net.gW if t is not None] + [_np(net.loss).copy()]
     net.step_stages(x, labels=lab, targets=tgt)
