@@ -260,6 +260,7 @@ class Network:
                                                                          dtype=torch.float32))
         u8 = torch.uint8
         self.spk = [torch.empty((T, B, d.n_out), dtype=u8, device=device) for d in self.descs]
+        self.in_shape = (T, B) + tuple(wl.in_shape)
         self.saved = [torch.empty(snn_layer_saved_bytes(d), dtype=u8, device=device)
                       for d in self.descs]
         self.gW = [None if w is None else torch.empty(w.shape, dtype=torch.float32, device=device)
@@ -308,6 +309,14 @@ class Network:
         self.loss_and_grad(labels, targets, stream)
         self.backward(x, stream)
 
+    def pool_arg(self, li):
+        """The 2x2 pool selection of conv layer li inside its saved buffer."""
+        d = self.descs[li]
+        if d.synapse != SYN_CONV5_POOL2:
+            return None
+        off = (d.T * d.B * d.n_out * 4 + 255) // 256 * 256
+        return self.saved[li][off:]
+
     # the same work through the stage calls, with a hook between stages
     def step_stages(self, x, labels=None, targets=None, stream=None, hook=None):
         hook = hook or (lambda name, li: None)
@@ -317,7 +326,8 @@ class Network:
             cur = self.saved[li]
             if d.synapse != SYN_NONE:
                 hook("synapse_fwd", li)
-                snn_synapse_fwd(d, h, self.W[li], self.b[li], cur, None, self.ws, stream)
+                snn_synapse_fwd(d, h, self.W[li], self.b[li], cur, self.pool_arg(li), self.ws,
+                                stream)
                 hook("synapse_fwd_end", li)
             else:
                 cur = h
@@ -345,7 +355,7 @@ class Network:
             snn_neuron_bwd(d, kind, g, self.saved[li], dcur, self.gb[li], rest, stream)
             hook("neuron_bwd_end", li)
             hook("synapse_bwd", li)
-            snn_synapse_bwd(d, dcur, None, xin, self.W[li], self.gW[li], self.gx[li], rest,
-                            stream)
+            snn_synapse_bwd(d, dcur, self.pool_arg(li), xin, self.W[li], self.gW[li], self.gx[li],
+                            rest, stream)
             hook("synapse_bwd_end", li)
             kind, g = GRAD_FULL, self.gx[li]

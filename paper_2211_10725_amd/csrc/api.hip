@@ -42,8 +42,8 @@ snn_status check_desc(const snn_layer_desc *d) {
             if ((int64_t)d->c_in * d->h_in * d->w_in != d->n_in) return SNN_ERR_SHAPE;
             if ((int64_t)d->c_out * hp * wp != d->n_out) return SNN_ERR_SHAPE;
             if (d->in_dtype != SNN_U8 && d->in_dtype != SNN_F32) return SNN_ERR_DTYPE;
-            if (d->w_dtype != SNN_F32) return SNN_ERR_DTYPE;
-            return SNN_ERR_UNSUPPORTED;  // convolutional synapse not in this build yet
+            if (d->w_dtype != SNN_F32 || d->grad_dtype != SNN_F32) return SNN_ERR_DTYPE;
+            break;
         }
         case SNN_SYN_NONE:
             if (d->n_in != d->n_out || d->n_out < 1) return SNN_ERR_SHAPE;
@@ -59,6 +59,23 @@ snn_status check_desc(const snn_layer_desc *d) {
 }
 
 int64_t rows(const snn_layer_desc *d) { return (int64_t)d->T * d->B; }
+
+ConvGeom conv_geom(const snn_layer_desc *d) {
+    ConvGeom g{};
+    g.NB = (int)rows(d);
+    g.Ci = d->c_in;
+    g.H = d->h_in;
+    g.W = d->w_in;
+    g.Co = d->c_out;
+    g.Ho = d->h_in - 4;
+    g.Wo = d->w_in - 4;
+    g.Hp = g.Ho / 2;
+    g.Wp = g.Wo / 2;
+    return g;
+}
+
+// byte offset of the pool selection inside the saved buffer (conv layers)
+size_t arg_offset(const snn_layer_desc *d) { return align_up((size_t)rows(d) * d->n_out * sizeof(float)); }
 
 // spike x fp32 contractions may use the exact three-pass bf16 kernels
 bool split_ok(const snn_layer_desc *d) { return (d->flags & SNN_FLAG_FP32_MFMA) == 0; }
@@ -79,6 +96,8 @@ size_t colsum_bytes(const snn_layer_desc *d) {
     return align_up((size_t)d->B * d->n_out * sizeof(float));
 }
 size_t bwd_gemm_ws(const snn_layer_desc *d) {
+    if (d->synapse == SNN_SYN_CONV5_POOL2)
+        return conv_workspace_bytes(conv_geom(d), d->in_dtype, d->w_dtype, d->grad_dtype);
     if (d->synapse != SNN_SYN_DENSE) return 0;
     const int M = (int)rows(d);
     const size_t dw = gemm_workspace_bytes(d->n_out, d->n_in, M, d->grad_dtype, d->in_dtype,
@@ -143,9 +162,12 @@ snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w
     if (!aligned16(x) || !aligned16(w) || !aligned16(cur) || (bias && !aligned16(bias)))
         return SNN_ERR_ALIGN;
     if (fwd_ws(d) > ws_bytes || (fwd_ws(d) > 0 && !ws)) return SNN_ERR_WORKSPACE;
-    (void)pool_arg;
+    if (d->synapse == SNN_SYN_CONV5_POOL2 && !pool_arg) return SNN_ERR_NULL;
     if (rows(d) == 0) return SNN_OK;
     (void)hipGetLastError();
+    if (d->synapse == SNN_SYN_CONV5_POOL2)
+        return hip_status(launch_conv_pool_fwd(conv_geom(d), x, d->in_dtype, w, d->w_dtype, bias,
+                                               cur, pool_arg, ws, ws_bytes, stream));
     GemmArgs g{};
     g.M = (int)rows(d);
     g.N = d->n_out;
@@ -227,7 +249,7 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
         return SNN_ERR_ALIGN;
     const size_t need = bwd_gemm_ws(d);
     if (need > ws_bytes || (need > 0 && !ws)) return SNN_ERR_WORKSPACE;
-    (void)pool_arg;
+    if (d->synapse == SNN_SYN_CONV5_POOL2 && !pool_arg) return SNN_ERR_NULL;
     if (rows(d) == 0) {
         // empty batch: the weight gradient is an empty sum
         if (grad_w)
@@ -235,6 +257,10 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
         return SNN_OK;
     }
     (void)hipGetLastError();
+    if (d->synapse == SNN_SYN_CONV5_POOL2)
+        return hip_status(launch_conv_pool_bwd(conv_geom(d), dcur, d->grad_dtype, pool_arg, x,
+                                               d->in_dtype, w, d->w_dtype, grad_w, grad_x, ws,
+                                               ws_bytes, stream));
     const int M = (int)rows(d);
     if (grad_w) {
         // dW[o,i] = sum_m dI[m,o] x[m,i]: both operands stored with the output
@@ -275,8 +301,7 @@ snn_status snn_layer_fwd(const snn_layer_desc *d, const void *x, const void *w,
     if (d->synapse == SNN_SYN_NONE)
         return snn_neuron_fwd(d, reinterpret_cast<const float *>(x), spk_out, u, counts, stream);
     uint8_t *arg = nullptr;
-    if (d->synapse == SNN_SYN_CONV5_POOL2)
-        arg = reinterpret_cast<uint8_t *>(saved) + align_up((size_t)rows(d) * d->n_out * sizeof(float));
+    if (d->synapse == SNN_SYN_CONV5_POOL2) arg = reinterpret_cast<uint8_t *>(saved) + arg_offset(d);
     st = snn_synapse_fwd(d, x, w, bias, u, arg, ws, ws_bytes, stream);
     if (st != SNN_OK) return st;
     return snn_neuron_fwd(d, u, spk_out, u, counts, stream);
@@ -307,9 +332,7 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     if (st != SNN_OK) return st;
     if (!grad_w && !grad_x) return SNN_OK;
     const uint8_t *arg = nullptr;
-    if (d->synapse == SNN_SYN_CONV5_POOL2)
-        arg = reinterpret_cast<const uint8_t *>(saved) +
-              align_up((size_t)rows(d) * d->n_out * sizeof(float));
+    if (d->synapse == SNN_SYN_CONV5_POOL2) arg = reinterpret_cast<const uint8_t *>(saved) + arg_offset(d);
     return snn_synapse_bwd(d, dcur, arg, x, w, grad_w, grad_x, gws, bwd_gemm_ws(d), stream);
 }
 

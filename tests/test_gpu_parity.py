@@ -178,6 +178,91 @@ def test_synapse_bwd(M, N, K, path):
 
 
 # ---------------------------------------------------------------------------
+# convolutional synapse: 5x5 valid conv + 2x2 max-pool of the currents
+# ---------------------------------------------------------------------------
+def _conv_case(NB, Ci, H, W, Co, seed, dens=0.5):
+    rng = np.random.default_rng(seed)
+    x = (rng.random((NB, Ci, H, W)) < dens).astype(np.uint8)
+    w = rng.uniform(-0.3, 0.3, (Co, Ci, 5, 5)).astype(np.float32)
+    b = rng.uniform(-0.2, 0.2, Co).astype(np.float32)
+    spec = dict(kind="conv", c_in=Ci, h=H, w=W, c_out=Co, neuron="leaky", beta=0.5)
+    d = snn.layer_desc(spec, 1, NB)
+    return x, w, b, d
+
+
+def _conv_fwd_gpu(d, x, w, b):
+    cur = torch.empty((d.B, d.n_out), dtype=torch.float32, device=DEV)
+    arg = torch.empty(d.B * d.n_out, dtype=torch.uint8, device=DEV)
+    snn.snn_synapse_fwd(d, _t(x), _t(w), _t(b), cur, arg, _ws(snn.snn_layer_workspace_bytes(d)))
+    return _np(cur), _np(arg)
+
+
+@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (5, 12, 12, 12, 64), (2, 3, 9, 11, 5),
+                                          (1, 2, 6, 6, 2)])
+def test_conv_pool_fwd(NB, Ci, H, W, Co):
+    x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=NB * 100 + Co)
+    cur, arg = _conv_fwd_gpu(d, x, w, b)
+    y = oracle.conv_fwd(x, w, b)                          # double
+    y32 = y.astype(np.float32).astype(np.float64)          # the pool decides on fp32 currents
+    p, a = oracle.maxpool2_fwd(y32)
+    cur = cur.reshape(p.shape)
+    arg = arg.reshape(a.shape)
+    assert_close(cur, p, 1e-3, what="pooled currents")
+    # fp32 accumulation of Ci*25 terms, any order
+    terms = oracle.conv_fwd(x, np.abs(w), np.abs(b))
+    bound = (Ci * 25 + 2) * 2.0 ** -24 * oracle.maxpool2_fwd(terms)[0]
+    assert (np.abs(cur - p) <= bound + 1e-30).all()
+    # the selection must agree wherever the window's top two differ by more
+    # than the fp32 error; elsewhere the chosen element must be a maximum
+    Hp, Wp = a.shape[2], a.shape[3]
+    win = y32[:, :, :2 * Hp, :2 * Wp].reshape(NB, Co, Hp, 2, Wp, 2)
+    win = win.transpose(0, 1, 2, 4, 3, 5).reshape(a.shape + (4,))
+    srt = np.sort(win, axis=-1)
+    clear = (srt[..., -1] - srt[..., -2]) > 2 * bound.reshape(a.shape) + 1e-6
+    assert (arg[clear] == a[clear]).all()
+    chosen = np.take_along_axis(win, arg[..., None].astype(np.int64), -1)[..., 0]
+    assert (np.abs(chosen - srt[..., -1]) <= 2 * bound.reshape(a.shape) + 1e-6).all()
+
+
+def test_conv_pool_ties_first_maximum():
+    """All-zero receptive fields give conv output = bias exactly in every
+    window position: the first element must be chosen."""
+    x = np.zeros((2, 1, 8, 8), np.uint8)
+    x[1, 0, 3, 3] = 1
+    w = np.full((3, 1, 5, 5), 0.25, np.float32)
+    b = np.array([0.5, -0.5, 0.0], np.float32)
+    spec = dict(kind="conv", c_in=1, h=8, w=8, c_out=3, neuron="leaky", beta=0.5)
+    d = snn.layer_desc(spec, 1, 2)
+    cur, arg = _conv_fwd_gpu(d, x, w, b)
+    p, a = oracle.maxpool2_fwd(oracle.conv_fwd(x, w, b).astype(np.float32).astype(np.float64))
+    np.testing.assert_array_equal(cur.reshape(p.shape), p)
+    np.testing.assert_array_equal(arg.reshape(a.shape), a)
+    assert (a[0] == 0).all()
+
+
+@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (4, 12, 12, 12, 64), (2, 3, 9, 11, 5)])
+def test_conv_pool_bwd(NB, Ci, H, W, Co):
+    """Backward teacher-forced on the GPU's own pool selection."""
+    x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=7 * NB + Co)
+    cur, arg = _conv_fwd_gpu(d, x, w, b)
+    rng = np.random.default_rng(1)
+    dI = rng.normal(0, 1, cur.shape).astype(np.float32)
+    gW = torch.empty(w.shape, dtype=torch.float32, device=DEV)
+    gx = torch.empty(x.shape, dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    arg_t = _t(arg)
+    snn.snn_synapse_bwd(d, _t(dI), arg_t, _t(x), _t(w), gW, gx, ws)
+    Ho, Wo = H - 4, W - 4
+    dY = oracle.maxpool2_bwd(dI.reshape(NB, Co, Ho // 2, Wo // 2), arg.reshape(NB, Co, Ho // 2, Wo // 2),
+                             Ho, Wo)
+    if Ho % 2 or Wo % 2:
+        pass  # the dropped row/column of the conv output gets no gradient (zeros from the pool)
+    rW, _, rx = oracle.conv_bwd(dY, x, w)
+    assert_close(_np(gW), rW, 1e-3, what="conv dW")
+    assert_close(_np(gx), rx, 1e-3, what="conv dx")
+
+
+# ---------------------------------------------------------------------------
 # losses
 # ---------------------------------------------------------------------------
 @pytest.mark.parametrize("B,K", [(1, 10), (32, 10), (513, 10), (7, 3)])
@@ -216,11 +301,20 @@ def _saved_u(net, li):
     return _np(net.saved[li][: n * 4].view(torch.float32)).reshape(d.T, d.B, d.n_out)
 
 
+def spec_n_out(spec):
+    if spec["kind"] == "conv":
+        return spec["c_out"] * ((spec["h"] - 4) // 2) * ((spec["w"] - 4) // 2)
+    return spec["n_out"] if spec["kind"] == "dense" else spec["n"]
+
+
 def _gpu_currents(net, li, xin):
-    """Currents of layer li recomputed by the stage call on the GPU's input."""
+    """Currents of layer li recomputed by the stage call on the GPU's input
+    (conv layers: into a scratch selection buffer, the saved one untouched)."""
     d = net.descs[li]
     cur = torch.empty((d.T, d.B, d.n_out), dtype=torch.float32, device=DEV)
-    snn.snn_synapse_fwd(d, xin, net.W[li], net.b[li], cur, None, net.ws)
+    arg = torch.empty(d.T * d.B * d.n_out, dtype=torch.uint8, device=DEV) \
+        if d.synapse == snn.SYN_CONV5_POOL2 else None
+    snn.snn_synapse_fwd(d, xin, net.W[li], net.b[li], cur, arg, net.ws)
     return _np(cur)
 
 
@@ -242,6 +336,12 @@ def _check_step_teacher_forced(wl, inp, net, x_dev, tol=1e-3):
             I_orc = oracle.dense_fwd(xin, W, b).reshape(T, B, -1)
             I = _gpu_currents(net, li, x_dev if li == 0 else net.spk[li - 1])
             assert_close(I, I_orc, tol, what=f"L{li} currents")
+        elif spec["kind"] == "conv":
+            xin = np.asarray(h, np.float64).reshape(T * B, spec["c_in"], spec["h"], spec["w"])
+            y32 = oracle.conv_fwd(xin, W, b).astype(np.float32).astype(np.float64)
+            I_orc = oracle.maxpool2_fwd(y32)[0].reshape(T, B, -1)
+            I = _gpu_currents(net, li, x_dev if li == 0 else net.spk[li - 1])
+            assert_close(I, I_orc, tol, what=f"L{li} conv currents")
         else:
             I = np.asarray(h, np.float32)
         z, u, c = oracle.scan_fwd(I, spec["neuron"], spec["beta"], spec["thr"],
@@ -265,6 +365,20 @@ def _check_step_teacher_forced(wl, inp, net, x_dev, tol=1e-3):
         if spec["kind"] == "none":
             assert_close(_np(net.gx[li]), dI, tol, what="dL/dI")
             break
+        if spec["kind"] == "conv":
+            Ho, Wo = spec["h"] - 4, spec["w"] - 4
+            pa = net.pool_arg(li)[: T * B * spec_n_out(spec)]
+            arg = _np(pa).reshape(T * B, spec["c_out"], Ho // 2, Wo // 2)
+            dY = oracle.maxpool2_bwd(dI.reshape(arg.shape), arg, Ho, Wo)
+            xin = np.asarray(xs[li], np.float64).reshape(T * B, spec["c_in"], spec["h"], spec["w"])
+            dW, db, dx = oracle.conv_bwd(dY, xin, W, want_dx=li > 0)
+            assert_close(_np(net.gW[li]), dW, tol, what=f"L{li} conv dW")
+            assert_close(_np(net.gb[li]), db, tol, what=f"L{li} conv db")
+            if li > 0:
+                gx = _np(net.gx[li])
+                assert_close(gx.reshape(dx.shape), dx, tol, what=f"L{li} conv dx")
+                g = gx
+            continue
         xin = np.asarray(xs[li], np.float64).reshape(T * B, -1)
         dW, db, dx = oracle.dense_bwd(dI.reshape(T * B, -1), xin, W, want_dx=li > 0)
         assert_close(_np(net.gW[li]), dW, tol, what=f"L{li} dW")
@@ -275,7 +389,7 @@ def _check_step_teacher_forced(wl, inp, net, x_dev, tol=1e-3):
             g = gx  # teacher-force the layer below on the GPU's gradient
 
 
-@pytest.mark.parametrize("name", ["dsnn_leaky_t25_b32", "dsnn_synaptic_t50_b256"])
+@pytest.mark.parametrize("name", ["dsnn_leaky_t25_b32", "dsnn_synaptic_t50_b256", "csnn_t25_b128"])
 @pytest.mark.parametrize("path", list(PATHS))
 def test_step_full_size_teacher_forced(name, path):
     wl = wls.get(name)
@@ -288,7 +402,8 @@ def test_step_full_size_teacher_forced(name, path):
 
 @pytest.mark.parametrize("name,T,B,width", [("dsnn_synaptic_t50_b256", 20, 16, 200),
                                             ("dsnn_leaky_t25_b32", 25, 8, 300),
-                                            ("scan_wide_t1000_b64", 60, 4, 1000)])
+                                            ("scan_wide_t1000_b64", 60, 4, 1000),
+                                            ("csnn_t25_b128", 6, 4, None)])
 @pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
 @pytest.mark.parametrize("path", list(PATHS))
 def test_step_scaled_teacher_forced(name, T, B, width, reset, path):
