@@ -31,6 +31,7 @@ METRIC = "SNN training samples/sec (fwd+BPTT) at 1 GPU; scan HBM GB/s, GEMM MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
 PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 PEAK_FP16_MFMA_TFLOPS = 2500.0
+PEAK_FP32_VALU_TFLOPS = 78.6   # 256 CUs x 4 SIMDs x 16 lanes x 2 flops x 2.4 GHz
 
 
 def csrc_hash() -> str:
@@ -243,14 +244,20 @@ def main():
     kind, work = stage_work(net, dom_name, dom_li)
     if kind == "flop":
         achieved = work / (k_avg_ms / 1000.0) / 1e12
-        passes = _mfma_passes(net, dom_name, dom_li, args.fp32_mfma)
-        if wl.dtype == "f16" or passes == 3:
-            peak, basis = PEAK_FP16_MFMA_TFLOPS, "bf16/fp16 dense MFMA"
+        ckind, passes = _contraction_kind(net, dom_li, args.fp32_mfma)
+        if ckind == "valu":
+            roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_VALU_TFLOPS,
+                    "unit": "TFLOP/s",
+                    "peak_basis": "fp32 vector FMA without packed instructions: 256 CUs x 4 "
+                                  "SIMDs x 16 lanes x 2 flops x 2.4 GHz"}
         else:
-            peak, basis = PEAK_FP32_MFMA_TFLOPS, "fp32 dense MFMA"
-        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
-                "peak_basis": basis, "mfma_passes": passes,
-                "executed_mfma_frac": round(passes * achieved / peak, 4)}
+            if ckind == "mfma16":
+                peak, basis = PEAK_FP16_MFMA_TFLOPS, "bf16/fp16 dense MFMA"
+            else:
+                peak, basis = PEAK_FP32_MFMA_TFLOPS, "fp32 dense MFMA"
+            roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
+                    "unit": "TFLOP/s", "peak_basis": basis, "mfma_passes": passes,
+                    "executed_mfma_frac": round(passes * achieved / peak, 4)}
     else:
         achieved = work / (k_avg_ms / 1000.0) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
@@ -285,70 +292,47 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def _contraction_kind(net, li, fp32_mfma):
+    """How the library contracts layer li's forward product (mirrors the
+    operand classification in gemm_mfma16.hip): ('mfma16', passes),
+    ('mfma32', 1) or ('valu', 1) for the direct convolution."""
+    d = net.descs[li]
+    if d.synapse == 1:
+        return "valu", 1
+    wide = d.T * d.B >= 64 and d.n_out >= 64
+    if fp32_mfma or not wide or d.in_dtype != 3:
+        return "mfma32", 1
+    if d.w_dtype == 0:
+        return "mfma16", 3   # fp32 weights: three exact bf16 parts
+    return "mfma16", 1       # fp16 weights: one fp16 pass
+
+
 def _stage_kernels(net, name, li, fp32_mfma):
-    """Kernels a single-launch-unit stage enqueues (for matching the profile)."""
+    """Kernels a stage enqueues (matched against the rocprofv3 summary)."""
     if name == "neuron_fwd":
         return ": neuron_fwd_kernel"
     if name == "neuron_bwd":
         return ": neuron_bwd_kernel"
-    if _mfma_passes(net, name, li, fp32_mfma) == 3:
-        return ": split_planes_kernel (W into bf16 planes) + gemm_bf16_kernel"
-    return ": gemm_f32_kernel"
-
-
-def _mfma_passes(net, name, li, fp32_mfma):
-    """MFMA passes per algorithmic product: 3 when a spike x fp32 contraction
-    runs on bf16 matrix cores over the exact three-part split, else 1."""
-    d = net.descs[li]
-    if fp32_mfma or name != "synapse_fwd":
-        return 1
-    wide = d.T * d.B >= 64 and d.n_out >= 64
-    return 3 if (d.in_dtype == 3 and d.w_dtype == 0 and wide) else 1
+    kind, passes = _contraction_kind(net, li, fp32_mfma)
+    if kind == "valu":
+        return ": conv_pool_fwd_kernel"
+    if kind == "mfma16" and passes == 3:
+        return (": split_planes_kernel (weights into bf16 planes) + gemm16_kernel"
+                " (+ splitk_reduce_kernel when split over K)")
+    if kind == "mfma16":
+        return ": gemm16_kernel (+ splitk_reduce_kernel when split over K)"
+    return ": gemm_f32_kernel (+ splitk_reduce_kernel when split over K)"
 
 
 def _single_kernel_stage(net, key):
-    """Stages that launch exactly one kernel: a forward scan, or a forward
-    contraction that is not split over K."""
+    """Roofline candidates: stages whose work is one kernel, or one
+    contraction (its weight split and split-K reduce are counted in)."""
     name, li = key.split("[L")[0], int(key.split("[L")[1].rstrip("]")) if "[L" in key else -1
-    if name == "neuron_fwd":
+    if name in ("neuron_fwd", "synapse_fwd"):
         return True
     if name == "neuron_bwd":  # one kernel unless a bias gradient is reduced too
         return net.descs[li].synapse == 2
-    if name == "synapse_fwd":
-        d = net.descs[li]
-        split = ((d.flags & 1) == 0 and d.in_dtype == 3 and d.w_dtype == 0 and
-                 d.T * d.B >= 64 and d.n_out >= 64)
-        return _gemm_splits(d.T * d.B, d.n_out, d.n_in, split) == 1
     return False
-
-
-def _gemm_splits(M, N, K, bf16_split=True):
-    """Mirror of the library's split-K choice (make_plan in gemm.hip and
-    bf16_plan in gemm_bf16.hip)."""
-    if bf16_split:
-        tiles = ((M + 127) // 128) * ((N + 127) // 128)
-        ksteps = (K + 31) // 32
-        S = 1
-        if tiles < 256:
-            S = min((512 + tiles - 1) // tiles, max(1, ksteps // 4), 64)
-        k_chunk = ((ksteps + S - 1) // S) * 32
-        return (K + k_chunk - 1) // k_chunk
-    BK = 16
-    if N <= 16:
-        BM, BN = 64, 16
-    elif M <= 16:
-        BM, BN = 16, 64
-    else:
-        big = ((M + 127) // 128) * ((N + 127) // 128)
-        BM, BN = (128, 128) if big >= 192 else (64, 64)
-    tiles = ((M + BM - 1) // BM) * ((N + BN - 1) // BN)
-    ksteps = (K + BK - 1) // BK
-    S = 1
-    if tiles < 256:
-        S = (512 + tiles - 1) // tiles
-        S = min(S, max(1, ksteps // 8), 64)
-    k_chunk = ((ksteps + S - 1) // S) * BK
-    return (K + k_chunk - 1) // k_chunk
 
 
 def _layer_str(s):

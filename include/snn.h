@@ -35,11 +35,13 @@
  *     the host before anything is launched; on error nothing is launched and
  *     outputs are untouched.  A failed launch returns SNN_ERR_HIP.
  *   - Outputs are overwritten, never accumulated into.
- *   - Arithmetic: contractions accumulate in fp32 with exact products
- *     (fp32 operands, fp16 weights, and spikes, which are exact in bf16: a
- *     spike x fp32 contraction runs as three bf16 MFMA passes over the exact
- *     split of the fp32 operand unless SNN_FLAG_FP32_MFMA is set); neuron
- *     state is fp32; loss reductions in fp64.
+ *   - Arithmetic: contractions accumulate in fp32 with exact products.
+ *     Spikes are exact in bf16 and fp16, an fp32 value is exactly three bf16
+ *     parts and an fp16 value two, so contractions with a spike, fp16 or
+ *     bf16 operand run on the 16-bit matrix cores as one pass per pair of
+ *     parts (spike x fp32: three bf16 passes; spike x fp16: one fp16 pass),
+ *     unless SNN_FLAG_FP32_MFMA is set; fp32 x fp32 runs on fp32 MFMA.
+ *     Neuron state is fp32; loss reductions in fp64.
  *   - T == 0 or B == 0 is valid: no compute is launched, and outputs that
  *     are sums over an empty range (counts, grad_w, grad_b) are set to 0.
  *     A loss over B == 0 or K == 0 is rejected (SNN_ERR_SHAPE).
@@ -95,10 +97,12 @@ typedef enum snn_status {
                             counts summed over T) */
 
 /* descriptor flags */
-#define SNN_FLAG_FP32_MFMA 1 /* contract spike x fp32 operands with fp32 MFMA
-                                instead of three exact bf16 MFMA passes (the
-                                fp32 operand split into hi + mid + lo bf16
-                                parts, every product exact, fp32 accumulate) */
+#define SNN_FLAG_FP32_MFMA 1 /* run every contraction on fp32 MFMA instead of
+                                exact multi-part passes on the 16-bit matrix
+                                cores (an fp32 operand split into hi + mid +
+                                lo bf16 parts, fp16 into two bf16 parts or
+                                kept as fp16; every product exact, fp32
+                                accumulate) */
 
 /* losses on spike counts */
 #define SNN_LOSS_CE_COUNT 0  /* labels int32 [B] in [0,K) */

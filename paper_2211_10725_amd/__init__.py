@@ -245,9 +245,11 @@ class Network:
         self.W, self.b = [], []
         for li, spec in enumerate(wl.layers):
             in_dt = F32 if spec["kind"] == "none" else U8
+            # half-precision nets hand dL/dI to the contractions in bf16, which
+            # keeps fp32's exponent range for the small BPTT gradients
             d = layer_desc(spec, T, B, in_dtype=in_dt, w_dtype=F16 if half else F32,
-                           out_dtype=U8, grad_dtype=F32, slope=wl.slope, reset_grad=reset_grad,
-                           flags=flags)
+                           out_dtype=U8, grad_dtype=BF16 if half else F32, slope=wl.slope,
+                           reset_grad=reset_grad, flags=flags)
             self.descs.append(d)
             W, b = params[li]
             if W is None:
@@ -319,6 +321,7 @@ class Network:
 
     # the same work through the stage calls, with a hook between stages
     def step_stages(self, x, labels=None, targets=None, stream=None, hook=None):
+        torch = self.torch
         hook = hook or (lambda name, li: None)
         n = len(self.descs)
         h = x
@@ -348,8 +351,14 @@ class Network:
                 snn_neuron_bwd(d, kind, g, self.saved[li], self.gx[li], None, None, stream)
                 hook("neuron_bwd_end", li)
                 continue
-            dcur_bytes = d.T * d.B * d.n_out * 4
+            dcur_bytes = d.T * d.B * d.n_out * (2 if d.grad_dtype in (F16, BF16) else 4)
             dcur = self.ws[:dcur_bytes]
+            if d.grad_dtype == BF16:
+                dcur = dcur.view(torch.bfloat16)
+            elif d.grad_dtype == F16:
+                dcur = dcur.view(torch.float16)
+            else:
+                dcur = dcur.view(torch.float32)
             rest = self.ws[(dcur_bytes + 255) // 256 * 256:]
             hook("neuron_bwd", li)
             snn_neuron_bwd(d, kind, g, self.saved[li], dcur, self.gb[li], rest, stream)

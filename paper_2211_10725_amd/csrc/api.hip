@@ -95,15 +95,81 @@ size_t dcur_bytes(const snn_layer_desc *d) {
 size_t colsum_bytes(const snn_layer_desc *d) {
     return align_up((size_t)d->B * d->n_out * sizeof(float));
 }
+// Weight and input gradients of a dense layer.  Large contractions whose
+// operands are stored M/N-contiguous (dI and x for dW, W for dx) are
+// transposed once into the workspace so that they run K-contiguous on the
+// 16-bit matrix cores; an fp32 dI is transposed straight into its three exact
+// bf16 planes.
+constexpr double kTransposeFlops = 1073741824.0;  // 2 M N K above which it pays
+
+struct DwPlan {
+    bool transposed;
+    int a_dtype;       // dtype of the transposed dI operand
+    size_t dit_bytes;  // dI^T (planes for fp32)
+    size_t xt_bytes;   // x^T
+    size_t gemm_bytes;
+};
+
+GemmArgs dw_probe_kc(const snn_layer_desc *d) {
+    GemmArgs g{};
+    g.M = d->n_out; g.N = d->n_in; g.K = (int)rows(d);
+    g.a_dtype = d->grad_dtype == SNN_F32 ? kPlanes3 : d->grad_dtype; g.a_kc = true;
+    g.b_dtype = d->in_dtype; g.b_kc = true;
+    return g;
+}
+
+DwPlan dw_plan(const snn_layer_desc *d) {
+    DwPlan p{};
+    const int M = (int)rows(d);
+    const GemmArgs kc = dw_probe_kc(d);
+    p.transposed = split_ok(d) && gemm16_applies(kc) &&
+                   2.0 * M * d->n_in * d->n_out >= kTransposeFlops;
+    if (p.transposed) {
+        p.a_dtype = kc.a_dtype;
+        p.dit_bytes = align_up((size_t)M * d->n_out * dtype_bytes(kc.a_dtype));
+        p.xt_bytes = align_up((size_t)M * d->n_in * dtype_bytes(d->in_dtype));
+        p.gemm_bytes = gemm_workspace_bytes(kc.M, kc.N, kc.K, kc.a_dtype, kc.b_dtype, true, true, true);
+    } else {
+        p.gemm_bytes = gemm_workspace_bytes(d->n_out, d->n_in, M, d->grad_dtype, d->in_dtype,
+                                            false, false, split_ok(d));
+    }
+    return p;
+}
+
+struct DxPlan {
+    bool transposed;
+    size_t wt_bytes;  // W^T
+    size_t gemm_bytes;
+};
+
+DxPlan dx_plan(const snn_layer_desc *d) {
+    DxPlan p{};
+    const int M = (int)rows(d);
+    GemmArgs kc{};
+    kc.M = M; kc.N = d->n_in; kc.K = d->n_out;
+    kc.a_dtype = d->grad_dtype; kc.a_kc = true;
+    kc.b_dtype = d->w_dtype; kc.b_kc = true;
+    p.transposed = split_ok(d) && gemm16_applies(kc) &&
+                   2.0 * M * d->n_in * d->n_out >= kTransposeFlops;
+    if (p.transposed) {
+        p.wt_bytes = align_up((size_t)d->n_in * d->n_out * dtype_bytes(d->w_dtype));
+        p.gemm_bytes = gemm_workspace_bytes(M, d->n_in, d->n_out, d->grad_dtype, d->w_dtype, true,
+                                            true, true);
+    } else {
+        p.gemm_bytes = gemm_workspace_bytes(M, d->n_in, d->n_out, d->grad_dtype, d->w_dtype, true,
+                                            false, split_ok(d));
+    }
+    return p;
+}
+
 size_t bwd_gemm_ws(const snn_layer_desc *d) {
     if (d->synapse == SNN_SYN_CONV5_POOL2)
         return conv_workspace_bytes(conv_geom(d), d->in_dtype, d->w_dtype, d->grad_dtype);
     if (d->synapse != SNN_SYN_DENSE) return 0;
-    const int M = (int)rows(d);
-    const size_t dw = gemm_workspace_bytes(d->n_out, d->n_in, M, d->grad_dtype, d->in_dtype,
-                                           false, false, split_ok(d));
-    const size_t dx = gemm_workspace_bytes(M, d->n_in, d->n_out, d->grad_dtype, d->w_dtype,
-                                           true, false, split_ok(d));
+    const DwPlan w = dw_plan(d);
+    const DxPlan x = dx_plan(d);
+    const size_t dw = w.dit_bytes + w.xt_bytes + w.gemm_bytes;
+    const size_t dx = x.wt_bytes + x.gemm_bytes;
     return dw > dx ? dw : dx;
 }
 size_t bwd_ws(const snn_layer_desc *d) { return dcur_bytes(d) + colsum_bytes(d) + bwd_gemm_ws(d); }
@@ -262,25 +328,53 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
                                                d->in_dtype, w, d->w_dtype, grad_w, grad_x, ws,
                                                ws_bytes, stream));
     const int M = (int)rows(d);
+    char *wsb = reinterpret_cast<char *>(ws);
     if (grad_w) {
-        // dW[o,i] = sum_m dI[m,o] x[m,i]: both operands stored with the output
-        // index contiguous, K = T*B.
+        // dW[o,i] = sum_m dI[m,o] x[m,i], K = T*B
+        const DwPlan pl = dw_plan(d);
         GemmArgs g{};
         g.M = d->n_out; g.N = d->n_in; g.K = M;
-        g.A = dcur; g.lda = d->n_out; g.a_dtype = d->grad_dtype; g.a_kc = false;
-        g.B = x; g.ldb = d->n_in; g.b_dtype = d->in_dtype; g.b_kc = false;
         g.C = grad_w; g.ldc = d->n_in; g.bias = nullptr; g.allow_split = split_ok(d);
-        hipError_t e = launch_gemm(g, ws, ws_bytes, stream);
+        hipError_t e;
+        if (pl.transposed) {
+            char *dit = wsb, *xt = wsb + pl.dit_bytes;
+            const bool planes = pl.a_dtype == kPlanes3;
+            e = launch_transpose(M, d->n_out, dcur, d->n_out, (int)dtype_bytes(d->grad_dtype), dit, M,
+                                 planes, (int64_t)M * d->n_out, stream);
+            if (e != hipSuccess) return SNN_ERR_HIP;
+            e = launch_transpose(M, d->n_in, x, d->n_in, (int)dtype_bytes(d->in_dtype), xt, M, false,
+                                 0, stream);
+            if (e != hipSuccess) return SNN_ERR_HIP;
+            g.A = dit; g.lda = M; g.a_dtype = pl.a_dtype; g.a_kc = true;
+            g.a_ps = (int64_t)M * d->n_out;
+            g.B = xt; g.ldb = M; g.b_dtype = d->in_dtype; g.b_kc = true;
+            e = launch_gemm(g, xt + pl.xt_bytes, ws_bytes - pl.dit_bytes - pl.xt_bytes, stream);
+        } else {
+            // both operands stored with the output index contiguous
+            g.A = dcur; g.lda = d->n_out; g.a_dtype = d->grad_dtype; g.a_kc = false;
+            g.B = x; g.ldb = d->n_in; g.b_dtype = d->in_dtype; g.b_kc = false;
+            e = launch_gemm(g, ws, ws_bytes, stream);
+        }
         if (e != hipSuccess) return SNN_ERR_HIP;
     }
     if (grad_x) {
         // dx[m,i] = sum_o dI[m,o] W[o,i]
+        const DxPlan pl = dx_plan(d);
         GemmArgs g{};
         g.M = M; g.N = d->n_in; g.K = d->n_out;
         g.A = dcur; g.lda = d->n_out; g.a_dtype = d->grad_dtype; g.a_kc = true;
-        g.B = w; g.ldb = d->n_in; g.b_dtype = d->w_dtype; g.b_kc = false;
         g.C = grad_x; g.ldc = d->n_in; g.bias = nullptr; g.allow_split = split_ok(d);
-        hipError_t e = launch_gemm(g, ws, ws_bytes, stream);
+        hipError_t e;
+        if (pl.transposed) {
+            e = launch_transpose(d->n_out, d->n_in, w, d->n_in, (int)dtype_bytes(d->w_dtype), wsb,
+                                 d->n_out, false, 0, stream);
+            if (e != hipSuccess) return SNN_ERR_HIP;
+            g.B = wsb; g.ldb = d->n_out; g.b_dtype = d->w_dtype; g.b_kc = true;
+            e = launch_gemm(g, wsb + pl.wt_bytes, ws_bytes - pl.wt_bytes, stream);
+        } else {
+            g.B = w; g.ldb = d->n_in; g.b_dtype = d->w_dtype; g.b_kc = false;
+            e = launch_gemm(g, ws, ws_bytes, stream);
+        }
         if (e != hipSuccess) return SNN_ERR_HIP;
     }
     return SNN_OK;

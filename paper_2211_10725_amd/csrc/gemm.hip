@@ -306,12 +306,12 @@ size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype, bool 
     GemmArgs probe{};
     probe.M = M;
     probe.N = N;
+    probe.K = K;
     probe.a_dtype = a_dtype;
     probe.b_dtype = b_dtype;
-    if (allow_split && gemm_bf16_applies(probe)) {
-        const bool a_f32 = a_dtype == SNN_F32;
-        return gemm_bf16_workspace_bytes(M, N, K, a_f32, a_f32 ? a_kc : b_kc);
-    }
+    probe.a_kc = a_kc;
+    probe.b_kc = b_kc;
+    if (allow_split && gemm16_applies(probe)) return gemm16_workspace_bytes(probe);
     const Plan p = make_plan(M, N, K);
     if (p.splits <= 1) return 0;
     return align_up((size_t)p.splits * M * N * sizeof(float));
@@ -323,7 +323,7 @@ hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t
         // empty contraction: C = bias (or 0)
         return hipErrorInvalidValue;
     }
-    if (g.allow_split && gemm_bf16_applies(g)) return launch_gemm_bf16(g, ws, ws_bytes, s);
+    if (g.allow_split && gemm16_applies(g)) return launch_gemm16(g, ws, ws_bytes, s);
     const Plan p = make_plan(g.M, g.N, g.K);
     float *out = g.C;
     int64_t ldo = g.ldc, ss = 0;

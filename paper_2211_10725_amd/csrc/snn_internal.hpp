@@ -26,8 +26,13 @@ __device__ inline int xcd_local_item() {
     return xcd < rem ? xcd * (per + 1) + idx : rem * (per + 1) + (xcd - rem) * per + idx;
 }
 
+// Internal operand type: an fp32 array held exactly as three bf16 planes
+// (hi, mid, lo), the plane stride given by GemmArgs::a_ps / b_ps.
+constexpr int kPlanes3 = 64;
+
 inline size_t dtype_bytes(int dt) {
     switch (dt) {
+        case kPlanes3: return 6;
         case SNN_F32: return 4;
         case SNN_F16: return 2;
         case SNN_BF16: return 2;
@@ -72,7 +77,8 @@ struct GemmArgs {
     float *C;
     int64_t ldc;
     const float *bias;  // [N] or NULL
-    bool allow_split;   // spike x fp32 may run as three exact bf16 passes
+    bool allow_split;   // may run on 16-bit MFMA as exact multi-part passes
+    int64_t a_ps = 0, b_ps = 0;  // plane strides (elements) of kPlanes3 operands
 };
 size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype, bool a_kc,
                             bool b_kc, bool allow_split);
@@ -81,10 +87,16 @@ hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t
 hipError_t launch_splitk_reduce(int M, int N, int S, const float *P, float *C, int64_t ldc,
                                 const float *bias, hipStream_t s);
 
-// ---- spike x fp32 on bf16 matrix cores (gemm_bf16.hip) -----------------------
-bool gemm_bf16_applies(const GemmArgs &g);
-size_t gemm_bf16_workspace_bytes(int M, int N, int K, bool a_f32, bool f32_kc);
-hipError_t launch_gemm_bf16(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
+// ---- 16-bit matrix cores, exact products (gemm_mfma16.hip) ---------------------
+bool gemm16_applies(const GemmArgs &g);
+size_t gemm16_workspace_bytes(const GemmArgs &g);
+hipError_t launch_gemm16(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
+int gemm16_passes(const GemmArgs &g);  // MFMA passes per product, 0 if not applicable
+// dst[c*ld_dst + r] = src[r*ld_src + c] for r < rows, c < cols; to_planes
+// writes an fp32 source as three bf16 planes `plane` elements apart.
+hipError_t launch_transpose(int rows, int cols, const void *src, int64_t ld_src, int elem_bytes,
+                            void *dst, int64_t ld_dst, bool to_planes, int64_t plane,
+                            hipStream_t s);
 
 // ---- losses (loss.hip) -----------------------------------------------------
 size_t loss_workspace_bytes(int kind, int B, int K);

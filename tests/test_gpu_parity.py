@@ -177,6 +177,41 @@ def test_synapse_bwd(M, N, K, path):
     _assert_fp32_sum(gotx - rx, aI @ np.abs(W).astype(np.float64), N, "dx")
 
 
+GRAD_TYPES = {"f32": (snn.F32, torch.float32), "bf16": (snn.BF16, torch.bfloat16),
+              "f16": (snn.F16, torch.float16)}
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 130, 77), (12800, 1000, 784), (2048, 512, 1024)])
+@pytest.mark.parametrize("gdt", list(GRAD_TYPES))
+@pytest.mark.parametrize("wdt", ["f32", "f16"])
+def test_synapse_bwd_operand_types(M, N, K, gdt, wdt):
+    """dW and dx with 16-bit gradient operands and/or fp16 weights: products
+    of the given (rounded) values are exact, so the result is their fp32 sum."""
+    rng = np.random.default_rng(M + 7 * N)
+    x = (rng.random((M, K)) < 0.5).astype(np.uint8)
+    W = rng.uniform(-1, 1, (N, K)).astype(np.float32)
+    if wdt == "f16":
+        W = W.astype(np.float16).astype(np.float32)
+    dI = rng.normal(0, 1e-3, (M, N)).astype(np.float32)
+    gcode, tdt = GRAD_TYPES[gdt]
+    dI_t = _t(dI, tdt)
+    dI_used = _np(dI_t.float()).astype(np.float64)      # the values the GPU sees
+    spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
+    d = snn.layer_desc(spec, 1, M, grad_dtype=gcode, w_dtype=snn.F16 if wdt == "f16" else snn.F32)
+    gW = torch.empty((N, K), dtype=torch.float32, device=DEV)
+    gx = torch.empty((M, K), dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    Wt = _t(W, torch.float16 if wdt == "f16" else torch.float32)
+    snn.snn_synapse_bwd(d, dI_t, None, _t(x), Wt, gW, gx, ws)
+    rW, _, rx = oracle.dense_bwd(dI_used, x, W)
+    gotW, gotx = _np(gW), _np(gx)
+    assert_close(gotW, rW, 1e-3, what="dW")
+    assert_close(gotx, rx, 1e-3, what="dx")
+    aI = np.abs(dI_used)
+    _assert_fp32_sum(gotW - rW, aI.T @ x.astype(np.float64), M, "dW")
+    _assert_fp32_sum(gotx - rx, aI @ np.abs(W).astype(np.float64), N, "dx")
+
+
 # ---------------------------------------------------------------------------
 # convolutional synapse: 5x5 valid conv + 2x2 max-pool of the currents
 # ---------------------------------------------------------------------------
@@ -381,11 +416,17 @@ def _check_step_teacher_forced(wl, inp, net, x_dev, tol=1e-3):
             continue
         xin = np.asarray(xs[li], np.float64).reshape(T * B, -1)
         dW, db, dx = oracle.dense_bwd(dI.reshape(T * B, -1), xin, W, want_dx=li > 0)
-        assert_close(_np(net.gW[li]), dW, tol, what=f"L{li} dW")
+        bW = bx = None
+        if net.descs[li].grad_dtype == snn.BF16:
+            # dL/dI handed to the contractions in bf16: a-priori rounding bound
+            aI = np.abs(dI.reshape(T * B, -1))
+            bW = 2.0 ** -8 * (aI.T @ np.abs(xin))
+            bx = 2.0 ** -8 * (aI @ np.abs(W).astype(np.float64)) if li > 0 else None
+        assert_close(_np(net.gW[li]), dW, tol, what=f"L{li} dW", abs_bound=bW)
         assert_close(_np(net.gb[li]), db, tol, what=f"L{li} db")
         if li > 0:
             gx = _np(net.gx[li])
-            assert_close(gx.reshape(T * B, -1), dx, tol, what=f"L{li} dx")
+            assert_close(gx.reshape(T * B, -1), dx, tol, what=f"L{li} dx", abs_bound=bx)
             g = gx  # teacher-force the layer below on the GPU's gradient
 
 
@@ -403,7 +444,8 @@ def test_step_full_size_teacher_forced(name, path):
 @pytest.mark.parametrize("name,T,B,width", [("dsnn_synaptic_t50_b256", 20, 16, 200),
                                             ("dsnn_leaky_t25_b32", 25, 8, 300),
                                             ("scan_wide_t1000_b64", 60, 4, 1000),
-                                            ("csnn_t25_b128", 6, 4, None)])
+                                            ("csnn_t25_b128", 6, 4, None),
+                                            ("dsnn_half_t100_b512", 12, 8, 320)])
 @pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
 @pytest.mark.parametrize("path", list(PATHS))
 def test_step_scaled_teacher_forced(name, T, B, width, reset, path):
@@ -415,7 +457,7 @@ def test_step_scaled_teacher_forced(name, T, B, width, reset, path):
     x = _t(inp["x"])
     net.step(x, labels=lab, targets=tgt)
     if reset == snn.RESET_DETACHED:
-        _check_step_teacher_forced(wl, inp, net, x)
+        _check_step_teacher_forced(wl, inp, net, x, tol=2e-2 if wl.dtype == "f16" else 1e-3)
     # the stage calls give the same bytes as the layer calls
     snap = [_np(t).copy() for t in net.gW if t is not None] + [_np(net.loss).copy()]
     net.step_stages(x, labels=lab, targets=tgt)
