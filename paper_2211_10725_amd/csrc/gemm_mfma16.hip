@@ -38,8 +38,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 
 constexpr int kThreads = 256;
-constexpr int BK = 32;
-constexpr int LDK = BK + 8;  // LDS row stride in 16-bit elements (80 bytes)
+constexpr int BK = 32;  // k-tile of the planning model (the kernels use 32 or 64)
 
 constexpr int MT_BF16 = 0;
 constexpr int MT_F16 = 1;
@@ -142,13 +141,14 @@ __device__ inline uint32_t part_of(const uint32_t (&w)[WORDS], int i, int part) 
 //  KC (row-major [row][k]): two to four threads per row, one vector load each.
 //  MN ([k][row]): consecutive threads take consecutive rows and gather their
 //  k-run one element per k; each such load is contiguous across the wave.
-template <int SRC, int MT, bool KC, int R>
+template <int SRC, int MT, bool KC, int R, int BK>
 struct Operand {
     typedef typename SrcTraits<SRC>::T T;
     static constexpr int P = SrcTraits<SRC>::P;
     static constexpr int PL = SrcTraits<SRC>::PLANES;
+    static constexpr int LDK = BK + 8;             // LDS row stride (16-bit elements)
     static constexpr int EPT = R * BK / kThreads;  // elements per thread
-    static_assert(EPT == 8 || EPT == 16 || EPT == 32, "tile");
+    static_assert(EPT == 8 || EPT == 16 || EPT == 32 || EPT == 64, "tile");
     static constexpr int TPR = BK / EPT;           // threads per row (KC)
     static constexpr int WORDS = EPT * (int)sizeof(T) / 4;
     uint32_t w[PL][WORDS];
@@ -235,6 +235,16 @@ __device__ inline floatx16 mfma32(const uint4 &a, const uint4 &b, const floatx16
                                                        __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// k-tile and LDS stages: single-part operand pairs use 64-deep k-tiles in a
+// two-stage LDS ring (one barrier per k-tile, the next tile staged while this
+// one is multiplied); multi-part pairs carry P times the MFMA work per staged
+// byte and keep a single 32-deep stage (two barriers), which leaves LDS for
+// more resident workgroups.
+template <int SA, int SB>
+constexpr int ktile() { return SrcTraits<SA>::P * SrcTraits<SB>::P == 1 ? 64 : 32; }
+template <int SA, int SB>
+constexpr int lds_stages() { return SrcTraits<SA>::P * SrcTraits<SB>::P == 1 ? 2 : 1; }
+
 template <int MT, int SA, bool A_KC, int SB, bool B_KC, int BM, int BN>
 __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_kernel(
     int M, int N, int K, int k_chunk, int tiles_n, const typename SrcTraits<SA>::T *__restrict__ A,
@@ -243,10 +253,14 @@ __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_ke
     const float *__restrict__ bias) {
     constexpr int PA = SrcTraits<SA>::P, PB = SrcTraits<SB>::P;
     static_assert(PA * PB <= 6, "at most six passes");
+    constexpr int KT = ktile<SA, SB>();
+    constexpr int LDK = KT + 8;
     constexpr int WM = BM / 2, WN = BN / 2;
     constexpr int FM = WM / 32, FN = WN / 32;
-    __shared__ __attribute__((aligned(16))) uint16_t As[PA * BM * LDK];
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[PB * BN * LDK];
+    constexpr int SZA = PA * BM * LDK, SZB = PB * BN * LDK;
+    constexpr int NS = lds_stages<SA, SB>();
+    __shared__ __attribute__((aligned(16))) uint16_t As[NS * SZA];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[NS * SZB];
 
     // Workgroups are dealt round-robin to the 8 XCDs (each with its own L2);
     // renumber them so that each XCD runs a contiguous range of work items,
@@ -269,37 +283,53 @@ __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_ke
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    Operand<SA, MT, A_KC, BM> oa;
-    Operand<SB, MT, B_KC, BN> ob;
+    Operand<SA, MT, A_KC, BM, KT> oa;
+    Operand<SB, MT, B_KC, BN, KT> ob;
+    // prologue: stage the first k-tile (two-stage ring) and fetch the next
     if (kbeg < kend) {
         oa.fetch(A, lda, a_ps, M, m0, kbeg, kend);
         ob.fetch(B, ldb, b_ps, N, n0, kbeg, kend);
-    }
-    const int lrow = lane & 31, lk = 8 * (lane >> 5);
-    for (int k0 = kbeg; k0 < kend; k0 += BK) {
-        __syncthreads();
-        oa.store(As);
-        ob.store(Bs);
-        __syncthreads();
-        if (k0 + BK < kend) {
-            oa.fetch(A, lda, a_ps, M, m0, k0 + BK, kend);
-            ob.fetch(B, ldb, b_ps, N, n0, k0 + BK, kend);
+        if constexpr (NS == 2) {
+            oa.store(As);
+            ob.store(Bs);
+            if (kbeg + KT < kend) {
+                oa.fetch(A, lda, a_ps, M, m0, kbeg + KT, kend);
+                ob.fetch(B, ldb, b_ps, N, n0, kbeg + KT, kend);
+            }
         }
+    }
+    if constexpr (NS == 2) __syncthreads();
+    const int lrow = lane & 31, lk = 8 * (lane >> 5);
+    int stage = 0;
+    for (int k0 = kbeg; k0 < kend; k0 += KT) {
+        if constexpr (NS == 1) {
+            // single stage: stage this tile, then fetch the next while multiplying
+            __syncthreads();
+            oa.store(As);
+            ob.store(Bs);
+            __syncthreads();
+            if (k0 + KT < kend) {
+                oa.fetch(A, lda, a_ps, M, m0, k0 + KT, kend);
+                ob.fetch(B, ldb, b_ps, N, n0, k0 + KT, kend);
+            }
+        }
+        const uint16_t *as = As + stage * SZA;
+        const uint16_t *bs = Bs + stage * SZB;
 #pragma unroll
-        for (int ks = 0; ks < BK; ks += 16) {
+        for (int ks = 0; ks < KT; ks += 16) {
             uint4 a[PA][FM], b[PB][FN];
 #pragma unroll
             for (int p = 0; p < PA; ++p)
 #pragma unroll
                 for (int i = 0; i < FM; ++i)
                     a[p][i] = *reinterpret_cast<const uint4 *>(
-                        As + ((size_t)p * BM + wm * WM + i * 32 + lrow) * LDK + ks + lk);
+                        as + ((size_t)p * BM + wm * WM + i * 32 + lrow) * LDK + ks + lk);
 #pragma unroll
             for (int q = 0; q < PB; ++q)
 #pragma unroll
                 for (int j = 0; j < FN; ++j)
                     b[q][j] = *reinterpret_cast<const uint4 *>(
-                        Bs + ((size_t)q * BN + wn * WN + j * 32 + lrow) * LDK + ks + lk);
+                        bs + ((size_t)q * BN + wn * WN + j * 32 + lrow) * LDK + ks + lk);
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -311,6 +341,20 @@ __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_ke
                         for (int q = PB - 1; q >= 0; --q)
                             acc[i][j] = mfma32<MT>(a[p][i], b[q][j], acc[i][j]);
                 }
+        }
+        if constexpr (NS == 2) {
+            // stage the next k-tile into the other buffer (last read before the
+            // previous barrier), then fetch the one after it
+            if (k0 + KT < kend) {
+                oa.store(As + (stage ^ 1) * SZA);
+                ob.store(Bs + (stage ^ 1) * SZB);
+                if (k0 + 2 * KT < kend) {
+                    oa.fetch(A, lda, a_ps, M, m0, k0 + 2 * KT, kend);
+                    ob.fetch(B, ldb, b_ps, N, n0, k0 + 2 * KT, kend);
+                }
+            }
+            __syncthreads();
+            stage ^= 1;
         }
     }
 
@@ -341,9 +385,10 @@ __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_ke
 constexpr int kShapes = 4;
 constexpr int kShapeBM[kShapes] = {128, 128, 256, 128};
 constexpr int kShapeBN[kShapes] = {128, 64, 128, 256};
-// Relative time per unit of tile work, measured on MI355X for the forward
-// contraction of the 784-1000 layer (128x128 = 1).
-constexpr float kShapeCost[kShapes] = {1.0f, 1.6f, 0.7f, 0.85f};
+// Relative time per unit of tile work (128x128 = 1), measured on MI355X for
+// the contractions of the dense benchmark layers: [multi-part single-stage
+// kernels, single-part two-stage kernels][shape].
+constexpr float kShapeCost[2][kShapes] = {{1.0f, 1.6f, 0.7f, 0.85f}, {1.0f, 1.3f, 1.2f, 1.2f}};
 constexpr int kMaxSlotsPerCu = 8;  // upper bound on resident 256-thread blocks
 
 struct Plan16 {
@@ -397,8 +442,10 @@ Kind classify(int a_dtype, int b_dtype) {
 }
 
 void finish_plan(Plan16 &p, int M, int N, int K, const Kind &kd, bool a_kc, bool b_kc, int S) {
-    const int ksteps = (K + BK - 1) / BK;
-    p.k_chunk = ((ksteps + S - 1) / S) * BK;
+    // split boundaries on whole k-tiles of the kernel that will run
+    const int kt = parts_of(kd.sa) * parts_of(kd.sb) == 1 ? 64 : 32;
+    const int ksteps = (K + kt - 1) / kt;
+    p.k_chunk = ((ksteps + S - 1) / S) * kt;
     p.splits = (K + p.k_chunk - 1) / p.k_chunk;
     // An fp32 operand against spikes is re-staged by every workgroup along the
     // other output side; when that is 16 or more times, split it once into
@@ -481,7 +528,8 @@ Plan16 plan_for(const GemmArgs &g, const Kind &kd) {
         const int64_t items = (int64_t)tiles * p.splits;
         const int64_t rounds = (items + slots - 1) / slots;
         // time ~ rounds x tile work, plus the partial-sum traffic of split-K
-        double cost = (double)rounds * p.BM * p.BN * p.k_chunk * kShapeCost[sh];
+        double cost = (double)rounds * p.BM * p.BN * p.k_chunk *
+                      kShapeCost[lds_stages<SA, SB>() - 1][sh];
         if (p.splits > 1) cost += (double)p.splits * g.M * g.N * 64.0 / cus;
         if (cost < best_cost) {
             best_cost = cost;
