@@ -31,7 +31,6 @@ METRIC = "SNN training samples/sec (fwd+BPTT) at 1 GPU; scan HBM GB/s, GEMM MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
 PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 PEAK_FP16_MFMA_TFLOPS = 2500.0
-PEAK_FP32_VALU_TFLOPS = 78.6   # 256 CUs x 4 SIMDs x 16 lanes x 2 flops x 2.4 GHz
 
 
 def csrc_hash() -> str:
@@ -70,13 +69,15 @@ def stage_work(net, name, li):
                    dL/dI per (t, b, n), + 4 B colsum per (b, n)."""
     d = net.descs[li]
     TB = d.T * d.B
+    if d.synapse == 1:
+        # 5x5 valid conv: Co x Ci x 25 MACs per conv output, all outputs
+        macs = TB * (d.h_in - 4) * (d.w_in - 4) * d.c_out * d.c_in * 25
+    else:
+        macs = TB * d.n_out * d.n_in
     if name == "synapse_fwd":
-        return "flop", 2.0 * TB * d.n_out * d.n_in
+        return "flop", 2.0 * macs
     if name == "synapse_bwd":
-        f = 2.0 * TB * d.n_out * d.n_in  # dW
-        if li > 0:
-            f *= 2  # and dx
-        return "flop", f
+        return "flop", 2.0 * macs * (2 if li > 0 else 1)  # dW, and dx below the input layer
     el = TB * d.n_out
     cols = d.B * d.n_out
     if name == "neuron_fwd":
@@ -227,15 +228,15 @@ def main():
                 e.record(stream)
                 kev.append(e)
 
-        start = torch.cuda.Event(enable_timing=True)
-        end = torch.cuda.Event(enable_timing=True)
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
         torch.cuda.synchronize()
-        start.record(stream)
-        for _ in range(args.steps):
+        marks[0].record(stream)
+        for i in range(args.steps):
             net.step_stages(x, labels=y, targets=tgt, hook=rec_dom)
-        end.record(stream)
+            marks[i + 1].record(stream)
         torch.cuda.synchronize()
-        total_ms = start.elapsed_time(end)
+        total_ms = marks[0].elapsed_time(marks[-1])
+        per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
         kms = [kev[i].elapsed_time(kev[i + 1]) for i in range(0, len(kev), 2)]
         k_avg_ms = sum(kms) / len(kms)
 
@@ -245,19 +246,13 @@ def main():
     if kind == "flop":
         achieved = work / (k_avg_ms / 1000.0) / 1e12
         ckind, passes = _contraction_kind(net, dom_li, args.fp32_mfma)
-        if ckind == "valu":
-            roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_VALU_TFLOPS,
-                    "unit": "TFLOP/s",
-                    "peak_basis": "fp32 vector FMA without packed instructions: 256 CUs x 4 "
-                                  "SIMDs x 16 lanes x 2 flops x 2.4 GHz"}
+        if ckind == "mfma16":
+            peak, basis = PEAK_FP16_MFMA_TFLOPS, "bf16/fp16 dense MFMA"
         else:
-            if ckind == "mfma16":
-                peak, basis = PEAK_FP16_MFMA_TFLOPS, "bf16/fp16 dense MFMA"
-            else:
-                peak, basis = PEAK_FP32_MFMA_TFLOPS, "fp32 dense MFMA"
-            roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
-                    "unit": "TFLOP/s", "peak_basis": basis, "mfma_passes": passes,
-                    "executed_mfma_frac": round(passes * achieved / peak, 4)}
+            peak, basis = PEAK_FP32_MFMA_TFLOPS, "fp32 dense MFMA"
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
+                "unit": "TFLOP/s", "peak_basis": basis, "mfma_passes": passes,
+                "executed_mfma_frac": round(passes * achieved / peak, 4)}
     else:
         achieved = work / (k_avg_ms / 1000.0) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
@@ -279,8 +274,12 @@ def main():
                    "surrogate_slope": wl.slope, "input": "Bernoulli rate-coded spikes"
                    if wl.input == "spikes" else "normal currents",
                    "includes": "forward + loss + BPTT backward, no optimizer update"},
+        "step_ms": {"median": round(per_step[len(per_step) // 2], 5),
+                    "p10": round(per_step[len(per_step) // 10], 5),
+                    "p90": round(per_step[(9 * len(per_step)) // 10], 5)},
         "roofline": roof,
         "stage_ms": {k: round(v, 5) for k, v in split.items()},
+        "stage_roofline": _stage_rooflines(net, split, args.fp32_mfma),
     }
     syn = sum(v for k, v in split.items() if k.startswith("synapse"))
     neu = sum(v for k, v in split.items() if k.startswith("neuron"))
@@ -292,14 +291,39 @@ def main():
     print(json.dumps(out), flush=True)
 
 
+def _stage_rooflines(net, split, fp32_mfma):
+    """Each stage's algorithmic rate against its own roof (scans: GB/s of
+    8 TB/s; contractions: TFLOP/s of the MFMA peak of the type they run on),
+    from the untimed split pass."""
+    out = {}
+    for key, ms in split.items():
+        if "[L" not in key or ms <= 0:
+            continue
+        name, li = key.split("[L")[0], int(key.split("[L")[1].rstrip("]"))
+        kind, work = stage_work(net, name, li)
+        if kind == "flop":
+            ck, _ = _contraction_kind(net, li, fp32_mfma)
+            peak = PEAK_FP16_MFMA_TFLOPS if ck == "mfma16" else PEAK_FP32_MFMA_TFLOPS
+            a = work / (ms / 1000.0) / 1e12
+            out[key] = {"TFLOP/s": round(a, 2), "frac": round(a / peak, 4)}
+        elif kind == "byte":
+            a = work / (ms / 1000.0) / 1e9
+            out[key] = {"GB/s": round(a, 1), "frac": round(a / PEAK_HBM_GBS, 4)}
+    return out
+
+
 def _contraction_kind(net, li, fp32_mfma):
     """How the library contracts layer li's forward product (mirrors the
-    operand classification in gemm_mfma16.hip): ('mfma16', passes),
-    ('mfma32', 1) or ('valu', 1) for the direct convolution."""
+    operand classification in gemm_mfma16.hip): ('mfma16', passes) or
+    ('mfma32', 1).  A conv layer's product has one row per conv output that a
+    pool window reads and one column per output channel."""
     d = net.descs[li]
     if d.synapse == 1:
-        return "valu", 1
-    wide = d.T * d.B >= 64 and d.n_out >= 64
+        rows = 4 * d.T * d.B * ((d.h_in - 4) // 2) * ((d.w_in - 4) // 2)
+        cols = d.c_out
+    else:
+        rows, cols = d.T * d.B, d.n_out
+    wide = rows >= 64 and cols >= 64
     if fp32_mfma or not wide or d.in_dtype != 3:
         return "mfma32", 1
     if d.w_dtype == 0:
@@ -314,8 +338,9 @@ def _stage_kernels(net, name, li, fp32_mfma):
     if name == "neuron_bwd":
         return ": neuron_bwd_kernel"
     kind, passes = _contraction_kind(net, li, fp32_mfma)
-    if kind == "valu":
-        return ": conv_pool_fwd_kernel"
+    if net.descs[li].synapse == 1:
+        g = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"
+        return f": im2col_kernel + {g} + pool_kernel (the whole stage is timed)"
     if kind == "mfma16" and passes == 3:
         return (": split_planes_kernel (weights into bf16 planes) + gemm16_kernel"
                 " (+ splitk_reduce_kernel when split over K)")

@@ -13,6 +13,22 @@ bool aligned16(const void *p) { return (((uintptr_t)p) & 15u) == 0; }
 
 bool finite(float x) { return isfinite(x) != 0; }
 
+int64_t rows(const snn_layer_desc *d) { return (int64_t)d->T * d->B; }
+
+ConvGeom conv_geom(const snn_layer_desc *d) {
+    ConvGeom g{};
+    g.NB = (int)rows(d);
+    g.Ci = d->c_in;
+    g.H = d->h_in;
+    g.W = d->w_in;
+    g.Co = d->c_out;
+    g.Ho = d->h_in - 4;
+    g.Wo = d->w_in - 4;
+    g.Hp = g.Ho / 2;
+    g.Wp = g.Wo / 2;
+    return g;
+}
+
 // Validates a layer descriptor; nothing here touches the device.
 snn_status check_desc(const snn_layer_desc *d) {
     if (!d) return SNN_ERR_NULL;
@@ -43,6 +59,8 @@ snn_status check_desc(const snn_layer_desc *d) {
             if ((int64_t)d->c_out * hp * wp != d->n_out) return SNN_ERR_SHAPE;
             if (d->in_dtype != SNN_U8 && d->in_dtype != SNN_F32) return SNN_ERR_DTYPE;
             if (d->w_dtype != SNN_F32 || d->grad_dtype != SNN_F32) return SNN_ERR_DTYPE;
+            if (d->c_out > 2047) return SNN_ERR_UNSUPPORTED;
+            if (!conv_fits_int32(conv_geom(d))) return SNN_ERR_SHAPE;
             break;
         }
         case SNN_SYN_NONE:
@@ -58,22 +76,6 @@ snn_status check_desc(const snn_layer_desc *d) {
     return SNN_OK;
 }
 
-int64_t rows(const snn_layer_desc *d) { return (int64_t)d->T * d->B; }
-
-ConvGeom conv_geom(const snn_layer_desc *d) {
-    ConvGeom g{};
-    g.NB = (int)rows(d);
-    g.Ci = d->c_in;
-    g.H = d->h_in;
-    g.W = d->w_in;
-    g.Co = d->c_out;
-    g.Ho = d->h_in - 4;
-    g.Wo = d->w_in - 4;
-    g.Hp = g.Ho / 2;
-    g.Wp = g.Wo / 2;
-    return g;
-}
-
 // byte offset of the pool selection inside the saved buffer (conv layers)
 size_t arg_offset(const snn_layer_desc *d) { return align_up((size_t)rows(d) * d->n_out * sizeof(float)); }
 
@@ -81,9 +83,11 @@ size_t arg_offset(const snn_layer_desc *d) { return align_up((size_t)rows(d) * d
 bool split_ok(const snn_layer_desc *d) { return (d->flags & SNN_FLAG_FP32_MFMA) == 0; }
 
 // ---- workspace layout ------------------------------------------------------
-// forward:  [gemm split-K partials]
-// backward: [dcur (grad_dtype) T*B*n_out][colsum fp32 B*n_out][gemm partials]
+// forward:  [contraction workspace]
+// backward: [dcur (grad_dtype) T*B*n_out][colsum fp32 B*n_out][contraction workspace]
 size_t fwd_ws(const snn_layer_desc *d) {
+    if (d->synapse == SNN_SYN_CONV5_POOL2)
+        return conv_fwd_workspace_bytes(conv_geom(d), d->in_dtype, split_ok(d));
     if (d->synapse != SNN_SYN_DENSE) return 0;
     return gemm_workspace_bytes((int)rows(d), d->n_out, d->n_in, d->in_dtype, d->w_dtype, true,
                                 true, split_ok(d));
@@ -164,7 +168,7 @@ DxPlan dx_plan(const snn_layer_desc *d) {
 
 size_t bwd_gemm_ws(const snn_layer_desc *d) {
     if (d->synapse == SNN_SYN_CONV5_POOL2)
-        return conv_workspace_bytes(conv_geom(d), d->in_dtype, d->w_dtype, d->grad_dtype);
+        return conv_bwd_workspace_bytes(conv_geom(d), d->in_dtype, split_ok(d));
     if (d->synapse != SNN_SYN_DENSE) return 0;
     const DwPlan w = dw_plan(d);
     const DxPlan x = dx_plan(d);
@@ -232,8 +236,8 @@ snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w
     if (rows(d) == 0) return SNN_OK;
     (void)hipGetLastError();
     if (d->synapse == SNN_SYN_CONV5_POOL2)
-        return hip_status(launch_conv_pool_fwd(conv_geom(d), x, d->in_dtype, w, d->w_dtype, bias,
-                                               cur, pool_arg, ws, ws_bytes, stream));
+        return hip_status(launch_conv_pool_fwd(conv_geom(d), x, d->in_dtype, w, bias, cur,
+                                               pool_arg, split_ok(d), ws, ws_bytes, stream));
     GemmArgs g{};
     g.M = (int)rows(d);
     g.N = d->n_out;
@@ -324,9 +328,9 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
     }
     (void)hipGetLastError();
     if (d->synapse == SNN_SYN_CONV5_POOL2)
-        return hip_status(launch_conv_pool_bwd(conv_geom(d), dcur, d->grad_dtype, pool_arg, x,
-                                               d->in_dtype, w, d->w_dtype, grad_w, grad_x, ws,
-                                               ws_bytes, stream));
+        return hip_status(launch_conv_pool_bwd(conv_geom(d), reinterpret_cast<const float *>(dcur),
+                                               pool_arg, x, d->in_dtype, w, split_ok(d), grad_w,
+                                               grad_x, ws, ws_bytes, stream));
     const int M = (int)rows(d);
     char *wsb = reinterpret_cast<char *>(ws);
     if (grad_w) {

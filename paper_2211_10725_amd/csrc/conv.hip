@@ -2,21 +2,34 @@
 // a 5x5 valid cross-correlation, stride 1, plus bias, followed by 2x2 / 2
 // max-pooling of the currents before the neuron.
 //
-// Forward: one lane per pooled current (image, channel, py, px).  It forms
-// the four conv outputs of its window, each accumulated in fp32 in the fixed
-// order bias, c, ky, kx, so equal receptive fields give bit-equal currents;
-// it keeps the first maximum in row-major window order (ties stay with the
-// first) and records the choice (0..3) for the backward.  Consecutive lanes
-// take consecutive px, so their input patches overlap in cache.
+// Both directions run as matrix products on the contraction kernels.  The
+// conv outputs that some pool window reads are enumerated window by window:
+//   row m = 4 q + d,  q = (nb * Hp + py) * Wp + px  (pooled cell),
+//   d = 2 dy + dx     (position in the window, row-major),
+// so conv output (oy, ox) = (2 py + dy, 2 px + dx), and a trailing odd row or
+// column of conv outputs, which no window reads, is never computed.  With
+// k = (c * 5 + ky) * 5 + kx (the weight layout [Co][Ci][5][5] flattened) and
+// Kc = Ci * 25:
 //
-// Backward, given dL/dI of the pooled currents:
-//   dx[n,c,y,x] = sum_{co,ky,kx} dI[n,co,py,px] w[co,c,ky,kx] over the conv
-//                 outputs (y-ky, x-kx) that were selected by their pool window
-//                 (gather form, fixed order co, ky, kx: deterministic);
-//   dw[co,c,ky,kx] = sum over images and pooled cells of dI times the input
-//                 under the selected output, in two passes (per image chunk,
-//                 then the chunks in order).
-// The bias gradient comes from the neuron scan's per-column sums.
+// Forward
+//   col[m][k]  = x[nb, c, oy + ky, ox + kx]               (gather)
+//   C[m][co]   = sum_k col[m][k] w[co][k] + bias[co]       (contraction)
+//   cur[nb, co, py, px] = max_d C[4q + d][co], the first maximum in window
+//                order; its d (0..3) is saved for the backward  (pool)
+//
+// Backward, given dI = dL/dcur:
+//   dC^T[co][m] = dI[nb, co, py, px] if d is the saved choice, else 0
+//   dW[co][k]   = sum_m dC^T[co][m] col^T[k][m]           (contraction)
+//   dx^T[k][m]  = sum_co w[co][k] dC^T[co][m]             (contraction)
+//   dx[nb, c, y, x] = sum_{ky, kx} dx^T[(c, ky, kx)][m(nb, y - ky, x - kx)]
+//                over the window rows that exist, in the fixed order ky, kx
+//
+// The contractions are the library's GEMMs (exact multi-part bf16 products
+// with fp32 accumulation on the 16-bit matrix cores where they apply, fp32
+// MFMA otherwise), so every sum is deterministic.  Spikes are staged as
+// bytes; an fp32 dC^T is written directly as three exact bf16 planes when the
+// weight gradient runs on the 16-bit cores.  The bias gradient comes from the
+// neuron scan's per-column sums.
 #include "snn_internal.hpp"
 
 namespace snn {
@@ -25,186 +38,515 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int KS = 5;  // kernel size
 
-template <typename TX>
-__device__ inline float xval(const TX *x, int64_t i) { return (float)x[i]; }
+// Sizes of the conv-as-GEMM buffers
+struct ConvDims {
+    int64_t Q;    // pooled cells, NB * Hp * Wp
+    int64_t Mw;   // GEMM rows, 4 Q
+    int Kc;       // Ci * 25
+    int64_t ldk;  // row stride of col (elements), Kc rounded up to 16
+    int64_t ldm;  // row stride of the transposed buffers (elements), Mw rounded up to 16
+};
 
-template <typename TX>
-__global__ __launch_bounds__(kThreads) void conv_pool_fwd_kernel(
-    int NB, int Ci, int H, int W, int Co, int Hp, int Wp, const TX *__restrict__ x,
-    const float *__restrict__ w, const float *__restrict__ bias, float *__restrict__ cur,
-    uint8_t *__restrict__ arg) {
-    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    const int64_t total = (int64_t)NB * Co * Hp * Wp;
-    if (idx >= total) return;
-    const int px = (int)(idx % Wp);
-    const int py = (int)((idx / Wp) % Hp);
-    const int co = (int)((idx / ((int64_t)Wp * Hp)) % Co);
-    const int64_t nb = idx / ((int64_t)Wp * Hp * Co);
-    const float b0 = bias ? bias[co] : 0.f;
-    const float *wc = w + (int64_t)co * Ci * KS * KS;
+ConvDims dims_of(const ConvGeom &g) {
+    ConvDims v{};
+    v.Q = (int64_t)g.NB * g.Hp * g.Wp;
+    v.Mw = 4 * v.Q;
+    v.Kc = g.Ci * KS * KS;
+    v.ldk = (v.Kc + 15) / 16 * 16;
+    v.ldm = (v.Mw + 15) / 16 * 16;
+    return v;
+}
+
+// conv output coordinates of GEMM row m
+struct RowPos {
+    int64_t nb;
+    int oy, ox;
+};
+__device__ inline RowPos row_pos(int64_t m, int Hp, int Wp) {
+    const int64_t q = m >> 2;
+    const int d = (int)(m & 3);
+    const int64_t hw = (int64_t)Hp * Wp;
+    const int p = (int)(q % hw);
+    RowPos r;
+    r.nb = q / hw;
+    r.oy = 2 * (p / Wp) + (d >> 1);
+    r.ox = 2 * (p % Wp) + (d & 1);
+    return r;
+}
+
+__device__ inline int64_t x_index(const RowPos &r, int k, int Ci, int H, int W) {
+    const int c = k / (KS * KS), t = k % (KS * KS);
+    return ((r.nb * Ci + c) * H + r.oy + t / KS) * W + r.ox + t % KS;
+}
+
+// 16 bytes of T, built element by element
+template <typename T>
+struct Chunk {
+    static constexpr int N = 16 / (int)sizeof(T);
+    union {
+        T e[N];
+        uint4 v;
+    };
+};
+
+// Every conv tensor and GEMM buffer of a layer holds fewer than 2^31
+// elements (checked when the layer is validated), so the kernels index in
+// 32-bit integers.
+
+// col[m][k0 .. k0 + N): one thread per 16-byte chunk of a row; k >= Kc is 0.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void im2col_kernel(int Mw, int Kc, int ldk, int Ci, int H,
+                                                          int W, int Hp, int Wp,
+                                                          const T *__restrict__ x,
+                                                          T *__restrict__ col) {
+    constexpr int N = Chunk<T>::N;
+    const int cpr = ldk / N;  // chunks per row
+    const int idx = blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= Mw * cpr) return;
+    const int m = idx / cpr, k0 = (idx - m * cpr) * N;
+    const int q = m >> 2, d = m & 3, hw = Hp * Wp;
+    const int nb = q / hw, p = q - nb * hw;
+    const int py = p / Wp, px = p - py * Wp;
+    const int base = (nb * Ci * H + 2 * py + (d >> 1)) * W + 2 * px + (d & 1);
+    Chunk<T> ch;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const int k = min(k0 + i, Kc - 1);  // padding columns load a valid element, stored as 0
+        const int c = k / (KS * KS), t = k - c * KS * KS, ky = t / KS, kx = t - ky * KS;
+        const T e = x[base + (c * H + ky) * W + kx];
+        ch.e[i] = (k0 + i < Kc) ? e : T(0);
+    }
+    *reinterpret_cast<uint4 *>(col + m * ldk + k0) = ch.v;
+}
+
+// col^T[k][m0 .. m0 + N): one thread per 16-byte chunk, N/4 whole windows
+// (their four positions are x offsets 0, 1, W, W + 1); m >= Mw is 0.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void im2col_t_kernel(int Mw, int Kc, int ldm, int Ci, int H,
+                                                            int W, int Hp, int Wp,
+                                                            const T *__restrict__ x,
+                                                            T *__restrict__ colt) {
+    constexpr int N = Chunk<T>::N;
+    const int cpr = ldm / N;
+    const int idx = blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= Kc * cpr) return;
+    const int k = idx / cpr, m0 = (idx - k * cpr) * N;
+    const int c = k / (KS * KS), t = k - c * KS * KS, ky = t / KS, kx = t - ky * KS;
+    const int off = (c * H + ky) * W + kx;
+    const int hw = Hp * Wp;
+    Chunk<T> ch;
+#pragma unroll
+    for (int j = 0; j < N / 4; ++j) {
+        const int qj = (m0 >> 2) + j;
+        const int q = min(qj, (Mw >> 2) - 1);  // windows past the end load the last, stored as 0
+        const int nb = q / hw, p = q - nb * hw, py = p / Wp, px = p - py * Wp;
+        const T *xp = x + (nb * Ci * H + 2 * py) * W + 2 * px + off;
+        const bool in = 4 * qj < Mw;
+        const T v0 = xp[0], v1 = xp[1], v2 = xp[W], v3 = xp[W + 1];
+        ch.e[4 * j] = in ? v0 : T(0);
+        ch.e[4 * j + 1] = in ? v1 : T(0);
+        ch.e[4 * j + 2] = in ? v2 : T(0);
+        ch.e[4 * j + 3] = in ? v3 : T(0);
+    }
+    *reinterpret_cast<uint4 *>(colt + k * ldm + m0) = ch.v;
+}
+
+// Pool: a block takes QB consecutive pooled cells, stages their 4 * QB rows
+// of C in LDS as [d][cell][co] (odd cell stride: the reads below are free of
+// bank conflicts), then writes cur and the selection in output order
+// (cell fastest, so consecutive lanes write consecutive addresses).
+constexpr int kPoolLdsFloats = 8192;  // 32 KiB
+
+__global__ __launch_bounds__(kThreads) void pool_kernel(int Q, int Co, int HW, int QB,
+                                                        const float *__restrict__ C,
+                                                        float *__restrict__ cur,
+                                                        uint8_t *__restrict__ arg) {
+    __shared__ float lds[kPoolLdsFloats];
+    const int S = Co | 1;  // cell stride in LDS, odd
+    const int q0 = blockIdx.x * QB;
+    const int nq = min(QB, Q - q0);
+    const float *Cb = C + q0 * 4 * Co;
+    const int ne = nq * 4 * Co;  // <= kPoolLdsFloats
+    constexpr int kPer = kPoolLdsFloats / kThreads;
+    float v[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {  // all loads in flight before the LDS stores
+        const int e = threadIdx.x + j * kThreads;
+        v[j] = e < ne ? Cb[e] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const int e = threadIdx.x + j * kThreads;
+        if (e < ne) {
+            const int row = e / Co, co = e - row * Co;
+            lds[((row & 3) * QB + (row >> 2)) * S + co] = v[j];
+        }
+    }
+    __syncthreads();
+    const int no = nq * Co;
+    for (int i = threadIdx.x; i < no; i += kThreads) {
+        const int co = i / nq, qq = i - co * nq;
+        float best = lds[qq * S + co];
+        int a = 0;
+#pragma unroll
+        for (int d = 1; d < 4; ++d) {
+            const float v = lds[(d * QB + qq) * S + co];
+            if (v > best) {
+                best = v;
+                a = d;
+            }
+        }
+        const int q = q0 + qq, nb = q / HW;
+        const int o = (nb * Co + co) * HW + (q - nb * HW);
+        cur[o] = best;
+        arg[o] = (uint8_t)a;
+    }
+}
+
+__device__ inline uint32_t bf16_rne(float x) {
+    const uint32_t b = __float_as_uint(x);
+    return (b + 0x7fffu + ((b >> 16) & 1u)) >> 16;
+}
+
+// dC^T[co][4q .. 4q + 3] from the pooled gradient and the saved choice; with
+// `planes`, also its three exact bf16 parts (hi, mid, lo), planes Co * ldm
+// elements apart.
+__global__ __launch_bounds__(kThreads) void unpool_t_kernel(int Q, int Co, int HW, int ldm,
+                                                            const float *__restrict__ dI,
+                                                            const uint8_t *__restrict__ arg,
+                                                            float *__restrict__ dct,
+                                                            uint16_t *__restrict__ planes) {
+    const int idx = blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= Q * Co) return;
+    const int co = idx / Q, q = idx - co * Q;
+    const int nb = q / HW;
+    const int src = (nb * Co + co) * HW + (q - nb * HW);
+    const float g = dI[src];
+    const int a = arg[src];
     float v[4];
 #pragma unroll
-    for (int d = 0; d < 4; ++d) {
-        const int oy = 2 * py + (d >> 1), ox = 2 * px + (d & 1);
-        float acc = b0;
-        for (int c = 0; c < Ci; ++c) {
-            const TX *xc = x + ((nb * Ci + c) * H + oy) * W + ox;
-            const float *wk = wc + c * KS * KS;
+    for (int d = 0; d < 4; ++d) v[d] = (d == a) ? g : 0.f;
+    const int o = co * ldm + 4 * q;
+    *reinterpret_cast<float4 *>(dct + o) = make_float4(v[0], v[1], v[2], v[3]);
+    if (planes) {
+        uint32_t p[3][4];
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+            const uint32_t hi = bf16_rne(v[d]);
+            const float r = v[d] - __uint_as_float(hi << 16);
+            const uint32_t mid = bf16_rne(r);
+            p[0][d] = hi;
+            p[1][d] = mid;
+            p[2][d] = bf16_rne(r - __uint_as_float(mid << 16));
+        }
+        const int64_t ps = (int64_t)Co * ldm;
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+            *reinterpret_cast<uint2 *>(planes + k * ps + o) =
+                make_uint2(p[k][0] | (p[k][1] << 16), p[k][2] | (p[k][3] << 16));
+    }
+}
+
+// dx[nb, c, y, x] = sum over (ky, kx) of dx^T[(c, ky, kx)][m(nb, y - ky, x - kx)]
+// for the conv outputs some window reads; fixed order ky, kx.  Lanes take the
+// input pixels in 2x2 blocks, (y, x) = (2 py + dy, 2 px + dx) with (dy, dx)
+// fastest, the order of the window rows m: for each (ky, kx) a wave then reads
+// one or two contiguous runs of dx^T.
+__global__ __launch_bounds__(kThreads) void col2im_kernel(int total, int Ci, int H, int W, int PH,
+                                                          int PW, int Hp, int Wp, int ldm,
+                                                          const float *__restrict__ dxt,
+                                                          float *__restrict__ dx) {
+    const int idx = blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= total) return;
+    const int e = idx & 3, cell = idx >> 2;
+    const int r = cell / PW, px = cell - r * PW;
+    const int img = r / PH, py = r - img * PH;
+    const int yy = 2 * py + (e >> 1), xx = 2 * px + (e & 1);
+    if (yy >= H || xx >= W) return;
+    const int nb = img / Ci, c = img - nb * Ci;
+    // all 25 loads are issued unconditionally (a tap outside the windows
+    // reads row 0 of its k and is not added), so they overlap in flight
+    float v[KS * KS];
+    bool ok[KS * KS];
+#pragma unroll
+    for (int ky = 0; ky < KS; ++ky) {
+        const int oy = yy - ky;
+        const bool oky = oy >= 0 && oy < 2 * Hp;
+        const int mrow = (nb * Hp + (oy >> 1)) * Wp;
+#pragma unroll
+        for (int kx = 0; kx < KS; ++kx) {
+            const int ox = xx - kx;
+            const bool okx = ox >= 0 && ox < 2 * Wp;
+            const int m = (oky && okx) ? (mrow + (ox >> 1)) * 4 + 2 * (oy & 1) + (ox & 1) : 0;
+            v[ky * KS + kx] = dxt[((c * KS + ky) * KS + kx) * ldm + m];
+            ok[ky * KS + kx] = oky && okx;
+        }
+    }
+    float acc = 0.f;
+#pragma unroll
+    for (int t = 0; t < KS * KS; ++t)
+        if (ok[t]) acc += v[t];
+    dx[(img * H + yy) * W + xx] = acc;
+}
+
+// Weight gradient of a layer with few inputs per channel (Kc = Ci * 25 = KC
+// <= 50: the network's input layer), straight from the pool's selection:
+//   dW[co][k] = sum over pooled cells of dI times x under the selected output.
+// Block (chunk, co) takes a fixed range of cells; each thread sums its cells
+// in fp32, then a fixed-order tree over the block gives partial[chunk][co][k].
+template <typename T, int KC>
+__global__ __launch_bounds__(kThreads) void conv_dw_small_kernel(
+    int Q, int cells, int Co, int H, int W, int Hp, int Wp, const float *__restrict__ dI,
+    const uint8_t *__restrict__ arg, const T *__restrict__ x, float *__restrict__ partial) {
+    constexpr int CI = KC / (KS * KS);
+    __shared__ float red[KC][kThreads];
+    const int co = blockIdx.y;
+    const int q0 = blockIdx.x * cells, q1 = min(Q, q0 + cells);
+    const int hw = Hp * Wp;
+    float acc[KC];
+#pragma unroll
+    for (int k = 0; k < KC; ++k) acc[k] = 0.f;
+    for (int q = q0 + threadIdx.x; q < q1; q += kThreads) {
+        const int nb = q / hw, p = q - nb * hw, py = p / Wp, px = p - py * Wp;
+        const int o = (nb * Co + co) * hw + p;
+        const float g = dI[o];
+        const int a = arg[o];
+        const T *xp = x + (nb * CI * H + 2 * py + (a >> 1)) * W + 2 * px + (a & 1);
+#pragma unroll
+        for (int c = 0; c < CI; ++c)
 #pragma unroll
             for (int ky = 0; ky < KS; ++ky)
 #pragma unroll
-                for (int kx = 0; kx < KS; ++kx)
-                    acc = __builtin_fmaf(wk[ky * KS + kx], xval<TX>(xc, ky * W + kx), acc);
-        }
-        v[d] = acc;
+                for (int kx = 0; kx < KS; ++kx) {
+                    const int k = (c * KS + ky) * KS + kx;
+                    acc[k] = __builtin_fmaf(g, (float)xp[(c * H + ky) * W + kx], acc[k]);
+                }
     }
-    float best = v[0];
-    int a = 0;
 #pragma unroll
-    for (int d = 1; d < 4; ++d)
-        if (v[d] > best) {
-            best = v[d];
-            a = d;
+    for (int k = 0; k < KC; ++k) red[k][threadIdx.x] = acc[k];
+    __syncthreads();
+    for (int s = kThreads / 2; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) {
+#pragma unroll
+            for (int k = 0; k < KC; ++k) red[k][threadIdx.x] += red[k][threadIdx.x + s];
         }
-    cur[idx] = best;
-    arg[idx] = (uint8_t)a;
-}
-
-// dL/dx of the conv input, one lane per input element.
-__global__ __launch_bounds__(kThreads) void conv_pool_bwd_dx_kernel(
-    int NB, int Ci, int H, int W, int Co, int Hp, int Wp, const float *__restrict__ dI,
-    const uint8_t *__restrict__ arg, const float *__restrict__ w, float *__restrict__ dx) {
-    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    const int64_t total = (int64_t)NB * Ci * H * W;
-    if (idx >= total) return;
-    const int xx = (int)(idx % W);
-    const int yy = (int)((idx / W) % H);
-    const int c = (int)((idx / ((int64_t)W * H)) % Ci);
-    const int64_t nb = idx / ((int64_t)W * H * Ci);
-    float acc = 0.f;
-    for (int co = 0; co < Co; ++co) {
-        const int64_t pbase = (nb * Co + co) * Hp * Wp;
-        const float *wk = w + ((int64_t)co * Ci + c) * KS * KS;
-#pragma unroll
-        for (int ky = 0; ky < KS; ++ky) {
-            const int oy = yy - ky;
-            if (oy < 0 || (oy >> 1) >= Hp) continue;
-#pragma unroll
-            for (int kx = 0; kx < KS; ++kx) {
-                const int ox = xx - kx;
-                if (ox < 0 || (ox >> 1) >= Wp) continue;
-                const int64_t p = pbase + (oy >> 1) * Wp + (ox >> 1);
-                if (arg[p] == (uint8_t)(((oy & 1) << 1) | (ox & 1)))
-                    acc = __builtin_fmaf(dI[p], wk[ky * KS + kx], acc);
-            }
-        }
+        __syncthreads();
     }
-    dx[idx] = acc;
+    if ((int)threadIdx.x < KC)
+        partial[(blockIdx.x * Co + co) * KC + threadIdx.x] = red[threadIdx.x][0];
 }
 
-// First pass of dL/dw: block (chunk, co); lane j owns weight (c, ky, kx) of
-// output channel co and sums over the chunk's images and pooled cells.
-template <typename TX>
-__global__ __launch_bounds__(kThreads) void conv_pool_bwd_dw_kernel(
-    int NB, int Ci, int H, int W, int Co, int Hp, int Wp, int chunk, const float *__restrict__ dI,
-    const uint8_t *__restrict__ arg, const TX *__restrict__ x, float *__restrict__ partial) {
-    const int co = blockIdx.y;
-    const int n0 = blockIdx.x * chunk;
-    const int n1 = min(NB, n0 + chunk);
-    const int nw = Ci * KS * KS;
-    for (int j = threadIdx.x; j < nw; j += kThreads) {
-        const int c = j / (KS * KS), ky = (j % (KS * KS)) / KS, kx = j % KS;
-        float acc = 0.f;
-        for (int nb = n0; nb < n1; ++nb) {
-            const int64_t pbase = ((int64_t)nb * Co + co) * Hp * Wp;
-            const TX *xc = x + ((int64_t)nb * Ci + c) * H * W;
-            for (int p = 0; p < Hp * Wp; ++p) {
-                const int a = arg[pbase + p];
-                const int oy = 2 * (p / Wp) + (a >> 1), ox = 2 * (p % Wp) + (a & 1);
-                acc = __builtin_fmaf(dI[pbase + p], xval<TX>(xc, (oy + ky) * W + ox + kx), acc);
-            }
-        }
-        partial[((int64_t)blockIdx.x * Co + co) * nw + j] = acc;
-    }
+// chunks of pooled cells per output channel for conv_dw_small_kernel
+int small_dw_chunks(const ConvGeom &g, int64_t Q) {
+    const int64_t by_cells = (Q + kThreads - 1) / kThreads;
+    const int64_t by_grid = max(1, 4096 / g.Co);
+    return (int)max((int64_t)1, min(by_cells, by_grid));
 }
 
-__global__ __launch_bounds__(kThreads) void conv_dw_reduce_kernel(int chunks, int64_t nwt,
-                                                                  const float *__restrict__ partial,
-                                                                  float *__restrict__ dw) {
-    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (i >= nwt) return;
-    float s = 0.f;
-    for (int k = 0; k < chunks; ++k) s += partial[(int64_t)k * nwt + i];
-    dw[i] = s;
-}
-
-int dw_chunks(const ConvGeom &g) {
-    // about 64 passes over the weights, at least one image each
-    return max(1, min(g.NB, 64));
-}
+bool small_dw(const ConvGeom &g) { return g.Ci * KS * KS <= 50; }
 
 unsigned blocks(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 
+// ---- plans and workspace ----------------------------------------------------
+// forward:  [col (in dtype) Mw x ldk][C fp32 Mw x Co][gemm]
+// backward: [dC^T fp32 Co x ldm] then, for dW, either [partial chunks x Co x Kc]
+//           (few inputs per channel) or [planes 3 x Co x ldm][col^T Kc x ldm][gemm],
+//           and, for dx (after dW), [dx^T fp32 Kc x ldm][gemm]
+
+GemmArgs fwd_args(const ConvGeom &g, const ConvDims &v, int in_dtype, bool allow_split) {
+    GemmArgs a{};
+    a.M = (int)v.Mw; a.N = g.Co; a.K = v.Kc;
+    a.lda = v.ldk; a.a_dtype = in_dtype; a.a_kc = true;
+    a.ldb = v.Kc; a.b_dtype = SNN_F32; a.b_kc = true;
+    a.ldc = g.Co; a.allow_split = allow_split;
+    return a;
+}
+
+GemmArgs dw_args(const ConvGeom &g, const ConvDims &v, int in_dtype, bool allow_split) {
+    GemmArgs a{};
+    a.M = g.Co; a.N = v.Kc; a.K = (int)v.Mw;
+    a.lda = v.ldm; a.a_dtype = kPlanes3; a.a_kc = true; a.a_ps = (int64_t)g.Co * v.ldm;
+    a.ldb = v.ldm; a.b_dtype = in_dtype; a.b_kc = true;
+    a.ldc = v.Kc; a.allow_split = allow_split;
+    if (!(allow_split && gemm16_applies(a))) {
+        a.a_dtype = SNN_F32;  // fp32 dC^T on the fp32 kernels
+        a.a_ps = 0;
+    }
+    return a;
+}
+
+GemmArgs dx_args(const ConvGeom &g, const ConvDims &v, bool allow_split) {
+    GemmArgs a{};
+    a.M = v.Kc; a.N = (int)v.Mw; a.K = g.Co;
+    a.lda = v.Kc; a.a_dtype = SNN_F32; a.a_kc = false;  // w[co][k]: k contiguous
+    a.ldb = v.ldm; a.b_dtype = SNN_F32; a.b_kc = false;  // dC^T[co][m]: m contiguous
+    a.ldc = v.ldm; a.allow_split = allow_split;
+    return a;
+}
+
+size_t gemm_ws(const GemmArgs &a) {
+    return gemm_workspace_bytes(a.M, a.N, a.K, a.a_dtype, a.b_dtype, a.a_kc, a.b_kc, a.allow_split);
+}
+
+struct BwdLayout {
+    bool small;  // weight gradient by conv_dw_small_kernel
+    int chunks;  // its cell chunks per channel
+    size_t dct, partial, planes, colt, dw_gemm, dxt, dx_gemm;
+    size_t dw_phase() const { return small ? partial : planes + colt + dw_gemm; }
+    size_t dx_phase() const { return dxt + dx_gemm; }
+};
+
+BwdLayout bwd_layout(const ConvGeom &g, const ConvDims &v, int in_dtype, bool allow_split) {
+    BwdLayout l{};
+    l.small = small_dw(g);
+    l.dct = align_up((size_t)g.Co * v.ldm * sizeof(float));
+    if (l.small) {
+        l.chunks = small_dw_chunks(g, v.Q);
+        l.partial = align_up((size_t)l.chunks * g.Co * v.Kc * sizeof(float));
+    } else {
+        const GemmArgs w = dw_args(g, v, in_dtype, allow_split);
+        l.planes = w.a_dtype == kPlanes3 ? align_up((size_t)3 * g.Co * v.ldm * sizeof(uint16_t)) : 0;
+        l.colt = align_up((size_t)v.Kc * v.ldm * dtype_bytes(in_dtype));
+        l.dw_gemm = gemm_ws(w);
+    }
+    l.dxt = align_up((size_t)v.Kc * v.ldm * sizeof(float));
+    l.dx_gemm = gemm_ws(dx_args(g, v, allow_split));
+    return l;
+}
+
+template <typename T>
+void launch_im2col(const ConvGeom &g, const ConvDims &v, const void *x, void *col, hipStream_t s) {
+    const int64_t n = v.Mw * (v.ldk / Chunk<T>::N);
+    im2col_kernel<T><<<blocks(n), kThreads, 0, s>>>((int)v.Mw, v.Kc, (int)v.ldk, g.Ci, g.H, g.W,
+                                                    g.Hp, g.Wp, reinterpret_cast<const T *>(x),
+                                                    reinterpret_cast<T *>(col));
+}
+
+template <typename T>
+void launch_im2col_t(const ConvGeom &g, const ConvDims &v, const void *x, void *colt,
+                     hipStream_t s) {
+    const int64_t n = (int64_t)v.Kc * (v.ldm / Chunk<T>::N);
+    im2col_t_kernel<T><<<blocks(n), kThreads, 0, s>>>((int)v.Mw, v.Kc, (int)v.ldm, g.Ci, g.H, g.W,
+                                                      g.Hp, g.Wp, reinterpret_cast<const T *>(x),
+                                                      reinterpret_cast<T *>(colt));
+}
+
+template <typename T>
+void launch_dw_small(const ConvGeom &g, const ConvDims &v, int chunks, const float *dI,
+                     const uint8_t *arg, const void *x, float *partial, hipStream_t s) {
+    const int cells = (int)((v.Q + chunks - 1) / chunks);
+    dim3 grid((unsigned)chunks, (unsigned)g.Co);
+    const T *xt = reinterpret_cast<const T *>(x);
+    if (g.Ci == 1)
+        conv_dw_small_kernel<T, 25><<<grid, kThreads, 0, s>>>((int)v.Q, cells, g.Co, g.H, g.W,
+                                                              g.Hp, g.Wp, dI, arg, xt, partial);
+    else
+        conv_dw_small_kernel<T, 50><<<grid, kThreads, 0, s>>>((int)v.Q, cells, g.Co, g.H, g.W,
+                                                              g.Hp, g.Wp, dI, arg, xt, partial);
+}
+
 }  // namespace
 
-size_t conv_workspace_bytes(const ConvGeom &g, int in_dtype, int w_dtype, int grad_dtype) {
-    (void)in_dtype; (void)w_dtype; (void)grad_dtype;
-    const int chunks = dw_chunks(g);
-    return align_up((size_t)chunks * g.Co * g.Ci * KS * KS * sizeof(float));
+bool conv_fits_int32(const ConvGeom &g) {
+    const ConvDims v = dims_of(g);
+    const int64_t lim = INT32_MAX;
+    return (int64_t)g.NB * g.Ci * (g.H + 1) * (g.W + 1) <= lim && v.Mw * v.ldk <= lim &&
+           (int64_t)v.Kc * v.ldm <= lim && (int64_t)g.Co * v.ldm <= lim && v.Mw * g.Co <= lim;
+}
+
+size_t conv_fwd_workspace_bytes(const ConvGeom &g, int in_dtype, bool allow_split) {
+    const ConvDims v = dims_of(g);
+    if (v.Mw == 0) return 0;
+    return align_up((size_t)v.Mw * v.ldk * dtype_bytes(in_dtype)) +
+           align_up((size_t)v.Mw * g.Co * sizeof(float)) +
+           gemm_ws(fwd_args(g, v, in_dtype, allow_split));
+}
+
+size_t conv_bwd_workspace_bytes(const ConvGeom &g, int in_dtype, bool allow_split) {
+    const ConvDims v = dims_of(g);
+    if (v.Mw == 0) return 0;
+    const BwdLayout l = bwd_layout(g, v, in_dtype, allow_split);
+    return l.dct + max(l.dw_phase(), l.dx_phase());
 }
 
 hipError_t launch_conv_pool_fwd(const ConvGeom &g, const void *x, int in_dtype, const void *w,
-                                int w_dtype, const float *bias, float *cur, uint8_t *arg,
+                                const float *bias, float *cur, uint8_t *arg, bool allow_split,
                                 void *ws, size_t ws_bytes, hipStream_t s) {
-    (void)w_dtype; (void)ws; (void)ws_bytes;
-    const int64_t total = (int64_t)g.NB * g.Co * g.Hp * g.Wp;
-    if (total <= 0) return hipSuccess;
-    const float *wf = reinterpret_cast<const float *>(w);
-    if (in_dtype == SNN_U8)
-        conv_pool_fwd_kernel<uint8_t><<<blocks(total), kThreads, 0, s>>>(
-            g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, reinterpret_cast<const uint8_t *>(x), wf, bias,
-            cur, arg);
-    else
-        conv_pool_fwd_kernel<float><<<blocks(total), kThreads, 0, s>>>(
-            g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, reinterpret_cast<const float *>(x), wf, bias,
-            cur, arg);
+    const ConvDims v = dims_of(g);
+    if (v.Mw == 0) return hipSuccess;
+    if (ws == nullptr || ws_bytes < conv_fwd_workspace_bytes(g, in_dtype, allow_split))
+        return hipErrorInvalidValue;
+    char *p = reinterpret_cast<char *>(ws);
+    void *col = p;
+    p += align_up((size_t)v.Mw * v.ldk * dtype_bytes(in_dtype));
+    float *C = reinterpret_cast<float *>(p);
+    p += align_up((size_t)v.Mw * g.Co * sizeof(float));
+    if (in_dtype == SNN_U8) launch_im2col<uint8_t>(g, v, x, col, s);
+    else launch_im2col<float>(g, v, x, col, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    GemmArgs a = fwd_args(g, v, in_dtype, allow_split);
+    a.A = col; a.B = w; a.C = C; a.bias = bias;
+    e = launch_gemm(a, p, ws_bytes - (size_t)(p - reinterpret_cast<char *>(ws)), s);
+    if (e != hipSuccess) return e;
+    const int S = g.Co | 1;
+    const int QB = max(1, kPoolLdsFloats / (4 * S));
+    pool_kernel<<<(unsigned)((v.Q + QB - 1) / QB), kThreads, 0, s>>>((int)v.Q, g.Co, g.Hp * g.Wp,
+                                                                   QB, C, cur, arg);
     return hipGetLastError();
 }
 
-hipError_t launch_conv_pool_bwd(const ConvGeom &g, const void *dcur, int grad_dtype,
-                                const uint8_t *arg, const void *x, int in_dtype, const void *w,
-                                int w_dtype, float *grad_w, float *grad_x, void *ws,
-                                size_t ws_bytes, hipStream_t s) {
-    (void)grad_dtype; (void)w_dtype;
-    const float *dI = reinterpret_cast<const float *>(dcur);
-    const float *wf = reinterpret_cast<const float *>(w);
-    if (grad_x) {
-        const int64_t total = (int64_t)g.NB * g.Ci * g.H * g.W;
-        conv_pool_bwd_dx_kernel<<<blocks(total), kThreads, 0, s>>>(
-            g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, dI, arg, wf, grad_x);
-        hipError_t e = hipGetLastError();
+hipError_t launch_conv_pool_bwd(const ConvGeom &g, const float *dI, const uint8_t *arg,
+                                const void *x, int in_dtype, const void *w, bool allow_split,
+                                float *grad_w, float *grad_x, void *ws, size_t ws_bytes,
+                                hipStream_t s) {
+    const ConvDims v = dims_of(g);
+    if (v.Mw == 0) return hipSuccess;
+    if (ws == nullptr || ws_bytes < conv_bwd_workspace_bytes(g, in_dtype, allow_split))
+        return hipErrorInvalidValue;
+    const BwdLayout l = bwd_layout(g, v, in_dtype, allow_split);
+    char *base = reinterpret_cast<char *>(ws);
+    float *dct = reinterpret_cast<float *>(base);
+    char *rest = base + l.dct;
+    const size_t rest_bytes = ws_bytes - l.dct;
+    hipError_t e;
+    if (grad_x || (grad_w && !l.small)) {
+        uint16_t *planes = (grad_w && l.planes > 0) ? reinterpret_cast<uint16_t *>(rest) : nullptr;
+        unpool_t_kernel<<<blocks(v.Q * g.Co), kThreads, 0, s>>>((int)v.Q, g.Co, g.Hp * g.Wp,
+                                                                (int)v.ldm, dI, arg, dct, planes);
+        e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (grad_w) {
-        const int chunks = dw_chunks(g);
-        const int per = (g.NB + chunks - 1) / chunks;
-        const int nchunks = (g.NB + per - 1) / per;
-        const int64_t nwt = (int64_t)g.Co * g.Ci * KS * KS;
-        if (ws == nullptr || ws_bytes < (size_t)nchunks * nwt * sizeof(float))
-            return hipErrorInvalidValue;
-        float *partial = reinterpret_cast<float *>(ws);
-        dim3 grid((unsigned)nchunks, (unsigned)g.Co);
-        if (in_dtype == SNN_U8)
-            conv_pool_bwd_dw_kernel<uint8_t><<<grid, kThreads, 0, s>>>(
-                g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, per, dI, arg,
-                reinterpret_cast<const uint8_t *>(x), partial);
-        else
-            conv_pool_bwd_dw_kernel<float><<<grid, kThreads, 0, s>>>(
-                g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, per, dI, arg,
-                reinterpret_cast<const float *>(x), partial);
-        hipError_t e = hipGetLastError();
+    if (grad_w && l.small) {
+        float *partial = reinterpret_cast<float *>(rest);
+        if (in_dtype == SNN_U8) launch_dw_small<uint8_t>(g, v, l.chunks, dI, arg, x, partial, s);
+        else launch_dw_small<float>(g, v, l.chunks, dI, arg, x, partial, s);
+        e = hipGetLastError();
         if (e != hipSuccess) return e;
-        conv_dw_reduce_kernel<<<blocks(nwt), kThreads, 0, s>>>(nchunks, nwt, partial, grad_w);
+        e = launch_splitk_reduce(g.Co, v.Kc, l.chunks, partial, grad_w, v.Kc, nullptr, s);
+        if (e != hipSuccess) return e;
+    } else if (grad_w) {
+        char *colt = rest + l.planes;
+        if (in_dtype == SNN_U8) launch_im2col_t<uint8_t>(g, v, x, colt, s);
+        else launch_im2col_t<float>(g, v, x, colt, s);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        GemmArgs a = dw_args(g, v, in_dtype, allow_split);
+        a.A = a.a_dtype == kPlanes3 ? static_cast<const void *>(rest) : dct;
+        a.B = colt; a.C = grad_w; a.bias = nullptr;
+        e = launch_gemm(a, colt + l.colt, rest_bytes - l.planes - l.colt, s);
+        if (e != hipSuccess) return e;
+    }
+    if (grad_x) {
+        float *dxt = reinterpret_cast<float *>(rest);
+        GemmArgs a = dx_args(g, v, allow_split);
+        a.A = w; a.B = dct; a.C = dxt; a.bias = nullptr;
+        e = launch_gemm(a, rest + l.dxt, rest_bytes - l.dxt, s);
+        if (e != hipSuccess) return e;
+        const int PH = (g.H + 1) / 2, PW = (g.W + 1) / 2;
+        const int total = g.NB * g.Ci * PH * PW * 4;
+        col2im_kernel<<<blocks(total), kThreads, 0, s>>>(total, g.Ci, g.H, g.W, PH, PW, g.Hp, g.Wp,
+                                                         (int)v.ldm, dxt, grad_x);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

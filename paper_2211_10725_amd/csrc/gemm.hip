@@ -225,6 +225,33 @@ __global__ __launch_bounds__(kThreads) void splitk_reduce_kernel(int M, int N, i
     C[(int64_t)m * ldc + n] = s;
 }
 
+// The same sum for many partials (S >= 16): a block reduces 64 outputs, its
+// four waves sum fixed quarters of z in ascending order, then the quarters
+// are added in order.
+__global__ __launch_bounds__(kThreads) void splitk_reduce_wide_kernel(
+    int M, int N, int S, const float *__restrict__ P, float *__restrict__ C, int64_t ldc,
+    const float *__restrict__ bias) {
+    __shared__ float part[4][64];
+    const int64_t total = (int64_t)M * N;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t idx = (int64_t)blockIdx.x * 64 + lane;
+    const int per = (S + 3) / 4;
+    const int z0 = wave * per, z1 = min(S, z0 + per);
+    float s = 0.f;
+    if (idx < total) {
+#pragma unroll 8
+        for (int z = z0; z < z1; ++z) s += P[(int64_t)z * total + idx];
+    }
+    part[wave][lane] = s;
+    __syncthreads();
+    if (wave == 0 && idx < total) {
+        float r = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
+        const int m = (int)(idx / N), n = (int)(idx % N);
+        if (bias) r += bias[n];
+        C[(int64_t)m * ldc + n] = r;
+    }
+}
+
 struct Plan {
     int cfg;  // 0: 128x128 (2x2 waves), 1: 64x64 (2x2), 2: 64x16 (4x1), 3: 16x64 (1x4)
     int BM, BN;
@@ -249,7 +276,9 @@ Plan make_plan(int M, int N, int K) {
     if (tiles < 256) {
         S = (int)((512 + tiles - 1) / tiles);
         S = min(S, max(1, ksteps / 8));  // keep at least 8 k-steps per split
-        S = min(S, 64);
+        // a small output over a long K (a conv weight gradient) may split
+        // further: its partial sums stay small
+        S = min(S, (int64_t)M * N <= 65536 ? 256 : 64);
     }
     p.k_chunk = ((ksteps + S - 1) / S) * BK;
     p.splits = (K + p.k_chunk - 1) / p.k_chunk;
@@ -351,8 +380,12 @@ hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t
 hipError_t launch_splitk_reduce(int M, int N, int S, const float *P, float *C, int64_t ldc,
                                 const float *bias, hipStream_t s) {
     const int64_t total = (int64_t)M * N;
-    splitk_reduce_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(
-        M, N, S, P, C, ldc, bias);
+    if (S >= 16)
+        splitk_reduce_wide_kernel<<<(unsigned)((total + 63) / 64), kThreads, 0, s>>>(M, N, S, P, C,
+                                                                                 ldc, bias);
+    else
+        splitk_reduce_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(
+            M, N, S, P, C, ldc, bias);
     return hipGetLastError();
 }
 

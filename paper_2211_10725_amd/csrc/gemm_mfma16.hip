@@ -213,13 +213,18 @@ struct Operand {
     }
 };
 
-// Three bf16 planes of an fp32 array: dst[p*n + i] = part p of src[i].
+// Three bf16 planes of an fp32 matrix src[rows][ld] (K columns used) into
+// dst[p][rows][ldp], ldp = K rounded up to 8 so that every plane row starts on
+// 16 bytes; the padding columns are 0.
 __global__ __launch_bounds__(kThreads) void split_planes_kernel(const float *__restrict__ src,
-                                                                uint16_t *__restrict__ dst,
-                                                                int64_t n) {
+                                                                int64_t ld, int K, int ldp,
+                                                                int64_t n,
+                                                                uint16_t *__restrict__ dst) {
     const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (i >= n) return;
-    uint32_t w[1] = {__float_as_uint(src[i])};
+    const int64_t r = i / ldp;
+    const int k = (int)(i - r * ldp);
+    uint32_t w[1] = {k < K ? __float_as_uint(src[r * ld + k]) : 0u};
     dst[i] = (uint16_t)part_of<SRC_F32, MT_BF16, 1>(w, 0, 0);
     dst[n + i] = (uint16_t)part_of<SRC_F32, MT_BF16, 1>(w, 0, 1);
     dst[2 * n + i] = (uint16_t)part_of<SRC_F32, MT_BF16, 1>(w, 0, 2);
@@ -398,11 +403,13 @@ struct Plan16 {
     size_t part_bytes;   // workspace for split-K partial sums
 };
 
-int max_splits(int tiles, int ksteps) {
-    // bounded by the most blocks a device could hold and by 4 k-tiles per split
+int max_splits(int tiles, int ksteps, int64_t mn) {
+    // bounded by the most blocks a device could hold and by 4 k-tiles per
+    // split; a small output over a long K (a conv weight gradient) may split
+    // further, its partial sums staying small
     int S = (kMaxSlotsPerCu * 256 + tiles - 1) / tiles;
     S = min(S, max(1, ksteps / 4));
-    return max(1, min(S, 64));
+    return max(1, min(S, mn <= 65536 ? 256 : 64));
 }
 
 // Operand classification --------------------------------------------------
@@ -452,12 +459,13 @@ void finish_plan(Plan16 &p, int M, int N, int K, const Kind &kd, bool a_kc, bool
     // planes instead.
     p.presplit = false;
     int64_t f32_elems = 0;
+    const int64_t ldp = (K + 7) / 8 * 8;  // plane rows padded to 16 bytes
     if (kd.sa == SRC_F32 && kd.sb == SRC_SPIKE && a_kc) {
         p.presplit = p.tiles_n >= 16;
-        f32_elems = (int64_t)M * K;
+        f32_elems = (int64_t)M * ldp;
     } else if (kd.sb == SRC_F32 && kd.sa == SRC_SPIKE && b_kc) {
         p.presplit = p.tiles_m >= 16;
-        f32_elems = (int64_t)N * K;
+        f32_elems = (int64_t)N * ldp;
     }
     p.plane_bytes = p.presplit ? align_up((size_t)3 * f32_elems * sizeof(uint16_t)) : 0;
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * M * N * sizeof(float)) : 0;
@@ -523,7 +531,7 @@ Plan16 plan_for(const GemmArgs &g, const Kind &kd) {
         const int tiles = p.tiles_m * p.tiles_n;
         const int slots = cus * occ[sh];
         int S = 1;
-        if (tiles < slots) S = max(1, min(slots / tiles, max_splits(tiles, ksteps)));
+        if (tiles < slots) S = max(1, min(slots / tiles, max_splits(tiles, ksteps, (int64_t)g.M * g.N)));
         finish_plan(p, g.M, g.N, g.K, kd, g.a_kc, g.b_kc, S);
         const int64_t items = (int64_t)tiles * p.splits;
         const int64_t rounds = (items + slots - 1) / slots;
@@ -576,19 +584,24 @@ hipError_t run16(const GemmArgs &g, const Kind &kd, void *ws, size_t ws_bytes, h
     }
     if constexpr ((SA == SRC_F32 && SB == SRC_SPIKE) || (SB == SRC_F32 && SA == SRC_SPIKE)) {
         if (p.presplit) {
-            // the fp32 operand is K-contiguous: the planes keep its leading dimension
+            // the fp32 operand is K-contiguous; its planes get 16-byte rows
             constexpr bool a_f32 = SA == SRC_F32;
             const int rows = a_f32 ? g.M : g.N;
-            const int64_t ld = a_f32 ? g.lda : g.ldb;
-            const int64_t n = (int64_t)(rows - 1) * ld + g.K;
+            const int ldp = (g.K + 7) / 8 * 8;
+            const int64_t n = (int64_t)rows * ldp;
             uint16_t *planes = reinterpret_cast<uint16_t *>(wsb);
             if (p.plane_bytes < (size_t)3 * n * sizeof(uint16_t)) return hipErrorInvalidValue;
             split_planes_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, s>>>(
-                reinterpret_cast<const float *>(a_f32 ? g.A : g.B), planes, n);
-            if constexpr (a_f32)
-                launch16<MT, SRC_PLANES, AK, SB, BKc>(g, p, planes, n, g.B, 0, out, ldo, ss, bias, s);
-            else
-                launch16<MT, SA, AK, SRC_PLANES, BKc>(g, p, g.A, 0, planes, n, out, ldo, ss, bias, s);
+                reinterpret_cast<const float *>(a_f32 ? g.A : g.B), a_f32 ? g.lda : g.ldb, g.K,
+                ldp, n, planes);
+            GemmArgs gp = g;
+            if constexpr (a_f32) {
+                gp.lda = ldp;
+                launch16<MT, SRC_PLANES, AK, SB, BKc>(gp, p, planes, n, g.B, 0, out, ldo, ss, bias, s);
+            } else {
+                gp.ldb = ldp;
+                launch16<MT, SA, AK, SRC_PLANES, BKc>(gp, p, g.A, 0, planes, n, out, ldo, ss, bias, s);
+            }
         } else {
             launch16<MT, SA, AK, SB, BKc>(g, p, g.A, g.a_ps, g.B, g.b_ps, out, ldo, ss, bias, s);
         }
@@ -660,7 +673,7 @@ size_t gemm16_workspace_bytes(const GemmArgs &g) {
         p.BN = kShapeBN[sh];
         p.tiles_m = (g.M + p.BM - 1) / p.BM;
         p.tiles_n = (g.N + p.BN - 1) / p.BN;
-        finish_plan(p, g.M, g.N, g.K, kd, g.a_kc, g.b_kc, max_splits(p.tiles_m * p.tiles_n, ksteps));
+        finish_plan(p, g.M, g.N, g.K, kd, g.a_kc, g.b_kc, max_splits(p.tiles_m * p.tiles_n, ksteps, (int64_t)g.M * g.N));
         best = max(best, p.plane_bytes + p.part_bytes);
     }
     return best;

@@ -240,6 +240,27 @@ __global__ __launch_bounds__(kThreads) void bias_reduce_kernel(int B, int F, int
     if (wave == 0 && f < F) db[f] = (float)(((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane]);
 }
 
+// The same sum for layers with P > 1 positions per feature (conv channels):
+// one 1024-thread block per feature, fp64 partial sums over a fixed
+// assignment of (b, p) to threads, then a fixed-order tree.
+constexpr int kReduceThreads = 1024;
+__global__ __launch_bounds__(kReduceThreads) void bias_reduce_pos_kernel(
+    int B, int F, int P, const float *__restrict__ colsum, float *__restrict__ db) {
+    __shared__ double part[kReduceThreads];
+    const int f = blockIdx.x;
+    const int64_t n = (int64_t)B * P;
+    double acc = 0.0;
+    for (int64_t j = threadIdx.x; j < n; j += kReduceThreads)
+        acc += (double)colsum[((j / P) * F + f) * P + j % P];
+    part[threadIdx.x] = acc;
+    __syncthreads();
+    for (int w = kReduceThreads / 2; w > 0; w >>= 1) {
+        if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) db[f] = (float)part[0];
+}
+
 __global__ __launch_bounds__(kThreads) void fill_zero_kernel(float *__restrict__ p, int64_t n) {
     const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (i < n) p[i] = 0.f;
@@ -330,7 +351,8 @@ hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s) {
 
 hipError_t launch_bias_reduce(int B, int F, int P, const float *colsum, float *db, hipStream_t s) {
     if (F <= 0) return hipSuccess;
-    bias_reduce_kernel<<<(F + 63) / 64, kThreads, 0, s>>>(B, F, P, colsum, db);
+    if (P > 1) bias_reduce_pos_kernel<<<F, kReduceThreads, 0, s>>>(B, F, P, colsum, db);
+    else bias_reduce_kernel<<<(F + 63) / 64, kThreads, 0, s>>>(B, F, P, colsum, db);
     return hipGetLastError();
 }
 

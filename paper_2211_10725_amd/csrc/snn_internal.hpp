@@ -110,13 +110,18 @@ struct ConvGeom {
     int Ci, H, W, Co;
     int Ho, Wo, Hp, Wp;  // conv output and pooled sizes
 };
-size_t conv_workspace_bytes(const ConvGeom &g, int in_dtype, int w_dtype, int grad_dtype);
+// every tensor and GEMM buffer of the layer indexes in int32
+bool conv_fits_int32(const ConvGeom &g);
+size_t conv_fwd_workspace_bytes(const ConvGeom &g, int in_dtype, bool allow_split);
+size_t conv_bwd_workspace_bytes(const ConvGeom &g, int in_dtype, bool allow_split);
+// cur [NB, Co, Hp, Wp] and the window choice (0..3) per pooled current
 hipError_t launch_conv_pool_fwd(const ConvGeom &g, const void *x, int in_dtype, const void *w,
-                                int w_dtype, const float *bias, float *cur, uint8_t *arg,
+                                const float *bias, float *cur, uint8_t *arg, bool allow_split,
                                 void *ws, size_t ws_bytes, hipStream_t s);
-hipError_t launch_conv_pool_bwd(const ConvGeom &g, const void *dcur, int grad_dtype,
-                                const uint8_t *arg, const void *x, int in_dtype, const void *w,
-                                int w_dtype, float *grad_w, float *grad_x, void *ws,
-                                size_t ws_bytes, hipStream_t s);
+// grad_w [Co, Ci, 5, 5] and grad_x [NB, Ci, H, W] (either may be NULL)
+hipError_t launch_conv_pool_bwd(const ConvGeom &g, const float *dI, const uint8_t *arg,
+                                const void *x, int in_dtype, const void *w, bool allow_split,
+                                float *grad_w, float *grad_x, void *ws, size_t ws_bytes,
+                                hipStream_t s);
 
 }  // namespace snn
