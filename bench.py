@@ -33,30 +33,40 @@ PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 PEAK_FP16_MFMA_TFLOPS = 2500.0
 
 
-def csrc_hash() -> str:
-    """Hash of the kernel sources, to tell whether a stored counter profile
-    still describes the kernels being timed."""
+# kernel sources behind each kind of stage (a stored counter profile of a
+# stage stays valid while these files are unchanged)
+STAGE_SOURCES = {
+    "synapse": ["snn_internal.hpp", "gemm.hip", "gemm_mfma16.hip", "conv.hip"],
+    "neuron": ["snn_internal.hpp", "scan.hip"],
+}
+
+
+def csrc_hash(files=None) -> str:
+    """Hash of kernel sources (all of them, or the named files)."""
     h = hashlib.sha256()
     d = os.path.join(ROOT, "paper_2211_10725_amd", "csrc")
-    for f in sorted(os.listdir(d)):
+    for f in sorted(files or os.listdir(d)):
         with open(os.path.join(d, f), "rb") as fh:
             h.update(f.encode() + fh.read())
     return h.hexdigest()[:16]
 
 
-def stored_traffic(kernel_key: str):
-    """HBM bytes per launch of `kernel_key` from the committed counter
-    summary, if it was taken on the current kernel sources; else None."""
+def stage_sources(stage_key: str):
+    return STAGE_SOURCES["synapse" if stage_key.startswith("synapse") else "neuron"]
+
+
+def stored_traffic(stage_key: str):
+    """HBM bytes per launch of a stage from the committed counter summary,
+    if its kernels' sources are unchanged since the counters were taken."""
     path = os.path.join(ROOT, "profiles", "traffic.md")
     if not os.path.exists(path):
         return None
     txt = open(path).read()
-    m = re.search(r"csrc_hash:\s*([0-9a-f]+)", txt)
-    if not m or m.group(1) != csrc_hash():
+    m = re.search(rf"^\|\s*{re.escape(stage_key)}\s*\|[^|]*\|[^|]*\|[^|]*\|\s*([0-9.eE+]+)\s*\|"
+                  rf"\s*([0-9a-f]+)\s*\|", txt, re.M)
+    if not m or m.group(2) != csrc_hash(stage_sources(stage_key)):
         return None
-    m = re.search(rf"^\|\s*{re.escape(kernel_key)}\s*\|[^|]*\|[^|]*\|[^|]*\|\s*([0-9.eE+]+)\s*\|",
-                  txt, re.M)
-    return float(m.group(1)) if m else None
+    return float(m.group(1))
 
 
 def stage_work(net, name, li):

@@ -217,27 +217,29 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
     if (colsum) Vec<VEC>::store(colsum + col, acc);
 }
 
-// Bias gradient: db[f] = sum over b (and pooled positions p) of the per-column
-// time sums.  A block owns 64 consecutive features (one per lane); its four
-// waves take every fourth batch row, each lane summing in fp64 in a fixed
-// order, and the four partial sums are added in wave order.
-__global__ __launch_bounds__(kThreads) void bias_reduce_kernel(int B, int F, int P,
-                                                               const float *__restrict__ colsum,
-                                                               float *__restrict__ db) {
-    __shared__ double part[4][64];
+// Bias gradient: db[f] = sum over b of the per-column time sums.  A block
+// owns 64 consecutive features (one per lane); its 16 waves take every 16th
+// batch row, each lane summing in fp64 in a fixed order, and the 16 partial
+// sums are added in wave order.
+__global__ __launch_bounds__(1024) void bias_reduce_kernel(int B, int F,
+                                                           const float *__restrict__ colsum,
+                                                           float *__restrict__ db) {
+    __shared__ double part[16][64];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int f = blockIdx.x * 64 + lane;
-    const int64_t row = (int64_t)F * P;
     double acc = 0.0;
     if (f < F) {
-        const float *base = colsum + (int64_t)f * P;
-#pragma unroll 8
-        for (int b = wave; b < B; b += 4)
-            for (int p = 0; p < P; ++p) acc += (double)base[b * row + p];
+#pragma unroll 4
+        for (int b = wave; b < B; b += 16) acc += (double)colsum[(int64_t)b * F + f];
     }
     part[wave][lane] = acc;
     __syncthreads();
-    if (wave == 0 && f < F) db[f] = (float)(((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane]);
+    if (wave == 0 && f < F) {
+        double s = 0.0;
+#pragma unroll
+        for (int w = 0; w < 16; ++w) s += part[w][lane];
+        db[f] = (float)s;
+    }
 }
 
 // The same sum for layers with P > 1 positions per feature (conv channels):
@@ -352,7 +354,7 @@ hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s) {
 hipError_t launch_bias_reduce(int B, int F, int P, const float *colsum, float *db, hipStream_t s) {
     if (F <= 0) return hipSuccess;
     if (P > 1) bias_reduce_pos_kernel<<<F, kReduceThreads, 0, s>>>(B, F, P, colsum, db);
-    else bias_reduce_kernel<<<(F + 63) / 64, kThreads, 0, s>>>(B, F, P, colsum, db);
+    else bias_reduce_kernel<<<(F + 63) / 64, 1024, 0, s>>>(B, F, colsum, db);
     return hipGetLastError();
 }
 
