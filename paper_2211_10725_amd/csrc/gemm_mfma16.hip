@@ -390,10 +390,11 @@ __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_ke
 constexpr int kShapes = 4;
 constexpr int kShapeBM[kShapes] = {128, 128, 256, 128};
 constexpr int kShapeBN[kShapes] = {128, 64, 128, 256};
-// Relative time per unit of tile work (128x128 = 1), measured on MI355X for
-// the contractions of the dense benchmark layers: [multi-part single-stage
-// kernels, single-part two-stage kernels][shape].
-constexpr float kShapeCost[2][kShapes] = {{1.0f, 1.6f, 0.7f, 0.85f}, {1.0f, 1.3f, 1.2f, 1.2f}};
+// Relative time per unit of tile work (128x128 = 1), measured on MI355X with
+// every shape forced in turn on the contractions of the dense benchmark
+// layers: [multi-part single-stage kernels, single-part two-stage
+// kernels][shape].
+constexpr float kShapeCost[2][kShapes] = {{1.0f, 1.6f, 0.6f, 0.85f}, {1.0f, 1.3f, 1.2f, 1.2f}};
 constexpr int kMaxSlotsPerCu = 8;  // upper bound on resident 256-thread blocks
 
 struct Plan16 {
@@ -475,19 +476,6 @@ bool shape_allowed(int sh, const Kind &kd) {
     if (sh == 2) return parts_of(kd.sa) <= parts_of(kd.sb);
     if (sh == 3) return parts_of(kd.sb) <= parts_of(kd.sa);
     return true;
-}
-
-int device_cus() {
-    static std::atomic<int> cache[64];
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    int v = cache[dev].load(std::memory_order_relaxed);
-    if (v == 0) {
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
-            v = 256;
-        cache[dev].store(v, std::memory_order_relaxed);
-    }
-    return v;
 }
 
 // Resident 256-thread blocks per CU of one kernel instance (runtime query,

@@ -8,15 +8,19 @@
 // next D steps do not depend on the state, so each lane keeps a ring of D
 // prefetched steps in registers to keep enough HBM requests in flight while
 // the sequential recurrence runs.
+#include <atomic>
+
 #include "snn_internal.hpp"
 
 namespace snn {
 namespace {
 
 constexpr int kThreads = 256;
-// Lanes own 4 columns and prefetch 8 steps when there are enough columns to
-// fill the chip; otherwise 1 column and 16 steps, which gives 4x the waves
-// and halves the number of exposed memory round trips of the serial scan.
+// Lanes own 4 columns and prefetch 6 steps when there are enough columns to
+// fill the chip (on the 65536 x 64-column layer 6 sustained at least the
+// bandwidth of 8 in every measurement, with fewer registers); otherwise 1
+// column and 16 steps, which gives 4x the waves and halves the number of
+// exposed memory round trips of the serial scan.
 constexpr int kWideColumns = 4 * 64 * 2048;  // 2048 waves of 4-column lanes
 
 template <int VEC>
@@ -273,7 +277,7 @@ void fwd_launch(int T, int64_t C, float alpha, float beta, float thr, const floa
                 void *spk, float *u_out, float *counts, hipStream_t s) {
     const int64_t lanes = (C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_fwd_kernel<NEURON, VEC, OUT, VEC == 4 ? 8 : 16><<<grid, kThreads, 0, s>>>(T, C, alpha, beta, thr, cur,
+    neuron_fwd_kernel<NEURON, VEC, OUT, VEC == 4 ? 6 : 16><<<grid, kThreads, 0, s>>>(T, C, alpha, beta, thr, cur,
                                                                  spk, u_out, counts);
 }
 
@@ -282,7 +286,7 @@ void bwd_launch(int T, int64_t C, float alpha, float beta, float thr, float slop
                 const float *u, const float *g, void *dcur, float *colsum, hipStream_t s) {
     const int64_t lanes = (C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_bwd_kernel<NEURON, VEC, BCAST, RS, GT, VEC == 4 ? 8 : 16><<<grid, kThreads, 0, s>>>(
+    neuron_bwd_kernel<NEURON, VEC, BCAST, RS, GT, VEC == 4 ? 6 : 16><<<grid, kThreads, 0, s>>>(
         T, C, alpha, beta, thr, slope, u, g, dcur, colsum);
 }
 
@@ -349,6 +353,20 @@ hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     fill_zero_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, s>>>(p, n);
     return hipGetLastError();
+}
+
+int device_cus() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int v = cache[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            v <= 0)
+            v = 256;
+        cache[dev].store(v, std::memory_order_relaxed);
+    }
+    return v;
 }
 
 hipError_t launch_bias_reduce(int B, int F, int P, const float *colsum, float *db, hipStream_t s) {

@@ -41,6 +41,9 @@ inline size_t dtype_bytes(int dt) {
     }
 }
 
+// Compute units of the current device (cached per device).
+int device_cus();
+
 // ---- neuron scans (scan.hip) ---------------------------------------------
 // Forward: C = B * N independent columns, time-major [T, C].
 hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, float alpha, float beta, float thr,
