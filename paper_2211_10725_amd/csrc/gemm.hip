@@ -340,6 +340,10 @@ size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype, bool 
     probe.b_dtype = b_dtype;
     probe.a_kc = a_kc;
     probe.b_kc = b_kc;
+    probe.allow_split = allow_split;
+    probe.lda = a_kc ? K : M;  // densely packed operands (the callers' layouts)
+    probe.ldb = b_kc ? K : N;
+    if (gemm_async_applies(probe)) return gemm_async_workspace_bytes(probe);
     if (allow_split && gemm16_applies(probe)) return gemm16_workspace_bytes(probe);
     const Plan p = make_plan(M, N, K);
     if (p.splits <= 1) return 0;
@@ -352,6 +356,7 @@ hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t
         // empty contraction: C = bias (or 0)
         return hipErrorInvalidValue;
     }
+    if (gemm_async_applies(g)) return launch_gemm_async(g, ws, ws_bytes, s);
     if (g.allow_split && gemm16_applies(g)) return launch_gemm16(g, ws, ws_bytes, s);
     const Plan p = make_plan(g.M, g.N, g.K);
     float *out = g.C;

@@ -95,6 +95,11 @@ bool gemm16_applies(const GemmArgs &g);
 size_t gemm16_workspace_bytes(const GemmArgs &g);
 hipError_t launch_gemm16(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
 int gemm16_passes(const GemmArgs &g);  // MFMA passes per product, 0 if not applicable
+// ---- large single-part contractions, asynchronous LDS pipeline (gemm_async.hip)
+bool gemm_async_applies(const GemmArgs &g);
+size_t gemm_async_workspace_bytes(const GemmArgs &g);
+hipError_t launch_gemm_async(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
+
 // dst[c*ld_dst + r] = src[r*ld_src + c] for r < rows, c < cols; to_planes
 // writes an fp32 source as three bf16 planes `plane` elements apart.
 hipError_t launch_transpose(int rows, int cols, const void *src, int64_t ld_src, int elem_bytes,

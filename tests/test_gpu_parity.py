@@ -130,7 +130,9 @@ GEMM_SHAPES = [(37, 29, 53), (800, 1000, 784), (128, 10, 1000), (300, 7, 33), (6
 PATHS = {"split": 0, "fp32mfma": snn.FLAG_FP32_MFMA}
 
 
-@pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784)])
+# (1040, 1100, 1000): large enough for the 256 x 256 asynchronous kernel with
+# fp16 weights, ragged in M and N, and a last k-tile of 8 values
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784), (1040, 1100, 1000)])
 @pytest.mark.parametrize("wdt", ["f32", "f16"])
 @pytest.mark.parametrize("path", list(PATHS))
 def test_synapse_fwd(M, N, K, wdt, path):
@@ -181,7 +183,8 @@ GRAD_TYPES = {"f32": (snn.F32, torch.float32), "bf16": (snn.BF16, torch.bfloat16
               "f16": (snn.F16, torch.float16)}
 
 
-@pytest.mark.parametrize("M,N,K", [(300, 130, 77), (12800, 1000, 784), (2048, 512, 1024)])
+@pytest.mark.parametrize("M,N,K", [(300, 130, 77), (12800, 1000, 784), (2048, 512, 1024),
+                                   (1040, 1100, 1000)])
 @pytest.mark.parametrize("gdt", list(GRAD_TYPES))
 @pytest.mark.parametrize("wdt", ["f32", "f16"])
 def test_synapse_bwd_operand_types(M, N, K, gdt, wdt):
