@@ -341,12 +341,26 @@ def _contraction_kind(net, li, fp32_mfma):
     return "mfma16", 1       # fp16 weights: one fp16 pass
 
 
+def _async_contraction(net, li, fp32_mfma):
+    """Whether layer li's forward product runs on the asynchronous 256x256
+    kernel (mirrors gemm_async_applies in gemm_async.hip)."""
+    d = net.descs[li]
+    if fp32_mfma or d.synapse != 0:
+        return False
+    a, b = d.in_dtype, d.w_dtype
+    ok_type = (a in (3, 1) and b in (3, 1)) or (a in (3, 2) and b in (3, 2))
+    M, N, K = d.T * d.B, d.n_out, d.n_in
+    return ok_type and K % 8 == 0 and K >= 256 and M >= 256 and N >= 256 and M * N * K >= 2 ** 30
+
+
 def _stage_kernels(net, name, li, fp32_mfma):
     """Kernels a stage enqueues (matched against the rocprofv3 summary)."""
     if name == "neuron_fwd":
         return ": neuron_fwd_kernel"
     if name == "neuron_bwd":
         return ": neuron_bwd_kernel"
+    if name == "synapse_fwd" and _async_contraction(net, li, fp32_mfma):
+        return ": widen_kernel (spikes to fp16) + gemm_async_kernel"
     kind, passes = _contraction_kind(net, li, fp32_mfma)
     if net.descs[li].synapse == 1:
         g = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"

@@ -126,7 +126,8 @@ DwPlan dw_plan(const snn_layer_desc *d) {
     DwPlan p{};
     const int M = (int)rows(d);
     const GemmArgs kc = dw_probe_kc(d);
-    p.transposed = split_ok(d) && gemm16_applies(kc) &&
+    // a layer with few outputs reads its operands in their own layouts
+    p.transposed = split_ok(d) && gemm16_applies(kc) && d->n_out > 16 &&
                    2.0 * M * d->n_in * d->n_out >= kTransposeFlops;
     if (p.transposed) {
         p.a_dtype = kc.a_dtype;
@@ -153,7 +154,8 @@ DxPlan dx_plan(const snn_layer_desc *d) {
     kc.M = M; kc.N = d->n_in; kc.K = d->n_out;
     kc.a_dtype = d->grad_dtype; kc.a_kc = true;
     kc.b_dtype = d->w_dtype; kc.b_kc = true;
-    p.transposed = split_ok(d) && gemm16_applies(kc) &&
+    // a layer with few outputs (short contraction) reads W in its own layout
+    p.transposed = split_ok(d) && gemm16_applies(kc) && d->n_out > 16 &&
                    2.0 * M * d->n_in * d->n_out >= kTransposeFlops;
     if (p.transposed) {
         p.wt_bytes = align_up((size_t)d->n_in * d->n_out * dtype_bytes(d->w_dtype));

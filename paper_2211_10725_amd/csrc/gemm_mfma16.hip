@@ -639,9 +639,12 @@ hipError_t dispatch16(const GemmArgs &g, const Kind &kd, void *ws, size_t ws_byt
 }  // namespace
 
 bool gemm16_applies(const GemmArgs &g) {
-    if (g.M < 64 || g.N < 64) return false;
+    if (g.M < 1 || g.N < 1) return false;
     const Kind kd = classify(g.a_dtype, g.b_dtype);
     if (!kd.ok) return false;
+    // a side below 64 wastes most of a tile: worth it only for one-pass pairs
+    // (measured: fp32 x spikes skinny products are faster on the fp32 kernels)
+    if ((g.M < 64 || g.N < 64) && parts_of(kd.sa) * parts_of(kd.sb) > 1) return false;
     bool sup = false;
     dispatch16(g, kd, nullptr, 0, nullptr, false, &sup);
     return sup;

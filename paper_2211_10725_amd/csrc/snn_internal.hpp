@@ -95,6 +95,15 @@ bool gemm16_applies(const GemmArgs &g);
 size_t gemm16_workspace_bytes(const GemmArgs &g);
 hipError_t launch_gemm16(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
 int gemm16_passes(const GemmArgs &g);  // MFMA passes per product, 0 if not applicable
+// ---- contractions of layers with few outputs (skinny.hip) --------------------
+// short contraction: K <= 16, A K-contiguous, B N-contiguous
+bool short_k_applies(const GemmArgs &g);
+hipError_t launch_short_k(const GemmArgs &g, hipStream_t s);
+// few rows: M <= 16, A and B M/N-contiguous (the weight gradient of such a layer)
+bool few_rows_applies(const GemmArgs &g);
+size_t few_rows_workspace_bytes(const GemmArgs &g);
+hipError_t launch_few_rows(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
+
 // ---- large single-part contractions, asynchronous LDS pipeline (gemm_async.hip)
 bool gemm_async_applies(const GemmArgs &g);
 size_t gemm_async_workspace_bytes(const GemmArgs &g);
