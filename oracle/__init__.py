@@ -13,6 +13,7 @@ reverse).  Every function names the passage of the paper it follows:
 * eq. (3)  Heaviside spike, strict ``u > thr``;
 * eq. (4)  Leaky neuron with reset by subtraction;
 * eqs. (5)-(6) current-based ("Synaptic") neuron;
+* eq. (7)  recurrent leaky neuron ("RLeaky", one recurrent weight per neuron);
 * eqs. (8)-(9) fast-sigmoid surrogate for the spike's derivative;
 * Sec. III-C / Table I  dense 784-1000-10 and conv 5C12-MP2-5C64-MP2-10 nets;
 * Sec. V  rate-coded readout (class = output neuron with the most spikes).
@@ -36,8 +37,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "snn_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-LEAKY, SYNAPTIC = 0, 1
-NEURONS = {"leaky": LEAKY, "synaptic": SYNAPTIC}
+LEAKY, SYNAPTIC, RLEAKY = 0, 1, 2
+NEURONS = {"leaky": LEAKY, "synaptic": SYNAPTIC, "rleaky": RLEAKY}
 
 
 def build(verbose: bool = False) -> str:
@@ -71,6 +72,10 @@ def lib():
         L.orc_scan_fwd.argtypes = [i32, i64, i64, flt, flt, flt, P, P, P, P]
         L.orc_scan_fwd_smooth.argtypes = [i32, i64, i64, dbl, dbl, dbl, dbl, i32, P, P, P, P]
         L.orc_scan_bwd.argtypes = [i32, i64, i64, dbl, dbl, dbl, dbl, dbl, i32, P, P, i32, P]
+        L.orc_scan_fwd_rleaky.argtypes = [i64, i64, i64, flt, flt, P, P, P, P, P]
+        L.orc_scan_fwd_smooth_rleaky.argtypes = [i64, i64, i64, dbl, dbl, dbl, i32, P, P, P, P, P]
+        L.orc_scan_bwd_rleaky.argtypes = [i64, i64, i64, dbl, dbl, dbl, dbl, i32, i32, P, P, P,
+                                          i32, P, P]
         L.orc_loss_ce.argtypes = [i64, i64, P, P, P]
         L.orc_loss_ce.restype = dbl
         L.orc_loss_mse.argtypes = [i64, i64, P, P, P]
@@ -165,8 +170,16 @@ def maxpool2_bwd(dy, arg, H, W_):
     return dx
 
 
-def scan_fwd(I, neuron, beta, thr=1.0, alpha=0.0):
-    """fp32 neuron scan (eqs. 3-6).  I [T, ...] fp32 currents, time-major.
+def _rec_weights(v, C, dtype):
+    """Recurrent weights of eq. (7), one per neuron; column c is neuron c % N."""
+    v = np.ascontiguousarray(np.ravel(v), dtype=dtype)
+    assert v.size >= 1 and C % v.size == 0, (v.size, C)
+    return v
+
+
+def scan_fwd(I, neuron, beta, thr=1.0, alpha=0.0, v=None):
+    """fp32 neuron scan (eqs. 3-7).  I [T, ...] fp32 currents, time-major; v
+    the recurrent weights [N] of the 'rleaky' neuron (N = last dim of I).
     Returns (z uint8, u fp32, counts fp32 [...])."""
     I = np.ascontiguousarray(I, dtype=np.float32)
     T = I.shape[0]
@@ -174,12 +187,18 @@ def scan_fwd(I, neuron, beta, thr=1.0, alpha=0.0):
     z = np.empty(I.shape, np.uint8)
     u = np.empty(I.shape, np.float32)
     cnt = np.empty(I.shape[1:], np.float32)
-    lib().orc_scan_fwd(NEURONS.get(neuron, neuron), T, C, float(alpha), float(beta),
-                       float(thr), _p(I), _p(z), _p(u), _p(cnt))
+    nt = NEURONS.get(neuron, neuron)
+    if nt == RLEAKY:
+        v = _rec_weights(v, C, np.float32)
+        lib().orc_scan_fwd_rleaky(T, C, v.size, float(beta), float(thr), _p(v), _p(I), _p(z),
+                                  _p(u), _p(cnt))
+    else:
+        lib().orc_scan_fwd(nt, T, C, float(alpha), float(beta), float(thr), _p(I), _p(z), _p(u),
+                           _p(cnt))
     return z, u, cnt
 
 
-def scan_fwd_smooth(I, neuron, beta, thr, slope, alpha=0.0, reset_surrogate=False):
+def scan_fwd_smooth(I, neuron, beta, thr, slope, alpha=0.0, reset_surrogate=False, v=None):
     """Double-precision smooth scan for finite differences (not the method)."""
     I = _f64(I)
     T = I.shape[0]
@@ -187,8 +206,15 @@ def scan_fwd_smooth(I, neuron, beta, thr, slope, alpha=0.0, reset_surrogate=Fals
     z = np.empty(I.shape)
     u = np.empty(I.shape)
     cnt = np.empty(I.shape[1:])
-    lib().orc_scan_fwd_smooth(NEURONS.get(neuron, neuron), T, C, alpha, beta, thr, slope,
-                              int(bool(reset_surrogate)), _p(I), _p(z), _p(u), _p(cnt))
+    nt = NEURONS.get(neuron, neuron)
+    if nt == RLEAKY:
+        v = _rec_weights(v, C, np.float64)
+        lib().orc_scan_fwd_smooth_rleaky(T, C, v.size, beta, thr, slope,
+                                         int(bool(reset_surrogate)), _p(v), _p(I), _p(z),
+                                         _p(u), _p(cnt))
+    else:
+        lib().orc_scan_fwd_smooth(nt, T, C, alpha, beta, thr, slope, int(bool(reset_surrogate)),
+                                  _p(I), _p(z), _p(u), _p(cnt))
     return z, u, cnt
 
 
@@ -208,6 +234,26 @@ def scan_bwd(u, g, neuron, beta, thr=1.0, slope=25.0, alpha=0.0,
     lib().orc_scan_bwd(NEURONS.get(neuron, neuron), T, C, alpha, beta, thr, slope, s_scale,
                        int(bool(reset_surrogate)), _p(u), _p(g), bcast, _p(dI))
     return dI
+
+
+def scan_bwd_rleaky(u, g, beta, thr, slope, v, reset_surrogate=False, s_scale=1.0,
+                    smooth_z=False):
+    """BPTT through the recurrent neuron of eq. (7).  Returns (dL/dI [T, ...],
+    dL/dv [N]) in double; dL/dv sums the columns of each neuron."""
+    u = _f64(u)
+    T = u.shape[0]
+    C = int(np.prod(u.shape[1:]))
+    g = _f64(g)
+    bcast = 1 if g.shape == u.shape[1:] else 0
+    if not bcast:
+        assert g.shape == u.shape
+    v = _rec_weights(v, C, np.float64)
+    dI = np.empty(u.shape)
+    dv_col = np.empty(C)
+    lib().orc_scan_bwd_rleaky(T, C, v.size, beta, thr, slope, s_scale, int(bool(reset_surrogate)),
+                              int(bool(smooth_z)), _p(v), _p(u), _p(g), bcast, _p(dI),
+                              _p(dv_col))
+    return dI, dv_col.reshape(-1, v.size).sum(axis=0)
 
 
 def loss_ce(counts, labels):
@@ -246,10 +292,12 @@ def _layer_out_shape(spec):
     raise ValueError(spec["kind"])
 
 
-def layer_fwd(spec, x, W=None, b=None, smooth=False, slope=25.0, reset_surrogate=False):
+def layer_fwd(spec, x, W=None, b=None, smooth=False, slope=25.0, reset_surrogate=False,
+              v=None):
     """One spiking layer forward.  ``spec`` is a plain dict:
-    kind ('dense' | 'conv' | 'none'), sizes, neuron ('leaky'|'synaptic'),
-    beta, alpha, thr.  x is [T, B, ...] (spikes as 0/1 or currents).
+    kind ('dense' | 'conv' | 'none'), sizes, neuron ('leaky'|'synaptic'|'rleaky'),
+    beta, alpha, thr; v the recurrent weights of an 'rleaky' layer.  x is
+    [T, B, ...] (spikes as 0/1 or currents).
     Method mode: currents are rounded to fp32 and the scan runs in fp32.
     Smooth mode: everything in double with the smooth spike."""
     T, B = x.shape[:2]
@@ -272,25 +320,32 @@ def layer_fwd(spec, x, W=None, b=None, smooth=False, slope=25.0, reset_surrogate
     nt = spec["neuron"]
     if smooth:
         z, u, cnt = scan_fwd_smooth(I, nt, spec["beta"], spec["thr"], slope,
-                                    spec.get("alpha", 0.0), reset_surrogate)
+                                    spec.get("alpha", 0.0), reset_surrogate, v=v)
         out.update(I=I, z=z, u=u, counts=cnt)
     else:
         I32 = np.asarray(I, np.float32)
-        z, u, cnt = scan_fwd(I32, nt, spec["beta"], spec["thr"], spec.get("alpha", 0.0))
+        z, u, cnt = scan_fwd(I32, nt, spec["beta"], spec["thr"], spec.get("alpha", 0.0), v=v)
         out.update(I=I32, z=z, u=u, counts=cnt)
     return out
 
 
 def layer_bwd(spec, fwd, g, W=None, slope=25.0, reset_surrogate=False, s_scale=1.0,
-              want_dx=True):
+              want_dx=True, v=None, smooth=False):
     """One spiking layer backward.  g = dL/dz of this layer's output spikes,
     [T, B, ...] or [B, ...] (broadcast over t).  Returns dict with dI and the
-    parameter / input gradients (double)."""
+    parameter / input gradients (double); 'dv' for an 'rleaky' layer.  smooth:
+    the forward was the smooth one, so z_{t-1} in dL/dv is the smooth spike."""
     u = fwd["u"]
     T, B = u.shape[:2]
-    dI = scan_bwd(u, g, spec["neuron"], spec["beta"], spec["thr"], slope,
-                  spec.get("alpha", 0.0), reset_surrogate, s_scale)
-    res = {"dI": dI}
+    res = {}
+    if spec["neuron"] == "rleaky":
+        dI, dv = scan_bwd_rleaky(u, g, spec["beta"], spec["thr"], slope, v, reset_surrogate,
+                                 s_scale, smooth_z=smooth)
+        res["dv"] = dv
+    else:
+        dI = scan_bwd(u, g, spec["neuron"], spec["beta"], spec["thr"], slope,
+                      spec.get("alpha", 0.0), reset_surrogate, s_scale)
+    res["dI"] = dI
     x = fwd["x"]
     if spec["kind"] == "dense":
         dW, db, dx = dense_bwd(dI.reshape(T * B, -1), np.reshape(x, (T * B, -1)), W,
@@ -311,15 +366,18 @@ def net_step(layers, params, x, loss="ce", labels=None, targets=None, smooth=Fal
              slope=25.0, reset_surrogate=False):
     """One forward + BPTT step of a feed-forward spiking network.
 
-    layers: list of layer spec dicts; params: list of (W, b) (None for 'none');
-    x: [T, B, ...] input.  The loss is taken on the last layer's spike counts
+    layers: list of layer spec dicts; params: list of (W, b) (None for 'none'),
+    or (W, b, v) for an 'rleaky' layer; x: [T, B, ...] input.  The loss is
+    taken on the last layer's spike counts
     summed over T.  Returns (loss, per-layer forward dicts, per-layer backward
     dicts)."""
     fwds = []
     h = x
-    for spec, (W, b) in zip(layers, params):
+    for spec, prm in zip(layers, params):
+        W, b = prm[0], prm[1]
+        v = prm[2] if len(prm) > 2 else None
         f = layer_fwd(spec, h, W, b, smooth=smooth, slope=slope,
-                      reset_surrogate=reset_surrogate)
+                      reset_surrogate=reset_surrogate, v=v)
         fwds.append(f)
         h = f["z"]
     counts = fwds[-1]["counts"]
@@ -334,8 +392,9 @@ def net_step(layers, params, x, loss="ce", labels=None, targets=None, smooth=Fal
     for li in range(len(layers) - 1, -1, -1):
         spec = layers[li]
         W = params[li][0]
+        v = params[li][2] if len(params[li]) > 2 else None
         r = layer_bwd(spec, fwds[li], g, W, slope, reset_surrogate, s_scale,
-                      want_dx=(li > 0) or spec["kind"] == "none")
+                      want_dx=(li > 0) or spec["kind"] == "none", v=v, smooth=smooth)
         bwds[li] = r
         g = r["dx"]
     return L, fwds, bwds

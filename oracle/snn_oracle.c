@@ -361,6 +361,107 @@ void orc_scan_bwd(int neuron, int64_t T, int64_t C, double alpha, double beta,
 }
 
 /* ------------------------------------------------------------------------
+ * Recurrent leaky integrate-and-fire neuron, eq. (7): the neuron's own
+ * previous spike, weighted by the recurrent weight v, joins the input:
+ *     u_t = beta*u_{t-1} + I_t + z_{t-1} * (v - thr)
+ * One recurrent weight per neuron; column c of [T, C] (C = B*N, neuron
+ * fastest) is neuron c % N.  fp32, op order of eq. (7) read left to right:
+ * the decay-plus-input term is one fused multiply-add, then (v - thr), rounded
+ * once to fp32, is added if the previous step spiked.  v = 0 gives eq. (4).
+ * ---------------------------------------------------------------------- */
+void orc_scan_fwd_rleaky(int64_t T, int64_t C, int64_t N, float beta, float thr,
+                         const float *v, const float *I, uint8_t *z_out,
+                         float *u_out, float *counts)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t c = 0; c < C; ++c) {
+        const float jump = v[c % N] - thr;
+        float u = 0.0f;
+        int zprev = 0, cnt = 0;
+        for (int64_t t = 0; t < T; ++t) {
+            u = fmaf(beta, u, I[t * C + c]);
+            if (zprev)
+                u = u + jump;
+            const int z = (u > thr) ? 1 : 0;
+            if (z_out)
+                z_out[t * C + c] = (uint8_t)z;
+            if (u_out)
+                u_out[t * C + c] = u;
+            cnt += z;
+            zprev = z;
+        }
+        if (counts)
+            counts[c] = (float)cnt;
+    }
+}
+
+/* Smooth version in double for finite differences (not the method): the
+ * spike is S(u - thr) as in orc_scan_fwd_smooth; the recurrent term uses the
+ * smooth spike v * S(u_{t-1} - thr), the reset term thr * S(u_{t-1} - thr)
+ * when reset_surrogate != 0, else thr * H(u_{t-1} - thr) (detached). */
+void orc_scan_fwd_smooth_rleaky(int64_t T, int64_t C, int64_t N, double beta,
+                                double thr, double slope, int reset_surrogate,
+                                const double *v, const double *I, double *z_out,
+                                double *u_out, double *counts)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t c = 0; c < C; ++c) {
+        const double vc = v[c % N];
+        double u = 0.0, zprev = 0.0, rprev = 0.0, cnt = 0.0;
+        for (int64_t t = 0; t < T; ++t) {
+            u = beta * u + I[t * C + c] + vc * zprev - thr * rprev;
+            const double d = u - thr;
+            const double z = 0.5 * (1.0 + slope * d / (1.0 + slope * fabs(d)));
+            zprev = z;
+            rprev = reset_surrogate ? z : (d > 0.0 ? 1.0 : 0.0);
+            if (z_out)
+                z_out[t * C + c] = z;
+            if (u_out)
+                u_out[t * C + c] = u;
+            cnt += z;
+        }
+        if (counts)
+            counts[c] = cnt;
+    }
+}
+
+/* BPTT through eq. (7), double.  s_t = s_scale / (1 + k|u_t - thr|)^2 as in
+ * orc_scan_bwd; the spike z_t reaches u_{t+1} through (v - r*thr), so
+ *     lam_t = g_t s_t + (beta + (v - r*thr) s_t) * lam_{t+1},   dI_t = lam_t,
+ * and the recurrent weight collects dv_col[c] = sum_{t>=1} lam_t z_{t-1}
+ * (per column; the caller sums the columns of each neuron).  z_{t-1} is the
+ * method's spike H(u_{t-1} - thr), or S(u_{t-1} - thr) when smooth_z != 0 (the
+ * smooth forward above). */
+void orc_scan_bwd_rleaky(int64_t T, int64_t C, int64_t N, double beta, double thr,
+                         double slope, double s_scale, int reset_surrogate,
+                         int smooth_z, const double *v, const double *u,
+                         const double *g, int g_bcast, double *dI, double *dv_col)
+{
+#pragma omp parallel for schedule(static)
+    for (int64_t c = 0; c < C; ++c) {
+        const double vc = v[c % N];
+        double lam = 0.0, dv = 0.0;
+        for (int64_t t = T - 1; t >= 0; --t) {
+            const double e = u[t * C + c] - thr;
+            const double d = 1.0 + slope * fabs(e);
+            const double s = s_scale / (d * d);
+            const double gt = g_bcast ? g[c] : g[t * C + c];
+            lam = gt * s + (beta + (vc - (reset_surrogate ? thr : 0.0)) * s) * lam;
+            dI[t * C + c] = lam;
+            if (t > 0) {
+                const double ep = u[(t - 1) * C + c] - thr;
+                const double zp = smooth_z
+                    ? 0.5 * (1.0 + slope * ep / (1.0 + slope * fabs(ep)))
+                    : (ep > 0.0 ? 1.0 : 0.0);
+                dv += lam * zp;
+            }
+        }
+        if (dv_col)
+            dv_col[c] = dv;
+    }
+}
+
+/* ------------------------------------------------------------------------
  * Rate-coded readout loss on output spike counts (the predicted class is the
  * output neuron with the most spikes, Sec. V).  Cross-entropy with the raw
  * counts as logits, mean over the batch:

@@ -336,16 +336,18 @@ def _fd_check(layers, params, x, labels, reset_surrogate, slope=25.0, eps=1e-6):
 
     def loss_of(ps):
         h = x
-        for spec, (W, b) in zip(layers, ps):
-            f = oracle.layer_fwd(spec, h, W, b, smooth=True, slope=slope,
-                                 reset_surrogate=reset_surrogate)
+        for spec, prm in zip(layers, ps):
+            f = oracle.layer_fwd(spec, h, prm[0], prm[1], smooth=True, slope=slope,
+                                 reset_surrogate=reset_surrogate,
+                                 v=prm[2] if len(prm) > 2 else None)
             h = f["z"]
         B = x.shape[1]
         return oracle.loss_ce(f["counts"].reshape(B, -1), labels)[0]
 
     worst = 0.0
     for li in range(len(params)):
-        for pi, grad in ((0, bwds[li]["dW"]), (1, bwds[li]["db"])):
+        names = ("dW", "db", "dv")[:len(params[li])]
+        for pi, grad in enumerate(bwds[li][k] for k in names):
             P = params[li][pi]
             flat = P.reshape(-1)          # a view: edits change params in place
             fd = np.zeros(P.size)
@@ -402,3 +404,112 @@ def test_finite_differences_conv(reset_surrogate):
         if _fd_check(layers, params, x, y, reset_surrogate) is not None:
             return
     pytest.fail("no seed with clear pool winners and reset margins")
+
+
+# ---------------------------------------------------------------------------
+# P6: recurrent leaky neuron (eq. 7), one recurrent weight per neuron
+# ---------------------------------------------------------------------------
+_RL = _golden("hand_rleaky_t4.json")
+_RL_TRACES = {t["name"]: t for t in _RL["traces"]}
+
+
+@pytest.mark.parametrize("tr", _RL["traces"], ids=lambda t: t["name"])
+def test_rleaky_hand_traces(tr):
+    I = np.array(tr["I"], np.float32).reshape(4, 1)
+    z, u, cnt = oracle.scan_fwd(I, "rleaky", tr["beta"], tr["thr"], v=[tr["v"]])
+    np.testing.assert_array_equal(u[:, 0], np.array(tr["u"], np.float32))
+    np.testing.assert_array_equal(z[:, 0], tr["z"])
+    assert cnt[0] == sum(tr["z"])
+
+
+@pytest.mark.parametrize("case", _RL["gradients"], ids=lambda c: c["name"])
+def test_rleaky_hand_gradients(case):
+    tr = _RL_TRACES[case["trace"]]
+    u = np.array(tr["u"]).reshape(4, 1)
+    g = np.array(case["g"], np.float64).reshape(4, 1)
+    dI, dv = oracle.scan_bwd_rleaky(u, g, tr["beta"], tr["thr"], case["slope"], [tr["v"]],
+                                    case["reset_surrogate"])
+    want = np.array([float(Fraction(q)) for q in case["dI"]])
+    np.testing.assert_allclose(dI[:, 0], want, rtol=1e-14, atol=1e-15)
+    assert abs(dv[0] - float(Fraction(case["dv"]))) <= 1e-14
+
+
+def _rand_currents(seed, T=40, B=3, N=7):
+    rng = np.random.default_rng(seed)
+    return rng.normal(0.4, 0.8, (T, B, N)).astype(np.float32), rng
+
+
+def test_rleaky_zero_weight_is_leaky():
+    """v = 0 leaves only the reset of eq. (4): same spikes and membrane bit for bit,
+    and the same BPTT gradients for either reading of the reset."""
+    I, rng = _rand_currents(11)
+    v = np.zeros(I.shape[-1], np.float32)
+    zr, ur, cr = oracle.scan_fwd(I, "rleaky", 0.9, 1.0, v=v)
+    zl, ul, cl = oracle.scan_fwd(I, "leaky", 0.9, 1.0)
+    np.testing.assert_array_equal(zr, zl)
+    np.testing.assert_array_equal(ur, ul)
+    np.testing.assert_array_equal(cr, cl)
+    assert zr.any() and not zr.all()
+    g = rng.normal(0, 1, I.shape)
+    for rs in (False, True):
+        dr, _ = oracle.scan_bwd_rleaky(ur, g, 0.9, 1.0, 25.0, v, rs)
+        dl = oracle.scan_bwd(ul, g, "leaky", 0.9, 1.0, 25.0, 0.0, rs)
+        np.testing.assert_allclose(dr, dl, rtol=1e-13, atol=1e-300)
+
+
+def test_rleaky_threshold_weight_is_integrator():
+    """v = thr cancels the reset: u_t = sum_j beta^(t-j) I_j, the plain linear
+    recurrence (computed here as a triangular matrix product in float64).  With
+    beta = 1/2 and currents on a coarse dyadic grid the fp32 scan is exact."""
+    T, C = 24, 64
+    rng = np.random.default_rng(5)
+    I = (rng.integers(-16, 48, (T, C)) / 16.0).astype(np.float32)
+    z, u, _ = oracle.scan_fwd(I, "rleaky", 0.5, 1.0, v=np.ones(C, np.float32))
+    t = np.arange(T)
+    Lmat = np.where(t[:, None] >= t[None, :], 0.5 ** (t[:, None] - t[None, :]).clip(0), 0.0)
+    np.testing.assert_allclose(u, Lmat @ I.astype(np.float64), rtol=1e-6, atol=1e-6)
+    np.testing.assert_array_equal(z, (Lmat @ I.astype(np.float64)) > 1.0)
+    assert z.any()
+    # backward: with the reset-through-surrogate reading the carry is exactly beta,
+    # the detached Leaky recursion; dL/dv is then sum_{t>=1} lam_t z_{t-1}
+    g = rng.normal(0, 1, (T, C))
+    dr, dv = oracle.scan_bwd_rleaky(u, g, 0.5, 1.0, 25.0, np.ones(C), True)
+    dl = oracle.scan_bwd(u, g, "leaky", 0.5, 1.0, 25.0, 0.0, False)
+    np.testing.assert_allclose(dr, dl, rtol=1e-13)
+    np.testing.assert_allclose(dv, (dl[1:] * z[:-1]).sum(axis=0), rtol=1e-12)
+
+
+def test_rleaky_weight_shared_across_batch():
+    """Column c is neuron c % N: the batch rows use the same v and dL/dv sums them."""
+    I, rng = _rand_currents(12)
+    T, B, N = I.shape
+    v = rng.uniform(-1, 1.5, N).astype(np.float32)
+    z, u, _ = oracle.scan_fwd(I, "rleaky", 0.85, 1.0, v=v)
+    g = rng.normal(0, 1, (B, N))
+    dI, dv = oracle.scan_bwd_rleaky(u, g, 0.85, 1.0, 25.0, v)
+    for b in range(B):
+        zb, ub, _ = oracle.scan_fwd(I[:, b], "rleaky", 0.85, 1.0, v=v)
+        np.testing.assert_array_equal(zb, z[:, b])
+        np.testing.assert_array_equal(ub, u[:, b])
+    parts = [oracle.scan_bwd_rleaky(u[:, b], g[b], 0.85, 1.0, 25.0, v)[1] for b in range(B)]
+    np.testing.assert_allclose(dv, np.sum(parts, axis=0), rtol=1e-12)
+
+
+@pytest.mark.parametrize("reset_surrogate", [False, True])
+def test_finite_differences_rleaky(reset_surrogate):
+    """Smooth dense 3-4-2 net with recurrent hidden and output layers: dW, db and
+    the recurrent weights' gradient dv against central differences."""
+    T, B = 6, 2
+    for seed in range(50):
+        rng = np.random.default_rng(500 + seed)
+        layers = [dict(kind="dense", n_in=3, n_out=4, neuron="rleaky", beta=0.8, thr=1.0),
+                  dict(kind="dense", n_in=4, n_out=2, neuron="rleaky", beta=0.8, thr=1.0)]
+        params = [(rng.uniform(-1, 1.5, (4, 3)), rng.uniform(-0.2, 0.8, 4),
+                   rng.uniform(-0.8, 1.2, 4)),
+                  (rng.uniform(-1, 1.5, (2, 4)), rng.uniform(-0.2, 0.8, 2),
+                   rng.uniform(-0.8, 1.2, 2))]
+        x = (rng.random((T, B, 3)) < 0.6).astype(np.float64)
+        y = rng.integers(0, 2, B)
+        if _fd_check(layers, params, x, y, reset_surrogate) is not None:
+            return
+    pytest.fail("no seed with a reset margin above 1e-4")
