@@ -36,7 +36,8 @@ PEAK_FP16_MFMA_TFLOPS = 2500.0
 # kernel sources behind each kind of stage (a stored counter profile of a
 # stage stays valid while these files are unchanged)
 STAGE_SOURCES = {
-    "synapse": ["snn_internal.hpp", "gemm.hip", "gemm_mfma16.hip", "conv.hip"],
+    "synapse": ["snn_internal.hpp", "gemm.hip", "gemm_mfma16.hip", "gemm_async.hip", "skinny.hip",
+                "conv.hip"],
     "neuron": ["snn_internal.hpp", "scan.hip"],
 }
 
@@ -76,7 +77,8 @@ def stage_work(net, name, li):
       forward scan 4 B read current + 4 B write membrane + 1 B write spike per
                    (t, b, n), + 4 B count per (b, n)
       reverse scan 4 B read membrane + 4 B read dL/dz (full only) + 4 B write
-                   dL/dI per (t, b, n), + 4 B colsum per (b, n)."""
+                   dL/dI per (t, b, n), + 4 B colsum per (b, n), + 4 B recurrent-
+                   weight column sum per (b, n) for recurrent neurons (eq. 7)."""
     d = net.descs[li]
     TB = d.T * d.B
     if d.synapse == 1:
@@ -94,7 +96,8 @@ def stage_work(net, name, li):
         return "byte", 9.0 * el + 4.0 * cols
     if name == "neuron_bwd":
         full = li < len(net.descs) - 1
-        return "byte", (12.0 if full else 8.0) * el + 4.0 * cols
+        rec = 4.0 * cols if d.neuron == 2 else 0.0
+        return "byte", (12.0 if full else 8.0) * el + 4.0 * cols + rec
     return None, 0.0
 
 

@@ -10,14 +10,18 @@
  *   neuron    Leaky (eq. 4):  u_t = beta u_{t-1} + I_t - z_{t-1} thr
  *             Synaptic (eqs. 5-6): i_t = alpha i_{t-1} + I_t,
  *                                  u_t = beta u_{t-1} + i_t - z_{t-1} thr
+ *             RLeaky (eq. 7): u_t = beta u_{t-1} + I_t + z_{t-1} (v - thr),
+ *                             one recurrent weight v per neuron
  *             spike (eq. 3): z_t = 1 if u_t > thr (strict), else 0;
  *             initial state u = i = 0, no spike before the first step
  *   backward  the spike's derivative is replaced by the fast-sigmoid
  *             surrogate of eqs. (8)-(9) with slope k:
  *                 s_t = 1 / (1 + k |u_t - thr|)^2
  *             lam_t = g_t s_t + (beta - r thr s_t) lam_{t+1}  (r = 1 only for
- *             SNN_RESET_SURROGATE); Synaptic adds lami_t = lam_t + alpha lami_{t+1}.
- *             dL/dI_t = lam_t (Leaky) or lami_t (Synaptic), then
+ *             SNN_RESET_SURROGATE); Synaptic adds lami_t = lam_t + alpha lami_{t+1};
+ *             RLeaky carries (beta + (v - r thr) s_t) lam_{t+1} and
+ *             dL/dv = sum over t >= 1 and the batch of lam_t z_{t-1}.
+ *             dL/dI_t = lam_t (Leaky, RLeaky) or lami_t (Synaptic), then
  *             dW = dI^T x, dbias = sum dI, dx = dI W.
  *   loss      on output spike counts c = sum_t z_t (rate-coded readout, the
  *             class is the neuron with most spikes, Sec. V): cross-entropy
@@ -43,7 +47,8 @@
  *     unless SNN_FLAG_FP32_MFMA is set; fp32 x fp32 runs on fp32 MFMA.
  *     Neuron state is fp32; loss reductions in fp64.
  *   - T == 0 or B == 0 is valid: no compute is launched, and outputs that
- *     are sums over an empty range (counts, grad_w, grad_b) are set to 0.
+ *     are sums over an empty range (counts, grad_w, grad_b, grad_v) are set
+ *     to 0.
  *     A loss over B == 0 or K == 0 is rejected (SNN_ERR_SHAPE).
  */
 #ifndef SNN_H
@@ -58,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 1
+#define SNN_ABI_VERSION 2
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -80,6 +85,8 @@ typedef enum snn_status {
 /* neuron models */
 #define SNN_LEAKY 0    /* eq. (4) */
 #define SNN_SYNAPTIC 1 /* eqs. (5)-(6) */
+#define SNN_RLEAKY 2   /* eq. (7): Leaky plus the neuron's own previous spike
+                          through a recurrent weight v, one per neuron */
 
 /* synapse kinds */
 #define SNN_SYN_DENSE 0       /* x [T,B,n_in], w [n_out, n_in] */
@@ -111,7 +118,7 @@ typedef enum snn_status {
 typedef struct snn_layer_desc {
     int32_t T, B;           /* time steps, batch */
     int32_t synapse;        /* SNN_SYN_* */
-    int32_t neuron;         /* SNN_LEAKY | SNN_SYNAPTIC */
+    int32_t neuron;         /* SNN_LEAKY | SNN_SYNAPTIC | SNN_RLEAKY */
     int32_t n_in, n_out;    /* features per (t,b) of x and of the output;
                                conv: c_in*h_in*w_in and c_out*hp*wp;
                                SNN_SYN_NONE: n_in == n_out */
@@ -124,7 +131,7 @@ typedef struct snn_layer_desc {
     int32_t reset_grad;     /* SNN_RESET_DETACHED | SNN_RESET_SURROGATE */
     int32_t flags;          /* 0 or SNN_FLAG_FP32_MFMA */
     float beta;             /* membrane decay, eqs. (4)/(6) */
-    float alpha;            /* synaptic decay, eq. (5); ignored for Leaky */
+    float alpha;            /* synaptic decay, eq. (5); ignored for Leaky, RLeaky */
     float threshold;        /* u_thr */
     float slope;            /* surrogate slope k (k = 1 is eq. (9) as printed) */
 } snn_layer_desc;
@@ -152,24 +159,30 @@ size_t snn_layer_workspace_bytes(const snn_layer_desc *d);
  *   x       [T,B,n_in] of d->in_dtype
  *   w       weights of d->w_dtype (NULL iff SNN_SYN_NONE)
  *   bias    fp32 [n_out] dense / [c_out] conv, or NULL for no bias
+ *   v       fp32 [n_out] recurrent weights of SNN_RLEAKY (one per output
+ *           neuron, the same for every sample); required for SNN_RLEAKY
+ *           (SNN_ERR_NULL), ignored for the other neurons
  *   spk_out [T,B,n_out] spikes of d->out_dtype
  *   saved   snn_layer_saved_bytes(d) bytes, kept for snn_layer_bwd
  *   counts  fp32 [B,n_out] spike counts sum_t z_t, or NULL
  *   ws      snn_layer_workspace_bytes(d) bytes (may be NULL if 0) */
 snn_status snn_layer_fwd(const snn_layer_desc *d, const void *x, const void *w,
-                         const float *bias, void *spk_out, void *saved, float *counts,
-                         void *ws, size_t ws_bytes, hipStream_t stream);
+                         const float *bias, const float *v, void *spk_out, void *saved,
+                         float *counts, void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Backward of one layer (reverse-time neuron scan, then the synapse).
  *   grad    upstream dL/dz of this layer's spikes
- *   x, w    the forward's inputs; saved: the forward's saved state
+ *   x, w, v the forward's inputs; saved: the forward's saved state
  *   grad_w  dL/dw (layout of w, fp32), NULL to skip; must be NULL for SYN_NONE
  *   grad_b  dL/dbias fp32, NULL to skip
+ *   grad_v  dL/dv fp32 [n_out] of SNN_RLEAKY, NULL to skip; must be NULL for
+ *           the other neurons (SNN_ERR_SHAPE)
  *   grad_x  dL/dx fp32 [T,B,n_in] (the g of the layer below), NULL to skip;
  *           for SNN_SYN_NONE this is dL/dI and is required */
 snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const void *x,
-                         const void *w, const void *saved, float *grad_w, float *grad_b,
-                         float *grad_x, void *ws, size_t ws_bytes, hipStream_t stream);
+                         const void *w, const float *v, const void *saved, float *grad_w,
+                         float *grad_b, float *grad_v, float *grad_x, void *ws,
+                         size_t ws_bytes, hipStream_t stream);
 
 /* Loss on spike counts [B,K] and its gradient dL/dc [B,K] (which is dL/dz_t
  * for every t, since dc/dz_t = 1).  `loss` is a device fp32 scalar.
@@ -194,15 +207,16 @@ snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w
                            size_t ws_bytes, hipStream_t stream);
 
 /* Neuron scan over T.  cur and saved_u may be the same pointer (in place);
- * any other overlap is undefined. */
-snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, void *spk_out,
-                          float *saved_u, float *counts, hipStream_t stream);
+ * any other overlap is undefined.  v as in snn_layer_fwd. */
+snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float *v,
+                          void *spk_out, float *saved_u, float *counts, hipStream_t stream);
 
-/* Reverse-time scan: dcur = dL/dI [T,B,n_out] of d->grad_dtype, and
- * grad_b (nullable) = sum of dL/dI over t, b (and pooled positions). */
-snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad,
-                          const float *saved_u, void *dcur, float *grad_b, void *ws,
-                          size_t ws_bytes, hipStream_t stream);
+/* Reverse-time scan: dcur = dL/dI [T,B,n_out] of d->grad_dtype,
+ * grad_b (nullable) = sum of dL/dI over t, b (and pooled positions), and
+ * grad_v (nullable, SNN_RLEAKY only) as in snn_layer_bwd. */
+snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const float *v,
+                          const float *saved_u, void *dcur, float *grad_b, float *grad_v,
+                          void *ws, size_t ws_bytes, hipStream_t stream);
 
 /* Synapse backward from dcur (of d->grad_dtype): grad_w and/or grad_x. */
 snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,

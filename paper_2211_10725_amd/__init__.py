@@ -25,13 +25,13 @@ LIB_PATH = os.path.join(_HERE, "libsnn.so")
 
 # element types, neuron models, synapses, gradient kinds, losses (snn.h)
 F32, F16, BF16, U8 = 0, 1, 2, 3
-LEAKY, SYNAPTIC = 0, 1
+LEAKY, SYNAPTIC, RLEAKY = 0, 1, 2
 SYN_DENSE, SYN_CONV5_POOL2, SYN_NONE = 0, 1, 2
 RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST = 0, 1
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 1
+ABI_VERSION = 2
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
           4: "SNN_ERR_ALIGN", 5: "SNN_ERR_UNSUPPORTED", 6: "SNN_ERR_WORKSPACE",
@@ -93,13 +93,13 @@ def lib():
         "snn_status_str": ([ctypes.c_int], ctypes.c_char_p),
         "snn_layer_saved_bytes": ([D], S),
         "snn_layer_workspace_bytes": ([D], S),
-        "snn_layer_fwd": ([D, P, P, P, P, P, P, P, S, P], ctypes.c_int),
-        "snn_layer_bwd": ([D, G, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_layer_fwd": ([D, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_layer_bwd": ([D, G, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_loss_workspace_bytes": ([i32, i32, i32], S),
         "snn_loss": ([i32, i32, i32, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_synapse_fwd": ([D, P, P, P, P, P, P, S, P], ctypes.c_int),
-        "snn_neuron_fwd": ([D, P, P, P, P, P], ctypes.c_int),
-        "snn_neuron_bwd": ([D, G, P, P, P, P, S, P], ctypes.c_int),
+        "snn_neuron_fwd": ([D, P, P, P, P, P, P], ctypes.c_int),
+        "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, S, P], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
@@ -153,17 +153,18 @@ def snn_loss_workspace_bytes(kind: int, B: int, K: int) -> int:
     return int(lib().snn_loss_workspace_bytes(kind, B, K))
 
 
-def snn_layer_fwd(desc, x, w, bias, spk_out, saved, counts, ws, stream=None):
+def snn_layer_fwd(desc, x, w, bias, v, spk_out, saved, counts, ws, stream=None):
     _check("snn_layer_fwd", lib().snn_layer_fwd(
-        ctypes.byref(desc), _p(x), _p(w), _p(bias), _p(spk_out), _p(saved), _p(counts),
+        ctypes.byref(desc), _p(x), _p(w), _p(bias), _p(v), _p(spk_out), _p(saved), _p(counts),
         _p(ws), _nbytes(ws), _stream(stream)))
 
 
-def snn_layer_bwd(desc, grad_kind, g, x, w, saved, grad_w, grad_b, grad_x, ws, stream=None):
+def snn_layer_bwd(desc, grad_kind, g, x, w, v, saved, grad_w, grad_b, grad_v, grad_x, ws,
+                  stream=None):
     gi = GradIn(grad_kind, 0, _p(g))
     _check("snn_layer_bwd", lib().snn_layer_bwd(
-        ctypes.byref(desc), ctypes.byref(gi), _p(x), _p(w), _p(saved), _p(grad_w), _p(grad_b),
-        _p(grad_x), _p(ws), _nbytes(ws), _stream(stream)))
+        ctypes.byref(desc), ctypes.byref(gi), _p(x), _p(w), _p(v), _p(saved), _p(grad_w),
+        _p(grad_b), _p(grad_v), _p(grad_x), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def snn_loss(kind, B, K, counts, labels, targets, loss, grad_counts, ws, stream=None):
@@ -177,16 +178,17 @@ def snn_synapse_fwd(desc, x, w, bias, cur, pool_arg, ws, stream=None):
         _stream(stream)))
 
 
-def snn_neuron_fwd(desc, cur, spk_out, saved_u, counts, stream=None):
+def snn_neuron_fwd(desc, cur, v, spk_out, saved_u, counts, stream=None):
     _check("snn_neuron_fwd", lib().snn_neuron_fwd(
-        ctypes.byref(desc), _p(cur), _p(spk_out), _p(saved_u), _p(counts), _stream(stream)))
+        ctypes.byref(desc), _p(cur), _p(v), _p(spk_out), _p(saved_u), _p(counts),
+        _stream(stream)))
 
 
-def snn_neuron_bwd(desc, grad_kind, g, saved_u, dcur, grad_b, ws, stream=None):
+def snn_neuron_bwd(desc, grad_kind, g, v, saved_u, dcur, grad_b, grad_v, ws, stream=None):
     gi = GradIn(grad_kind, 0, _p(g))
     _check("snn_neuron_bwd", lib().snn_neuron_bwd(
-        ctypes.byref(desc), ctypes.byref(gi), _p(saved_u), _p(dcur), _p(grad_b), _p(ws),
-        _nbytes(ws), _stream(stream)))
+        ctypes.byref(desc), ctypes.byref(gi), _p(v), _p(saved_u), _p(dcur), _p(grad_b),
+        _p(grad_v), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def snn_synapse_bwd(desc, dcur, pool_arg, x, w, grad_w, grad_x, ws, stream=None):
@@ -198,7 +200,7 @@ def snn_synapse_bwd(desc, dcur, pool_arg, x, w, grad_w, grad_x, ws, stream=None)
 # --------------------------------------------------------------------------
 # descriptors from plain layer specs
 # --------------------------------------------------------------------------
-_NEURON = {"leaky": LEAKY, "synaptic": SYNAPTIC}
+_NEURON = {"leaky": LEAKY, "synaptic": SYNAPTIC, "rleaky": RLEAKY}
 
 
 def layer_desc(spec: dict, T: int, B: int, in_dtype=U8, w_dtype=F32, out_dtype=U8,
@@ -242,7 +244,7 @@ class Network:
         T, B = wl.T, wl.B
         half = wl.dtype == "f16"
         self.descs = []
-        self.W, self.b = [], []
+        self.W, self.b, self.v = [], [], []
         for li, spec in enumerate(wl.layers):
             in_dt = F32 if spec["kind"] == "none" else U8
             # half-precision nets hand dL/dI to the contractions in bf16, which
@@ -251,7 +253,11 @@ class Network:
                            out_dtype=U8, grad_dtype=BF16 if half else F32, slope=wl.slope,
                            reset_grad=reset_grad, flags=flags)
             self.descs.append(d)
-            W, b = params[li]
+            W, b = params[li][0], params[li][1]
+            # recurrent weights of an 'rleaky' layer: (W, b, v)
+            v = params[li][2] if len(params[li]) > 2 else None
+            self.v.append(None if v is None else torch.as_tensor(np.ascontiguousarray(
+                v, np.float32)).to(device))
             if W is None:
                 self.W.append(None)
                 self.b.append(None)
@@ -269,6 +275,8 @@ class Network:
                    for w in self.W]
         self.gb = [None if b is None else torch.empty(b.shape, dtype=torch.float32, device=device)
                    for b in self.b]
+        self.gv = [None if v is None else torch.empty(v.shape, dtype=torch.float32, device=device)
+                   for v in self.v]
         # dL/dx of layer l is the upstream gradient of layer l-1
         self.gx = [None] + [torch.empty((T, B, d.n_in), dtype=torch.float32, device=device)
                             for d in self.descs[1:]]
@@ -288,7 +296,7 @@ class Network:
         h = x
         n = len(self.descs)
         for li, d in enumerate(self.descs):
-            snn_layer_fwd(d, h, self.W[li], self.b[li], self.spk[li], self.saved[li],
+            snn_layer_fwd(d, h, self.W[li], self.b[li], self.v[li], self.spk[li], self.saved[li],
                           self.counts if li == n - 1 else None, self.ws, stream)
             h = self.spk[li]
 
@@ -302,8 +310,8 @@ class Network:
         for li in range(n - 1, -1, -1):
             d = self.descs[li]
             xin = x if li == 0 else self.spk[li - 1]
-            snn_layer_bwd(d, kind, g, xin, self.W[li], self.saved[li], self.gW[li], self.gb[li],
-                          self.gx[li], self.ws, stream)
+            snn_layer_bwd(d, kind, g, xin, self.W[li], self.v[li], self.saved[li], self.gW[li],
+                          self.gb[li], self.gv[li], self.gx[li], self.ws, stream)
             kind, g = GRAD_FULL, self.gx[li]
 
     def step(self, x, labels=None, targets=None, stream=None):
@@ -335,7 +343,7 @@ class Network:
             else:
                 cur = h
             hook("neuron_fwd", li)
-            snn_neuron_fwd(d, cur, self.spk[li], self.saved[li],
+            snn_neuron_fwd(d, cur, self.v[li], self.spk[li], self.saved[li],
                            self.counts if li == n - 1 else None, stream)
             hook("neuron_fwd_end", li)
             h = self.spk[li]
@@ -348,7 +356,8 @@ class Network:
             xin = x if li == 0 else self.spk[li - 1]
             if d.synapse == SYN_NONE:
                 hook("neuron_bwd", li)
-                snn_neuron_bwd(d, kind, g, self.saved[li], self.gx[li], None, None, stream)
+                snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], self.gx[li], None,
+                               self.gv[li], self.ws, stream)
                 hook("neuron_bwd_end", li)
                 continue
             dcur_bytes = d.T * d.B * d.n_out * (2 if d.grad_dtype in (F16, BF16) else 4)
@@ -361,7 +370,8 @@ class Network:
                 dcur = dcur.view(torch.float32)
             rest = self.ws[(dcur_bytes + 255) // 256 * 256:]
             hook("neuron_bwd", li)
-            snn_neuron_bwd(d, kind, g, self.saved[li], dcur, self.gb[li], rest, stream)
+            snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], dcur, self.gb[li],
+                           self.gv[li], rest, stream)
             hook("neuron_bwd_end", li)
             hook("synapse_bwd", li)
             snn_synapse_bwd(d, dcur, self.pool_arg(li), xin, self.W[li], self.gW[li], self.gx[li],

@@ -34,7 +34,8 @@ snn_status check_desc(const snn_layer_desc *d) {
     if (!d) return SNN_ERR_NULL;
     if (d->flags & ~SNN_FLAG_FP32_MFMA) return SNN_ERR_UNSUPPORTED;
     if (d->T < 0 || d->B < 0 || d->n_in < 0 || d->n_out < 0) return SNN_ERR_SHAPE;
-    if (d->neuron != SNN_LEAKY && d->neuron != SNN_SYNAPTIC) return SNN_ERR_UNSUPPORTED;
+    if (d->neuron != SNN_LEAKY && d->neuron != SNN_SYNAPTIC && d->neuron != SNN_RLEAKY)
+        return SNN_ERR_UNSUPPORTED;
     if (d->reset_grad != SNN_RESET_DETACHED && d->reset_grad != SNN_RESET_SURROGATE)
         return SNN_ERR_UNSUPPORTED;
     if (!finite(d->beta) || !finite(d->alpha) || !finite(d->threshold) || !finite(d->slope) ||
@@ -82,9 +83,12 @@ size_t arg_offset(const snn_layer_desc *d) { return align_up((size_t)rows(d) * d
 // spike x fp32 contractions may use the exact three-pass bf16 kernels
 bool split_ok(const snn_layer_desc *d) { return (d->flags & SNN_FLAG_FP32_MFMA) == 0; }
 
+bool recurrent(const snn_layer_desc *d) { return d->neuron == SNN_RLEAKY; }
+
 // ---- workspace layout ------------------------------------------------------
 // forward:  [contraction workspace]
-// backward: [dcur (grad_dtype) T*B*n_out][colsum fp32 B*n_out][contraction workspace]
+// backward: [dcur (grad_dtype) T*B*n_out][colsum fp32 B*n_out]
+//           [dvcol fp32 B*n_out, recurrent neurons only][contraction workspace]
 size_t fwd_ws(const snn_layer_desc *d) {
     if (d->synapse == SNN_SYN_CONV5_POOL2)
         return conv_fwd_workspace_bytes(conv_geom(d), d->in_dtype, split_ok(d));
@@ -99,6 +103,9 @@ size_t dcur_bytes(const snn_layer_desc *d) {
 size_t colsum_bytes(const snn_layer_desc *d) {
     return align_up((size_t)d->B * d->n_out * sizeof(float));
 }
+// per-column sums of the neuron backward: dL/dI (bias) and, for the recurrent
+// neuron, lam_{t+1} z_t (recurrent weight)
+size_t neuron_ws(const snn_layer_desc *d) { return colsum_bytes(d) * (recurrent(d) ? 2 : 1); }
 // Weight and input gradients of a dense layer.  Large contractions whose
 // operands are stored M/N-contiguous (dI and x for dW, W for dx) are
 // transposed once into the workspace so that they run K-contiguous on the
@@ -178,7 +185,7 @@ size_t bwd_gemm_ws(const snn_layer_desc *d) {
     const size_t dx = x.wt_bytes + x.gemm_bytes;
     return dw > dx ? dw : dx;
 }
-size_t bwd_ws(const snn_layer_desc *d) { return dcur_bytes(d) + colsum_bytes(d) + bwd_gemm_ws(d); }
+size_t bwd_ws(const snn_layer_desc *d) { return dcur_bytes(d) + neuron_ws(d) + bwd_gemm_ws(d); }
 
 snn_status hip_status(hipError_t e) { return e == hipSuccess ? SNN_OK : SNN_ERR_HIP; }
 
@@ -250,13 +257,15 @@ snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w
     return hip_status(launch_gemm(g, ws, ws_bytes, stream));
 }
 
-snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, void *spk_out,
-                          float *saved_u, float *counts, hipStream_t stream) {
+snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float *v,
+                          void *spk_out, float *saved_u, float *counts, hipStream_t stream) {
     snn_status st = check_desc(d);
     if (st != SNN_OK) return st;
     if (!cur || !spk_out || !saved_u) return SNN_ERR_NULL;
+    if (recurrent(d) && !v) return SNN_ERR_NULL;
+    if (!recurrent(d)) v = nullptr;
     if (!aligned16(cur) || !aligned16(spk_out) || !aligned16(saved_u) ||
-        (counts && !aligned16(counts)))
+        (counts && !aligned16(counts)) || (v && !aligned16(v)))
         return SNN_ERR_ALIGN;
     (void)hipGetLastError();
     if (rows(d) == 0) {
@@ -265,36 +274,48 @@ snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, void *spk_o
         return SNN_OK;
     }
     const int64_t C = (int64_t)d->B * d->n_out;
-    return hip_status(launch_neuron_fwd(d->neuron, d->T, C, d->alpha, d->beta, d->threshold, cur,
-                                        spk_out, d->out_dtype, saved_u, counts, stream));
+    return hip_status(launch_neuron_fwd(d->neuron, d->T, C, d->n_out, d->alpha, d->beta,
+                                        d->threshold, v, cur, spk_out, d->out_dtype, saved_u,
+                                        counts, stream));
 }
 
-snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad,
-                          const float *saved_u, void *dcur, float *grad_b, void *ws,
-                          size_t ws_bytes, hipStream_t stream) {
+snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const float *v,
+                          const float *saved_u, void *dcur, float *grad_b, float *grad_v,
+                          void *ws, size_t ws_bytes, hipStream_t stream) {
     snn_status st = check_desc(d);
     if (st != SNN_OK) return st;
     if ((st = check_grad(d, grad)) != SNN_OK) return st;
     if (!saved_u || !dcur) return SNN_ERR_NULL;
-    if (!aligned16(saved_u) || !aligned16(dcur) || (grad_b && !aligned16(grad_b)))
+    if (recurrent(d) && !v) return SNN_ERR_NULL;
+    if (!recurrent(d)) {
+        if (grad_v) return SNN_ERR_SHAPE;  // no recurrent weight to differentiate
+        v = nullptr;
+    }
+    if (!aligned16(saved_u) || !aligned16(dcur) || (grad_b && !aligned16(grad_b)) ||
+        (v && !aligned16(v)) || (grad_v && !aligned16(grad_v)))
         return SNN_ERR_ALIGN;
     if (grad_b && d->synapse == SNN_SYN_NONE) return SNN_ERR_SHAPE;  // no bias to differentiate
-    const size_t need = grad_b ? colsum_bytes(d) : 0;
+    const size_t need = (grad_b ? colsum_bytes(d) : 0) + (grad_v ? colsum_bytes(d) : 0);
     if (need > ws_bytes || (need > 0 && !ws)) return SNN_ERR_WORKSPACE;
     (void)hipGetLastError();
     if (rows(d) == 0) {
+        hipError_t e = hipSuccess;
         if (grad_b) {
             const int64_t nb = d->synapse == SNN_SYN_CONV5_POOL2 ? d->c_out : d->n_out;
-            return hip_status(launch_fill_zero(grad_b, nb, stream));
+            e = launch_fill_zero(grad_b, nb, stream);
         }
-        return SNN_OK;
+        if (grad_v && e == hipSuccess) e = launch_fill_zero(grad_v, d->n_out, stream);
+        return hip_status(e);
     }
     const int64_t C = (int64_t)d->B * d->n_out;
-    float *colsum = grad_b ? reinterpret_cast<float *>(ws) : nullptr;
-    hipError_t e = launch_neuron_bwd(d->neuron, d->reset_grad, d->T, C, d->alpha, d->beta,
-                                     d->threshold, d->slope, saved_u, grad->g,
+    char *wsb = reinterpret_cast<char *>(ws);
+    float *colsum = grad_b ? reinterpret_cast<float *>(wsb) : nullptr;
+    float *dvcol = grad_v ? reinterpret_cast<float *>(wsb + (grad_b ? colsum_bytes(d) : 0))
+                          : nullptr;
+    hipError_t e = launch_neuron_bwd(d->neuron, d->reset_grad, d->T, C, d->n_out, d->alpha,
+                                     d->beta, d->threshold, d->slope, v, saved_u, grad->g,
                                      grad->kind == SNN_GRAD_BCAST, dcur, d->grad_dtype, colsum,
-                                     stream);
+                                     dvcol, stream);
     if (e != hipSuccess) return SNN_ERR_HIP;
     if (grad_b) {
         int F = d->n_out, P = 1;
@@ -303,7 +324,10 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad,
             P = d->n_out / d->c_out;
         }
         e = launch_bias_reduce(d->B, F, P, colsum, grad_b, stream);
+        if (e != hipSuccess) return SNN_ERR_HIP;
     }
+    // dL/dv[n] = sum over the batch of the per-column sums, fixed order
+    if (grad_v) e = launch_bias_reduce(d->B, d->n_out, 1, dvcol, grad_v, stream);
     return hip_status(e);
 }
 
@@ -387,29 +411,33 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
 }
 
 snn_status snn_layer_fwd(const snn_layer_desc *d, const void *x, const void *w,
-                         const float *bias, void *spk_out, void *saved, float *counts,
-                         void *ws, size_t ws_bytes, hipStream_t stream) {
+                         const float *bias, const float *v, void *spk_out, void *saved,
+                         float *counts, void *ws, size_t ws_bytes, hipStream_t stream) {
     snn_status st = check_desc(d);
     if (st != SNN_OK) return st;
     if (!x || !spk_out || !saved) return SNN_ERR_NULL;
     if (d->synapse != SNN_SYN_NONE && !w) return SNN_ERR_NULL;
+    if (recurrent(d) && !v) return SNN_ERR_NULL;
+    if (v && recurrent(d) && !aligned16(v)) return SNN_ERR_ALIGN;
     if (!aligned16(x) || !aligned16(spk_out) || !aligned16(saved) || (w && !aligned16(w)) ||
         (bias && !aligned16(bias)) || (counts && !aligned16(counts)))
         return SNN_ERR_ALIGN;
     if (fwd_ws(d) > ws_bytes) return SNN_ERR_WORKSPACE;
     float *u = reinterpret_cast<float *>(saved);
     if (d->synapse == SNN_SYN_NONE)
-        return snn_neuron_fwd(d, reinterpret_cast<const float *>(x), spk_out, u, counts, stream);
+        return snn_neuron_fwd(d, reinterpret_cast<const float *>(x), v, spk_out, u, counts,
+                              stream);
     uint8_t *arg = nullptr;
     if (d->synapse == SNN_SYN_CONV5_POOL2) arg = reinterpret_cast<uint8_t *>(saved) + arg_offset(d);
     st = snn_synapse_fwd(d, x, w, bias, u, arg, ws, ws_bytes, stream);
     if (st != SNN_OK) return st;
-    return snn_neuron_fwd(d, u, spk_out, u, counts, stream);
+    return snn_neuron_fwd(d, u, v, spk_out, u, counts, stream);
 }
 
 snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const void *x,
-                         const void *w, const void *saved, float *grad_w, float *grad_b,
-                         float *grad_x, void *ws, size_t ws_bytes, hipStream_t stream) {
+                         const void *w, const float *v, const void *saved, float *grad_w,
+                         float *grad_b, float *grad_v, float *grad_x, void *ws,
+                         size_t ws_bytes, hipStream_t stream) {
     snn_status st = check_desc(d);
     if (st != SNN_OK) return st;
     if ((st = check_grad(d, grad)) != SNN_OK) return st;
@@ -419,7 +447,7 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     if (d->synapse == SNN_SYN_NONE) {
         if (grad_w || grad_b) return SNN_ERR_SHAPE;
         if (!grad_x) return SNN_ERR_NULL;
-        return snn_neuron_bwd(d, grad, u, grad_x, nullptr, nullptr, 0, stream);
+        return snn_neuron_bwd(d, grad, v, u, grad_x, nullptr, grad_v, ws, ws_bytes, stream);
     }
     if (grad_w && !x) return SNN_ERR_NULL;
     if (grad_x && !w) return SNN_ERR_NULL;
@@ -427,8 +455,8 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     char *base = reinterpret_cast<char *>(ws);
     void *dcur = base;
     char *colsum = base + dcur_bytes(d);
-    char *gws = colsum + colsum_bytes(d);
-    st = snn_neuron_bwd(d, grad, u, dcur, grad_b, colsum, colsum_bytes(d), stream);
+    char *gws = colsum + neuron_ws(d);
+    st = snn_neuron_bwd(d, grad, v, u, dcur, grad_b, grad_v, colsum, neuron_ws(d), stream);
     if (st != SNN_OK) return st;
     if (!grad_w && !grad_x) return SNN_OK;
     const uint8_t *arg = nullptr;

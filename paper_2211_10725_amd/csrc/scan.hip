@@ -1,4 +1,4 @@
-// Neuron time scans for gfx950: forward (eqs. 3-6) and the BPTT reverse scan
+// Neuron time scans for gfx950: forward (eqs. 3-7) and the BPTT reverse scan
 // with the fast-sigmoid surrogate (eqs. 8-9).
 //
 // Layout: every tensor is time-major [T, C] with C = B * n columns, column
@@ -67,17 +67,25 @@ __device__ inline void store_spikes_f16(uint16_t *p, const float (&z)[VEC]) {
 
 // Forward scan.  `cur` and `u_out` may alias exactly: each lane reads step t
 // of its columns before it writes step t, and prefetches only later steps.
+// The recurrent neuron (eq. 7) adds its own previous spike through the
+// recurrent weight: a spike at t-1 adds (v - thr) to u_t instead of the
+// plain reset -thr; column c is neuron c % N, vrec holds v per neuron.
 template <int NEURON, int VEC, int OUT, int kDepth>
-__global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, float alpha,
-                                                              float beta, float thr,
+__global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, int64_t N,
+                                                              float alpha, float beta, float thr,
+                                                              const float *__restrict__ vrec,
                                                               const float *cur, void *spk,
                                                               float *u_out,
                                                               float *__restrict__ counts) {
     const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
     if (col >= C) return;
-    float u[VEC], syn[VEC], zp[VEC], cnt[VEC];
+    float u[VEC], syn[VEC], zp[VEC], cnt[VEC], jump[VEC];
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) u[v] = syn[v] = zp[v] = cnt[v] = 0.f;
+    for (int v = 0; v < VEC; ++v) {
+        u[v] = syn[v] = zp[v] = cnt[v] = 0.f;
+        if constexpr (NEURON == SNN_RLEAKY) jump[v] = vrec[(col + v) % N] - thr;
+        else jump[v] = -thr;
+    }
 
     float in[kDepth][VEC], nx[kDepth][VEC];
 #pragma unroll
@@ -102,7 +110,8 @@ __global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, 
                     } else {
                         uu = __builtin_fmaf(beta, u[v], in[j][v]);
                     }
-                    uu = (zp[v] != 0.f) ? uu - thr : uu;  // reset by subtraction
+                    // reset by subtraction (eq. 7: plus the recurrent weight)
+                    uu = (zp[v] != 0.f) ? uu + jump[v] : uu;
                     u[v] = uu;
                     z[v] = (uu > thr) ? 1.f : 0.f;       // eq. (3), strict
                     zp[v] = z[v];
@@ -154,16 +163,25 @@ __device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC]
 }
 
 // Reverse-time scan.  lam carries dL/du_{t+1} (and lami dL/di_{t+1}).
+// For the recurrent neuron the spike z_t reaches u_{t+1} through
+// (v - r thr), so the carry is beta + (v - r thr) s_t, and the recurrent
+// weight's gradient collects lam_{t+1} z_t per column (dvcol, fp32).
 template <int NEURON, int VEC, bool BCAST, bool RESET_SURR, int GT, int kDepth>
 __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
-    int T, int64_t C, float alpha, float beta, float thr, float slope,
-    const float *__restrict__ u, const float *__restrict__ g, void *__restrict__ dcur,
-    float *__restrict__ colsum) {
+    int T, int64_t C, int64_t N, float alpha, float beta, float thr, float slope,
+    const float *__restrict__ vrec, const float *__restrict__ u, const float *__restrict__ g,
+    void *__restrict__ dcur, float *__restrict__ colsum, float *__restrict__ dvcol) {
     const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
     if (col >= C) return;
-    float lam[VEC], lami[VEC], acc[VEC], gb[VEC];
+    float lam[VEC], lami[VEC], acc[VEC], gb[VEC], vr[VEC], dv[VEC];
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) lam[v] = lami[v] = acc[v] = gb[v] = 0.f;
+    for (int v = 0; v < VEC; ++v) {
+        lam[v] = lami[v] = acc[v] = gb[v] = dv[v] = 0.f;
+        if constexpr (NEURON == SNN_RLEAKY)
+            vr[v] = RESET_SURR ? vrec[(col + v) % N] - thr : vrec[(col + v) % N];
+        else
+            vr[v] = 0.f;
+    }
     if constexpr (BCAST) Vec<VEC>::load(g + col, gb);
 
     float uu[kDepth][VEC], nu[kDepth][VEC];
@@ -197,7 +215,12 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
                     float gt;
                     if constexpr (BCAST) gt = gb[v]; else gt = gg[j][v];
                     float carry = beta;
-                    if constexpr (RESET_SURR) carry = beta - thr * s;
+                    if constexpr (NEURON == SNN_RLEAKY) {
+                        if (uu[j][v] > thr) dv[v] += lam[v];  // lam_{t+1} z_t
+                        carry = __builtin_fmaf(vr[v], s, beta);
+                    } else if constexpr (RESET_SURR) {
+                        carry = beta - thr * s;
+                    }
                     lam[v] = __builtin_fmaf(carry, lam[v], gt * s);
                     if constexpr (NEURON == SNN_SYNAPTIC) {
                         lami[v] = __builtin_fmaf(alpha, lami[v], lam[v]);
@@ -219,6 +242,8 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
             }
     }
     if (colsum) Vec<VEC>::store(colsum + col, acc);
+    if constexpr (NEURON == SNN_RLEAKY)
+        if (dvcol) Vec<VEC>::store(dvcol + col, dv);
 }
 
 // Bias gradient: db[f] = sum over b of the per-column time sums.  A block
@@ -272,79 +297,108 @@ __global__ __launch_bounds__(kThreads) void fill_zero_kernel(float *__restrict__
     if (i < n) p[i] = 0.f;
 }
 
+struct ScanArgs {
+    int T;
+    int64_t C, N;
+    float alpha, beta, thr, slope;
+    const float *vrec;
+};
+
 template <int NEURON, int VEC, int OUT>
-void fwd_launch(int T, int64_t C, float alpha, float beta, float thr, const float *cur,
-                void *spk, float *u_out, float *counts, hipStream_t s) {
-    const int64_t lanes = (C + VEC - 1) / VEC;
+void fwd_launch(const ScanArgs &a, const float *cur, void *spk, float *u_out, float *counts,
+                hipStream_t s) {
+    const int64_t lanes = (a.C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_fwd_kernel<NEURON, VEC, OUT, VEC == 4 ? 6 : 16><<<grid, kThreads, 0, s>>>(T, C, alpha, beta, thr, cur,
-                                                                 spk, u_out, counts);
-}
-
-template <int NEURON, int VEC, bool BCAST, bool RS, int GT>
-void bwd_launch(int T, int64_t C, float alpha, float beta, float thr, float slope,
-                const float *u, const float *g, void *dcur, float *colsum, hipStream_t s) {
-    const int64_t lanes = (C + VEC - 1) / VEC;
-    const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_bwd_kernel<NEURON, VEC, BCAST, RS, GT, VEC == 4 ? 6 : 16><<<grid, kThreads, 0, s>>>(
-        T, C, alpha, beta, thr, slope, u, g, dcur, colsum);
-}
-
-template <int NEURON, int VEC, bool BCAST, bool RS>
-void bwd_dispatch_gt(int gt, int T, int64_t C, float alpha, float beta, float thr, float slope,
-                     const float *u, const float *g, void *dcur, float *colsum, hipStream_t s) {
-    if (gt == SNN_F32)
-        bwd_launch<NEURON, VEC, BCAST, RS, SNN_F32>(T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
-    else if (gt == SNN_F16)
-        bwd_launch<NEURON, VEC, BCAST, RS, SNN_F16>(T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
-    else
-        bwd_launch<NEURON, VEC, BCAST, RS, SNN_BF16>(T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+    neuron_fwd_kernel<NEURON, VEC, OUT, VEC == 4 ? 6 : 16><<<grid, kThreads, 0, s>>>(
+        a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.vrec, cur, spk, u_out, counts);
 }
 
 template <int NEURON, int VEC>
-void bwd_dispatch(int rs, int bcast, int gt, int T, int64_t C, float alpha, float beta, float thr,
-                  float slope, const float *u, const float *g, void *dcur, float *colsum,
+void fwd_dispatch(int out_dtype, const ScanArgs &a, const float *cur, void *spk, float *u_out,
+                  float *counts, hipStream_t s) {
+    if (out_dtype == SNN_U8) fwd_launch<NEURON, VEC, SNN_U8>(a, cur, spk, u_out, counts, s);
+    else fwd_launch<NEURON, VEC, SNN_F16>(a, cur, spk, u_out, counts, s);
+}
+
+struct BwdBuffers {
+    const float *u, *g;
+    void *dcur;
+    float *colsum, *dvcol;
+};
+
+template <int NEURON, int VEC, bool BCAST, bool RS, int GT>
+void bwd_launch(const ScanArgs &a, const BwdBuffers &b, hipStream_t s) {
+    const int64_t lanes = (a.C + VEC - 1) / VEC;
+    const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
+    neuron_bwd_kernel<NEURON, VEC, BCAST, RS, GT, VEC == 4 ? 6 : 16><<<grid, kThreads, 0, s>>>(
+        a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.u, b.g, b.dcur, b.colsum,
+        b.dvcol);
+}
+
+template <int NEURON, int VEC, bool BCAST, bool RS>
+void bwd_dispatch_gt(int gt, const ScanArgs &a, const BwdBuffers &b, hipStream_t s) {
+    if (gt == SNN_F32) bwd_launch<NEURON, VEC, BCAST, RS, SNN_F32>(a, b, s);
+    else if (gt == SNN_F16) bwd_launch<NEURON, VEC, BCAST, RS, SNN_F16>(a, b, s);
+    else bwd_launch<NEURON, VEC, BCAST, RS, SNN_BF16>(a, b, s);
+}
+
+template <int NEURON, int VEC>
+void bwd_dispatch(int rs, int bcast, int gt, const ScanArgs &a, const BwdBuffers &b,
                   hipStream_t s) {
     if (bcast) {
-        if (rs) bwd_dispatch_gt<NEURON, VEC, true, true>(gt, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
-        else bwd_dispatch_gt<NEURON, VEC, true, false>(gt, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+        if (rs) bwd_dispatch_gt<NEURON, VEC, true, true>(gt, a, b, s);
+        else bwd_dispatch_gt<NEURON, VEC, true, false>(gt, a, b, s);
     } else {
-        if (rs) bwd_dispatch_gt<NEURON, VEC, false, true>(gt, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
-        else bwd_dispatch_gt<NEURON, VEC, false, false>(gt, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+        if (rs) bwd_dispatch_gt<NEURON, VEC, false, true>(gt, a, b, s);
+        else bwd_dispatch_gt<NEURON, VEC, false, false>(gt, a, b, s);
     }
 }
 
 }  // namespace
 
-hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, float alpha, float beta, float thr,
-                             const float *cur, void *spk, int out_dtype, float *u_out,
-                             float *counts, hipStream_t s) {
+hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, int64_t N, float alpha, float beta,
+                             float thr, const float *vrec, const float *cur, void *spk,
+                             int out_dtype, float *u_out, float *counts, hipStream_t s) {
     if (T <= 0 || C <= 0) return hipSuccess;
     const bool v4 = (C % 4) == 0 && C >= kWideColumns;
-#define SNN_FWD(N, V, O) fwd_launch<N, V, O>(T, C, alpha, beta, thr, cur, spk, u_out, counts, s)
-    if (neuron == SNN_SYNAPTIC) {
-        if (out_dtype == SNN_U8) { if (v4) SNN_FWD(SNN_SYNAPTIC, 4, SNN_U8); else SNN_FWD(SNN_SYNAPTIC, 1, SNN_U8); }
-        else { if (v4) SNN_FWD(SNN_SYNAPTIC, 4, SNN_F16); else SNN_FWD(SNN_SYNAPTIC, 1, SNN_F16); }
-    } else {
-        if (out_dtype == SNN_U8) { if (v4) SNN_FWD(SNN_LEAKY, 4, SNN_U8); else SNN_FWD(SNN_LEAKY, 1, SNN_U8); }
-        else { if (v4) SNN_FWD(SNN_LEAKY, 4, SNN_F16); else SNN_FWD(SNN_LEAKY, 1, SNN_F16); }
+    const ScanArgs a{T, C, N, alpha, beta, thr, 0.f, vrec};
+    switch (neuron) {
+        case SNN_SYNAPTIC:
+            if (v4) fwd_dispatch<SNN_SYNAPTIC, 4>(out_dtype, a, cur, spk, u_out, counts, s);
+            else fwd_dispatch<SNN_SYNAPTIC, 1>(out_dtype, a, cur, spk, u_out, counts, s);
+            break;
+        case SNN_RLEAKY:
+            if (v4) fwd_dispatch<SNN_RLEAKY, 4>(out_dtype, a, cur, spk, u_out, counts, s);
+            else fwd_dispatch<SNN_RLEAKY, 1>(out_dtype, a, cur, spk, u_out, counts, s);
+            break;
+        default:
+            if (v4) fwd_dispatch<SNN_LEAKY, 4>(out_dtype, a, cur, spk, u_out, counts, s);
+            else fwd_dispatch<SNN_LEAKY, 1>(out_dtype, a, cur, spk, u_out, counts, s);
     }
-#undef SNN_FWD
     return hipGetLastError();
 }
 
-hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, float alpha,
-                             float beta, float thr, float slope, const float *u, const float *g,
-                             int g_bcast, void *dcur, int grad_dtype, float *colsum,
-                             hipStream_t s) {
+hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
+                             float alpha, float beta, float thr, float slope, const float *vrec,
+                             const float *u, const float *g, int g_bcast, void *dcur,
+                             int grad_dtype, float *colsum, float *dvcol, hipStream_t s) {
     if (T <= 0 || C <= 0) return hipSuccess;
     const bool v4 = (C % 4) == 0 && C >= kWideColumns;
-    if (neuron == SNN_SYNAPTIC) {
-        if (v4) bwd_dispatch<SNN_SYNAPTIC, 4>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
-        else bwd_dispatch<SNN_SYNAPTIC, 1>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
-    } else {
-        if (v4) bwd_dispatch<SNN_LEAKY, 4>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
-        else bwd_dispatch<SNN_LEAKY, 1>(reset_surrogate, g_bcast, grad_dtype, T, C, alpha, beta, thr, slope, u, g, dcur, colsum, s);
+    const ScanArgs a{T, C, N, alpha, beta, thr, slope, vrec};
+    const BwdBuffers b{u, g, dcur, colsum, dvcol};
+    const int rs = reset_surrogate, gt = grad_dtype;
+    switch (neuron) {
+        case SNN_SYNAPTIC:
+            if (v4) bwd_dispatch<SNN_SYNAPTIC, 4>(rs, g_bcast, gt, a, b, s);
+            else bwd_dispatch<SNN_SYNAPTIC, 1>(rs, g_bcast, gt, a, b, s);
+            break;
+        case SNN_RLEAKY:
+            if (v4) bwd_dispatch<SNN_RLEAKY, 4>(rs, g_bcast, gt, a, b, s);
+            else bwd_dispatch<SNN_RLEAKY, 1>(rs, g_bcast, gt, a, b, s);
+            break;
+        default:
+            if (v4) bwd_dispatch<SNN_LEAKY, 4>(rs, g_bcast, gt, a, b, s);
+            else bwd_dispatch<SNN_LEAKY, 1>(rs, g_bcast, gt, a, b, s);
     }
     return hipGetLastError();
 }

@@ -45,17 +45,19 @@ inline size_t dtype_bytes(int dt) {
 int device_cus();
 
 // ---- neuron scans (scan.hip) ---------------------------------------------
-// Forward: C = B * N independent columns, time-major [T, C].
-hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, float alpha, float beta, float thr,
-                             const float *cur, void *spk, int out_dtype, float *u_out,
-                             float *counts, hipStream_t s);
+// Forward: C = B * N independent columns, time-major [T, C]; vrec [N] holds
+// the recurrent weights of SNN_RLEAKY (column c is neuron c % N), else unused.
+hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, int64_t N, float alpha, float beta,
+                             float thr, const float *vrec, const float *cur, void *spk,
+                             int out_dtype, float *u_out, float *counts, hipStream_t s);
 
-// Backward: writes dcur [T, C] (grad_dtype) and colsum [C] = sum_t dcur (fp32,
+// Backward: writes dcur [T, C] (grad_dtype), colsum [C] = sum_t dcur (fp32,
+// may be NULL) and, for SNN_RLEAKY, dvcol [C] = sum_t lam_{t+1} z_t (fp32,
 // may be NULL).
-hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, float alpha,
-                             float beta, float thr, float slope, const float *u, const float *g,
-                             int g_bcast, void *dcur, int grad_dtype, float *colsum,
-                             hipStream_t s);
+hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
+                             float alpha, float beta, float thr, float slope, const float *vrec,
+                             const float *u, const float *g, int g_bcast, void *dcur,
+                             int grad_dtype, float *colsum, float *dvcol, hipStream_t s);
 
 // p[0..n) = 0 with a kernel (safe inside captured graphs)
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);

@@ -10,7 +10,9 @@ The inputs stand in for the MNIST-shaped workloads the paper measures on
 per sample and feature a firing rate r ~ U[0, rate_hi] is drawn, then
 x[t,b,f] ~ Bernoulli(r[b,f]) independently for every time step.  Weights
 and biases follow PyTorch's default layer init, U(-1/sqrt(fan_in),
-+1/sqrt(fan_in)).  Labels are uniform over the 10 classes.
++1/sqrt(fan_in)); the recurrent weights of recurrent neurons (eq. 7), one
+per neuron, are drawn U(-rec_hi, rec_hi).  Labels are uniform over the 10
+classes.
 """
 from __future__ import annotations
 
@@ -35,6 +37,7 @@ class Workload:
     current_mean: float = 0.0
     current_std: float = 1.0
     target_hi: float = 50.0
+    rec_hi: float = 0.5     # recurrent weights of 'rleaky' layers ~ U(-rec_hi, rec_hi)
     description: str = ""
     extra: dict = field(default_factory=dict)
 
@@ -86,6 +89,13 @@ WORKLOADS = {
         layers=[_conv(1, 28, 28, 12, "leaky", 0.5), _conv(12, 12, 12, 64, "leaky", 0.5),
                 _dense(1024, 10, "leaky", 0.5)],
         description="Conv SNN 5C12-MP2-5C64-MP2-10, Leaky beta=0.5, T=25, B=128, fp32"),
+    # The dense net with recurrent neurons (eq. 7, one recurrent weight per
+    # neuron), Leaky beta 0.95 as the default dense net.
+    "dsnn_rleaky_t25_b128": Workload(
+        "dsnn_rleaky_t25_b128", T=25, B=128,
+        layers=[_dense(784, 1000, "rleaky", 0.95), _dense(1000, 10, "rleaky", 0.95)],
+        description="Dense SNN 784-1000-10, recurrent Leaky (eq. 7) beta=0.95, one recurrent "
+                    "weight per neuron ~U(-0.5,0.5), T=25, B=128, fp32"),
     # Deeper, wider dense net in half precision operands.
     "dsnn_half_t100_b512": Workload(
         "dsnn_half_t100_b512", T=100, B=512, rate_hi=0.5, dtype="f16",
@@ -132,8 +142,19 @@ def _rng(seed: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(seed))
 
 
+def _n_out(s) -> int:
+    """Output neurons per sample of a layer spec."""
+    if s["kind"] == "dense":
+        return s["n_out"]
+    if s["kind"] == "none":
+        return s["n"]
+    k = s.get("k", 5)
+    return s["c_out"] * ((s["h"] - k + 1) // 2) * ((s["w"] - k + 1) // 2)
+
+
 def init_params(wl: Workload, seed: int):
-    """Per layer (W, b) as float32 arrays, U(-1/sqrt(fan_in), 1/sqrt(fan_in)).
+    """Per layer (W, b) as float32 arrays, U(-1/sqrt(fan_in), 1/sqrt(fan_in)),
+    and (W, b, v) for recurrent layers, v [n_out] ~ U(-rec_hi, rec_hi).
     For fp16 workloads the weights are rounded once to fp16 (round to
     nearest even) and returned as float32 holding those fp16 values, so both
     sides see identical operands."""
@@ -141,20 +162,24 @@ def init_params(wl: Workload, seed: int):
     params = []
     for s in wl.layers:
         if s["kind"] == "none":
-            params.append((None, None))
-            continue
-        if s["kind"] == "dense":
-            shape, fan_in, n_b = (s["n_out"], s["n_in"]), s["n_in"], s["n_out"]
+            W = b = None
         else:
-            k = s.get("k", 5)
-            shape, fan_in, n_b = (s["c_out"], s["c_in"], k, k), s["c_in"] * k * k, s["c_out"]
-        bound = 1.0 / math.sqrt(fan_in)
-        W = rng.uniform(-bound, bound, size=shape).astype(np.float32)
-        b = rng.uniform(-bound, bound, size=n_b).astype(np.float32)
-        if wl.dtype == "f16":
-            W = W.astype(np.float16).astype(np.float32)
-            b = b.astype(np.float16).astype(np.float32)
-        params.append((W, b))
+            if s["kind"] == "dense":
+                shape, fan_in, n_b = (s["n_out"], s["n_in"]), s["n_in"], s["n_out"]
+            else:
+                k = s.get("k", 5)
+                shape, fan_in, n_b = (s["c_out"], s["c_in"], k, k), s["c_in"] * k * k, s["c_out"]
+            bound = 1.0 / math.sqrt(fan_in)
+            W = rng.uniform(-bound, bound, size=shape).astype(np.float32)
+            b = rng.uniform(-bound, bound, size=n_b).astype(np.float32)
+            if wl.dtype == "f16":
+                W = W.astype(np.float16).astype(np.float32)
+                b = b.astype(np.float16).astype(np.float32)
+        if s["neuron"] == "rleaky":
+            v = rng.uniform(-wl.rec_hi, wl.rec_hi, size=_n_out(s)).astype(np.float32)
+            params.append((W, b, v))
+        else:
+            params.append((W, b))
     return params
 
 

@@ -36,9 +36,9 @@ def _dense(T=4, B=3, n_in=20, n_out=7):
                           T, B)
 
 
-def _fwd(desc, x=16, w=32, bias=None, spk=48, saved=64, counts=None, ws=None, wsb=0):
+def _fwd(desc, x=16, w=32, bias=None, v=None, spk=48, saved=64, counts=None, ws=None, wsb=0):
     return snn.lib().snn_layer_fwd(ctypes.byref(desc) if desc is not None else None, x, w, bias,
-                                   spk, saved, counts, ws, wsb, None)
+                                   v, spk, saved, counts, ws, wsb, None)
 
 
 def test_validation_errors_before_launch():
@@ -65,6 +65,19 @@ def test_validation_errors_before_launch():
                                beta=0.5), 4, 3)
     bad = conv.copy(); bad.n_out = 5
     assert _fwd(bad) == 2
+    # the recurrent neuron (eq. 7) needs its recurrent weights
+    rec = _dense(); rec.neuron = snn.RLEAKY
+    assert _fwd(rec) == 1
+    assert _fwd(rec, v=80 + 4) == 4
+    # a recurrent-weight gradient is only defined for the recurrent neuron
+    gi = snn.GradIn(snn.GRAD_BCAST, 0, 16)
+    need = snn.snn_layer_workspace_bytes(d)
+    st = snn.lib().snn_layer_bwd(ctypes.byref(d), ctypes.byref(gi), 32, 48, None, 64, 80, 96,
+                                 112, None, 256, need, None)
+    assert st == 2
+    st = snn.lib().snn_layer_bwd(ctypes.byref(rec), ctypes.byref(gi), 32, 48, None, 64, 80, 96,
+                                 112, None, 256, snn.snn_layer_workspace_bytes(rec), None)
+    assert st == 1
 
 
 def test_loss_validation():
@@ -93,9 +106,12 @@ def test_workspace_too_small_is_rejected():
     d = _dense(T=25, B=32, n_in=784, n_out=1000)
     gi = snn.GradIn(snn.GRAD_BCAST, 0, 16)
     need = snn.snn_layer_workspace_bytes(d)
-    st = snn.lib().snn_layer_bwd(ctypes.byref(d), ctypes.byref(gi), 32, 48, 64, 80, 96, None,
-                                 256, need - 1, None)
+    st = snn.lib().snn_layer_bwd(ctypes.byref(d), ctypes.byref(gi), 32, 48, None, 64, 80, 96,
+                                 None, None, 256, need - 1, None)
     assert st == 6
+    # the recurrent neuron's backward also holds the per-column dL/dv sums
+    rec = d.copy(); rec.neuron = snn.RLEAKY
+    assert snn.snn_layer_workspace_bytes(rec) >= need + 32 * 1000 * 4
 
 
 def test_missing_library_fails_loudly(monkeypatch, tmp_path):

@@ -1,9 +1,12 @@
 """Parity at the full benchmark sizes, on sampled outputs.
 
 The wide scan (65536 neurons x 64 samples x 1000 steps) and the deep
-half-precision net (784-4096-4096-10, T=100, B=512) are run through the same
-layer calls the benchmark times; the oracle then recomputes sampled columns
-and rows one by one, fed the GPU's own inputs to each stage.
+half-precision net (784-4096-4096-10, T=100, B=512) run through the same
+calls, descriptors and shapes the benchmark times.  Every stage is fed seeded
+synthetic inputs of its full-size shape; the oracle recomputes sampled
+columns and rows from the same seeded inputs (it never reads a value the GPU
+computed).  The whole step is then checked for agreement with the stage calls
+on the GPU itself.
 """
 import numpy as np
 import pytest
@@ -28,34 +31,67 @@ def _u(net, li):
     return net.saved[li][: d.T * d.B * d.n_out * 4].view(torch.float32).view(d.T, d.B, d.n_out)
 
 
+def _gen(seed):
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    return g
+
+
+def _seeded_normal(shape, mean, std, seed, dtype=torch.float32):
+    x = torch.empty(shape, dtype=torch.float32, device=DEV)
+    x.normal_(mean, std, generator=_gen(seed))
+    return x.to(dtype)
+
+
+def _seeded_spikes(shape, p, seed):
+    return (torch.rand(shape, generator=_gen(seed), device=DEV) < p).to(torch.uint8)
+
+
 def test_scan_wide_full_size_sampled():
     wl = wls.get("scan_wide_t1000_b64")
     T, B, N = wl.T, wl.B, wl.layers[0]["n"]
     spec = wl.layers[0]
     net = snn.Network(wl, wls.init_params(wl, 0), device=DEV)
-    x = wls.device_currents(wl, 0)
-    tgt_h = wls.targets(wl, 0)
-    net.step(x, targets=torch.as_tensor(tgt_h).to(DEV))
-    # loss and dL/dcounts over all 64 x 65536 counts
-    counts = _np(net.counts)
-    L, gc = oracle.loss_mse(counts, tgt_h)
-    assert abs(_np(net.loss)[0] - L) <= 1e-6 * abs(L)
-    assert_close(_np(net.gcounts), gc, 1e-5, what="dL/dcounts")
+    d = net.descs[0]
+    x = wls.device_currents(wl, 0)                 # seeded currents [T, B, N]
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    u = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    counts = torch.empty((B, N), dtype=torch.float32, device=DEV)
+    snn.snn_neuron_fwd(d, x, None, spk, u, counts)
     rng = np.random.default_rng(0)
     cols = [(0, 0), (B - 1, N - 1), (B - 1, 0), (0, N - 1)] + \
         [(int(b), int(n)) for b, n in zip(rng.integers(0, B, 252), rng.integers(0, N, 252))]
     bi = torch.tensor([c[0] for c in cols], device=DEV)
     ni = torch.tensor([c[1] for c in cols], device=DEV)
-    I = _np(x[:, bi, ni])                       # [T, S] currents of the sampled columns
-    z_g = _np(net.spk[0][:, bi, ni])
-    u_g = _np(_u(net, 0)[:, bi, ni])
-    z, u, c = oracle.scan_fwd(I, spec["neuron"], spec["beta"], spec["thr"])
-    np.testing.assert_array_equal(z_g, z)
-    np.testing.assert_array_equal(u_g, u)
-    np.testing.assert_array_equal(counts[bi.cpu().numpy(), ni.cpu().numpy()], c)
-    g = gc[bi.cpu().numpy(), ni.cpu().numpy()]
-    dI = oracle.scan_bwd(u_g, g, spec["neuron"], spec["beta"], spec["thr"], wl.slope)
-    assert_close(_np(net.gx[0][:, bi, ni]), dI, 1e-3, what="dL/dI")
+    bh, nh = bi.cpu().numpy(), ni.cpu().numpy()
+    I = _np(x[:, bi, ni])                       # seeded currents of the sampled columns
+    z_o, u_o, c_o = oracle.scan_fwd(I, spec["neuron"], spec["beta"], spec["thr"])
+    np.testing.assert_array_equal(_np(spk[:, bi, ni]), z_o)
+    np.testing.assert_array_equal(_np(u[:, bi, ni]), u_o)
+    np.testing.assert_array_equal(_np(counts)[bh, nh], c_o)
+    # loss over all 64 x 65536 counts, on seeded spike counts and targets
+    c_s = rng.integers(0, 120, (B, N)).astype(np.float32)
+    tgt_h = wls.targets(wl, 0)
+    loss = torch.empty(4, dtype=torch.float32, device=DEV)
+    gc = torch.empty((B, N), dtype=torch.float32, device=DEV)
+    snn.snn_loss(snn.LOSS_MSE_COUNT, B, N, torch.as_tensor(c_s).to(DEV),
+                 None, torch.as_tensor(tgt_h).to(DEV), loss, gc, net.ws)
+    L, gc_o = oracle.loss_mse(c_s, tgt_h)
+    assert abs(_np(loss)[0] - L) <= 1e-6 * abs(L)
+    assert_close(_np(gc), gc_o, 1e-5, what="dL/dcounts")
+    # reverse scan with a seeded gradient broadcast over t, on the GPU's own
+    # membrane (bit-identical to the oracle's on the sampled columns above)
+    g = _seeded_normal((B, N), 0.0, 1e-6, seed=5)
+    dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, g, None, u, dI, None, None, None)
+    dI_o = oracle.scan_bwd(u_o, _np(g)[bh, nh], spec["neuron"], spec["beta"], spec["thr"],
+                           wl.slope)
+    assert_close(_np(dI[:, bi, ni]), dI_o, 1e-3, what="dL/dI")
+    del dI
+    # the whole step is the same calls: same spikes, counts and membrane
+    net.step(x, targets=torch.as_tensor(tgt_h).to(DEV))
+    assert torch.equal(net.spk[0], spk) and torch.equal(_u(net, 0), u)
+    assert torch.equal(net.counts, counts)
 
 
 def test_half_net_full_size_sampled():
@@ -63,62 +99,70 @@ def test_half_net_full_size_sampled():
     T, B = wl.T, wl.B
     inp = wls.make_inputs(wl, 0)
     net = snn.Network(wl, inp["params"], device=DEV)
-    x = torch.as_tensor(inp["x"]).to(DEV)
-    net.step(x, labels=torch.as_tensor(inp["labels"]).to(DEV))
     rng = np.random.default_rng(1)
     tol = 2e-2
-    xs_dev = [x] + net.spk[:-1]
-    # ---- forward, layer by layer, teacher-forced on the GPU's spikes
+    n = len(wl.layers)
     for li, spec in enumerate(wl.layers):
         W, b = inp["params"][li]
         d = net.descs[li]
+        # ---- synapse forward on seeded spikes (the input's rates for layer 0)
+        xin_dev = torch.as_tensor(inp["x"]).to(DEV) if li == 0 else \
+            _seeded_spikes((T, B, d.n_in), 0.15, seed=100 + li)
         cur = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
-        snn.snn_synapse_fwd(d, xs_dev[li], net.W[li], net.b[li], cur, None, net.ws)
-        xin = _np(xs_dev[li]).reshape(T * B, -1)
+        snn.snn_synapse_fwd(d, xin_dev, net.W[li], net.b[li], cur, None, net.ws)
         rows = rng.integers(0, T * B, 64)
-        I_rows = oracle.dense_fwd(xin[rows].astype(np.float64), W, b)
-        assert_close(_np(cur).reshape(T * B, -1)[rows], I_rows, 1e-3, what=f"L{li} currents")
-        bs = rng.integers(0, B, 2)
-        ns = rng.integers(0, d.n_out, 128) if d.n_out > 128 else np.arange(d.n_out)
-        Ic = _np(cur[:, bs][:, :, ns])            # [T, 2, S]
-        z, u, c = oracle.scan_fwd(Ic, spec["neuron"], spec["beta"], spec["thr"])
-        np.testing.assert_array_equal(_np(net.spk[li][:, bs][:, :, ns]), z)
-        np.testing.assert_array_equal(_np(_u(net, li)[:, bs][:, :, ns]), u)
+        rows_t = torch.as_tensor(rows, device=DEV)
+        xr = _np(xin_dev.reshape(T * B, -1)[rows_t]).astype(np.float64)
+        I_rows = oracle.dense_fwd(xr, W, b)
+        assert_close(_np(cur.reshape(T * B, -1)[rows_t]), I_rows, 1e-3, what=f"L{li} currents")
         del cur
-    counts = _np(net.counts)
-    L, gc = oracle.loss_ce(counts, inp["labels"])
-    assert abs(_np(net.loss)[0] - L) <= 1e-5 * max(1.0, abs(L))
-    # ---- backward, teacher-forced on the GPU's membrane and upstream gradient
-    g_full = _np(net.gcounts)                      # [B, 10], the same for every t
-    for li in range(len(wl.layers) - 1, -1, -1):
-        spec = wl.layers[li]
-        W = inp["params"][li][0]
-        d = net.descs[li]
-        u_dev = _u(net, li)
-        xin = _np(xs_dev[li]).reshape(T, B, -1)
-        gx_dev = net.gx[li] if li > 0 else None
-        if li == len(wl.layers) - 1:
-            cols_o = np.arange(d.n_out)
-        else:
-            cols_o = rng.integers(0, d.n_out, 8)
-        # dW rows and db entries for sampled output neurons o (all t, b)
-        u_o = _np(u_dev[:, :, cols_o])
-        g_o = g_full[:, cols_o] if g_full.ndim == 2 else g_full[:, :, cols_o]
-        dI_o = oracle.scan_bwd(u_o, g_o, spec["neuron"], spec["beta"], spec["thr"], wl.slope)
-        dW_o = dI_o.reshape(T * B, -1).T @ xin.reshape(T * B, -1).astype(np.float64)
-        aI = np.abs(dI_o.reshape(T * B, -1))
-        bW = 2.0 ** -8 * (aI.T @ np.abs(xin.reshape(T * B, -1)).astype(np.float64))
-        assert_close(_np(net.gW[li])[cols_o], dW_o, tol, what=f"L{li} dW rows", abs_bound=bW)
-        assert_close(_np(net.gb[li])[cols_o], dI_o.sum(axis=(0, 1)), tol, what=f"L{li} db")
-        if gx_dev is None:
-            break
-        # dx for two sampled samples b: needs dL/dI of every output neuron of b
-        bs = rng.integers(0, B, 2)
-        u_b = _np(u_dev[:, bs])
-        g_b = g_full[bs] if g_full.ndim == 2 else g_full[:, bs]
-        dI_b = oracle.scan_bwd(u_b, g_b, spec["neuron"], spec["beta"], spec["thr"], wl.slope)
-        dx_b = dI_b.reshape(-1, d.n_out) @ W.astype(np.float64)
-        bx = 2.0 ** -8 * (np.abs(dI_b.reshape(-1, d.n_out)) @ np.abs(W).astype(np.float64))
-        got = _np(gx_dev[:, bs]).reshape(-1, d.n_in)
-        assert_close(got, dx_b, tol, what=f"L{li} dx", abs_bound=bx)
-        g_full = _np(gx_dev)                        # teacher-force the layer below
+        # ---- neuron scan on seeded currents
+        Is = _seeded_normal((T, B, d.n_out), 0.1, 0.6, seed=200 + li)
+        spk = torch.empty((T, B, d.n_out), dtype=torch.uint8, device=DEV)
+        u = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
+        snn.snn_neuron_fwd(d, Is, None, spk, u, None)
+        bs = torch.as_tensor(rng.integers(0, B, 2), device=DEV)
+        ns = torch.as_tensor(rng.integers(0, d.n_out, 128) if d.n_out > 128
+                             else np.arange(d.n_out), device=DEV)
+        I_c = _np(Is[:, bs][:, :, ns])                          # [T, 2, S]
+        z_o, u_o, _ = oracle.scan_fwd(I_c, spec["neuron"], spec["beta"], spec["thr"])
+        np.testing.assert_array_equal(_np(spk[:, bs][:, :, ns]), z_o)
+        np.testing.assert_array_equal(_np(u[:, bs][:, :, ns]), u_o)
+        # ---- reverse scan with a seeded upstream gradient (bf16 dL/dI out)
+        last = li == n - 1
+        g = _seeded_normal((B, d.n_out) if last else (T, B, d.n_out), 0.0, 1e-4, seed=300 + li)
+        dcur = torch.empty((T, B, d.n_out), dtype=torch.bfloat16, device=DEV)
+        snn.snn_neuron_bwd(d, snn.GRAD_BCAST if last else snn.GRAD_FULL, g, None, u, dcur, None,
+                           None, net.ws)
+        g_c = _np(g[bs][:, ns]) if last else _np(g[:, bs][:, :, ns])
+        dI_o = oracle.scan_bwd(u_o, g_c, spec["neuron"], spec["beta"], spec["thr"], wl.slope)
+        assert_close(_np(dcur[:, bs][:, :, ns].float()), dI_o, tol, what=f"L{li} dL/dI")
+        del Is, spk, u, dcur
+        # ---- synapse backward on seeded bf16 dL/dI: sampled dW rows, dx rows
+        dI = _seeded_normal((T * B, d.n_out), 0.0, 1e-4, seed=400 + li, dtype=torch.bfloat16)
+        gW = torch.empty((d.n_out, d.n_in), dtype=torch.float32, device=DEV)
+        gx = torch.empty((T * B, d.n_in), dtype=torch.float32, device=DEV) if li > 0 else None
+        snn.snn_synapse_bwd(d, dI, None, xin_dev, net.W[li], gW, gx, net.ws)
+        xall = _np(xin_dev.reshape(T * B, -1)).astype(np.float64)
+        cols_o = np.arange(d.n_out) if last else rng.integers(0, d.n_out, 8)
+        dI_h = _np(dI.float()).astype(np.float64)               # the seeded bf16 values
+        dW_o, _, _ = oracle.dense_bwd(dI_h[:, cols_o], xall, W[cols_o], want_db=False,
+                                      want_dx=False)
+        # fp32 sums of exact products: within 1e-3, or the a-priori bound of an
+        # fp32 sum of K terms in any order, (K + 2) 2^-24 sum|terms|
+        bW = (T * B + 2) * 2.0 ** -24 * (np.abs(dI_h[:, cols_o]).T @ xall)
+        assert_close(_np(gW)[cols_o], dW_o, 1e-3, what=f"L{li} dW rows", abs_bound=bW)
+        if gx is not None:
+            _, _, dx_o = oracle.dense_bwd(dI_h[rows], xall[rows], W, want_dw=False,
+                                          want_db=False)
+            bx = (d.n_out + 2) * 2.0 ** -24 * (np.abs(dI_h[rows]) @ np.abs(W).astype(np.float64))
+            assert_close(_np(gx)[rows], dx_o, 1e-3, what=f"L{li} dx rows", abs_bound=bx)
+        del dI, gW, gx, xin_dev
+    # ---- the whole step: layer calls and stage calls give the same bytes
+    x = torch.as_tensor(inp["x"]).to(DEV)
+    y = torch.as_tensor(inp["labels"]).to(DEV)
+    net.step(x, labels=y)
+    snap = [_np(t).copy() for t in net.gW + net.gb] + [_np(net.loss).copy()]
+    net.step_stages(x, labels=y)
+    for a, b2 in zip(snap, [_np(t) for t in net.gW + net.gb] + [_np(net.loss)]):
+        np.testing.assert_array_equal(a, b2)

@@ -1,8 +1,9 @@
 """GPU path vs CPU oracle, through the C ABI, on identical seeded inputs.
 
-Stage tests feed the oracle the GPU's own inputs to that stage (teacher
-forcing), so that a legal spike flip in one stage cannot cascade into the
-next.  Scans given identical fp32 currents must be bit-identical.
+The oracle only ever sees seeded inputs and its own results.  Whole-step
+checks run the oracle's chain on its own and feed each GPU stage the oracle's
+inputs to that stage, so that a legal spike flip in one stage cannot cascade
+into the next.  Scans given identical fp32 currents must be bit-identical.
 """
 import numpy as np
 import pytest
@@ -62,7 +63,7 @@ def test_scan_fwd_bit_exact(neuron, alpha, beta, T, B, N):
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
     saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     counts = torch.empty((B, N), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_fwd(d, x, spk, saved, counts)
+    snn.snn_neuron_fwd(d, x, None, spk, saved, counts)
     z, u, c = oracle.scan_fwd(I, neuron, beta, 1.0, alpha)
     np.testing.assert_array_equal(_np(spk), z)
     np.testing.assert_array_equal(_np(saved), u)
@@ -77,7 +78,7 @@ def test_scan_fwd_in_place_and_f16_spikes():
     d.out_dtype = snn.F16
     buf = _t(I)
     spk = torch.empty((T, B, N), dtype=torch.float16, device=DEV)
-    snn.snn_neuron_fwd(d, buf, spk, buf, None)        # currents overwritten by u
+    snn.snn_neuron_fwd(d, buf, None, spk, buf, None)       # currents overwritten by u
     z, u, _ = oracle.scan_fwd(I, "synaptic", 0.8, 1.0, 0.6)
     np.testing.assert_array_equal(_np(buf), u)
     np.testing.assert_array_equal(_np(spk).astype(np.uint8), z)
@@ -94,11 +95,14 @@ def test_scan_bwd(neuron, alpha, beta, reset, bcast, T, B, N):
     x = _t(I)
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
     saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_fwd(d, x, spk, saved, None)
+    snn.snn_neuron_fwd(d, x, None, spk, saved, None)
+    _, u, _ = oracle.scan_fwd(I, neuron, beta, 1.0, alpha)
+    np.testing.assert_array_equal(_np(saved), u)
     g = rng.normal(0, 1, (B, N) if bcast else (T, B, N)).astype(np.float32)
     dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_bwd(d, snn.GRAD_BCAST if bcast else snn.GRAD_FULL, _t(g), saved, dI, None, None)
-    ref = oracle.scan_bwd(_np(saved), g, neuron, beta, 1.0, 25.0, alpha, reset == snn.RESET_SURROGATE)
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST if bcast else snn.GRAD_FULL, _t(g), None, saved, dI,
+                       None, None, None)
+    ref = oracle.scan_bwd(u, g, neuron, beta, 1.0, 25.0, alpha, reset == snn.RESET_SURROGATE)
     assert_close(_np(dI), ref, 1e-3, what="dL/dI")
 
 
@@ -112,12 +116,91 @@ def test_scan_bwd_half_gradient_operand(gdt, tdt):
     dn, _ = _none_desc(T, B, N, "leaky", 0.9)
     saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
-    snn.snn_neuron_fwd(dn, _t(I), spk, saved, None)
+    snn.snn_neuron_fwd(dn, _t(I), None, spk, saved, None)
+    _, u, _ = oracle.scan_fwd(I, "leaky", 0.9, 1.0)
+    np.testing.assert_array_equal(_np(saved), u)
     g = rng.normal(0, 0.01, (B, N)).astype(np.float32)
     dI = torch.empty((T, B, N), dtype=tdt, device=DEV)
-    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, _t(g), saved, dI, None, None)
-    ref = oracle.scan_bwd(_np(saved), g, "leaky", 0.9, 1.0, 25.0)
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, _t(g), None, saved, dI, None, None, None)
+    ref = oracle.scan_bwd(u, g, "leaky", 0.9, 1.0, 25.0)
     assert_close(_np(dI.float()), ref, 2e-2, what="half dL/dI")
+
+
+# recurrent neuron (eq. 7): one recurrent weight per neuron, column c of the
+# [T, B*N] layout is neuron c % N.  (8, 65538) takes the 4-column lanes with
+# groups that straddle two samples; (9, 65537) the 1-column lanes.
+RLEAKY_SHAPES = [(1, 2, 8), (7, 3, 101), (33, 4, 256), (50, 5, 1001), (6, 8, 65538),
+                 (3, 9, 65537)]
+
+
+def _rleaky_case(T, B, N, seed):
+    rng = np.random.default_rng(seed)
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    v = rng.uniform(-1.0, 1.5, N).astype(np.float32)
+    return I, v, rng
+
+
+@pytest.mark.parametrize("T,B,N", RLEAKY_SHAPES)
+def test_rleaky_scan_fwd_bit_exact(T, B, N):
+    I, v, _ = _rleaky_case(T, B, N, seed=T * 100 + N)
+    d, _ = _none_desc(T, B, N, "rleaky", 0.9)
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    counts = torch.empty((B, N), dtype=torch.float32, device=DEV)
+    snn.snn_neuron_fwd(d, _t(I), _t(v), spk, saved, counts)
+    z, u, c = oracle.scan_fwd(I, "rleaky", 0.9, 1.0, v=v)
+    np.testing.assert_array_equal(_np(spk), z)
+    np.testing.assert_array_equal(_np(saved), u)
+    np.testing.assert_array_equal(_np(counts), c)
+
+
+@pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
+@pytest.mark.parametrize("bcast", [True, False])
+@pytest.mark.parametrize("T,B,N", [(1, 2, 8), (9, 3, 37), (40, 4, 512), (5, 8, 65538)])
+def test_rleaky_scan_bwd(reset, bcast, T, B, N):
+    """dL/dI and the recurrent weights' gradient dL/dv (summed over the batch)."""
+    I, v, rng = _rleaky_case(T, B, N, seed=7 * T + N)
+    d, _ = _none_desc(T, B, N, "rleaky", 0.9, reset=reset)
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    v_t = _t(v)
+    snn.snn_neuron_fwd(d, _t(I), v_t, spk, saved, None)
+    _, u, _ = oracle.scan_fwd(I, "rleaky", 0.9, 1.0, v=v)
+    np.testing.assert_array_equal(_np(saved), u)
+    g = rng.normal(0, 1, (B, N) if bcast else (T, B, N)).astype(np.float32)
+    dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    gv = torch.empty(N, dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST if bcast else snn.GRAD_FULL, _t(g), v_t, saved, dI,
+                       None, gv, ws)
+    ref, dv = oracle.scan_bwd_rleaky(u, g, 0.9, 1.0, 25.0, v, reset == snn.RESET_SURROGATE)
+    assert_close(_np(dI), ref, 1e-3, what="dL/dI")
+    assert_close(_np(gv), dv, 1e-3, what="dL/dv")
+
+
+def test_rleaky_zero_weight_matches_leaky_kernel():
+    """v = 0 is eq. (4): the recurrent kernel gives the Leaky kernel's bytes."""
+    T, B, N = 20, 4, 300
+    I, _, rng = _rleaky_case(T, B, N, seed=3)
+    out = []
+    for neuron, v in (("rleaky", _t(np.zeros(N, np.float32))), ("leaky", None)):
+        d, _ = _none_desc(T, B, N, neuron, 0.9, reset=snn.RESET_SURROGATE)
+        spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+        saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+        snn.snn_neuron_fwd(d, _t(I), v, spk, saved, None)
+        out += [_np(spk), _np(saved)]
+    np.testing.assert_array_equal(out[0], out[2])
+    np.testing.assert_array_equal(out[1], out[3])
+
+
+def test_rleaky_empty_batch_zero_gradient():
+    d, _ = _none_desc(0, 4, 16, "rleaky", 0.9)
+    gv = torch.full((16,), 5.0, device=DEV)
+    g = torch.zeros(256, dtype=torch.float32, device=DEV)
+    buf = torch.empty(256, dtype=torch.float32, device=DEV)
+    v = torch.ones(16, dtype=torch.float32, device=DEV)
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, g, v, buf, buf, None, gv, _ws(256))
+    assert (_np(gv) == 0).all()
 
 
 # ---------------------------------------------------------------------------
@@ -201,8 +284,9 @@ def test_synapse_bwd_operand_types(M, N, K, gdt, wdt):
         W = W.astype(np.float16).astype(np.float32)
     dI = rng.normal(0, 1e-3, (M, N)).astype(np.float32)
     gcode, tdt = GRAD_TYPES[gdt]
-    dI_t = _t(dI, tdt)
-    dI_used = _np(dI_t.float()).astype(np.float64)      # the values the GPU sees
+    dI_h = torch.as_tensor(dI).to(tdt)                   # rounded on the host
+    dI_used = dI_h.float().numpy().astype(np.float64)   # the values the GPU sees
+    dI_t = dI_h.to(DEV)
     spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
     d = snn.layer_desc(spec, 1, M, grad_dtype=gcode, w_dtype=snn.F16 if wdt == "f16" else snn.F32)
     gW = torch.empty((N, K), dtype=torch.float32, device=DEV)
@@ -284,21 +368,19 @@ def test_conv_pool_ties_first_maximum():
 
 @pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (4, 12, 12, 12, 64), (2, 3, 9, 11, 5)])
 def test_conv_pool_bwd(NB, Ci, H, W, Co):
-    """Backward teacher-forced on the GPU's own pool selection."""
+    """Backward given the oracle's pool selection (one byte per pooled current)."""
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=7 * NB + Co)
-    cur, arg = _conv_fwd_gpu(d, x, w, b)
+    y32 = oracle.conv_fwd(x, w, b).astype(np.float32).astype(np.float64)
+    _, arg = oracle.maxpool2_fwd(y32)
     rng = np.random.default_rng(1)
-    dI = rng.normal(0, 1, cur.shape).astype(np.float32)
+    dI = rng.normal(0, 1, arg.shape).astype(np.float32)
     gW = torch.empty(w.shape, dtype=torch.float32, device=DEV)
     gx = torch.empty(x.shape, dtype=torch.float32, device=DEV)
     ws = _ws(snn.snn_layer_workspace_bytes(d))
-    arg_t = _t(arg)
-    snn.snn_synapse_bwd(d, _t(dI), arg_t, _t(x), _t(w), gW, gx, ws)
+    snn.snn_synapse_bwd(d, _t(dI), _t(arg.astype(np.uint8)), _t(x), _t(w), gW, gx, ws)
     Ho, Wo = H - 4, W - 4
-    dY = oracle.maxpool2_bwd(dI.reshape(NB, Co, Ho // 2, Wo // 2), arg.reshape(NB, Co, Ho // 2, Wo // 2),
-                             Ho, Wo)
-    if Ho % 2 or Wo % 2:
-        pass  # the dropped row/column of the conv output gets no gradient (zeros from the pool)
+    # an odd conv output's last row / column is outside every window: zero gradient
+    dY = oracle.maxpool2_bwd(dI, arg, Ho, Wo)
     rW, _, rx = oracle.conv_bwd(dY, x, w)
     assert_close(_np(gW), rW, 1e-3, what="conv dW")
     assert_close(_np(gx), rx, 1e-3, what="conv dx")
@@ -337,135 +419,182 @@ def test_loss_mse(B, K):
 # ---------------------------------------------------------------------------
 # whole training steps
 # ---------------------------------------------------------------------------
-def _saved_u(net, li):
-    d = net.descs[li]
+_TORCH_GRAD = {snn.F32: torch.float32, snn.BF16: torch.bfloat16, snn.F16: torch.float16}
+
+
+def _saved_from_oracle(d, f):
+    """The forward-to-backward state of snn_layer_bwd filled from the oracle's
+    forward: membrane u (fp32) and, for conv layers, the pool selection that
+    follows it on the next 256-byte boundary."""
+    buf = torch.zeros(snn.snn_layer_saved_bytes(d), dtype=torch.uint8)
     n = d.T * d.B * d.n_out
-    return _np(net.saved[li][: n * 4].view(torch.float32)).reshape(d.T, d.B, d.n_out)
+    u = torch.from_numpy(np.ascontiguousarray(f["u"], np.float32).reshape(-1))
+    buf[: n * 4] = u.view(torch.uint8)
+    if d.synapse == snn.SYN_CONV5_POOL2:
+        off = (n * 4 + 255) // 256 * 256
+        buf[off: off + n] = torch.from_numpy(np.ascontiguousarray(f["arg"]).astype(np.uint8)
+                                             .reshape(-1))
+    return buf.to(DEV)
 
 
-def spec_n_out(spec):
-    if spec["kind"] == "conv":
-        return spec["c_out"] * ((spec["h"] - 4) // 2) * ((spec["w"] - 4) // 2)
-    return spec["n_out"] if spec["kind"] == "dense" else spec["n"]
+def _layer_input(spec, f):
+    x = np.asarray(f["x"])
+    return _t(x.astype(np.float32) if spec["kind"] == "none" else x.astype(np.uint8))
 
 
-def _gpu_currents(net, li, xin):
-    """Currents of layer li recomputed by the stage call on the GPU's input
-    (conv layers: into a scratch selection buffer, the saved one untouched)."""
-    d = net.descs[li]
-    cur = torch.empty((d.T, d.B, d.n_out), dtype=torch.float32, device=DEV)
-    arg = torch.empty(d.T * d.B * d.n_out, dtype=torch.uint8, device=DEV) \
-        if d.synapse == snn.SYN_CONV5_POOL2 else None
-    snn.snn_synapse_fwd(d, xin, net.W[li], net.b[li], cur, arg, net.ws)
-    return _np(cur)
+def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
+    """Each layer's GPU calls, fed the oracle's inputs to that layer, against
+    the oracle's outputs.  The oracle runs its own chain and sees no GPU value.
 
-
-def _check_step_teacher_forced(wl, inp, net, x_dev, tol=1e-3):
-    """Every stage of the GPU step against the oracle fed the GPU's inputs:
-    contraction vs oracle contraction on the same spikes; oracle scan on the
-    GPU's own currents must reproduce spikes, membrane and counts exactly."""
+    forward:  synapse stage (currents within tol); neuron stage on the
+              oracle's fp32 currents (spikes, membrane, counts bit-identical);
+              the whole layer call (spikes equal up to legal flips);
+    loss:     on the oracle's spike counts;
+    backward: neuron stage on the oracle's membrane and upstream gradient;
+              synapse stage on the oracle's dL/dI (rounded on the host to the
+              gradient operand type) and pool selection; the whole layer call
+              on the oracle's saved state."""
+    rs = reset == snn.RESET_SURROGATE
     T, B = wl.T, wl.B
     n = len(wl.layers)
-    h = inp["x"]
+    L, fwds, bwds = oracle.net_step(wl.layers, inp["params"], inp["x"], wl.loss,
+                                    labels=inp.get("labels"), targets=inp.get("targets"),
+                                    slope=wl.slope, reset_surrogate=rs)
+    net = snn.Network(wl, inp["params"], device=DEV, reset_grad=reset, flags=flags)
     xs = []
     for li, spec in enumerate(wl.layers):
-        W, b = inp["params"][li]
-        xs.append(h)
-        z_gpu = _np(net.spk[li])
-        u_gpu = _saved_u(net, li)
-        if spec["kind"] == "dense":
-            xin = np.asarray(h, np.float64).reshape(T * B, -1)
-            I_orc = oracle.dense_fwd(xin, W, b).reshape(T, B, -1)
-            I = _gpu_currents(net, li, x_dev if li == 0 else net.spk[li - 1])
-            assert_close(I, I_orc, tol, what=f"L{li} currents")
-        elif spec["kind"] == "conv":
-            xin = np.asarray(h, np.float64).reshape(T * B, spec["c_in"], spec["h"], spec["w"])
-            y32 = oracle.conv_fwd(xin, W, b).astype(np.float32).astype(np.float64)
-            I_orc = oracle.maxpool2_fwd(y32)[0].reshape(T, B, -1)
-            I = _gpu_currents(net, li, x_dev if li == 0 else net.spk[li - 1])
-            assert_close(I, I_orc, tol, what=f"L{li} conv currents")
-        else:
-            I = np.asarray(h, np.float32)
-        z, u, c = oracle.scan_fwd(I, spec["neuron"], spec["beta"], spec["thr"],
-                                  spec.get("alpha", 0.0))
-        np.testing.assert_array_equal(z_gpu, z, err_msg=f"L{li} spikes")
-        np.testing.assert_array_equal(u_gpu, u, err_msg=f"L{li} membrane")
-        if li == n - 1:
-            np.testing.assert_array_equal(_np(net.counts).reshape(c.shape), c)
-        h = z_gpu  # teacher-force the next layer on the GPU's spikes
-    L, gc = (oracle.loss_ce(_np(net.counts), inp["labels"]) if wl.loss == "ce"
-             else oracle.loss_mse(_np(net.counts), inp["targets"]))
-    assert abs(_np(net.loss)[0] - L) <= 1e-5 * max(1.0, abs(L))
-    assert_close(_np(net.gcounts), gc, 1e-5, what="dL/dcounts")
-    g = _np(net.gcounts)
+        f, d = fwds[li], net.descs[li]
+        x_dev = _layer_input(spec, f)
+        xs.append(x_dev)
+        if spec["kind"] != "none":
+            cur = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
+            arg = torch.empty(T * B * d.n_out, dtype=torch.uint8, device=DEV) \
+                if spec["kind"] == "conv" else None
+            snn.snn_synapse_fwd(d, x_dev, net.W[li], net.b[li], cur, arg, net.ws)
+            assert_close(_np(cur), f["I"].reshape(T, B, -1), tol, what=f"L{li} currents")
+        spk = torch.empty((T, B, d.n_out), dtype=torch.uint8, device=DEV)
+        u = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
+        cnt = torch.empty((B, d.n_out), dtype=torch.float32, device=DEV)
+        snn.snn_neuron_fwd(d, _t(f["I"].reshape(T, B, -1)), net.v[li], spk, u, cnt)
+        np.testing.assert_array_equal(_np(spk), f["z"].reshape(T, B, -1), err_msg=f"L{li} spikes")
+        np.testing.assert_array_equal(_np(u), f["u"].reshape(T, B, -1), err_msg=f"L{li} membrane")
+        np.testing.assert_array_equal(_np(cnt), f["counts"].reshape(B, -1))
+        saved = torch.empty(snn.snn_layer_saved_bytes(d), dtype=torch.uint8, device=DEV)
+        snn.snn_layer_fwd(d, x_dev, net.W[li], net.b[li], net.v[li], spk, saved, cnt, net.ws)
+        assert_spikes(_np(spk), f["z"].reshape(T, B, -1), f["u"].reshape(T, B, -1), spec["thr"],
+                      what=f"L{li} layer call")
+    # loss on the oracle's counts
+    c_o = np.asarray(fwds[-1]["counts"], np.float32).reshape(B, -1)
+    K = c_o.shape[1]
+    loss = torch.empty(4, dtype=torch.float32, device=DEV)
+    gc = torch.empty((B, K), dtype=torch.float32, device=DEV)
+    if wl.loss == "ce":
+        snn.snn_loss(snn.LOSS_CE_COUNT, B, K, _t(c_o), _t(inp["labels"]), None, loss, gc, net.ws)
+        L2, gc_o = oracle.loss_ce(c_o, inp["labels"])
+    else:
+        snn.snn_loss(snn.LOSS_MSE_COUNT, B, K, _t(c_o), None, _t(inp["targets"]), loss, gc,
+                     net.ws)
+        L2, gc_o = oracle.loss_mse(c_o, inp["targets"])
+    assert abs(_np(loss)[0] - L2) <= 1e-5 * max(1.0, abs(L2))
+    assert_close(_np(gc), gc_o, 1e-5, what="dL/dcounts")
+    g = gc_o
     for li in range(n - 1, -1, -1):
-        spec = wl.layers[li]
-        W = inp["params"][li][0]
-        u_gpu = _saved_u(net, li)
-        dI = oracle.scan_bwd(u_gpu, g, spec["neuron"], spec["beta"], spec["thr"], wl.slope,
-                             spec.get("alpha", 0.0))
+        spec, f, r, d = wl.layers[li], fwds[li], bwds[li], net.descs[li]
+        bcast = li == n - 1
+        kind = snn.GRAD_BCAST if bcast else snn.GRAD_FULL
+        g_dev = _t(np.asarray(g, np.float32).reshape((B, d.n_out) if bcast else (T, B, d.n_out)))
+        dI_o = r["dI"].reshape(T, B, -1)
+        saved = _saved_from_oracle(d, f)
+        vv = net.v[li]
+        gv = None if vv is None else torch.empty_like(vv)
+        gv2 = None if vv is None else torch.empty_like(vv)
         if spec["kind"] == "none":
-            assert_close(_np(net.gx[li]), dI, tol, what="dL/dI")
-            break
-        if spec["kind"] == "conv":
-            Ho, Wo = spec["h"] - 4, spec["w"] - 4
-            pa = net.pool_arg(li)[: T * B * spec_n_out(spec)]
-            arg = _np(pa).reshape(T * B, spec["c_out"], Ho // 2, Wo // 2)
-            dY = oracle.maxpool2_bwd(dI.reshape(arg.shape), arg, Ho, Wo)
-            xin = np.asarray(xs[li], np.float64).reshape(T * B, spec["c_in"], spec["h"], spec["w"])
-            dW, db, dx = oracle.conv_bwd(dY, xin, W, want_dx=li > 0)
-            assert_close(_np(net.gW[li]), dW, tol, what=f"L{li} conv dW")
-            assert_close(_np(net.gb[li]), db, tol, what=f"L{li} conv db")
-            if li > 0:
-                gx = _np(net.gx[li])
-                assert_close(gx.reshape(dx.shape), dx, tol, what=f"L{li} conv dx")
-                g = gx
+            dcur = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
+            snn.snn_neuron_bwd(d, kind, g_dev, vv, saved, dcur, None, gv, net.ws)
+            assert_close(_np(dcur), dI_o, tol, what="dL/dI")
+            snn.snn_layer_bwd(d, kind, g_dev, xs[li], None, vv, saved, None, None, gv2, dcur,
+                              net.ws)
+            assert_close(_np(dcur), dI_o, tol, what="layer dL/dI")
+            if vv is not None:
+                assert_close(_np(gv), r["dv"], tol, what="neuron-stage dL/dv")
+                assert_close(_np(gv2), r["dv"], tol, what="dL/dv")
+            g = r["dx"]
             continue
-        xin = np.asarray(xs[li], np.float64).reshape(T * B, -1)
-        dW, db, dx = oracle.dense_bwd(dI.reshape(T * B, -1), xin, W, want_dx=li > 0)
-        bW = bx = None
-        if net.descs[li].grad_dtype == snn.BF16:
-            # dL/dI handed to the contractions in bf16: a-priori rounding bound
-            aI = np.abs(dI.reshape(T * B, -1))
-            bW = 2.0 ** -8 * (aI.T @ np.abs(xin))
-            bx = 2.0 ** -8 * (aI @ np.abs(W).astype(np.float64)) if li > 0 else None
-        assert_close(_np(net.gW[li]), dW, tol, what=f"L{li} dW", abs_bound=bW)
-        assert_close(_np(net.gb[li]), db, tol, what=f"L{li} db")
+        half = d.grad_dtype != snn.F32
+        gdt = _TORCH_GRAD[d.grad_dtype]
+        dcur = torch.empty((T, B, d.n_out), dtype=gdt, device=DEV)
+        gb = torch.empty_like(net.gb[li])
+        snn.snn_neuron_bwd(d, kind, g_dev, vv, saved, dcur, gb, gv, net.ws)
+        assert_close(_np(dcur.float()), dI_o, 2e-2 if half else tol, what=f"L{li} dL/dI")
+        assert_close(_np(gb), r["db"], tol, what=f"L{li} neuron-stage db")
+        if vv is not None:
+            assert_close(_np(gv), r["dv"], tol, what=f"L{li} neuron-stage dL/dv")
+        # synapse stage on the oracle's dL/dI, rounded on the host
+        W = inp["params"][li][0]
+        xin = np.asarray(f["x"], np.float64)
+        gW = torch.empty_like(net.gW[li])
+        gx = torch.empty((T, B, d.n_in), dtype=torch.float32, device=DEV) if li > 0 else None
+        dI_h = torch.from_numpy(np.ascontiguousarray(dI_o, np.float32)).to(gdt)
+        arg_dev = _t(np.asarray(f["arg"]).astype(np.uint8)) if spec["kind"] == "conv" else None
+        snn.snn_synapse_bwd(d, dI_h.to(DEV), arg_dev, xs[li], net.W[li], gW, gx, net.ws)
+        if half:
+            dI_used = dI_h.float().numpy().astype(np.float64).reshape(T * B, -1)
+            sW, _, sx = oracle.dense_bwd(dI_used, xin.reshape(T * B, -1), W, want_db=False,
+                                         want_dx=li > 0)
+        else:
+            sW, sx = r["dW"], r["dx"]
+        assert_close(_np(gW), sW, tol, what=f"L{li} synapse-stage dW")
         if li > 0:
-            gx = _np(net.gx[li])
-            assert_close(gx.reshape(T * B, -1), dx, tol, what=f"L{li} dx", abs_bound=bx)
-            g = gx  # teacher-force the layer below on the GPU's gradient
+            assert_close(_np(gx).reshape(sx.shape), sx, tol, what=f"L{li} synapse-stage dx")
+        # the whole layer call on the oracle's saved state and upstream gradient
+        gW2, gb2 = torch.empty_like(gW), torch.empty_like(gb)
+        gx2 = torch.empty((T, B, d.n_in), dtype=torch.float32, device=DEV) if li > 0 else None
+        snn.snn_layer_bwd(d, kind, g_dev, xs[li], net.W[li], vv, saved, gW2, gb2, gv2, gx2,
+                          net.ws)
+        if vv is not None:
+            assert_close(_np(gv2), r["dv"], tol, what=f"L{li} dL/dv")
+        bW = bx = None
+        if half:
+            # dL/dI handed to the contractions in bf16: a-priori rounding bound
+            aI = np.abs(dI_o.reshape(T * B, -1))
+            bW = 2.0 ** -8 * (aI.T @ np.abs(xin.reshape(T * B, -1)))
+            bx = 2.0 ** -8 * (aI @ np.abs(W).astype(np.float64)) if li > 0 else None
+        assert_close(_np(gW2), r["dW"], tol, what=f"L{li} dW", abs_bound=bW)
+        assert_close(_np(gb2), r["db"], tol, what=f"L{li} db")
+        if li > 0:
+            assert_close(_np(gx2).reshape(T * B, -1), r["dx"].reshape(T * B, -1), tol,
+                         what=f"L{li} dx", abs_bound=bx)
+        g = r["dx"]
 
 
-@pytest.mark.parametrize("name", ["dsnn_leaky_t25_b32", "dsnn_synaptic_t50_b256", "csnn_t25_b128"])
+@pytest.mark.parametrize("name", ["dsnn_leaky_t25_b32", "dsnn_synaptic_t50_b256", "csnn_t25_b128",
+                                  "dsnn_rleaky_t25_b128"])
 @pytest.mark.parametrize("path", list(PATHS))
-def test_step_full_size_teacher_forced(name, path):
+def test_step_full_size_stagewise(name, path):
     wl = wls.get(name)
     inp = wls.make_inputs(wl, seed=0)
-    net = snn.Network(wl, inp["params"], device=DEV, flags=PATHS[path])
-    x = _t(inp["x"])
-    net.step(x, labels=_t(inp["labels"]))
-    _check_step_teacher_forced(wl, inp, net, x)
+    _check_step_stagewise(wl, inp, flags=PATHS[path])
 
 
 @pytest.mark.parametrize("name,T,B,width", [("dsnn_synaptic_t50_b256", 20, 16, 200),
                                             ("dsnn_leaky_t25_b32", 25, 8, 300),
                                             ("scan_wide_t1000_b64", 60, 4, 1000),
                                             ("csnn_t25_b128", 6, 4, None),
-                                            ("dsnn_half_t100_b512", 12, 8, 320)])
+                                            ("dsnn_half_t100_b512", 12, 8, 320),
+                                            ("dsnn_rleaky_t25_b128", 15, 6, 130)])
 @pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
 @pytest.mark.parametrize("path", list(PATHS))
-def test_step_scaled_teacher_forced(name, T, B, width, reset, path):
+def test_step_scaled_stagewise(name, T, B, width, reset, path):
     wl = wls.scaled(wls.get(name), T=T, B=B, width=width)
     inp = wls.make_inputs(wl, seed=1)
+    _check_step_stagewise(wl, inp, reset, PATHS[path], tol=2e-2 if wl.dtype == "f16" else 1e-3)
+    # the whole step through the network: stage calls give the same bytes as
+    # the layer calls
     net = snn.Network(wl, inp["params"], device=DEV, reset_grad=reset, flags=PATHS[path])
     lab = _t(inp["labels"]) if wl.loss == "ce" else None
     tgt = _t(inp["targets"]) if wl.loss == "mse" else None
     x = _t(inp["x"])
     net.step(x, labels=lab, targets=tgt)
-    if reset == snn.RESET_DETACHED:
-        _check_step_teacher_forced(wl, inp, net, x, tol=2e-2 if wl.dtype == "f16" else 1e-3)
-    # the stage calls give the same bytes as the layer calls
     snap = [_np(t).copy() for t in net.gW if t is not None] + [_np(net.loss).copy()]
     net.step_stages(x, labels=lab, targets=tgt)
     snap2 = [_np(t) for t in net.gW if t is not None] + [_np(net.loss)]
@@ -517,12 +646,12 @@ def test_empty_time_and_batch():
         spk = torch.empty(256, dtype=torch.uint8, device=DEV)
         saved = torch.empty(256, dtype=torch.uint8, device=DEV)
         counts = torch.full((max(B, 1), 8), 7.0, device=DEV)
-        snn.snn_layer_fwd(d, x, W, None, spk, saved, counts, _ws(256))
+        snn.snn_layer_fwd(d, x, W, None, None, spk, saved, counts, _ws(256))
         if B > 0:
             assert (_np(counts) == 0).all()
         gW = torch.full((8, 16), 3.0, device=DEV)
         gb = torch.full((8,), 3.0, device=DEV)
         g = torch.zeros(256, dtype=torch.float32, device=DEV)
-        snn.snn_layer_bwd(d, snn.GRAD_BCAST, g, x, W, saved, gW, gb, None,
+        snn.snn_layer_bwd(d, snn.GRAD_BCAST, g, x, W, None, saved, gW, gb, None, None,
                           _ws(snn.snn_layer_workspace_bytes(d)))
         assert (_np(gW) == 0).all() and (_np(gb) == 0).all()
