@@ -16,7 +16,8 @@ reverse).  Every function names the passage of the paper it follows:
 * eq. (7)  recurrent leaky neuron ("RLeaky", one recurrent weight per neuron);
 * eqs. (8)-(9) fast-sigmoid surrogate for the spike's derivative;
 * Sec. III-C / Table I  dense 784-1000-10 and conv 5C12-MP2-5C64-MP2-10 nets;
-* Sec. V  rate-coded readout (class = output neuron with the most spikes).
+* Sec. V  rate-coded readout (class = output neuron with the most spikes);
+* Sec. IV  the AdamW weight update the paper trains with.
 
 Parity status: the dense and convolutional synapses, the scans, the losses
 and the backward recursion are pinned by the tests in ``tests/test_oracle_*``
@@ -80,6 +81,7 @@ def lib():
         L.orc_loss_ce.restype = dbl
         L.orc_loss_mse.argtypes = [i64, i64, P, P, P]
         L.orc_loss_mse.restype = dbl
+        L.orc_adamw.argtypes = [i64, P, P, P, P, i64, dbl, dbl, dbl, dbl, dbl]
         L.orc_num_threads.restype = i32
         _lib = L
     return _lib
@@ -254,6 +256,17 @@ def scan_bwd_rleaky(u, g, beta, thr, slope, v, reset_surrogate=False, s_scale=1.
                               int(bool(smooth_z)), _p(v), _p(u), _p(g), bcast, _p(dI),
                               _p(dv_col))
     return dI, dv_col.reshape(-1, v.size).sum(axis=0)
+
+
+def adamw(theta, g, m, v, t, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2):
+    """One AdamW step t >= 1 (Sec. IV: every network is trained with AdamW),
+    in double.  Returns new (theta, m, v); the inputs are not modified."""
+    th, m2, v2 = _f64(theta).copy(), _f64(m).copy(), _f64(v).copy()
+    gg = _f64(g)
+    assert th.shape == gg.shape == m2.shape == v2.shape and t >= 1
+    lib().orc_adamw(th.size, _p(th), _p(gg), _p(m2), _p(v2), int(t), float(lr),
+                    float(betas[0]), float(betas[1]), float(eps), float(weight_decay))
+    return th, m2, v2
 
 
 def loss_ce(counts, labels):

@@ -508,6 +508,36 @@ double orc_loss_mse(int64_t B, int64_t K, const double *counts,
     return total / (double)n;
 }
 
+/* ------------------------------------------------------------------------
+ * Weight update with AdamW, the optimizer the paper trains every network with
+ * (Sec. IV): Adam's moment estimates with bias correction (Kingma and Ba) and
+ * weight decay decoupled from the gradient (Loshchilov and Hutter), one step
+ * t >= 1, in double, elementwise:
+ *     theta <- theta - lr * wd * theta
+ *     m     <- beta1 m + (1 - beta1) g
+ *     v     <- beta2 v + (1 - beta2) g^2
+ *     mhat  =  m / (1 - beta1^t),   vhat = v / (1 - beta2^t)
+ *     theta <- theta - lr * mhat / (sqrt(vhat) + eps)
+ * theta, m, v are updated in place.
+ * ---------------------------------------------------------------------- */
+void orc_adamw(int64_t n, double *theta, const double *g, double *m, double *v,
+               int64_t t, double lr, double beta1, double beta2, double eps,
+               double wd)
+{
+    const double bc1 = 1.0 - pow(beta1, (double)t);
+    const double bc2 = 1.0 - pow(beta2, (double)t);
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        double th = theta[i];
+        th = th - lr * wd * th;
+        m[i] = beta1 * m[i] + (1.0 - beta1) * g[i];
+        v[i] = beta2 * v[i] + (1.0 - beta2) * g[i] * g[i];
+        const double mhat = m[i] / bc1;
+        const double vhat = v[i] / bc2;
+        theta[i] = th - lr * mhat / (sqrt(vhat) + eps);
+    }
+}
+
 /* Number of OpenMP threads a parallel region uses (for reporting). */
 int orc_num_threads(void)
 {

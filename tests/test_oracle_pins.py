@@ -513,3 +513,75 @@ def test_finite_differences_rleaky(reset_surrogate):
         if _fd_check(layers, params, x, y, reset_surrogate) is not None:
             return
     pytest.fail("no seed with a reset margin above 1e-4")
+
+
+# ---------------------------------------------------------------------------
+# P7: the AdamW weight update (Sec. IV trains every network with AdamW)
+# ---------------------------------------------------------------------------
+def test_adamw_first_step_closed_form():
+    """From zero moments the bias-corrected estimates are g and g^2, so the
+    first step is theta (1 - lr wd) - lr g / (|g| + eps)."""
+    rng = np.random.default_rng(1)
+    th0 = rng.normal(0, 1, 1000)
+    g = rng.normal(0, 0.1, 1000)
+    lr, wd, eps = 3e-3, 0.05, 1e-8
+    th, m, v = oracle.adamw(th0, g, np.zeros(1000), np.zeros(1000), 1, lr, (0.9, 0.999), eps, wd)
+    np.testing.assert_allclose(th, th0 * (1 - lr * wd) - lr * g / (np.abs(g) + eps), rtol=1e-13,
+                               atol=1e-16)
+    np.testing.assert_allclose(m, 0.1 * g, rtol=1e-14)
+    np.testing.assert_allclose(v, 0.001 * g * g, rtol=1e-12)
+
+
+def test_adamw_constant_gradient_moves_linearly():
+    """A constant gradient keeps mhat = g and vhat = g^2 at every step: without
+    weight decay each step moves theta by lr g / (|g| + eps)."""
+    th0 = np.array([0.5, -1.0, 2.0, 0.0])
+    g = np.array([0.2, -0.05, 1e-3, 3.0])
+    th, m, v = th0, np.zeros(4), np.zeros(4)
+    lr, eps = 1e-2, 1e-8
+    for t in range(1, 31):
+        th, m, v = oracle.adamw(th, g, m, v, t, lr, (0.9, 0.999), eps, 0.0)
+    np.testing.assert_allclose(th, th0 - 30 * lr * g / (np.abs(g) + eps), rtol=1e-11)
+
+
+def test_adamw_decay_is_decoupled():
+    """With a zero gradient only the decay acts: theta (1 - lr wd), exactly."""
+    th0 = np.linspace(-3, 3, 101)
+    th, m, v = oracle.adamw(th0, np.zeros(101), np.zeros(101), np.zeros(101), 1, 1e-3,
+                            (0.9, 0.999), 1e-8, 0.1)
+    np.testing.assert_array_equal(th, th0 - 1e-3 * 0.1 * th0)
+    assert not m.any() and not v.any()
+
+
+def test_adamw_matches_torch_float64():
+    """torch.optim.AdamW in float64 over several steps (a library special case)."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(2)
+    th0 = rng.normal(0, 1, (37, 11))
+    grads = [rng.normal(0, 0.3, th0.shape) for _ in range(6)]
+    P = torch.nn.Parameter(torch.tensor(th0, dtype=torch.float64))
+    opt = torch.optim.AdamW([P], lr=2e-3, betas=(0.85, 0.995), eps=1e-7, weight_decay=0.02)
+    th, m, v = th0, np.zeros_like(th0), np.zeros_like(th0)
+    for t, g in enumerate(grads, start=1):
+        P.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        th, m, v = oracle.adamw(th, g, m, v, t, 2e-3, (0.85, 0.995), 1e-7, 0.02)
+    np.testing.assert_allclose(th, P.detach().numpy(), rtol=1e-12, atol=1e-15)
+    st = opt.state[P]
+    np.testing.assert_allclose(m, st["exp_avg"].numpy(), rtol=1e-12, atol=1e-18)
+    np.testing.assert_allclose(v, st["exp_avg_sq"].numpy(), rtol=1e-12, atol=1e-20)
+
+
+def test_adamw_scale_invariance():
+    """With eps = 0 the update does not depend on the gradient's scale."""
+    rng = np.random.default_rng(3)
+    th0 = rng.normal(0, 1, 50)
+    gs = [rng.normal(0, 1, 50) for _ in range(4)]
+    runs = []
+    for c in (1.0, 1e-3, 256.0):
+        th, m, v = th0, np.zeros(50), np.zeros(50)
+        for t, g in enumerate(gs, start=1):
+            th, m, v = oracle.adamw(th, c * g, m, v, t, 1e-2, (0.9, 0.99), 0.0, 0.01)
+        runs.append(th)
+    np.testing.assert_allclose(runs[1], runs[0], rtol=1e-12)
+    np.testing.assert_allclose(runs[2], runs[0], rtol=1e-12)
