@@ -163,6 +163,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mode", choices=["bench", "pmc"], default="bench")
+    ap.add_argument("--update", action="store_true",
+                    help="end every step with the fused AdamW update (the paper's "
+                         "training step); the default step is forward + BPTT")
     ap.add_argument("--fp32-mfma", action="store_true",
                     help="contract spike x fp32 with fp32 MFMA instead of the exact "
                          "three-pass bf16 split")
@@ -189,6 +192,9 @@ def main():
     params = wls.init_params(wl, args.seed)
     net = snn.Network(wl, params, device="cuda",
                       flags=snn.FLAG_FP32_MFMA if args.fp32_mfma else 0)
+    if args.update:
+        net.init_adamw(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2)
+    upd = bool(args.update)
     with torch.cuda.stream(stream):
         if wl.input == "currents":
             # 4 bytes x T x B x N: drawn directly in device memory
@@ -206,7 +212,7 @@ def main():
 
     with torch.cuda.stream(stream):
         for _ in range(args.warmup):
-            net.step_stages(x, labels=y, targets=tgt)
+            net.step_stages(x, labels=y, targets=tgt, update=upd)
         torch.cuda.synchronize()
 
         # per-stage split (one pass, outside the timed region): find the
@@ -220,7 +226,7 @@ def main():
 
         split_steps = 5
         for _ in range(split_steps):
-            net.step_stages(x, labels=y, targets=tgt, hook=rec)
+            net.step_stages(x, labels=y, targets=tgt, hook=rec, update=upd)
         torch.cuda.synchronize()
         split = {}
         for (n0, l0, e0), (n1, l1, e1) in zip(evs, evs[1:]):
@@ -245,7 +251,7 @@ def main():
         torch.cuda.synchronize()
         marks[0].record(stream)
         for i in range(args.steps):
-            net.step_stages(x, labels=y, targets=tgt, hook=rec_dom)
+            net.step_stages(x, labels=y, targets=tgt, hook=rec_dom, update=upd)
             marks[i + 1].record(stream)
         torch.cuda.synchronize()
         total_ms = marks[0].elapsed_time(marks[-1])
@@ -286,7 +292,8 @@ def main():
                    "batch": wl.B, "layers": [_layer_str(s) for s in wl.layers],
                    "surrogate_slope": wl.slope, "input": "Bernoulli rate-coded spikes"
                    if wl.input == "spikes" else "normal currents",
-                   "includes": "forward + loss + BPTT backward, no optimizer update"},
+                   "includes": "forward + loss + BPTT backward + fused AdamW update"
+                   if upd else "forward + loss + BPTT backward, no optimizer update"},
         "step_ms": {"median": round(per_step[len(per_step) // 2], 5),
                     "p10": round(per_step[len(per_step) // 10], 5),
                     "p90": round(per_step[(9 * len(per_step)) // 10], 5)},
@@ -294,6 +301,15 @@ def main():
         "stage_ms": {k: round(v, 5) for k, v in split.items()},
         "stage_roofline": _stage_rooflines(net, split, args.fp32_mfma),
     }
+    if upd and split.get("update"):
+        # fused AdamW: read param, grad, m, v and write param, m, v (4 B each)
+        # per parameter, plus the 2 B fp16 copy of fp16 weights
+        nb = sum(28 * t[0].numel() + (2 * t[0].numel() if t[4] is not None else 0)
+                 for t in net.opt_tensors)
+        gbs = nb / (split["update"] / 1000.0) / 1e9
+        out["stage_roofline"]["update"] = {"GB/s": round(gbs, 1),
+                                           "frac": round(gbs / PEAK_HBM_GBS, 4),
+                                           "bytes": nb}
     syn = sum(v for k, v in split.items() if k.startswith("synapse"))
     neu = sum(v for k, v in split.items() if k.startswith("neuron"))
     out["spiking_vs_synaptic_ms"] = {"neuron_scans": round(neu, 5), "contractions": round(syn, 5)}

@@ -193,6 +193,43 @@ snn_status snn_loss(int32_t kind, int32_t B, int32_t K, const float *counts,
                     const int32_t *labels, const float *targets, float *loss,
                     float *grad_counts, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* ---- weight update ---------------------------------------------------------
+ * AdamW, the optimizer the paper trains every network with (Sec. IV): for
+ * each parameter tensor, elementwise, with step t >= 1,
+ *     theta <- theta (1 - lr wd)
+ *     m <- beta1 m + (1 - beta1) g,      v <- beta2 v + (1 - beta2) g^2
+ *     theta <- theta - lr (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ * (Adam's bias-corrected moments, weight decay decoupled from the gradient).
+ * All tensors of a call are updated by one fused pass (one kernel launch per
+ * 16 non-empty tensors).  param, m, v are fp32 and updated in place (param is
+ * the fp32 master copy); grad is fp32 (the grad_w / grad_b / grad_v of the
+ * backward).  param_half, if not NULL, receives the updated param rounded to
+ * fp16 (nearest even): the weights an SNN_F16 layer contracts with.  The
+ * arrays of one tensor must not overlap each other or another tensor's. */
+typedef struct snn_adamw_tensor {
+    float *param;        /* fp32 [n], in place */
+    const float *grad;   /* fp32 [n] */
+    float *m;            /* fp32 [n] first moment, in place (zeros before step 1) */
+    float *v;            /* fp32 [n] second moment, in place (zeros before step 1) */
+    void *param_half;    /* fp16 [n] copy of the updated param, or NULL */
+    int64_t n;           /* elements, 0 <= n <= 2^36 (n = 0: skipped) */
+} snn_adamw_tensor;
+
+typedef struct snn_adamw_hparams {
+    float lr;            /* >= 0 */
+    float beta1, beta2;  /* in [0, 1) */
+    float eps;           /* >= 0 */
+    float weight_decay;  /* >= 0 */
+    int32_t step;        /* t >= 1: the t-th update of these moments */
+} snn_adamw_hparams;
+
+/* tensors: HOST array of `count` descriptors (count >= 0; NULL iff 0) whose
+ * pointers are device pointers; hp: host pointer.  SNN_ERR_NULL for a
+ * missing pointer of a non-empty tensor, SNN_ERR_SHAPE for bad sizes or
+ * hyper-parameters (non-finite, out of range, step < 1). */
+snn_status snn_adamw(const snn_adamw_tensor *tensors, int32_t count,
+                     const snn_adamw_hparams *hp, hipStream_t stream);
+
 /* ---- stage calls: the two halves of snn_layer_fwd / snn_layer_bwd -------
  * snn_layer_fwd == snn_synapse_fwd(cur = saved) + snn_neuron_fwd(cur = saved,
  * saved_u = saved); snn_layer_bwd == snn_neuron_bwd + snn_synapse_bwd.  They

@@ -40,7 +40,7 @@ STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE"
 EXPORTS = ["snn_abi_version", "snn_status_str", "snn_layer_saved_bytes",
            "snn_layer_workspace_bytes", "snn_layer_fwd", "snn_layer_bwd",
            "snn_loss_workspace_bytes", "snn_loss", "snn_synapse_fwd", "snn_neuron_fwd",
-           "snn_neuron_bwd", "snn_synapse_bwd"]
+           "snn_neuron_bwd", "snn_synapse_bwd", "snn_adamw"]
 
 
 class LayerDesc(ctypes.Structure):
@@ -64,6 +64,17 @@ class LayerDesc(ctypes.Structure):
 class GradIn(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("g", ctypes.c_void_p)]
+
+
+class AdamwTensor(ctypes.Structure):
+    _fields_ = [("param", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("m", ctypes.c_void_p),
+                ("v", ctypes.c_void_p), ("param_half", ctypes.c_void_p), ("n", ctypes.c_int64)]
+
+
+class AdamwHparams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_float), ("beta1", ctypes.c_float), ("beta2", ctypes.c_float),
+                ("eps", ctypes.c_float), ("weight_decay", ctypes.c_float),
+                ("step", ctypes.c_int32)]
 
 
 class SNNError(RuntimeError):
@@ -101,6 +112,8 @@ def lib():
         "snn_neuron_fwd": ([D, P, P, P, P, P, P], ctypes.c_int),
         "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_adamw": ([ctypes.POINTER(AdamwTensor), i32, ctypes.POINTER(AdamwHparams), P],
+                      ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         f = getattr(L, name)
@@ -195,6 +208,17 @@ def snn_synapse_bwd(desc, dcur, pool_arg, x, w, grad_w, grad_x, ws, stream=None)
     _check("snn_synapse_bwd", lib().snn_synapse_bwd(
         ctypes.byref(desc), _p(dcur), _p(pool_arg), _p(x), _p(w), _p(grad_w), _p(grad_x),
         _p(ws), _nbytes(ws), _stream(stream)))
+
+
+def snn_adamw(tensors, step, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2,
+              stream=None):
+    """tensors: sequence of (param, grad, m, v, param_half or None) device
+    tensors (fp32, param_half fp16), all updated in one fused pass."""
+    arr = (AdamwTensor * max(1, len(tensors)))()
+    for i, (p, g, m, v, h) in enumerate(tensors):
+        arr[i] = AdamwTensor(_p(p), _p(g), _p(m), _p(v), _p(h), p.numel())
+    hp = AdamwHparams(lr, betas[0], betas[1], eps, weight_decay, step)
+    _check("snn_adamw", lib().snn_adamw(arr, len(tensors), ctypes.byref(hp), _stream(stream)))
 
 
 # --------------------------------------------------------------------------
@@ -319,6 +343,30 @@ class Network:
         self.loss_and_grad(labels, targets, stream)
         self.backward(x, stream)
 
+    def init_adamw(self, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2):
+        """Optimizer state for ``update``: zero moments per parameter tensor
+        and, for fp16 weights, an fp32 master copy (the fp16 weights the
+        contractions read are rewritten from it after every update)."""
+        torch = self.torch
+        self.opt = dict(lr=lr, betas=betas, eps=eps, weight_decay=weight_decay)
+        self.opt_t = 0
+        self.opt_tensors = []
+        for li in range(len(self.descs)):
+            for P, G in ((self.W[li], self.gW[li]), (self.b[li], self.gb[li]),
+                         (self.v[li], self.gv[li])):
+                if P is None:
+                    continue
+                half = P.dtype == torch.float16
+                master = P.float().contiguous() if half else P
+                self.opt_tensors.append((master, G, torch.zeros_like(master),
+                                         torch.zeros_like(master), P if half else None))
+
+    def update(self, stream=None):
+        """One AdamW step over every parameter with the gradients of the last
+        backward (Sec. IV: the paper's training step ends with it)."""
+        self.opt_t += 1
+        snn_adamw(self.opt_tensors, self.opt_t, stream=stream, **self.opt)
+
     def pool_arg(self, li):
         """The 2x2 pool selection of conv layer li inside its saved buffer."""
         d = self.descs[li]
@@ -328,7 +376,8 @@ class Network:
         return self.saved[li][off:]
 
     # the same work through the stage calls, with a hook between stages
-    def step_stages(self, x, labels=None, targets=None, stream=None, hook=None):
+    # (update: finish with the AdamW step of ``init_adamw``)
+    def step_stages(self, x, labels=None, targets=None, stream=None, hook=None, update=False):
         torch = self.torch
         hook = hook or (lambda name, li: None)
         n = len(self.descs)
@@ -378,3 +427,7 @@ class Network:
                             rest, stream)
             hook("synapse_bwd_end", li)
             kind, g = GRAD_FULL, self.gx[li]
+        if update:
+            hook("update", -1)
+            self.update(stream)
+            hook("update_end", -1)

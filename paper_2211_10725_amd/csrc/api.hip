@@ -487,4 +487,43 @@ snn_status snn_loss(int32_t kind, int32_t B, int32_t K, const float *counts,
                                   stream));
 }
 
+snn_status snn_adamw(const snn_adamw_tensor *tensors, int32_t count,
+                     const snn_adamw_hparams *hp, hipStream_t stream) {
+    if (count < 0) return SNN_ERR_SHAPE;
+    if (!hp || (count > 0 && !tensors)) return SNN_ERR_NULL;
+    if (!finite(hp->lr) || !finite(hp->beta1) || !finite(hp->beta2) || !finite(hp->eps) ||
+        !finite(hp->weight_decay) || hp->lr < 0.f || hp->beta1 < 0.f || hp->beta1 >= 1.f ||
+        hp->beta2 < 0.f || hp->beta2 >= 1.f || hp->eps < 0.f || hp->weight_decay < 0.f ||
+        hp->step < 1)
+        return SNN_ERR_SHAPE;
+    bool any = false;
+    for (int i = 0; i < count; ++i) {
+        const snn_adamw_tensor &t = tensors[i];
+        if (t.n < 0 || t.n > ((int64_t)1 << 36)) return SNN_ERR_SHAPE;
+        if (t.n == 0) continue;
+        any = true;
+        if (!t.param || !t.grad || !t.m || !t.v) return SNN_ERR_NULL;
+        if (!aligned16(t.param) || !aligned16(t.grad) || !aligned16(t.m) || !aligned16(t.v) ||
+            (t.param_half && !aligned16(t.param_half)))
+            return SNN_ERR_ALIGN;
+    }
+    // bias corrections and step size in double, handed to the kernel in fp32
+    const double lr = hp->lr, b1 = hp->beta1, b2 = hp->beta2;
+    const double bc1 = 1.0 - pow(b1, (double)hp->step);
+    const double bc2 = 1.0 - pow(b2, (double)hp->step);
+    if (!(bc1 > 0.0) || !(bc2 > 0.0)) return SNN_ERR_SHAPE;  // beta = 0 at t = 1 is fine
+    AdamwCoef c{};
+    c.decay = (float)(1.0 - lr * hp->weight_decay);
+    c.beta1 = hp->beta1;
+    c.one_minus_beta1 = (float)(1.0 - b1);
+    c.beta2 = hp->beta2;
+    c.one_minus_beta2 = (float)(1.0 - b2);
+    c.step_size = (float)(lr / bc1);
+    c.inv_sqrt_bc2 = (float)(1.0 / sqrt(bc2));
+    c.eps = hp->eps;
+    if (!any) return SNN_OK;
+    (void)hipGetLastError();
+    return hip_status(launch_adamw(tensors, count, c, stream));
+}
+
 }  // extern "C"

@@ -123,6 +123,20 @@ hipError_t launch_loss(int kind, int B, int K, const float *counts, const int32_
                        const float *targets, float *loss, float *grad, void *ws,
                        hipStream_t s);
 
+// ---- AdamW weight update (optim.hip) -------------------------------------------
+// per-step coefficients, computed on the host in double
+struct AdamwCoef {
+    float decay;            // 1 - lr * weight_decay
+    float beta1, one_minus_beta1, beta2, one_minus_beta2;
+    float step_size;        // lr / (1 - beta1^t)
+    float inv_sqrt_bc2;     // 1 / sqrt(1 - beta2^t)
+    float eps;
+};
+constexpr int kAdamwMaxTensors = 16;  // tensors per launch (kernel arguments by value)
+int64_t adamw_blocks(int64_t n);
+// tensors: host array of the caller's descriptors (validated)
+hipError_t launch_adamw(const snn_adamw_tensor *t, int count, const AdamwCoef &c, hipStream_t s);
+
 // ---- convolution + pool (conv.hip) -------------------------------------------
 struct ConvGeom {
     int NB;   // T * B images

@@ -119,3 +119,23 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(snn, "LIB_PATH", str(tmp_path / "libsnn.so"))
     with pytest.raises(RuntimeError, match="not built"):
         snn.lib()
+
+
+def test_adamw_validation():
+    """Host-side checks of snn_adamw; no call here reaches a launch."""
+    L = snn.lib()
+    hp = snn.AdamwHparams(1e-3, 0.9, 0.999, 1e-8, 0.0, 1)
+    arr = (snn.AdamwTensor * 1)()
+    assert L.snn_adamw(arr, 0, hp, None) == 0                     # nothing to do
+    assert L.snn_adamw(None, 1, hp, None) == 1
+    arr[0] = snn.AdamwTensor(None, None, None, None, None, 0)
+    assert L.snn_adamw(arr, 1, hp, None) == 0                     # empty tensor
+    arr[0] = snn.AdamwTensor(16, None, 48, 64, None, 8)
+    assert L.snn_adamw(arr, 1, hp, None) == 1                     # missing grad
+    arr[0] = snn.AdamwTensor(16, 32, 48, 72, None, 8)
+    assert L.snn_adamw(arr, 1, hp, None) == 4                     # misaligned moment
+    for bad in (snn.AdamwHparams(1e-3, 1.0, 0.999, 1e-8, 0.0, 1),
+                snn.AdamwHparams(-1.0, 0.9, 0.999, 1e-8, 0.0, 1),
+                snn.AdamwHparams(1e-3, 0.9, 0.999, 1e-8, 0.0, 0),
+                snn.AdamwHparams(float("nan"), 0.9, 0.999, 1e-8, 0.0, 1)):
+        assert L.snn_adamw(arr, 1, bad, None) == 2
