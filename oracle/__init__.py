@@ -269,26 +269,39 @@ def adamw(theta, g, m, v, t, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay
     return th, m2, v2
 
 
-def loss_ce(counts, labels):
-    """Spike-count cross-entropy, mean over the batch.  Returns (L, dL/dc)."""
+def population_counts(counts, P):
+    """Population code (Sec. V): P output neurons per class, class k pooling
+    the spike counts of neurons k*P .. k*P + P - 1 of each sample.
+    counts [B, K*P] -> [B, K]."""
     c = _f64(counts)
+    B = c.shape[0]
+    return c.reshape(B, -1, P).sum(axis=2)
+
+
+def loss_ce(counts, labels, P=1):
+    """Spike-count cross-entropy, mean over the batch, on the class counts
+    (pooled over populations of P neurons when P > 1).  Returns (L, dL/dc)
+    with dL/dc per output neuron: every neuron of a population receives its
+    class's gradient."""
+    c = population_counts(counts, P) if P > 1 else _f64(counts)
     B, K = c.shape
     y = np.ascontiguousarray(labels, np.int32)
     g = np.empty((B, K))
     L = lib().orc_loss_ce(B, K, _p(c), _p(y), _p(g))
-    return L, g
+    return L, (np.repeat(g, P, axis=1) if P > 1 else g)
 
 
-def loss_mse(counts, targets):
-    """Spike-count mean-squared error, mean over all entries."""
-    c = _f64(counts)
+def loss_mse(counts, targets, P=1):
+    """Spike-count mean-squared error, mean over all class entries (pooled
+    over populations of P neurons when P > 1; targets [B, K])."""
+    c = population_counts(counts, P) if P > 1 else _f64(counts)
     y = _f64(targets)
     assert c.shape == y.shape
     g = np.empty(c.shape)
     B = c.shape[0]
     K = int(np.prod(c.shape[1:]))
     L = lib().orc_loss_mse(B, K, _p(c), _p(y), _p(g))
-    return L, g
+    return L, (np.repeat(g, P, axis=1) if P > 1 else g)
 
 
 # --------------------------------------------------------------------------
@@ -376,13 +389,13 @@ def layer_bwd(spec, fwd, g, W=None, slope=25.0, reset_surrogate=False, s_scale=1
 
 
 def net_step(layers, params, x, loss="ce", labels=None, targets=None, smooth=False,
-             slope=25.0, reset_surrogate=False):
+             slope=25.0, reset_surrogate=False, pop=1):
     """One forward + BPTT step of a feed-forward spiking network.
 
     layers: list of layer spec dicts; params: list of (W, b) (None for 'none'),
     or (W, b, v) for an 'rleaky' layer; x: [T, B, ...] input.  The loss is
-    taken on the last layer's spike counts
-    summed over T.  Returns (loss, per-layer forward dicts, per-layer backward
+    taken on the last layer's spike counts summed over T (and pooled over
+    populations of ``pop`` neurons per class, Sec. V).  Returns (loss, per-layer forward dicts, per-layer backward
     dicts)."""
     fwds = []
     h = x
@@ -396,9 +409,9 @@ def net_step(layers, params, x, loss="ce", labels=None, targets=None, smooth=Fal
     counts = fwds[-1]["counts"]
     B = counts.shape[0]
     if loss == "ce":
-        L, gc = loss_ce(counts.reshape(B, -1), labels)
+        L, gc = loss_ce(counts.reshape(B, -1), labels, pop)
     else:
-        L, gc = loss_mse(counts.reshape(B, -1), targets)
+        L, gc = loss_mse(counts.reshape(B, -1), targets, pop)
     g = gc.reshape(counts.shape)
     s_scale = slope / 2.0 if smooth else 1.0
     bwds = [None] * len(layers)

@@ -585,3 +585,57 @@ def test_adamw_scale_invariance():
         runs.append(th)
     np.testing.assert_allclose(runs[1], runs[0], rtol=1e-12)
     np.testing.assert_allclose(runs[2], runs[0], rtol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# P8: population code (Sec. V): P output neurons per class, counts pooled
+# ---------------------------------------------------------------------------
+def test_population_of_one_is_the_plain_readout():
+    rng = np.random.default_rng(4)
+    c = rng.integers(0, 26, (9, 10)).astype(np.float64)
+    y = rng.integers(0, 10, 9)
+    L1, g1 = oracle.loss_ce(c, y, P=1)
+    L0, g0 = oracle.loss_ce(c, y)
+    assert L1 == L0 and np.array_equal(g1, g0)
+
+
+def test_population_uniform_counts_closed_form():
+    """Equal pooled counts: L = log K and every neuron of class k gets
+    (1/K - [k = y]) / B."""
+    B, K, P = 4, 10, 50
+    c = np.ones((B, K * P))
+    y = np.array([0, 3, 9, 3])
+    L, g = oracle.loss_ce(c, y, P)
+    assert abs(L - math.log(K)) < 1e-14
+    want = np.repeat((np.full((B, K), 1.0 / K) - np.eye(K)[y]) / B, P, axis=1)
+    np.testing.assert_allclose(g, want, rtol=1e-14, atol=1e-17)
+
+
+def test_population_pooling_by_hand():
+    """Two classes of three neurons: class counts 1+0+2 = 3 and 4+1+0 = 5;
+    MSE against targets (2, 7): L = ((3-2)^2 + (5-7)^2) / 2 = 2.5, and each
+    neuron of class k receives 2 (c_k - y_k) / 2."""
+    c = np.array([[1.0, 0.0, 2.0, 4.0, 1.0, 0.0]])
+    L, g = oracle.loss_mse(c, np.array([[2.0, 7.0]]), P=3)
+    assert L == 2.5
+    np.testing.assert_array_equal(g, [[1.0, 1.0, 1.0, -2.0, -2.0, -2.0]])
+
+
+def test_population_invariant_to_order_within_class_and_fd():
+    rng = np.random.default_rng(6)
+    B, K, P = 5, 4, 7
+    c = rng.integers(0, 3, (B, K * P)).astype(np.float64)
+    y = rng.integers(0, K, B)
+    L, g = oracle.loss_ce(c, y, P)
+    perm = np.concatenate([k * P + rng.permutation(P) for k in range(K)])
+    L2, _ = oracle.loss_ce(c[:, perm], y, P)
+    assert abs(L - L2) < 1e-14
+    # central differences of the loss in each neuron's count
+    eps = 1e-6
+    for j in rng.integers(0, K * P, 6):
+        for b in range(B):
+            cp, cm = c.copy(), c.copy()
+            cp[b, j] += eps
+            cm[b, j] -= eps
+            fd = (oracle.loss_ce(cp, y, P)[0] - oracle.loss_ce(cm, y, P)[0]) / (2 * eps)
+            assert abs(fd - g[b, j]) < 1e-8
