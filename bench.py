@@ -146,7 +146,7 @@ def cpu_baseline(wl, seed, target_macs=3.0e11):
     inp = wls.make_inputs(ws_, seed)
     t0 = time.perf_counter()
     oracle.net_step(ws_.layers, inp["params"], inp["x"], ws_.loss, labels=inp.get("labels"),
-                    targets=inp.get("targets"), slope=ws_.slope)
+                    targets=inp.get("targets"), slope=ws_.slope, pop=ws_.pop)
     dt = time.perf_counter() - t0
     return {"value": round(bs / dt, 3), "unit": "samples/s", "cores": oracle.num_threads(),
             "kind": "oracle",

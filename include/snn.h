@@ -49,7 +49,7 @@
  *   - T == 0 or B == 0 is valid: no compute is launched, and outputs that
  *     are sums over an empty range (counts, grad_w, grad_b, grad_v) are set
  *     to 0.
- *     A loss over B == 0 or K == 0 is rejected (SNN_ERR_SHAPE).
+ *     A loss over B == 0, K == 0 or P == 0 is rejected (SNN_ERR_SHAPE).
  */
 #ifndef SNN_H
 #define SNN_H
@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 2
+#define SNN_ABI_VERSION 3
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -184,12 +184,16 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
                          float *grad_b, float *grad_v, float *grad_x, void *ws,
                          size_t ws_bytes, hipStream_t stream);
 
-/* Loss on spike counts [B,K] and its gradient dL/dc [B,K] (which is dL/dz_t
- * for every t, since dc/dz_t = 1).  `loss` is a device fp32 scalar.
+/* Loss on spike counts and its gradient dL/dcounts (which is dL/dz_t for
+ * every t, since dc/dz_t = 1).  K classes, P >= 1 output neurons per class:
+ * counts and grad_counts are [B, K*P]; with P > 1 (a population code, Sec. V)
+ * class k's count c_k is the sum of neurons kP .. kP+P-1, and each neuron of
+ * a population receives its class's gradient.  `loss` is a device fp32
+ * scalar.  Over the class counts c [B,K]:
  * CE: L = mean_b (logsumexp(c_b) - c_b[y_b]),  g = (softmax(c_b) - onehot)/B.
- * MSE: L = mean (c - y)^2,                    g = 2 (c - y) / (B K). */
+ * MSE: L = mean (c - y)^2 (targets [B,K]),    g = 2 (c - y) / (B K). */
 size_t snn_loss_workspace_bytes(int32_t kind, int32_t B, int32_t K);
-snn_status snn_loss(int32_t kind, int32_t B, int32_t K, const float *counts,
+snn_status snn_loss(int32_t kind, int32_t B, int32_t K, int32_t P, const float *counts,
                     const int32_t *labels, const float *targets, float *loss,
                     float *grad_counts, void *ws, size_t ws_bytes, hipStream_t stream);
 

@@ -31,7 +31,7 @@ RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST = 0, 1
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
           4: "SNN_ERR_ALIGN", 5: "SNN_ERR_UNSUPPORTED", 6: "SNN_ERR_WORKSPACE",
@@ -107,7 +107,7 @@ def lib():
         "snn_layer_fwd": ([D, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_layer_bwd": ([D, G, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_loss_workspace_bytes": ([i32, i32, i32], S),
-        "snn_loss": ([i32, i32, i32, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_loss": ([i32, i32, i32, i32, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_synapse_fwd": ([D, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_neuron_fwd": ([D, P, P, P, P, P, P], ctypes.c_int),
         "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, S, P], ctypes.c_int),
@@ -180,9 +180,10 @@ def snn_layer_bwd(desc, grad_kind, g, x, w, v, saved, grad_w, grad_b, grad_v, gr
         _p(grad_b), _p(grad_v), _p(grad_x), _p(ws), _nbytes(ws), _stream(stream)))
 
 
-def snn_loss(kind, B, K, counts, labels, targets, loss, grad_counts, ws, stream=None):
-    _check("snn_loss", lib().snn_loss(kind, B, K, _p(counts), _p(labels), _p(targets), _p(loss),
-                                      _p(grad_counts), _p(ws), _nbytes(ws), _stream(stream)))
+def snn_loss(kind, B, K, P, counts, labels, targets, loss, grad_counts, ws, stream=None):
+    _check("snn_loss", lib().snn_loss(kind, B, K, P, _p(counts), _p(labels), _p(targets),
+                                      _p(loss), _p(grad_counts), _p(ws), _nbytes(ws),
+                                      _stream(stream)))
 
 
 def snn_synapse_fwd(desc, x, w, bias, cur, pool_arg, ws, stream=None):
@@ -306,11 +307,15 @@ class Network:
                             for d in self.descs[1:]]
         if self.descs[0].synapse == SYN_NONE:
             self.gx[0] = torch.empty((T, B, self.descs[0].n_in), dtype=torch.float32, device=device)
-        K = self.descs[-1].n_out
+        # K classes, P output neurons per class (a population code when P > 1)
+        self.P = getattr(wl, "pop", 1)
+        n_last = self.descs[-1].n_out
+        assert n_last % self.P == 0, (n_last, self.P)
+        K = n_last // self.P
         self.K = K
-        self.counts = torch.empty((B, K), dtype=torch.float32, device=device)
+        self.counts = torch.empty((B, n_last), dtype=torch.float32, device=device)
         self.loss = torch.empty(4, dtype=torch.float32, device=device)  # [0] is the loss
-        self.gcounts = torch.empty((B, K), dtype=torch.float32, device=device)
+        self.gcounts = torch.empty((B, n_last), dtype=torch.float32, device=device)
         self.loss_kind = LOSS_CE_COUNT if wl.loss == "ce" else LOSS_MSE_COUNT
         ws = max([snn_layer_workspace_bytes(d) for d in self.descs] +
                  [snn_loss_workspace_bytes(self.loss_kind, B, K), 256])
@@ -325,8 +330,8 @@ class Network:
             h = self.spk[li]
 
     def loss_and_grad(self, labels=None, targets=None, stream=None):
-        snn_loss(self.loss_kind, self.wl.B, self.K, self.counts, labels, targets, self.loss,
-                 self.gcounts, self.ws, stream)
+        snn_loss(self.loss_kind, self.wl.B, self.K, self.P, self.counts, labels, targets,
+                 self.loss, self.gcounts, self.ws, stream)
 
     def backward(self, x, stream=None):
         n = len(self.descs)

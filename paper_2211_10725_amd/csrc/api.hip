@@ -469,11 +469,11 @@ size_t snn_loss_workspace_bytes(int32_t kind, int32_t B, int32_t K) {
     return loss_workspace_bytes(kind, B, K);
 }
 
-snn_status snn_loss(int32_t kind, int32_t B, int32_t K, const float *counts,
+snn_status snn_loss(int32_t kind, int32_t B, int32_t K, int32_t P, const float *counts,
                     const int32_t *labels, const float *targets, float *loss,
                     float *grad_counts, void *ws, size_t ws_bytes, hipStream_t stream) {
     if (kind != SNN_LOSS_CE_COUNT && kind != SNN_LOSS_MSE_COUNT) return SNN_ERR_UNSUPPORTED;
-    if (B < 1 || K < 1) return SNN_ERR_SHAPE;
+    if (B < 1 || K < 1 || P < 1 || (int64_t)K * P > INT32_MAX) return SNN_ERR_SHAPE;
     if (!counts || !loss) return SNN_ERR_NULL;
     if (kind == SNN_LOSS_CE_COUNT && !labels) return SNN_ERR_NULL;
     if (kind == SNN_LOSS_MSE_COUNT && !targets) return SNN_ERR_NULL;
@@ -483,7 +483,7 @@ snn_status snn_loss(int32_t kind, int32_t B, int32_t K, const float *counts,
     const size_t need = loss_workspace_bytes(kind, B, K);
     if (need > ws_bytes || (need > 0 && !ws)) return SNN_ERR_WORKSPACE;
     (void)hipGetLastError();
-    return hip_status(launch_loss(kind, B, K, counts, labels, targets, loss, grad_counts, ws,
+    return hip_status(launch_loss(kind, B, K, P, counts, labels, targets, loss, grad_counts, ws,
                                   stream));
 }
 

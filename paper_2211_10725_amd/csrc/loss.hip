@@ -1,5 +1,8 @@
 // Losses on output spike counts (rate-coded readout: the predicted class is
-// the output neuron with the most spikes, Sec. V) and dL/dcounts.
+// the output neuron with the most spikes, Sec. V) and dL/dcounts.  With a
+// population code (Sec. V) each class owns P consecutive output neurons and
+// the loss is taken on the class counts, the sums over each population; every
+// neuron of a population receives its class's gradient.
 //
 // Reductions are fixed-order trees in fp64 (wave64 shuffles, then LDS), so
 // the scalar loss is bit-reproducible run to run.
@@ -31,40 +34,99 @@ __device__ inline double block_sum(double v) {
     return s;  // valid in thread 0 only
 }
 
-// Cross-entropy with the counts as logits, mean over the batch.  One block;
-// thread i handles rows i, i+256, ...  A label outside [0, K) makes that
-// row's loss and gradient NaN (no out-of-range access).
-__global__ __launch_bounds__(kThreads) void ce_kernel(int B, int K, const float *__restrict__ counts,
-                                                      const int32_t *__restrict__ labels,
-                                                      float *__restrict__ loss,
-                                                      float *__restrict__ grad) {
-    double part = 0.0;
-    const double invB = 1.0 / (double)B;
-    for (int b = threadIdx.x; b < B; b += kThreads) {
-        const float *c = counts + (int64_t)b * K;
-        const int y = labels[b];
-        const bool ok = (y >= 0 && y < K);
-        double mx = c[0];
-        for (int k = 1; k < K; ++k) mx = fmax(mx, (double)c[k]);
-        double se = 0.0;
-        for (int k = 0; k < K; ++k) se += exp((double)c[k] - mx);
-        const double lse = mx + log(se);
-        part += ok ? (lse - (double)c[y]) : __builtin_nan("");
-        if (grad) {
-            for (int k = 0; k < K; ++k) {
-                const double p = exp((double)c[k] - mx) / se;
-                const double gk = ok ? (p - (k == y ? 1.0 : 0.0)) * invB : __builtin_nan("");
-                grad[(int64_t)b * K + k] = (float)gk;
-            }
-        }
-    }
-    const double s = block_sum(part);
-    if (threadIdx.x == 0) *loss = (float)(s * invB);
+// class count k of a row: the sum of its population (exact in fp64)
+__device__ inline double class_count(const float *c, int k, int P) {
+    double s = 0.0;
+    for (int p = 0; p < P; ++p) s += (double)c[(int64_t)k * P + p];
+    return s;
 }
 
-// Mean squared error, first pass: block z sums (c - y)^2 over its chunk and
-// writes the gradient 2 (c - y) / n.
-__global__ __launch_bounds__(kThreads) void mse_pass1_kernel(int64_t n, int64_t chunk,
+__device__ inline double wave_max(double v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) v = fmax(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// Cross-entropy with the class counts as logits.  One wave per row (4 rows
+// per workgroup).  Rows of up to kCeRowLds counts are staged in LDS with
+// coalesced loads; lane l sums the populations of classes l, l+64, ... once
+// into LDS, max and sum of exponentials are wave reductions in a fixed
+// butterfly order, and the per-class gradient is written back to the row's
+// K*P neurons with coalesced stores.  Longer rows read the counts from
+// global memory.  The row's loss goes to partial[b] (fp64), summed in fixed
+// order by ce_sum_kernel.  A label outside [0, K) makes that row's loss and
+// gradient NaN (no out-of-range access).
+constexpr int kCeRowLds = 1024;
+constexpr int kRowsPerBlock = kThreads / 64;
+__global__ __launch_bounds__(kThreads) void ce_rows_kernel(int B, int K, int P,
+                                                           const float *__restrict__ counts,
+                                                           const int32_t *__restrict__ labels,
+                                                           float *__restrict__ grad,
+                                                           double *__restrict__ partial) {
+    __shared__ float rowbuf[kRowsPerBlock][kCeRowLds];
+    __shared__ double cls[kRowsPerBlock][kCeRowLds];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int b = blockIdx.x * kRowsPerBlock + wave;
+    const int64_t row = (int64_t)K * P;
+    const bool staged = row <= kCeRowLds;
+    const float *cg = counts + (int64_t)(b < B ? b : 0) * row;
+    if (staged && b < B)
+        for (int j = lane; j < (int)row; j += 64) rowbuf[wave][j] = cg[j];
+    __syncthreads();  // every wave reaches it, rows past B included
+    if (staged && b < B)
+        for (int k = lane; k < K; k += 64) cls[wave][k] = class_count(rowbuf[wave], k, P);
+    __syncthreads();
+    if (b >= B) return;
+    const int y = labels[b];
+    const bool ok = (y >= 0 && y < K);
+    double mx = -__builtin_inf();
+    for (int k = lane; k < K; k += 64)
+        mx = fmax(mx, staged ? cls[wave][k] : class_count(cg, k, P));
+    mx = wave_max(mx);
+    double se = 0.0;
+    for (int k = lane; k < K; k += 64)
+        se += exp((staged ? cls[wave][k] : class_count(cg, k, P)) - mx);
+    se = wave_sum(se);
+    const double invB = 1.0 / (double)B;
+    float *gr = grad ? grad + (int64_t)b * row : nullptr;
+    if (gr && staged) {
+        // per-class gradient in place of the class counts, then spread
+        // over each population with coalesced stores
+        for (int k = lane; k < K; k += 64) {
+            const double p = exp(cls[wave][k] - mx) / se;
+            rowbuf[wave][k] = ok ? (float)((p - (k == y ? 1.0 : 0.0)) * invB)
+                                 : __builtin_nanf("");
+        }
+        // read back by other lanes of the same wave: a wave's LDS accesses
+        // complete in order, so only the compiler must keep the order
+        __builtin_amdgcn_wave_barrier();
+        for (int j = lane; j < (int)row; j += 64) gr[j] = rowbuf[wave][j / P];
+    } else if (gr) {
+        for (int k = lane; k < K; k += 64) {
+            const double p = exp(class_count(cg, k, P) - mx) / se;
+            const double gk = ok ? (p - (k == y ? 1.0 : 0.0)) * invB : __builtin_nan("");
+            for (int q = 0; q < P; ++q) gr[(int64_t)k * P + q] = (float)gk;
+        }
+    }
+    if (lane == 0) {
+        const double cy = ok ? (staged ? cls[wave][y] : class_count(cg, y, P)) : 0.0;
+        partial[b] = ok ? (mx + log(se)) - cy : __builtin_nan("");
+    }
+}
+
+// loss = sum_b partial[b] / B, fixed order (strided per thread, then tree)
+__global__ __launch_bounds__(kThreads) void ce_sum_kernel(int B, const double *__restrict__ partial,
+                                                          float *__restrict__ loss) {
+    double part = 0.0;
+    for (int b = threadIdx.x; b < B; b += kThreads) part += partial[b];
+    const double s = block_sum(part);
+    if (threadIdx.x == 0) *loss = (float)(s / (double)B);
+}
+
+// Mean squared error, first pass: block z sums (c - y)^2 over its chunk of
+// the n = B K class entries and writes the gradient 2 (c - y) / n to each
+// neuron of the class's population.
+__global__ __launch_bounds__(kThreads) void mse_pass1_kernel(int64_t n, int64_t chunk, int P,
                                                              const float *__restrict__ counts,
                                                              const float *__restrict__ targets,
                                                              float *__restrict__ grad,
@@ -74,9 +136,11 @@ __global__ __launch_bounds__(kThreads) void mse_pass1_kernel(int64_t n, int64_t 
     const double scale = 2.0 / (double)n;
     double part = 0.0;
     for (int64_t j = beg + threadIdx.x; j < end; j += kThreads) {
-        const double d = (double)counts[j] - (double)targets[j];
+        // class entry j owns neurons j*P .. j*P + P - 1 of the [B, K*P] counts
+        const double d = class_count(counts + j * P, 0, P) - (double)targets[j];
         part += d * d;
-        if (grad) grad[j] = (float)(scale * d);
+        if (grad)
+            for (int q = 0; q < P; ++q) grad[j * P + q] = (float)(scale * d);
     }
     const double s = block_sum(part);
     if (threadIdx.x == 0) partial[blockIdx.x] = s;
@@ -102,18 +166,24 @@ void mse_shape(int64_t n, int &blocks, int64_t &chunk) {
 }  // namespace
 
 size_t loss_workspace_bytes(int kind, int B, int K) {
-    if (kind != SNN_LOSS_MSE_COUNT || B <= 0 || K <= 0) return 0;
+    if (B <= 0 || K <= 0) return 0;
+    if (kind == SNN_LOSS_CE_COUNT) return align_up((size_t)B * sizeof(double));  // row losses
     int blocks;
     int64_t chunk;
     mse_shape((int64_t)B * K, blocks, chunk);
     return align_up((size_t)blocks * sizeof(double));
 }
 
-hipError_t launch_loss(int kind, int B, int K, const float *counts, const int32_t *labels,
-                       const float *targets, float *loss, float *grad, void *ws,
-                       hipStream_t s) {
+hipError_t launch_loss(int kind, int B, int K, int P, const float *counts,
+                       const int32_t *labels, const float *targets, float *loss, float *grad,
+                       void *ws, hipStream_t s) {
     if (kind == SNN_LOSS_CE_COUNT) {
-        ce_kernel<<<1, kThreads, 0, s>>>(B, K, counts, labels, loss, grad);
+        double *partial = reinterpret_cast<double *>(ws);
+        ce_rows_kernel<<<(B + kRowsPerBlock - 1) / kRowsPerBlock, kThreads, 0, s>>>(
+            B, K, P, counts, labels, grad, partial);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        ce_sum_kernel<<<1, kThreads, 0, s>>>(B, partial, loss);
         return hipGetLastError();
     }
     const int64_t n = (int64_t)B * K;
@@ -121,7 +191,7 @@ hipError_t launch_loss(int kind, int B, int K, const float *counts, const int32_
     int64_t chunk;
     mse_shape(n, blocks, chunk);
     double *partial = reinterpret_cast<double *>(ws);
-    mse_pass1_kernel<<<blocks, kThreads, 0, s>>>(n, chunk, counts, targets, grad, partial);
+    mse_pass1_kernel<<<blocks, kThreads, 0, s>>>(n, chunk, P, counts, targets, grad, partial);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     mse_pass2_kernel<<<1, kThreads, 0, s>>>(blocks, n, partial, loss);

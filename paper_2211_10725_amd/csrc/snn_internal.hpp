@@ -119,9 +119,10 @@ hipError_t launch_transpose(int rows, int cols, const void *src, int64_t ld_src,
 
 // ---- losses (loss.hip) -----------------------------------------------------
 size_t loss_workspace_bytes(int kind, int B, int K);
-hipError_t launch_loss(int kind, int B, int K, const float *counts, const int32_t *labels,
-                       const float *targets, float *loss, float *grad, void *ws,
-                       hipStream_t s);
+// counts / grad [B, K*P] (P neurons per class), targets [B, K]
+hipError_t launch_loss(int kind, int B, int K, int P, const float *counts,
+                       const int32_t *labels, const float *targets, float *loss, float *grad,
+                       void *ws, hipStream_t s);
 
 // ---- AdamW weight update (optim.hip) -------------------------------------------
 // per-step coefficients, computed on the host in double

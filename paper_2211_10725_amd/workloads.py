@@ -38,6 +38,7 @@ class Workload:
     current_std: float = 1.0
     target_hi: float = 50.0
     rec_hi: float = 0.5     # recurrent weights of 'rleaky' layers ~ U(-rec_hi, rec_hi)
+    pop: int = 1            # output neurons per class (population code when > 1)
     description: str = ""
     extra: dict = field(default_factory=dict)
 
@@ -49,6 +50,11 @@ class Workload:
         if s["kind"] == "conv":
             return (s["c_in"], s["h"], s["w"])
         return (s["n"],)
+
+    @property
+    def classes(self):
+        """Number of classes: output neurons divided by the population size."""
+        return self.out_features // self.pop
 
     @property
     def out_features(self):
@@ -96,6 +102,20 @@ WORKLOADS = {
         layers=[_dense(784, 1000, "rleaky", 0.95), _dense(1000, 10, "rleaky", 0.95)],
         description="Dense SNN 784-1000-10, recurrent Leaky (eq. 7) beta=0.95, one recurrent "
                     "weight per neuron ~U(-0.5,0.5), T=25, B=128, fp32"),
+    # Population codes (Sec. V): one time step, 500 output neurons pooled as
+    # 50 per class, on CIFAR-10-shaped 3x32x32 rate-coded inputs; the DSNN
+    # with the wider input layer and the CSNN with the wider terminal layer.
+    "pop_dsnn_t1_b128": Workload(
+        "pop_dsnn_t1_b128", T=1, B=128, pop=50,
+        layers=[_dense(3072, 1000, "leaky", 0.95), _dense(1000, 500, "leaky", 0.95)],
+        description="Population-coded dense SNN 3072-1000-500 (50 neurons per class), "
+                    "Leaky beta=0.95, T=1, B=128, fp32"),
+    "pop_csnn_t1_b128": Workload(
+        "pop_csnn_t1_b128", T=1, B=128, pop=50,
+        layers=[_conv(3, 32, 32, 12, "leaky", 0.5), _conv(12, 14, 14, 64, "leaky", 0.5),
+                _dense(1600, 500, "leaky", 0.5)],
+        description="Population-coded conv SNN 3x32x32-5C12-MP2-5C64-MP2-500 (50 neurons "
+                    "per class), Leaky beta=0.5, T=1, B=128, fp32"),
     # Deeper, wider dense net in half precision operands.
     "dsnn_half_t100_b512": Workload(
         "dsnn_half_t100_b512", T=100, B=512, rate_hi=0.5, dtype="f16",
@@ -202,12 +222,12 @@ def current_input(wl: Workload, seed: int) -> np.ndarray:
 
 
 def labels(wl: Workload, seed: int) -> np.ndarray:
-    return _rng(20_000 + seed).integers(0, wl.out_features, size=wl.B).astype(np.int32)
+    return _rng(20_000 + seed).integers(0, wl.classes, size=wl.B).astype(np.int32)
 
 
 def targets(wl: Workload, seed: int) -> np.ndarray:
     return _rng(30_000 + seed).uniform(0.0, wl.target_hi,
-                                       size=(wl.B, wl.out_features)).astype(np.float32)
+                                       size=(wl.B, wl.classes)).astype(np.float32)
 
 
 def make_inputs(wl: Workload, seed: int = 0) -> dict:

@@ -82,13 +82,18 @@ def test_validation_errors_before_launch():
 
 def test_loss_validation():
     L = snn.lib()
-    assert L.snn_loss(0, 0, 10, 16, 32, None, 48, 64, None, 0, None) == 2   # B = 0
-    assert L.snn_loss(0, 4, 10, 16, None, None, 48, 64, None, 0, None) == 1  # CE needs labels
-    assert L.snn_loss(1, 4, 10, 16, None, None, 48, 64, None, 0, None) == 1  # MSE needs targets
-    assert L.snn_loss(5, 4, 10, 16, 32, None, 48, 64, None, 0, None) == 5
+    assert L.snn_loss(0, 0, 10, 1, 16, 32, None, 48, 64, None, 0, None) == 2   # B = 0
+    assert L.snn_loss(0, 4, 10, 1, 16, None, None, 48, 64, None, 0, None) == 1  # CE needs labels
+    assert L.snn_loss(1, 4, 10, 1, 16, None, None, 48, 64, None, 0, None) == 1  # MSE needs targets
+    assert L.snn_loss(5, 4, 10, 1, 16, 32, None, 48, 64, None, 0, None) == 5
+    assert L.snn_loss(0, 4, 10, 0, 16, 32, None, 48, 64, None, 0, None) == 2   # P = 0
     need = L.snn_loss_workspace_bytes(1, 64, 65536)
     assert need > 0
-    assert L.snn_loss(1, 64, 65536, 16, None, 32, 48, 64, 256, need - 1, None) == 6
+    assert L.snn_loss(1, 64, 65536, 1, 16, None, 32, 48, 64, 256, need - 1, None) == 6
+    # cross-entropy keeps one fp64 loss per row for its fixed-order sum
+    need = L.snn_loss_workspace_bytes(0, 128, 10)
+    assert need >= 128 * 8
+    assert L.snn_loss(0, 128, 10, 50, 16, 32, None, 48, 64, 256, need - 1, None) == 6
 
 
 def test_sizes_queries():

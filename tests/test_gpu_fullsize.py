@@ -74,7 +74,7 @@ def test_scan_wide_full_size_sampled():
     tgt_h = wls.targets(wl, 0)
     loss = torch.empty(4, dtype=torch.float32, device=DEV)
     gc = torch.empty((B, N), dtype=torch.float32, device=DEV)
-    snn.snn_loss(snn.LOSS_MSE_COUNT, B, N, torch.as_tensor(c_s).to(DEV),
+    snn.snn_loss(snn.LOSS_MSE_COUNT, B, N, 1, torch.as_tensor(c_s).to(DEV),
                  None, torch.as_tensor(tgt_h).to(DEV), loss, gc, net.ws)
     L, gc_o = oracle.loss_mse(c_s, tgt_h)
     assert abs(_np(loss)[0] - L) <= 1e-6 * abs(L)

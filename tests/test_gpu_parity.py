@@ -396,7 +396,8 @@ def test_loss_ce(B, K):
     y = rng.integers(0, K, B).astype(np.int32)
     loss = torch.empty(4, dtype=torch.float32, device=DEV)
     g = torch.empty((B, K), dtype=torch.float32, device=DEV)
-    snn.snn_loss(snn.LOSS_CE_COUNT, B, K, _t(c), _t(y), None, loss, g, None)
+    ws = _ws(snn.snn_loss_workspace_bytes(snn.LOSS_CE_COUNT, B, K))
+    snn.snn_loss(snn.LOSS_CE_COUNT, B, K, 1, _t(c), _t(y), None, loss, g, ws)
     L, rg = oracle.loss_ce(c, y)
     assert abs(_np(loss)[0] - L) <= 1e-6 * max(1.0, abs(L))
     assert_close(_np(g), rg, 1e-5, what="CE grad")
@@ -410,10 +411,31 @@ def test_loss_mse(B, K):
     loss = torch.empty(4, dtype=torch.float32, device=DEV)
     g = torch.empty((B, K), dtype=torch.float32, device=DEV)
     ws = _ws(snn.snn_loss_workspace_bytes(snn.LOSS_MSE_COUNT, B, K))
-    snn.snn_loss(snn.LOSS_MSE_COUNT, B, K, _t(c), None, _t(y), loss, g, ws)
+    snn.snn_loss(snn.LOSS_MSE_COUNT, B, K, 1, _t(c), None, _t(y), loss, g, ws)
     L, rg = oracle.loss_mse(c, y)
     assert abs(_np(loss)[0] - L) <= 1e-6 * abs(L)
     assert_close(_np(g), rg, 1e-6, what="MSE grad")
+
+
+@pytest.mark.parametrize("kind", [snn.LOSS_CE_COUNT, snn.LOSS_MSE_COUNT])
+@pytest.mark.parametrize("B,K,P", [(128, 10, 50), (3, 7, 2), (300, 10, 1), (2, 1, 9)])
+def test_loss_population(kind, B, K, P):
+    """Population code (Sec. V): class k pools neurons kP .. kP+P-1."""
+    rng = np.random.default_rng(B * K + P)
+    c = rng.integers(0, 3, (B, K * P)).astype(np.float32)
+    loss = torch.empty(4, dtype=torch.float32, device=DEV)
+    g = torch.empty((B, K * P), dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_loss_workspace_bytes(kind, B, K))
+    if kind == snn.LOSS_CE_COUNT:
+        y = rng.integers(0, K, B).astype(np.int32)
+        snn.snn_loss(kind, B, K, P, _t(c), _t(y), None, loss, g, ws)
+        L, rg = oracle.loss_ce(c, y, P)
+    else:
+        y = rng.uniform(0, 2 * P, (B, K)).astype(np.float32)
+        snn.snn_loss(kind, B, K, P, _t(c), None, _t(y), loss, g, ws)
+        L, rg = oracle.loss_mse(c, y, P)
+    assert abs(_np(loss)[0] - L) <= 1e-6 * max(1.0, abs(L))
+    assert_close(_np(g), rg, 1e-5, what="dL/dcounts")
 
 
 # ---------------------------------------------------------------------------
@@ -457,9 +479,10 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
     rs = reset == snn.RESET_SURROGATE
     T, B = wl.T, wl.B
     n = len(wl.layers)
+    P = wl.pop
     L, fwds, bwds = oracle.net_step(wl.layers, inp["params"], inp["x"], wl.loss,
                                     labels=inp.get("labels"), targets=inp.get("targets"),
-                                    slope=wl.slope, reset_surrogate=rs)
+                                    slope=wl.slope, reset_surrogate=rs, pop=P)
     net = snn.Network(wl, inp["params"], device=DEV, reset_grad=reset, flags=flags)
     xs = []
     for li, spec in enumerate(wl.layers):
@@ -485,16 +508,17 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
                       what=f"L{li} layer call")
     # loss on the oracle's counts
     c_o = np.asarray(fwds[-1]["counts"], np.float32).reshape(B, -1)
-    K = c_o.shape[1]
+    K = c_o.shape[1] // P
     loss = torch.empty(4, dtype=torch.float32, device=DEV)
-    gc = torch.empty((B, K), dtype=torch.float32, device=DEV)
+    gc = torch.empty(c_o.shape, dtype=torch.float32, device=DEV)
     if wl.loss == "ce":
-        snn.snn_loss(snn.LOSS_CE_COUNT, B, K, _t(c_o), _t(inp["labels"]), None, loss, gc, net.ws)
-        L2, gc_o = oracle.loss_ce(c_o, inp["labels"])
-    else:
-        snn.snn_loss(snn.LOSS_MSE_COUNT, B, K, _t(c_o), None, _t(inp["targets"]), loss, gc,
+        snn.snn_loss(snn.LOSS_CE_COUNT, B, K, P, _t(c_o), _t(inp["labels"]), None, loss, gc,
                      net.ws)
-        L2, gc_o = oracle.loss_mse(c_o, inp["targets"])
+        L2, gc_o = oracle.loss_ce(c_o, inp["labels"], P)
+    else:
+        snn.snn_loss(snn.LOSS_MSE_COUNT, B, K, P, _t(c_o), None, _t(inp["targets"]), loss, gc,
+                     net.ws)
+        L2, gc_o = oracle.loss_mse(c_o, inp["targets"], P)
     assert abs(_np(loss)[0] - L2) <= 1e-5 * max(1.0, abs(L2))
     assert_close(_np(gc), gc_o, 1e-5, what="dL/dcounts")
     g = gc_o
@@ -568,7 +592,7 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
 
 
 @pytest.mark.parametrize("name", ["dsnn_leaky_t25_b32", "dsnn_synaptic_t50_b256", "csnn_t25_b128",
-                                  "dsnn_rleaky_t25_b128"])
+                                  "dsnn_rleaky_t25_b128", "pop_dsnn_t1_b128", "pop_csnn_t1_b128"])
 @pytest.mark.parametrize("path", list(PATHS))
 def test_step_full_size_stagewise(name, path):
     wl = wls.get(name)
@@ -581,7 +605,9 @@ def test_step_full_size_stagewise(name, path):
                                             ("scan_wide_t1000_b64", 60, 4, 1000),
                                             ("csnn_t25_b128", 6, 4, None),
                                             ("dsnn_half_t100_b512", 12, 8, 320),
-                                            ("dsnn_rleaky_t25_b128", 15, 6, 130)])
+                                            ("dsnn_rleaky_t25_b128", 15, 6, 130),
+                                            ("pop_dsnn_t1_b128", 1, 16, 200),
+                                            ("pop_csnn_t1_b128", 1, 5, None)])
 @pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
 @pytest.mark.parametrize("path", list(PATHS))
 def test_step_scaled_stagewise(name, T, B, width, reset, path):
