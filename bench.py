@@ -163,6 +163,10 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mode", choices=["bench", "pmc"], default="bench")
+    ap.add_argument("--batch", type=int, default=None,
+                    help="run the workload at this batch size (same layers and T)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the forward + BPTT step in a HIP graph and time its replays")
     ap.add_argument("--update", action="store_true",
                     help="end every step with the fused AdamW update (the paper's "
                          "training step); the default step is forward + BPTT")
@@ -188,6 +192,12 @@ def main():
     snn.lib()  # fail loudly before anything else if the HIP library is missing
     torch.cuda.set_device(0)
     wl = wls.get(args.workload)
+    if args.batch is not None:
+        wl = wls.scaled(wl, B=args.batch)
+    if args.graph and args.update:
+        print("--graph captures the forward + BPTT step only (the AdamW step count is a "
+              "host value)", file=sys.stderr)
+        sys.exit(2)
     stream = torch.cuda.Stream()  # default priority
     params = wls.init_params(wl, args.seed)
     net = snn.Network(wl, params, device="cuda",
@@ -248,12 +258,28 @@ def main():
                 kev.append(e)
 
         marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-        torch.cuda.synchronize()
-        marks[0].record(stream)
-        for i in range(args.steps):
-            net.step_stages(x, labels=y, targets=tgt, hook=rec_dom, update=upd)
-            marks[i + 1].record(stream)
-        torch.cuda.synchronize()
+        if args.graph:
+            graph = net.capture_step(x, labels=y, targets=tgt)
+            for _ in range(args.warmup):
+                graph.replay()
+            torch.cuda.synchronize()
+            marks[0].record(stream)
+            for i in range(args.steps):
+                graph.replay()
+                marks[i + 1].record(stream)
+            torch.cuda.synchronize()
+            # graph replays cannot host events between their kernels: the
+            # dominant stage is timed in eager steps right after them
+            for _ in range(min(args.steps, 20)):
+                net.step_stages(x, labels=y, targets=tgt, hook=rec_dom)
+            torch.cuda.synchronize()
+        else:
+            torch.cuda.synchronize()
+            marks[0].record(stream)
+            for i in range(args.steps):
+                net.step_stages(x, labels=y, targets=tgt, hook=rec_dom, update=upd)
+                marks[i + 1].record(stream)
+            torch.cuda.synchronize()
         total_ms = marks[0].elapsed_time(marks[-1])
         per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
         kms = [kev[i].elapsed_time(kev[i + 1]) for i in range(0, len(kev), 2)]
@@ -281,6 +307,8 @@ def main():
     roof["traffic"] = tr
     roof["kernel"] = dom_key + _stage_kernels(net, dom_name, dom_li, args.fp32_mfma)
     roof["avg_launch_ms"] = round(k_avg_ms, 5)
+    if args.graph:
+        roof["timed"] = "eager steps right after the graph replays"
     roof["algorithmic_per_launch"] = work
 
     out = {
@@ -293,7 +321,9 @@ def main():
                    "surrogate_slope": wl.slope, "input": "Bernoulli rate-coded spikes"
                    if wl.input == "spikes" else "normal currents",
                    "includes": "forward + loss + BPTT backward + fused AdamW update"
-                   if upd else "forward + loss + BPTT backward, no optimizer update"},
+                   if upd else "forward + loss + BPTT backward, no optimizer update",
+                   "launch": "one HIP graph replay per step" if args.graph
+                   else "eager library calls"},
         "step_ms": {"median": round(per_step[len(per_step) // 2], 5),
                     "p10": round(per_step[len(per_step) // 10], 5),
                     "p90": round(per_step[(9 * len(per_step)) // 10], 5)},

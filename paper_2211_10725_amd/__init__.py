@@ -348,6 +348,24 @@ class Network:
         self.loss_and_grad(labels, targets, stream)
         self.backward(x, stream)
 
+    def capture_step(self, x, labels=None, targets=None, warmup=2):
+        """Capture one forward + loss + BPTT step into a HIP graph (torch's
+        CUDAGraph on ROCm) and return it; ``graph.replay()`` then reruns the
+        step on the same buffers with one launch from the host.  The library
+        records no memset, allocates nothing and never synchronises, so every
+        call of the step can be captured."""
+        torch = self.torch
+        side = torch.cuda.Stream()  # default priority
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for _ in range(warmup):
+                self.step(x, labels, targets)
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            self.step(x, labels, targets)
+        return graph
+
     def init_adamw(self, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2):
         """Optimizer state for ``update``: zero moments per parameter tensor
         and, for fp16 weights, an fp32 master copy (the fp16 weights the
