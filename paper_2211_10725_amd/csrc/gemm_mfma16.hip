@@ -723,6 +723,53 @@ __global__ __launch_bounds__(256) void transpose_kernel(int rows, int cols, cons
     }
 }
 
+// Bytes: dst[c][r] = src[r][c] for a 64 x 64 tile with 16-byte global loads
+// and stores (4 threads per tile row).  The LDS tile has a 68-byte row
+// stride: written 4 bytes at a time, and the column reads of 16 rows spaced
+// 16 apart fall in distinct banks.
+__global__ __launch_bounds__(256) void transpose_u8_kernel(int rows, int cols,
+                                                           const uint8_t *__restrict__ src,
+                                                           int64_t lds_, uint8_t *__restrict__ dst,
+                                                           int64_t ldd) {
+    __shared__ __attribute__((aligned(16))) uint8_t tile[64 * 68];
+    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    const int t = threadIdx.x;
+    {
+        const int r = t >> 2, cc = (t & 3) * 16;
+        const int gr = r0 + r, gc = c0 + cc;
+        uint32_t w[4] = {0u, 0u, 0u, 0u};
+        if (gr < rows) {
+            const uint8_t *p = src + (int64_t)gr * lds_ + gc;
+            if (gc + 16 <= cols && (((uintptr_t)p) & 15) == 0) {
+                const uint4 v = *reinterpret_cast<const uint4 *>(p);
+                w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+            } else {
+                for (int e = 0; e < 16; ++e)
+                    if (gc + e < cols) w[e / 4] |= (uint32_t)p[e] << (8 * (e % 4));
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) *reinterpret_cast<uint32_t *>(&tile[r * 68 + cc + 4 * q]) = w[q];
+    }
+    __syncthreads();
+    {
+        const int c = t >> 2, rr = (t & 3) * 16;
+        const int gc = c0 + c, gr = r0 + rr;
+        if (gc < cols) {
+            uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+            for (int e = 0; e < 16; ++e) w[e / 4] |= (uint32_t)tile[(rr + e) * 68 + c] << (8 * (e % 4));
+            uint8_t *q = dst + (int64_t)gc * ldd + gr;
+            if (gr + 16 <= rows && (((uintptr_t)q) & 15) == 0) {
+                *reinterpret_cast<uint4 *>(q) = make_uint4(w[0], w[1], w[2], w[3]);
+            } else {
+                for (int e = 0; e < 16; ++e)
+                    if (gr + e < rows) q[e] = (uint8_t)(w[e / 4] >> (8 * (e % 4)));
+            }
+        }
+    }
+}
+
 }  // namespace
 
 hipError_t launch_transpose(int rows, int cols, const void *src, int64_t ld_src, int elem_bytes,
@@ -741,8 +788,8 @@ hipError_t launch_transpose(int rows, int cols, const void *src, int64_t ld_src,
         transpose_kernel<uint16_t, false><<<grid, 256, 0, s>>>(
             rows, cols, reinterpret_cast<const uint16_t *>(src), ld_src, dst, ld_dst, 0);
     } else {
-        transpose_kernel<uint8_t, false><<<grid, 256, 0, s>>>(
-            rows, cols, reinterpret_cast<const uint8_t *>(src), ld_src, dst, ld_dst, 0);
+        transpose_u8_kernel<<<grid, 256, 0, s>>>(rows, cols, reinterpret_cast<const uint8_t *>(src),
+                                                 ld_src, reinterpret_cast<uint8_t *>(dst), ld_dst);
     }
     return hipGetLastError();
 }

@@ -214,8 +214,12 @@ PATHS = {"split": 0, "fp32mfma": snn.FLAG_FP32_MFMA}
 
 
 # (1040, 1100, 1000): large enough for the 256 x 256 asynchronous kernel with
-# fp16 weights, ragged in M and N, and a last k-tile of 8 values
-@pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784), (1040, 1100, 1000)])
+# fp16 weights, ragged in M and N, and a last k-tile of 8 values.  Layers with
+# at most 16 outputs: (12800, 10, 1000) the readout, (5000, 7, 1003) rows not
+# 4-aligned, (777, 16, 1500) and (2000, 10, 4096) long contractions.
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784), (1040, 1100, 1000),
+                                                 (12800, 10, 1000), (5000, 7, 1003),
+                                                 (777, 16, 1500), (2000, 10, 4096)])
 @pytest.mark.parametrize("wdt", ["f32", "f16"])
 @pytest.mark.parametrize("path", list(PATHS))
 def test_synapse_fwd(M, N, K, wdt, path):
