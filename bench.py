@@ -56,10 +56,11 @@ def stage_sources(stage_key: str):
     return STAGE_SOURCES["synapse" if stage_key.startswith("synapse") else "neuron"]
 
 
-def stored_traffic(stage_key: str):
-    """HBM bytes per launch of a stage from the committed counter summary,
-    if its kernels' sources are unchanged since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", "traffic.md")
+def stored_traffic(workload: str, stage_key: str):
+    """HBM bytes per launch of a stage of a workload from its committed counter
+    summary, if the stage's kernel sources are unchanged since the counters
+    were taken."""
+    path = os.path.join(ROOT, "profiles", f"{workload}_traffic.md")
     if not os.path.exists(path):
         return None
     txt = open(path).read()
@@ -303,7 +304,7 @@ def main():
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                 "unit": "GB/s"}
     roof["frac"] = round(achieved / roof["peak"], 4)
-    tr = stored_traffic(dom_key)
+    tr = stored_traffic(wl.name, dom_key)
     roof["traffic"] = tr
     roof["kernel"] = dom_key + _stage_kernels(net, dom_name, dom_li, args.fp32_mfma)
     roof["avg_launch_ms"] = round(k_avg_ms, 5)
@@ -415,8 +416,8 @@ def _stage_kernels(net, name, li, fp32_mfma):
         g = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"
         return f": im2col_kernel + {g} + pool_kernel (the whole stage is timed)"
     if kind == "mfma16" and passes == 3:
-        return (": split_planes_kernel (weights into bf16 planes) + gemm16_kernel"
-                " (+ splitk_reduce_kernel when split over K)")
+        return (": gemm16_kernel, 3 exact bf16 passes (+ split_planes_kernel when the weights"
+                " are split into planes up front, + splitk_reduce_kernel when split over K)")
     if kind == "mfma16":
         return ": gemm16_kernel (+ splitk_reduce_kernel when split over K)"
     return ": gemm_f32_kernel (+ splitk_reduce_kernel when split over K)"
