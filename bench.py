@@ -332,7 +332,7 @@ def main():
         "stage_ms": {k: round(v, 5) for k, v in split.items()},
         "stage_roofline": _stage_rooflines(net, split, args.fp32_mfma),
     }
-    if upd and split.get("update"):
+    if upd and split.get("update") and net.opt_tensors:
         # fused AdamW: read param, grad, m, v and write param, m, v (4 B each)
         # per parameter, plus the 2 B fp16 copy of fp16 weights
         nb = sum(28 * t[0].numel() + (2 * t[0].numel() if t[4] is not None else 0)
