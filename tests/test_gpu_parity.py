@@ -632,6 +632,18 @@ def test_step_scaled_stagewise(name, T, B, width, reset, path):
         np.testing.assert_array_equal(a, b)
 
 
+@pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
+def test_step_recurrent_conv_stagewise(reset):
+    """Recurrent neurons (eq. 7) behind the convolutional synapses: one
+    recurrent weight per pooled output neuron."""
+    wl = wls.scaled(wls.get("csnn_t25_b128"), T=6, B=3)
+    for spec in wl.layers:
+        spec["neuron"] = "rleaky"
+    inp = wls.make_inputs(wl, seed=4)
+    assert all(len(p) == 3 for p in inp["params"])
+    _check_step_stagewise(wl, inp, reset)
+
+
 def test_step_end_to_end_unforced():
     """The whole step, oracle run on its own; flips are counted, gradient
     columns downstream of a flip are excluded."""
