@@ -79,7 +79,11 @@ def stage_work(net, name, li):
                    (t, b, n), + 4 B count per (b, n)
       reverse scan 4 B read membrane + 4 B read dL/dz (full only) + 4 B write
                    dL/dI per (t, b, n), + 4 B colsum per (b, n), + 4 B recurrent-
-                   weight column sum per (b, n) for recurrent neurons (eq. 7)."""
+                   weight column sum per (b, n) for recurrent neurons (eq. 7);
+                   with the readout's input gradient folded in, dL/dz is not
+                   read but computed from the readout's dL/dI (4 B per
+                   (t, b, readout neuron)), and the readout's synapse
+                   backward computes dW only."""
     d = net.descs[li]
     TB = d.T * d.B
     if d.synapse == 1:
@@ -90,14 +94,19 @@ def stage_work(net, name, li):
     if name == "synapse_fwd":
         return "flop", 2.0 * macs
     if name == "synapse_bwd":
-        return "flop", 2.0 * macs * (2 if li > 0 else 1)  # dW, and dx below the input layer
+        # dW, and dx below the input layer unless the layer below folds it in
+        dx = li > 0 and net.dup[li] is None
+        return "flop", 2.0 * macs * (2 if dx else 1)
     el = TB * d.n_out
     cols = d.B * d.n_out
     if name == "neuron_fwd":
         return "byte", 9.0 * el + 4.0 * cols
     if name == "neuron_bwd":
-        full = li < len(net.descs) - 1
         rec = 4.0 * cols if d.neuron == 2 else 0.0
+        if net.fold[li]:
+            up = 4.0 * TB * net.descs[li + 1].n_out
+            return "byte", 8.0 * el + up + 4.0 * cols + rec
+        full = li < len(net.descs) - 1
         return "byte", (12.0 if full else 8.0) * el + 4.0 * cols + rec
     return None, 0.0
 
@@ -378,6 +387,8 @@ def _contraction_kind(net, li, fp32_mfma):
     ('mfma32', 1).  A conv layer's product has one row per conv output that a
     pool window reads and one column per output channel."""
     d = net.descs[li]
+    if _narrow_contraction(net, li, fp32_mfma):
+        return "mfma16", 3 if d.w_dtype == 0 else 1
     if d.synapse == 1:
         rows = 4 * d.T * d.B * ((d.h_in - 4) // 2) * ((d.w_in - 4) // 2)
         cols = d.c_out
@@ -389,6 +400,15 @@ def _contraction_kind(net, li, fp32_mfma):
     if d.w_dtype == 0:
         return "mfma16", 3   # fp32 weights: three exact bf16 parts
     return "mfma16", 1       # fp16 weights: one fp16 pass
+
+
+def _narrow_contraction(net, li, fp32_mfma):
+    """Whether layer li's forward product runs on the kernel for at most 16
+    outputs (mirrors narrow_fwd_applies in skinny.hip)."""
+    d = net.descs[li]
+    if fp32_mfma or d.synapse != 0 or d.n_out > 16 or d.n_in < 256:
+        return False
+    return (d.in_dtype == 3 and d.w_dtype in (0, 1)) or (d.in_dtype == 1 and d.w_dtype == 1)
 
 
 def _async_contraction(net, li, fp32_mfma):
@@ -411,6 +431,10 @@ def _stage_kernels(net, name, li, fp32_mfma):
         return ": neuron_bwd_kernel"
     if name == "synapse_fwd" and _async_contraction(net, li, fp32_mfma):
         return ": widen_kernel (spikes to fp16) + gemm_async_kernel"
+    if name == "synapse_fwd" and _narrow_contraction(net, li, fp32_mfma):
+        return ": narrow_fwd_kernel (16 outputs per MFMA tile, weights staged in LDS)"
+    if name == "neuron_bwd" and net.fold[li]:
+        return ": neuron_bwd_kernel (the readout's dx folded in)"
     kind, passes = _contraction_kind(net, li, fp32_mfma)
     if net.descs[li].synapse == 1:
         g = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"

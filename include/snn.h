@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 3
+#define SNN_ABI_VERSION 4
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -102,6 +102,16 @@ typedef enum snn_status {
 #define SNN_GRAD_FULL 0  /* g [T,B,n_out] fp32 */
 #define SNN_GRAD_BCAST 1 /* g [B,n_out] fp32, the same for every t (a loss on
                             counts summed over T) */
+#define SNN_GRAD_FOLD 2  /* g is the input gradient of a dense layer above with
+                            n_up <= 16 outputs (a readout), computed inside the
+                            reverse scan instead of being read:
+                              g[t,b,n] = sum_{j < n_up} dcur_up[t,b,j] w_up[j,n]
+                            in fp32 with j ascending (exact products), i.e.
+                            the grad_x (dx = dI W) that layer's backward
+                            would return.  It saves writing and re-reading
+                            the [T,B,n_out] fp32 gradient.  Supported for
+                            layers with n_out >= 64 (SNN_ERR_UNSUPPORTED
+                            otherwise). */
 
 /* descriptor flags */
 #define SNN_FLAG_FP32_MFMA 1 /* run every contraction on fp32 MFMA instead of
@@ -137,9 +147,18 @@ typedef struct snn_layer_desc {
 } snn_layer_desc;
 
 typedef struct snn_grad_in {
-    int32_t kind;       /* SNN_GRAD_FULL | SNN_GRAD_BCAST */
-    int32_t reserved;   /* must be 0 */
-    const float *g;     /* dL/dz of this layer's output spikes, fp32 */
+    int32_t kind;          /* SNN_GRAD_FULL | SNN_GRAD_BCAST | SNN_GRAD_FOLD */
+    int32_t n_up;          /* SNN_GRAD_FOLD: outputs of the layer above, 1..16
+                              (SNN_ERR_SHAPE otherwise); must be 0 for the
+                              other kinds (SNN_ERR_UNSUPPORTED) */
+    const float *g;        /* FULL / BCAST: dL/dz of this layer's output
+                              spikes, fp32; ignored for FOLD */
+    const void *dcur_up;   /* FOLD: dL/dI of the layer above, [T,B,n_up] of
+                              dcur_up_dtype (its snn_neuron_bwd output) */
+    const void *w_up;      /* FOLD: weights of the layer above, [n_up, n_out]
+                              of w_up_dtype */
+    int32_t dcur_up_dtype; /* FOLD: SNN_F32 | SNN_BF16 | SNN_F16 */
+    int32_t w_up_dtype;    /* FOLD: SNN_F32 | SNN_F16 */
 } snn_grad_in;
 
 int snn_abi_version(void);

@@ -28,10 +28,10 @@ F32, F16, BF16, U8 = 0, 1, 2, 3
 LEAKY, SYNAPTIC, RLEAKY = 0, 1, 2
 SYN_DENSE, SYN_CONV5_POOL2, SYN_NONE = 0, 1, 2
 RESET_DETACHED, RESET_SURROGATE = 0, 1
-GRAD_FULL, GRAD_BCAST = 0, 1
+GRAD_FULL, GRAD_BCAST, GRAD_FOLD = 0, 1, 2
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 3
+ABI_VERSION = 4
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
           4: "SNN_ERR_ALIGN", 5: "SNN_ERR_UNSUPPORTED", 6: "SNN_ERR_WORKSPACE",
@@ -62,8 +62,9 @@ class LayerDesc(ctypes.Structure):
 
 
 class GradIn(ctypes.Structure):
-    _fields_ = [("kind", ctypes.c_int32), ("reserved", ctypes.c_int32),
-                ("g", ctypes.c_void_p)]
+    _fields_ = [("kind", ctypes.c_int32), ("n_up", ctypes.c_int32),
+                ("g", ctypes.c_void_p), ("dcur_up", ctypes.c_void_p), ("w_up", ctypes.c_void_p),
+                ("dcur_up_dtype", ctypes.c_int32), ("w_up_dtype", ctypes.c_int32)]
 
 
 class AdamwTensor(ctypes.Structure):
@@ -154,6 +155,22 @@ def _check(fn, st):
         raise SNNError(fn, st)
 
 
+def _dtype_code(t):
+    import torch
+    return {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}[t.dtype]
+
+
+def _grad_in(kind, g):
+    """The upstream gradient argument: g a tensor for GRAD_FULL / GRAD_BCAST,
+    or (dcur_up, w_up) for GRAD_FOLD (dL/dI [T,B,n_up] and the weights
+    [n_up, n_out] of the dense layer above)."""
+    if kind == GRAD_FOLD:
+        dup, wup = g
+        return GradIn(kind, int(wup.shape[0]), None, _p(dup), _p(wup), _dtype_code(dup),
+                      _dtype_code(wup))
+    return GradIn(kind, 0, _p(g), None, None, 0, 0)
+
+
 def snn_layer_saved_bytes(desc: LayerDesc) -> int:
     return int(lib().snn_layer_saved_bytes(ctypes.byref(desc)))
 
@@ -174,7 +191,7 @@ def snn_layer_fwd(desc, x, w, bias, v, spk_out, saved, counts, ws, stream=None):
 
 def snn_layer_bwd(desc, grad_kind, g, x, w, v, saved, grad_w, grad_b, grad_v, grad_x, ws,
                   stream=None):
-    gi = GradIn(grad_kind, 0, _p(g))
+    gi = _grad_in(grad_kind, g)
     _check("snn_layer_bwd", lib().snn_layer_bwd(
         ctypes.byref(desc), ctypes.byref(gi), _p(x), _p(w), _p(v), _p(saved), _p(grad_w),
         _p(grad_b), _p(grad_v), _p(grad_x), _p(ws), _nbytes(ws), _stream(stream)))
@@ -199,7 +216,7 @@ def snn_neuron_fwd(desc, cur, v, spk_out, saved_u, counts, stream=None):
 
 
 def snn_neuron_bwd(desc, grad_kind, g, v, saved_u, dcur, grad_b, grad_v, ws, stream=None):
-    gi = GradIn(grad_kind, 0, _p(g))
+    gi = _grad_in(grad_kind, g)
     _check("snn_neuron_bwd", lib().snn_neuron_bwd(
         ctypes.byref(desc), ctypes.byref(gi), _p(v), _p(saved_u), _p(dcur), _p(grad_b),
         _p(grad_v), _p(ws), _nbytes(ws), _stream(stream)))
@@ -261,7 +278,7 @@ class Network:
     All buffers are allocated once here (torch, device memory only); ``step``
     then only enqueues library calls on the current stream."""
 
-    def __init__(self, wl, params, device="cuda", reset_grad=RESET_DETACHED, flags=0):
+    def __init__(self, wl, params, device="cuda", reset_grad=RESET_DETACHED, flags=0, fold=True):
         import torch
         self.torch = torch
         self.wl = wl
@@ -307,6 +324,22 @@ class Network:
                             for d in self.descs[1:]]
         if self.descs[0].synapse == SYN_NONE:
             self.gx[0] = torch.empty((T, B, self.descs[0].n_in), dtype=torch.float32, device=device)
+        # A dense layer with at most 16 outputs (the readout) above a layer of
+        # at least 64 neurons: its input gradient dx = dI W is folded into the
+        # reverse scan of the layer below (SNN_GRAD_FOLD), which then reads the
+        # readout's dL/dI (kept in dup) instead of a [T,B,n] gradient.
+        n = len(self.descs)
+        self.fold = [fold and li + 1 < n and self.descs[li + 1].synapse == SYN_DENSE
+                     and self.descs[li + 1].n_out <= 16 and self.descs[li].n_out >= 64
+                     for li in range(n)]
+        gdt = {F32: torch.float32, BF16: torch.bfloat16, F16: torch.float16}
+        self.dup = [None] * n
+        for li in range(n - 1):
+            if self.fold[li]:
+                up = self.descs[li + 1]
+                self.dup[li + 1] = torch.empty((T, B, up.n_out), dtype=gdt[up.grad_dtype],
+                                               device=device)
+                self.gx[li + 1] = None
         # K classes, P output neurons per class (a population code when P > 1)
         self.P = getattr(wl, "pop", 1)
         n_last = self.descs[-1].n_out
@@ -333,15 +366,29 @@ class Network:
         snn_loss(self.loss_kind, self.wl.B, self.K, self.P, self.counts, labels, targets,
                  self.loss, self.gcounts, self.ws, stream)
 
+    def _grad_below(self, li):
+        """The upstream gradient argument of layer li - 1."""
+        if self.fold[li - 1]:
+            return GRAD_FOLD, (self.dup[li], self.W[li])
+        return GRAD_FULL, self.gx[li]
+
     def backward(self, x, stream=None):
         n = len(self.descs)
         kind, g = GRAD_BCAST, self.gcounts
         for li in range(n - 1, -1, -1):
             d = self.descs[li]
             xin = x if li == 0 else self.spk[li - 1]
-            snn_layer_bwd(d, kind, g, xin, self.W[li], self.v[li], self.saved[li], self.gW[li],
-                          self.gb[li], self.gv[li], self.gx[li], self.ws, stream)
-            kind, g = GRAD_FULL, self.gx[li]
+            if self.dup[li] is not None:
+                # dL/dI kept for the layer below; no dx of its own
+                snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], self.dup[li], self.gb[li],
+                               self.gv[li], self.ws, stream)
+                snn_synapse_bwd(d, self.dup[li], self.pool_arg(li), xin, self.W[li], self.gW[li],
+                                None, self.ws, stream)
+            else:
+                snn_layer_bwd(d, kind, g, xin, self.W[li], self.v[li], self.saved[li],
+                              self.gW[li], self.gb[li], self.gv[li], self.gx[li], self.ws, stream)
+            if li > 0:
+                kind, g = self._grad_below(li)
 
     def step(self, x, labels=None, targets=None, stream=None):
         self.forward(x, stream)
@@ -433,14 +480,17 @@ class Network:
                 hook("neuron_bwd_end", li)
                 continue
             dcur_bytes = d.T * d.B * d.n_out * (2 if d.grad_dtype in (F16, BF16) else 4)
-            dcur = self.ws[:dcur_bytes]
-            if d.grad_dtype == BF16:
-                dcur = dcur.view(torch.bfloat16)
-            elif d.grad_dtype == F16:
-                dcur = dcur.view(torch.float16)
+            if self.dup[li] is not None:
+                dcur, rest = self.dup[li], self.ws
             else:
-                dcur = dcur.view(torch.float32)
-            rest = self.ws[(dcur_bytes + 255) // 256 * 256:]
+                dcur = self.ws[:dcur_bytes]
+                if d.grad_dtype == BF16:
+                    dcur = dcur.view(torch.bfloat16)
+                elif d.grad_dtype == F16:
+                    dcur = dcur.view(torch.float16)
+                else:
+                    dcur = dcur.view(torch.float32)
+                rest = self.ws[(dcur_bytes + 255) // 256 * 256:]
             hook("neuron_bwd", li)
             snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], dcur, self.gb[li],
                            self.gv[li], rest, stream)
@@ -449,7 +499,8 @@ class Network:
             snn_synapse_bwd(d, dcur, self.pool_arg(li), xin, self.W[li], self.gW[li], self.gx[li],
                             rest, stream)
             hook("synapse_bwd_end", li)
-            kind, g = GRAD_FULL, self.gx[li]
+            if li > 0:
+                kind, g = self._grad_below(li)
         if update:
             hook("update", -1)
             self.update(stream)

@@ -190,12 +190,36 @@ size_t bwd_ws(const snn_layer_desc *d) { return dcur_bytes(d) + neuron_ws(d) + b
 snn_status hip_status(hipError_t e) { return e == hipSuccess ? SNN_OK : SNN_ERR_HIP; }
 
 snn_status check_grad(const snn_layer_desc *d, const snn_grad_in *g) {
-    if (!g || !g->g) return SNN_ERR_NULL;
-    if (g->kind != SNN_GRAD_FULL && g->kind != SNN_GRAD_BCAST) return SNN_ERR_UNSUPPORTED;
-    if (g->reserved != 0) return SNN_ERR_UNSUPPORTED;
-    if (!aligned16(g->g)) return SNN_ERR_ALIGN;
-    (void)d;
+    if (!g) return SNN_ERR_NULL;
+    if (g->kind == SNN_GRAD_FULL || g->kind == SNN_GRAD_BCAST) {
+        if (!g->g) return SNN_ERR_NULL;
+        if (g->n_up != 0) return SNN_ERR_UNSUPPORTED;
+        if (!aligned16(g->g)) return SNN_ERR_ALIGN;
+        return SNN_OK;
+    }
+    if (g->kind != SNN_GRAD_FOLD) return SNN_ERR_UNSUPPORTED;
+    if (!g->dcur_up || !g->w_up) return SNN_ERR_NULL;
+    if (g->n_up < 1 || g->n_up > 16) return SNN_ERR_SHAPE;
+    if (g->dcur_up_dtype != SNN_F32 && g->dcur_up_dtype != SNN_BF16 && g->dcur_up_dtype != SNN_F16)
+        return SNN_ERR_DTYPE;
+    if (g->w_up_dtype != SNN_F32 && g->w_up_dtype != SNN_F16) return SNN_ERR_DTYPE;
+    if (!aligned16(g->dcur_up) || !aligned16(g->w_up)) return SNN_ERR_ALIGN;
+    if (!neuron_fold_supported(d->n_out)) return SNN_ERR_UNSUPPORTED;
     return SNN_OK;
+}
+
+BwdGrad bwd_grad(const snn_grad_in *g) {
+    BwdGrad b{};
+    b.mode = g->kind;
+    b.g = g->kind == SNN_GRAD_FOLD ? nullptr : g->g;
+    if (g->kind == SNN_GRAD_FOLD) {
+        b.dup = g->dcur_up;
+        b.wup = g->w_up;
+        b.nup = g->n_up;
+        b.dt_up = g->dcur_up_dtype;
+        b.dt_w = g->w_up_dtype;
+    }
+    return b;
 }
 
 }  // namespace
@@ -313,9 +337,8 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
     float *dvcol = grad_v ? reinterpret_cast<float *>(wsb + (grad_b ? colsum_bytes(d) : 0))
                           : nullptr;
     hipError_t e = launch_neuron_bwd(d->neuron, d->reset_grad, d->T, C, d->n_out, d->alpha,
-                                     d->beta, d->threshold, d->slope, v, saved_u, grad->g,
-                                     grad->kind == SNN_GRAD_BCAST, dcur, d->grad_dtype, colsum,
-                                     dvcol, stream);
+                                     d->beta, d->threshold, d->slope, v, saved_u, bwd_grad(grad),
+                                     d->B, dcur, d->grad_dtype, colsum, dvcol, stream);
     if (e != hipSuccess) return SNN_ERR_HIP;
     if (grad_b) {
         int F = d->n_out, P = 1;

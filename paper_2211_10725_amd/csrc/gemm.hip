@@ -343,7 +343,7 @@ size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype, bool 
     probe.allow_split = allow_split;
     probe.lda = a_kc ? K : M;  // densely packed operands (the callers' layouts)
     probe.ldb = b_kc ? K : N;
-    if (short_k_applies(probe)) return 0;
+    if (short_k_applies(probe) || narrow_fwd_applies(probe)) return 0;
     if (few_rows_applies(probe)) return few_rows_workspace_bytes(probe);
     if (gemm_async_applies(probe)) return gemm_async_workspace_bytes(probe);
     if (allow_split && gemm16_applies(probe)) return gemm16_workspace_bytes(probe);
@@ -359,6 +359,7 @@ hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t
         return hipErrorInvalidValue;
     }
     if (short_k_applies(g)) return launch_short_k(g, s);
+    if (narrow_fwd_applies(g)) return launch_narrow_fwd(g, s);
     if (few_rows_applies(g)) return launch_few_rows(g, ws, ws_bytes, s);
     if (gemm_async_applies(g)) return launch_gemm_async(g, ws, ws_bytes, s);
     if (g.allow_split && gemm16_applies(g)) return launch_gemm16(g, ws, ws_bytes, s);

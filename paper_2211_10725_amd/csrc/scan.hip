@@ -22,6 +22,8 @@ constexpr int kThreads = 256;
 // column and 16 steps, which gives 4x the waves and halves the number of
 // exposed memory round trips of the serial scan.
 constexpr int kWideColumns = 4 * 64 * 2048;  // 2048 waves of 4-column lanes
+constexpr int kFoldMax = 16;   // most outputs of a dense layer whose input gradient is folded
+constexpr int kFoldRows = 5;   // batch rows one workgroup's columns can span when folding
 
 template <int VEC>
 struct Vec;
@@ -162,58 +164,160 @@ __device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC]
     }
 }
 
+// Sources of the upstream gradient g_t = dL/dz_t of the reverse scan.
+constexpr int GM_FULL = 0;   // g [T, C]
+constexpr int GM_BCAST = 1;  // g [C], the same for every t
+constexpr int GM_FOLD = 2;   // g_t[b, n] = sum_j dI_up[t, b, j] W_up[j, n]: the input
+                             // gradient of a dense layer above with at most
+                             // kFoldMax outputs, computed here instead of read
+constexpr int GM_FOLD12 = 3; // the same for at most 12 outputs (10 classes)
+
+// The layer above, for GM_FOLD.  A workgroup's 256 VEC consecutive columns
+// span at most kFoldRows batch rows (the launcher only folds layers with
+// n >= 64, and n >= 256 for VEC = 4); the dI_up rows of those batch rows for
+// one block of kDepth steps are staged in LDS (double-buffered, one barrier
+// per block), the next block's loaded into registers while this one runs.
+struct FoldIn {
+    const void *dup;  // [T, B, nup] of dt_up
+    const void *wup;  // [nup, N] of dt_w
+    int nup, dt_up, dt_w, B;
+};
+
+__device__ inline float load_as_f32(const void *p, int64_t i, int dt) {
+    if (dt == SNN_F32) return reinterpret_cast<const float *>(p)[i];
+    const uint16_t h = reinterpret_cast<const uint16_t *>(p)[i];
+    if (dt == SNN_BF16) return __uint_as_float((uint32_t)h << 16);
+    return (float)__builtin_bit_cast(_Float16, h);
+}
+
+template <int kDepth, int KF>
+struct FoldStage {
+    static constexpr int kElems = kDepth * kFoldRows * KF;
+    static constexpr int kPer = (kElems + 255) / 256;  // per thread (256-thread blocks)
+    float v[kPer];
+
+    // the dI_up values of steps t0, t0 - 1, ..., t0 - kDepth + 1 and batch
+    // rows b_lo .. b_lo + kFoldRows - 1 (zeros outside)
+    __device__ inline void load(const FoldIn &f, int t0, int64_t b_lo) {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            const int e = threadIdx.x + i * 256;
+            const int jt = e / (kFoldRows * KF), bb = (e / KF) % kFoldRows, j = e % KF;
+            const int t = t0 - jt;
+            const int64_t b = b_lo + bb;
+            v[i] = (e < kElems && t >= 0 && b < f.B && j < f.nup)
+                       ? load_as_f32(f.dup, ((int64_t)t * f.B + b) * f.nup + j, f.dt_up)
+                       : 0.f;
+        }
+    }
+    __device__ inline void store(float *rows) const {
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) {
+            const int e = threadIdx.x + i * 256;
+            if (e < kElems) rows[e] = v[i];
+        }
+    }
+};
+
 // Reverse-time scan.  lam carries dL/du_{t+1} (and lami dL/di_{t+1}).
 // For the recurrent neuron the spike z_t reaches u_{t+1} through
 // (v - r thr), so the carry is beta + (v - r thr) s_t, and the recurrent
 // weight's gradient collects lam_{t+1} z_t per column (dvcol, fp32).
-template <int NEURON, int VEC, bool BCAST, bool RESET_SURR, int GT, int kDepth>
+template <int NEURON, int VEC, int GM, bool RESET_SURR, int GT, int kDepth>
 __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
     int T, int64_t C, int64_t N, float alpha, float beta, float thr, float slope,
     const float *__restrict__ vrec, const float *__restrict__ u, const float *__restrict__ g,
-    void *__restrict__ dcur, float *__restrict__ colsum, float *__restrict__ dvcol) {
+    FoldIn fold, void *__restrict__ dcur, float *__restrict__ colsum, float *__restrict__ dvcol) {
+    constexpr bool BCAST = GM == GM_BCAST, FOLD = GM == GM_FOLD || GM == GM_FOLD12;
+    constexpr int KF = GM == GM_FOLD12 ? 12 : kFoldMax;  // dI_up values per row (padded)
     const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
-    if (col >= C) return;
+    // the fold's lanes past the last column still take part in the staging
+    const bool active = col < C;
+    if (!FOLD && !active) return;
     float lam[VEC], lami[VEC], acc[VEC], gb[VEC], vr[VEC], dv[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
         lam[v] = lami[v] = acc[v] = gb[v] = dv[v] = 0.f;
         if constexpr (NEURON == SNN_RLEAKY)
-            vr[v] = RESET_SURR ? vrec[(col + v) % N] - thr : vrec[(col + v) % N];
+            vr[v] = active ? (RESET_SURR ? vrec[(col + v) % N] - thr : vrec[(col + v) % N]) : 0.f;
         else
             vr[v] = 0.f;
     }
     if constexpr (BCAST) Vec<VEC>::load(g + col, gb);
 
+    // fold: the lane's columns of W_up, its batch row within the staged rows
+    __shared__ __attribute__((aligned(16))) float frows[FOLD ? 2 : 1][FOLD ? FoldStage<kDepth, KF>::kElems : 1];
+    float wcol[FOLD ? VEC : 1][FOLD ? KF : 1];
+    int fbb = 0;
+    int64_t b_lo = 0;
+    FoldStage<kDepth, KF> fst;
+    if constexpr (FOLD) {
+        b_lo = ((int64_t)blockIdx.x * kThreads * VEC) / N;
+        fbb = active ? (int)(col / N - b_lo) : 0;
+#pragma unroll
+        for (int v = 0; v < VEC; ++v)
+#pragma unroll
+            for (int j = 0; j < KF; ++j)
+                wcol[v][j] = (active && j < fold.nup)
+                                 ? load_as_f32(fold.wup, (int64_t)j * N + (col + v) % N, fold.dt_w)
+                                 : 0.f;
+        fst.load(fold, T - 1, b_lo);
+        fst.store(frows[0]);
+        if (T - 1 - kDepth >= 0) fst.load(fold, T - 1 - kDepth, b_lo);
+        __syncthreads();
+    }
+
     float uu[kDepth][VEC], nu[kDepth][VEC];
-    float gg[BCAST ? 1 : kDepth][VEC], ng[BCAST ? 1 : kDepth][VEC];
+    float gg[GM == GM_FULL ? kDepth : 1][VEC], ng[GM == GM_FULL ? kDepth : 1][VEC];
 #pragma unroll
     for (int j = 0; j < kDepth; ++j) {
         const int t = T - 1 - j;
-        if (t >= 0) {
+        if (t >= 0 && active) {
             Vec<VEC>::load(u + (int64_t)t * C + col, uu[j]);
-            if constexpr (!BCAST) Vec<VEC>::load(g + (int64_t)t * C + col, gg[j]);
+            if constexpr (GM == GM_FULL) Vec<VEC>::load(g + (int64_t)t * C + col, gg[j]);
         }
     }
-    for (int t0 = T - 1; t0 >= 0; t0 -= kDepth) {
+    int blk = 0;
+    for (int t0 = T - 1; t0 >= 0; t0 -= kDepth, ++blk) {
 #pragma unroll
         for (int j = 0; j < kDepth; ++j) {
             const int t = t0 - kDepth - j;
-            if (t >= 0) {
+            if (t >= 0 && active) {
                 Vec<VEC>::load(u + (int64_t)t * C + col, nu[j]);
-                if constexpr (!BCAST) Vec<VEC>::load(g + (int64_t)t * C + col, ng[j]);
+                if constexpr (GM == GM_FULL) Vec<VEC>::load(g + (int64_t)t * C + col, ng[j]);
             }
         }
+        const float *fr = FOLD ? frows[blk & 1] : nullptr;
 #pragma unroll
         for (int j = 0; j < kDepth; ++j) {
             const int t = t0 - j;
-            if (t >= 0) {
+            if (t >= 0 && active) {
                 float d[VEC];
+                float grow[FOLD ? KF : 1];
+                if constexpr (FOLD) {
+                    const float4 *r4 = reinterpret_cast<const float4 *>(
+                        fr + (j * kFoldRows + fbb) * KF);
+#pragma unroll
+                    for (int q = 0; q < KF / 4; ++q) {
+                        const float4 x = r4[q];
+                        grow[4 * q] = x.x; grow[4 * q + 1] = x.y;
+                        grow[4 * q + 2] = x.z; grow[4 * q + 3] = x.w;
+                    }
+                }
 #pragma unroll
                 for (int v = 0; v < VEC; ++v) {
                     const float e = 1.f + slope * __builtin_fabsf(uu[j][v] - thr);
                     const float s = __builtin_amdgcn_rcpf(e * e);  // eq. (9) with slope
                     float gt;
-                    if constexpr (BCAST) gt = gb[v]; else gt = gg[j][v];
+                    if constexpr (BCAST) {
+                        gt = gb[v];
+                    } else if constexpr (FOLD) {
+                        gt = 0.f;  // j ascending: the order of the short contraction
+#pragma unroll
+                        for (int q = 0; q < KF; ++q) gt = __builtin_fmaf(grow[q], wcol[v][q], gt);
+                    } else {
+                        gt = gg[j][v];
+                    }
                     float carry = beta;
                     if constexpr (NEURON == SNN_RLEAKY) {
                         if (uu[j][v] > thr) dv[v] += lam[v];  // lam_{t+1} z_t
@@ -233,14 +337,24 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
                 store_grad<GT, VEC>(dcur, (int64_t)t * C + col, d);
             }
         }
+        if constexpr (FOLD) {
+            // stage the next block (its buffer was last read before the
+            // previous barrier), then load the one after it
+            if (t0 - kDepth >= 0) {
+                fst.store(frows[(blk + 1) & 1]);
+                if (t0 - 2 * kDepth >= 0) fst.load(fold, t0 - 2 * kDepth, b_lo);
+            }
+            __syncthreads();
+        }
 #pragma unroll
         for (int j = 0; j < kDepth; ++j)
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
                 uu[j][v] = nu[j][v];
-                if constexpr (!BCAST) gg[j][v] = ng[j][v];
+                if constexpr (GM == GM_FULL) gg[j][v] = ng[j][v];
             }
     }
+    if (!active) return;
     if (colsum) Vec<VEC>::store(colsum + col, acc);
     if constexpr (NEURON == SNN_RLEAKY)
         if (dvcol) Vec<VEC>::store(dvcol + col, dv);
@@ -322,36 +436,40 @@ void fwd_dispatch(int out_dtype, const ScanArgs &a, const float *cur, void *spk,
 
 struct BwdBuffers {
     const float *u, *g;
+    FoldIn fold;
     void *dcur;
     float *colsum, *dvcol;
 };
 
-template <int NEURON, int VEC, bool BCAST, bool RS, int GT>
+template <int NEURON, int VEC, int GM, bool RS, int GT>
 void bwd_launch(const ScanArgs &a, const BwdBuffers &b, hipStream_t s) {
     const int64_t lanes = (a.C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_bwd_kernel<NEURON, VEC, BCAST, RS, GT, VEC == 4 ? 6 : 16><<<grid, kThreads, 0, s>>>(
-        a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.u, b.g, b.dcur, b.colsum,
-        b.dvcol);
+    neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, VEC == 4 ? 6 : 16><<<grid, kThreads, 0, s>>>(
+        a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.u, b.g, b.fold, b.dcur,
+        b.colsum, b.dvcol);
 }
 
-template <int NEURON, int VEC, bool BCAST, bool RS>
+template <int NEURON, int VEC, int GM, bool RS>
 void bwd_dispatch_gt(int gt, const ScanArgs &a, const BwdBuffers &b, hipStream_t s) {
-    if (gt == SNN_F32) bwd_launch<NEURON, VEC, BCAST, RS, SNN_F32>(a, b, s);
-    else if (gt == SNN_F16) bwd_launch<NEURON, VEC, BCAST, RS, SNN_F16>(a, b, s);
-    else bwd_launch<NEURON, VEC, BCAST, RS, SNN_BF16>(a, b, s);
+    if (gt == SNN_F32) bwd_launch<NEURON, VEC, GM, RS, SNN_F32>(a, b, s);
+    else if (gt == SNN_F16) bwd_launch<NEURON, VEC, GM, RS, SNN_F16>(a, b, s);
+    else bwd_launch<NEURON, VEC, GM, RS, SNN_BF16>(a, b, s);
+}
+
+template <int NEURON, int VEC, int GM>
+void bwd_dispatch_rs(int rs, int gt, const ScanArgs &a, const BwdBuffers &b, hipStream_t s) {
+    if (rs) bwd_dispatch_gt<NEURON, VEC, GM, true>(gt, a, b, s);
+    else bwd_dispatch_gt<NEURON, VEC, GM, false>(gt, a, b, s);
 }
 
 template <int NEURON, int VEC>
-void bwd_dispatch(int rs, int bcast, int gt, const ScanArgs &a, const BwdBuffers &b,
+void bwd_dispatch(int rs, int gm, int gt, const ScanArgs &a, const BwdBuffers &b,
                   hipStream_t s) {
-    if (bcast) {
-        if (rs) bwd_dispatch_gt<NEURON, VEC, true, true>(gt, a, b, s);
-        else bwd_dispatch_gt<NEURON, VEC, true, false>(gt, a, b, s);
-    } else {
-        if (rs) bwd_dispatch_gt<NEURON, VEC, false, true>(gt, a, b, s);
-        else bwd_dispatch_gt<NEURON, VEC, false, false>(gt, a, b, s);
-    }
+    if (gm == GM_BCAST) bwd_dispatch_rs<NEURON, VEC, GM_BCAST>(rs, gt, a, b, s);
+    else if (gm == GM_FOLD12) bwd_dispatch_rs<NEURON, VEC, GM_FOLD12>(rs, gt, a, b, s);
+    else if (gm == GM_FOLD) bwd_dispatch_rs<NEURON, VEC, GM_FOLD>(rs, gt, a, b, s);
+    else bwd_dispatch_rs<NEURON, VEC, GM_FULL>(rs, gt, a, b, s);
 }
 
 }  // namespace
@@ -378,27 +496,37 @@ hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, int64_t N, float alph
     return hipGetLastError();
 }
 
+bool neuron_fold_supported(int64_t N) { return N >= 64; }
+
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
-                             const float *u, const float *g, int g_bcast, void *dcur,
+                             const float *u, const BwdGrad &grad, int B, void *dcur,
                              int grad_dtype, float *colsum, float *dvcol, hipStream_t s) {
     if (T <= 0 || C <= 0) return hipSuccess;
-    const bool v4 = (C % 4) == 0 && C >= kWideColumns;
+    int gm = grad.mode == SNN_GRAD_FOLD ? GM_FOLD
+             : grad.mode == SNN_GRAD_BCAST ? GM_BCAST : GM_FULL;
+    if (gm == GM_FOLD && (!neuron_fold_supported(N) || grad.nup < 1 || grad.nup > kFoldMax))
+        return hipErrorInvalidValue;
+    if (gm == GM_FOLD && grad.nup <= 12) gm = GM_FOLD12;
+    bool v4 = (C % 4) == 0 && C >= kWideColumns;
+    // a lane's four columns in one batch row, and at most kFoldRows rows per workgroup
+    if ((gm == GM_FOLD || gm == GM_FOLD12) && v4 && (N % 4 != 0 || N < 256)) v4 = false;
     const ScanArgs a{T, C, N, alpha, beta, thr, slope, vrec};
-    const BwdBuffers b{u, g, dcur, colsum, dvcol};
+    const FoldIn fold{grad.dup, grad.wup, grad.nup, grad.dt_up, grad.dt_w, B};
+    const BwdBuffers b{u, grad.g, fold, dcur, colsum, dvcol};
     const int rs = reset_surrogate, gt = grad_dtype;
     switch (neuron) {
         case SNN_SYNAPTIC:
-            if (v4) bwd_dispatch<SNN_SYNAPTIC, 4>(rs, g_bcast, gt, a, b, s);
-            else bwd_dispatch<SNN_SYNAPTIC, 1>(rs, g_bcast, gt, a, b, s);
+            if (v4) bwd_dispatch<SNN_SYNAPTIC, 4>(rs, gm, gt, a, b, s);
+            else bwd_dispatch<SNN_SYNAPTIC, 1>(rs, gm, gt, a, b, s);
             break;
         case SNN_RLEAKY:
-            if (v4) bwd_dispatch<SNN_RLEAKY, 4>(rs, g_bcast, gt, a, b, s);
-            else bwd_dispatch<SNN_RLEAKY, 1>(rs, g_bcast, gt, a, b, s);
+            if (v4) bwd_dispatch<SNN_RLEAKY, 4>(rs, gm, gt, a, b, s);
+            else bwd_dispatch<SNN_RLEAKY, 1>(rs, gm, gt, a, b, s);
             break;
         default:
-            if (v4) bwd_dispatch<SNN_LEAKY, 4>(rs, g_bcast, gt, a, b, s);
-            else bwd_dispatch<SNN_LEAKY, 1>(rs, g_bcast, gt, a, b, s);
+            if (v4) bwd_dispatch<SNN_LEAKY, 4>(rs, gm, gt, a, b, s);
+            else bwd_dispatch<SNN_LEAKY, 1>(rs, gm, gt, a, b, s);
     }
     return hipGetLastError();
 }

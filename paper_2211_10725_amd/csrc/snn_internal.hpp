@@ -51,12 +51,24 @@ hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, int64_t N, float alph
                              float thr, const float *vrec, const float *cur, void *spk,
                              int out_dtype, float *u_out, float *counts, hipStream_t s);
 
+// Upstream gradient of the reverse scan: g [T, C] (SNN_GRAD_FULL), g [C] for
+// every t (SNN_GRAD_BCAST), or, for SNN_GRAD_FOLD, computed in the scan as
+// g[t, b, n] = sum_{j < nup} dup[t, b, j] wup[j, n] (nup <= 16; layers with
+// N >= 64 only, see neuron_fold_supported).
+struct BwdGrad {
+    int mode;
+    const float *g;
+    const void *dup, *wup;
+    int nup, dt_up, dt_w;
+};
+bool neuron_fold_supported(int64_t N);
+
 // Backward: writes dcur [T, C] (grad_dtype), colsum [C] = sum_t dcur (fp32,
 // may be NULL) and, for SNN_RLEAKY, dvcol [C] = sum_t lam_{t+1} z_t (fp32,
-// may be NULL).
+// may be NULL).  C = B * N.
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
-                             const float *u, const float *g, int g_bcast, void *dcur,
+                             const float *u, const BwdGrad &grad, int B, void *dcur,
                              int grad_dtype, float *colsum, float *dvcol, hipStream_t s);
 
 // p[0..n) = 0 with a kernel (safe inside captured graphs)
@@ -105,6 +117,12 @@ hipError_t launch_short_k(const GemmArgs &g, hipStream_t s);
 bool few_rows_applies(const GemmArgs &g);
 size_t few_rows_workspace_bytes(const GemmArgs &g);
 hipError_t launch_few_rows(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
+
+// forward of a layer with at most 16 outputs and a long contraction: A
+// spikes (bytes) or fp16, W fp32 or fp16, both K-contiguous; 16-bit MFMA with
+// exact products (needs allow_split)
+bool narrow_fwd_applies(const GemmArgs &g);
+hipError_t launch_narrow_fwd(const GemmArgs &g, hipStream_t s);
 
 // ---- large single-part contractions, asynchronous LDS pipeline (gemm_async.hip)
 bool gemm_async_applies(const GemmArgs &g);

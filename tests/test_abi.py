@@ -80,6 +80,35 @@ def test_validation_errors_before_launch():
     assert st == 1
 
 
+def test_fold_validation():
+    """SNN_GRAD_FOLD arguments are checked on the host.  Every call here stops
+    before a launch: a valid fold reaches the misaligned dcur (SNN_ERR_ALIGN)."""
+    L = snn.lib()
+    d = _dense(T=4, B=3, n_in=20, n_out=100)
+
+    def bwd(gi, desc=d):
+        return L.snn_neuron_bwd(ctypes.byref(desc), ctypes.byref(gi), None, 64, 80 + 1, None,
+                                None, None, 0, None)
+
+    F = snn.GRAD_FOLD
+    assert bwd(snn.GradIn(F, 10, None, 96, 112, snn.F32, snn.F32)) == 4     # valid up to dcur
+    assert bwd(snn.GradIn(F, 16, None, 96, 112, snn.BF16, snn.F16)) == 4
+    assert bwd(snn.GradIn(F, 0, None, 96, 112, snn.F32, snn.F32)) == 2      # n_up < 1
+    assert bwd(snn.GradIn(F, 17, None, 96, 112, snn.F32, snn.F32)) == 2     # n_up > 16
+    assert bwd(snn.GradIn(F, 10, None, None, 112, snn.F32, snn.F32)) == 1   # no dL/dI above
+    assert bwd(snn.GradIn(F, 10, None, 96, None, snn.F32, snn.F32)) == 1    # no weights above
+    assert bwd(snn.GradIn(F, 10, None, 96, 112, snn.U8, snn.F32)) == 3
+    assert bwd(snn.GradIn(F, 10, None, 96, 112, snn.F32, snn.BF16)) == 3
+    assert bwd(snn.GradIn(F, 10, None, 96 + 8, 112, snn.F32, snn.F32)) == 4
+    # layers narrower than 64 neurons are not folded into
+    narrow = _dense(T=4, B=3, n_in=20, n_out=63)
+    assert bwd(snn.GradIn(F, 10, None, 96, 112, snn.F32, snn.F32), narrow) == 5
+    # the other kinds keep n_up = 0; unknown kinds are rejected
+    assert bwd(snn.GradIn(snn.GRAD_FULL, 3, 16)) == 5
+    assert bwd(snn.GradIn(snn.GRAD_FULL, 0, 16)) == 4
+    assert bwd(snn.GradIn(3, 0, 16)) == 5
+
+
 def test_loss_validation():
     L = snn.lib()
     assert L.snn_loss(0, 0, 10, 1, 16, 32, None, 48, 64, None, 0, None) == 2   # B = 0

@@ -126,6 +126,70 @@ def test_scan_bwd_half_gradient_operand(gdt, tdt):
     assert_close(_np(dI.float()), ref, 2e-2, what="half dL/dI")
 
 
+# The input gradient of a readout (dense, <= 16 outputs) folded into the
+# reverse scan of the layer below (SNN_GRAD_FOLD): the scan computes
+# g[t,b,n] = sum_j dI_up[t,b,j] W_up[j,n] itself.  N = 64: a workgroup's 256
+# columns span 5 batch rows; ragged column counts; n_up 1 and 16; N = 4096
+# (over 512k columns) the 4-column lanes; N = 1018 over 512k columns but not
+# a multiple of 4, the 1-column lanes.
+FOLD_SHAPES = [(7, 5, 64, 10), (9, 3, 1000, 10), (5, 4, 100, 1), (6, 2, 130, 16),
+               (40, 3, 257, 7), (3, 128, 4096, 10), (2, 516, 1018, 10)]
+
+
+@pytest.mark.parametrize("neuron,alpha,beta", [("leaky", 0.0, 0.95), ("synaptic", 0.9, 0.8),
+                                               ("rleaky", 0.0, 0.9)])
+@pytest.mark.parametrize("T,B,N,nup", FOLD_SHAPES)
+def test_scan_bwd_fold(neuron, alpha, beta, T, B, N, nup):
+    rng = np.random.default_rng(T * 31 + N + nup)
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    v = rng.uniform(-1.0, 1.5, N).astype(np.float32) if neuron == "rleaky" else None
+    d, _ = _none_desc(T, B, N, neuron, beta, alpha)
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    v_t = None if v is None else _t(v)
+    snn.snn_neuron_fwd(d, _t(I), v_t, spk, saved, None)
+    _, u, _ = oracle.scan_fwd(I, neuron, beta, 1.0, alpha, v=v)
+    np.testing.assert_array_equal(_np(saved), u)
+    dup = rng.normal(0, 0.1, (T, B, nup)).astype(np.float32)
+    wup = rng.uniform(-1, 1, (nup, N)).astype(np.float32)
+    g = dup.astype(np.float64) @ wup.astype(np.float64)   # the readout's dx
+    dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    gv = None if v is None else torch.empty(N, dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    snn.snn_neuron_bwd(d, snn.GRAD_FOLD, (_t(dup), _t(wup)), v_t, saved, dI, None, gv, ws)
+    if neuron == "rleaky":
+        ref, dv = oracle.scan_bwd_rleaky(u, g, beta, 1.0, 25.0, v)
+        assert_close(_np(gv), dv, 1e-3, what="dL/dv")
+    else:
+        ref = oracle.scan_bwd(u, g, neuron, beta, 1.0, 25.0, alpha)
+    assert_close(_np(dI), ref, 1e-3, what="dL/dI (folded)")
+
+
+def test_scan_bwd_fold_half_operands():
+    """bf16 dL/dI and fp16 weights above (the fp16 network's readout), a bf16
+    gradient written below; products of the given values are exact."""
+    T, B, N, nup = 12, 6, 320, 10
+    rng = np.random.default_rng(21)
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    spec = dict(kind="dense", n_in=8, n_out=N, neuron="leaky", beta=0.9)
+    d = snn.layer_desc(spec, T, B, grad_dtype=snn.BF16)
+    dn, _ = _none_desc(T, B, N, "leaky", 0.9)
+    saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    snn.snn_neuron_fwd(dn, _t(I), None, spk, saved, None)
+    _, u, _ = oracle.scan_fwd(I, "leaky", 0.9, 1.0)
+    dup = torch.as_tensor(rng.normal(0, 0.01, (T, B, nup)).astype(np.float32)).to(torch.bfloat16)
+    wup = torch.as_tensor(rng.uniform(-1, 1, (nup, N)).astype(np.float32)).to(torch.float16)
+    g = dup.float().numpy().astype(np.float64) @ wup.float().numpy().astype(np.float64)
+    dI = torch.empty((T, B, N), dtype=torch.bfloat16, device=DEV)
+    gb = torch.empty(N, dtype=torch.float32, device=DEV)
+    snn.snn_neuron_bwd(d, snn.GRAD_FOLD, (dup.to(DEV), wup.to(DEV)), None, saved, dI, gb, None,
+                       _ws(snn.snn_layer_workspace_bytes(d)))
+    ref = oracle.scan_bwd(u, g, "leaky", 0.9, 1.0, 25.0)
+    assert_close(_np(dI.float()), ref, 2e-2, what="half dL/dI (folded)")
+    assert_close(_np(gb), ref.sum(axis=(0, 1)), 1e-3, what="db (folded)")
+
+
 # recurrent neuron (eq. 7): one recurrent weight per neuron, column c of the
 # [T, B*N] layout is neuron c % N.  (8, 65538) takes the 4-column lanes with
 # groups that straddle two samples; (9, 65537) the 1-column lanes.
@@ -557,6 +621,40 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
         assert_close(_np(gb), r["db"], tol, what=f"L{li} neuron-stage db")
         if vv is not None:
             assert_close(_np(gv), r["dv"], tol, what=f"L{li} neuron-stage dL/dv")
+        if net.fold[li]:
+            # the readout's dx computed inside this scan, from the oracle's
+            # dL/dI of the readout (rounded to its gradient type) and weights
+            up = net.descs[li + 1]
+            dup = torch.from_numpy(np.ascontiguousarray(bwds[li + 1]["dI"], np.float32)
+                                   .reshape(T, B, -1)).to(_TORCH_GRAD[up.grad_dtype]).to(DEV)
+            fold_g = (dup, net.W[li + 1])
+            dI_r, db_r, dW_r, bW_f = dI_o, r["db"], r["dW"], None
+            if half:
+                # the oracle's chain from the dL/dI the fold reads (bf16)
+                assert spec["kind"] == "dense" and vv is None
+                g_r = (dup.float().cpu().numpy().astype(np.float64).reshape(T * B, -1)
+                       @ np.asarray(inp["params"][li + 1][0], np.float64)).reshape(T, B, -1)
+                dI_r = oracle.scan_bwd(f["u"].reshape(T, B, -1), g_r, spec["neuron"],
+                                       spec["beta"], spec["thr"], wl.slope,
+                                       spec.get("alpha", 0.0), rs)
+                db_r = dI_r.reshape(T * B, -1).sum(axis=0)
+                xin_ = np.asarray(f["x"], np.float64).reshape(T * B, -1)
+                dW_r, _, _ = oracle.dense_bwd(dI_r.reshape(T * B, -1), xin_, inp["params"][li][0],
+                                              want_db=False, want_dx=False)
+                # dL/dI handed to the contraction in bf16
+                bW_f = 2.0 ** -8 * (np.abs(dI_r.reshape(T * B, -1)).T @ np.abs(xin_))
+            dcur_f, gb_f = torch.empty_like(dcur), torch.empty_like(gb)
+            gv_f = None if vv is None else torch.empty_like(vv)
+            snn.snn_neuron_bwd(d, snn.GRAD_FOLD, fold_g, vv, saved, dcur_f, gb_f, gv_f, net.ws)
+            assert_close(_np(dcur_f.float()), dI_r, 2e-2 if half else tol,
+                         what=f"L{li} folded dL/dI")
+            assert_close(_np(gb_f), db_r, tol, what=f"L{li} folded db")
+            if vv is not None:
+                assert_close(_np(gv_f), r["dv"], tol, what=f"L{li} folded dL/dv")
+            gW_f = torch.empty_like(net.gW[li])
+            snn.snn_layer_bwd(d, snn.GRAD_FOLD, fold_g, xs[li], net.W[li], vv, saved, gW_f,
+                              gb_f, gv_f, None, net.ws)
+            assert_close(_np(gW_f), dW_r, tol, what=f"L{li} folded layer dW", abs_bound=bW_f)
         # synapse stage on the oracle's dL/dI, rounded on the host
         W = inp["params"][li][0]
         xin = np.asarray(f["x"], np.float64)
@@ -630,6 +728,15 @@ def test_step_scaled_stagewise(name, T, B, width, reset, path):
     snap2 = [_np(t) for t in net.gW if t is not None] + [_np(net.loss)]
     for a, b in zip(snap, snap2):
         np.testing.assert_array_equal(a, b)
+    # the readout's dx folded into the scan below, or contracted and read back
+    if any(net.fold):
+        plain = snn.Network(wl, inp["params"], device=DEV, reset_grad=reset, flags=PATHS[path],
+                            fold=False)
+        plain.step(x, labels=lab, targets=tgt)
+        for li, (a, b) in enumerate(zip(net.gW, plain.gW)):
+            if a is not None:
+                assert_close(_np(a), _np(b), 2e-2 if wl.dtype == "f16" else 1e-3,
+                             what=f"L{li} dW folded vs not")
 
 
 @pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
