@@ -116,8 +116,10 @@ __device__ inline void load_words(const T *p, int valid, uint32_t (&w)[N * sizeo
 template <int SRC, int MT, int WORDS>
 __device__ inline uint32_t part_of(const uint32_t (&w)[WORDS], int i, int part) {
     if constexpr (SRC == SRC_SPIKE) {
+        // a byte has at most 8 significant bits: its fp32 value's upper half
+        // is its bf16 value, no rounding needed
         const float v = (float)((w[i / 4] >> (8 * (i % 4))) & 0xffu);
-        return MT == MT_F16 ? f16_bits(v) : bf16_bits(v);
+        return MT == MT_F16 ? f16_bits(v) : (__float_as_uint(v) >> 16);
     } else if constexpr (SRC == SRC_H16 || SRC == SRC_PLANES) {
         return (w[i / 2] >> (16 * (i % 2))) & 0xffffu;
     } else if constexpr (SRC == SRC_F16X2) {
