@@ -245,12 +245,18 @@ __device__ inline floatx16 mfma32(const uint4 &a, const uint4 &b, const floatx16
 // k-tile and LDS stages: single-part operand pairs use 64-deep k-tiles in a
 // two-stage LDS ring (one barrier per k-tile, the next tile staged while this
 // one is multiplied); multi-part pairs carry P times the MFMA work per staged
-// byte and keep a single 32-deep stage (two barriers), which leaves LDS for
-// more resident workgroups.
+// byte and use 32-deep k-tiles, in two stages too when they have at most three
+// parts and the A side is not spikes (the weight gradient dI x, the fp16
+// net's input gradient: measured faster), else in a single stage (two
+// barriers), which leaves LDS for more resident workgroups (the forward
+// spikes x W: measured faster).
 template <int SA, int SB>
 constexpr int ktile() { return SrcTraits<SA>::P * SrcTraits<SB>::P == 1 ? 64 : 32; }
 template <int SA, int SB>
-constexpr int lds_stages() { return SrcTraits<SA>::P * SrcTraits<SB>::P == 1 ? 2 : 1; }
+constexpr int lds_stages() {
+    constexpr int parts = SrcTraits<SA>::P * SrcTraits<SB>::P;
+    return (parts == 1 || (parts <= 3 && SA != SRC_SPIKE)) ? 2 : 1;
+}
 
 template <int MT, int SA, bool A_KC, int SB, bool B_KC, int BM, int BN>
 __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_kernel(
@@ -394,8 +400,7 @@ constexpr int kShapeBM[kShapes] = {128, 128, 256, 128};
 constexpr int kShapeBN[kShapes] = {128, 64, 128, 256};
 // Relative time per unit of tile work (128x128 = 1), measured on MI355X with
 // every shape forced in turn on the contractions of the dense benchmark
-// layers: [multi-part single-stage kernels, single-part two-stage
-// kernels][shape].
+// layers: [multi-part kernels, single-part kernels][shape].
 constexpr float kShapeCost[2][kShapes] = {{1.0f, 1.6f, 0.6f, 0.85f}, {1.0f, 1.3f, 1.2f, 1.2f}};
 constexpr int kMaxSlotsPerCu = 8;  // upper bound on resident 256-thread blocks
 
@@ -527,7 +532,7 @@ Plan16 plan_for(const GemmArgs &g, const Kind &kd) {
         const int64_t rounds = (items + slots - 1) / slots;
         // time ~ rounds x tile work, plus the partial-sum traffic of split-K
         double cost = (double)rounds * p.BM * p.BN * p.k_chunk *
-                      kShapeCost[lds_stages<SA, SB>() - 1][sh];
+                      kShapeCost[SrcTraits<SA>::P * SrcTraits<SB>::P == 1 ? 1 : 0][sh];
         if (p.splits > 1) cost += (double)p.splits * g.M * g.N * 64.0 / cus;
         if (cost < best_cost) {
             best_cost = cost;
