@@ -47,15 +47,62 @@ __device__ inline double wave_max(double v) {
     return v;
 }
 
-// Cross-entropy with the class counts as logits.  One wave per row (4 rows
-// per workgroup).  Rows of up to kCeRowLds counts are staged in LDS with
-// coalesced loads; lane l sums the populations of classes l, l+64, ... once
-// into LDS, max and sum of exponentials are wave reductions in a fixed
-// butterfly order, and the per-class gradient is written back to the row's
-// K*P neurons with coalesced stores.  Longer rows read the counts from
-// global memory.  The row's loss goes to partial[b] (fp64), summed in fixed
-// order by ce_sum_kernel.  A label outside [0, K) makes that row's loss and
-// gradient NaN (no out-of-range access).
+// Cross-entropy with the class counts as logits, one wave per row.  Rows of
+// up to LDSROW counts are staged in the wave's LDS buffers with coalesced
+// loads; lane l sums the populations of classes l, l+64, ... once, max and
+// sum of exponentials are wave reductions in a fixed butterfly order, and the
+// per-class gradient is written back to the row's K*P neurons with coalesced
+// stores.  Longer rows read the counts from global memory.  Returns the
+// row's loss (fp64) in every lane.  A label outside [0, K) makes that row's
+// loss and gradient NaN (no out-of-range access).
+template <int LDSROW>
+__device__ inline double ce_row(int b, int B, int K, int P, int lane, const float *__restrict__ counts,
+                                const int32_t *__restrict__ labels, float *__restrict__ grad,
+                                float *rowbuf, double *cls) {
+    const int64_t row = (int64_t)K * P;
+    const bool staged = row <= LDSROW;
+    const float *cg = counts + (int64_t)b * row;
+    if (staged) {
+        for (int j = lane; j < (int)row; j += 64) rowbuf[j] = cg[j];
+        // read back by other lanes of the same wave: a wave's LDS accesses
+        // complete in order, so only the compiler must keep the order
+        __builtin_amdgcn_wave_barrier();
+        for (int k = lane; k < K; k += 64) cls[k] = class_count(rowbuf, k, P);
+        __builtin_amdgcn_wave_barrier();
+    }
+    const int y = labels[b];
+    const bool ok = (y >= 0 && y < K);
+    double mx = -__builtin_inf();
+    for (int k = lane; k < K; k += 64) mx = fmax(mx, staged ? cls[k] : class_count(cg, k, P));
+    mx = wave_max(mx);
+    double se = 0.0;
+    for (int k = lane; k < K; k += 64) se += exp((staged ? cls[k] : class_count(cg, k, P)) - mx);
+    se = wave_sum(se);
+    const double invB = 1.0 / (double)B;
+    float *gr = grad ? grad + (int64_t)b * row : nullptr;
+    if (gr && staged) {
+        // per-class gradient in place of the class counts, then spread over
+        // each population with coalesced stores
+        for (int k = lane; k < K; k += 64) {
+            const double p = exp(cls[k] - mx) / se;
+            rowbuf[k] = ok ? (float)((p - (k == y ? 1.0 : 0.0)) * invB) : __builtin_nanf("");
+        }
+        __builtin_amdgcn_wave_barrier();
+        for (int j = lane; j < (int)row; j += 64) gr[j] = rowbuf[j / P];
+        __builtin_amdgcn_wave_barrier();  // the buffers are reused by the next row
+    } else if (gr) {
+        for (int k = lane; k < K; k += 64) {
+            const double p = exp(class_count(cg, k, P) - mx) / se;
+            const double gk = ok ? (p - (k == y ? 1.0 : 0.0)) * invB : __builtin_nan("");
+            for (int q = 0; q < P; ++q) gr[(int64_t)k * P + q] = (float)gk;
+        }
+    }
+    const double cy = ok ? (staged ? cls[y] : class_count(cg, y, P)) : 0.0;
+    return ok ? (mx + log(se)) - cy : __builtin_nan("");
+}
+
+// Rows spread over workgroups (4 rows each); the row losses go to
+// partial[b] (fp64), summed in fixed order by ce_sum_kernel.
 constexpr int kCeRowLds = 1024;
 constexpr int kRowsPerBlock = kThreads / 64;
 __global__ __launch_bounds__(kThreads) void ce_rows_kernel(int B, int K, int P,
@@ -67,51 +114,9 @@ __global__ __launch_bounds__(kThreads) void ce_rows_kernel(int B, int K, int P,
     __shared__ double cls[kRowsPerBlock][kCeRowLds];
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int b = blockIdx.x * kRowsPerBlock + wave;
-    const int64_t row = (int64_t)K * P;
-    const bool staged = row <= kCeRowLds;
-    const float *cg = counts + (int64_t)(b < B ? b : 0) * row;
-    if (staged && b < B)
-        for (int j = lane; j < (int)row; j += 64) rowbuf[wave][j] = cg[j];
-    __syncthreads();  // every wave reaches it, rows past B included
-    if (staged && b < B)
-        for (int k = lane; k < K; k += 64) cls[wave][k] = class_count(rowbuf[wave], k, P);
-    __syncthreads();
-    if (b >= B) return;
-    const int y = labels[b];
-    const bool ok = (y >= 0 && y < K);
-    double mx = -__builtin_inf();
-    for (int k = lane; k < K; k += 64)
-        mx = fmax(mx, staged ? cls[wave][k] : class_count(cg, k, P));
-    mx = wave_max(mx);
-    double se = 0.0;
-    for (int k = lane; k < K; k += 64)
-        se += exp((staged ? cls[wave][k] : class_count(cg, k, P)) - mx);
-    se = wave_sum(se);
-    const double invB = 1.0 / (double)B;
-    float *gr = grad ? grad + (int64_t)b * row : nullptr;
-    if (gr && staged) {
-        // per-class gradient in place of the class counts, then spread
-        // over each population with coalesced stores
-        for (int k = lane; k < K; k += 64) {
-            const double p = exp(cls[wave][k] - mx) / se;
-            rowbuf[wave][k] = ok ? (float)((p - (k == y ? 1.0 : 0.0)) * invB)
-                                 : __builtin_nanf("");
-        }
-        // read back by other lanes of the same wave: a wave's LDS accesses
-        // complete in order, so only the compiler must keep the order
-        __builtin_amdgcn_wave_barrier();
-        for (int j = lane; j < (int)row; j += 64) gr[j] = rowbuf[wave][j / P];
-    } else if (gr) {
-        for (int k = lane; k < K; k += 64) {
-            const double p = exp(class_count(cg, k, P) - mx) / se;
-            const double gk = ok ? (p - (k == y ? 1.0 : 0.0)) * invB : __builtin_nan("");
-            for (int q = 0; q < P; ++q) gr[(int64_t)k * P + q] = (float)gk;
-        }
-    }
-    if (lane == 0) {
-        const double cy = ok ? (staged ? cls[wave][y] : class_count(cg, y, P)) : 0.0;
-        partial[b] = ok ? (mx + log(se)) - cy : __builtin_nan("");
-    }
+    if (b >= B) return;  // no workgroup barrier follows
+    const double l = ce_row<kCeRowLds>(b, B, K, P, lane, counts, labels, grad, rowbuf[wave], cls[wave]);
+    if (lane == 0) partial[b] = l;
 }
 
 // loss = sum_b partial[b] / B, fixed order (strided per thread, then tree)
@@ -121,6 +126,45 @@ __global__ __launch_bounds__(kThreads) void ce_sum_kernel(int B, const double *_
     for (int b = threadIdx.x; b < B; b += kThreads) part += partial[b];
     const double s = block_sum(part);
     if (threadIdx.x == 0) *loss = (float)(s / (double)B);
+}
+
+// Small rows (K*P <= 64) and batches (B <= 4096), the readouts of the
+// benchmark networks: one workgroup of 16 waves takes every row (wave w rows
+// w, w+16, ...), keeps the row losses in LDS and sums them in the same fixed
+// order as ce_sum_kernel: one launch instead of two.
+constexpr int kCeSmallThreads = 1024;
+constexpr int kCeSmallRow = 64;
+constexpr int kCeSmallMaxB = 4096;
+__global__ __launch_bounds__(kCeSmallThreads) void ce_small_kernel(int B, int K, int P,
+                                                                   const float *__restrict__ counts,
+                                                                   const int32_t *__restrict__ labels,
+                                                                   float *__restrict__ grad,
+                                                                   float *__restrict__ loss) {
+    constexpr int W = kCeSmallThreads / 64;
+    __shared__ float rowbuf[W][kCeSmallRow];
+    __shared__ double cls[W][kCeSmallRow];
+    __shared__ double part[kCeSmallMaxB];
+    __shared__ double red[kCeSmallThreads / 64];
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    for (int b = wave; b < B; b += W) {
+        const double l = ce_row<kCeSmallRow>(b, B, K, P, lane, counts, labels, grad, rowbuf[wave],
+                                             cls[wave]);
+        if (lane == 0) part[b] = l;
+    }
+    __syncthreads();
+    // the order of ce_sum_kernel: thread t sums rows t, t + 256, ...; the
+    // 256 sums in 4 waves by butterfly, the waves in order
+    double s = 0.0;
+    if (threadIdx.x < kThreads)
+        for (int b = threadIdx.x; b < B; b += kThreads) s += part[b];
+    s = wave_sum(s);
+    if (lane == 0 && wave < kThreads / 64) red[wave] = s;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double t = 0.0;
+        for (int w = 0; w < kThreads / 64; ++w) t += red[w];
+        *loss = (float)(t / (double)B);
+    }
 }
 
 // Mean squared error, first pass: block z sums (c - y)^2 over its chunk of
@@ -178,6 +222,10 @@ hipError_t launch_loss(int kind, int B, int K, int P, const float *counts,
                        const int32_t *labels, const float *targets, float *loss, float *grad,
                        void *ws, hipStream_t s) {
     if (kind == SNN_LOSS_CE_COUNT) {
+        if ((int64_t)K * P <= kCeSmallRow && B <= kCeSmallMaxB) {
+            ce_small_kernel<<<1, kCeSmallThreads, 0, s>>>(B, K, P, counts, labels, grad, loss);
+            return hipGetLastError();
+        }
         double *partial = reinterpret_cast<double *>(ws);
         ce_rows_kernel<<<(B + kRowsPerBlock - 1) / kRowsPerBlock, kThreads, 0, s>>>(
             B, K, P, counts, labels, grad, partial);
