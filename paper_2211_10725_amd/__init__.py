@@ -446,8 +446,11 @@ class Network:
         return self.saved[li][off:]
 
     # the same work through the stage calls, with a hook between stages
-    # (update: finish with the AdamW step of ``init_adamw``)
-    def step_stages(self, x, labels=None, targets=None, stream=None, hook=None, update=False):
+    # (update: finish with the AdamW step of ``init_adamw``; fused_bwd: each
+    # layer's backward as one snn_layer_bwd call, hooked as "layer_bwd", as in
+    # ``backward``)
+    def step_stages(self, x, labels=None, targets=None, stream=None, hook=None, update=False,
+                    fused_bwd=False):
         torch = self.torch
         hook = hook or (lambda name, li: None)
         n = len(self.descs)
@@ -478,6 +481,14 @@ class Network:
                 snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], self.gx[li], None,
                                self.gv[li], self.ws, stream)
                 hook("neuron_bwd_end", li)
+                continue
+            if fused_bwd and self.dup[li] is None:
+                hook("layer_bwd", li)
+                snn_layer_bwd(d, kind, g, xin, self.W[li], self.v[li], self.saved[li],
+                              self.gW[li], self.gb[li], self.gv[li], self.gx[li], self.ws, stream)
+                hook("layer_bwd_end", li)
+                if li > 0:
+                    kind, g = self._grad_below(li)
                 continue
             dcur_bytes = d.T * d.B * d.n_out * (2 if d.grad_dtype in (F16, BF16) else 4)
             if self.dup[li] is not None:

@@ -133,8 +133,13 @@ DwPlan dw_plan(const snn_layer_desc *d) {
     DwPlan p{};
     const int M = (int)rows(d);
     const GemmArgs kc = dw_probe_kc(d);
-    // a layer with few outputs reads its operands in their own layouts
-    p.transposed = split_ok(d) && gemm16_applies(kc) && d->n_out > 16 &&
+    // A layer with few outputs reads its operands in their own layouts, and
+    // so does an fp32 dL/dI against spikes over at most 8192 rows: the 16-bit
+    // kernel stages both M/N-contiguous tiles in LDS as they are and reads
+    // transposed fragments (measured: 42 against 34 + 17 us of contraction and
+    // transposes at 3200 rows, 127 against 85 + 34 us at 12800 rows).
+    const bool mn_direct = d->grad_dtype == SNN_F32 && d->in_dtype == SNN_U8 && M <= 8192;
+    p.transposed = split_ok(d) && gemm16_applies(kc) && d->n_out > 16 && !mn_direct &&
                    2.0 * M * d->n_in * d->n_out >= kTransposeFlops;
     if (p.transposed) {
         p.a_dtype = kc.a_dtype;

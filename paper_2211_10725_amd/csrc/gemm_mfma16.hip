@@ -27,6 +27,7 @@
 // shape and split-K come from the runtime occupancy; workgroups are
 // renumbered so each XCD covers a contiguous range of tiles.
 #include <atomic>
+#include <type_traits>
 
 #include "snn_internal.hpp"
 
@@ -149,6 +150,7 @@ struct Operand {
     static constexpr int P = SrcTraits<SRC>::P;
     static constexpr int PL = SrcTraits<SRC>::PLANES;
     static constexpr int LDK = BK + 8;             // LDS row stride (16-bit elements)
+    static constexpr int STAGE = P * R * LDK;      // 16-bit units per LDS stage
     static constexpr int EPT = R * BK / kThreads;  // elements per thread
     static_assert(EPT == 8 || EPT == 16 || EPT == 32 || EPT == 64, "tile");
     static constexpr int TPR = BK / EPT;           // threads per row (KC)
@@ -232,6 +234,135 @@ __global__ __launch_bounds__(kThreads) void split_planes_kernel(const float *__r
     dst[2 * n + i] = (uint16_t)part_of<SRC_F32, MT_BF16, 1>(w, 0, 2);
 }
 
+// Operand tile stored M/N-contiguous ([k][row], the layout of dL/dI and of
+// the spikes x in the weight gradient dW = dI^T x) without a transpose in
+// global memory.  The tile is copied in its own layout into LDS with
+// coalesced 16-byte loads along the rows ([part][k][row], rows of RS 16-bit
+// elements or RSB bytes), and the MFMA fragments are read with gfx950's
+// transposing LDS loads: within each 16 lanes, ds_read_b64_tr_b16 hands lane
+// i element e of lane 4e + i/4's 4-element run (position i % 4), and
+// ds_read_b64_tr_b8 element e of lane 2e + i/8's 8-byte run (position i % 8)
+// (measured on the GPU with an in-bounds probe).  With lane L of a group
+// pointing at k-row kb + L/4 (16-bit) or kb + L/2 (bytes) and row j0 +
+// 4 (L % 4) or j0 + 8 (L % 2), lane i receives k = kb, kb+1, ... of row j0 + i:
+// the k-contiguous run the MFMA operand needs.  fp32 is split into its three
+// exact bf16 parts while staged.  Row strides put the 4 (or 8) k-rows a group
+// reads on distinct banks: RS = 16 mod 64 elements, RSB = 16 mod 128 bytes.
+typedef short v4s16 __attribute__((ext_vector_type(4)));
+typedef int v2i32 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) v4s16 lds_v4s16;
+typedef __attribute__((address_space(3))) v2i32 lds_v2i32;
+
+template <int SRC>
+constexpr bool mn_staged() {
+    return SRC == SRC_SPIKE || SRC == SRC_H16 || SRC == SRC_PLANES || SRC == SRC_F32;
+}
+
+template <int SRC, int MT, int R, int BK>
+struct OperandMN {
+    typedef typename SrcTraits<SRC>::T T;
+    static constexpr int P = SrcTraits<SRC>::P;
+    static constexpr int PL = SrcTraits<SRC>::PLANES;
+    static constexpr bool BYTES = SRC == SRC_SPIKE;
+    static constexpr int RS = (R + 63) / 64 * 64 + 16;    // 16-bit elements per k-row
+    static constexpr int RSB = (R + 127) / 128 * 128 + 16; // bytes per k-row (spikes)
+    static constexpr int STAGE = BYTES ? BK * RSB / 2 : P * BK * RS;  // 16-bit units
+    static constexpr int VE = 16 / (int)sizeof(T);         // elements per 16-byte run
+    static constexpr int CPR = R / VE;                     // runs per k-row
+    static constexpr int RUNS = BK * CPR;                  // runs per tile (per plane)
+    static constexpr int CPT = (RUNS + kThreads - 1) / kThreads;  // runs per thread
+    uint4 v[PL][CPT];
+
+    __device__ inline void fetch(const T *base, int64_t ld, int64_t ps, int rows, int row0, int k0,
+                                 int kend) {
+        const bool vec = ((((uintptr_t)base) | (uintptr_t)(ld * (int64_t)sizeof(T)) |
+                           (uintptr_t)(ps * (int64_t)sizeof(T))) & 15) == 0;
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+            const int q = threadIdx.x + c * kThreads;
+            const int kr = q / CPR, row = row0 + (q % CPR) * VE, k = k0 + kr;
+            const int valid = (q < RUNS && k < kend) ? min(VE, rows - row) : 0;
+#pragma unroll
+            for (int pl = 0; pl < PL; ++pl) {
+                const T *src = base + pl * ps + (int64_t)k * ld + row;
+                if (valid == VE && vec) {
+                    v[pl][c] = *reinterpret_cast<const uint4 *>(src);
+                } else {
+                    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+                    for (int e = 0; e < VE; ++e) {
+                        if (e < valid) {
+                            if constexpr (sizeof(T) == 1) w[e / 4] |= (uint32_t)src[e] << (8 * (e % 4));
+                            else if constexpr (sizeof(T) == 2) w[e / 2] |= (uint32_t)src[e] << (16 * (e % 2));
+                            else w[e] = __float_as_uint(src[e]);
+                        }
+                    }
+                    v[pl][c] = make_uint4(w[0], w[1], w[2], w[3]);
+                }
+            }
+        }
+    }
+
+    __device__ inline void store(uint16_t *lds) const {
+#pragma unroll
+        for (int c = 0; c < CPT; ++c) {
+            const int q = threadIdx.x + c * kThreads;
+            if (RUNS % kThreads != 0 && q >= RUNS) break;
+            const int kr = q / CPR, col = (q % CPR) * VE;
+            if constexpr (BYTES) {
+                *reinterpret_cast<uint4 *>(reinterpret_cast<uint8_t *>(lds) + kr * RSB + col) = v[0][c];
+            } else if constexpr (SRC == SRC_F32) {
+                // four fp32 values -> their hi, mid, lo bf16 parts
+                const uint32_t x[4] = {v[0][c].x, v[0][c].y, v[0][c].z, v[0][c].w};
+                uint32_t hp[3][4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int p = 0; p < 3; ++p) hp[p][e] = part_of<SRC_F32, MT, 4>(x, e, p);
+#pragma unroll
+                for (int p = 0; p < 3; ++p)
+                    *reinterpret_cast<uint2 *>(lds + (p * BK + kr) * RS + col) =
+                        make_uint2(hp[p][0] | (hp[p][1] << 16), hp[p][2] | (hp[p][3] << 16));
+            } else {
+#pragma unroll
+                for (int p = 0; p < P; ++p)
+                    *reinterpret_cast<uint4 *>(lds + (p * BK + kr) * RS + col) = v[p][c];
+            }
+        }
+    }
+
+    // the MFMA fragment of part p for operand rows r0 .. r0 + 31 and k-step ks
+    __device__ static inline uint4 frag(const uint16_t *lds, int p, int r0, int ks, int lane) {
+        const int g = lane >> 4, L = lane & 15;
+        const int j0 = r0 + 16 * (g & 1), kb = ks + 8 * (g >> 1);
+        if constexpr (BYTES) {
+            const uint8_t *b = reinterpret_cast<const uint8_t *>(lds) + (kb + (L >> 1)) * RSB + j0 + 8 * (L & 1);
+            const v2i32 r = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_v2i32 *)b);
+            uint2 raw;
+            raw.x = (uint32_t)r[0];
+            raw.y = (uint32_t)r[1];
+            uint32_t o[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t wd = i < 2 ? raw.x : raw.y;
+                const float lo = (float)((wd >> (16 * (i % 2))) & 0xffu);
+                const float hi = (float)((wd >> (16 * (i % 2) + 8)) & 0xffu);
+                if constexpr (MT == MT_F16)
+                    o[i] = f16_bits(lo) | (f16_bits(hi) << 16);
+                else
+                    o[i] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xffff0000u);
+            }
+            return make_uint4(o[0], o[1], o[2], o[3]);
+        } else {
+            const uint16_t *a = lds + (p * BK + kb + (L >> 2)) * RS + j0 + 4 * (L & 3);
+            const v4s16 r0v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s16 *)a);
+            const v4s16 r1v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s16 *)(a + 4 * RS));
+            const uint2 x0 = __builtin_bit_cast(uint2, r0v), x1 = __builtin_bit_cast(uint2, r1v);
+            return make_uint4(x0.x, x0.y, x1.x, x1.y);
+        }
+    }
+};
+
 template <int MT>
 __device__ inline floatx16 mfma32(const uint4 &a, const uint4 &b, const floatx16 &c) {
     if constexpr (MT == MT_F16)
@@ -270,7 +401,12 @@ __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_ke
     constexpr int LDK = KT + 8;
     constexpr int WM = BM / 2, WN = BN / 2;
     constexpr int FM = WM / 32, FN = WN / 32;
-    constexpr int SZA = PA * BM * LDK, SZB = PB * BN * LDK;
+    using OA = std::conditional_t<!A_KC && mn_staged<SA>(), OperandMN<SA, MT, BM, KT>,
+                                  Operand<SA, MT, A_KC, BM, KT>>;
+    using OB = std::conditional_t<!B_KC && mn_staged<SB>(), OperandMN<SB, MT, BN, KT>,
+                                  Operand<SB, MT, B_KC, BN, KT>>;
+    constexpr bool A_MN = !A_KC && mn_staged<SA>(), B_MN = !B_KC && mn_staged<SB>();
+    constexpr int SZA = OA::STAGE, SZB = OB::STAGE;
     constexpr int NS = lds_stages<SA, SB>();
     __shared__ __attribute__((aligned(16))) uint16_t As[NS * SZA];
     __shared__ __attribute__((aligned(16))) uint16_t Bs[NS * SZB];
@@ -296,8 +432,8 @@ __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_ke
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    Operand<SA, MT, A_KC, BM, KT> oa;
-    Operand<SB, MT, B_KC, BN, KT> ob;
+    OA oa;
+    OB ob;
     // prologue: stage the first k-tile (two-stage ring) and fetch the next
     if (kbeg < kend) {
         oa.fetch(A, lda, a_ps, M, m0, kbeg, kend);
@@ -334,15 +470,23 @@ __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_ke
 #pragma unroll
             for (int p = 0; p < PA; ++p)
 #pragma unroll
-                for (int i = 0; i < FM; ++i)
-                    a[p][i] = *reinterpret_cast<const uint4 *>(
-                        as + ((size_t)p * BM + wm * WM + i * 32 + lrow) * LDK + ks + lk);
+                for (int i = 0; i < FM; ++i) {
+                    if constexpr (A_MN)
+                        a[p][i] = OA::frag(as, p, wm * WM + i * 32, ks, lane);
+                    else
+                        a[p][i] = *reinterpret_cast<const uint4 *>(
+                            as + ((size_t)p * BM + wm * WM + i * 32 + lrow) * LDK + ks + lk);
+                }
 #pragma unroll
             for (int q = 0; q < PB; ++q)
 #pragma unroll
-                for (int j = 0; j < FN; ++j)
-                    b[q][j] = *reinterpret_cast<const uint4 *>(
-                        bs + ((size_t)q * BN + wn * WN + j * 32 + lrow) * LDK + ks + lk);
+                for (int j = 0; j < FN; ++j) {
+                    if constexpr (B_MN)
+                        b[q][j] = OB::frag(bs, q, wn * WN + j * 32, ks, lane);
+                    else
+                        b[q][j] = *reinterpret_cast<const uint4 *>(
+                            bs + ((size_t)q * BN + wn * WN + j * 32 + lrow) * LDK + ks + lk);
+                }
 #pragma unroll
             for (int i = 0; i < FM; ++i)
 #pragma unroll
