@@ -839,36 +839,99 @@ int gemm16_passes(const GemmArgs &g) {
 namespace snn {
 namespace {
 
-// dst[c][r] = src[r][c] through a 64x64 LDS tile (+1 column of padding so the
-// column-wise reads are free of bank conflicts).  With PLANES, an fp32 source
-// is written as three bf16 planes (dst + p*plane) of its exact split.
+// dst[c][r] = src[r][c] through a 64x64 LDS tile (+1 column of padding).  A
+// thread moves runs of 4 elements: it loads 4 consecutive columns of a source
+// row and stores 4 consecutive rows of a destination row (16 threads cover
+// one 64-element row), so both sides are 4-wide vector accesses when aligned;
+// the LDS accesses of a wave fall on 64 distinct banks either way.  With
+// PLANES, an fp32 source is written as three bf16 planes (dst + p*plane) of
+// its exact split.
 template <typename T, bool PLANES>
 __global__ __launch_bounds__(256) void transpose_kernel(int rows, int cols, const T *__restrict__ src,
                                                         int64_t lds_, void *__restrict__ dst,
                                                         int64_t ldd, int64_t plane) {
     __shared__ T tile[64][65];
+    typedef uint16_t O;  // element type of the destination when PLANES
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    const int q = threadIdx.x & 15, g = threadIdx.x >> 4;
+    {
+        const int c = c0 + 4 * q;
+        const bool vec = c + 4 <= cols && (lds_ & 3) == 0 &&
+                         (((uintptr_t)src) & (4 * sizeof(T) - 1)) == 0;
 #pragma unroll
-    for (int i = 0; i < 64; i += 4) {
-        const int r = r0 + ty + i, c = c0 + tx;
-        if (r < rows && c < cols) tile[ty + i][tx] = src[(int64_t)r * lds_ + c];
+        for (int j = 0; j < 4; ++j) {
+            const int rl = g + 16 * j, r = r0 + rl;
+            T v[4] = {T(0), T(0), T(0), T(0)};
+            if (r < rows) {
+                const T *p = src + (int64_t)r * lds_ + c;
+                if (vec) {
+                    if constexpr (sizeof(T) == 4) {
+                        const uint4 u = *reinterpret_cast<const uint4 *>(p);
+                        v[0] = __uint_as_float(u.x); v[1] = __uint_as_float(u.y);
+                        v[2] = __uint_as_float(u.z); v[3] = __uint_as_float(u.w);
+                    } else {
+                        const uint2 u = *reinterpret_cast<const uint2 *>(p);
+                        v[0] = (T)(u.x & 0xffffu); v[1] = (T)(u.x >> 16);
+                        v[2] = (T)(u.y & 0xffffu); v[3] = (T)(u.y >> 16);
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (c + e < cols) v[e] = p[e];
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e) tile[rl][4 * q + e] = v[e];
+        }
     }
     __syncthreads();
+    const int r = r0 + 4 * q;
+    constexpr int OB = PLANES ? 2 : (int)sizeof(T);  // bytes per stored element
+    const bool vec = r + 4 <= rows && (ldd & 3) == 0 && (!PLANES || (plane & 3) == 0) &&
+                     (((uintptr_t)dst) & (4 * OB - 1)) == 0;
 #pragma unroll
-    for (int i = 0; i < 64; i += 4) {
-        const int c = c0 + ty + i, r = r0 + tx;
-        if (r < rows && c < cols) {
-            const T v = tile[tx][ty + i];
-            const int64_t o = (int64_t)c * ldd + r;
-            if constexpr (PLANES) {
-                uint32_t w[1] = {__float_as_uint((float)v)};
-                uint16_t *d16 = reinterpret_cast<uint16_t *>(dst);
-                d16[o] = (uint16_t)part_of<SRC_F32, MT_BF16, 1>(w, 0, 0);
-                d16[plane + o] = (uint16_t)part_of<SRC_F32, MT_BF16, 1>(w, 0, 1);
-                d16[2 * plane + o] = (uint16_t)part_of<SRC_F32, MT_BF16, 1>(w, 0, 2);
+    for (int j = 0; j < 4; ++j) {
+        const int cl = g + 16 * j, c = c0 + cl;
+        if (c >= cols) continue;
+        T v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = tile[4 * q + e][cl];
+        const int64_t o = (int64_t)c * ldd + r;
+        if constexpr (PLANES) {
+            O *d16 = reinterpret_cast<O *>(dst);
+#pragma unroll
+            for (int p = 0; p < 3; ++p) {
+                uint32_t h[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    uint32_t w[1] = {__float_as_uint((float)v[e])};
+                    h[e] = part_of<SRC_F32, MT_BF16, 1>(w, 0, p);
+                }
+                O *d = d16 + p * plane + o;
+                if (vec) {
+                    *reinterpret_cast<uint2 *>(d) = make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        if (r + e < rows) d[e] = (O)h[e];
+                }
+            }
+        } else {
+            T *d = reinterpret_cast<T *>(dst) + o;
+            if (vec) {
+                if constexpr (sizeof(T) == 4) {
+                    *reinterpret_cast<uint4 *>(d) =
+                        make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]),
+                                   __float_as_uint(v[2]), __float_as_uint(v[3]));
+                } else {
+                    *reinterpret_cast<uint2 *>(d) =
+                        make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16),
+                                   (uint32_t)v[2] | ((uint32_t)v[3] << 16));
+                }
             } else {
-                reinterpret_cast<T *>(dst)[o] = v;
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (r + e < rows) d[e] = v[e];
             }
         }
     }

@@ -309,9 +309,11 @@ def test_synapse_fwd(M, N, K, wdt, path):
 
 # (12800, 10, 1000) and (5000, 7, 1003): layers with few outputs, large enough
 # for the skinny kernels (short contraction for dx, few rows for dW); 1003
-# inputs give unaligned rows and a partial last group of 4 columns
+# inputs give unaligned rows and a partial last group of 4 columns.
+# (8197, 130, 1003): the weight gradient's operands are transposed first, with
+# ragged rows and columns on both sides of every transpose
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784), (12800, 10, 1000),
-                                                 (5000, 7, 1003)])
+                                                 (5000, 7, 1003), (8197, 130, 1003)])
 @pytest.mark.parametrize("path", list(PATHS))
 def test_synapse_bwd(M, N, K, path):
     """dW = dI^T x (split over K = T*B) and dx = dI W."""
@@ -339,7 +341,8 @@ GRAD_TYPES = {"f32": (snn.F32, torch.float32), "bf16": (snn.BF16, torch.bfloat16
 
 
 @pytest.mark.parametrize("M,N,K", [(300, 130, 77), (12800, 1000, 784), (2048, 512, 1024),
-                                   (1040, 1100, 1000), (12800, 10, 1000), (5000, 7, 1003)])
+                                   (1040, 1100, 1000), (12800, 10, 1000), (5000, 7, 1003),
+                                   (1037, 1101, 1003)])
 @pytest.mark.parametrize("gdt", list(GRAD_TYPES))
 @pytest.mark.parametrize("wdt", ["f32", "f16"])
 def test_synapse_bwd_operand_types(M, N, K, gdt, wdt):
