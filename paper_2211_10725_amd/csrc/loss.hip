@@ -128,32 +128,75 @@ __global__ __launch_bounds__(kThreads) void ce_sum_kernel(int B, const double *_
     if (threadIdx.x == 0) *loss = (float)(s / (double)B);
 }
 
-// Small rows (K*P <= 64) and batches (B <= 4096), the readouts of the
-// benchmark networks: one workgroup of 16 waves takes every row (wave w rows
-// w, w+16, ...), keeps the row losses in LDS and sums them in the same fixed
-// order as ce_sum_kernel: one launch instead of two.
+// Small readouts (at most 16 classes, 128 rows and 12288 counts): one
+// workgroup stages every count and label in LDS with coalesced loads, then
+// each 16-lane group takes rows g, g + 64, ... with one class per lane.  The
+// group's butterfly reductions combine the same values in the same tree as
+// ce_row's wave-wide ones (there the other lanes add exact zeros, or -inf to
+// the maximum), and the row losses are summed in ce_sum_kernel's fixed order,
+// so the results equal the two-launch path's bit for bit: one launch whose
+// rows are all in flight at once.
+constexpr int kCeGroup = 16;
 constexpr int kCeSmallThreads = 1024;
-constexpr int kCeSmallRow = 64;
-constexpr int kCeSmallMaxB = 4096;
+constexpr int kCeSmallElems = 12288;
+constexpr int kCeSmallMaxB = 128;  // more rows run faster over many workgroups
+
+__device__ inline double group_sum(double v) {
+#pragma unroll
+    for (int off = kCeGroup / 2; off >= 1; off >>= 1) v += __shfl_xor(v, off, kCeGroup);
+    return v;
+}
+
+__device__ inline double group_max(double v) {
+#pragma unroll
+    for (int off = kCeGroup / 2; off >= 1; off >>= 1) v = fmax(v, __shfl_xor(v, off, kCeGroup));
+    return v;
+}
+
 __global__ __launch_bounds__(kCeSmallThreads) void ce_small_kernel(int B, int K, int P,
                                                                    const float *__restrict__ counts,
                                                                    const int32_t *__restrict__ labels,
                                                                    float *__restrict__ grad,
                                                                    float *__restrict__ loss) {
-    constexpr int W = kCeSmallThreads / 64;
-    __shared__ float rowbuf[W][kCeSmallRow];
-    __shared__ double cls[W][kCeSmallRow];
+    __shared__ float cnt[kCeSmallElems];
+    __shared__ int32_t lab[kCeSmallMaxB];
     __shared__ double part[kCeSmallMaxB];
-    __shared__ double red[kCeSmallThreads / 64];
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    for (int b = wave; b < B; b += W) {
-        const double l = ce_row<kCeSmallRow>(b, B, K, P, lane, counts, labels, grad, rowbuf[wave],
-                                             cls[wave]);
-        if (lane == 0) part[b] = l;
+    __shared__ double red[kThreads / 64];
+    const int row = K * P, n = B * row;
+    for (int i = threadIdx.x; i < n; i += kCeSmallThreads) cnt[i] = counts[i];
+    for (int b = threadIdx.x; b < B; b += kCeSmallThreads) lab[b] = labels[b];
+    __syncthreads();
+    const int sub = threadIdx.x % kCeGroup, grp = threadIdx.x / kCeGroup;
+    constexpr int G = kCeSmallThreads / kCeGroup;
+    const double invB = 1.0 / (double)B;
+    for (int b = grp; b < B; b += G) {
+        float *rb = cnt + b * row;
+        const bool has = sub < K;
+        const double c = has ? class_count(rb, sub, P) : 0.0;
+        const int y = lab[b];
+        const bool ok = (y >= 0 && y < K);
+        const double mx = group_max(has ? c : -__builtin_inf());
+        const double e = has ? exp(c - mx) : 0.0;
+        const double se = group_sum(e);
+        const double cy = __shfl(c, ok ? y : 0, kCeGroup);
+        if (grad) {
+            // the class gradient replaces the class's first count (every
+            // count of the row has been read), then spreads over its population
+            __builtin_amdgcn_wave_barrier();
+            if (has) {
+                const double p = e / se;  // e is exp(c - mx), as ce_row recomputes it
+                rb[sub] = ok ? (float)((p - (sub == y ? 1.0 : 0.0)) * invB) : __builtin_nanf("");
+            }
+            __builtin_amdgcn_wave_barrier();
+            float *gr = grad + (int64_t)b * row;
+            for (int j = sub; j < row; j += kCeGroup) gr[j] = rb[j / P];
+        }
+        if (sub == 0) part[b] = ok ? (mx + log(se)) - cy : __builtin_nan("");
     }
     __syncthreads();
     // the order of ce_sum_kernel: thread t sums rows t, t + 256, ...; the
     // 256 sums in 4 waves by butterfly, the waves in order
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     double s = 0.0;
     if (threadIdx.x < kThreads)
         for (int b = threadIdx.x; b < B; b += kThreads) s += part[b];
@@ -222,7 +265,7 @@ hipError_t launch_loss(int kind, int B, int K, int P, const float *counts,
                        const int32_t *labels, const float *targets, float *loss, float *grad,
                        void *ws, hipStream_t s) {
     if (kind == SNN_LOSS_CE_COUNT) {
-        if ((int64_t)K * P <= kCeSmallRow && B <= kCeSmallMaxB) {
+        if (K <= kCeGroup && B <= kCeSmallMaxB && (int64_t)B * K * P <= kCeSmallElems) {
             ce_small_kernel<<<1, kCeSmallThreads, 0, s>>>(B, K, P, counts, labels, grad, loss);
             return hipGetLastError();
         }

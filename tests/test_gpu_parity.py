@@ -460,11 +460,12 @@ def test_conv_pool_bwd(NB, Ci, H, W, Co):
 # ---------------------------------------------------------------------------
 # losses
 # ---------------------------------------------------------------------------
-# rows of at most 64 counts and at most 4096 rows take the one-workgroup
-# kernel; (4097, 10), (64, 65) and (5, 1500) (a row past the LDS staging)
-# the row-per-wave kernel and its separate sum
-@pytest.mark.parametrize("B,K", [(1, 10), (32, 10), (513, 10), (7, 3), (4096, 64), (4097, 10),
-                                 (64, 65), (5, 1500)])
+# at most 16 classes, 128 rows and 12288 counts take the one-workgroup kernel
+# ((1, 10), (32, 10), (7, 3), (128, 16)); (129, 16), (513, 10), (4096, 64),
+# (4097, 10), (64, 65) and (5, 1500) (a row past the LDS staging) the
+# row-per-wave kernel and its separate sum
+@pytest.mark.parametrize("B,K", [(1, 10), (32, 10), (7, 3), (128, 16), (129, 16), (513, 10),
+                                 (4096, 64), (4097, 10), (64, 65), (5, 1500)])
 def test_loss_ce(B, K):
     rng = np.random.default_rng(B)
     c = rng.integers(0, 26, (B, K)).astype(np.float32)
@@ -478,13 +479,15 @@ def test_loss_ce(B, K):
     assert_close(_np(g), rg, 1e-5, what="CE grad")
 
 
-def test_loss_ce_one_and_two_launches_agree():
-    """The one-workgroup cross-entropy (4096 rows) and the row-per-wave path
-    (the same rows and one more) give the same per-row gradients up to the
-    1/B factor, and the loss matches the oracle."""
-    rng = np.random.default_rng(77)
-    B, K = 4096, 10
-    c = rng.integers(0, 26, (B, K)).astype(np.float32)
+@pytest.mark.parametrize("K,P", [(10, 1), (16, 1), (7, 3), (16, 6)])
+def test_loss_ce_one_and_two_launches_agree(K, P):
+    """The one-workgroup cross-entropy (the most rows it takes: 128) and the
+    row-per-wave path (the same rows and one more) give the same per-row
+    gradients up to the 1/B factor, and the loss matches the oracle.  16
+    classes of 6 neurons over 128 rows fill its 12288-count LDS buffer."""
+    rng = np.random.default_rng(77 + K)
+    B = 128
+    c = rng.integers(0, 26, (B, K * P)).astype(np.float32)
     y = rng.integers(0, K, B).astype(np.int32)
     ws = _ws(snn.snn_loss_workspace_bytes(snn.LOSS_CE_COUNT, B + 1, K))
     # B rows: one launch; B + 1 rows (one repeated): the row-per-wave path
@@ -493,10 +496,13 @@ def test_loss_ce_one_and_two_launches_agree():
     for cc, yy in ((c, y), (c2, y2)):
         loss = torch.empty(4, dtype=torch.float32, device=DEV)
         g = torch.empty(cc.shape, dtype=torch.float32, device=DEV)
-        snn.snn_loss(snn.LOSS_CE_COUNT, len(cc), K, 1, _t(cc), _t(yy), None, loss, g, ws)
+        snn.snn_loss(snn.LOSS_CE_COUNT, len(cc), K, P, _t(cc), _t(yy), None, loss, g, ws)
         out.append((_np(loss)[0], _np(g)))
-    L, _ = oracle.loss_ce(c, y)
+    L, rg = oracle.loss_ce(c, y, P)
     assert abs(out[0][0] - L) <= 1e-6 * max(1.0, abs(L))
+    assert_close(out[0][1], rg, 1e-5, what="CE grad")
+    L2, _ = oracle.loss_ce(c2, y2, P)
+    assert abs(out[1][0] - L2) <= 1e-6 * max(1.0, abs(L2))
     # the gradient is (softmax - onehot) / B: rescale the B + 1 rows' by (B + 1) / B
     g1 = out[0][1].astype(np.float64) * B
     g2 = out[1][1][:B].astype(np.float64) * (B + 1)
