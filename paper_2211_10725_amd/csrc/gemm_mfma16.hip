@@ -937,49 +937,65 @@ __global__ __launch_bounds__(256) void transpose_kernel(int rows, int cols, cons
     }
 }
 
-// Bytes: dst[c][r] = src[r][c] for a 64 x 64 tile with 16-byte global loads
-// and stores (4 threads per tile row).  The LDS tile has a 68-byte row
-// stride: written 4 bytes at a time, and the column reads of 16 rows spaced
-// 16 apart fall in distinct banks.
+// Bytes: dst[c][r] = src[r][c] through a 128 x 128 LDS tile.  Loads are 16
+// bytes of a source row (8 threads per row); a thread then takes 4 columns
+// of 16 rows (16 LDS words), regroups their bytes in registers and stores 4
+// destination runs of 16 bytes (8 threads cover a 128-byte destination row).
+// The tile's 132-byte row stride keeps the column-wise word reads of a wave
+// within two rows per bank.
+constexpr int kT8 = 128;       // tile side (bytes)
+constexpr int kT8Row = 132;    // LDS row stride (bytes)
 __global__ __launch_bounds__(256) void transpose_u8_kernel(int rows, int cols,
                                                            const uint8_t *__restrict__ src,
                                                            int64_t lds_, uint8_t *__restrict__ dst,
                                                            int64_t ldd) {
-    __shared__ __attribute__((aligned(16))) uint8_t tile[64 * 68];
-    const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
+    __shared__ __attribute__((aligned(16))) uint32_t tile[kT8 * kT8Row / 4];
+    const int r0 = blockIdx.y * kT8, c0 = blockIdx.x * kT8;
     const int t = threadIdx.x;
     {
-        const int r = t >> 2, cc = (t & 3) * 16;
-        const int gr = r0 + r, gc = c0 + cc;
-        uint32_t w[4] = {0u, 0u, 0u, 0u};
-        if (gr < rows) {
-            const uint8_t *p = src + (int64_t)gr * lds_ + gc;
-            if (gc + 16 <= cols && (((uintptr_t)p) & 15) == 0) {
-                const uint4 v = *reinterpret_cast<const uint4 *>(p);
-                w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
-            } else {
-                for (int e = 0; e < 16; ++e)
-                    if (gc + e < cols) w[e / 4] |= (uint32_t)p[e] << (8 * (e % 4));
-            }
-        }
+        const int cc = (t & 7) * 16;
+        const int gc = c0 + cc;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) *reinterpret_cast<uint32_t *>(&tile[r * 68 + cc + 4 * q]) = w[q];
+        for (int i = 0; i < 4; ++i) {
+            const int r = (t >> 3) + 32 * i, gr = r0 + r;
+            uint32_t w[4] = {0u, 0u, 0u, 0u};
+            if (gr < rows) {
+                const uint8_t *p = src + (int64_t)gr * lds_ + gc;
+                if (gc + 16 <= cols && (((uintptr_t)p) & 15) == 0) {
+                    const uint4 v = *reinterpret_cast<const uint4 *>(p);
+                    w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
+                } else {
+                    for (int e = 0; e < 16; ++e)
+                        if (gc + e < cols) w[e / 4] |= (uint32_t)p[e] << (8 * (e % 4));
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) tile[(r * kT8Row + cc) / 4 + q] = w[q];
+        }
     }
     __syncthreads();
-    {
-        const int c = t >> 2, rr = (t & 3) * 16;
-        const int gc = c0 + c, gr = r0 + rr;
-        if (gc < cols) {
-            uint32_t w[4] = {0u, 0u, 0u, 0u};
+    // thread: destination rows c0 + 4 cw .. + 3, source rows r0 + 16 rg .. + 15
+    const int rg = t & 7, cw = t >> 3;
+    uint32_t w[16];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) w[e / 4] |= (uint32_t)tile[(rr + e) * 68 + c] << (8 * (e % 4));
-            uint8_t *q = dst + (int64_t)gc * ldd + gr;
-            if (gr + 16 <= rows && (((uintptr_t)q) & 15) == 0) {
-                *reinterpret_cast<uint4 *>(q) = make_uint4(w[0], w[1], w[2], w[3]);
-            } else {
-                for (int e = 0; e < 16; ++e)
-                    if (gr + e < rows) q[e] = (uint8_t)(w[e / 4] >> (8 * (e % 4)));
-            }
+    for (int e = 0; e < 16; ++e) w[e] = tile[((16 * rg + e) * kT8Row) / 4 + cw];
+    const int gr = r0 + 16 * rg;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int gc = c0 + 4 * cw + j;
+        if (gc >= cols) continue;
+        uint32_t o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            o[q] = ((w[4 * q] >> (8 * j)) & 0xffu) | (((w[4 * q + 1] >> (8 * j)) & 0xffu) << 8) |
+                   (((w[4 * q + 2] >> (8 * j)) & 0xffu) << 16) |
+                   (((w[4 * q + 3] >> (8 * j)) & 0xffu) << 24);
+        uint8_t *q8 = dst + (int64_t)gc * ldd + gr;
+        if (gr + 16 <= rows && (((uintptr_t)q8) & 15) == 0) {
+            *reinterpret_cast<uint4 *>(q8) = make_uint4(o[0], o[1], o[2], o[3]);
+        } else {
+            for (int e = 0; e < 16; ++e)
+                if (gr + e < rows) q8[e] = (uint8_t)(o[e / 4] >> (8 * (e % 4)));
         }
     }
 }
@@ -1002,7 +1018,8 @@ hipError_t launch_transpose(int rows, int cols, const void *src, int64_t ld_src,
         transpose_kernel<uint16_t, false><<<grid, 256, 0, s>>>(
             rows, cols, reinterpret_cast<const uint16_t *>(src), ld_src, dst, ld_dst, 0);
     } else {
-        transpose_u8_kernel<<<grid, 256, 0, s>>>(rows, cols, reinterpret_cast<const uint8_t *>(src),
+        const dim3 g8((unsigned)((cols + kT8 - 1) / kT8), (unsigned)((rows + kT8 - 1) / kT8));
+        transpose_u8_kernel<<<g8, 256, 0, s>>>(rows, cols, reinterpret_cast<const uint8_t *>(src),
                                                  ld_src, reinterpret_cast<uint8_t *>(dst), ld_dst);
     }
     return hipGetLastError();
