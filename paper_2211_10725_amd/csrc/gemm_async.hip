@@ -149,43 +149,51 @@ __device__ inline void mask_fragments(u32x4 (&f)[F], uint32_t mask) {
     for (int i = 0; i < F; ++i) f[i] &= mask;
 }
 
-// The 16 MFMAs of k16 steps ks and ks + 1 of a stage, fragments read two
-// steps at a time.  A wave covers rows wm * 128 + [0, 128) and columns
-// wn * 64 + [0, 64).
-template <int MT, int S>
-__device__ inline void multiply_pair(floatx16 (&acc)[4][2], int wm, int wn, int ks, int kvalid) {
-    const int half = (threadIdx.x & 63) >> 5;
-    u32x4 a0[4], b0[2], a1[4], b1[2];
-    read_fragments<4>(stage_a<S>(), wm * 128, ks, a0);
-    read_fragments<2>(stage_b<S>(), wn * 64, ks, b0);
-    read_fragments<4>(stage_a<S>(), wm * 128, ks + 1, a1);
-    read_fragments<2>(stage_b<S>(), wn * 64, ks + 1, b1);
-    wait_lgkm6(a0, b0);
-    if (kvalid < kKT) {
-        const uint32_t m = 8 * (2 * ks + half) < kvalid ? 0xffffffffu : 0u;
-        mask_fragments(a0, m);
-        mask_fragments(b0, m);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32<MT>(a0[i], b0[j], acc[i][j]);
-    wait_lgkm0(a1, b1);
-    if (kvalid < kKT) {
-        const uint32_t m = 8 * (2 * ks + 2 + half) < kvalid ? 0xffffffffu : 0u;
-        mask_fragments(a1, m);
-        mask_fragments(b1, m);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32<MT>(a1[i], b1[j], acc[i][j]);
+// LDS address of fragment i of k16 step ks: A fragments i = 0..3 (rows
+// wm * 128 + 32 i), B fragments i = 4, 5 (rows wn * 64 + 32 (i - 4)).
+template <int S>
+__device__ inline uint32_t frag_addr(int wm, int wn, int ks, int i) {
+    const int lane = threadIdx.x & 63;
+    const int c = 2 * ks + (lane >> 5);
+    const uint16_t *stage = i < 4 ? stage_a<S>() : stage_b<S>();
+    const int r = (i < 4 ? wm * 128 + i * 32 : wn * 64 + (i - 4) * 32) + (lane & 31);
+    return lds_addr(stage + r * kKT + (c ^ swz(r)) * 8);
 }
 
+// The 32 MFMAs of the four k16 steps of a stage.  A wave covers rows
+// wm * 128 + [0, 128) and columns wn * 64 + [0, 64).  The 6 fragment reads of
+// step ks + 1 are issued one by one between the 8 MFMAs of step ks
+// (scheduling barriers keep that order), so the wave issues them while the
+// matrix core is busy instead of stalling on them between steps.
 template <int MT, int S>
 __device__ inline void multiply_stage(floatx16 (&acc)[4][2], int wm, int wn, int kvalid) {
-    multiply_pair<MT, S>(acc, wm, wn, 0, kvalid);
-    multiply_pair<MT, S>(acc, wm, wn, 2, kvalid);
+    const int half = (threadIdx.x & 63) >> 5;
+    u32x4 f[2][6];
+#pragma unroll
+    for (int i = 0; i < 6; ++i) lds_read(f[0][i], frag_addr<S>(wm, wn, 0, i));
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+        u32x4(&cur)[6] = f[ks & 1];
+        u32x4(&nxt)[6] = f[(ks + 1) & 1];
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(cur[0]), "+v"(cur[1]), "+v"(cur[2]), "+v"(cur[3]), "+v"(cur[4]),
+                       "+v"(cur[5]));
+        if (kvalid < kKT) {
+            const uint32_t m = 8 * (2 * ks + half) < kvalid ? 0xffffffffu : 0u;
+#pragma unroll
+            for (int i = 0; i < 6; ++i) cur[i] &= m;
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int i = q >> 1, j = q & 1;
+            acc[i][j] = mfma32<MT>(cur[i], cur[4 + j], acc[i][j]);
+            __builtin_amdgcn_sched_barrier(0);
+            if (ks + 1 < 4 && q < 6) {
+                lds_read(nxt[q], frag_addr<S>(wm, wn, ks + 1, q));
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
 }
 
 template <int MT>
