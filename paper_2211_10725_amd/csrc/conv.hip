@@ -203,6 +203,91 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(int Q, int Co, int HW, i
     }
 }
 
+// One input channel (the first layer): the convolution and the pool in one
+// kernel, without the gathered matrix or the unpooled currents.  A workgroup
+// per image stages the image (as fp32) and the weights in LDS; a thread takes
+// pooled currents (co, py, px), pooled column fastest, holds the 6x6 input
+// patch of the window in registers and accumulates the window's four conv
+// outputs tap by tap (ky, kx ascending) with fp32 fma, then adds the bias and
+// keeps the first maximum in window order, as the pool after the contraction.
+constexpr int kDirectMaxHW = 4096;  // image pixels staged in LDS
+constexpr int kDirectMaxCo = 128;  // 14 KiB of padded weights
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void conv1_pool_kernel(int H, int W, int Co, int Hp, int Wp,
+                                                              const T *__restrict__ x,
+                                                              const float *__restrict__ w,
+                                                              const float *__restrict__ bias,
+                                                              float *__restrict__ cur,
+                                                              uint8_t *__restrict__ arg) {
+    constexpr int WS = 28;  // weights of one output channel, padded to 16 bytes
+    __shared__ __attribute__((aligned(16))) float xs[kDirectMaxHW];
+    __shared__ __attribute__((aligned(16))) float wsh[kDirectMaxCo * WS];
+    const int64_t nb = blockIdx.x;
+    const int hw = H * W;
+    const T *xi = x + nb * hw;
+    for (int i = threadIdx.x; i < hw; i += kThreads) xs[i] = (float)xi[i];
+    for (int i = threadIdx.x; i < Co * WS; i += kThreads) {
+        const int co = i / WS, t = i - co * WS;
+        wsh[i] = t < KS * KS ? w[co * KS * KS + t] : 0.f;
+    }
+    __syncthreads();
+    const bool pairs = (W & 1) == 0;  // patch rows start at even offsets: 8-byte reads
+    const int cells = Hp * Wp, total = Co * cells;
+    float *cb = cur + nb * total;
+    uint8_t *ab = arg + nb * total;
+    for (int o = threadIdx.x; o < total; o += kThreads) {
+        const int co = o / cells, p = o - co * cells;
+        const int py = p / Wp, px = p - py * Wp;
+        const float *xp = xs + 2 * py * W + 2 * px;
+        float patch[KS + 1][KS + 1];
+        if (pairs) {
+#pragma unroll
+            for (int r = 0; r <= KS; ++r)
+#pragma unroll
+                for (int c = 0; c <= KS; c += 2) {
+                    const float2 v = *reinterpret_cast<const float2 *>(xp + r * W + c);
+                    patch[r][c] = v.x;
+                    patch[r][c + 1] = v.y;
+                }
+        } else {
+#pragma unroll
+            for (int r = 0; r <= KS; ++r)
+#pragma unroll
+                for (int c = 0; c <= KS; ++c) patch[r][c] = xp[r * W + c];
+        }
+        float wv[WS];
+#pragma unroll
+        for (int q = 0; q < WS / 4; ++q) {
+            const float4 v = *reinterpret_cast<const float4 *>(wsh + co * WS + 4 * q);
+            wv[4 * q] = v.x; wv[4 * q + 1] = v.y; wv[4 * q + 2] = v.z; wv[4 * q + 3] = v.w;
+        }
+        float acc[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ky = 0; ky < KS; ++ky)
+#pragma unroll
+            for (int kx = 0; kx < KS; ++kx) {
+                const float wv1 = wv[ky * KS + kx];
+#pragma unroll
+                for (int d = 0; d < 4; ++d)
+                    acc[d] = __builtin_fmaf(patch[(d >> 1) + ky][(d & 1) + kx], wv1, acc[d]);
+            }
+        const float bco = bias ? bias[co] : 0.f;
+        float best = acc[0] + bco;
+        int a = 0;
+#pragma unroll
+        for (int d = 1; d < 4; ++d) {
+            const float v = acc[d] + bco;
+            if (v > best) {
+                best = v;
+                a = d;
+            }
+        }
+        cb[o] = best;
+        ab[o] = (uint8_t)a;
+    }
+}
+
 __device__ inline uint32_t bf16_rne(float x) {
     const uint32_t b = __float_as_uint(x);
     return (b + 0x7fffu + ((b >> 16) & 1u)) >> 16;
@@ -476,6 +561,17 @@ hipError_t launch_conv_pool_fwd(const ConvGeom &g, const void *x, int in_dtype, 
     if (v.Mw == 0) return hipSuccess;
     if (ws == nullptr || ws_bytes < conv_fwd_workspace_bytes(g, in_dtype, allow_split))
         return hipErrorInvalidValue;
+    if (g.Ci == 1 && g.H * g.W <= kDirectMaxHW && g.Co <= kDirectMaxCo) {
+        if (in_dtype == SNN_U8)
+            conv1_pool_kernel<uint8_t><<<(unsigned)g.NB, kThreads, 0, s>>>(
+                g.H, g.W, g.Co, g.Hp, g.Wp, reinterpret_cast<const uint8_t *>(x),
+                reinterpret_cast<const float *>(w), bias, cur, arg);
+        else
+            conv1_pool_kernel<float><<<(unsigned)g.NB, kThreads, 0, s>>>(
+                g.H, g.W, g.Co, g.Hp, g.Wp, reinterpret_cast<const float *>(x),
+                reinterpret_cast<const float *>(w), bias, cur, arg);
+        return hipGetLastError();
+    }
     char *p = reinterpret_cast<char *>(ws);
     void *col = p;
     p += align_up((size_t)v.Mw * v.ldk * dtype_bytes(in_dtype));

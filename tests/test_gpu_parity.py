@@ -398,6 +398,27 @@ def _conv_fwd_gpu(d, x, w, b):
                                           (1, 2, 6, 6, 2)])
 def test_conv_pool_fwd(NB, Ci, H, W, Co):
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=NB * 100 + Co)
+    _check_conv_fwd(x, w, b, d)
+
+
+# One input channel takes the direct convolution-and-pool kernel while the
+# image fits its LDS buffer (4096 pixels): odd sizes, more output channels
+# than threads per image, the largest staged image, one past it (contraction
+# path), and real-valued input currents.
+@pytest.mark.parametrize("NB,H,W,Co,real", [(4, 9, 11, 5, False), (2, 64, 64, 70, False),
+                                           (3, 65, 64, 3, False), (3, 28, 28, 12, True)])
+def test_conv_pool_fwd_one_channel(NB, H, W, Co, real):
+    x, w, b, d = _conv_case(NB, 1, H, W, Co, seed=NB + H + Co)
+    if real:
+        x = np.random.default_rng(H).uniform(-1, 1, x.shape).astype(np.float32)
+        spec = dict(kind="conv", c_in=1, h=H, w=W, c_out=Co, neuron="leaky", beta=0.5)
+        d = snn.layer_desc(spec, 1, NB, in_dtype=snn.F32)
+    _check_conv_fwd(x, w, b, d)
+
+
+def _check_conv_fwd(x, w, b, d):
+    NB, Ci = x.shape[0], x.shape[1]
+    Co = w.shape[0]
     cur, arg = _conv_fwd_gpu(d, x, w, b)
     y = oracle.conv_fwd(x, w, b)                          # double
     y32 = y.astype(np.float32).astype(np.float64)          # the pool decides on fp32 currents
@@ -406,7 +427,7 @@ def test_conv_pool_fwd(NB, Ci, H, W, Co):
     arg = arg.reshape(a.shape)
     assert_close(cur, p, 1e-3, what="pooled currents")
     # fp32 accumulation of Ci*25 terms, any order
-    terms = oracle.conv_fwd(x, np.abs(w), np.abs(b))
+    terms = oracle.conv_fwd(np.abs(x), np.abs(w), np.abs(b))
     bound = (Ci * 25 + 2) * 2.0 ** -24 * oracle.maxpool2_fwd(terms)[0]
     assert (np.abs(cur - p) <= bound + 1e-30).all()
     # the selection must agree wherever the window's top two differ by more
