@@ -30,6 +30,9 @@ if ROOT not in sys.path:
 METRIC = "SNN training samples/sec (fwd+BPTT) at 1 GPU; scan HBM GB/s, GEMM MFMA %"
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
 PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
+# fp32 fma on the vector ALUs without packed math: 256 CUs x 4 SIMDs x 16
+# lanes x 2 flops x 2.4 GHz (the packed-fp32 rate, 157.3, is not used)
+PEAK_FP32_VALU_TFLOPS = 78.6
 PEAK_FP16_MFMA_TFLOPS = 2500.0
 
 
@@ -304,13 +307,17 @@ def main():
     if kind == "flop":
         achieved = work / (k_avg_ms / 1000.0) / 1e12
         ckind, passes = _contraction_kind(net, dom_li, args.fp32_mfma)
-        if ckind == "mfma16":
-            peak, basis = PEAK_FP16_MFMA_TFLOPS, "bf16/fp16 dense MFMA"
+        if ckind == "valu":
+            roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_VALU_TFLOPS,
+                    "unit": "TFLOP/s", "peak_basis": "fp32 fma on the vector ALUs, no packed math"}
         else:
-            peak, basis = PEAK_FP32_MFMA_TFLOPS, "fp32 dense MFMA"
-        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
-                "unit": "TFLOP/s", "peak_basis": basis, "mfma_passes": passes,
-                "executed_mfma_frac": round(passes * achieved / peak, 4)}
+            if ckind == "mfma16":
+                peak, basis = PEAK_FP16_MFMA_TFLOPS, "bf16/fp16 dense MFMA"
+            else:
+                peak, basis = PEAK_FP32_MFMA_TFLOPS, "fp32 dense MFMA"
+            roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
+                    "unit": "TFLOP/s", "peak_basis": basis, "mfma_passes": passes,
+                    "executed_mfma_frac": round(passes * achieved / peak, 4)}
     else:
         achieved = work / (k_avg_ms / 1000.0) / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
@@ -375,7 +382,8 @@ def _stage_rooflines(net, split, fp32_mfma):
         kind, work = stage_work(net, name, li)
         if kind == "flop":
             ck, _ = _contraction_kind(net, li, fp32_mfma)
-            peak = PEAK_FP16_MFMA_TFLOPS if ck == "mfma16" else PEAK_FP32_MFMA_TFLOPS
+            peak = {"mfma16": PEAK_FP16_MFMA_TFLOPS, "valu": PEAK_FP32_VALU_TFLOPS}.get(
+                ck, PEAK_FP32_MFMA_TFLOPS)
             a = work / (ms / 1000.0) / 1e12
             out[key] = {"TFLOP/s": round(a, 2), "frac": round(a / peak, 4)}
         elif kind == "byte":
@@ -390,6 +398,8 @@ def _contraction_kind(net, li, fp32_mfma):
     ('mfma32', 1).  A conv layer's product has one row per conv output that a
     pool window reads and one column per output channel."""
     d = net.descs[li]
+    if _direct_conv(net, li):
+        return "valu", 1
     if _narrow_contraction(net, li, fp32_mfma):
         return "mfma16", 3 if d.w_dtype == 0 else 1
     if d.synapse == 1:
@@ -403,6 +413,14 @@ def _contraction_kind(net, li, fp32_mfma):
     if d.w_dtype == 0:
         return "mfma16", 3   # fp32 weights: three exact bf16 parts
     return "mfma16", 1       # fp16 weights: one fp16 pass
+
+
+def _direct_conv(net, li):
+    """Whether layer li's forward runs as the one-kernel convolution and pool
+    on the vector ALUs (mirrors the routing in conv.hip: one input channel,
+    at most 4096 pixels, at most 128 output channels)."""
+    d = net.descs[li]
+    return d.synapse == 1 and d.c_in == 1 and d.h_in * d.w_in <= 4096 and d.c_out <= 128
 
 
 def _narrow_contraction(net, li, fp32_mfma):
@@ -438,6 +456,8 @@ def _stage_kernels(net, name, li, fp32_mfma):
         return ": narrow_fwd_kernel (16 outputs per MFMA tile, weights staged in LDS)"
     if name == "neuron_bwd" and net.fold[li]:
         return ": neuron_bwd_kernel (the readout's dx folded in)"
+    if name == "synapse_fwd" and _direct_conv(net, li):
+        return ": conv1_pool_kernel (convolution and pool in one kernel)"
     kind, passes = _contraction_kind(net, li, fp32_mfma)
     if net.descs[li].synapse == 1:
         g = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"
