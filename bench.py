@@ -461,7 +461,9 @@ def _stage_kernels(net, name, li, fp32_mfma):
     kind, passes = _contraction_kind(net, li, fp32_mfma)
     if net.descs[li].synapse == 1:
         g = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"
-        return f": im2col_kernel + {g} + pool_kernel (the whole stage is timed)"
+        pool = (" pooling in its epilogue (+ pool_kernel when split over K)" if kind == "mfma16"
+                else " + pool_kernel")
+        return f": im2col_kernel + {g}{pool} (the whole stage is timed)"
     if kind == "mfma16" and passes == 3:
         return (": gemm16_kernel, 3 exact bf16 passes (+ split_planes_kernel when the weights"
                 " are split into planes up front, + splitk_reduce_kernel when split over K)")

@@ -15,7 +15,10 @@
 //   col[m][k]  = x[nb, c, oy + ky, ox + kx]               (gather)
 //   C[m][co]   = sum_k col[m][k] w[co][k] + bias[co]       (contraction)
 //   cur[nb, co, py, px] = max_d C[4q + d][co], the first maximum in window
-//                order; its d (0..3) is saved for the backward  (pool)
+//                order; its d (0..3) is saved for the backward  (pool; the
+//                16-bit contraction does it in its epilogue when it makes one
+//                pass over K, a window being four rows of one lane's tile)
+// One input channel: conv1_pool_kernel computes the pooled currents directly.
 //
 // Backward, given dI = dL/dcur:
 //   dC^T[co][m] = dI[nb, co, py, px] if d is the saved choice, else 0
@@ -583,8 +586,12 @@ hipError_t launch_conv_pool_fwd(const ConvGeom &g, const void *x, int in_dtype, 
     if (e != hipSuccess) return e;
     GemmArgs a = fwd_args(g, v, in_dtype, allow_split);
     a.A = col; a.B = w; a.C = C; a.bias = bias;
+    // the contraction pools its own output when it can (else C, then the pool)
+    bool pooled = false;
+    a.pool_hw = g.Hp * g.Wp; a.pool_cur = cur; a.pool_arg = arg; a.pooled = &pooled;
     e = launch_gemm(a, p, ws_bytes - (size_t)(p - reinterpret_cast<char *>(ws)), s);
     if (e != hipSuccess) return e;
+    if (pooled) return hipSuccess;
     const int S = g.Co | 1;
     const int QB = max(1, kPoolLdsFloats / (4 * S));
     pool_kernel<<<(unsigned)((v.Q + QB - 1) / QB), kThreads, 0, s>>>((int)v.Q, g.Co, g.Hp * g.Wp,

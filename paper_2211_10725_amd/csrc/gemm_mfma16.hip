@@ -389,12 +389,13 @@ constexpr int lds_stages() {
     return (parts == 1 || (parts <= 3 && SA != SRC_SPIKE)) ? 2 : 1;
 }
 
-template <int MT, int SA, bool A_KC, int SB, bool B_KC, int BM, int BN>
+template <int MT, int SA, bool A_KC, int SB, bool B_KC, int BM, int BN, bool POOL = false>
 __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_kernel(
     int M, int N, int K, int k_chunk, int tiles_n, const typename SrcTraits<SA>::T *__restrict__ A,
     int64_t lda, int64_t a_ps, const typename SrcTraits<SB>::T *__restrict__ B, int64_t ldb,
     int64_t b_ps, float *__restrict__ C, int64_t ldc, int64_t split_stride,
-    const float *__restrict__ bias) {
+    const float *__restrict__ bias, int pool_hw, float *__restrict__ pool_cur,
+    uint8_t *__restrict__ pool_arg) {
     constexpr int PA = SrcTraits<SA>::P, PB = SrcTraits<SB>::P;
     static_assert(PA * PB <= 6, "at most six passes");
     constexpr int KT = ktile<SA, SB>();
@@ -517,6 +518,38 @@ __global__ __launch_bounds__(kThreads, (BM * BN > 16384) ? 2 : 1) void gemm16_ke
 
     // 32x32 block: lane holds column (lane & 31); register r holds row
     // 8*(r/4) + 4*(lane/32) + r%4.
+    if constexpr (POOL) {
+        // registers 4g .. 4g + 3 of a lane are the four rows of one pool
+        // window (M is a multiple of 4): the first maximum of C + bias
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) {
+                const int n = n0 + wn * WN + j * 32 + (lane & 31);
+                if (n >= N) continue;
+                const float bn = bias ? bias[n] : 0.f;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const int m = m0 + wm * WM + i * 32 + 8 * g + 4 * (lane >> 5);
+                    if (m >= M) continue;
+                    float best = acc[i][j][4 * g] + bn;
+                    int a = 0;
+#pragma unroll
+                    for (int d = 1; d < 4; ++d) {
+                        const float v = acc[i][j][4 * g + d] + bn;
+                        if (v > best) {
+                            best = v;
+                            a = d;
+                        }
+                    }
+                    const int q = m >> 2, nb = q / pool_hw;
+                    const int64_t o = ((int64_t)nb * N + n) * pool_hw + (q - nb * pool_hw);
+                    pool_cur[o] = best;
+                    pool_arg[o] = (uint8_t)a;
+                }
+            }
+        return;
+    }
     float *Cz = C + (int64_t)zk * split_stride;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -686,15 +719,16 @@ Plan16 plan_for(const GemmArgs &g, const Kind &kd) {
     return best;
 }
 
-template <int MT, int SA, bool AK, int SB, bool BKc>
+template <int MT, int SA, bool AK, int SB, bool BKc, bool POOL = false>
 void launch16(const GemmArgs &g, const Plan16 &p, const void *A, int64_t a_ps, const void *B,
               int64_t b_ps, float *out, int64_t ldo, int64_t ss, const float *bias, hipStream_t s) {
     dim3 grid((unsigned)(p.tiles_m * p.tiles_n), 1, (unsigned)p.splits);
     const auto *a = reinterpret_cast<const typename SrcTraits<SA>::T *>(A);
     const auto *b = reinterpret_cast<const typename SrcTraits<SB>::T *>(B);
 #define SNN_G16_LAUNCH(BM_, BN_)                                                                \
-    gemm16_kernel<MT, SA, AK, SB, BKc, BM_, BN_><<<grid, kThreads, 0, s>>>(                        \
-        g.M, g.N, g.K, p.k_chunk, p.tiles_n, a, g.lda, a_ps, b, g.ldb, b_ps, out, ldo, ss, bias)
+    gemm16_kernel<MT, SA, AK, SB, BKc, BM_, BN_, POOL><<<grid, kThreads, 0, s>>>(                  \
+        g.M, g.N, g.K, p.k_chunk, p.tiles_n, a, g.lda, a_ps, b, g.ldb, b_ps, out, ldo, ss, bias,   \
+        g.pool_hw, g.pool_cur, g.pool_arg)
     switch (p.shape) {
         case 0: SNN_G16_LAUNCH(128, 128); break;
         case 1: SNN_G16_LAUNCH(128, 64); break;
@@ -721,6 +755,10 @@ hipError_t run16(const GemmArgs &g, const Kind &kd, void *ws, size_t ws_bytes, h
         ss = (int64_t)g.M * g.N;
         bias = nullptr;
     }
+    // the pool epilogue: spikes against fp32 weights (a convolution's
+    // forward), one pass over K, whole windows
+    constexpr bool CAN_POOL = MT == MT_BF16 && SA == SRC_SPIKE && SB == SRC_F32 && AK && BKc;
+    const bool pool = g.pool_hw > 0 && g.pooled && p.splits == 1 && g.M % 4 == 0;
     if constexpr ((SA == SRC_F32 && SB == SRC_SPIKE) || (SB == SRC_F32 && SA == SRC_SPIKE)) {
         if (p.presplit) {
             // the fp32 operand is K-contiguous; its planes get 16-byte rows
@@ -739,7 +777,27 @@ hipError_t run16(const GemmArgs &g, const Kind &kd, void *ws, size_t ws_bytes, h
                 launch16<MT, SRC_PLANES, AK, SB, BKc>(gp, p, planes, n, g.B, 0, out, ldo, ss, bias, s);
             } else {
                 gp.ldb = ldp;
-                launch16<MT, SA, AK, SRC_PLANES, BKc>(gp, p, g.A, 0, planes, n, out, ldo, ss, bias, s);
+                if constexpr (CAN_POOL) {
+                    if (pool) {
+                        launch16<MT, SA, AK, SRC_PLANES, BKc, true>(gp, p, g.A, 0, planes, n, out,
+                                                                    ldo, ss, bias, s);
+                        *g.pooled = true;
+                    } else {
+                        launch16<MT, SA, AK, SRC_PLANES, BKc>(gp, p, g.A, 0, planes, n, out, ldo,
+                                                              ss, bias, s);
+                    }
+                } else {
+                    launch16<MT, SA, AK, SRC_PLANES, BKc>(gp, p, g.A, 0, planes, n, out, ldo, ss,
+                                                          bias, s);
+                }
+            }
+        } else if constexpr (CAN_POOL) {
+            if (pool) {
+                launch16<MT, SA, AK, SB, BKc, true>(g, p, g.A, g.a_ps, g.B, g.b_ps, out, ldo, ss,
+                                                    bias, s);
+                *g.pooled = true;
+            } else {
+                launch16<MT, SA, AK, SB, BKc>(g, p, g.A, g.a_ps, g.B, g.b_ps, out, ldo, ss, bias, s);
             }
         } else {
             launch16<MT, SA, AK, SB, BKc>(g, p, g.A, g.a_ps, g.B, g.b_ps, out, ldo, ss, bias, s);

@@ -96,6 +96,15 @@ struct GemmArgs {
     const float *bias;  // [N] or NULL
     bool allow_split;   // may run on 16-bit MFMA as exact multi-part passes
     int64_t a_ps = 0, b_ps = 0;  // plane strides (elements) of kPlanes3 operands
+    // 2x2 max-pool epilogue (convolution forward): rows m = 4 q + d are the
+    // four window positions of pooled cell q.  A contraction that can pool
+    // its own output (one pass over K, no split) writes the first maximum
+    // (C + bias) to pool_cur[(q / pool_hw) * N + n][q % pool_hw] and its d to
+    // pool_arg instead of C, and sets *pooled; otherwise C is written.
+    int pool_hw = 0;
+    float *pool_cur = nullptr;
+    uint8_t *pool_arg = nullptr;
+    bool *pooled = nullptr;
 };
 size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype, bool a_kc,
                             bool b_kc, bool allow_split);

@@ -394,8 +394,11 @@ def _conv_fwd_gpu(d, x, w, b):
     return _np(cur), _np(arg)
 
 
+# (800, 12, 12, 12, 64): 51200 conv rows, one pass over K, so the contraction
+# pools its own output; (5, 12, 12, 12, 64) is split over K and pooled after
 @pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (5, 12, 12, 12, 64), (2, 3, 9, 11, 5),
-                                          (1, 2, 6, 6, 2)])
+                                          (1, 2, 6, 6, 2), (800, 12, 12, 12, 64),
+                                          (300, 3, 15, 13, 70)])
 def test_conv_pool_fwd(NB, Ci, H, W, Co):
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=NB * 100 + Co)
     _check_conv_fwd(x, w, b, d)
