@@ -122,6 +122,53 @@ __global__ __launch_bounds__(kThreads) void im2col_kernel(int Mw, int Kc, int ld
     *reinterpret_cast<uint4 *>(col + m * ldk + k0) = ch.v;
 }
 
+// The same gather with a workgroup per image: the image and a table of the
+// x offsets of every k ((c * H + ky) * W + kx) are staged in LDS, so an
+// element costs a table read, an add and an LDS read instead of the
+// divisions that decompose k (and a global load).  For images of at most
+// 16 KiB and Kc <= 1024.
+constexpr int kIm2colLdsBytes = 16384;
+constexpr int kIm2colMaxK = 1024;
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void im2col_lds_kernel(int Kc, int ldk, int Ci, int H, int W,
+                                                              int Hp, int Wp, const T *__restrict__ x,
+                                                              T *__restrict__ col) {
+    constexpr int N = Chunk<T>::N;
+    __shared__ __attribute__((aligned(16))) T xs[kIm2colLdsBytes / sizeof(T)];
+    __shared__ __attribute__((aligned(16))) uint16_t off[kIm2colMaxK];
+    const int img = Ci * H * W;
+    const T *xi = x + (int64_t)blockIdx.x * img;
+    for (int i = threadIdx.x; i < img; i += kThreads) xs[i] = xi[i];
+    for (int k = threadIdx.x; k < ldk; k += kThreads) {
+        const int kk = min(k, Kc - 1);  // padding columns read a valid element, stored as 0
+        const int c = kk / (KS * KS), t = kk - c * KS * KS, ky = t / KS, kx = t - ky * KS;
+        off[k] = (uint16_t)((c * H + ky) * W + kx);
+    }
+    __syncthreads();
+    const int rows = 4 * Hp * Wp, cpr = ldk / N;
+    T *colb = col + (int64_t)blockIdx.x * rows * ldk;
+    for (int idx = threadIdx.x; idx < rows * cpr; idx += kThreads) {
+        const int r = idx / cpr, k0 = (idx - r * cpr) * N;
+        const int q = r >> 2, d = r & 3, py = q / Wp, px = q - py * Wp;
+        const int base = (2 * py + (d >> 1)) * W + 2 * px + (d & 1);
+        uint16_t o[N];
+#pragma unroll
+        for (int h = 0; h < N / 4; ++h) {
+            const uint2 v = *reinterpret_cast<const uint2 *>(off + k0 + 4 * h);
+            o[4 * h] = (uint16_t)(v.x & 0xffffu); o[4 * h + 1] = (uint16_t)(v.x >> 16);
+            o[4 * h + 2] = (uint16_t)(v.y & 0xffffu); o[4 * h + 3] = (uint16_t)(v.y >> 16);
+        }
+        Chunk<T> ch;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const T e = xs[base + o[i]];
+            ch.e[i] = (k0 + i < Kc) ? e : T(0);
+        }
+        *reinterpret_cast<uint4 *>(colb + (int64_t)r * ldk + k0) = ch.v;
+    }
+}
+
 // col^T[k][m0 .. m0 + N): one thread per 16-byte chunk, N/4 whole windows
 // (their four positions are x offsets 0, 1, W, W + 1); m >= Mw is 0.
 template <typename T>
@@ -504,6 +551,12 @@ BwdLayout bwd_layout(const ConvGeom &g, const ConvDims &v, int in_dtype, bool al
 
 template <typename T>
 void launch_im2col(const ConvGeom &g, const ConvDims &v, const void *x, void *col, hipStream_t s) {
+    if ((int64_t)g.Ci * g.H * g.W * (int64_t)sizeof(T) <= kIm2colLdsBytes && v.ldk <= kIm2colMaxK) {
+        im2col_lds_kernel<T><<<(unsigned)g.NB, kThreads, 0, s>>>(
+            v.Kc, (int)v.ldk, g.Ci, g.H, g.W, g.Hp, g.Wp, reinterpret_cast<const T *>(x),
+            reinterpret_cast<T *>(col));
+        return;
+    }
     const int64_t n = v.Mw * (v.ldk / Chunk<T>::N);
     im2col_kernel<T><<<blocks(n), kThreads, 0, s>>>((int)v.Mw, v.Kc, (int)v.ldk, g.Ci, g.H, g.W,
                                                     g.Hp, g.Wp, reinterpret_cast<const T *>(x),
