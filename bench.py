@@ -463,7 +463,10 @@ def _stage_kernels(net, name, li, fp32_mfma):
         g = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"
         pool = (" pooling in its epilogue (+ pool_kernel when split over K)" if kind == "mfma16"
                 else " + pool_kernel")
-        return f": im2col_kernel + {g}{pool} (the whole stage is timed)"
+        d = net.descs[li]
+        gather = ("im2col_lds_kernel" if d.c_in * d.h_in * d.w_in <= 16384 and d.c_in * 25 <= 1008
+                  else "im2col_kernel")
+        return f": {gather} + {g}{pool} (the whole stage is timed)"
     if kind == "mfma16" and passes == 3:
         return (": gemm16_kernel, 3 exact bf16 passes (+ split_planes_kernel when the weights"
                 " are split into planes up front, + splitk_reduce_kernel when split over K)")
