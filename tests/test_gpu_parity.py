@@ -461,7 +461,9 @@ def test_conv_pool_ties_first_maximum():
     assert (a[0] == 0).all()
 
 
-@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (4, 12, 12, 12, 64), (2, 3, 9, 11, 5)])
+# (3, 8, 11, 12, 16): an odd conv row outside every window
+@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (4, 12, 12, 12, 64), (2, 3, 9, 11, 5),
+                                          (3, 8, 11, 12, 16), (300, 12, 12, 12, 64)])
 def test_conv_pool_bwd(NB, Ci, H, W, Co):
     """Backward given the oracle's pool selection (one byte per pooled current)."""
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=7 * NB + Co)
