@@ -60,28 +60,6 @@ ConvDims dims_of(const ConvGeom &g) {
     return v;
 }
 
-// conv output coordinates of GEMM row m
-struct RowPos {
-    int64_t nb;
-    int oy, ox;
-};
-__device__ inline RowPos row_pos(int64_t m, int Hp, int Wp) {
-    const int64_t q = m >> 2;
-    const int d = (int)(m & 3);
-    const int64_t hw = (int64_t)Hp * Wp;
-    const int p = (int)(q % hw);
-    RowPos r;
-    r.nb = q / hw;
-    r.oy = 2 * (p / Wp) + (d >> 1);
-    r.ox = 2 * (p % Wp) + (d & 1);
-    return r;
-}
-
-__device__ inline int64_t x_index(const RowPos &r, int k, int Ci, int H, int W) {
-    const int c = k / (KS * KS), t = k % (KS * KS);
-    return ((r.nb * Ci + c) * H + r.oy + t / KS) * W + r.ox + t % KS;
-}
-
 // 16 bytes of T, built element by element
 template <typename T>
 struct Chunk {

@@ -114,39 +114,11 @@ __device__ inline uint32_t lds_addr(const uint16_t *p) {
 
 // The fragment reads are issued as asm: the compiler's own wait insertion
 // cannot tell the stages apart and would wait for every copy in flight
-// before any LDS read.  The asm waits below name the fragments as operands,
-// so no MFMA that uses them is scheduled before the data has arrived (LDS
-// returns in order: lgkmcnt(8) means the older 8 reads are done).
+// before any LDS read.  The asm waits in multiply_stage name the fragments
+// as operands, so no MFMA that uses them is scheduled before the data has
+// arrived (LDS returns in order).
 __device__ inline void lds_read(u32x4 &v, uint32_t addr) {
     asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
-}
-__device__ inline void wait_lgkm6(u32x4 (&a)[4], u32x4 (&b)[2]) {
-    asm volatile("s_waitcnt lgkmcnt(6)"
-                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]));
-}
-__device__ inline void wait_lgkm0(u32x4 (&a)[4], u32x4 (&b)[2]) {
-    asm volatile("s_waitcnt lgkmcnt(0)"
-                 : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]), "+v"(b[0]), "+v"(b[1]));
-}
-
-// Fragments of 32 rows x 8 k (one 16-byte chunk per lane) of k16 step ks
-// for F row blocks of 32 starting at row0, from a stage.
-template <int F>
-__device__ inline void read_fragments(const uint16_t *stage, int row0, int ks, u32x4 (&f)[F]) {
-    const int lane = threadIdx.x & 63;
-    const int c = 2 * ks + (lane >> 5);
-#pragma unroll
-    for (int i = 0; i < F; ++i) {
-        const int r = row0 + i * 32 + (lane & 31);
-        lds_read(f[i], lds_addr(stage + r * kKT + (c ^ swz(r)) * 8));
-    }
-}
-
-// chunks past K (the last k-tile) read as 0
-template <int F>
-__device__ inline void mask_fragments(u32x4 (&f)[F], uint32_t mask) {
-#pragma unroll
-    for (int i = 0; i < F; ++i) f[i] &= mask;
 }
 
 // LDS address of fragment i of k16 step ks: A fragments i = 0..3 (rows
