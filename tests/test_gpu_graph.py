@@ -32,7 +32,9 @@ def _outputs(net):
                                             ("csnn_t25_b128", 5, 4, None),
                                             ("dsnn_rleaky_t25_b128", 10, 8, 200),
                                             ("pop_dsnn_t1_b128", 1, 32, None),
-                                            ("scan_wide_t1000_b64", 50, 4, 2000)])
+                                            ("scan_wide_t1000_b64", 50, 4, 2000),
+                                            # the benchmark's default network at full size
+                                            ("dsnn_synaptic_t50_b256", 50, 256, None)])
 def test_graph_replay_matches_eager(name, T, B, width):
     wl = wls.scaled(wls.get(name), T=T, B=B, width=width)
     lab = tgt = None
