@@ -304,11 +304,11 @@ bool few_rows_mfma_ok(const GemmArgs &g) {
 }
 
 // Chunks of rows: about two workgroups per compute unit, the partial sums
-// kept under 4 MiB, at least 32 rows per chunk.
+// kept under 8 MiB, at least 32 rows per chunk.
 int few_rows_mfma_chunks(int M, int N, int R) {
     const int64_t strips = (N + 511) / 512;
     int64_t S = 2 * (int64_t)device_cus() / strips;
-    S = S < ((int64_t)4 << 20) / ((int64_t)M * N * 4) ? S : ((int64_t)4 << 20) / ((int64_t)M * N * 4);
+    S = S < ((int64_t)8 << 20) / ((int64_t)M * N * 4) ? S : ((int64_t)8 << 20) / ((int64_t)M * N * 4);
     S = S < (R + 31) / 32 ? S : (R + 31) / 32;
     return S < 1 ? 1 : (int)S;
 }
