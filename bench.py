@@ -189,7 +189,7 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
@@ -256,9 +256,12 @@ def main():
             if n1 == n0 + "_end" and l1 == l0:
                 key = f"{n0}[L{l0}]" if l0 >= 0 else n0
                 split[key] = split.get(key, 0.0) + e0.elapsed_time(e1) / split_steps
-        # candidates: stages that launch exactly one kernel in this build
+        # candidates: stages that launch one kernel (or one contraction); of
+        # those within 10 % of the longest, the first in step order, so that
+        # two near-equal stages do not trade places from run to run
         single = {k: v for k, v in split.items() if _single_kernel_stage(net, k)}
-        dom_key = max(single, key=single.get)
+        longest = max(single.values())
+        dom_key = next(k for k, v in single.items() if v >= 0.9 * longest)
         dom_name, dom_li = dom_key.split("[L")[0], int(dom_key.split("[L")[1].rstrip("]"))
 
         # timed region: K steps, events around the dominant kernel's launch

@@ -71,7 +71,7 @@ typedef enum snn_status {
     SNN_ERR_SHAPE = 2,       /* sizes negative, inconsistent or too large */
     SNN_ERR_DTYPE = 3,       /* dtype / format combination not supported */
     SNN_ERR_ALIGN = 4,       /* a device pointer is not 16-byte aligned */
-    SNN_ERR_UNSUPPORTED = 5, /* valid request this build does not implement */
+    SNN_ERR_UNSUPPORTED = 5, /* a valid request the library does not implement */
     SNN_ERR_WORKSPACE = 6,   /* ws_bytes smaller than the query returned */
     SNN_ERR_HIP = 7          /* a kernel launch failed */
 } snn_status;

@@ -240,7 +240,7 @@ const char *snn_status_str(snn_status s) {
         case SNN_ERR_SHAPE: return "invalid or inconsistent sizes";
         case SNN_ERR_DTYPE: return "unsupported dtype combination";
         case SNN_ERR_ALIGN: return "device pointer not 16-byte aligned";
-        case SNN_ERR_UNSUPPORTED: return "not supported by this build";
+        case SNN_ERR_UNSUPPORTED: return "not supported by this library";
         case SNN_ERR_WORKSPACE: return "workspace too small";
         case SNN_ERR_HIP: return "HIP launch failed";
     }
