@@ -5,13 +5,17 @@ A step is one forward + BPTT pass of the whole spiking network over one batch
 of synthetic rate-coded input (synapse and neuron scan per layer, loss on the
 output spike counts, then the reverse scan and weight/input gradients per
 layer), the quantity the paper times per minibatch (Sec. IV, "Baseline
-Throughput") minus the optimizer update.  Default workload: dense
-784-1000-10 with current-based neurons (eqs. 5-6), alpha 0.9, beta 0.8,
-T = 50, batch 256, fp32.
+Throughput") minus the optimizer update.  Default workload: the largest
+network, dense 784-4096-4096-10 with Leaky neurons (beta 0.9), T = 100,
+batch 512, fp16 weights and spikes with fp32 accumulation and fp32 membrane
+state; after it, in the same run, the scan-bound wide layer (65536 Leaky
+neurons driven by given currents, T = 1000, batch 64).
 
 Prints one JSON line: samples/s over the timed steps, the roofline of the
-dominant kernel (timed with HIP events on its own stream inside the timed
-region), the per-stage time split, and the CPU oracle timed on this host.
+stage that takes the most time per step (any stage of the step, forward or
+backward; timed with HIP events on the step's stream inside the timed
+region), the per-stage time split, the CPU oracle timed on this host, and the
+scan-bound layer's own figures under "scan_wide".
 """
 from __future__ import annotations
 
@@ -34,6 +38,8 @@ PEAK_FP32_MFMA_TFLOPS = 157.3  # MI355X dense fp32 matrix
 # lanes x 2 flops x 2.4 GHz (the packed-fp32 rate, 157.3, is not used)
 PEAK_FP32_VALU_TFLOPS = 78.6
 PEAK_FP16_MFMA_TFLOPS = 2500.0
+DEFAULT_WORKLOAD = "dsnn_half_t100_b512"
+SCAN_WORKLOAD = "scan_wide_t1000_b64"
 
 
 # kernel sources behind each kind of stage (a stored counter profile of a
@@ -74,60 +80,89 @@ def stored_traffic(workload: str, stage_key: str):
     return float(m.group(1))
 
 
+def _dtype_bytes(code):
+    return {0: 4, 1: 2, 2: 2, 3: 1}[code]
+
+
+def _macs(d):
+    """Multiply-adds of a layer's product over all T*B rows (a 5x5 valid conv
+    counts Co x Ci x 25 per conv output, every output)."""
+    TB = d.T * d.B
+    if d.synapse == 1:
+        return TB * (d.h_in - 4) * (d.w_in - 4) * d.c_out * d.c_in * 25
+    return TB * d.n_out * d.n_in
+
+
 def stage_work(net, name, li):
     """Algorithmic work of one stage launch: ('flop', F) for contractions,
     ('byte', Bytes) for scans.  Per-unit figures:
-      contraction  2 M N K flops (one multiply and one add per MAC)
-      forward scan 4 B read current + 4 B write membrane + 1 B write spike per
-                   (t, b, n), + 4 B count per (b, n)
-      reverse scan 4 B read membrane + 4 B read dL/dz (full only) + 4 B write
-                   dL/dI per (t, b, n), + 4 B colsum per (b, n), + 4 B recurrent-
-                   weight column sum per (b, n) for recurrent neurons (eq. 7);
-                   with the readout's input gradient folded in, dL/dz is not
-                   read but computed from the readout's dL/dI (4 B per
-                   (t, b, readout neuron)), and the readout's synapse
-                   backward computes dW only."""
+      contraction  2 M N K flops (one multiply and one add per MAC); the
+                   synapse backward of a dense layer is two stages, dW
+                   (K = T*B) and dx (K = n_out), each 2 M N K; a conv layer's
+                   backward is one stage with both
+      forward scan 4 B read current + 4 B write membrane + s B write spike
+                   per (t, b, n) (s = 1 for bytes, 2 for fp16 spikes), + 4 B
+                   count per (b, n) of the layer that counts
+      reverse scan 4 B read membrane + 4 B read dL/dz (full upstream gradient
+                   only) + w B write dL/dI per (t, b, n) (w = 4 for fp32, 2 for
+                   a 16-bit gradient operand), + 4 B colsum per (b, n), + 4 B
+                   recurrent-weight column sum per (b, n) for recurrent
+                   neurons (eq. 7); with the readout's input gradient folded
+                   in, dL/dz is not read but computed from the readout's
+                   dL/dI (its operand bytes per (t, b, readout neuron))"""
     d = net.descs[li]
     TB = d.T * d.B
-    if d.synapse == 1:
-        # 5x5 valid conv: Co x Ci x 25 MACs per conv output, all outputs
-        macs = TB * (d.h_in - 4) * (d.w_in - 4) * d.c_out * d.c_in * 25
-    else:
-        macs = TB * d.n_out * d.n_in
+    macs = _macs(d)
     if name == "synapse_fwd":
         return "flop", 2.0 * macs
+    if name in ("synapse_bwd_dw", "synapse_bwd_dx"):
+        return "flop", 2.0 * macs
     if name == "synapse_bwd":
-        # dW, and dx below the input layer unless the layer below folds it in
-        dx = li > 0 and net.dup[li] is None
+        # conv: dW, and dx below the input layer unless the layer below folds it in
+        dx = li > 0 and net.gx[li] is not None
         return "flop", 2.0 * macs * (2 if dx else 1)
     el = TB * d.n_out
     cols = d.B * d.n_out
     if name == "neuron_fwd":
-        return "byte", 9.0 * el + 4.0 * cols
+        counts = 4.0 * cols if li == len(net.descs) - 1 else 0.0
+        return "byte", (8.0 + _dtype_bytes(d.out_dtype)) * el + counts
     if name == "neuron_bwd":
         rec = 4.0 * cols if d.neuron == 2 else 0.0
+        wr = _dtype_bytes(d.grad_dtype) if d.synapse != 2 else 4.0
+        colsum = 4.0 * cols if d.synapse != 2 else 0.0
         if net.fold[li]:
-            up = 4.0 * TB * net.descs[li + 1].n_out
-            return "byte", 8.0 * el + up + 4.0 * cols + rec
+            up = net.descs[li + 1]
+            return "byte", (4.0 + wr) * el + _dtype_bytes(up.grad_dtype) * TB * up.n_out + \
+                colsum + rec
         full = li < len(net.descs) - 1
-        return "byte", (12.0 if full else 8.0) * el + 4.0 * cols + rec
+        return "byte", (4.0 + (4.0 if full else 0.0) + wr) * el + colsum + rec
     return None, 0.0
 
 
 def run_pmc_mode(net, x, y, tgt, steps):
     """Kernels for counter collection: a 1 GiB device copy (calibration of
-    FETCH_SIZE / WRITE_SIZE against known bytes) and a few training steps."""
+    FETCH_SIZE / WRITE_SIZE against known bytes) and a few training steps
+    through the stage calls.  A one-element fill kernel marks every stage
+    boundary, so a dispatch list can be cut into stages; the stage names are
+    printed in order."""
     import torch
     a = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
     b = torch.empty_like(a)
     a.fill_(1)
     for _ in range(3):
         b.copy_(a)
+    mark = torch.zeros(1, dtype=torch.int32, device="cuda")
+    names = []
+
+    def hook(name, li):
+        mark.fill_(len(names))
+        names.append(f"{name}[L{li}]" if li >= 0 else name)
+
     for _ in range(steps):
-        net.step_stages(x, labels=y, targets=tgt)
+        net.step_stages(x, labels=y, targets=tgt, hook=hook)
     torch.cuda.synchronize()
     print(json.dumps({"pmc_mode": True, "copy_bytes": 2 * (1 << 30), "steps": steps,
-                      "csrc_hash": csrc_hash()}))
+                      "csrc_hash": csrc_hash(), "stage_marks": names}))
 
 
 def macs_per_sample(wl):
@@ -153,18 +188,71 @@ def cpu_baseline(wl, seed, target_macs=3.0e11):
     import oracle
     from paper_2211_10725_amd import workloads as wls
     bs = int(max(1, min(wl.B, round(target_macs / macs_per_sample(wl)))))
+    chunks = 1
     if wl.input == "currents":
-        bs = min(bs, 4)  # host memory: each sample is T x N currents plus fp64 adjoints
+        # host memory: each sample is T x N currents plus fp64 adjoints, so
+        # the scan-only layer runs as steps of 4 samples (samples are
+        # independent), as many as fit in about ten seconds
+        bs, chunks = min(bs, 4), max(1, wl.B // 4)
     ws_ = wls.scaled(wl, B=bs)
-    inp = wls.make_inputs(ws_, seed)
-    t0 = time.perf_counter()
-    oracle.net_step(ws_.layers, inp["params"], inp["x"], ws_.loss, labels=inp.get("labels"),
-                    targets=inp.get("targets"), slope=ws_.slope, pop=ws_.pop)
-    dt = time.perf_counter() - t0
-    return {"value": round(bs / dt, 3), "unit": "samples/s", "cores": oracle.num_threads(),
+    done, dt = 0, 0.0
+    for c in range(chunks):
+        inp = wls.make_inputs(ws_, seed + c)
+        t0 = time.perf_counter()
+        oracle.net_step(ws_.layers, inp["params"], inp["x"], ws_.loss, labels=inp.get("labels"),
+                        targets=inp.get("targets"), slope=ws_.slope, pop=ws_.pop)
+        dt += time.perf_counter() - t0
+        done += bs
+        if dt >= 10.0:
+            break
+    steps = done // bs
+    what = (f"{done} of {wl.B} samples" if steps == 1 else
+            f"{steps} steps of {bs} samples ({done} of {wl.B})")
+    return {"value": round(done / dt, 3), "unit": "samples/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"{bs} of {wl.B} samples of {wl.name} (T={wl.T}), one fwd+BPTT step "
-                      f"in {dt:.2f} s; C oracle, OpenMP, fp64 contractions"}
+            "sample": f"{what} of {wl.name} (T={wl.T}), fwd+BPTT in {dt:.2f} s; C oracle, "
+                      f"OpenMP, fp64 contractions"}
+
+
+def _inputs(wl, seed):
+    import torch
+    from paper_2211_10725_amd import workloads as wls
+    if wl.input == "currents":
+        # 4 bytes x T x B x N: drawn directly in device memory
+        x = wls.device_currents(wl, seed)
+    else:
+        x = torch.as_tensor(wls.spike_input(wl, seed)).to("cuda")
+    y = torch.as_tensor(wls.labels(wl, seed)).cuda() if wl.loss == "ce" else None
+    tgt = torch.as_tensor(wls.targets(wl, seed)).cuda() if wl.loss == "mse" else None
+    return x, y, tgt
+
+
+def _split(net, x, y, tgt, stream, steps, upd=False):
+    """Per-stage time (ms, mean over ``steps`` passes through the stage calls,
+    outside the timed region), keyed "name[Lli]" ("loss", "update")."""
+    import torch
+    evs = []
+
+    def rec(name, li):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        evs.append((name, li, e))
+
+    for _ in range(steps):
+        net.step_stages(x, labels=y, targets=tgt, hook=rec, update=upd)
+    torch.cuda.synchronize()
+    split = {}
+    for (n0, l0, e0), (n1, l1, e1) in zip(evs, evs[1:]):
+        if n1 == n0 + "_end" and l1 == l0:
+            key = f"{n0}[L{l0}]" if l0 >= 0 else n0
+            split[key] = split.get(key, 0.0) + e0.elapsed_time(e1) / steps
+    return split
+
+
+def _parse_key(key):
+    if "[L" not in key:
+        return key, -1
+    return key.split("[L")[0], int(key.split("[L")[1].rstrip("]"))
 
 
 def main():
@@ -172,9 +260,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="dsnn_synaptic_t50_b256")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--scan-leg", choices=["auto", "on", "off"], default="auto",
+                    help="after the main workload, time the scan-bound wide layer in the "
+                         "same run (auto: only with the default workload)")
     ap.add_argument("--mode", choices=["bench", "pmc"], default="bench")
     ap.add_argument("--batch", type=int, default=None,
                     help="run the workload at this batch size (same layers and T)")
@@ -193,7 +284,6 @@ def main():
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
-    import numpy as np
     import torch
 
     import paper_2211_10725_amd as snn
@@ -219,13 +309,7 @@ def main():
         net.init_adamw(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2)
     upd = bool(args.update)
     with torch.cuda.stream(stream):
-        if wl.input == "currents":
-            # 4 bytes x T x B x N: drawn directly in device memory
-            x = wls.device_currents(wl, args.seed)
-        else:
-            x = torch.as_tensor(wls.spike_input(wl, args.seed)).to("cuda")
-        y = torch.as_tensor(wls.labels(wl, args.seed)).cuda() if wl.loss == "ce" else None
-        tgt = torch.as_tensor(wls.targets(wl, args.seed)).cuda() if wl.loss == "mse" else None
+        x, y, tgt = _inputs(wl, args.seed)
     torch.cuda.synchronize()
 
     if args.mode == "pmc":
@@ -238,33 +322,18 @@ def main():
             net.step_stages(x, labels=y, targets=tgt, update=upd, fused_bwd=True)
         torch.cuda.synchronize()
 
-        # per-stage split (one pass, outside the timed region): find the
-        # dominant single-kernel stage
-        evs = []
+        # per-stage split (untimed passes through the stage calls): the
+        # roofline stage is the one that takes the most time per step, over
+        # every stage of the step
+        split = _split(net, x, y, tgt, stream, 5, upd)
+        cand = {k: v for k, v in split.items() if k != "update"}
+        dom_key = max(cand, key=cand.get)
+        dom_name, dom_li = _parse_key(dom_key)
+        # the backward of the layer holding the roofline stage runs as stage
+        # calls (the same kernels in the same order as its one layer call),
+        # so that events can bracket that stage
+        staged = (dom_li,) if dom_name.startswith(("neuron_bwd", "synapse_bwd")) else ()
 
-        def rec(name, li):
-            e = torch.cuda.Event(enable_timing=True)
-            e.record(stream)
-            evs.append((name, li, e))
-
-        split_steps = 5
-        for _ in range(split_steps):
-            net.step_stages(x, labels=y, targets=tgt, hook=rec, update=upd)
-        torch.cuda.synchronize()
-        split = {}
-        for (n0, l0, e0), (n1, l1, e1) in zip(evs, evs[1:]):
-            if n1 == n0 + "_end" and l1 == l0:
-                key = f"{n0}[L{l0}]" if l0 >= 0 else n0
-                split[key] = split.get(key, 0.0) + e0.elapsed_time(e1) / split_steps
-        # candidates: stages that launch one kernel (or one contraction); of
-        # those within 10 % of the longest, the first in step order, so that
-        # two near-equal stages do not trade places from run to run
-        single = {k: v for k, v in split.items() if _single_kernel_stage(net, k)}
-        longest = max(single.values())
-        dom_key = next(k for k, v in single.items() if v >= 0.9 * longest)
-        dom_name, dom_li = dom_key.split("[L")[0], int(dom_key.split("[L")[1].rstrip("]"))
-
-        # timed region: K steps, events around the dominant kernel's launch
         kev = []
 
         def rec_dom(name, li):
@@ -285,7 +354,7 @@ def main():
                 marks[i + 1].record(stream)
             torch.cuda.synchronize()
             # graph replays cannot host events between their kernels: the
-            # dominant stage is timed in eager steps right after them
+            # roofline stage is timed in eager steps right after them
             for _ in range(min(args.steps, 20)):
                 net.step_stages(x, labels=y, targets=tgt, hook=rec_dom)
             torch.cuda.synchronize()
@@ -293,10 +362,9 @@ def main():
             torch.cuda.synchronize()
             marks[0].record(stream)
             for i in range(args.steps):
-                # layer calls for the backward (the stage split above is only
-                # needed to find the dominant stage)
+                # stage calls forward, one layer call per layer backward
                 net.step_stages(x, labels=y, targets=tgt, hook=rec_dom, update=upd,
-                                fused_bwd=True)
+                                fused_bwd=True, staged=staged)
                 marks[i + 1].record(stream)
             torch.cuda.synchronize()
         total_ms = marks[0].elapsed_time(marks[-1])
@@ -306,41 +374,26 @@ def main():
 
     ms_per_step = total_ms / args.steps
     value = wl.B * args.steps / (total_ms / 1000.0)
-    kind, work = stage_work(net, dom_name, dom_li)
-    if kind == "flop":
-        achieved = work / (k_avg_ms / 1000.0) / 1e12
-        ckind, passes = _contraction_kind(net, dom_li, args.fp32_mfma)
-        if ckind == "valu":
-            roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_VALU_TFLOPS,
-                    "unit": "TFLOP/s", "peak_basis": "fp32 fma on the vector ALUs, no packed math"}
-        else:
-            if ckind == "mfma16":
-                peak, basis = PEAK_FP16_MFMA_TFLOPS, "bf16/fp16 dense MFMA"
-            else:
-                peak, basis = PEAK_FP32_MFMA_TFLOPS, "fp32 dense MFMA"
-            roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
-                    "unit": "TFLOP/s", "peak_basis": basis, "mfma_passes": passes,
-                    "executed_mfma_frac": round(passes * achieved / peak, 4)}
-    else:
-        achieved = work / (k_avg_ms / 1000.0) / 1e9
-        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
-                "unit": "GB/s"}
-    roof["frac"] = round(achieved / roof["peak"], 4)
-    tr = stored_traffic(wl.name, dom_key)
-    roof["traffic"] = tr
+    roof = _roofline(net, dom_name, dom_li, k_avg_ms, args.fp32_mfma)
+    roof["traffic"] = stored_traffic(wl.name, dom_key)
     roof["kernel"] = dom_key + _stage_kernels(net, dom_name, dom_li, args.fp32_mfma)
     roof["avg_launch_ms"] = round(k_avg_ms, 5)
+    roof["share_of_step"] = round(cand[dom_key] / sum(cand.values()), 4)
     if args.graph:
         roof["timed"] = "eager steps right after the graph replays"
-    roof["algorithmic_per_launch"] = work
-
+    half = wl.dtype == "f16"
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "samples/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "f16" if wl.dtype == "f16" else "f32", "data": "synthetic",
+        "dtype": "f16" if half else "f32", "data": "synthetic",
         "config": {"workload": wl.name, "description": wl.description, "T": wl.T,
                    "batch": wl.B, "layers": [_layer_str(s) for s in wl.layers],
+                   "precision": ("fp16 weights and spikes, fp32 MFMA accumulation, fp32 "
+                                 "currents and membrane state, 16-bit dL/dI operand of the "
+                                 "backward contractions, fp32 weight gradients") if half else
+                                ("fp32 weights, currents, state and gradients; products "
+                                 "exact, fp32 accumulation"),
                    "surrogate_slope": wl.slope, "input": "Bernoulli rate-coded spikes"
                    if wl.input == "spikes" else "normal currents",
                    "includes": "forward + loss + BPTT backward + fused AdamW update"
@@ -366,11 +419,89 @@ def main():
     syn = sum(v for k, v in split.items() if k.startswith("synapse"))
     neu = sum(v for k, v in split.items() if k.startswith("neuron"))
     out["spiking_vs_synaptic_ms"] = {"neuron_scans": round(neu, 5), "contractions": round(syn, 5)}
+    del net, x
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
-        del net, x
-        torch.cuda.empty_cache()
         out["cpu_baseline"] = cpu_baseline(wl, args.seed)
+    scan_leg = args.scan_leg == "on" or (args.scan_leg == "auto" and
+                                         args.workload == DEFAULT_WORKLOAD and
+                                         args.batch is None and not args.graph)
+    if scan_leg:
+        out["scan_wide"] = scan_wide_leg(args, stream)
     print(json.dumps(out), flush=True)
+
+
+def scan_wide_leg(args, stream):
+    """The scan-bound workload in the same run, after the main workload's
+    buffers are freed: one Leaky layer of 65536 neurons on given currents
+    [T=1000, B=64], forward scan, MSE loss on the counts, reverse scan.  Its
+    kernels are HBM-bound; each scan is reported against its algorithmic
+    bytes."""
+    import torch
+
+    import paper_2211_10725_amd as snn
+    from paper_2211_10725_amd import workloads as wls
+    wl = wls.get(SCAN_WORKLOAD)
+    net = snn.Network(wl, wls.init_params(wl, args.seed), device="cuda")
+    steps, warm = max(2, min(args.steps, 10)), 2
+    with torch.cuda.stream(stream):
+        x, y, tgt = _inputs(wl, args.seed)
+        for _ in range(warm):
+            net.step_stages(x, labels=y, targets=tgt, fused_bwd=True)
+        torch.cuda.synchronize()
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        marks[0].record(stream)
+        for i in range(steps):
+            net.step_stages(x, labels=y, targets=tgt, fused_bwd=True)
+            marks[i + 1].record(stream)
+        torch.cuda.synchronize()
+        total_ms = marks[0].elapsed_time(marks[-1])
+        split = _split(net, x, y, tgt, stream, 3)
+    el = wl.T * wl.B * wl.layers[0]["n"]
+    scans = {}
+    for key in ("neuron_fwd[L0]", "neuron_bwd[L0]"):
+        name, li = _parse_key(key)
+        _, nbytes = stage_work(net, name, li)
+        gbs = nbytes / (split[key] / 1000.0) / 1e9
+        scans[key] = {"ms": round(split[key], 4), "GB/s": round(gbs, 1),
+                      "frac": round(gbs / PEAK_HBM_GBS, 4),
+                      "bytes_per_element": round(nbytes / el, 4),
+                      "kernel": _stage_kernels(net, name, li, False).lstrip(": ")}
+    out = {"workload": wl.name, "description": wl.description, "steps": steps,
+           "warmup": warm, "ms_per_step": round(total_ms / steps, 5),
+           "value": round(wl.B * steps / (total_ms / 1000.0), 1), "unit": "samples/s",
+           "dtype": "f32", "stage_ms": {k: round(v, 5) for k, v in split.items()},
+           "scan_roofline": scans}
+    del net, x
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, args.seed)
+    return out
+
+
+def _roofline(net, name, li, ms, fp32_mfma):
+    kind, work = stage_work(net, name, li)
+    if kind == "flop":
+        achieved = work / (ms / 1000.0) / 1e12
+        ckind, passes = _contraction_kind(net, li, fp32_mfma, name)
+        if ckind == "valu":
+            roof = {"bound": "alu", "achieved": round(achieved, 3), "peak": PEAK_FP32_VALU_TFLOPS,
+                    "unit": "TFLOP/s", "peak_basis": "fp32 fma on the vector ALUs, no packed math"}
+        else:
+            if ckind == "mfma16":
+                peak, basis = PEAK_FP16_MFMA_TFLOPS, "bf16/fp16 dense MFMA"
+            else:
+                peak, basis = PEAK_FP32_MFMA_TFLOPS, "fp32 dense MFMA"
+            roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
+                    "unit": "TFLOP/s", "peak_basis": basis, "mfma_passes": passes,
+                    "executed_mfma_frac": round(passes * achieved / peak, 4)}
+    else:
+        achieved = work / (ms / 1000.0) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s"}
+    roof["frac"] = round(achieved / roof["peak"], 4)
+    roof["algorithmic_per_launch"] = work
+    return roof
 
 
 def _stage_rooflines(net, split, fp32_mfma):
@@ -381,10 +512,10 @@ def _stage_rooflines(net, split, fp32_mfma):
     for key, ms in split.items():
         if "[L" not in key or ms <= 0:
             continue
-        name, li = key.split("[L")[0], int(key.split("[L")[1].rstrip("]"))
+        name, li = _parse_key(key)
         kind, work = stage_work(net, name, li)
         if kind == "flop":
-            ck, _ = _contraction_kind(net, li, fp32_mfma)
+            ck, _ = _contraction_kind(net, li, fp32_mfma, name)
             peak = {"mfma16": PEAK_FP16_MFMA_TFLOPS, "valu": PEAK_FP32_VALU_TFLOPS}.get(
                 ck, PEAK_FP32_MFMA_TFLOPS)
             a = work / (ms / 1000.0) / 1e12
@@ -395,27 +526,53 @@ def _stage_rooflines(net, split, fp32_mfma):
     return out
 
 
-def _contraction_kind(net, li, fp32_mfma):
-    """How the library contracts layer li's forward product (mirrors the
-    operand classification in gemm_mfma16.hip): ('mfma16', passes) or
-    ('mfma32', 1).  A conv layer's product has one row per conv output that a
+# exact 16-bit parts of an operand type on the matrix cores (mirrors the
+# operand classification in gemm_mfma16.hip): spikes, bf16 and fp16 (against
+# fp16 or spikes) are one part, fp32 three bf16 parts, fp16 against a bf16
+# operand two bf16 parts
+def _parts(dt, other):
+    if dt == 0:
+        return 3
+    if dt == 1 and other == 2:
+        return 2
+    return 1
+
+
+def _contraction_kind(net, li, fp32_mfma, stage="synapse_fwd"):
+    """How the library runs a contraction of layer li: ('mfma16', passes),
+    ('mfma32', 1) or ('valu', 1).  Mirrors the routing in gemm.hip, api.hip
+    and conv.hip.  A conv layer's product has one row per conv output that a
     pool window reads and one column per output channel."""
     d = net.descs[li]
-    if _direct_conv(net, li):
-        return "valu", 1
-    if _narrow_contraction(net, li, fp32_mfma):
-        return "mfma16", 3 if d.w_dtype == 0 else 1
-    if d.synapse == 1:
-        rows = 4 * d.T * d.B * ((d.h_in - 4) // 2) * ((d.w_in - 4) // 2)
-        cols = d.c_out
-    else:
-        rows, cols = d.T * d.B, d.n_out
-    wide = rows >= 64 and cols >= 64
-    if fp32_mfma or not wide or d.in_dtype != 3:
-        return "mfma32", 1
-    if d.w_dtype == 0:
-        return "mfma16", 3   # fp32 weights: three exact bf16 parts
-    return "mfma16", 1       # fp16 weights: one fp16 pass
+    if stage == "synapse_fwd":
+        if _direct_conv(net, li):
+            return "valu", 1
+        if _narrow_contraction(net, li, fp32_mfma):
+            return "mfma16", 3 if d.w_dtype == 0 else 1
+        if d.synapse == 1:
+            rows = 4 * d.T * d.B * ((d.h_in - 4) // 2) * ((d.w_in - 4) // 2)
+            cols = d.c_out
+        else:
+            rows, cols = d.T * d.B, d.n_out
+        wide = rows >= 64 and cols >= 64
+        if fp32_mfma or not wide or d.in_dtype != 3:
+            return "mfma32", 1
+        return "mfma16", _parts(d.w_dtype, 3)
+    if stage == "synapse_bwd_dw":
+        # dW = dI^T x: dL/dI (grad_dtype) against the layer's input
+        if fp32_mfma:
+            return "mfma32", 1
+        a, b = d.grad_dtype, d.in_dtype
+        p = _parts(a, b) * _parts(b, a)
+        return ("mfma16", p) if p <= 6 else ("mfma32", 1)
+    if stage == "synapse_bwd_dx":
+        if fp32_mfma:
+            return "mfma32", 1
+        a, b = d.grad_dtype, d.w_dtype
+        p = _parts(a, b) * _parts(b, a)
+        return ("mfma16", p) if p <= 6 else ("mfma32", 1)
+    # conv backward: dW on the 16-bit cores (three planes of dC), dx on fp32 MFMA
+    return "mfma32", 1
 
 
 def _direct_conv(net, li):
@@ -435,38 +592,68 @@ def _narrow_contraction(net, li, fp32_mfma):
     return (d.in_dtype == 3 and d.w_dtype in (0, 1)) or (d.in_dtype == 1 and d.w_dtype == 1)
 
 
+def _async_ok(a, b, M, N, K):
+    """Mirrors gemm_async_applies in gemm_async.hip (both operands K-contiguous)."""
+    ok_type = (a in (3, 1) and b in (3, 1)) or (a in (3, 2) and b in (3, 2))
+    return ok_type and K % 8 == 0 and K >= 256 and M >= 256 and N >= 256 and M * N * K >= 2 ** 30
+
+
 def _async_contraction(net, li, fp32_mfma):
     """Whether layer li's forward product runs on the asynchronous 256x256
-    kernel (mirrors gemm_async_applies in gemm_async.hip)."""
+    kernel."""
     d = net.descs[li]
     if fp32_mfma or d.synapse != 0:
         return False
-    a, b = d.in_dtype, d.w_dtype
-    ok_type = (a in (3, 1) and b in (3, 1)) or (a in (3, 2) and b in (3, 2))
-    M, N, K = d.T * d.B, d.n_out, d.n_in
-    return ok_type and K % 8 == 0 and K >= 256 and M >= 256 and N >= 256 and M * N * K >= 2 ** 30
+    return _async_ok(d.in_dtype, d.w_dtype, d.T * d.B, d.n_out, d.n_in)
 
 
 def _stage_kernels(net, name, li, fp32_mfma):
     """Kernels a stage enqueues (matched against the rocprofv3 summary)."""
+    d = net.descs[li]
     if name == "neuron_fwd":
         return ": neuron_fwd_kernel"
+    if name == "neuron_bwd" and net.fold[li]:
+        return ": neuron_bwd_kernel (the readout's dx folded in) + bias_reduce_kernel"
     if name == "neuron_bwd":
-        return ": neuron_bwd_kernel"
+        return ": neuron_bwd_kernel" + (" + bias_reduce_kernel" if d.synapse != 2 else "")
+    if name in ("synapse_bwd_dw", "synapse_bwd_dx"):
+        kind, passes = _contraction_kind(net, li, fp32_mfma, name)
+        M, K = d.T * d.B, d.n_out
+        if name == "synapse_bwd_dw":
+            if d.n_out <= 16:
+                return ": few_rows_mfma_kernel / few_rows_kernel + splitk_reduce_kernel"
+            big = 2.0 * M * d.n_in * d.n_out >= 2 ** 30
+            trans = big and not (d.grad_dtype == 0 and d.in_dtype == 3 and M <= 8192)
+            gemm = ("gemm_async_kernel" if trans and passes == 1 and
+                    _async_ok(d.grad_dtype, d.in_dtype, d.n_out, d.n_in, M) else
+                    "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel")
+            pre = ("transpose_kernel (dL/dI^T" + (" as 3 bf16 planes" if d.grad_dtype == 0
+                                                  else "") + ") + transpose_u8_kernel (x^T) + "
+                   if trans else "")
+            return f": {pre}{gemm} ({passes} pass{'es' if passes > 1 else ''}, " \
+                   "+ splitk_reduce_kernel when split over K)"
+        big = 2.0 * M * d.n_in * K >= 2 ** 30
+        gemm = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"
+        pre = "transpose_kernel (W^T) + " if big and kind == "mfma16" else ""
+        return f": {pre}{gemm} ({passes} pass{'es' if passes > 1 else ''}, " \
+               "+ splitk_reduce_kernel when split over K)"
+    if name == "synapse_bwd":
+        return ": unpool_t_kernel + im2col_t_kernel + contractions + col2im_kernel " \
+               "(conv weight and input gradients)"
     if name == "synapse_fwd" and _async_contraction(net, li, fp32_mfma):
-        return ": widen_kernel (spikes to fp16) + gemm_async_kernel"
+        widen = " widen_kernel (spikes to fp16) +" if d.in_dtype == 3 else ""
+        return f":{widen} gemm_async_kernel"
     if name == "synapse_fwd" and _narrow_contraction(net, li, fp32_mfma):
         return ": narrow_fwd_kernel (16 outputs per MFMA tile, weights staged in LDS)"
-    if name == "neuron_bwd" and net.fold[li]:
-        return ": neuron_bwd_kernel (the readout's dx folded in)"
     if name == "synapse_fwd" and _direct_conv(net, li):
         return ": conv1_pool_kernel (convolution and pool in one kernel)"
+    if name == "loss":
+        return ": loss kernels"
     kind, passes = _contraction_kind(net, li, fp32_mfma)
-    if net.descs[li].synapse == 1:
+    if d.synapse == 1:
         g = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"
         pool = (" pooling in its epilogue (+ pool_kernel when split over K)" if kind == "mfma16"
                 else " + pool_kernel")
-        d = net.descs[li]
         gather = ("im2col_lds_kernel" if d.c_in * d.h_in * d.w_in <= 16384 and d.c_in * 25 <= 1008
                   else "im2col_kernel")
         return f": {gather} + {g}{pool} (the whole stage is timed)"
@@ -476,17 +663,6 @@ def _stage_kernels(net, name, li, fp32_mfma):
     if kind == "mfma16":
         return ": gemm16_kernel (+ splitk_reduce_kernel when split over K)"
     return ": gemm_f32_kernel (+ splitk_reduce_kernel when split over K)"
-
-
-def _single_kernel_stage(net, key):
-    """Roofline candidates: stages whose work is one kernel, or one
-    contraction (its weight split and split-K reduce are counted in)."""
-    name, li = key.split("[L")[0], int(key.split("[L")[1].rstrip("]")) if "[L" in key else -1
-    if name in ("neuron_fwd", "synapse_fwd"):
-        return True
-    if name == "neuron_bwd":  # one kernel unless a bias gradient is reduced too
-        return net.descs[li].synapse == 2
-    return False
 
 
 def _layer_str(s):

@@ -448,9 +448,12 @@ class Network:
     # the same work through the stage calls, with a hook between stages
     # (update: finish with the AdamW step of ``init_adamw``; fused_bwd: each
     # layer's backward as one snn_layer_bwd call, hooked as "layer_bwd", as in
-    # ``backward``)
+    # ``backward``, except for the layers listed in ``staged``).  A dense
+    # layer's synapse backward is two stage calls, the weight gradient
+    # ("synapse_bwd_dw") then the input gradient ("synapse_bwd_dx"): the same
+    # kernels in the same order as one snn_synapse_bwd call with both outputs.
     def step_stages(self, x, labels=None, targets=None, stream=None, hook=None, update=False,
-                    fused_bwd=False):
+                    fused_bwd=False, staged=()):
         torch = self.torch
         hook = hook or (lambda name, li: None)
         n = len(self.descs)
@@ -482,7 +485,7 @@ class Network:
                                self.gv[li], self.ws, stream)
                 hook("neuron_bwd_end", li)
                 continue
-            if fused_bwd and self.dup[li] is None:
+            if fused_bwd and self.dup[li] is None and li not in staged:
                 hook("layer_bwd", li)
                 snn_layer_bwd(d, kind, g, xin, self.W[li], self.v[li], self.saved[li],
                               self.gW[li], self.gb[li], self.gv[li], self.gx[li], self.ws, stream)
@@ -506,10 +509,20 @@ class Network:
             snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], dcur, self.gb[li],
                            self.gv[li], rest, stream)
             hook("neuron_bwd_end", li)
-            hook("synapse_bwd", li)
-            snn_synapse_bwd(d, dcur, self.pool_arg(li), xin, self.W[li], self.gW[li], self.gx[li],
-                            rest, stream)
-            hook("synapse_bwd_end", li)
+            if d.synapse == SYN_DENSE:
+                hook("synapse_bwd_dw", li)
+                snn_synapse_bwd(d, dcur, None, xin, self.W[li], self.gW[li], None, rest, stream)
+                hook("synapse_bwd_dw_end", li)
+                if self.gx[li] is not None:
+                    hook("synapse_bwd_dx", li)
+                    snn_synapse_bwd(d, dcur, None, xin, self.W[li], None, self.gx[li], rest,
+                                    stream)
+                    hook("synapse_bwd_dx_end", li)
+            else:
+                hook("synapse_bwd", li)
+                snn_synapse_bwd(d, dcur, self.pool_arg(li), xin, self.W[li], self.gW[li],
+                                self.gx[li], rest, stream)
+                hook("synapse_bwd_end", li)
             if li > 0:
                 kind, g = self._grad_below(li)
         if update:

@@ -1,0 +1,244 @@
+"""The GPU scans against values worked by hand from the paper's equations.
+
+The fixtures under tests/golden/ pin the oracle; here the same hand-worked
+traces run through the library's neuron scans (``snn_neuron_fwd`` /
+``snn_neuron_bwd``) and must reproduce the golden values themselves, not only
+the oracle's.  They hold the method's defining edge case, a membrane exactly
+at threshold: eq. (3) spikes only for u > thr, so L2 (u_1 = 1), S1 (u_2 =
+u_3 = 1), R3 (u_3 = 1) and the fp32 silent boundary (I/(1-beta) = thr, u
+reaches exactly 1.0) must not spike, and the surrogate of eq. (9) there is
+exactly 1.
+
+Each case runs on both lane layouts of the scans: one column per lane
+(a small layer) and four consecutive columns per lane (layers of at least
+2^19 columns).  Every column holds one of the group's traces, interleaved so
+that the four columns of a wide lane hold different traces.
+"""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import paper_2211_10725_amd as snn
+from tests.conftest import GOLDEN
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+# (B, N): 111 columns (one column per lane); 2^19 columns (four per lane)
+LANES = {"narrow": (3, 37), "wide": (8, 65536)}
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+HAND = {c["name"]: c for c in _golden("hand_tables_t4.json")["cases"]}
+GRADS = _golden("hand_gradients_t4.json")["cases"]
+RLK = _golden("hand_rleaky_t4.json")
+RTR = {t["name"]: t for t in RLK["traces"]}
+CLOSED = _golden("closed_form_lif.json")["cases"]
+
+
+def _desc(T, B, N, neuron, beta, alpha=0.0, thr=1.0, slope=25.0, reset=snn.RESET_DETACHED):
+    spec = dict(kind="none", n=N, neuron=neuron, beta=beta, alpha=alpha, thr=thr)
+    return snn.layer_desc(spec, T, B, slope=slope, reset_grad=reset)
+
+
+def _columns(traces, B, N):
+    """[T, B*N] currents with column c holding trace c % len(traces)."""
+    C = B * N
+    idx = np.arange(C) % len(traces)
+    I = np.stack([np.asarray(tr, np.float32) for tr in traces], axis=1)  # [T, ncase]
+    return I[:, idx], idx
+
+
+def _fwd(d, I, v=None):
+    """GPU forward of the scan on currents I [T, B*N]: spikes, membrane, counts."""
+    T, B, N = d.T, d.B, d.n_out
+    x = torch.as_tensor(np.ascontiguousarray(I.reshape(T, B, N))).to(DEV)
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    u = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    cnt = torch.empty((B, N), dtype=torch.float32, device=DEV)
+    vt = None if v is None else torch.as_tensor(np.asarray(v, np.float32)).to(DEV)
+    snn.snn_neuron_fwd(d, x, vt, spk, u, cnt)
+    torch.cuda.synchronize()
+    return (spk.cpu().numpy().reshape(T, -1), u.cpu().numpy().reshape(T, -1),
+            cnt.cpu().numpy().reshape(-1), x, u, vt)
+
+
+def _bwd(d, x, u, g, full, vt=None):
+    """GPU reverse scan: dL/dI [T, B*N] (and dL/dv [N] for the recurrent neuron)."""
+    T, B, N = d.T, d.B, d.n_out
+    gt = torch.as_tensor(np.ascontiguousarray(g, np.float32)).to(DEV)
+    dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    gv = torch.empty(N, dtype=torch.float32, device=DEV) if vt is not None else None
+    ws = torch.empty(max(256, 2 * B * N * 4 + 512), dtype=torch.uint8, device=DEV)
+    snn.snn_neuron_bwd(d, snn.GRAD_FULL if full else snn.GRAD_BCAST, gt, vt, u, dI, None, gv, ws)
+    torch.cuda.synchronize()
+    return dI.cpu().numpy().reshape(T, -1), (None if gv is None else gv.cpu().numpy())
+
+
+# groups of hand-worked traces that share the layer's parameters
+GROUPS = [("leaky", 0.5, 0.0, ["L1", "L2", "L3"]), ("leaky", 0.75, 0.0, ["L4"]),
+          ("synaptic", 0.5, 0.5, ["S1", "S2"])]
+
+
+@pytest.mark.parametrize("lanes", list(LANES))
+@pytest.mark.parametrize("neuron,beta,alpha,names", GROUPS, ids=lambda g: str(g))
+def test_hand_tables_on_gpu(lanes, neuron, beta, alpha, names):
+    B, N = LANES[lanes]
+    cases = [HAND[n] for n in names]
+    I, idx = _columns([c["I"] for c in cases], B, N)
+    z, u, cnt, *_ = _fwd(_desc(4, B, N, neuron, beta, alpha), I)
+    for k, c in enumerate(cases):
+        cols = idx == k
+        want_z = np.array(c["z"], np.uint8)[:, None]
+        np.testing.assert_array_equal(z[:, cols], np.broadcast_to(want_z, z[:, cols].shape),
+                                      err_msg=f"{c['name']} spikes")
+        assert (cnt[cols] == c["count"]).all(), c["name"]
+        want_u = np.array(c["u"], np.float32)[:, None]
+        if c["exact"]:
+            # dyadic values: the fp32 recurrence is exact, ties included
+            np.testing.assert_array_equal(u[:, cols], np.broadcast_to(want_u, u[:, cols].shape),
+                                          err_msg=f"{c['name']} membrane")
+        else:
+            np.testing.assert_allclose(u[:, cols], np.broadcast_to(want_u, u[:, cols].shape),
+                                       rtol=1e-6, err_msg=f"{c['name']} membrane")
+
+
+@pytest.mark.parametrize("lanes", list(LANES))
+@pytest.mark.parametrize("case", GRADS, ids=lambda c: c["name"])
+def test_hand_gradients_on_gpu(lanes, case):
+    """L = sum_t z_t, so dL/dz_t = 1 for every t: the broadcast upstream
+    gradient of a loss on counts."""
+    B, N = LANES[lanes]
+    tr = HAND[case["trace"]]
+    reset = snn.RESET_SURROGATE if case["reset_surrogate"] else snn.RESET_DETACHED
+    d = _desc(4, B, N, tr["neuron"], tr["beta"], tr["alpha"], slope=case["slope"], reset=reset)
+    I, _ = _columns([tr["I"]], B, N)
+    z, u, _, x, ut, _ = _fwd(d, I)
+    np.testing.assert_array_equal(u[:, 0], np.array(tr["u"], np.float32))
+    dI, _ = _bwd(d, x, ut, np.ones((B, N), np.float32), full=False)
+    want = np.array(case["dI"], np.float64)[:, None]
+    assert np.abs(dI - want).max() <= 1e-6, (case["name"], dI[:, 0], want[:, 0])
+    # the surrogate at the tie is exactly 1: with T = 1 the current is the
+    # membrane u_t of the trace and the gradient is s_t itself
+    d1 = _desc(1, B, N, "leaky", tr["beta"], slope=case["slope"], reset=reset)
+    for t, s in enumerate(case["s"]):
+        _, _, _, x1, u1, _ = _fwd(d1, np.full((1, B * N), tr["u"][t], np.float32))
+        g1, _ = _bwd(d1, x1, u1, np.ones((B, N), np.float32), full=False)
+        assert np.abs(g1 - float(Fraction(s))).max() <= 1e-6 * float(Fraction(s)), (t, s)
+        if s == "1":
+            assert (g1 == 1.0).all()
+
+
+@pytest.mark.parametrize("lanes", list(LANES))
+def test_rleaky_hand_traces_on_gpu(lanes):
+    """Eq. (7) traces: self-excitation, inhibition and a tie at threshold
+    (R3, u_3 = 1).  v is one recurrent weight per neuron, so the traces with
+    different v share one layer: neuron n gets trace n % 3."""
+    B, N = LANES[lanes]
+    trs = RLK["traces"]
+    n_idx = np.arange(N) % len(trs)
+    v = np.array([trs[k]["v"] for k in n_idx], np.float32)
+    I = np.stack([np.array(trs[k]["I"], np.float32) for k in n_idx], axis=1)  # [4, N]
+    I = np.tile(I, (1, B))
+    z, u, cnt, *_ = _fwd(_desc(4, B, N, "rleaky", trs[0]["beta"], thr=trs[0]["thr"]), I, v)
+    cols = np.tile(n_idx, B)
+    for k, tr in enumerate(trs):
+        sel = cols == k
+        np.testing.assert_array_equal(
+            u[:, sel], np.broadcast_to(np.array(tr["u"], np.float32)[:, None], u[:, sel].shape))
+        np.testing.assert_array_equal(
+            z[:, sel], np.broadcast_to(np.array(tr["z"], np.uint8)[:, None], z[:, sel].shape))
+        assert (cnt[sel] == sum(tr["z"])).all()
+
+
+@pytest.mark.parametrize("lanes", list(LANES))
+@pytest.mark.parametrize("case", RLK["gradients"], ids=lambda c: c["name"])
+def test_rleaky_hand_gradients_on_gpu(lanes, case):
+    """Per-step upstream gradients (GRAD_FULL) with slope 1 (eq. 9 as
+    printed); dL/dv sums lam_t z_{t-1} over t and the batch."""
+    B, N = LANES[lanes]
+    tr = RTR[case["trace"]]
+    reset = snn.RESET_SURROGATE if case["reset_surrogate"] else snn.RESET_DETACHED
+    d = _desc(4, B, N, "rleaky", tr["beta"], thr=tr["thr"], slope=case["slope"], reset=reset)
+    I, _ = _columns([tr["I"]], B, N)
+    _, u, _, x, ut, vt = _fwd(d, I, np.full(N, tr["v"], np.float32))
+    np.testing.assert_array_equal(u[:, 0], np.array(tr["u"], np.float32))
+    g = np.broadcast_to(np.array(case["g"], np.float32)[:, None, None], (4, B, N))
+    dI, dv = _bwd(d, x, ut, g, full=True, vt=vt)
+    want = np.array([float(Fraction(q)) for q in case["dI"]])[:, None]
+    assert np.abs(dI - want).max() <= 1e-6, (case["name"], dI[:, 0], want[:, 0])
+    # every sample has the same trace: dL/dv is B times the one-sample value
+    want_dv = B * float(Fraction(case["dv"]))
+    assert np.abs(dv - want_dv).max() <= 1e-6 * B, (dv[:4], want_dv)
+
+
+def _closed_form_train(I, beta, thr, T):
+    """Spike steps (1-based) and membrane from the between-spike closed form
+    of eq. (4) under constant input, in double."""
+    spikes, us = [], []
+    t_last, u_last = 0, None
+    for t in range(1, T + 1):
+        if u_last is None:
+            u = I * (1 - beta ** t) / (1 - beta)
+        else:
+            k = t - t_last
+            u = beta ** (k - 1) * (beta * u_last + I - thr) + I * (1 - beta ** (k - 1)) / (1 - beta)
+        us.append(u)
+        if u > thr:
+            spikes.append(t)
+            t_last, u_last = t, u
+    return spikes, np.array(us)
+
+
+@pytest.mark.parametrize("lanes", list(LANES))
+@pytest.mark.parametrize("case", [c for c in CLOSED if c["t1"] is not None],
+                         ids=lambda c: f"I{c['I']}b{c['beta']}")
+def test_closed_form_train_on_gpu(lanes, case):
+    B, N = LANES[lanes]
+    T = 200
+    I, beta, thr = case["I"], case["beta"], case["thr"]
+    z, u, cnt, *_ = _fwd(_desc(T, B, N, "leaky", beta, thr=thr), np.full((T, B * N), I, np.float32))
+    # every column is the same neuron
+    assert (z == z[:, :1]).all() and (u == u[:, :1]).all()
+    got = (np.nonzero(z[:, 0])[0] + 1).tolist()
+    assert got[0] == case["t1"]
+    assert u[case["t1"] - 1, 0] == pytest.approx(case["u_t1"], rel=2e-6)
+    if "u_t1_minus_1" in case:
+        assert u[case["t1"] - 2, 0] == pytest.approx(case["u_t1_minus_1"], rel=2e-6)
+    spikes, us = _closed_form_train(I, beta, thr, T)
+    assert got == spikes
+    np.testing.assert_allclose(u[:, 0], us, rtol=0, atol=2e-5)
+    assert (cnt == len(spikes)).all()
+    if "period" in case:
+        assert all(b - a == case["period"] for a, b in zip(got, got[1:]))
+
+
+@pytest.mark.parametrize("lanes", list(LANES))
+def test_silent_boundary_on_gpu(lanes):
+    """I/(1-beta) == thr: u_t = 1 - 2^-t exactly while representable, then
+    exactly 1.0 (from t = 25 in fp32), and never a spike; the reverse scan sees
+    the surrogate's maximum 1 at those steps."""
+    case = next(c for c in CLOSED if c["t1"] is None)
+    B, N = LANES[lanes]
+    T = 64
+    d = _desc(T, B, N, "leaky", case["beta"], thr=case["thr"])
+    z, u, cnt, x, ut, _ = _fwd(d, np.full((T, B * N), case["I"], np.float32))
+    assert z.sum() == 0 and (cnt == 0).all()
+    for t in range(1, 25):
+        assert (u[t - 1] == np.float32(1.0 - 2.0 ** -t)).all(), t
+    assert (u[24:] == 1.0).all()
+    # g = 1 at the last step only: lam_t = beta^(T-t) s_T ... with s = 1 at u = thr
+    g = np.zeros((T, B, N), np.float32)
+    g[T - 1] = 1.0
+    dI, _ = _bwd(d, x, ut, g, full=True)
+    assert (dI[T - 1] == 1.0).all()
+    want = np.array([case["beta"] ** (T - 1 - t) for t in range(T)])[:, None]
+    np.testing.assert_allclose(dI, np.broadcast_to(want, dI.shape), rtol=1e-6, atol=0)
