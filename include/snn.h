@@ -216,6 +216,19 @@ snn_status snn_loss(int32_t kind, int32_t B, int32_t K, int32_t P, const float *
                     const int32_t *labels, const float *targets, float *loss,
                     float *grad_counts, void *ws, size_t ws_bytes, hipStream_t stream);
 
+/* The same loss for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * no workspace argument; the partial sums live in a 1 MiB device array the
+ * library holds on every device it runs on (until the process ends).  Sizes
+ * whose snn_loss_workspace_bytes exceeds 1 MiB (cross-entropy over more than
+ * 131072 rows) are rejected with SNN_ERR_WORKSPACE; the other checks and
+ * errors are those of snn_loss.  Nothing is allocated and no state carries
+ * over between calls, but every call on one device shares that array: calls
+ * that overlap on one device (two streams, two host threads) race. */
+snn_status snn_loss_noalloc(int32_t kind, int32_t B, int32_t K, int32_t P, const float *counts,
+                            const int32_t *labels, const float *targets, float *loss,
+                            float *grad_counts, hipStream_t stream);
+
 /* ---- weight update ---------------------------------------------------------
  * AdamW, the optimizer the paper trains every network with (Sec. IV): for
  * each parameter tensor, elementwise, with step t >= 1,

@@ -40,7 +40,7 @@ STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE"
 EXPORTS = ["snn_abi_version", "snn_status_str", "snn_layer_saved_bytes",
            "snn_layer_workspace_bytes", "snn_layer_fwd", "snn_layer_bwd",
            "snn_loss_workspace_bytes", "snn_loss", "snn_synapse_fwd", "snn_neuron_fwd",
-           "snn_neuron_bwd", "snn_synapse_bwd", "snn_adamw"]
+           "snn_neuron_bwd", "snn_synapse_bwd", "snn_adamw", "snn_loss_noalloc"]
 
 
 class LayerDesc(ctypes.Structure):
@@ -109,6 +109,7 @@ def lib():
         "snn_layer_bwd": ([D, G, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_loss_workspace_bytes": ([i32, i32, i32], S),
         "snn_loss": ([i32, i32, i32, i32, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_loss_noalloc": ([i32, i32, i32, i32, P, P, P, P, P, P], ctypes.c_int),
         "snn_synapse_fwd": ([D, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_neuron_fwd": ([D, P, P, P, P, P, P], ctypes.c_int),
         "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, S, P], ctypes.c_int),
@@ -201,6 +202,12 @@ def snn_loss(kind, B, K, P, counts, labels, targets, loss, grad_counts, ws, stre
     _check("snn_loss", lib().snn_loss(kind, B, K, P, _p(counts), _p(labels), _p(targets),
                                       _p(loss), _p(grad_counts), _p(ws), _nbytes(ws),
                                       _stream(stream)))
+
+
+def snn_loss_noalloc(kind, B, K, P, counts, labels, targets, loss, grad_counts, stream=None):
+    _check("snn_loss_noalloc", lib().snn_loss_noalloc(kind, B, K, P, _p(counts), _p(labels),
+                                                      _p(targets), _p(loss), _p(grad_counts),
+                                                      _stream(stream)))
 
 
 def snn_synapse_fwd(desc, x, w, bias, cur, pool_arg, ws, stream=None):

@@ -213,6 +213,20 @@ snn_status check_grad(const snn_layer_desc *d, const snn_grad_in *g) {
     return SNN_OK;
 }
 
+snn_status check_loss(int32_t kind, int32_t B, int32_t K, int32_t P, const float *counts,
+                      const int32_t *labels, const float *targets, const float *loss,
+                      const float *grad_counts) {
+    if (kind != SNN_LOSS_CE_COUNT && kind != SNN_LOSS_MSE_COUNT) return SNN_ERR_UNSUPPORTED;
+    if (B < 1 || K < 1 || P < 1 || (int64_t)K * P > INT32_MAX) return SNN_ERR_SHAPE;
+    if (!counts || !loss) return SNN_ERR_NULL;
+    if (kind == SNN_LOSS_CE_COUNT && !labels) return SNN_ERR_NULL;
+    if (kind == SNN_LOSS_MSE_COUNT && !targets) return SNN_ERR_NULL;
+    if (!aligned16(counts) || !aligned16(loss) || (labels && !aligned16(labels)) ||
+        (targets && !aligned16(targets)) || (grad_counts && !aligned16(grad_counts)))
+        return SNN_ERR_ALIGN;
+    return SNN_OK;
+}
+
 BwdGrad bwd_grad(const snn_grad_in *g) {
     BwdGrad b{};
     b.mode = g->kind;
@@ -500,19 +514,26 @@ size_t snn_loss_workspace_bytes(int32_t kind, int32_t B, int32_t K) {
 snn_status snn_loss(int32_t kind, int32_t B, int32_t K, int32_t P, const float *counts,
                     const int32_t *labels, const float *targets, float *loss,
                     float *grad_counts, void *ws, size_t ws_bytes, hipStream_t stream) {
-    if (kind != SNN_LOSS_CE_COUNT && kind != SNN_LOSS_MSE_COUNT) return SNN_ERR_UNSUPPORTED;
-    if (B < 1 || K < 1 || P < 1 || (int64_t)K * P > INT32_MAX) return SNN_ERR_SHAPE;
-    if (!counts || !loss) return SNN_ERR_NULL;
-    if (kind == SNN_LOSS_CE_COUNT && !labels) return SNN_ERR_NULL;
-    if (kind == SNN_LOSS_MSE_COUNT && !targets) return SNN_ERR_NULL;
-    if (!aligned16(counts) || !aligned16(loss) || (labels && !aligned16(labels)) ||
-        (targets && !aligned16(targets)) || (grad_counts && !aligned16(grad_counts)))
-        return SNN_ERR_ALIGN;
+    snn_status st = check_loss(kind, B, K, P, counts, labels, targets, loss, grad_counts);
+    if (st != SNN_OK) return st;
     const size_t need = loss_workspace_bytes(kind, B, K);
     if (need > ws_bytes || (need > 0 && !ws)) return SNN_ERR_WORKSPACE;
     (void)hipGetLastError();
     return hip_status(launch_loss(kind, B, K, P, counts, labels, targets, loss, grad_counts, ws,
                                   stream));
+}
+
+snn_status snn_loss_noalloc(int32_t kind, int32_t B, int32_t K, int32_t P, const float *counts,
+                            const int32_t *labels, const float *targets, float *loss,
+                            float *grad_counts, hipStream_t stream) {
+    snn_status st = check_loss(kind, B, K, P, counts, labels, targets, loss, grad_counts);
+    if (st != SNN_OK) return st;
+    if (loss_workspace_bytes(kind, B, K) > kLossScratchBytes) return SNN_ERR_WORKSPACE;
+    void *scratch = nullptr;
+    if (loss_static_scratch(&scratch) != hipSuccess) return SNN_ERR_HIP;
+    (void)hipGetLastError();
+    return hip_status(launch_loss(kind, B, K, P, counts, labels, targets, loss, grad_counts,
+                                  scratch, stream));
 }
 
 snn_status snn_adamw(const snn_adamw_tensor *tensors, int32_t count,

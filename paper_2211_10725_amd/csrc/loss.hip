@@ -6,6 +6,8 @@
 //
 // Reductions are fixed-order trees in fp64 (wave64 shuffles, then LDS), so
 // the scalar loss is bit-reproducible run to run.
+#include <atomic>
+
 #include "snn_internal.hpp"
 
 namespace snn {
@@ -287,6 +289,38 @@ hipError_t launch_loss(int kind, int B, int K, int P, const float *counts,
     if (e != hipSuccess) return e;
     mse_pass2_kernel<<<1, kThreads, 0, s>>>(blocks, n, partial, loss);
     return hipGetLastError();
+}
+
+// ---- scratch for callers that cannot allocate ------------------------------
+// The loss's partial sums (one double per row for cross-entropy, one per
+// first-pass block for MSE) in a file-scope device array instead of a
+// caller's workspace.  Every device the library runs on holds its own copy
+// until the process ends; its address differs per device and is looked up
+// once per device with that device current.  Each partial is written before
+// it is read, so nothing needs clearing between calls; calls that overlap on
+// one device share the array and race.
+static __device__ __align__(256) unsigned char scratch[kLossScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<void *> scratch_ptr[kMaxDevices];
+}  // namespace
+
+hipError_t loss_static_scratch(void **ptr) {
+    *ptr = nullptr;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    void *p = scratch_ptr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+    *ptr = p;
+    return hipSuccess;
 }
 
 }  // namespace snn

@@ -150,6 +150,10 @@ size_t loss_workspace_bytes(int kind, int B, int K);
 hipError_t launch_loss(int kind, int B, int K, int P, const float *counts,
                        const int32_t *labels, const float *targets, float *loss, float *grad,
                        void *ws, hipStream_t s);
+// The loss's scratch held by the library (a static device array, 1 MiB per
+// device): its address on the current device, looked up on first use.
+constexpr size_t kLossScratchBytes = (size_t)1 << 20;
+hipError_t loss_static_scratch(void **ptr);
 
 // ---- AdamW weight update (optim.hip) -------------------------------------------
 // per-step coefficients, computed on the host in double
