@@ -612,8 +612,10 @@ def _stage_kernels(net, name, li, fp32_mfma):
     d = net.descs[li]
     if name == "neuron_fwd":
         return ": neuron_fwd_kernel"
+    scale = (" (+ grad_bound_kernel + grad_scale_kernel: the power of two of the fp16 dL/dI)"
+             if d.grad_dtype == 1 else "")
     if name == "neuron_bwd" and net.fold[li]:
-        return ": neuron_bwd_kernel (the readout's dx folded in) + bias_reduce_kernel"
+        return ": neuron_bwd_kernel (the readout's dx folded in) + bias_reduce_kernel" + scale
     if name == "neuron_bwd":
         return ": neuron_bwd_kernel" + (" + bias_reduce_kernel" if d.synapse != 2 else "")
     if name in ("synapse_bwd_dw", "synapse_bwd_dx"):
@@ -633,7 +635,9 @@ def _stage_kernels(net, name, li, fp32_mfma):
             return f": {pre}{gemm} ({passes} pass{'es' if passes > 1 else ''}, " \
                    "+ splitk_reduce_kernel when split over K)"
         big = 2.0 * M * d.n_in * K >= 2 ** 30
-        gemm = "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel"
+        gemm = ("gemm_async_kernel" if big and passes == 1 and
+                _async_ok(d.grad_dtype, d.w_dtype, M, d.n_in, K) else
+                "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel")
         pre = "transpose_kernel (W^T) + " if big and kind == "mfma16" else ""
         return f": {pre}{gemm} ({passes} pass{'es' if passes > 1 else ''}, " \
                "+ splitk_reduce_kernel when split over K)"

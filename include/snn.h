@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 4
+#define SNN_ABI_VERSION 5
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -137,7 +137,11 @@ typedef struct snn_layer_desc {
     int32_t w_dtype;        /* w: SNN_F32 | SNN_F16 */
     int32_t out_dtype;      /* spikes written as SNN_U8 | SNN_F16 (0.0 / 1.0) */
     int32_t grad_dtype;     /* dL/dI handed to the weight / input gradient
-                               contractions: SNN_F32 | SNN_BF16 | SNN_F16 */
+                               contractions: SNN_F32 | SNN_BF16 | SNN_F16.
+                               SNN_F16 holds dL/dI * S, S a power of two
+                               chosen per backward call so that every value
+                               stays below 2^15 (see snn_neuron_bwd); not for
+                               SNN_RLEAKY */
     int32_t reset_grad;     /* SNN_RESET_DETACHED | SNN_RESET_SURROGATE */
     int32_t flags;          /* 0 or SNN_FLAG_FP32_MFMA */
     float beta;             /* membrane decay, eqs. (4)/(6) */
@@ -284,15 +288,29 @@ snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w
 snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float *v,
                           void *spk_out, float *saved_u, float *counts, hipStream_t stream);
 
-/* Reverse-time scan: dcur = dL/dI [T,B,n_out] of d->grad_dtype,
- * grad_b (nullable) = sum of dL/dI over t, b (and pooled positions), and
- * grad_v (nullable, SNN_RLEAKY only) as in snn_layer_bwd. */
+/* Reverse-time scan (eqs. 8-9 through the recursion of the header above):
+ * dcur = dL/dI [T,B,n_out] of d->grad_dtype, grad_b (nullable) = sum of dL/dI
+ * over t, b (and pooled positions), and grad_v (nullable, SNN_RLEAKY only) as
+ * in snn_layer_bwd.
+ * dcur_scale: with grad_dtype SNN_F16, a device fp32 scalar (required) that
+ * receives the power of two S; dcur then holds fp16(dL/dI * S).  S is the
+ * largest power of two with G F S <= 2^15, where G bounds |dL/dz| over the
+ * upstream gradient (max |g|; for SNN_GRAD_FOLD max over (t,b) of
+ * sum_j |dcur_up| times max |w_up|, a device reduction) and F bounds the
+ * growth of the recursion, sum_{k<T} c^k with c = max(|beta|, |beta - r thr|)
+ * (times sum_{k<T} |alpha|^k for SNN_SYNAPTIC); so no value overflows fp16
+ * and the rounding of each value is relative 2^-11 above 2^-14 / S.
+ * SNN_F16 is rejected for SNN_RLEAKY and where F exceeds 1e30
+ * (SNN_ERR_UNSUPPORTED).  Ignored (may be NULL) for the other dtypes. */
 snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const float *v,
-                          const float *saved_u, void *dcur, float *grad_b, float *grad_v,
-                          void *ws, size_t ws_bytes, hipStream_t stream);
+                          const float *saved_u, void *dcur, float *dcur_scale, float *grad_b,
+                          float *grad_v, void *ws, size_t ws_bytes, hipStream_t stream);
 
-/* Synapse backward from dcur (of d->grad_dtype): grad_w and/or grad_x. */
-snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
+/* Synapse backward from dcur (of d->grad_dtype): grad_w and/or grad_x
+ * (dW = dI^T x and dx = dI W, BPTT through the w x_t term of eqs. (4)/(5)).
+ * dcur_scale: for SNN_F16, the scale snn_neuron_bwd wrote (required); the
+ * contractions divide it out.  Ignored for the other dtypes. */
+snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const float *dcur_scale,
                            const uint8_t *pool_arg, const void *x, const void *w,
                            float *grad_w, float *grad_x, void *ws, size_t ws_bytes,
                            hipStream_t stream);

@@ -31,7 +31,7 @@ RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST, GRAD_FOLD = 0, 1, 2
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 4
+ABI_VERSION = 5
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
           4: "SNN_ERR_ALIGN", 5: "SNN_ERR_UNSUPPORTED", 6: "SNN_ERR_WORKSPACE",
@@ -112,8 +112,8 @@ def lib():
         "snn_loss_noalloc": ([i32, i32, i32, i32, P, P, P, P, P, P], ctypes.c_int),
         "snn_synapse_fwd": ([D, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_neuron_fwd": ([D, P, P, P, P, P, P], ctypes.c_int),
-        "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, S, P], ctypes.c_int),
-        "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_adamw": ([ctypes.POINTER(AdamwTensor), i32, ctypes.POINTER(AdamwHparams), P],
                       ctypes.c_int),
     }
@@ -222,17 +222,21 @@ def snn_neuron_fwd(desc, cur, v, spk_out, saved_u, counts, stream=None):
         _stream(stream)))
 
 
-def snn_neuron_bwd(desc, grad_kind, g, v, saved_u, dcur, grad_b, grad_v, ws, stream=None):
+def snn_neuron_bwd(desc, grad_kind, g, v, saved_u, dcur, grad_b, grad_v, ws, stream=None,
+                   dcur_scale=None):
+    """dcur_scale: device fp32 scalar receiving the power of two an fp16 dcur
+    is scaled by (required for grad_dtype F16)."""
     gi = _grad_in(grad_kind, g)
     _check("snn_neuron_bwd", lib().snn_neuron_bwd(
-        ctypes.byref(desc), ctypes.byref(gi), _p(v), _p(saved_u), _p(dcur), _p(grad_b),
-        _p(grad_v), _p(ws), _nbytes(ws), _stream(stream)))
+        ctypes.byref(desc), ctypes.byref(gi), _p(v), _p(saved_u), _p(dcur), _p(dcur_scale),
+        _p(grad_b), _p(grad_v), _p(ws), _nbytes(ws), _stream(stream)))
 
 
-def snn_synapse_bwd(desc, dcur, pool_arg, x, w, grad_w, grad_x, ws, stream=None):
+def snn_synapse_bwd(desc, dcur, pool_arg, x, w, grad_w, grad_x, ws, stream=None,
+                    dcur_scale=None):
     _check("snn_synapse_bwd", lib().snn_synapse_bwd(
-        ctypes.byref(desc), _p(dcur), _p(pool_arg), _p(x), _p(w), _p(grad_w), _p(grad_x),
-        _p(ws), _nbytes(ws), _stream(stream)))
+        ctypes.byref(desc), _p(dcur), _p(dcur_scale), _p(pool_arg), _p(x), _p(w), _p(grad_w),
+        _p(grad_x), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def snn_adamw(tensors, step, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2,
@@ -343,10 +347,25 @@ class Network:
         self.dup = [None] * n
         for li in range(n - 1):
             if self.fold[li]:
+                self.gx[li + 1] = None
+        # The fp16 net's gradient operand dL/dI: fp16 scaled by a power of two
+        # (one MFMA pass against the fp16 weights of the input gradient) for
+        # layers whose input gradient is a contraction; bf16 otherwise (the
+        # weight gradient against spikes is one pass in either type).  The
+        # scale needs a bound of the upstream gradient: cheap for a broadcast
+        # or folded one, one extra read of a full [T,B,n] gradient otherwise.
+        self.scale = [None] * n
+        for li, d in enumerate(self.descs):
+            if not half or d.synapse != SYN_DENSE or d.neuron == RLEAKY:
+                continue
+            if li > 0 and self.gx[li] is not None:
+                d.grad_dtype = F16
+                self.scale[li] = torch.empty(4, dtype=torch.float32, device=device)
+        for li in range(n - 1):
+            if self.fold[li]:
                 up = self.descs[li + 1]
                 self.dup[li + 1] = torch.empty((T, B, up.n_out), dtype=gdt[up.grad_dtype],
                                                device=device)
-                self.gx[li + 1] = None
         # K classes, P output neurons per class (a population code when P > 1)
         self.P = getattr(wl, "pop", 1)
         n_last = self.descs[-1].n_out
@@ -388,9 +407,9 @@ class Network:
             if self.dup[li] is not None:
                 # dL/dI kept for the layer below; no dx of its own
                 snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], self.dup[li], self.gb[li],
-                               self.gv[li], self.ws, stream)
+                               self.gv[li], self.ws, stream, dcur_scale=self.scale[li])
                 snn_synapse_bwd(d, self.dup[li], self.pool_arg(li), xin, self.W[li], self.gW[li],
-                                None, self.ws, stream)
+                                None, self.ws, stream, dcur_scale=self.scale[li])
             else:
                 snn_layer_bwd(d, kind, g, xin, self.W[li], self.v[li], self.saved[li],
                               self.gW[li], self.gb[li], self.gv[li], self.gx[li], self.ws, stream)
@@ -512,18 +531,20 @@ class Network:
                 else:
                     dcur = dcur.view(torch.float32)
                 rest = self.ws[(dcur_bytes + 255) // 256 * 256:]
+            sc = self.scale[li]
             hook("neuron_bwd", li)
             snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], dcur, self.gb[li],
-                           self.gv[li], rest, stream)
+                           self.gv[li], rest, stream, dcur_scale=sc)
             hook("neuron_bwd_end", li)
             if d.synapse == SYN_DENSE:
                 hook("synapse_bwd_dw", li)
-                snn_synapse_bwd(d, dcur, None, xin, self.W[li], self.gW[li], None, rest, stream)
+                snn_synapse_bwd(d, dcur, None, xin, self.W[li], self.gW[li], None, rest, stream,
+                                dcur_scale=sc)
                 hook("synapse_bwd_dw_end", li)
                 if self.gx[li] is not None:
                     hook("synapse_bwd_dx", li)
                     snn_synapse_bwd(d, dcur, None, xin, self.W[li], None, self.gx[li], rest,
-                                    stream)
+                                    stream, dcur_scale=sc)
                     hook("synapse_bwd_dx_end", li)
             else:
                 hook("synapse_bwd", li)

@@ -103,9 +103,45 @@ size_t dcur_bytes(const snn_layer_desc *d) {
 size_t colsum_bytes(const snn_layer_desc *d) {
     return align_up((size_t)d->B * d->n_out * sizeof(float));
 }
+// An fp16 dL/dI is written scaled by a power of two S chosen per call from a
+// bound of |dL/dI|: a device reduction over the upstream gradient (its
+// partial maxima need grad_scale_workspace_bytes()) times the growth of the
+// reverse recursion.
+bool scaled_grad(const snn_layer_desc *d) { return d->grad_dtype == SNN_F16; }
+size_t scale_scratch_bytes(const snn_layer_desc *d) {
+    return scaled_grad(d) ? align_up(grad_scale_workspace_bytes()) : 0;
+}
+// |dL/dI_t| <= G * growth with G = max |g|: each step of the reverse
+// recursion multiplies the carried adjoint by beta - r thr s, s in (0, 1]
+// (|.| <= c = max(|beta|, |beta - r thr|)), and adds g s (|g s| <= G), so
+// |lam_t| <= G sum_{k<T} c^k; the current-based neuron's lami sums lam with
+// powers of alpha.  The recurrent neuron's carry depends on its weights v
+// (device data): no fp16 gradient operand for it.
+double grad_growth(const snn_layer_desc *d) {
+    auto geo = [&](double q) {
+        if (q == 1.0) return (double)d->T;
+        return (1.0 - pow(q, (double)d->T)) / (1.0 - q);
+    };
+    const double r = d->reset_grad == SNN_RESET_SURROGATE ? 1.0 : 0.0;
+    const double c = fmax(fabs((double)d->beta), fabs((double)d->beta - r * d->threshold));
+    double F = geo(c);
+    if (d->neuron == SNN_SYNAPTIC) F *= geo(fabs((double)d->alpha));
+    return F;
+}
+bool scale_ok(const snn_layer_desc *d) {
+    if (!scaled_grad(d)) return true;
+    if (d->neuron == SNN_RLEAKY) return false;
+    const double F = grad_growth(d);
+    return isfinite(F) && F <= 1e30;
+}
 // per-column sums of the neuron backward: dL/dI (bias) and, for the recurrent
-// neuron, lam_{t+1} z_t (recurrent weight)
-size_t neuron_ws(const snn_layer_desc *d) { return colsum_bytes(d) * (recurrent(d) ? 2 : 1); }
+// neuron, lam_{t+1} z_t (recurrent weight); the partial maxima of an fp16
+// dL/dI's scale
+size_t neuron_ws(const snn_layer_desc *d) {
+    return colsum_bytes(d) * (recurrent(d) ? 2 : 1) + scale_scratch_bytes(d);
+}
+// the device scalar S of an fp16 dL/dI inside the layer workspace
+size_t scale_slot_bytes(const snn_layer_desc *d) { return scaled_grad(d) ? kAlign : 0; }
 // Weight and input gradients of a dense layer.  Large contractions whose
 // operands are stored M/N-contiguous (dI and x for dW, W for dx) are
 // transposed once into the workspace so that they run K-contiguous on the
@@ -190,7 +226,9 @@ size_t bwd_gemm_ws(const snn_layer_desc *d) {
     const size_t dx = x.wt_bytes + x.gemm_bytes;
     return dw > dx ? dw : dx;
 }
-size_t bwd_ws(const snn_layer_desc *d) { return dcur_bytes(d) + neuron_ws(d) + bwd_gemm_ws(d); }
+size_t bwd_ws(const snn_layer_desc *d) {
+    return dcur_bytes(d) + neuron_ws(d) + scale_slot_bytes(d) + bwd_gemm_ws(d);
+}
 
 snn_status hip_status(hipError_t e) { return e == hipSuccess ? SNN_OK : SNN_ERR_HIP; }
 
@@ -323,12 +361,19 @@ snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float
 }
 
 snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const float *v,
-                          const float *saved_u, void *dcur, float *grad_b, float *grad_v,
-                          void *ws, size_t ws_bytes, hipStream_t stream) {
+                          const float *saved_u, void *dcur, float *dcur_scale, float *grad_b,
+                          float *grad_v, void *ws, size_t ws_bytes, hipStream_t stream) {
     snn_status st = check_desc(d);
     if (st != SNN_OK) return st;
     if ((st = check_grad(d, grad)) != SNN_OK) return st;
     if (!saved_u || !dcur) return SNN_ERR_NULL;
+    if (scaled_grad(d)) {
+        if (!dcur_scale) return SNN_ERR_NULL;
+        if (!aligned16(dcur_scale)) return SNN_ERR_ALIGN;
+        if (!scale_ok(d)) return SNN_ERR_UNSUPPORTED;
+    } else {
+        dcur_scale = nullptr;
+    }
     if (recurrent(d) && !v) return SNN_ERR_NULL;
     if (!recurrent(d)) {
         if (grad_v) return SNN_ERR_SHAPE;  // no recurrent weight to differentiate
@@ -338,7 +383,8 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
         (v && !aligned16(v)) || (grad_v && !aligned16(grad_v)))
         return SNN_ERR_ALIGN;
     if (grad_b && d->synapse == SNN_SYN_NONE) return SNN_ERR_SHAPE;  // no bias to differentiate
-    const size_t need = (grad_b ? colsum_bytes(d) : 0) + (grad_v ? colsum_bytes(d) : 0);
+    const size_t sums = (grad_b ? colsum_bytes(d) : 0) + (grad_v ? colsum_bytes(d) : 0);
+    const size_t need = sums + scale_scratch_bytes(d);
     if (need > ws_bytes || (need > 0 && !ws)) return SNN_ERR_WORKSPACE;
     (void)hipGetLastError();
     if (rows(d) == 0) {
@@ -348,6 +394,13 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
             e = launch_fill_zero(grad_b, nb, stream);
         }
         if (grad_v && e == hipSuccess) e = launch_fill_zero(grad_v, d->n_out, stream);
+        // an empty gradient: its scale is 1
+        if (dcur_scale && e == hipSuccess)
+            e = launch_grad_scale(d->T, (int64_t)d->B * d->n_out, bwd_grad(grad), d->B, 1.0,
+                                  dcur_scale, reinterpret_cast<float *>(
+                                      reinterpret_cast<char *>(ws) +
+                                      (grad_b ? colsum_bytes(d) : 0) + (grad_v ? colsum_bytes(d) : 0)),
+                                  stream);
         return hip_status(e);
     }
     const int64_t C = (int64_t)d->B * d->n_out;
@@ -355,9 +408,16 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
     float *colsum = grad_b ? reinterpret_cast<float *>(wsb) : nullptr;
     float *dvcol = grad_v ? reinterpret_cast<float *>(wsb + (grad_b ? colsum_bytes(d) : 0))
                           : nullptr;
-    hipError_t e = launch_neuron_bwd(d->neuron, d->reset_grad, d->T, C, d->n_out, d->alpha,
-                                     d->beta, d->threshold, d->slope, v, saved_u, bwd_grad(grad),
-                                     d->B, dcur, d->grad_dtype, colsum, dvcol, stream);
+    const BwdGrad bg = bwd_grad(grad);
+    hipError_t e = hipSuccess;
+    if (dcur_scale) {
+        e = launch_grad_scale(d->T, C, bg, d->B, grad_growth(d), dcur_scale,
+                              reinterpret_cast<float *>(wsb + sums), stream);
+        if (e != hipSuccess) return SNN_ERR_HIP;
+    }
+    e = launch_neuron_bwd(d->neuron, d->reset_grad, d->T, C, d->n_out, d->alpha, d->beta,
+                          d->threshold, d->slope, v, saved_u, bg, d->B, dcur, d->grad_dtype,
+                          dcur_scale, colsum, dvcol, stream);
     if (e != hipSuccess) return SNN_ERR_HIP;
     if (grad_b) {
         int F = d->n_out, P = 1;
@@ -373,7 +433,7 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
     return hip_status(e);
 }
 
-snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
+snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const float *dcur_scale,
                            const uint8_t *pool_arg, const void *x, const void *w,
                            float *grad_w, float *grad_x, void *ws, size_t ws_bytes,
                            hipStream_t stream) {
@@ -381,6 +441,12 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
     if (st != SNN_OK) return st;
     if (d->synapse == SNN_SYN_NONE) return SNN_ERR_UNSUPPORTED;
     if (!dcur) return SNN_ERR_NULL;
+    if (scaled_grad(d)) {
+        if (!dcur_scale) return SNN_ERR_NULL;
+        if (!aligned16(dcur_scale)) return SNN_ERR_ALIGN;
+    } else {
+        dcur_scale = nullptr;
+    }
     if ((grad_w && !x) || (grad_x && !w)) return SNN_ERR_NULL;
     if (!aligned16(dcur) || (x && !aligned16(x)) || (w && !aligned16(w)) ||
         (grad_w && !aligned16(grad_w)) || (grad_x && !aligned16(grad_x)))
@@ -407,6 +473,7 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
         GemmArgs g{};
         g.M = d->n_out; g.N = d->n_in; g.K = M;
         g.C = grad_w; g.ldc = d->n_in; g.bias = nullptr; g.allow_split = split_ok(d);
+        g.c_div = dcur_scale;
         hipError_t e;
         if (pl.transposed) {
             char *dit = wsb, *xt = wsb + pl.dit_bytes;
@@ -436,6 +503,7 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur,
         g.M = M; g.N = d->n_in; g.K = d->n_out;
         g.A = dcur; g.lda = d->n_out; g.a_dtype = d->grad_dtype; g.a_kc = true;
         g.C = grad_x; g.ldc = d->n_in; g.bias = nullptr; g.allow_split = split_ok(d);
+        g.c_div = dcur_scale;
         hipError_t e;
         if (pl.transposed) {
             e = launch_transpose(d->n_out, d->n_in, w, d->n_in, (int)dtype_bytes(d->w_dtype), wsb,
@@ -489,7 +557,8 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     if (d->synapse == SNN_SYN_NONE) {
         if (grad_w || grad_b) return SNN_ERR_SHAPE;
         if (!grad_x) return SNN_ERR_NULL;
-        return snn_neuron_bwd(d, grad, v, u, grad_x, nullptr, grad_v, ws, ws_bytes, stream);
+        return snn_neuron_bwd(d, grad, v, u, grad_x, nullptr, nullptr, grad_v, ws, ws_bytes,
+                              stream);
     }
     if (grad_w && !x) return SNN_ERR_NULL;
     if (grad_x && !w) return SNN_ERR_NULL;
@@ -497,13 +566,14 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     char *base = reinterpret_cast<char *>(ws);
     void *dcur = base;
     char *colsum = base + dcur_bytes(d);
-    char *gws = colsum + neuron_ws(d);
-    st = snn_neuron_bwd(d, grad, v, u, dcur, grad_b, grad_v, colsum, neuron_ws(d), stream);
+    float *scale = scaled_grad(d) ? reinterpret_cast<float *>(colsum + neuron_ws(d)) : nullptr;
+    char *gws = colsum + neuron_ws(d) + scale_slot_bytes(d);
+    st = snn_neuron_bwd(d, grad, v, u, dcur, scale, grad_b, grad_v, colsum, neuron_ws(d), stream);
     if (st != SNN_OK) return st;
     if (!grad_w && !grad_x) return SNN_OK;
     const uint8_t *arg = nullptr;
     if (d->synapse == SNN_SYN_CONV5_POOL2) arg = reinterpret_cast<const uint8_t *>(saved) + arg_offset(d);
-    return snn_synapse_bwd(d, dcur, arg, x, w, grad_w, grad_x, gws, bwd_gemm_ws(d), stream);
+    return snn_synapse_bwd(d, dcur, scale, arg, x, w, grad_w, grad_x, gws, bwd_gemm_ws(d), stream);
 }
 
 size_t snn_loss_workspace_bytes(int32_t kind, int32_t B, int32_t K) {

@@ -211,18 +211,30 @@ __global__ __launch_bounds__(kThreads) void gemm_f32_kernel(
 }
 
 // C[m,n] = sum_{z < S} P[z][m][n] (+ bias[n]), z ascending.
+// (divided by the power of two c_div[0] when c_div is set: exact)
 __global__ __launch_bounds__(kThreads) void splitk_reduce_kernel(int M, int N, int S,
                                                                  const float *__restrict__ P,
                                                                  float *__restrict__ C, int64_t ldc,
-                                                                 const float *__restrict__ bias) {
+                                                                 const float *__restrict__ bias,
+                                                                 const float *__restrict__ c_div) {
     const int64_t total = (int64_t)M * N;
     const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (idx >= total) return;
     float s = 0.f;
     for (int z = 0; z < S; ++z) s += P[(int64_t)z * total + idx];
+    if (c_div) s /= c_div[0];
     const int m = (int)(idx / N), n = (int)(idx % N);
     if (bias) s += bias[n];
     C[(int64_t)m * ldc + n] = s;
+}
+
+__global__ __launch_bounds__(kThreads) void divide_kernel(int M, int N, float *__restrict__ C,
+                                                          int64_t ldc,
+                                                          const float *__restrict__ c_div) {
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= (int64_t)M * N) return;
+    const int m = (int)(idx / N), n = (int)(idx % N);
+    C[(int64_t)m * ldc + n] /= c_div[0];
 }
 
 // The same sum for many partials (S >= 16): a block reduces 64 outputs, its
@@ -230,7 +242,7 @@ __global__ __launch_bounds__(kThreads) void splitk_reduce_kernel(int M, int N, i
 // are added in order.
 __global__ __launch_bounds__(kThreads) void splitk_reduce_wide_kernel(
     int M, int N, int S, const float *__restrict__ P, float *__restrict__ C, int64_t ldc,
-    const float *__restrict__ bias) {
+    const float *__restrict__ bias, const float *__restrict__ c_div) {
     __shared__ float part[4][64];
     const int64_t total = (int64_t)M * N;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -246,6 +258,7 @@ __global__ __launch_bounds__(kThreads) void splitk_reduce_wide_kernel(
     __syncthreads();
     if (wave == 0 && idx < total) {
         float r = ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
+        if (c_div) r /= c_div[0];
         const int m = (int)(idx / N), n = (int)(idx % N);
         if (bias) r += bias[n];
         C[(int64_t)m * ldc + n] = r;
@@ -352,17 +365,27 @@ size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype, bool 
     return align_up((size_t)p.splits * M * N * sizeof(float));
 }
 
+namespace {
+// a contraction kernel without its own division, then C /= c_div[0] (no bias:
+// scaled operands only occur in the backward)
+hipError_t divided(hipError_t e, const GemmArgs &g, hipStream_t s) {
+    if (e != hipSuccess || g.c_div == nullptr) return e;
+    return launch_divide(g.M, g.N, g.C, g.ldc, g.c_div, s);
+}
+}  // namespace
+
 hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s) {
     if (g.M <= 0 || g.N <= 0) return hipSuccess;
     if (g.K <= 0) {
         // empty contraction: C = bias (or 0)
         return hipErrorInvalidValue;
     }
-    if (short_k_applies(g)) return launch_short_k(g, s);
-    if (narrow_fwd_applies(g)) return launch_narrow_fwd(g, s);
-    if (few_rows_applies(g)) return launch_few_rows(g, ws, ws_bytes, s);
+    if (g.c_div && g.bias) return hipErrorInvalidValue;
+    if (short_k_applies(g)) return divided(launch_short_k(g, s), g, s);
+    if (narrow_fwd_applies(g)) return divided(launch_narrow_fwd(g, s), g, s);
+    if (few_rows_applies(g)) return divided(launch_few_rows(g, ws, ws_bytes, s), g, s);
     if (gemm_async_applies(g)) return launch_gemm_async(g, ws, ws_bytes, s);
-    if (g.allow_split && gemm16_applies(g)) return launch_gemm16(g, ws, ws_bytes, s);
+    if (g.allow_split && gemm16_applies(g)) return divided(launch_gemm16(g, ws, ws_bytes, s), g, s);
     const Plan p = make_plan(g.M, g.N, g.K);
     float *out = g.C;
     int64_t ldo = g.ldc, ss = 0;
@@ -383,19 +406,28 @@ hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (p.splits > 1) e = launch_splitk_reduce(g.M, g.N, p.splits, out, g.C, g.ldc, g.bias, s);
-    return e;
+    if (p.splits > 1)
+        return launch_splitk_reduce(g.M, g.N, p.splits, out, g.C, g.ldc, g.bias, s, g.c_div);
+    return divided(e, g, s);
 }
 
 hipError_t launch_splitk_reduce(int M, int N, int S, const float *P, float *C, int64_t ldc,
-                                const float *bias, hipStream_t s) {
+                                const float *bias, hipStream_t s, const float *c_div) {
     const int64_t total = (int64_t)M * N;
     if (S >= 16)
         splitk_reduce_wide_kernel<<<(unsigned)((total + 63) / 64), kThreads, 0, s>>>(M, N, S, P, C,
-                                                                                 ldc, bias);
+                                                                                 ldc, bias, c_div);
     else
         splitk_reduce_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(
-            M, N, S, P, C, ldc, bias);
+            M, N, S, P, C, ldc, bias, c_div);
+    return hipGetLastError();
+}
+
+hipError_t launch_divide(int M, int N, float *C, int64_t ldc, const float *c_div, hipStream_t s) {
+    const int64_t total = (int64_t)M * N;
+    if (total <= 0) return hipSuccess;
+    divide_kernel<<<(unsigned)((total + kThreads - 1) / kThreads), kThreads, 0, s>>>(M, N, C, ldc,
+                                                                                  c_div);
     return hipGetLastError();
 }
 

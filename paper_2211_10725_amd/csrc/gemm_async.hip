@@ -172,7 +172,7 @@ template <int MT>
 __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
     int M, int N, int K, int k_chunk, int tiles_n, const uint16_t *__restrict__ A, int64_t lda,
     const uint16_t *__restrict__ B, int64_t ldb, float *__restrict__ C, int64_t ldc,
-    int64_t split_stride, const float *__restrict__ bias) {
+    int64_t split_stride, const float *__restrict__ bias, const float *__restrict__ c_div) {
     const int item = xcd_local_item();
     const int tiles = gridDim.x;
     const int zk = item / tiles, tile = item % tiles;
@@ -217,9 +217,19 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
 #undef SNN_KTILE
 
     // 32x32 block: lane holds column (lane & 31); register r holds row
-    // 8*(r/4) + 4*(lane/32) + r%4.
+    // 8*(r/4) + 4*(lane/32) + r%4.  A scaled operand's power of two is
+    // divided out exactly (multiplication by its exact reciprocal).
     const int lane = threadIdx.x & 63;
     float *Cz = C + (int64_t)zk * split_stride;
+    if (c_div) {
+        const float inv = 1.f / c_div[0];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][j][r] *= inv;
+    }
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
@@ -344,23 +354,25 @@ hipError_t launch_gemm_async(const GemmArgs &g, void *ws, size_t ws_bytes, hipSt
     if (e != hipSuccess) return e;
     float *out = g.C;
     int64_t ldo = g.ldc, ss = 0;
-    const float *bias = g.bias;
+    const float *bias = g.bias, *c_div = g.c_div;
     if (p.splits > 1) {
         out = reinterpret_cast<float *>(w + p.a_bytes + p.b_bytes);
         ldo = g.N;
         ss = (int64_t)g.M * g.N;
         bias = nullptr;
+        c_div = nullptr;  // divided in the reduction
     }
     dim3 grid((unsigned)(p.tiles_m * p.tiles_n), 1, (unsigned)p.splits);
     if (mt == MT_F16)
         gemm_async_kernel<MT_F16><<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n, A,
-                                                            lda, B, ldb, out, ldo, ss, bias);
+                                                            lda, B, ldb, out, ldo, ss, bias, c_div);
     else
         gemm_async_kernel<MT_BF16><<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n, A,
-                                                             lda, B, ldb, out, ldo, ss, bias);
+                                                             lda, B, ldb, out, ldo, ss, bias, c_div);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (p.splits > 1) e = launch_splitk_reduce(g.M, g.N, p.splits, out, g.C, g.ldc, g.bias, s);
+    if (p.splits > 1)
+        e = launch_splitk_reduce(g.M, g.N, p.splits, out, g.C, g.ldc, g.bias, s, g.c_div);
     return e;
 }
 

@@ -140,8 +140,11 @@ __device__ inline uint16_t f32_to_bf16_rne(float x) {
     return (uint16_t)((b + 0x7fffu + ((b >> 16) & 1u)) >> 16);
 }
 
+// dL/dI in the operand type of the contractions.  fp16 is written scaled by
+// the power of two `scale` (exact), chosen per call so that every value
+// stays below 2^15 (grad_scale_*_kernel below).
 template <int GT, int VEC>
-__device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC]) {
+__device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC], float scale) {
     if constexpr (GT == SNN_F32) {
         Vec<VEC>::store(reinterpret_cast<float *>(base) + off, v);
     } else {
@@ -149,7 +152,7 @@ __device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC]
 #pragma unroll
         for (int i = 0; i < VEC; ++i) {
             if constexpr (GT == SNN_F16) {
-                const _Float16 f = (_Float16)v[i];
+                const _Float16 f = (_Float16)(v[i] * scale);
                 h[i] = __builtin_bit_cast(uint16_t, f);
             } else {
                 h[i] = f32_to_bf16_rne(v[i]);
@@ -227,8 +230,10 @@ template <int NEURON, int VEC, int GM, bool RESET_SURR, int GT, int kDepth>
 __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
     int T, int64_t C, int64_t N, float alpha, float beta, float thr, float slope,
     const float *__restrict__ vrec, const float *__restrict__ u, const float *__restrict__ g,
-    FoldIn fold, void *__restrict__ dcur, float *__restrict__ colsum, float *__restrict__ dvcol) {
+    FoldIn fold, void *__restrict__ dcur, const float *__restrict__ dscale,
+    float *__restrict__ colsum, float *__restrict__ dvcol) {
     constexpr bool BCAST = GM == GM_BCAST, FOLD = GM == GM_FOLD || GM == GM_FOLD12;
+    const float scale = GT == SNN_F16 ? *dscale : 1.f;
     constexpr int KF = GM == GM_FOLD12 ? 12 : kFoldMax;  // dI_up values per row (padded)
     const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
     // the fold's lanes past the last column still take part in the staging
@@ -334,7 +339,7 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
                     }
                     acc[v] += d[v];
                 }
-                store_grad<GT, VEC>(dcur, (int64_t)t * C + col, d);
+                store_grad<GT, VEC>(dcur, (int64_t)t * C + col, d, scale);
             }
         }
         if constexpr (FOLD) {
@@ -406,6 +411,84 @@ __global__ __launch_bounds__(kReduceThreads) void bias_reduce_pos_kernel(
     if (threadIdx.x == 0) db[f] = (float)part[0];
 }
 
+// ---- the power-of-two scale of an fp16 dL/dI ------------------------------
+// |lam_t| <= G F with G a bound on |g| and F = sum_k c^k the growth of the
+// reverse recursion (computed by the caller from beta, alpha, thr and T), so
+// dL/dI S with S = 2^e, e = floor(log2(2^15 / (G F))), stays below 2^15
+// (fp16 holds up to 65504: a factor 2 of headroom for the fp32 rounding of
+// the bound and the recursion).  G is a max over the upstream gradient:
+//   FULL / BCAST  G = max |g|
+//   FOLD          G = max_{t,b} sum_j |dup[t,b,j]|  *  max_{j,n} |wup[j,n]|
+//                 (>= |sum_j dup[t,b,j] wup[j,n]| for every n)
+// First pass: per-workgroup maxima (partial[2 blk], partial[2 blk + 1]);
+// second pass, one workgroup: the maxima, G and S (written to scale[0]).
+// Max is order-independent: the result is deterministic.
+constexpr int kScaleBlocks = 1024;
+
+__device__ inline float block_max(float v, float *red) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    float m = 0.f;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) m = fmaxf(m, red[w]);
+    __syncthreads();
+    return m;
+}
+
+__global__ __launch_bounds__(kThreads) void grad_bound_kernel(int64_t rows, int width, int dt,
+                                                              const void *__restrict__ src,
+                                                              int64_t nw, int dt_w,
+                                                              const void *__restrict__ w,
+                                                              float *__restrict__ partial) {
+    __shared__ float red[kThreads / 64];
+    // rows of `width` values: the max over rows of sum |x| (width 1: max |x|)
+    float m1 = 0.f;
+    for (int64_t r = (int64_t)blockIdx.x * kThreads + threadIdx.x; r < rows;
+         r += (int64_t)gridDim.x * kThreads) {
+        float a = 0.f;
+        for (int j = 0; j < width; ++j) a += __builtin_fabsf(load_as_f32(src, r * width + j, dt));
+        m1 = fmaxf(m1, a);
+    }
+    float m2 = 0.f;
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < nw;
+         i += (int64_t)gridDim.x * kThreads)
+        m2 = fmaxf(m2, __builtin_fabsf(load_as_f32(w, i, dt_w)));
+    m1 = block_max(m1, red);
+    m2 = block_max(m2, red);
+    if (threadIdx.x == 0) {
+        partial[2 * blockIdx.x] = m1;
+        partial[2 * blockIdx.x + 1] = m2;
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void grad_scale_kernel(int nblk, bool product, double growth,
+                                                              const float *__restrict__ partial,
+                                                              float *__restrict__ scale) {
+    __shared__ float red[kThreads / 64];
+    float m1 = 0.f, m2 = 0.f;
+    for (int i = threadIdx.x; i < nblk; i += kThreads) {
+        m1 = fmaxf(m1, partial[2 * i]);
+        m2 = fmaxf(m2, partial[2 * i + 1]);
+    }
+    m1 = block_max(m1, red);
+    m2 = block_max(m2, red);
+    if (threadIdx.x == 0) {
+        const double G = product ? (double)m1 * (double)m2 : (double)m1;
+        const double bound = G * growth;
+        int e = 0;
+        if (bound > 0.0 && bound < 1e300) {
+            int ex;
+            (void)frexp(32768.0 / bound, &ex);  // 32768 / bound in [2^(ex-1), 2^ex)
+            e = ex - 1;
+            if (e > 120) e = 120;
+            if (e < -120) e = -120;
+        }
+        scale[0] = ldexpf(1.f, e);
+    }
+}
+
 __global__ __launch_bounds__(kThreads) void fill_zero_kernel(float *__restrict__ p, int64_t n) {
     const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
     if (i < n) p[i] = 0.f;
@@ -438,6 +521,7 @@ struct BwdBuffers {
     const float *u, *g;
     FoldIn fold;
     void *dcur;
+    const float *dscale;
     float *colsum, *dvcol;
 };
 
@@ -450,7 +534,7 @@ void bwd_launch(const ScanArgs &a, const BwdBuffers &b, hipStream_t s) {
     constexpr bool FOLD = GM == GM_FOLD || GM == GM_FOLD12;
     neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, VEC == 4 ? 6 : FOLD ? 8 : 16><<<grid, kThreads, 0, s>>>(
         a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.u, b.g, b.fold, b.dcur,
-        b.colsum, b.dvcol);
+        b.dscale, b.colsum, b.dvcol);
 }
 
 template <int NEURON, int VEC, int GM, bool RS>
@@ -504,7 +588,9 @@ bool neuron_fold_supported(int64_t N) { return N >= 64; }
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
                              const float *u, const BwdGrad &grad, int B, void *dcur,
-                             int grad_dtype, float *colsum, float *dvcol, hipStream_t s) {
+                             int grad_dtype, const float *dscale, float *colsum, float *dvcol,
+                             hipStream_t s) {
+    if (grad_dtype == SNN_F16 && dscale == nullptr) return hipErrorInvalidValue;
     if (T <= 0 || C <= 0) return hipSuccess;
     int gm = grad.mode == SNN_GRAD_FOLD ? GM_FOLD
              : grad.mode == SNN_GRAD_BCAST ? GM_BCAST : GM_FULL;
@@ -516,7 +602,7 @@ hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, 
     if ((gm == GM_FOLD || gm == GM_FOLD12) && v4 && (N % 4 != 0 || N < 256)) v4 = false;
     const ScanArgs a{T, C, N, alpha, beta, thr, slope, vrec};
     const FoldIn fold{grad.dup, grad.wup, grad.nup, grad.dt_up, grad.dt_w, B};
-    const BwdBuffers b{u, grad.g, fold, dcur, colsum, dvcol};
+    const BwdBuffers b{u, grad.g, fold, dcur, dscale, colsum, dvcol};
     const int rs = reset_surrogate, gt = grad_dtype;
     switch (neuron) {
         case SNN_SYNAPTIC:
@@ -537,6 +623,37 @@ hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, 
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     fill_zero_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, s>>>(p, n);
+    return hipGetLastError();
+}
+
+size_t grad_scale_workspace_bytes() { return 2 * kScaleBlocks * sizeof(float); }
+
+hipError_t launch_grad_scale(int T, int64_t C, const BwdGrad &grad, int B, double growth,
+                             float *scale, float *scratch, hipStream_t s) {
+    int64_t rows, nw = 0;
+    int width = 1, dt = SNN_F32, dt_w = SNN_F32;
+    const void *src, *w = nullptr;
+    if (grad.mode == SNN_GRAD_FOLD) {
+        rows = (int64_t)T * B;
+        width = grad.nup;
+        dt = grad.dt_up;
+        src = grad.dup;
+        nw = (int64_t)grad.nup * (C / B);
+        w = grad.wup;
+        dt_w = grad.dt_w;
+    } else {
+        rows = grad.mode == SNN_GRAD_BCAST ? C : (int64_t)T * C;
+        src = grad.g;
+    }
+    const int64_t work = rows * width > nw ? rows * width : nw;
+    int nblk = (int)((work + 16 * kThreads - 1) / (16 * kThreads));
+    if (nblk < 1) nblk = 1;
+    if (nblk > kScaleBlocks) nblk = kScaleBlocks;
+    grad_bound_kernel<<<nblk, kThreads, 0, s>>>(rows, width, dt, src, nw, dt_w, w, scratch);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    grad_scale_kernel<<<1, kThreads, 0, s>>>(nblk, grad.mode == SNN_GRAD_FOLD, growth, scratch,
+                                             scale);
     return hipGetLastError();
 }
 

@@ -63,13 +63,21 @@ struct BwdGrad {
 };
 bool neuron_fold_supported(int64_t N);
 
-// Backward: writes dcur [T, C] (grad_dtype), colsum [C] = sum_t dcur (fp32,
+// Backward: writes dcur [T, C] (grad_dtype), colsum [C] = sum_t dL/dI (fp32,
 // may be NULL) and, for SNN_RLEAKY, dvcol [C] = sum_t lam_{t+1} z_t (fp32,
-// may be NULL).  C = B * N.
+// may be NULL).  C = B * N.  An SNN_F16 dcur holds dL/dI * S with the power
+// of two S read from dscale[0] (launch_grad_scale writes it).
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
                              const float *u, const BwdGrad &grad, int B, void *dcur,
-                             int grad_dtype, float *colsum, float *dvcol, hipStream_t s);
+                             int grad_dtype, const float *dscale, float *colsum, float *dvcol,
+                             hipStream_t s);
+// scale[0] = S = 2^e, the largest power of two with G * growth * S <= 2^15,
+// G a bound on |g| over the upstream gradient (device reduction into
+// `scratch`, grad_scale_workspace_bytes()); growth bounds |dL/dI| / G.
+size_t grad_scale_workspace_bytes();
+hipError_t launch_grad_scale(int T, int64_t C, const BwdGrad &grad, int B, double growth,
+                             float *scale, float *scratch, hipStream_t s);
 
 // p[0..n) = 0 with a kernel (safe inside captured graphs)
 hipError_t launch_fill_zero(float *p, int64_t n, hipStream_t s);
@@ -105,13 +113,18 @@ struct GemmArgs {
     float *pool_cur = nullptr;
     uint8_t *pool_arg = nullptr;
     bool *pooled = nullptr;
+    // C is divided by c_div[0] (a device power of two, the scale of an fp16
+    // dL/dI operand); NULL: no scaling
+    const float *c_div = nullptr;
 };
 size_t gemm_workspace_bytes(int M, int N, int K, int a_dtype, int b_dtype, bool a_kc,
                             bool b_kc, bool allow_split);
 hipError_t launch_gemm(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
-// C[m,n] = sum_{z<S} P[z][m][n] (+ bias[n]), fixed order
+// C[m,n] = sum_{z<S} P[z][m][n] / c_div[0] (+ bias[n]), fixed order (c_div may be NULL)
 hipError_t launch_splitk_reduce(int M, int N, int S, const float *P, float *C, int64_t ldc,
-                                const float *bias, hipStream_t s);
+                                const float *bias, hipStream_t s, const float *c_div = nullptr);
+// C[m,n] /= c_div[0] for m < M, n < N
+hipError_t launch_divide(int M, int N, float *C, int64_t ldc, const float *c_div, hipStream_t s);
 
 // ---- 16-bit matrix cores, exact products (gemm_mfma16.hip) ---------------------
 bool gemm16_applies(const GemmArgs &g);

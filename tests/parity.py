@@ -60,3 +60,18 @@ def assert_spikes(z_gpu, z_orc, u_orc, thr, what=""):
     assert illegal == 0, f"{what}: {illegal} spike flips where |u - thr| >= 1e-4"
     assert agree >= 0.9999, f"{what}: spike agreement {agree:.6f}"
     return roots
+
+
+def pow2_scale(x, top=2.0 ** 15):
+    """The largest power of two S with max|x| * S <= top (1 for all zeros):
+    the scale under which an fp16 gradient operand is handed to the
+    contractions."""
+    m = float(np.abs(np.asarray(x, np.float64)).max()) if np.size(x) else 0.0
+    if m == 0.0:
+        return 1.0
+    e = int(np.floor(np.log2(top / m)))
+    while m * 2.0 ** e > top:
+        e -= 1
+    while m * 2.0 ** (e + 1) <= top:
+        e += 1
+    return 2.0 ** e

@@ -131,21 +131,28 @@ def test_half_net_full_size_sampled():
         # ---- reverse scan with a seeded upstream gradient (bf16 dL/dI out)
         last = li == n - 1
         g = _seeded_normal((B, d.n_out) if last else (T, B, d.n_out), 0.0, 1e-4, seed=300 + li)
-        dcur = torch.empty((T, B, d.n_out), dtype=torch.bfloat16, device=DEV)
+        # (the layer's 16-bit dL/dI operand: bf16, or fp16 scaled by a power of two)
+        scaled = d.grad_dtype == snn.F16
+        gdt = torch.float16 if scaled else torch.bfloat16
+        sc = torch.empty(4, dtype=torch.float32, device=DEV) if scaled else None
+        dcur = torch.empty((T, B, d.n_out), dtype=gdt, device=DEV)
         snn.snn_neuron_bwd(d, snn.GRAD_BCAST if last else snn.GRAD_FULL, g, None, u, dcur, None,
-                           None, net.ws)
+                           None, net.ws, dcur_scale=sc)
+        S = float(_np(sc)[0]) if scaled else 1.0
         g_c = _np(g[bs][:, ns]) if last else _np(g[:, bs][:, :, ns])
         dI_o = oracle.scan_bwd(u_o, g_c, spec["neuron"], spec["beta"], spec["thr"], wl.slope)
-        assert_close(_np(dcur[:, bs][:, :, ns].float()), dI_o, tol, what=f"L{li} dL/dI")
+        assert_close(_np(dcur[:, bs][:, :, ns].float()) / S, dI_o, tol, what=f"L{li} dL/dI")
         del Is, spk, u, dcur
-        # ---- synapse backward on seeded bf16 dL/dI: sampled dW rows, dx rows
-        dI = _seeded_normal((T * B, d.n_out), 0.0, 1e-4, seed=400 + li, dtype=torch.bfloat16)
+        # ---- synapse backward on seeded 16-bit dL/dI: sampled dW rows, dx rows
+        S = 2.0 ** 20 if scaled else 1.0
+        dI = _seeded_normal((T * B, d.n_out), 0.0, 1e-4 * S, seed=400 + li, dtype=gdt)
+        sc = torch.full((4,), S, dtype=torch.float32, device=DEV) if scaled else None
         gW = torch.empty((d.n_out, d.n_in), dtype=torch.float32, device=DEV)
         gx = torch.empty((T * B, d.n_in), dtype=torch.float32, device=DEV) if li > 0 else None
-        snn.snn_synapse_bwd(d, dI, None, xin_dev, net.W[li], gW, gx, net.ws)
+        snn.snn_synapse_bwd(d, dI, None, xin_dev, net.W[li], gW, gx, net.ws, dcur_scale=sc)
         xall = _np(xin_dev.reshape(T * B, -1)).astype(np.float64)
         cols_o = np.arange(d.n_out) if last else rng.integers(0, d.n_out, 8)
-        dI_h = _np(dI.float()).astype(np.float64)               # the seeded bf16 values
+        dI_h = _np(dI.float()).astype(np.float64) / S           # the seeded 16-bit values
         dW_o, _, _ = oracle.dense_bwd(dI_h[:, cols_o], xall, W[cols_o], want_db=False,
                                       want_dx=False)
         # fp32 sums of exact products: within 1e-3, or the a-priori bound of an
