@@ -172,6 +172,27 @@ def _grad_in(kind, g):
     return GradIn(kind, 0, _p(g), None, None, 0, 0)
 
 
+_ELEM = {F32: 4, F16: 2, BF16: 2, U8: 1}
+
+
+def _need(fn, t, dtype_code, count, what):
+    """A tensor argument must hold at least `count` elements of the type the
+    descriptor names (the library cannot see buffer sizes): raise before the
+    call instead of letting a kernel run past the buffer."""
+    if t is None or isinstance(t, int):
+        return
+    es = _ELEM[dtype_code]
+    if t.element_size() != es or t.numel() < count:
+        raise ValueError(f"{fn}: {what} needs {count} elements of {es} bytes, got "
+                         f"{t.numel()} of {t.element_size()}")
+
+
+def _check_fwd_io(fn, d, x=None, spk=None):
+    rows = d.T * d.B
+    _need(fn, x, d.in_dtype, rows * d.n_in, "x")
+    _need(fn, spk, d.out_dtype, rows * d.n_out, "spk_out")
+
+
 def snn_layer_saved_bytes(desc: LayerDesc) -> int:
     return int(lib().snn_layer_saved_bytes(ctypes.byref(desc)))
 
@@ -185,6 +206,7 @@ def snn_loss_workspace_bytes(kind: int, B: int, K: int) -> int:
 
 
 def snn_layer_fwd(desc, x, w, bias, v, spk_out, saved, counts, ws, stream=None):
+    _check_fwd_io("snn_layer_fwd", desc, x, spk_out)
     _check("snn_layer_fwd", lib().snn_layer_fwd(
         ctypes.byref(desc), _p(x), _p(w), _p(bias), _p(v), _p(spk_out), _p(saved), _p(counts),
         _p(ws), _nbytes(ws), _stream(stream)))
@@ -192,6 +214,7 @@ def snn_layer_fwd(desc, x, w, bias, v, spk_out, saved, counts, ws, stream=None):
 
 def snn_layer_bwd(desc, grad_kind, g, x, w, v, saved, grad_w, grad_b, grad_v, grad_x, ws,
                   stream=None):
+    _check_fwd_io("snn_layer_bwd", desc, x)
     gi = _grad_in(grad_kind, g)
     _check("snn_layer_bwd", lib().snn_layer_bwd(
         ctypes.byref(desc), ctypes.byref(gi), _p(x), _p(w), _p(v), _p(saved), _p(grad_w),
@@ -211,12 +234,14 @@ def snn_loss_noalloc(kind, B, K, P, counts, labels, targets, loss, grad_counts, 
 
 
 def snn_synapse_fwd(desc, x, w, bias, cur, pool_arg, ws, stream=None):
+    _check_fwd_io("snn_synapse_fwd", desc, x)
     _check("snn_synapse_fwd", lib().snn_synapse_fwd(
         ctypes.byref(desc), _p(x), _p(w), _p(bias), _p(cur), _p(pool_arg), _p(ws), _nbytes(ws),
         _stream(stream)))
 
 
 def snn_neuron_fwd(desc, cur, v, spk_out, saved_u, counts, stream=None):
+    _check_fwd_io("snn_neuron_fwd", desc, None, spk_out)
     _check("snn_neuron_fwd", lib().snn_neuron_fwd(
         ctypes.byref(desc), _p(cur), _p(v), _p(spk_out), _p(saved_u), _p(counts),
         _stream(stream)))
@@ -226,6 +251,8 @@ def snn_neuron_bwd(desc, grad_kind, g, v, saved_u, dcur, grad_b, grad_v, ws, str
                    dcur_scale=None):
     """dcur_scale: device fp32 scalar receiving the power of two an fp16 dcur
     is scaled by (required for grad_dtype F16)."""
+    _need("snn_neuron_bwd", dcur, desc.grad_dtype if desc.synapse != SYN_NONE else F32,
+          desc.T * desc.B * desc.n_out, "dcur")
     gi = _grad_in(grad_kind, g)
     _check("snn_neuron_bwd", lib().snn_neuron_bwd(
         ctypes.byref(desc), ctypes.byref(gi), _p(v), _p(saved_u), _p(dcur), _p(dcur_scale),
@@ -234,6 +261,8 @@ def snn_neuron_bwd(desc, grad_kind, g, v, saved_u, dcur, grad_b, grad_v, ws, str
 
 def snn_synapse_bwd(desc, dcur, pool_arg, x, w, grad_w, grad_x, ws, stream=None,
                     dcur_scale=None):
+    _check_fwd_io("snn_synapse_bwd", desc, x)
+    _need("snn_synapse_bwd", dcur, desc.grad_dtype, desc.T * desc.B * desc.n_out, "dcur")
     _check("snn_synapse_bwd", lib().snn_synapse_bwd(
         ctypes.byref(desc), _p(dcur), _p(dcur_scale), _p(pool_arg), _p(x), _p(w), _p(grad_w),
         _p(grad_x), _p(ws), _nbytes(ws), _stream(stream)))
@@ -320,7 +349,16 @@ class Network:
                 self.b.append(torch.as_tensor(np.ascontiguousarray(b)).to(device=device,
                                                                          dtype=torch.float32))
         u8 = torch.uint8
-        self.spk = [torch.empty((T, B, d.n_out), dtype=u8, device=device) for d in self.descs]
+        # Spikes that feed a large fp16 contraction (a dense layer above with
+        # at least 256 outputs) are written as fp16 0/1 by the scan, the
+        # operand type that contraction stages directly; other spikes as bytes.
+        for li in range(len(self.descs) - 1):
+            up = self.descs[li + 1]
+            if half and up.synapse == SYN_DENSE and up.n_out >= 256 and up.n_in >= 256:
+                self.descs[li].out_dtype = F16
+                up.in_dtype = F16
+        self.spk = [torch.empty((T, B, d.n_out), dtype=torch.float16 if d.out_dtype == F16
+                                else u8, device=device) for d in self.descs]
         self.in_shape = (T, B) + tuple(wl.in_shape)
         self.saved = [torch.empty(snn_layer_saved_bytes(d), dtype=u8, device=device)
                       for d in self.descs]

@@ -108,6 +108,8 @@ def test_half_net_full_size_sampled():
         # ---- synapse forward on seeded spikes (the input's rates for layer 0)
         xin_dev = torch.as_tensor(inp["x"]).to(DEV) if li == 0 else \
             _seeded_spikes((T, B, d.n_in), 0.15, seed=100 + li)
+        if d.in_dtype == snn.F16:
+            xin_dev = xin_dev.to(torch.float16)  # spikes as the layer reads them
         cur = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
         snn.snn_synapse_fwd(d, xin_dev, net.W[li], net.b[li], cur, None, net.ws)
         rows = rng.integers(0, T * B, 64)
@@ -118,7 +120,8 @@ def test_half_net_full_size_sampled():
         del cur
         # ---- neuron scan on seeded currents
         Is = _seeded_normal((T, B, d.n_out), 0.1, 0.6, seed=200 + li)
-        spk = torch.empty((T, B, d.n_out), dtype=torch.uint8, device=DEV)
+        spk = torch.empty((T, B, d.n_out), device=DEV,
+                          dtype=torch.float16 if d.out_dtype == snn.F16 else torch.uint8)
         u = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
         snn.snn_neuron_fwd(d, Is, None, spk, u, None)
         bs = torch.as_tensor(rng.integers(0, B, 2), device=DEV)

@@ -603,9 +603,18 @@ def _saved_from_oracle(d, f):
     return buf.to(DEV)
 
 
-def _layer_input(spec, f):
+def _layer_input(spec, f, d):
+    """The oracle's input to a layer in the type the layer's descriptor reads
+    (currents fp32; spikes as bytes or as fp16 0/1)."""
     x = np.asarray(f["x"])
-    return _t(x.astype(np.float32) if spec["kind"] == "none" else x.astype(np.uint8))
+    if spec["kind"] == "none":
+        return _t(x.astype(np.float32))
+    return _t(x.astype(np.float16) if d.in_dtype == snn.F16 else x.astype(np.uint8))
+
+
+def _spk_buf(d):
+    return torch.empty((d.T, d.B, d.n_out), dtype=torch.float16 if d.out_dtype == snn.F16
+                       else torch.uint8, device=DEV)
 
 
 def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
@@ -631,7 +640,7 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
     xs = []
     for li, spec in enumerate(wl.layers):
         f, d = fwds[li], net.descs[li]
-        x_dev = _layer_input(spec, f)
+        x_dev = _layer_input(spec, f, d)
         xs.append(x_dev)
         if spec["kind"] != "none":
             cur = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
@@ -639,7 +648,7 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
                 if spec["kind"] == "conv" else None
             snn.snn_synapse_fwd(d, x_dev, net.W[li], net.b[li], cur, arg, net.ws)
             assert_close(_np(cur), f["I"].reshape(T, B, -1), tol, what=f"L{li} currents")
-        spk = torch.empty((T, B, d.n_out), dtype=torch.uint8, device=DEV)
+        spk = _spk_buf(d)
         u = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
         cnt = torch.empty((B, d.n_out), dtype=torch.float32, device=DEV)
         snn.snn_neuron_fwd(d, _t(f["I"].reshape(T, B, -1)), net.v[li], spk, u, cnt)
