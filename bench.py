@@ -100,16 +100,19 @@ def stage_work(net, name, li):
                    synapse backward of a dense layer is two stages, dW
                    (K = T*B) and dx (K = n_out), each 2 M N K; a conv layer's
                    backward is one stage with both
-      forward scan 4 B read current + 4 B write membrane + s B write spike
-                   per (t, b, n) (s = 1 for bytes, 2 for fp16 spikes), + 4 B
-                   count per (b, n) of the layer that counts
-      reverse scan 4 B read membrane + 4 B read dL/dz (full upstream gradient
-                   only) + w B write dL/dI per (t, b, n) (w = 4 for fp32, 2 for
-                   a 16-bit gradient operand), + 4 B colsum per (b, n), + 4 B
-                   recurrent-weight column sum per (b, n) for recurrent
-                   neurons (eq. 7); with the readout's input gradient folded
-                   in, dL/dz is not read but computed from the readout's
-                   dL/dI (its operand bytes per (t, b, readout neuron))"""
+      forward scan 4 B read current + s B write spike per (t, b, n) (s = 1
+                   for bytes, 2 for fp16 spikes), + 4 P B per (b, n) per
+                   checkpoint (P = 1 state plane, 2 for the current-based
+                   neuron), + 4 B count per (b, n) of the layer that counts
+      reverse scan 4 B read current (the membrane is recomputed from it) +
+                   4 B read dL/dz (full upstream gradient only) + w B write
+                   dL/dI per (t, b, n) (w = 4 for fp32, 2 for a 16-bit
+                   gradient operand), + the checkpoints read, + 4 B colsum
+                   per (b, n), + 4 B recurrent-weight column sum per (b, n)
+                   for recurrent neurons (eq. 7); with the readout's input
+                   gradient folded in, dL/dz is not read but computed from
+                   the readout's dL/dI (its operand bytes per (t, b, readout
+                   neuron))"""
     d = net.descs[li]
     TB = d.T * d.B
     macs = _macs(d)
@@ -123,9 +126,11 @@ def stage_work(net, name, li):
         return "flop", 2.0 * macs * (2 if dx else 1)
     el = TB * d.n_out
     cols = d.B * d.n_out
+    lay = net.layouts[li]
+    ckpt = 4.0 * lay.ckpt_planes * lay.ckpt_count * cols
     if name == "neuron_fwd":
         counts = 4.0 * cols if li == len(net.descs) - 1 else 0.0
-        return "byte", (8.0 + _dtype_bytes(d.out_dtype)) * el + counts
+        return "byte", (4.0 + _dtype_bytes(d.out_dtype)) * el + ckpt + counts
     if name == "neuron_bwd":
         rec = 4.0 * cols if d.neuron == 2 else 0.0
         wr = _dtype_bytes(d.grad_dtype) if d.synapse != 2 else 4.0
@@ -133,9 +138,9 @@ def stage_work(net, name, li):
         if net.fold[li]:
             up = net.descs[li + 1]
             return "byte", (4.0 + wr) * el + _dtype_bytes(up.grad_dtype) * TB * up.n_out + \
-                colsum + rec
+                ckpt + colsum + rec
         full = li < len(net.descs) - 1
-        return "byte", (4.0 + (4.0 if full else 0.0) + wr) * el + colsum + rec
+        return "byte", (4.0 + (4.0 if full else 0.0) + wr) * el + ckpt + colsum + rec
     return None, 0.0
 
 

@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 5
+#define SNN_ABI_VERSION 6
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -168,17 +168,44 @@ typedef struct snn_grad_in {
 int snn_abi_version(void);
 const char *snn_status_str(snn_status s);
 
-/* Bytes of the forward-to-backward state: the membrane u_t after each step
- * (fp32 [T,B,n_out]) and, for conv layers, the 2x2 pool selection (one byte
- * per pooled current).  The backward needs nothing else: the surrogate only
- * depends on u_t. */
+/* Bytes of the forward-to-backward state (BPTT keeps O(n T) state, Sec.
+ * II-B).  The backward needs the membrane u_t of every step (the surrogate
+ * of eq. (9) depends on nothing else); instead of u_t the state holds the
+ * currents and the neuron state every ckpt_interval steps, from which the
+ * reverse scan recomputes u_t chunk by chunk (bit-identical: the same fp32
+ * operations as the forward). */
 size_t snn_layer_saved_bytes(const snn_layer_desc *d);
+
+/* Where each part of the saved state lies inside the snn_layer_saved_bytes
+ * buffer (byte offsets, each a multiple of 256):
+ *   cur    fp32 currents I [T,B,n_out] of the synapse, as the forward scan
+ *          read them (0 bytes for SNN_SYN_NONE: the layer's x holds them)
+ *   ckpt   checkpoints: fp32 [ckpt_planes][ckpt_count][B*n_out]; slot c
+ *          (0 <= c < ckpt_count = (T - 1) / ckpt_interval) holds the state
+ *          after step (c + 1) * ckpt_interval - 1 (0-based): plane 0 the
+ *          membrane u, plane 1 (SNN_SYNAPTIC only) the synaptic current i
+ *   pool   conv only: u8 [T,B,n_out] 2x2 pool selection 0..3 (row-major in
+ *          the window, first maximum wins); 0 bytes otherwise
+ * The stage calls take these parts as separate pointers. */
+typedef struct snn_saved_layout {
+    size_t bytes;               /* == snn_layer_saved_bytes */
+    size_t cur_offset, cur_bytes;
+    size_t ckpt_offset, ckpt_bytes;
+    size_t pool_offset, pool_bytes;
+    int32_t ckpt_interval;      /* steps between checkpoints */
+    int32_t ckpt_count;         /* checkpoints per plane */
+    int32_t ckpt_planes;        /* 1, or 2 for SNN_SYNAPTIC */
+    int32_t reserved;
+} snn_saved_layout;
+/* SNN_ERR_NULL for a NULL out; the descriptor's errors otherwise. */
+snn_status snn_layer_saved_layout(const snn_layer_desc *d, snn_saved_layout *out);
 
 /* Scratch bytes needed by snn_layer_fwd / snn_layer_bwd and the stage calls
  * below (the maximum over all of them).  0 is a valid answer. */
 size_t snn_layer_workspace_bytes(const snn_layer_desc *d);
 
-/* Forward of one layer (synapse, then the neuron scan over all T).
+/* Forward of one layer (synapse, then the neuron scan over all T; eqs.
+ * (3)-(7) after the w x_t contraction).
  *   x       [T,B,n_in] of d->in_dtype
  *   w       weights of d->w_dtype (NULL iff SNN_SYN_NONE)
  *   bias    fp32 [n_out] dense / [c_out] conv, or NULL for no bias
@@ -193,9 +220,11 @@ snn_status snn_layer_fwd(const snn_layer_desc *d, const void *x, const void *w,
                          const float *bias, const float *v, void *spk_out, void *saved,
                          float *counts, void *ws, size_t ws_bytes, hipStream_t stream);
 
-/* Backward of one layer (reverse-time neuron scan, then the synapse).
+/* Backward of one layer (reverse-time neuron scan, then the synapse; BPTT
+ * with the surrogate of eqs. (8)-(9)).
  *   grad    upstream dL/dz of this layer's spikes
- *   x, w, v the forward's inputs; saved: the forward's saved state
+ *   x, w, v the forward's inputs (x required for SNN_SYN_NONE: its currents);
+ *           saved: the forward's saved state
  *   grad_w  dL/dw (layout of w, fp32), NULL to skip; must be NULL for SYN_NONE
  *   grad_b  dL/dbias fp32, NULL to skip
  *   grad_v  dL/dv fp32 [n_out] of SNN_RLEAKY, NULL to skip; must be NULL for
@@ -277,18 +306,26 @@ snn_status snn_adamw(const snn_adamw_tensor *tensors, int32_t count,
  * split of time between synaptic and neuron work, Sec. IV) and check each
  * stage on its own. */
 
-/* Currents I [T,B,n_out] fp32.  pool_arg: conv only, u8 [T,B,n_out] pool
+/* Synapse forward (the w x_t term of eqs. (4)/(5); Table I's conv + pool):
+ * currents I [T,B,n_out] fp32.  pool_arg: conv only, u8 [T,B,n_out] pool
  * selection 0..3 (row-major in the 2x2 window, first maximum wins). */
 snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w,
                            const float *bias, float *cur, uint8_t *pool_arg, void *ws,
                            size_t ws_bytes, hipStream_t stream);
 
-/* Neuron scan over T.  cur and saved_u may be the same pointer (in place);
- * any other overlap is undefined.  v as in snn_layer_fwd. */
+/* Neuron scan over T (eqs. 3-7): spikes spk_out [T,B,n_out] of
+ * d->out_dtype, counts (nullable) [B,n_out], and the checkpoints ckpt laid
+ * out as the ckpt part of snn_saved_layout (required when ckpt_count > 0).
+ * u_out (nullable): the membrane u_t of every step, fp32 [T,B,n_out]; it may
+ * be the same pointer as cur (in place), any other overlap is undefined.
+ * v as in snn_layer_fwd. */
 snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float *v,
-                          void *spk_out, float *saved_u, float *counts, hipStream_t stream);
+                          void *spk_out, float *ckpt, float *u_out, float *counts,
+                          hipStream_t stream);
 
-/* Reverse-time scan (eqs. 8-9 through the recursion of the header above):
+/* Reverse-time scan (eqs. 8-9 through the recursion of the header above)
+ * from the forward's currents cur [T,B,n_out] fp32 and checkpoints ckpt (as
+ * written by snn_neuron_fwd on the same currents; u_t is recomputed):
  * dcur = dL/dI [T,B,n_out] of d->grad_dtype, grad_b (nullable) = sum of dL/dI
  * over t, b (and pooled positions), and grad_v (nullable, SNN_RLEAKY only) as
  * in snn_layer_bwd.
@@ -303,8 +340,9 @@ snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float
  * SNN_F16 is rejected for SNN_RLEAKY and where F exceeds 1e30
  * (SNN_ERR_UNSUPPORTED).  Ignored (may be NULL) for the other dtypes. */
 snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const float *v,
-                          const float *saved_u, void *dcur, float *dcur_scale, float *grad_b,
-                          float *grad_v, void *ws, size_t ws_bytes, hipStream_t stream);
+                          const float *cur, const float *ckpt, void *dcur, float *dcur_scale,
+                          float *grad_b, float *grad_v, void *ws, size_t ws_bytes,
+                          hipStream_t stream);
 
 /* Synapse backward from dcur (of d->grad_dtype): grad_w and/or grad_x
  * (dW = dI^T x and dx = dI W, BPTT through the w x_t term of eqs. (4)/(5)).

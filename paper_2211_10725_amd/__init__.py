@@ -31,7 +31,7 @@ RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST, GRAD_FOLD = 0, 1, 2
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 5
+ABI_VERSION = 6
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
           4: "SNN_ERR_ALIGN", 5: "SNN_ERR_UNSUPPORTED", 6: "SNN_ERR_WORKSPACE",
@@ -40,7 +40,8 @@ STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE"
 EXPORTS = ["snn_abi_version", "snn_status_str", "snn_layer_saved_bytes",
            "snn_layer_workspace_bytes", "snn_layer_fwd", "snn_layer_bwd",
            "snn_loss_workspace_bytes", "snn_loss", "snn_synapse_fwd", "snn_neuron_fwd",
-           "snn_neuron_bwd", "snn_synapse_bwd", "snn_adamw", "snn_loss_noalloc"]
+           "snn_neuron_bwd", "snn_synapse_bwd", "snn_adamw", "snn_loss_noalloc",
+           "snn_layer_saved_layout"]
 
 
 class LayerDesc(ctypes.Structure):
@@ -59,6 +60,15 @@ class LayerDesc(ctypes.Structure):
         d = LayerDesc()
         ctypes.pointer(d)[0] = self
         return d
+
+
+class SavedLayout(ctypes.Structure):
+    _fields_ = [("bytes", ctypes.c_size_t), ("cur_offset", ctypes.c_size_t),
+                ("cur_bytes", ctypes.c_size_t), ("ckpt_offset", ctypes.c_size_t),
+                ("ckpt_bytes", ctypes.c_size_t), ("pool_offset", ctypes.c_size_t),
+                ("pool_bytes", ctypes.c_size_t), ("ckpt_interval", ctypes.c_int32),
+                ("ckpt_count", ctypes.c_int32), ("ckpt_planes", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
 
 
 class GradIn(ctypes.Structure):
@@ -104,6 +114,7 @@ def lib():
         "snn_abi_version": ([], ctypes.c_int),
         "snn_status_str": ([ctypes.c_int], ctypes.c_char_p),
         "snn_layer_saved_bytes": ([D], S),
+        "snn_layer_saved_layout": ([D, ctypes.POINTER(SavedLayout)], ctypes.c_int),
         "snn_layer_workspace_bytes": ([D], S),
         "snn_layer_fwd": ([D, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_layer_bwd": ([D, G, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
@@ -111,8 +122,8 @@ def lib():
         "snn_loss": ([i32, i32, i32, i32, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_loss_noalloc": ([i32, i32, i32, i32, P, P, P, P, P, P], ctypes.c_int),
         "snn_synapse_fwd": ([D, P, P, P, P, P, P, S, P], ctypes.c_int),
-        "snn_neuron_fwd": ([D, P, P, P, P, P, P], ctypes.c_int),
-        "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_neuron_fwd": ([D, P, P, P, P, P, P, P], ctypes.c_int),
+        "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_adamw": ([ctypes.POINTER(AdamwTensor), i32, ctypes.POINTER(AdamwHparams), P],
                       ctypes.c_int),
@@ -197,6 +208,38 @@ def snn_layer_saved_bytes(desc: LayerDesc) -> int:
     return int(lib().snn_layer_saved_bytes(ctypes.byref(desc)))
 
 
+def snn_layer_saved_layout(desc: LayerDesc) -> SavedLayout:
+    out = SavedLayout()
+    _check("snn_layer_saved_layout", lib().snn_layer_saved_layout(ctypes.byref(desc),
+                                                                  ctypes.byref(out)))
+    return out
+
+
+def saved_parts(desc: LayerDesc, saved):
+    """Views of a saved-state buffer (uint8 tensor of snn_layer_saved_bytes):
+    (currents fp32 [T,B,n_out] or None, checkpoints fp32, pool selection u8
+    [T,B,n_out] or None), at the offsets the library reports."""
+    lay = snn_layer_saved_layout(desc)
+    T, B, n = desc.T, desc.B, desc.n_out
+    cur = None
+    if lay.cur_bytes:
+        cur = saved[lay.cur_offset: lay.cur_offset + T * B * n * 4].view(
+            __import__("torch").float32).view(T, B, n)
+    ck = saved[lay.ckpt_offset: lay.ckpt_offset + lay.ckpt_bytes].view(
+        __import__("torch").float32)
+    pool = None
+    if lay.pool_bytes:
+        pool = saved[lay.pool_offset: lay.pool_offset + T * B * n].view(T, B, n)
+    return cur, ck, pool
+
+
+def ckpt_buffer(desc: LayerDesc, device="cuda"):
+    """A device buffer for the checkpoints of snn_neuron_fwd / snn_neuron_bwd."""
+    import torch
+    lay = snn_layer_saved_layout(desc)
+    return torch.empty(max(64, lay.ckpt_bytes // 4), dtype=torch.float32, device=device)
+
+
 def snn_layer_workspace_bytes(desc: LayerDesc) -> int:
     return int(lib().snn_layer_workspace_bytes(ctypes.byref(desc)))
 
@@ -240,23 +283,29 @@ def snn_synapse_fwd(desc, x, w, bias, cur, pool_arg, ws, stream=None):
         _stream(stream)))
 
 
-def snn_neuron_fwd(desc, cur, v, spk_out, saved_u, counts, stream=None):
+def snn_neuron_fwd(desc, cur, v, spk_out, ckpt, counts, stream=None, u_out=None):
+    """ckpt: checkpoints (ckpt_buffer); u_out: the membrane of every step, or None."""
     _check_fwd_io("snn_neuron_fwd", desc, None, spk_out)
+    _need("snn_neuron_fwd", u_out, F32, desc.T * desc.B * desc.n_out, "u_out")
+    _need("snn_neuron_fwd", ckpt, F32, snn_layer_saved_layout(desc).ckpt_bytes // 4, "ckpt")
     _check("snn_neuron_fwd", lib().snn_neuron_fwd(
-        ctypes.byref(desc), _p(cur), _p(v), _p(spk_out), _p(saved_u), _p(counts),
+        ctypes.byref(desc), _p(cur), _p(v), _p(spk_out), _p(ckpt), _p(u_out), _p(counts),
         _stream(stream)))
 
 
-def snn_neuron_bwd(desc, grad_kind, g, v, saved_u, dcur, grad_b, grad_v, ws, stream=None,
+def snn_neuron_bwd(desc, grad_kind, g, v, cur, ckpt, dcur, grad_b, grad_v, ws, stream=None,
                    dcur_scale=None):
-    """dcur_scale: device fp32 scalar receiving the power of two an fp16 dcur
-    is scaled by (required for grad_dtype F16)."""
+    """cur, ckpt: the forward's currents and checkpoints.  dcur_scale: device
+    fp32 scalar receiving the power of two an fp16 dcur is scaled by
+    (required for grad_dtype F16)."""
+    _need("snn_neuron_bwd", cur, F32, desc.T * desc.B * desc.n_out, "cur")
+    _need("snn_neuron_bwd", ckpt, F32, snn_layer_saved_layout(desc).ckpt_bytes // 4, "ckpt")
     _need("snn_neuron_bwd", dcur, desc.grad_dtype if desc.synapse != SYN_NONE else F32,
           desc.T * desc.B * desc.n_out, "dcur")
     gi = _grad_in(grad_kind, g)
     _check("snn_neuron_bwd", lib().snn_neuron_bwd(
-        ctypes.byref(desc), ctypes.byref(gi), _p(v), _p(saved_u), _p(dcur), _p(dcur_scale),
-        _p(grad_b), _p(grad_v), _p(ws), _nbytes(ws), _stream(stream)))
+        ctypes.byref(desc), ctypes.byref(gi), _p(v), _p(cur), _p(ckpt), _p(dcur),
+        _p(dcur_scale), _p(grad_b), _p(grad_v), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def snn_synapse_bwd(desc, dcur, pool_arg, x, w, grad_w, grad_x, ws, stream=None,
@@ -362,6 +411,9 @@ class Network:
         self.in_shape = (T, B) + tuple(wl.in_shape)
         self.saved = [torch.empty(snn_layer_saved_bytes(d), dtype=u8, device=device)
                       for d in self.descs]
+        # (currents, checkpoints, pool selection) views of each saved buffer
+        self.layouts = [snn_layer_saved_layout(d) for d in self.descs]
+        self.parts = [saved_parts(d, sv) for d, sv in zip(self.descs, self.saved)]
         self.gW = [None if w is None else torch.empty(w.shape, dtype=torch.float32, device=device)
                    for w in self.W]
         self.gb = [None if b is None else torch.empty(b.shape, dtype=torch.float32, device=device)
@@ -444,8 +496,10 @@ class Network:
             xin = x if li == 0 else self.spk[li - 1]
             if self.dup[li] is not None:
                 # dL/dI kept for the layer below; no dx of its own
-                snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], self.dup[li], self.gb[li],
-                               self.gv[li], self.ws, stream, dcur_scale=self.scale[li])
+                cur, ck, _ = self.parts[li]
+                snn_neuron_bwd(d, kind, g, self.v[li], xin if cur is None else cur, ck,
+                               self.dup[li], self.gb[li], self.gv[li], self.ws, stream,
+                               dcur_scale=self.scale[li])
                 snn_synapse_bwd(d, self.dup[li], self.pool_arg(li), xin, self.W[li], self.gW[li],
                                 None, self.ws, stream, dcur_scale=self.scale[li])
             else:
@@ -502,12 +556,9 @@ class Network:
         snn_adamw(self.opt_tensors, self.opt_t, stream=stream, **self.opt)
 
     def pool_arg(self, li):
-        """The 2x2 pool selection of conv layer li inside its saved buffer."""
-        d = self.descs[li]
-        if d.synapse != SYN_CONV5_POOL2:
-            return None
-        off = (d.T * d.B * d.n_out * 4 + 255) // 256 * 256
-        return self.saved[li][off:]
+        """The 2x2 pool selection of conv layer li inside its saved buffer
+        (None for other layers), at the offset the library reports."""
+        return self.parts[li][2]
 
     # the same work through the stage calls, with a hook between stages
     # (update: finish with the AdamW step of ``init_adamw``; fused_bwd: each
@@ -523,7 +574,7 @@ class Network:
         n = len(self.descs)
         h = x
         for li, d in enumerate(self.descs):
-            cur = self.saved[li]
+            cur, ck, _ = self.parts[li]
             if d.synapse != SYN_NONE:
                 hook("synapse_fwd", li)
                 snn_synapse_fwd(d, h, self.W[li], self.b[li], cur, self.pool_arg(li), self.ws,
@@ -532,7 +583,7 @@ class Network:
             else:
                 cur = h
             hook("neuron_fwd", li)
-            snn_neuron_fwd(d, cur, self.v[li], self.spk[li], self.saved[li],
+            snn_neuron_fwd(d, cur, self.v[li], self.spk[li], ck,
                            self.counts if li == n - 1 else None, stream)
             hook("neuron_fwd_end", li)
             h = self.spk[li]
@@ -545,7 +596,7 @@ class Network:
             xin = x if li == 0 else self.spk[li - 1]
             if d.synapse == SYN_NONE:
                 hook("neuron_bwd", li)
-                snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], self.gx[li], None,
+                snn_neuron_bwd(d, kind, g, self.v[li], xin, self.parts[li][1], self.gx[li], None,
                                self.gv[li], self.ws, stream)
                 hook("neuron_bwd_end", li)
                 continue
@@ -571,7 +622,8 @@ class Network:
                 rest = self.ws[(dcur_bytes + 255) // 256 * 256:]
             sc = self.scale[li]
             hook("neuron_bwd", li)
-            snn_neuron_bwd(d, kind, g, self.v[li], self.saved[li], dcur, self.gb[li],
+            cur, ck, _ = self.parts[li]
+            snn_neuron_bwd(d, kind, g, self.v[li], cur, ck, dcur, self.gb[li],
                            self.gv[li], rest, stream, dcur_scale=sc)
             hook("neuron_bwd_end", li)
             if d.synapse == SYN_DENSE:

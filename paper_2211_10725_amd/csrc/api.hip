@@ -77,8 +77,24 @@ snn_status check_desc(const snn_layer_desc *d) {
     return SNN_OK;
 }
 
-// byte offset of the pool selection inside the saved buffer (conv layers)
-size_t arg_offset(const snn_layer_desc *d) { return align_up((size_t)rows(d) * d->n_out * sizeof(float)); }
+// ---- saved state ------------------------------------------------------------
+// [currents fp32 T*B*n_out (not for SYN_NONE, whose x holds them)]
+// [checkpoints: planes (u; i too for SNN_SYNAPTIC) x count x B*n_out fp32]
+// [pool selection u8 T*B*n_out (conv only)], each on a 256-byte boundary
+snn_saved_layout saved_layout(const snn_layer_desc *d) {
+    snn_saved_layout l{};
+    const size_t el = (size_t)rows(d) * d->n_out;
+    l.cur_bytes = d->synapse == SNN_SYN_NONE ? 0 : align_up(el * sizeof(float));
+    l.ckpt_interval = kCheckpointInterval;
+    l.ckpt_count = (int32_t)neuron_ckpt_count(d->T);
+    l.ckpt_planes = d->neuron == SNN_SYNAPTIC ? 2 : 1;
+    l.ckpt_offset = l.cur_offset + l.cur_bytes;
+    l.ckpt_bytes = align_up((size_t)l.ckpt_planes * l.ckpt_count * d->B * d->n_out * sizeof(float));
+    l.pool_offset = l.ckpt_offset + l.ckpt_bytes;
+    l.pool_bytes = d->synapse == SNN_SYN_CONV5_POOL2 ? align_up(el) : 0;
+    l.bytes = l.pool_offset + l.pool_bytes;
+    return l;
+}
 
 // spike x fp32 contractions may use the exact three-pass bf16 kernels
 bool split_ok(const snn_layer_desc *d) { return (d->flags & SNN_FLAG_FP32_MFMA) == 0; }
@@ -301,9 +317,15 @@ const char *snn_status_str(snn_status s) {
 
 size_t snn_layer_saved_bytes(const snn_layer_desc *d) {
     if (check_desc(d) != SNN_OK) return 0;
-    size_t b = align_up((size_t)rows(d) * d->n_out * sizeof(float));
-    if (d->synapse == SNN_SYN_CONV5_POOL2) b += align_up((size_t)rows(d) * d->n_out);
-    return b;
+    return saved_layout(d).bytes;
+}
+
+snn_status snn_layer_saved_layout(const snn_layer_desc *d, snn_saved_layout *out) {
+    if (!out) return SNN_ERR_NULL;
+    snn_status st = check_desc(d);
+    if (st != SNN_OK) return st;
+    *out = saved_layout(d);
+    return SNN_OK;
 }
 
 size_t snn_layer_workspace_bytes(const snn_layer_desc *d) {
@@ -339,14 +361,16 @@ snn_status snn_synapse_fwd(const snn_layer_desc *d, const void *x, const void *w
 }
 
 snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float *v,
-                          void *spk_out, float *saved_u, float *counts, hipStream_t stream) {
+                          void *spk_out, float *ckpt, float *u_out, float *counts,
+                          hipStream_t stream) {
     snn_status st = check_desc(d);
     if (st != SNN_OK) return st;
-    if (!cur || !spk_out || !saved_u) return SNN_ERR_NULL;
+    if (!cur || !spk_out) return SNN_ERR_NULL;
+    if (neuron_ckpt_count(d->T) > 0 && d->B > 0 && !ckpt) return SNN_ERR_NULL;
     if (recurrent(d) && !v) return SNN_ERR_NULL;
     if (!recurrent(d)) v = nullptr;
-    if (!aligned16(cur) || !aligned16(spk_out) || !aligned16(saved_u) ||
-        (counts && !aligned16(counts)) || (v && !aligned16(v)))
+    if (!aligned16(cur) || !aligned16(spk_out) || (ckpt && !aligned16(ckpt)) ||
+        (u_out && !aligned16(u_out)) || (counts && !aligned16(counts)) || (v && !aligned16(v)))
         return SNN_ERR_ALIGN;
     (void)hipGetLastError();
     if (rows(d) == 0) {
@@ -356,17 +380,20 @@ snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float
     }
     const int64_t C = (int64_t)d->B * d->n_out;
     return hip_status(launch_neuron_fwd(d->neuron, d->T, C, d->n_out, d->alpha, d->beta,
-                                        d->threshold, v, cur, spk_out, d->out_dtype, saved_u,
+                                        d->threshold, v, cur, spk_out, d->out_dtype, u_out, ckpt,
                                         counts, stream));
 }
 
 snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const float *v,
-                          const float *saved_u, void *dcur, float *dcur_scale, float *grad_b,
-                          float *grad_v, void *ws, size_t ws_bytes, hipStream_t stream) {
+                          const float *cur, const float *ckpt, void *dcur, float *dcur_scale,
+                          float *grad_b, float *grad_v, void *ws, size_t ws_bytes,
+                          hipStream_t stream) {
     snn_status st = check_desc(d);
     if (st != SNN_OK) return st;
     if ((st = check_grad(d, grad)) != SNN_OK) return st;
-    if (!saved_u || !dcur) return SNN_ERR_NULL;
+    if (!cur || !dcur) return SNN_ERR_NULL;
+    if (neuron_ckpt_count(d->T) > 0 && d->B > 0 && !ckpt) return SNN_ERR_NULL;
+    if (ckpt && !aligned16(ckpt)) return SNN_ERR_ALIGN;
     if (scaled_grad(d)) {
         if (!dcur_scale) return SNN_ERR_NULL;
         if (!aligned16(dcur_scale)) return SNN_ERR_ALIGN;
@@ -379,7 +406,7 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
         if (grad_v) return SNN_ERR_SHAPE;  // no recurrent weight to differentiate
         v = nullptr;
     }
-    if (!aligned16(saved_u) || !aligned16(dcur) || (grad_b && !aligned16(grad_b)) ||
+    if (!aligned16(cur) || !aligned16(dcur) || (grad_b && !aligned16(grad_b)) ||
         (v && !aligned16(v)) || (grad_v && !aligned16(grad_v)))
         return SNN_ERR_ALIGN;
     if (grad_b && d->synapse == SNN_SYN_NONE) return SNN_ERR_SHAPE;  // no bias to differentiate
@@ -416,7 +443,7 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
         if (e != hipSuccess) return SNN_ERR_HIP;
     }
     e = launch_neuron_bwd(d->neuron, d->reset_grad, d->T, C, d->n_out, d->alpha, d->beta,
-                          d->threshold, d->slope, v, saved_u, bg, d->B, dcur, d->grad_dtype,
+                          d->threshold, d->slope, v, cur, ckpt, bg, d->B, dcur, d->grad_dtype,
                           dcur_scale, colsum, dvcol, stream);
     if (e != hipSuccess) return SNN_ERR_HIP;
     if (grad_b) {
@@ -533,15 +560,18 @@ snn_status snn_layer_fwd(const snn_layer_desc *d, const void *x, const void *w,
         (bias && !aligned16(bias)) || (counts && !aligned16(counts)))
         return SNN_ERR_ALIGN;
     if (fwd_ws(d) > ws_bytes) return SNN_ERR_WORKSPACE;
-    float *u = reinterpret_cast<float *>(saved);
+    const snn_saved_layout l = saved_layout(d);
+    char *sb = reinterpret_cast<char *>(saved);
+    float *ckpt = reinterpret_cast<float *>(sb + l.ckpt_offset);
     if (d->synapse == SNN_SYN_NONE)
-        return snn_neuron_fwd(d, reinterpret_cast<const float *>(x), v, spk_out, u, counts,
-                              stream);
+        return snn_neuron_fwd(d, reinterpret_cast<const float *>(x), v, spk_out, ckpt, nullptr,
+                              counts, stream);
+    float *cur = reinterpret_cast<float *>(sb + l.cur_offset);
     uint8_t *arg = nullptr;
-    if (d->synapse == SNN_SYN_CONV5_POOL2) arg = reinterpret_cast<uint8_t *>(saved) + arg_offset(d);
-    st = snn_synapse_fwd(d, x, w, bias, u, arg, ws, ws_bytes, stream);
+    if (d->synapse == SNN_SYN_CONV5_POOL2) arg = reinterpret_cast<uint8_t *>(sb + l.pool_offset);
+    st = snn_synapse_fwd(d, x, w, bias, cur, arg, ws, ws_bytes, stream);
     if (st != SNN_OK) return st;
-    return snn_neuron_fwd(d, u, v, spk_out, u, counts, stream);
+    return snn_neuron_fwd(d, cur, v, spk_out, ckpt, nullptr, counts, stream);
 }
 
 snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const void *x,
@@ -553,13 +583,17 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     if ((st = check_grad(d, grad)) != SNN_OK) return st;
     if (!saved) return SNN_ERR_NULL;
     if (!aligned16(saved)) return SNN_ERR_ALIGN;
-    const float *u = reinterpret_cast<const float *>(saved);
+    const snn_saved_layout l = saved_layout(d);
+    const char *sb = reinterpret_cast<const char *>(saved);
+    const float *ckpt = reinterpret_cast<const float *>(sb + l.ckpt_offset);
     if (d->synapse == SNN_SYN_NONE) {
         if (grad_w || grad_b) return SNN_ERR_SHAPE;
-        if (!grad_x) return SNN_ERR_NULL;
-        return snn_neuron_bwd(d, grad, v, u, grad_x, nullptr, nullptr, grad_v, ws, ws_bytes,
-                              stream);
+        if (!grad_x || !x) return SNN_ERR_NULL;
+        // the currents are the layer's input
+        return snn_neuron_bwd(d, grad, v, reinterpret_cast<const float *>(x), ckpt, grad_x,
+                              nullptr, nullptr, grad_v, ws, ws_bytes, stream);
     }
+    const float *cur = reinterpret_cast<const float *>(sb + l.cur_offset);
     if (grad_w && !x) return SNN_ERR_NULL;
     if (grad_x && !w) return SNN_ERR_NULL;
     if (bwd_ws(d) > ws_bytes || !ws) return SNN_ERR_WORKSPACE;
@@ -568,11 +602,12 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     char *colsum = base + dcur_bytes(d);
     float *scale = scaled_grad(d) ? reinterpret_cast<float *>(colsum + neuron_ws(d)) : nullptr;
     char *gws = colsum + neuron_ws(d) + scale_slot_bytes(d);
-    st = snn_neuron_bwd(d, grad, v, u, dcur, scale, grad_b, grad_v, colsum, neuron_ws(d), stream);
+    st = snn_neuron_bwd(d, grad, v, cur, ckpt, dcur, scale, grad_b, grad_v, colsum, neuron_ws(d),
+                        stream);
     if (st != SNN_OK) return st;
     if (!grad_w && !grad_x) return SNN_OK;
     const uint8_t *arg = nullptr;
-    if (d->synapse == SNN_SYN_CONV5_POOL2) arg = reinterpret_cast<const uint8_t *>(saved) + arg_offset(d);
+    if (d->synapse == SNN_SYN_CONV5_POOL2) arg = reinterpret_cast<const uint8_t *>(sb + l.pool_offset);
     return snn_synapse_bwd(d, dcur, scale, arg, x, w, grad_w, grad_x, gws, bwd_gemm_ws(d), stream);
 }
 

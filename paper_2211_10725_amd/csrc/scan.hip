@@ -8,6 +8,14 @@
 // next D steps do not depend on the state, so each lane keeps a ring of D
 // prefetched steps in registers to keep enough HBM requests in flight while
 // the sequential recurrence runs.
+//
+// Saved state: the backward needs u_t at every step (the surrogate is a
+// function of u_t alone).  Instead of writing u (4 B per step and column) the
+// forward writes the state every kCkpt steps (checkpoints: u, and i for the
+// current-based neuron), and the reverse scan recomputes each chunk of kCkpt
+// steps forward from its checkpoint and the currents, in registers and with
+// the forward's exact fp32 operations (so u is bit-identical), before
+// running the chunk backwards.
 #include <atomic>
 
 #include "snn_internal.hpp"
@@ -22,6 +30,7 @@ constexpr int kThreads = 256;
 // column and 16 steps, which gives 4x the waves and halves the number of
 // exposed memory round trips of the serial scan.
 constexpr int kWideColumns = 4 * 64 * 2048;  // 2048 waves of 4-column lanes
+constexpr int kCkpt = kCheckpointInterval;  // steps per recomputed chunk
 constexpr int kFoldMax = 16;   // most outputs of a dense layer whose input gradient is folded
 constexpr int kFoldRows = 5;   // batch rows one workgroup's columns can span when folding
 
@@ -38,6 +47,16 @@ struct Vec<4> {
     }
 };
 template <>
+struct Vec<2> {
+    static __device__ inline void load(const float *p, float (&v)[2]) {
+        const float2 x = *reinterpret_cast<const float2 *>(p);
+        v[0] = x.x; v[1] = x.y;
+    }
+    static __device__ inline void store(float *p, const float (&v)[2]) {
+        *reinterpret_cast<float2 *>(p) = make_float2(v[0], v[1]);
+    }
+};
+template <>
 struct Vec<1> {
     static __device__ inline void load(const float *p, float (&v)[1]) { v[0] = *p; }
     static __device__ inline void store(float *p, const float (&v)[1]) { *p = v[0]; }
@@ -50,6 +69,8 @@ __device__ inline void store_spikes_u8(uint8_t *p, const float (&z)[VEC]) {
         const uint32_t w = (uint32_t)z[0] | ((uint32_t)z[1] << 8) | ((uint32_t)z[2] << 16) |
                            ((uint32_t)z[3] << 24);
         *reinterpret_cast<uint32_t *>(p) = w;
+    } else if constexpr (VEC == 2) {
+        *reinterpret_cast<uint16_t *>(p) = (uint16_t)((uint32_t)z[0] | ((uint32_t)z[1] << 8));
     } else {
         p[0] = (uint8_t)z[0];
     }
@@ -62,25 +83,53 @@ __device__ inline void store_spikes_f16(uint16_t *p, const float (&z)[VEC]) {
         const uint32_t lo = (z[0] != 0.f ? 0x3c00u : 0u) | (z[1] != 0.f ? 0x3c000000u : 0u);
         const uint32_t hi = (z[2] != 0.f ? 0x3c00u : 0u) | (z[3] != 0.f ? 0x3c000000u : 0u);
         *reinterpret_cast<uint2 *>(p) = make_uint2(lo, hi);
+    } else if constexpr (VEC == 2) {
+        *reinterpret_cast<uint32_t *>(p) =
+            (z[0] != 0.f ? 0x3c00u : 0u) | (z[1] != 0.f ? 0x3c000000u : 0u);
     } else {
         p[0] = z[0] != 0.f ? 0x3c00u : 0u;
     }
 }
 
-// Forward scan.  `cur` and `u_out` may alias exactly: each lane reads step t
-// of its columns before it writes step t, and prefetches only later steps.
-// The recurrent neuron (eq. 7) adds its own previous spike through the
-// recurrent weight: a spike at t-1 adds (v - thr) to u_t instead of the
-// plain reset -thr; column c is neuron c % N, vrec holds v per neuron.
+// One step of the forward recurrence for one column (eqs. 3-7), in the exact
+// fp32 operations both scans use: the decay-plus-input term as one fused
+// multiply-add, then the reset (eq. 7: plus the recurrent weight) if the
+// previous step spiked.  Returns the new membrane; the spike is u > thr.
+template <int NEURON>
+__device__ inline float neuron_step(float &u, float &syn, float zp, float in, float alpha,
+                                    float beta, float jump) {
+    float uu;
+    if constexpr (NEURON == SNN_SYNAPTIC) {
+        syn = __builtin_fmaf(alpha, syn, in);
+        uu = __builtin_fmaf(beta, u, syn);
+    } else {
+        uu = __builtin_fmaf(beta, u, in);
+    }
+    uu = (zp != 0.f) ? uu + jump : uu;
+    u = uu;
+    return uu;
+}
+
+// Forward scan.  Writes the spikes, the spike counts (nullable), the full
+// membrane (u_out, nullable; it may alias cur exactly: each lane reads step
+// t before it writes it) and the checkpoints: after step t with
+// (t + 1) % kCkpt == 0 and t + 1 < T, u to ckpt[(t + 1) / kCkpt - 1][C]
+// and, for the current-based neuron, i to the same slot of a second plane
+// nck chunks further.  The recurrent neuron (eq. 7) adds its own previous
+// spike through the recurrent weight: a spike at t-1 adds (v - thr) to u_t
+// instead of the plain reset -thr; column c is neuron c % N.
 template <int NEURON, int VEC, int OUT, int kDepth>
 __global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, int64_t N,
                                                               float alpha, float beta, float thr,
                                                               const float *__restrict__ vrec,
                                                               const float *cur, void *spk,
                                                               float *u_out,
+                                                              float *__restrict__ ckpt,
                                                               float *__restrict__ counts) {
+    static_assert(kCkpt % kDepth == 0, "checkpoints fall on block boundaries");
     const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
     if (col >= C) return;
+    const int nck = (T - 1) / kCkpt;
     float u[VEC], syn[VEC], zp[VEC], cnt[VEC], jump[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
@@ -105,27 +154,25 @@ __global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, 
                 float z[VEC];
 #pragma unroll
                 for (int v = 0; v < VEC; ++v) {
-                    float uu;
-                    if constexpr (NEURON == SNN_SYNAPTIC) {
-                        syn[v] = __builtin_fmaf(alpha, syn[v], in[j][v]);
-                        uu = __builtin_fmaf(beta, u[v], syn[v]);
-                    } else {
-                        uu = __builtin_fmaf(beta, u[v], in[j][v]);
-                    }
-                    // reset by subtraction (eq. 7: plus the recurrent weight)
-                    uu = (zp[v] != 0.f) ? uu + jump[v] : uu;
-                    u[v] = uu;
+                    const float uu = neuron_step<NEURON>(u[v], syn[v], zp[v], in[j][v], alpha,
+                                                         beta, jump[v]);
                     z[v] = (uu > thr) ? 1.f : 0.f;       // eq. (3), strict
                     zp[v] = z[v];
                     cnt[v] += z[v];
                 }
                 const int64_t off = (int64_t)t * C + col;
-                Vec<VEC>::store(u_out + off, u);
+                if (u_out) Vec<VEC>::store(u_out + off, u);
                 if constexpr (OUT == SNN_U8)
                     store_spikes_u8<VEC>(reinterpret_cast<uint8_t *>(spk) + off, z);
                 else
                     store_spikes_f16<VEC>(reinterpret_cast<uint16_t *>(spk) + off, z);
             }
+        }
+        const int tn = t0 + kDepth;  // steps done
+        if (tn % kCkpt == 0 && tn < T) {
+            const int64_t slot = (int64_t)(tn / kCkpt - 1) * C + col;
+            Vec<VEC>::store(ckpt + slot, u);
+            if constexpr (NEURON == SNN_SYNAPTIC) Vec<VEC>::store(ckpt + (int64_t)nck * C + slot, syn);
         }
 #pragma unroll
         for (int j = 0; j < kDepth; ++j)
@@ -162,6 +209,8 @@ __device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC]
         if constexpr (VEC == 4)
             *reinterpret_cast<uint2 *>(p) =
                 make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+        else if constexpr (VEC == 2)
+            *reinterpret_cast<uint32_t *>(p) = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
         else
             p[0] = h[0];
     }
@@ -177,9 +226,9 @@ constexpr int GM_FOLD12 = 3; // the same for at most 12 outputs (10 classes)
 
 // The layer above, for GM_FOLD.  A workgroup's 256 VEC consecutive columns
 // span at most kFoldRows batch rows (the launcher only folds layers with
-// n >= 64, and n >= 256 for VEC = 4); the dI_up rows of those batch rows for
-// one block of kDepth steps are staged in LDS (double-buffered, one barrier
-// per block), the next block's loaded into registers while this one runs.
+// n >= 64, and n >= 128 for VEC = 2); the dI_up rows of those batch rows for
+// one chunk of kCkpt steps are staged in LDS (double-buffered, one barrier
+// per chunk), the next chunk's loaded into registers while this one runs.
 struct FoldIn {
     const void *dup;  // [T, B, nup] of dt_up
     const void *wup;  // [nup, N] of dt_w
@@ -193,22 +242,22 @@ __device__ inline float load_as_f32(const void *p, int64_t i, int dt) {
     return (float)__builtin_bit_cast(_Float16, h);
 }
 
-template <int kDepth, int KF>
+template <int KF>
 struct FoldStage {
-    static constexpr int kElems = kDepth * kFoldRows * KF;
+    static constexpr int kElems = kCkpt * kFoldRows * KF;
     static constexpr int kPer = (kElems + 255) / 256;  // per thread (256-thread blocks)
     float v[kPer];
 
-    // the dI_up values of steps t0, t0 - 1, ..., t0 - kDepth + 1 and batch
+    // the dI_up values of the steps t0 .. t0 + kCkpt - 1 of a chunk and batch
     // rows b_lo .. b_lo + kFoldRows - 1 (zeros outside)
-    __device__ inline void load(const FoldIn &f, int t0, int64_t b_lo) {
+    __device__ inline void load(const FoldIn &f, int T, int t0, int64_t b_lo) {
 #pragma unroll
         for (int i = 0; i < kPer; ++i) {
             const int e = threadIdx.x + i * 256;
             const int jt = e / (kFoldRows * KF), bb = (e / KF) % kFoldRows, j = e % KF;
-            const int t = t0 - jt;
+            const int t = t0 + jt;
             const int64_t b = b_lo + bb;
-            v[i] = (e < kElems && t >= 0 && b < f.B && j < f.nup)
+            v[i] = (e < kElems && t < T && b < f.B && j < f.nup)
                        ? load_as_f32(f.dup, ((int64_t)t * f.B + b) * f.nup + j, f.dt_up)
                        : 0.f;
         }
@@ -222,40 +271,45 @@ struct FoldStage {
     }
 };
 
-// Reverse-time scan.  lam carries dL/du_{t+1} (and lami dL/di_{t+1}).
+// Reverse-time scan over chunks of kCkpt steps, last chunk first.  For each
+// chunk the lane loads its currents and the checkpoint before it (prefetched
+// while the previous chunk runs), recomputes u_t forward in registers, then
+// runs the adjoint backwards.  lam carries dL/du_{t+1} (and lami dL/di_{t+1}).
 // For the recurrent neuron the spike z_t reaches u_{t+1} through
 // (v - r thr), so the carry is beta + (v - r thr) s_t, and the recurrent
 // weight's gradient collects lam_{t+1} z_t per column (dvcol, fp32).
-template <int NEURON, int VEC, int GM, bool RESET_SURR, int GT, int kDepth>
+template <int NEURON, int VEC, int GM, bool RESET_SURR, int GT>
 __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
     int T, int64_t C, int64_t N, float alpha, float beta, float thr, float slope,
-    const float *__restrict__ vrec, const float *__restrict__ u, const float *__restrict__ g,
-    FoldIn fold, void *__restrict__ dcur, const float *__restrict__ dscale,
-    float *__restrict__ colsum, float *__restrict__ dvcol) {
+    const float *__restrict__ vrec, const float *__restrict__ cur, const float *__restrict__ ckpt,
+    const float *__restrict__ g, FoldIn fold, void *__restrict__ dcur,
+    const float *__restrict__ dscale, float *__restrict__ colsum, float *__restrict__ dvcol) {
     constexpr bool BCAST = GM == GM_BCAST, FOLD = GM == GM_FOLD || GM == GM_FOLD12;
+    constexpr bool FULL = GM == GM_FULL;
+    constexpr int K = kCkpt;
     const float scale = GT == SNN_F16 ? *dscale : 1.f;
     constexpr int KF = GM == GM_FOLD12 ? 12 : kFoldMax;  // dI_up values per row (padded)
     const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
     // the fold's lanes past the last column still take part in the staging
     const bool active = col < C;
     if (!FOLD && !active) return;
-    float lam[VEC], lami[VEC], acc[VEC], gb[VEC], vr[VEC], dv[VEC];
+    const int nch = (T + K - 1) / K, nck = nch - 1;
+    float lam[VEC], lami[VEC], acc[VEC], gb[VEC], vr[VEC], dv[VEC], jump[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
         lam[v] = lami[v] = acc[v] = gb[v] = dv[v] = 0.f;
-        if constexpr (NEURON == SNN_RLEAKY)
-            vr[v] = active ? (RESET_SURR ? vrec[(col + v) % N] - thr : vrec[(col + v) % N]) : 0.f;
-        else
-            vr[v] = 0.f;
+        const float vv = (NEURON == SNN_RLEAKY && active) ? vrec[(col + v) % N] : 0.f;
+        jump[v] = NEURON == SNN_RLEAKY ? vv - thr : -thr;
+        vr[v] = NEURON == SNN_RLEAKY ? (RESET_SURR ? vv - thr : vv) : 0.f;
     }
     if constexpr (BCAST) Vec<VEC>::load(g + col, gb);
 
     // fold: the lane's columns of W_up, its batch row within the staged rows
-    __shared__ __attribute__((aligned(16))) float frows[FOLD ? 2 : 1][FOLD ? FoldStage<kDepth, KF>::kElems : 1];
+    __shared__ __attribute__((aligned(16))) float frows[FOLD ? 2 : 1][FOLD ? FoldStage<KF>::kElems : 1];
     float wcol[FOLD ? VEC : 1][FOLD ? KF : 1];
     int fbb = 0;
     int64_t b_lo = 0;
-    FoldStage<kDepth, KF> fst;
+    FoldStage<KF> fst;
     if constexpr (FOLD) {
         b_lo = ((int64_t)blockIdx.x * kThreads * VEC) / N;
         fbb = active ? (int)(col / N - b_lo) : 0;
@@ -266,37 +320,68 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
                 wcol[v][j] = (active && j < fold.nup)
                                  ? load_as_f32(fold.wup, (int64_t)j * N + (col + v) % N, fold.dt_w)
                                  : 0.f;
-        fst.load(fold, T - 1, b_lo);
-        fst.store(frows[0]);
-        if (T - 1 - kDepth >= 0) fst.load(fold, T - 1 - kDepth, b_lo);
+        fst.load(fold, T, nck * K, b_lo);
+        fst.store(frows[nck & 1]);
+        if (nck >= 1) fst.load(fold, T, (nck - 1) * K, b_lo);
         __syncthreads();
     }
 
-    float uu[kDepth][VEC], nu[kDepth][VEC];
-    float gg[GM == GM_FULL ? kDepth : 1][VEC], ng[GM == GM_FULL ? kDepth : 1][VEC];
+    // chunk registers: currents (then the recomputed membrane) of this chunk
+    // and of the one before it, the full upstream gradient likewise, and the
+    // checkpointed state at the start of each
+    float ii[K][VEC], ni[K][VEC];
+    float gg[FULL ? K : 1][VEC], ng[FULL ? K : 1][VEC];
+    float cu[VEC], ci[VEC], nu[VEC], nci[VEC];
+    auto load_chunk = [&](int c, float (&xi)[K][VEC], float (&xg)[FULL ? K : 1][VEC],
+                          float (&su)[VEC], float (&si)[VEC]) {
+        const int t_lo = c * K;
 #pragma unroll
-    for (int j = 0; j < kDepth; ++j) {
-        const int t = T - 1 - j;
-        if (t >= 0 && active) {
-            Vec<VEC>::load(u + (int64_t)t * C + col, uu[j]);
-            if constexpr (GM == GM_FULL) Vec<VEC>::load(g + (int64_t)t * C + col, gg[j]);
-        }
-    }
-    int blk = 0;
-    for (int t0 = T - 1; t0 >= 0; t0 -= kDepth, ++blk) {
-#pragma unroll
-        for (int j = 0; j < kDepth; ++j) {
-            const int t = t0 - kDepth - j;
-            if (t >= 0 && active) {
-                Vec<VEC>::load(u + (int64_t)t * C + col, nu[j]);
-                if constexpr (GM == GM_FULL) Vec<VEC>::load(g + (int64_t)t * C + col, ng[j]);
+        for (int j = 0; j < K; ++j) {
+            if (t_lo + j < T) {
+                Vec<VEC>::load(cur + (int64_t)(t_lo + j) * C + col, xi[j]);
+                if constexpr (FULL) Vec<VEC>::load(g + (int64_t)(t_lo + j) * C + col, xg[j]);
             }
         }
-        const float *fr = FOLD ? frows[blk & 1] : nullptr;
+        if (c > 0) {
+            Vec<VEC>::load(ckpt + (int64_t)(c - 1) * C + col, su);
+            if constexpr (NEURON == SNN_SYNAPTIC)
+                Vec<VEC>::load(ckpt + (int64_t)(nck + c - 1) * C + col, si);
+            else
 #pragma unroll
-        for (int j = 0; j < kDepth; ++j) {
-            const int t = t0 - j;
-            if (t >= 0 && active) {
+                for (int v = 0; v < VEC; ++v) si[v] = 0.f;
+        } else {
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) su[v] = si[v] = 0.f;
+        }
+    };
+    if (active) load_chunk(nck, ii, gg, cu, ci);
+
+    for (int c = nck; c >= 0; --c) {
+        const int t_lo = c * K;
+        if (active) {
+            if (c > 0) load_chunk(c - 1, ni, ng, nu, nci);
+            // recompute u_t of the chunk from the state before it (u_{t_lo-1},
+            // i_{t_lo-1}; z_{t_lo-1} = [u_{t_lo-1} > thr]), in place of I_t
+#pragma unroll
+            for (int v = 0; v < VEC; ++v) {
+                float u = cu[v], syn = ci[v];
+                float zp = (c > 0 && cu[v] > thr) ? 1.f : 0.f;
+#pragma unroll
+                for (int j = 0; j < K; ++j) {
+                    if (t_lo + j < T) {
+                        const float uu = neuron_step<NEURON>(u, syn, zp, ii[j][v], alpha, beta,
+                                                             jump[v]);
+                        ii[j][v] = uu;
+                        zp = (uu > thr) ? 1.f : 0.f;
+                    }
+                }
+            }
+        }
+        const float *fr = FOLD ? frows[c & 1] : nullptr;
+#pragma unroll
+        for (int j = K - 1; j >= 0; --j) {
+            const int t = t_lo + j;
+            if (t < T && active) {
                 float d[VEC];
                 float grow[FOLD ? KF : 1];
                 if constexpr (FOLD) {
@@ -311,7 +396,8 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
                 }
 #pragma unroll
                 for (int v = 0; v < VEC; ++v) {
-                    const float e = 1.f + slope * __builtin_fabsf(uu[j][v] - thr);
+                    const float uu = ii[j][v];
+                    const float e = 1.f + slope * __builtin_fabsf(uu - thr);
                     const float s = __builtin_amdgcn_rcpf(e * e);  // eq. (9) with slope
                     float gt;
                     if constexpr (BCAST) {
@@ -325,7 +411,7 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
                     }
                     float carry = beta;
                     if constexpr (NEURON == SNN_RLEAKY) {
-                        if (uu[j][v] > thr) dv[v] += lam[v];  // lam_{t+1} z_t
+                        if (uu > thr) dv[v] += lam[v];  // lam_{t+1} z_t
                         carry = __builtin_fmaf(vr[v], s, beta);
                     } else if constexpr (RESET_SURR) {
                         carry = beta - thr * s;
@@ -343,21 +429,26 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
             }
         }
         if constexpr (FOLD) {
-            // stage the next block (its buffer was last read before the
+            // stage the next chunk (its buffer was last read before the
             // previous barrier), then load the one after it
-            if (t0 - kDepth >= 0) {
-                fst.store(frows[(blk + 1) & 1]);
-                if (t0 - 2 * kDepth >= 0) fst.load(fold, t0 - 2 * kDepth, b_lo);
+            if (c >= 1) {
+                fst.store(frows[(c - 1) & 1]);
+                if (c >= 2) fst.load(fold, T, (c - 2) * K, b_lo);
             }
             __syncthreads();
         }
 #pragma unroll
-        for (int j = 0; j < kDepth; ++j)
+        for (int j = 0; j < K; ++j)
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
-                uu[j][v] = nu[j][v];
-                if constexpr (GM == GM_FULL) gg[j][v] = ng[j][v];
+                ii[j][v] = ni[j][v];
+                if constexpr (FULL) gg[j][v] = ng[j][v];
             }
+#pragma unroll
+        for (int v = 0; v < VEC; ++v) {
+            cu[v] = nu[v];
+            ci[v] = nci[v];
+        }
     }
     if (!active) return;
     if (colsum) Vec<VEC>::store(colsum + col, acc);
@@ -501,24 +592,28 @@ struct ScanArgs {
     const float *vrec;
 };
 
+struct FwdBuffers {
+    const float *cur;
+    void *spk;
+    float *u_out, *ckpt, *counts;
+};
+
 template <int NEURON, int VEC, int OUT>
-void fwd_launch(const ScanArgs &a, const float *cur, void *spk, float *u_out, float *counts,
-                hipStream_t s) {
+void fwd_launch(const ScanArgs &a, const FwdBuffers &b, hipStream_t s) {
     const int64_t lanes = (a.C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_fwd_kernel<NEURON, VEC, OUT, VEC == 4 ? 6 : 16><<<grid, kThreads, 0, s>>>(
-        a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.vrec, cur, spk, u_out, counts);
+    neuron_fwd_kernel<NEURON, VEC, OUT, VEC == 4 ? 8 : 16><<<grid, kThreads, 0, s>>>(
+        a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.vrec, b.cur, b.spk, b.u_out, b.ckpt, b.counts);
 }
 
 template <int NEURON, int VEC>
-void fwd_dispatch(int out_dtype, const ScanArgs &a, const float *cur, void *spk, float *u_out,
-                  float *counts, hipStream_t s) {
-    if (out_dtype == SNN_U8) fwd_launch<NEURON, VEC, SNN_U8>(a, cur, spk, u_out, counts, s);
-    else fwd_launch<NEURON, VEC, SNN_F16>(a, cur, spk, u_out, counts, s);
+void fwd_dispatch(int out_dtype, const ScanArgs &a, const FwdBuffers &b, hipStream_t s) {
+    if (out_dtype == SNN_U8) fwd_launch<NEURON, VEC, SNN_U8>(a, b, s);
+    else fwd_launch<NEURON, VEC, SNN_F16>(a, b, s);
 }
 
 struct BwdBuffers {
-    const float *u, *g;
+    const float *cur, *ckpt, *g;
     FoldIn fold;
     void *dcur;
     const float *dscale;
@@ -529,12 +624,9 @@ template <int NEURON, int VEC, int GM, bool RS, int GT>
 void bwd_launch(const ScanArgs &a, const BwdBuffers &b, hipStream_t s) {
     const int64_t lanes = (a.C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    // steps loaded ahead per lane; the folded scan does better with 8 than 16
-    // (34 against 38 us on the 12800 x 1000 synaptic layer, T = 50)
-    constexpr bool FOLD = GM == GM_FOLD || GM == GM_FOLD12;
-    neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, VEC == 4 ? 6 : FOLD ? 8 : 16><<<grid, kThreads, 0, s>>>(
-        a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.u, b.g, b.fold, b.dcur,
-        b.dscale, b.colsum, b.dvcol);
+    neuron_bwd_kernel<NEURON, VEC, GM, RS, GT><<<grid, kThreads, 0, s>>>(
+        a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.cur, b.ckpt, b.g, b.fold,
+        b.dcur, b.dscale, b.colsum, b.dvcol);
 }
 
 template <int NEURON, int VEC, int GM, bool RS>
@@ -550,35 +642,53 @@ void bwd_dispatch_rs(int rs, int gt, const ScanArgs &a, const BwdBuffers &b, hip
     else bwd_dispatch_gt<NEURON, VEC, GM, false>(gt, a, b, s);
 }
 
-template <int NEURON, int VEC>
-void bwd_dispatch(int rs, int gm, int gt, const ScanArgs &a, const BwdBuffers &b,
+// Lane widths: four columns for layers of at least kWideColumns columns
+// (two with a full upstream gradient, whose chunk also holds kCkpt steps of
+// g per column, and two with a folded one, whose lanes also hold their
+// columns of W_up), else one.
+template <int NEURON>
+void bwd_dispatch(int vec, int rs, int gm, int gt, const ScanArgs &a, const BwdBuffers &b,
                   hipStream_t s) {
-    if (gm == GM_BCAST) bwd_dispatch_rs<NEURON, VEC, GM_BCAST>(rs, gt, a, b, s);
-    else if (gm == GM_FOLD12) bwd_dispatch_rs<NEURON, VEC, GM_FOLD12>(rs, gt, a, b, s);
-    else if (gm == GM_FOLD) bwd_dispatch_rs<NEURON, VEC, GM_FOLD>(rs, gt, a, b, s);
-    else bwd_dispatch_rs<NEURON, VEC, GM_FULL>(rs, gt, a, b, s);
+    if (gm == GM_BCAST) {
+        if (vec == 4) bwd_dispatch_rs<NEURON, 4, GM_BCAST>(rs, gt, a, b, s);
+        else bwd_dispatch_rs<NEURON, 1, GM_BCAST>(rs, gt, a, b, s);
+    } else if (gm == GM_FOLD12) {
+        if (vec == 2) bwd_dispatch_rs<NEURON, 2, GM_FOLD12>(rs, gt, a, b, s);
+        else bwd_dispatch_rs<NEURON, 1, GM_FOLD12>(rs, gt, a, b, s);
+    } else if (gm == GM_FOLD) {
+        if (vec == 2) bwd_dispatch_rs<NEURON, 2, GM_FOLD>(rs, gt, a, b, s);
+        else bwd_dispatch_rs<NEURON, 1, GM_FOLD>(rs, gt, a, b, s);
+    } else {
+        if (vec == 2) bwd_dispatch_rs<NEURON, 2, GM_FULL>(rs, gt, a, b, s);
+        else bwd_dispatch_rs<NEURON, 1, GM_FULL>(rs, gt, a, b, s);
+    }
 }
 
 }  // namespace
 
+int64_t neuron_ckpt_count(int T) { return T > 0 ? (T - 1) / kCkpt : 0; }
+
 hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, int64_t N, float alpha, float beta,
                              float thr, const float *vrec, const float *cur, void *spk,
-                             int out_dtype, float *u_out, float *counts, hipStream_t s) {
+                             int out_dtype, float *u_out, float *ckpt, float *counts,
+                             hipStream_t s) {
     if (T <= 0 || C <= 0) return hipSuccess;
+    if (neuron_ckpt_count(T) > 0 && ckpt == nullptr) return hipErrorInvalidValue;
     const bool v4 = (C % 4) == 0 && C >= kWideColumns;
     const ScanArgs a{T, C, N, alpha, beta, thr, 0.f, vrec};
+    const FwdBuffers b{cur, spk, u_out, ckpt, counts};
     switch (neuron) {
         case SNN_SYNAPTIC:
-            if (v4) fwd_dispatch<SNN_SYNAPTIC, 4>(out_dtype, a, cur, spk, u_out, counts, s);
-            else fwd_dispatch<SNN_SYNAPTIC, 1>(out_dtype, a, cur, spk, u_out, counts, s);
+            if (v4) fwd_dispatch<SNN_SYNAPTIC, 4>(out_dtype, a, b, s);
+            else fwd_dispatch<SNN_SYNAPTIC, 1>(out_dtype, a, b, s);
             break;
         case SNN_RLEAKY:
-            if (v4) fwd_dispatch<SNN_RLEAKY, 4>(out_dtype, a, cur, spk, u_out, counts, s);
-            else fwd_dispatch<SNN_RLEAKY, 1>(out_dtype, a, cur, spk, u_out, counts, s);
+            if (v4) fwd_dispatch<SNN_RLEAKY, 4>(out_dtype, a, b, s);
+            else fwd_dispatch<SNN_RLEAKY, 1>(out_dtype, a, b, s);
             break;
         default:
-            if (v4) fwd_dispatch<SNN_LEAKY, 4>(out_dtype, a, cur, spk, u_out, counts, s);
-            else fwd_dispatch<SNN_LEAKY, 1>(out_dtype, a, cur, spk, u_out, counts, s);
+            if (v4) fwd_dispatch<SNN_LEAKY, 4>(out_dtype, a, b, s);
+            else fwd_dispatch<SNN_LEAKY, 1>(out_dtype, a, b, s);
     }
     return hipGetLastError();
 }
@@ -587,35 +697,36 @@ bool neuron_fold_supported(int64_t N) { return N >= 64; }
 
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
-                             const float *u, const BwdGrad &grad, int B, void *dcur,
-                             int grad_dtype, const float *dscale, float *colsum, float *dvcol,
-                             hipStream_t s) {
+                             const float *cur, const float *ckpt, const BwdGrad &grad, int B,
+                             void *dcur, int grad_dtype, const float *dscale, float *colsum,
+                             float *dvcol, hipStream_t s) {
     if (grad_dtype == SNN_F16 && dscale == nullptr) return hipErrorInvalidValue;
     if (T <= 0 || C <= 0) return hipSuccess;
+    if (neuron_ckpt_count(T) > 0 && ckpt == nullptr) return hipErrorInvalidValue;
     int gm = grad.mode == SNN_GRAD_FOLD ? GM_FOLD
              : grad.mode == SNN_GRAD_BCAST ? GM_BCAST : GM_FULL;
     if (gm == GM_FOLD && (!neuron_fold_supported(N) || grad.nup < 1 || grad.nup > kFoldMax))
         return hipErrorInvalidValue;
     if (gm == GM_FOLD && grad.nup <= 12) gm = GM_FOLD12;
-    bool v4 = (C % 4) == 0 && C >= kWideColumns;
-    // a lane's four columns in one batch row, and at most kFoldRows rows per workgroup
-    if ((gm == GM_FOLD || gm == GM_FOLD12) && v4 && (N % 4 != 0 || N < 256)) v4 = false;
+    const bool wide = C >= kWideColumns;
+    int vec = 1;
+    if (gm == GM_FULL) {
+        if (wide && C % 2 == 0) vec = 2;
+    } else if (gm == GM_BCAST) {
+        if (wide && C % 4 == 0) vec = 4;
+    } else if (wide && N % 2 == 0 && N >= 128) {
+        // a lane's two columns in one batch row, and the workgroup's 512
+        // columns within kFoldRows batch rows
+        vec = 2;
+    }
     const ScanArgs a{T, C, N, alpha, beta, thr, slope, vrec};
     const FoldIn fold{grad.dup, grad.wup, grad.nup, grad.dt_up, grad.dt_w, B};
-    const BwdBuffers b{u, grad.g, fold, dcur, dscale, colsum, dvcol};
+    const BwdBuffers b{cur, ckpt, grad.g, fold, dcur, dscale, colsum, dvcol};
     const int rs = reset_surrogate, gt = grad_dtype;
     switch (neuron) {
-        case SNN_SYNAPTIC:
-            if (v4) bwd_dispatch<SNN_SYNAPTIC, 4>(rs, gm, gt, a, b, s);
-            else bwd_dispatch<SNN_SYNAPTIC, 1>(rs, gm, gt, a, b, s);
-            break;
-        case SNN_RLEAKY:
-            if (v4) bwd_dispatch<SNN_RLEAKY, 4>(rs, gm, gt, a, b, s);
-            else bwd_dispatch<SNN_RLEAKY, 1>(rs, gm, gt, a, b, s);
-            break;
-        default:
-            if (v4) bwd_dispatch<SNN_LEAKY, 4>(rs, gm, gt, a, b, s);
-            else bwd_dispatch<SNN_LEAKY, 1>(rs, gm, gt, a, b, s);
+        case SNN_SYNAPTIC: bwd_dispatch<SNN_SYNAPTIC>(vec, rs, gm, gt, a, b, s); break;
+        case SNN_RLEAKY: bwd_dispatch<SNN_RLEAKY>(vec, rs, gm, gt, a, b, s); break;
+        default: bwd_dispatch<SNN_LEAKY>(vec, rs, gm, gt, a, b, s);
     }
     return hipGetLastError();
 }

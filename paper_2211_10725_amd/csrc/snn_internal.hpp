@@ -45,11 +45,19 @@ inline size_t dtype_bytes(int dt) {
 int device_cus();
 
 // ---- neuron scans (scan.hip) ---------------------------------------------
+// The forward saves the neuron state every kCheckpointInterval steps; the
+// reverse scan recomputes each chunk from it and the currents.  Checkpoint c
+// (0 <= c < neuron_ckpt_count(T)) is the state after step (c + 1) K - 1:
+// ckpt[c][C] holds u and, for SNN_SYNAPTIC, ckpt[count + c][C] holds i.
+constexpr int kCheckpointInterval = 16;
+int64_t neuron_ckpt_count(int T);
 // Forward: C = B * N independent columns, time-major [T, C]; vrec [N] holds
 // the recurrent weights of SNN_RLEAKY (column c is neuron c % N), else unused.
+// u_out (nullable) receives the membrane of every step.
 hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, int64_t N, float alpha, float beta,
                              float thr, const float *vrec, const float *cur, void *spk,
-                             int out_dtype, float *u_out, float *counts, hipStream_t s);
+                             int out_dtype, float *u_out, float *ckpt, float *counts,
+                             hipStream_t s);
 
 // Upstream gradient of the reverse scan: g [T, C] (SNN_GRAD_FULL), g [C] for
 // every t (SNN_GRAD_BCAST), or, for SNN_GRAD_FOLD, computed in the scan as
@@ -69,9 +77,9 @@ bool neuron_fold_supported(int64_t N);
 // of two S read from dscale[0] (launch_grad_scale writes it).
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
-                             const float *u, const BwdGrad &grad, int B, void *dcur,
-                             int grad_dtype, const float *dscale, float *colsum, float *dvcol,
-                             hipStream_t s);
+                             const float *cur, const float *ckpt, const BwdGrad &grad, int B,
+                             void *dcur, int grad_dtype, const float *dscale, float *colsum,
+                             float *dvcol, hipStream_t s);
 // scale[0] = S = 2^e, the largest power of two with G * growth * S <= 2^15,
 // G a bound on |g| over the upstream gradient (device reduction into
 // `scratch`, grad_scale_workspace_bytes()); growth bounds |dL/dI| / G.

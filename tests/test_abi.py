@@ -87,8 +87,8 @@ def test_fold_validation():
     d = _dense(T=4, B=3, n_in=20, n_out=100)
 
     def bwd(gi, desc=d):
-        return L.snn_neuron_bwd(ctypes.byref(desc), ctypes.byref(gi), None, 64, 80 + 1, None,
-                                None, None, None, 0, None)
+        return L.snn_neuron_bwd(ctypes.byref(desc), ctypes.byref(gi), None, 64, 128, 80 + 1,
+                                None, None, None, None, 0, None)
 
     F = snn.GRAD_FOLD
     assert bwd(snn.GradIn(F, 10, None, 96, 112, snn.F32, snn.F32)) == 4     # valid up to dcur
@@ -132,8 +132,52 @@ def test_sizes_queries():
     assert ws >= 25 * 32 * 1000 * 4          # holds dL/dI for the backward
     bad = d.copy(); bad.n_in = 0
     assert snn.snn_layer_saved_bytes(bad) == 0
+    # the scan-only layer keeps only checkpoints: its currents are its input
     none = snn.layer_desc(dict(kind="none", n=65536, neuron="leaky", beta=0.95), 1000, 64)
-    assert snn.snn_layer_saved_bytes(none) == 1000 * 64 * 65536 * 4
+    assert snn.snn_layer_saved_bytes(none) == ((1000 - 1) // 16) * 64 * 65536 * 4
+
+
+def _al(x):
+    return (x + 255) // 256 * 256
+
+
+@pytest.mark.parametrize("kind,neuron,T,B", [("dense", "leaky", 25, 32), ("dense", "synaptic", 50, 7),
+                                             ("dense", "rleaky", 16, 3), ("dense", "leaky", 17, 3),
+                                             ("dense", "leaky", 1, 5), ("conv", "leaky", 25, 4),
+                                             ("none", "synaptic", 33, 2), ("none", "leaky", 0, 2)])
+def test_saved_layout(kind, neuron, T, B):
+    """The saved state's parts as the library lays them out: the currents
+    (not for a scan-only layer), a checkpoint after every 16th step but the
+    last (u, and i for the current-based neuron), the conv pool selection;
+    on 256-byte boundaries, disjoint, inside snn_layer_saved_bytes."""
+    if kind == "conv":
+        spec = dict(kind="conv", c_in=2, h=12, w=10, c_out=3, neuron=neuron, beta=0.5)
+    elif kind == "dense":
+        spec = dict(kind="dense", n_in=20, n_out=37, neuron=neuron, beta=0.9, alpha=0.5)
+    else:
+        spec = dict(kind="none", n=37, neuron=neuron, beta=0.9, alpha=0.5)
+    d = snn.layer_desc(spec, T, B)
+    lay = snn.snn_layer_saved_layout(d)
+    el = T * B * d.n_out
+    assert lay.bytes == snn.snn_layer_saved_bytes(d)
+    assert lay.ckpt_interval == 16
+    assert lay.ckpt_count == (max(T, 1) - 1) // 16
+    assert lay.ckpt_planes == (2 if neuron == "synaptic" else 1)
+    assert lay.cur_bytes == (0 if kind == "none" else _al(el * 4))
+    assert lay.ckpt_bytes == _al(lay.ckpt_planes * lay.ckpt_count * B * d.n_out * 4)
+    assert lay.pool_bytes == (_al(el) if kind == "conv" else 0)
+    parts = sorted([(lay.cur_offset, lay.cur_bytes), (lay.ckpt_offset, lay.ckpt_bytes),
+                    (lay.pool_offset, lay.pool_bytes)])
+    end = 0
+    for off, nb in parts:
+        assert off % 256 == 0 and off >= end
+        end = off + nb
+    assert end <= lay.bytes
+    # errors: no output struct, a bad descriptor
+    assert snn.lib().snn_layer_saved_layout(ctypes.byref(d), None) == 1
+    bad = d.copy(); bad.T = -1
+    out = snn.SavedLayout()
+    assert snn.lib().snn_layer_saved_layout(ctypes.byref(bad), ctypes.byref(out)) == 2
 
 
 def test_workspace_too_small_is_rejected():

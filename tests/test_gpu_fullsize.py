@@ -26,11 +26,6 @@ def _np(t):
     return t.detach().cpu().numpy()
 
 
-def _u(net, li):
-    d = net.descs[li]
-    return net.saved[li][: d.T * d.B * d.n_out * 4].view(torch.float32).view(d.T, d.B, d.n_out)
-
-
 def _gen(seed):
     g = torch.Generator(device=DEV)
     g.manual_seed(seed)
@@ -57,7 +52,8 @@ def test_scan_wide_full_size_sampled():
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
     u = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     counts = torch.empty((B, N), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_fwd(d, x, None, spk, u, counts)
+    ck = snn.ckpt_buffer(d)
+    snn.snn_neuron_fwd(d, x, None, spk, ck, counts, u_out=u)
     rng = np.random.default_rng(0)
     cols = [(0, 0), (B - 1, N - 1), (B - 1, 0), (0, N - 1)] + \
         [(int(b), int(n)) for b, n in zip(rng.integers(0, B, 252), rng.integers(0, N, 252))]
@@ -79,18 +75,19 @@ def test_scan_wide_full_size_sampled():
     L, gc_o = oracle.loss_mse(c_s, tgt_h)
     assert abs(_np(loss)[0] - L) <= 1e-6 * abs(L)
     assert_close(_np(gc), gc_o, 1e-5, what="dL/dcounts")
-    # reverse scan with a seeded gradient broadcast over t, on the GPU's own
-    # membrane (bit-identical to the oracle's on the sampled columns above)
+    # reverse scan with a seeded gradient broadcast over t, recomputing the
+    # membrane from the currents and the forward's checkpoints
     g = _seeded_normal((B, N), 0.0, 1e-6, seed=5)
     dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, g, None, u, dI, None, None, None)
+    del u
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, g, None, x, ck, dI, None, None, None)
     dI_o = oracle.scan_bwd(u_o, _np(g)[bh, nh], spec["neuron"], spec["beta"], spec["thr"],
                            wl.slope)
     assert_close(_np(dI[:, bi, ni]), dI_o, 1e-3, what="dL/dI")
     del dI
-    # the whole step is the same calls: same spikes, counts and membrane
+    # the whole step is the same calls: same spikes, counts and checkpoints
     net.step(x, targets=torch.as_tensor(tgt_h).to(DEV))
-    assert torch.equal(net.spk[0], spk) and torch.equal(_u(net, 0), u)
+    assert torch.equal(net.spk[0], spk) and torch.equal(net.parts[0][1][: ck.numel()], ck)
     assert torch.equal(net.counts, counts)
 
 
@@ -123,7 +120,8 @@ def test_half_net_full_size_sampled():
         spk = torch.empty((T, B, d.n_out), device=DEV,
                           dtype=torch.float16 if d.out_dtype == snn.F16 else torch.uint8)
         u = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
-        snn.snn_neuron_fwd(d, Is, None, spk, u, None)
+        ck = snn.ckpt_buffer(d)
+        snn.snn_neuron_fwd(d, Is, None, spk, ck, None, u_out=u)
         bs = torch.as_tensor(rng.integers(0, B, 2), device=DEV)
         ns = torch.as_tensor(rng.integers(0, d.n_out, 128) if d.n_out > 128
                              else np.arange(d.n_out), device=DEV)
@@ -139,13 +137,13 @@ def test_half_net_full_size_sampled():
         gdt = torch.float16 if scaled else torch.bfloat16
         sc = torch.empty(4, dtype=torch.float32, device=DEV) if scaled else None
         dcur = torch.empty((T, B, d.n_out), dtype=gdt, device=DEV)
-        snn.snn_neuron_bwd(d, snn.GRAD_BCAST if last else snn.GRAD_FULL, g, None, u, dcur, None,
-                           None, net.ws, dcur_scale=sc)
+        snn.snn_neuron_bwd(d, snn.GRAD_BCAST if last else snn.GRAD_FULL, g, None, Is, ck, dcur,
+                           None, None, net.ws, dcur_scale=sc)
         S = float(_np(sc)[0]) if scaled else 1.0
         g_c = _np(g[bs][:, ns]) if last else _np(g[:, bs][:, :, ns])
         dI_o = oracle.scan_bwd(u_o, g_c, spec["neuron"], spec["beta"], spec["thr"], wl.slope)
         assert_close(_np(dcur[:, bs][:, :, ns].float()) / S, dI_o, tol, what=f"L{li} dL/dI")
-        del Is, spk, u, dcur
+        del Is, spk, u, dcur, ck
         # ---- synapse backward on seeded 16-bit dL/dI: sampled dW rows, dx rows
         S = 2.0 ** 20 if scaled else 1.0
         dI = _seeded_normal((T * B, d.n_out), 0.0, 1e-4 * S, seed=400 + li, dtype=gdt)

@@ -65,20 +65,23 @@ def _fwd(d, I, v=None):
     u = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     cnt = torch.empty((B, N), dtype=torch.float32, device=DEV)
     vt = None if v is None else torch.as_tensor(np.asarray(v, np.float32)).to(DEV)
-    snn.snn_neuron_fwd(d, x, vt, spk, u, cnt)
+    ck = snn.ckpt_buffer(d)
+    snn.snn_neuron_fwd(d, x, vt, spk, ck, cnt, u_out=u)
     torch.cuda.synchronize()
     return (spk.cpu().numpy().reshape(T, -1), u.cpu().numpy().reshape(T, -1),
-            cnt.cpu().numpy().reshape(-1), x, u, vt)
+            cnt.cpu().numpy().reshape(-1), x, ck, vt)
 
 
-def _bwd(d, x, u, g, full, vt=None):
-    """GPU reverse scan: dL/dI [T, B*N] (and dL/dv [N] for the recurrent neuron)."""
+def _bwd(d, x, ck, g, full, vt=None):
+    """GPU reverse scan from the currents and checkpoints of _fwd: dL/dI
+    [T, B*N] (and dL/dv [N] for the recurrent neuron)."""
     T, B, N = d.T, d.B, d.n_out
     gt = torch.as_tensor(np.ascontiguousarray(g, np.float32)).to(DEV)
     dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     gv = torch.empty(N, dtype=torch.float32, device=DEV) if vt is not None else None
     ws = torch.empty(max(256, 2 * B * N * 4 + 512), dtype=torch.uint8, device=DEV)
-    snn.snn_neuron_bwd(d, snn.GRAD_FULL if full else snn.GRAD_BCAST, gt, vt, u, dI, None, gv, ws)
+    snn.snn_neuron_bwd(d, snn.GRAD_FULL if full else snn.GRAD_BCAST, gt, vt, x, ck, dI, None, gv,
+                       ws)
     torch.cuda.synchronize()
     return dI.cpu().numpy().reshape(T, -1), (None if gv is None else gv.cpu().numpy())
 
@@ -121,17 +124,17 @@ def test_hand_gradients_on_gpu(lanes, case):
     reset = snn.RESET_SURROGATE if case["reset_surrogate"] else snn.RESET_DETACHED
     d = _desc(4, B, N, tr["neuron"], tr["beta"], tr["alpha"], slope=case["slope"], reset=reset)
     I, _ = _columns([tr["I"]], B, N)
-    z, u, _, x, ut, _ = _fwd(d, I)
+    z, u, _, x, ck, _ = _fwd(d, I)
     np.testing.assert_array_equal(u[:, 0], np.array(tr["u"], np.float32))
-    dI, _ = _bwd(d, x, ut, np.ones((B, N), np.float32), full=False)
+    dI, _ = _bwd(d, x, ck, np.ones((B, N), np.float32), full=False)
     want = np.array(case["dI"], np.float64)[:, None]
     assert np.abs(dI - want).max() <= 1e-6, (case["name"], dI[:, 0], want[:, 0])
     # the surrogate at the tie is exactly 1: with T = 1 the current is the
     # membrane u_t of the trace and the gradient is s_t itself
     d1 = _desc(1, B, N, "leaky", tr["beta"], slope=case["slope"], reset=reset)
     for t, s in enumerate(case["s"]):
-        _, _, _, x1, u1, _ = _fwd(d1, np.full((1, B * N), tr["u"][t], np.float32))
-        g1, _ = _bwd(d1, x1, u1, np.ones((B, N), np.float32), full=False)
+        _, _, _, x1, ck1, _ = _fwd(d1, np.full((1, B * N), tr["u"][t], np.float32))
+        g1, _ = _bwd(d1, x1, ck1, np.ones((B, N), np.float32), full=False)
         assert np.abs(g1 - float(Fraction(s))).max() <= 1e-6 * float(Fraction(s)), (t, s)
         if s == "1":
             assert (g1 == 1.0).all()
@@ -169,10 +172,10 @@ def test_rleaky_hand_gradients_on_gpu(lanes, case):
     reset = snn.RESET_SURROGATE if case["reset_surrogate"] else snn.RESET_DETACHED
     d = _desc(4, B, N, "rleaky", tr["beta"], thr=tr["thr"], slope=case["slope"], reset=reset)
     I, _ = _columns([tr["I"]], B, N)
-    _, u, _, x, ut, vt = _fwd(d, I, np.full(N, tr["v"], np.float32))
+    _, u, _, x, ck, vt = _fwd(d, I, np.full(N, tr["v"], np.float32))
     np.testing.assert_array_equal(u[:, 0], np.array(tr["u"], np.float32))
     g = np.broadcast_to(np.array(case["g"], np.float32)[:, None, None], (4, B, N))
-    dI, dv = _bwd(d, x, ut, g, full=True, vt=vt)
+    dI, dv = _bwd(d, x, ck, g, full=True, vt=vt)
     want = np.array([float(Fraction(q)) for q in case["dI"]])[:, None]
     assert np.abs(dI - want).max() <= 1e-6, (case["name"], dI[:, 0], want[:, 0])
     # every sample has the same trace: dL/dv is B times the one-sample value
@@ -230,7 +233,7 @@ def test_silent_boundary_on_gpu(lanes):
     B, N = LANES[lanes]
     T = 64
     d = _desc(T, B, N, "leaky", case["beta"], thr=case["thr"])
-    z, u, cnt, x, ut, _ = _fwd(d, np.full((T, B * N), case["I"], np.float32))
+    z, u, cnt, x, ck, _ = _fwd(d, np.full((T, B * N), case["I"], np.float32))
     assert z.sum() == 0 and (cnt == 0).all()
     for t in range(1, 25):
         assert (u[t - 1] == np.float32(1.0 - 2.0 ** -t)).all(), t
@@ -238,7 +241,7 @@ def test_silent_boundary_on_gpu(lanes):
     # g = 1 at the last step only: lam_t = beta^(T-t) s_T ... with s = 1 at u = thr
     g = np.zeros((T, B, N), np.float32)
     g[T - 1] = 1.0
-    dI, _ = _bwd(d, x, ut, g, full=True)
+    dI, _ = _bwd(d, x, ck, g, full=True)
     assert (dI[T - 1] == 1.0).all()
     want = np.array([case["beta"] ** (T - 1 - t) for t in range(T)])[:, None]
     np.testing.assert_allclose(dI, np.broadcast_to(want, dI.shape), rtol=1e-6, atol=0)

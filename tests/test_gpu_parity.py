@@ -45,6 +45,19 @@ def _assert_fp32_sum(a, terms_abs, K, what):
     assert (err <= bound).all(), f"{what}: error above the fp32 summation bound"
 
 
+def _assert_checkpoints(d, ck, u):
+    """The forward's checkpoints are the oracle's membrane after every
+    ckpt_interval-th step (the current-based neuron's second plane, i, is
+    checked through the recomputed backward)."""
+    lay = snn.snn_layer_saved_layout(d)
+    C = d.B * d.n_out
+    got = _np(ck)[: lay.ckpt_count * C].reshape(lay.ckpt_count, C)
+    for c in range(lay.ckpt_count):
+        t = (c + 1) * lay.ckpt_interval - 1
+        np.testing.assert_array_equal(got[c], np.asarray(u).reshape(d.T, C)[t],
+                                      err_msg=f"checkpoint {c}")
+
+
 def _ws(nbytes):
     return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=DEV)
 
@@ -63,11 +76,21 @@ def test_scan_fwd_bit_exact(neuron, alpha, beta, T, B, N):
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
     saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     counts = torch.empty((B, N), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_fwd(d, x, None, spk, saved, counts)
+    ck = snn.ckpt_buffer(d)
+    snn.snn_neuron_fwd(d, x, None, spk, ck, counts, u_out=saved)
     z, u, c = oracle.scan_fwd(I, neuron, beta, 1.0, alpha)
     np.testing.assert_array_equal(_np(spk), z)
     np.testing.assert_array_equal(_np(saved), u)
     np.testing.assert_array_equal(_np(counts), c)
+    _assert_checkpoints(d, ck, u)
+    # without the membrane output: the same spikes, counts and checkpoints
+    spk2, ck2 = torch.empty_like(spk), snn.ckpt_buffer(d)
+    snn.snn_neuron_fwd(d, x, None, spk2, ck2, counts)
+    np.testing.assert_array_equal(_np(spk2), z)
+    np.testing.assert_array_equal(_np(counts), c)
+    lay = snn.snn_layer_saved_layout(d)
+    used = lay.ckpt_planes * lay.ckpt_count * B * N
+    np.testing.assert_array_equal(_np(ck2)[:used], _np(ck)[:used])
 
 
 def test_scan_fwd_in_place_and_f16_spikes():
@@ -78,7 +101,8 @@ def test_scan_fwd_in_place_and_f16_spikes():
     d.out_dtype = snn.F16
     buf = _t(I)
     spk = torch.empty((T, B, N), dtype=torch.float16, device=DEV)
-    snn.snn_neuron_fwd(d, buf, None, spk, buf, None)       # currents overwritten by u
+    snn.snn_neuron_fwd(d, buf, None, spk, snn.ckpt_buffer(d), None,
+                       u_out=buf)                           # currents overwritten by u
     z, u, _ = oracle.scan_fwd(I, "synaptic", 0.8, 1.0, 0.6)
     np.testing.assert_array_equal(_np(buf), u)
     np.testing.assert_array_equal(_np(spk).astype(np.uint8), z)
@@ -95,12 +119,13 @@ def test_scan_bwd(neuron, alpha, beta, reset, bcast, T, B, N):
     x = _t(I)
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
     saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_fwd(d, x, None, spk, saved, None)
+    ck = snn.ckpt_buffer(d)
+    snn.snn_neuron_fwd(d, x, None, spk, ck, None, u_out=saved)
     _, u, _ = oracle.scan_fwd(I, neuron, beta, 1.0, alpha)
     np.testing.assert_array_equal(_np(saved), u)
     g = rng.normal(0, 1, (B, N) if bcast else (T, B, N)).astype(np.float32)
     dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_bwd(d, snn.GRAD_BCAST if bcast else snn.GRAD_FULL, _t(g), None, saved, dI,
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST if bcast else snn.GRAD_FULL, _t(g), None, x, ck, dI,
                        None, None, None)
     ref = oracle.scan_bwd(u, g, neuron, beta, 1.0, 25.0, alpha, reset == snn.RESET_SURROGATE)
     assert_close(_np(dI), ref, 1e-3, what="dL/dI")
@@ -116,13 +141,14 @@ def test_scan_bwd_half_gradient_operand(gdt, tdt):
     dn, _ = _none_desc(T, B, N, "leaky", 0.9)
     saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
-    snn.snn_neuron_fwd(dn, _t(I), None, spk, saved, None)
+    x, ck = _t(I), snn.ckpt_buffer(dn)
+    snn.snn_neuron_fwd(dn, x, None, spk, ck, None, u_out=saved)
     _, u, _ = oracle.scan_fwd(I, "leaky", 0.9, 1.0)
     np.testing.assert_array_equal(_np(saved), u)
     g = rng.normal(0, 0.01, (B, N)).astype(np.float32)
     dI = torch.empty((T, B, N), dtype=tdt, device=DEV)
     sc = torch.full((4,), float("nan"), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, _t(g), None, saved, dI, None, None,
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, _t(g), None, x, ck, dI, None, None,
                        _ws(snn.snn_layer_workspace_bytes(d)), dcur_scale=sc)
     ref = oracle.scan_bwd(u, g, "leaky", 0.9, 1.0, 25.0)
     S = 1.0
@@ -156,7 +182,8 @@ def test_scan_bwd_fold(neuron, alpha, beta, T, B, N, nup):
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
     saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     v_t = None if v is None else _t(v)
-    snn.snn_neuron_fwd(d, _t(I), v_t, spk, saved, None)
+    x, ck = _t(I), snn.ckpt_buffer(d)
+    snn.snn_neuron_fwd(d, x, v_t, spk, ck, None, u_out=saved)
     _, u, _ = oracle.scan_fwd(I, neuron, beta, 1.0, alpha, v=v)
     np.testing.assert_array_equal(_np(saved), u)
     dup = rng.normal(0, 0.1, (T, B, nup)).astype(np.float32)
@@ -165,7 +192,7 @@ def test_scan_bwd_fold(neuron, alpha, beta, T, B, N, nup):
     dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     gv = None if v is None else torch.empty(N, dtype=torch.float32, device=DEV)
     ws = _ws(snn.snn_layer_workspace_bytes(d))
-    snn.snn_neuron_bwd(d, snn.GRAD_FOLD, (_t(dup), _t(wup)), v_t, saved, dI, None, gv, ws)
+    snn.snn_neuron_bwd(d, snn.GRAD_FOLD, (_t(dup), _t(wup)), v_t, x, ck, dI, None, gv, ws)
     if neuron == "rleaky":
         ref, dv = oracle.scan_bwd_rleaky(u, g, beta, 1.0, 25.0, v)
         assert_close(_np(gv), dv, 1e-3, what="dL/dv")
@@ -183,16 +210,16 @@ def test_scan_bwd_fold_half_operands():
     spec = dict(kind="dense", n_in=8, n_out=N, neuron="leaky", beta=0.9)
     d = snn.layer_desc(spec, T, B, grad_dtype=snn.BF16)
     dn, _ = _none_desc(T, B, N, "leaky", 0.9)
-    saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
-    snn.snn_neuron_fwd(dn, _t(I), None, spk, saved, None)
+    x, ck = _t(I), snn.ckpt_buffer(dn)
+    snn.snn_neuron_fwd(dn, x, None, spk, ck, None)
     _, u, _ = oracle.scan_fwd(I, "leaky", 0.9, 1.0)
     dup = torch.as_tensor(rng.normal(0, 0.01, (T, B, nup)).astype(np.float32)).to(torch.bfloat16)
     wup = torch.as_tensor(rng.uniform(-1, 1, (nup, N)).astype(np.float32)).to(torch.float16)
     g = dup.float().numpy().astype(np.float64) @ wup.float().numpy().astype(np.float64)
     dI = torch.empty((T, B, N), dtype=torch.bfloat16, device=DEV)
     gb = torch.empty(N, dtype=torch.float32, device=DEV)
-    snn.snn_neuron_bwd(d, snn.GRAD_FOLD, (dup.to(DEV), wup.to(DEV)), None, saved, dI, gb, None,
+    snn.snn_neuron_bwd(d, snn.GRAD_FOLD, (dup.to(DEV), wup.to(DEV)), None, x, ck, dI, gb, None,
                        _ws(snn.snn_layer_workspace_bytes(d)))
     ref = oracle.scan_bwd(u, g, "leaky", 0.9, 1.0, 25.0)
     assert_close(_np(dI.float()), ref, 2e-2, what="half dL/dI (folded)")
@@ -220,8 +247,10 @@ def test_rleaky_scan_fwd_bit_exact(T, B, N):
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
     saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     counts = torch.empty((B, N), dtype=torch.float32, device=DEV)
-    snn.snn_neuron_fwd(d, _t(I), _t(v), spk, saved, counts)
+    ck = snn.ckpt_buffer(d)
+    snn.snn_neuron_fwd(d, _t(I), _t(v), spk, ck, counts, u_out=saved)
     z, u, c = oracle.scan_fwd(I, "rleaky", 0.9, 1.0, v=v)
+    _assert_checkpoints(d, ck, u)
     np.testing.assert_array_equal(_np(spk), z)
     np.testing.assert_array_equal(_np(saved), u)
     np.testing.assert_array_equal(_np(counts), c)
@@ -237,14 +266,15 @@ def test_rleaky_scan_bwd(reset, bcast, T, B, N):
     spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
     saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     v_t = _t(v)
-    snn.snn_neuron_fwd(d, _t(I), v_t, spk, saved, None)
+    x, ck = _t(I), snn.ckpt_buffer(d)
+    snn.snn_neuron_fwd(d, x, v_t, spk, ck, None, u_out=saved)
     _, u, _ = oracle.scan_fwd(I, "rleaky", 0.9, 1.0, v=v)
     np.testing.assert_array_equal(_np(saved), u)
     g = rng.normal(0, 1, (B, N) if bcast else (T, B, N)).astype(np.float32)
     dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
     gv = torch.empty(N, dtype=torch.float32, device=DEV)
     ws = _ws(snn.snn_layer_workspace_bytes(d))
-    snn.snn_neuron_bwd(d, snn.GRAD_BCAST if bcast else snn.GRAD_FULL, _t(g), v_t, saved, dI,
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST if bcast else snn.GRAD_FULL, _t(g), v_t, x, ck, dI,
                        None, gv, ws)
     ref, dv = oracle.scan_bwd_rleaky(u, g, 0.9, 1.0, 25.0, v, reset == snn.RESET_SURROGATE)
     assert_close(_np(dI), ref, 1e-3, what="dL/dI")
@@ -260,7 +290,7 @@ def test_rleaky_zero_weight_matches_leaky_kernel():
         d, _ = _none_desc(T, B, N, neuron, 0.9, reset=snn.RESET_SURROGATE)
         spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
         saved = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
-        snn.snn_neuron_fwd(d, _t(I), v, spk, saved, None)
+        snn.snn_neuron_fwd(d, _t(I), v, spk, snn.ckpt_buffer(d), None, u_out=saved)
         out += [_np(spk), _np(saved)]
     np.testing.assert_array_equal(out[0], out[2])
     np.testing.assert_array_equal(out[1], out[3])
@@ -272,7 +302,7 @@ def test_rleaky_empty_batch_zero_gradient():
     g = torch.zeros(256, dtype=torch.float32, device=DEV)
     buf = torch.empty(256, dtype=torch.float32, device=DEV)
     v = torch.ones(16, dtype=torch.float32, device=DEV)
-    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, g, v, buf, buf, None, gv, _ws(256))
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, g, v, buf, buf, buf, None, gv, _ws(256))
     assert (_np(gv) == 0).all()
 
 
@@ -588,19 +618,24 @@ def test_loss_population(kind, B, K, P):
 _TORCH_GRAD = {snn.F32: torch.float32, snn.BF16: torch.bfloat16, snn.F16: torch.float16}
 
 
-def _saved_from_oracle(d, f):
-    """The forward-to-backward state of snn_layer_bwd filled from the oracle's
-    forward: membrane u (fp32) and, for conv layers, the pool selection that
-    follows it on the next 256-byte boundary."""
-    buf = torch.zeros(snn.snn_layer_saved_bytes(d), dtype=torch.uint8)
-    n = d.T * d.B * d.n_out
-    u = torch.from_numpy(np.ascontiguousarray(f["u"], np.float32).reshape(-1))
-    buf[: n * 4] = u.view(torch.uint8)
-    if d.synapse == snn.SYN_CONV5_POOL2:
-        off = (n * 4 + 255) // 256 * 256
-        buf[off: off + n] = torch.from_numpy(np.ascontiguousarray(f["arg"]).astype(np.uint8)
-                                             .reshape(-1))
-    return buf.to(DEV)
+def _saved_from_oracle(d, f, v, x_dev):
+    """The forward-to-backward state of snn_layer_bwd built from the oracle's
+    forward, at the offsets the library reports: the oracle's currents, the
+    checkpoints of a forward scan of those currents (bit-identical to the
+    oracle's scan, as the neuron-stage checks show), and, for conv layers,
+    the oracle's pool selection.  Returns (saved, currents, checkpoints)."""
+    saved = torch.zeros(snn.snn_layer_saved_bytes(d), dtype=torch.uint8, device=DEV)
+    cur, ck, pool = snn.saved_parts(d, saved)
+    I = _t(np.ascontiguousarray(f["I"], np.float32).reshape(d.T, d.B, d.n_out))
+    if cur is not None:
+        cur.copy_(I)
+    else:
+        cur = x_dev  # the layer's input holds its currents
+    if pool is not None:
+        pool.copy_(_t(np.asarray(f["arg"]).astype(np.uint8).reshape(pool.shape)))
+    spk = _spk_buf(d)
+    snn.snn_neuron_fwd(d, cur, v, spk, ck, None)
+    return saved, cur, ck
 
 
 def _layer_input(spec, f, d):
@@ -651,7 +686,8 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
         spk = _spk_buf(d)
         u = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
         cnt = torch.empty((B, d.n_out), dtype=torch.float32, device=DEV)
-        snn.snn_neuron_fwd(d, _t(f["I"].reshape(T, B, -1)), net.v[li], spk, u, cnt)
+        snn.snn_neuron_fwd(d, _t(f["I"].reshape(T, B, -1)), net.v[li], spk, snn.ckpt_buffer(d),
+                           cnt, u_out=u)
         np.testing.assert_array_equal(_np(spk), f["z"].reshape(T, B, -1), err_msg=f"L{li} spikes")
         np.testing.assert_array_equal(_np(u), f["u"].reshape(T, B, -1), err_msg=f"L{li} membrane")
         np.testing.assert_array_equal(_np(cnt), f["counts"].reshape(B, -1))
@@ -681,13 +717,13 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
         kind = snn.GRAD_BCAST if bcast else snn.GRAD_FULL
         g_dev = _t(np.asarray(g, np.float32).reshape((B, d.n_out) if bcast else (T, B, d.n_out)))
         dI_o = r["dI"].reshape(T, B, -1)
-        saved = _saved_from_oracle(d, f)
+        saved, cur_s, ck_s = _saved_from_oracle(d, f, net.v[li], xs[li])
         vv = net.v[li]
         gv = None if vv is None else torch.empty_like(vv)
         gv2 = None if vv is None else torch.empty_like(vv)
         if spec["kind"] == "none":
             dcur = torch.empty((T, B, d.n_out), dtype=torch.float32, device=DEV)
-            snn.snn_neuron_bwd(d, kind, g_dev, vv, saved, dcur, None, gv, net.ws)
+            snn.snn_neuron_bwd(d, kind, g_dev, vv, cur_s, ck_s, dcur, None, gv, net.ws)
             assert_close(_np(dcur), dI_o, tol, what="dL/dI")
             snn.snn_layer_bwd(d, kind, g_dev, xs[li], None, vv, saved, None, None, gv2, dcur,
                               net.ws)
@@ -703,7 +739,7 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
         sc = torch.empty(4, dtype=torch.float32, device=DEV) if scaled else None
         dcur = torch.empty((T, B, d.n_out), dtype=gdt, device=DEV)
         gb = torch.empty_like(net.gb[li])
-        snn.snn_neuron_bwd(d, kind, g_dev, vv, saved, dcur, gb, gv, net.ws, dcur_scale=sc)
+        snn.snn_neuron_bwd(d, kind, g_dev, vv, cur_s, ck_s, dcur, gb, gv, net.ws, dcur_scale=sc)
         S = float(_np(sc)[0]) if scaled else 1.0
         assert_close(_np(dcur.float()) / S, dI_o, 2e-2 if half else tol, what=f"L{li} dL/dI")
         assert_close(_np(gb), r["db"], tol, what=f"L{li} neuron-stage db")
@@ -733,7 +769,8 @@ def _check_step_stagewise(wl, inp, reset=snn.RESET_DETACHED, flags=0, tol=1e-3):
                 bW_f = 2.0 ** -8 * (np.abs(dI_r.reshape(T * B, -1)).T @ np.abs(xin_))
             dcur_f, gb_f = torch.empty_like(dcur), torch.empty_like(gb)
             gv_f = None if vv is None else torch.empty_like(vv)
-            snn.snn_neuron_bwd(d, snn.GRAD_FOLD, fold_g, vv, saved, dcur_f, gb_f, gv_f, net.ws,
+            snn.snn_neuron_bwd(d, snn.GRAD_FOLD, fold_g, vv, cur_s, ck_s, dcur_f, gb_f, gv_f,
+                               net.ws,
                                dcur_scale=sc)
             S = float(_np(sc)[0]) if scaled else 1.0
             assert_close(_np(dcur_f.float()) / S, dI_r, 2e-2 if half else tol,
