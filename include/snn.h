@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 6
+#define SNN_ABI_VERSION 7
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -338,20 +338,36 @@ snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float
  * (times sum_{k<T} |alpha|^k for SNN_SYNAPTIC); so no value overflows fp16
  * and the rounding of each value is relative 2^-11 above 2^-14 / S.
  * SNN_F16 is rejected for SNN_RLEAKY and where F exceeds 1e30
- * (SNN_ERR_UNSUPPORTED).  Ignored (may be NULL) for the other dtypes. */
+ * (SNN_ERR_UNSUPPORTED).  Ignored (may be NULL) for the other dtypes.
+ * dcur_t (nullable, dense layers only, snn_layer_dcur_t_bytes(d) bytes): the
+ * same dL/dI written as the weight gradient's operand, so that
+ * snn_synapse_bwd needs no transpose: 16-bit [P][n_out][B*T], row n holding
+ * neuron n of every sample, column b*T + t (sample-major), P = 3 exact bf16
+ * parts (hi, mid, lo: hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi -
+ * mid)) for SNN_F32, else 1 plane of d->grad_dtype (fp16 scaled as dcur).
+ * dcur may be NULL when dcur_t is given. */
 snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const float *v,
-                          const float *cur, const float *ckpt, void *dcur, float *dcur_scale,
-                          float *grad_b, float *grad_v, void *ws, size_t ws_bytes,
-                          hipStream_t stream);
+                          const float *cur, const float *ckpt, void *dcur, void *dcur_t,
+                          float *dcur_scale, float *grad_b, float *grad_v, void *ws,
+                          size_t ws_bytes, hipStream_t stream);
 
 /* Synapse backward from dcur (of d->grad_dtype): grad_w and/or grad_x
  * (dW = dI^T x and dx = dI W, BPTT through the w x_t term of eqs. (4)/(5)).
- * dcur_scale: for SNN_F16, the scale snn_neuron_bwd wrote (required); the
- * contractions divide it out.  Ignored for the other dtypes. */
-snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const float *dcur_scale,
-                           const uint8_t *pool_arg, const void *x, const void *w,
-                           float *grad_w, float *grad_x, void *ws, size_t ws_bytes,
-                           hipStream_t stream);
+ * dcur_t (nullable): the transposed operand snn_neuron_bwd wrote; the weight
+ * gradient contracts it instead of transposing dcur (used when
+ * snn_layer_dcur_t_bytes(d) > 0).  dcur may then be NULL unless grad_x is
+ * requested.  dcur_scale: for SNN_F16, the scale snn_neuron_bwd wrote
+ * (required); the contractions divide it out.  Ignored for the other
+ * dtypes. */
+snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const void *dcur_t,
+                           const float *dcur_scale, const uint8_t *pool_arg, const void *x,
+                           const void *w, float *grad_w, float *grad_x, void *ws,
+                           size_t ws_bytes, hipStream_t stream);
+
+/* Bytes of the transposed dL/dI operand (dcur_t of snn_neuron_bwd /
+ * snn_synapse_bwd), or 0 when the layer's weight gradient does not take it
+ * (conv layers, layers with at most 16 outputs, small products). */
+size_t snn_layer_dcur_t_bytes(const snn_layer_desc *d);
 
 #ifdef __cplusplus
 }

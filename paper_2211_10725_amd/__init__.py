@@ -31,7 +31,7 @@ RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST, GRAD_FOLD = 0, 1, 2
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 6
+ABI_VERSION = 7
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
           4: "SNN_ERR_ALIGN", 5: "SNN_ERR_UNSUPPORTED", 6: "SNN_ERR_WORKSPACE",
@@ -41,7 +41,7 @@ EXPORTS = ["snn_abi_version", "snn_status_str", "snn_layer_saved_bytes",
            "snn_layer_workspace_bytes", "snn_layer_fwd", "snn_layer_bwd",
            "snn_loss_workspace_bytes", "snn_loss", "snn_synapse_fwd", "snn_neuron_fwd",
            "snn_neuron_bwd", "snn_synapse_bwd", "snn_adamw", "snn_loss_noalloc",
-           "snn_layer_saved_layout"]
+           "snn_layer_saved_layout", "snn_layer_dcur_t_bytes"]
 
 
 class LayerDesc(ctypes.Structure):
@@ -123,8 +123,9 @@ def lib():
         "snn_loss_noalloc": ([i32, i32, i32, i32, P, P, P, P, P, P], ctypes.c_int),
         "snn_synapse_fwd": ([D, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_neuron_fwd": ([D, P, P, P, P, P, P, P], ctypes.c_int),
-        "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
-        "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
+        "snn_layer_dcur_t_bytes": ([D], S),
         "snn_adamw": ([ctypes.POINTER(AdamwTensor), i32, ctypes.POINTER(AdamwHparams), P],
                       ctypes.c_int),
     }
@@ -240,6 +241,10 @@ def ckpt_buffer(desc: LayerDesc, device="cuda"):
     return torch.empty(max(64, lay.ckpt_bytes // 4), dtype=torch.float32, device=device)
 
 
+def snn_layer_dcur_t_bytes(desc: LayerDesc) -> int:
+    return int(lib().snn_layer_dcur_t_bytes(ctypes.byref(desc)))
+
+
 def snn_layer_workspace_bytes(desc: LayerDesc) -> int:
     return int(lib().snn_layer_workspace_bytes(ctypes.byref(desc)))
 
@@ -294,27 +299,34 @@ def snn_neuron_fwd(desc, cur, v, spk_out, ckpt, counts, stream=None, u_out=None)
 
 
 def snn_neuron_bwd(desc, grad_kind, g, v, cur, ckpt, dcur, grad_b, grad_v, ws, stream=None,
-                   dcur_scale=None):
+                   dcur_scale=None, dcur_t=None):
     """cur, ckpt: the forward's currents and checkpoints.  dcur_scale: device
     fp32 scalar receiving the power of two an fp16 dcur is scaled by
-    (required for grad_dtype F16)."""
+    (required for grad_dtype F16).  dcur_t: the transposed weight-gradient
+    operand (snn_layer_dcur_t_bytes), or None; dcur may then be None."""
+    if dcur_t is not None and dcur_t.numel() * dcur_t.element_size() < \
+            snn_layer_dcur_t_bytes(desc):
+        raise ValueError("snn_neuron_bwd: dcur_t smaller than snn_layer_dcur_t_bytes")
     _need("snn_neuron_bwd", cur, F32, desc.T * desc.B * desc.n_out, "cur")
     _need("snn_neuron_bwd", ckpt, F32, snn_layer_saved_layout(desc).ckpt_bytes // 4, "ckpt")
     _need("snn_neuron_bwd", dcur, desc.grad_dtype if desc.synapse != SYN_NONE else F32,
           desc.T * desc.B * desc.n_out, "dcur")
     gi = _grad_in(grad_kind, g)
     _check("snn_neuron_bwd", lib().snn_neuron_bwd(
-        ctypes.byref(desc), ctypes.byref(gi), _p(v), _p(cur), _p(ckpt), _p(dcur),
+        ctypes.byref(desc), ctypes.byref(gi), _p(v), _p(cur), _p(ckpt), _p(dcur), _p(dcur_t),
         _p(dcur_scale), _p(grad_b), _p(grad_v), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def snn_synapse_bwd(desc, dcur, pool_arg, x, w, grad_w, grad_x, ws, stream=None,
-                    dcur_scale=None):
+                    dcur_scale=None, dcur_t=None):
     _check_fwd_io("snn_synapse_bwd", desc, x)
     _need("snn_synapse_bwd", dcur, desc.grad_dtype, desc.T * desc.B * desc.n_out, "dcur")
+    if dcur_t is not None and dcur_t.numel() * dcur_t.element_size() < \
+            snn_layer_dcur_t_bytes(desc):
+        raise ValueError("snn_synapse_bwd: dcur_t smaller than snn_layer_dcur_t_bytes")
     _check("snn_synapse_bwd", lib().snn_synapse_bwd(
-        ctypes.byref(desc), _p(dcur), _p(dcur_scale), _p(pool_arg), _p(x), _p(w), _p(grad_w),
-        _p(grad_x), _p(ws), _nbytes(ws), _stream(stream)))
+        ctypes.byref(desc), _p(dcur), _p(dcur_t), _p(dcur_scale), _p(pool_arg), _p(x), _p(w),
+        _p(grad_w), _p(grad_x), _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def snn_adamw(tensors, step, lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2,
@@ -469,6 +481,11 @@ class Network:
         ws = max([snn_layer_workspace_bytes(d) for d in self.descs] +
                  [snn_loss_workspace_bytes(self.loss_kind, B, K), 256])
         self.ws = torch.empty(ws, dtype=u8, device=device)
+        # the reverse scan's transposed dL/dI for the weight gradient (stage
+        # calls; the layer calls keep it in the workspace)
+        self.dcur_t_bytes = [snn_layer_dcur_t_bytes(d) for d in self.descs]
+        self.transposed_operand = False
+        self.dcur_t = torch.empty(max(self.dcur_t_bytes + [256]), dtype=u8, device=device)
 
     def forward(self, x, stream=None):
         h = x
@@ -621,15 +638,23 @@ class Network:
                     dcur = dcur.view(torch.float32)
                 rest = self.ws[(dcur_bytes + 255) // 256 * 256:]
             sc = self.scale[li]
+            # the weight gradient's operand written transposed by the scan
+            # (transposed_operand=True); the row-major dL/dI only where the
+            # input gradient needs it.  Off by default: it measured slower
+            # than one transpose (as in the layer call).
+            dt = self.dcur_t if self.transposed_operand and self.dcur_t_bytes[li] > 0 and \
+                self.dup[li] is None else None
+            rm = dcur if dt is None or self.gx[li] is not None or self.dup[li] is not None \
+                else None
             hook("neuron_bwd", li)
             cur, ck, _ = self.parts[li]
-            snn_neuron_bwd(d, kind, g, self.v[li], cur, ck, dcur, self.gb[li],
-                           self.gv[li], rest, stream, dcur_scale=sc)
+            snn_neuron_bwd(d, kind, g, self.v[li], cur, ck, rm, self.gb[li],
+                           self.gv[li], rest, stream, dcur_scale=sc, dcur_t=dt)
             hook("neuron_bwd_end", li)
             if d.synapse == SYN_DENSE:
                 hook("synapse_bwd_dw", li)
-                snn_synapse_bwd(d, dcur, None, xin, self.W[li], self.gW[li], None, rest, stream,
-                                dcur_scale=sc)
+                snn_synapse_bwd(d, rm, None, xin, self.W[li], self.gW[li], None, rest, stream,
+                                dcur_scale=sc, dcur_t=dt)
                 hook("synapse_bwd_dw_end", li)
                 if self.gx[li] is not None:
                     hook("synapse_bwd_dx", li)

@@ -205,6 +205,14 @@ DwPlan dw_plan(const snn_layer_desc *d) {
     return p;
 }
 
+// bytes of the transposed dL/dI operand of the weight gradient ([planes][n_out]
+// [T*B] 16-bit), 0 when the layer's weight gradient does not contract it
+size_t dcur_t_bytes(const snn_layer_desc *d) {
+    if (d->synapse != SNN_SYN_DENSE || rows(d) == 0) return 0;
+    const DwPlan p = dw_plan(d);
+    return p.transposed ? p.dit_bytes : 0;
+}
+
 struct DxPlan {
     bool transposed;
     size_t wt_bytes;  // W^T
@@ -320,6 +328,11 @@ size_t snn_layer_saved_bytes(const snn_layer_desc *d) {
     return saved_layout(d).bytes;
 }
 
+size_t snn_layer_dcur_t_bytes(const snn_layer_desc *d) {
+    if (check_desc(d) != SNN_OK) return 0;
+    return dcur_t_bytes(d);
+}
+
 snn_status snn_layer_saved_layout(const snn_layer_desc *d, snn_saved_layout *out) {
     if (!out) return SNN_ERR_NULL;
     snn_status st = check_desc(d);
@@ -385,13 +398,15 @@ snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float
 }
 
 snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const float *v,
-                          const float *cur, const float *ckpt, void *dcur, float *dcur_scale,
-                          float *grad_b, float *grad_v, void *ws, size_t ws_bytes,
-                          hipStream_t stream) {
+                          const float *cur, const float *ckpt, void *dcur, void *dcur_t,
+                          float *dcur_scale, float *grad_b, float *grad_v, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
     snn_status st = check_desc(d);
     if (st != SNN_OK) return st;
     if ((st = check_grad(d, grad)) != SNN_OK) return st;
-    if (!cur || !dcur) return SNN_ERR_NULL;
+    if (!cur || (!dcur && !dcur_t)) return SNN_ERR_NULL;
+    if (dcur_t && (d->synapse != SNN_SYN_DENSE || !aligned16(dcur_t)))
+        return d->synapse != SNN_SYN_DENSE ? SNN_ERR_UNSUPPORTED : SNN_ERR_ALIGN;
     if (neuron_ckpt_count(d->T) > 0 && d->B > 0 && !ckpt) return SNN_ERR_NULL;
     if (ckpt && !aligned16(ckpt)) return SNN_ERR_ALIGN;
     if (scaled_grad(d)) {
@@ -406,7 +421,7 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
         if (grad_v) return SNN_ERR_SHAPE;  // no recurrent weight to differentiate
         v = nullptr;
     }
-    if (!aligned16(cur) || !aligned16(dcur) || (grad_b && !aligned16(grad_b)) ||
+    if (!aligned16(cur) || (dcur && !aligned16(dcur)) || (grad_b && !aligned16(grad_b)) ||
         (v && !aligned16(v)) || (grad_v && !aligned16(grad_v)))
         return SNN_ERR_ALIGN;
     if (grad_b && d->synapse == SNN_SYN_NONE) return SNN_ERR_SHAPE;  // no bias to differentiate
@@ -443,8 +458,8 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
         if (e != hipSuccess) return SNN_ERR_HIP;
     }
     e = launch_neuron_bwd(d->neuron, d->reset_grad, d->T, C, d->n_out, d->alpha, d->beta,
-                          d->threshold, d->slope, v, cur, ckpt, bg, d->B, dcur, d->grad_dtype,
-                          dcur_scale, colsum, dvcol, stream);
+                          d->threshold, d->slope, v, cur, ckpt, bg, d->B, dcur, dcur_t,
+                          d->grad_dtype, dcur_scale, colsum, dvcol, stream);
     if (e != hipSuccess) return SNN_ERR_HIP;
     if (grad_b) {
         int F = d->n_out, P = 1;
@@ -460,14 +475,19 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
     return hip_status(e);
 }
 
-snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const float *dcur_scale,
-                           const uint8_t *pool_arg, const void *x, const void *w,
-                           float *grad_w, float *grad_x, void *ws, size_t ws_bytes,
-                           hipStream_t stream) {
+snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const void *dcur_t,
+                           const float *dcur_scale, const uint8_t *pool_arg, const void *x,
+                           const void *w, float *grad_w, float *grad_x, void *ws,
+                           size_t ws_bytes, hipStream_t stream) {
     snn_status st = check_desc(d);
     if (st != SNN_OK) return st;
     if (d->synapse == SNN_SYN_NONE) return SNN_ERR_UNSUPPORTED;
-    if (!dcur) return SNN_ERR_NULL;
+    // dcur_t (the transposed weight-gradient operand) serves the weight
+    // gradient when the layer's plan contracts it; dcur everything else
+    const bool use_t = dcur_t && grad_w && dcur_t_bytes(d) > 0;
+    if (dcur_t && !aligned16(dcur_t)) return SNN_ERR_ALIGN;
+    if (!dcur && (grad_x || (grad_w && !use_t))) return SNN_ERR_NULL;
+    if (!dcur && !dcur_t) return SNN_ERR_NULL;
     if (scaled_grad(d)) {
         if (!dcur_scale) return SNN_ERR_NULL;
         if (!aligned16(dcur_scale)) return SNN_ERR_ALIGN;
@@ -475,7 +495,7 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const floa
         dcur_scale = nullptr;
     }
     if ((grad_w && !x) || (grad_x && !w)) return SNN_ERR_NULL;
-    if (!aligned16(dcur) || (x && !aligned16(x)) || (w && !aligned16(w)) ||
+    if ((dcur && !aligned16(dcur)) || (x && !aligned16(x)) || (w && !aligned16(w)) ||
         (grad_w && !aligned16(grad_w)) || (grad_x && !aligned16(grad_x)))
         return SNN_ERR_ALIGN;
     const size_t need = bwd_gemm_ws(d);
@@ -503,15 +523,22 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const floa
         g.c_div = dcur_scale;
         hipError_t e;
         if (pl.transposed) {
+            // K = T*B in the order k = b*T + t on both operands: the order in
+            // which the reverse scan writes dL/dI transposed (one lane's
+            // column is one row there)
             char *dit = wsb, *xt = wsb + pl.dit_bytes;
             const bool planes = pl.a_dtype == kPlanes3;
-            e = launch_transpose(M, d->n_out, dcur, d->n_out, (int)dtype_bytes(d->grad_dtype), dit, M,
-                                 planes, (int64_t)M * d->n_out, stream);
-            if (e != hipSuccess) return SNN_ERR_HIP;
+            const void *A = dcur_t;
+            if (!use_t) {
+                e = launch_transpose(M, d->n_out, dcur, d->n_out, (int)dtype_bytes(d->grad_dtype),
+                                     dit, M, planes, (int64_t)M * d->n_out, stream, d->T);
+                if (e != hipSuccess) return SNN_ERR_HIP;
+                A = dit;
+            }
             e = launch_transpose(M, d->n_in, x, d->n_in, (int)dtype_bytes(d->in_dtype), xt, M, false,
-                                 0, stream);
+                                 0, stream, d->T);
             if (e != hipSuccess) return SNN_ERR_HIP;
-            g.A = dit; g.lda = M; g.a_dtype = pl.a_dtype; g.a_kc = true;
+            g.A = A; g.lda = M; g.a_dtype = pl.a_dtype; g.a_kc = true;
             g.a_ps = (int64_t)M * d->n_out;
             g.B = xt; g.ldb = M; g.b_dtype = d->in_dtype; g.b_kc = true;
             e = launch_gemm(g, xt + pl.xt_bytes, ws_bytes - pl.dit_bytes - pl.xt_bytes, stream);
@@ -591,7 +618,7 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
         if (!grad_x || !x) return SNN_ERR_NULL;
         // the currents are the layer's input
         return snn_neuron_bwd(d, grad, v, reinterpret_cast<const float *>(x), ckpt, grad_x,
-                              nullptr, nullptr, grad_v, ws, ws_bytes, stream);
+                              nullptr, nullptr, nullptr, grad_v, ws, ws_bytes, stream);
     }
     const float *cur = reinterpret_cast<const float *>(sb + l.cur_offset);
     if (grad_w && !x) return SNN_ERR_NULL;
@@ -602,13 +629,22 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     char *colsum = base + dcur_bytes(d);
     float *scale = scaled_grad(d) ? reinterpret_cast<float *>(colsum + neuron_ws(d)) : nullptr;
     char *gws = colsum + neuron_ws(d) + scale_slot_bytes(d);
-    st = snn_neuron_bwd(d, grad, v, cur, ckpt, dcur, scale, grad_b, grad_v, colsum, neuron_ws(d),
-                        stream);
+    // The reverse scan could write the weight gradient's transposed operand
+    // itself (dcur_t), but its rows are written in runs of one chunk (16
+    // steps, 32 bytes) per lane, which measured slower than the row-major
+    // write plus one transpose (fp16 net: 0.72 + 0.78 ms of scans against
+    // 0.41 + 0.47 ms and 0.31 ms of transposes), so the layer call keeps the
+    // transpose.
+    void *dcur_t = nullptr;
+    void *dcur_rm = dcur;
+    st = snn_neuron_bwd(d, grad, v, cur, ckpt, dcur_rm, dcur_t, scale, grad_b, grad_v, colsum,
+                        neuron_ws(d), stream);
     if (st != SNN_OK) return st;
     if (!grad_w && !grad_x) return SNN_OK;
     const uint8_t *arg = nullptr;
     if (d->synapse == SNN_SYN_CONV5_POOL2) arg = reinterpret_cast<const uint8_t *>(sb + l.pool_offset);
-    return snn_synapse_bwd(d, dcur, scale, arg, x, w, grad_w, grad_x, gws, bwd_gemm_ws(d), stream);
+    return snn_synapse_bwd(d, dcur_rm, dcur_t, scale, arg, x, w, grad_w, grad_x, gws,
+                           bwd_gemm_ws(d), stream);
 }
 
 size_t snn_loss_workspace_bytes(int32_t kind, int32_t B, int32_t K) {

@@ -168,38 +168,67 @@ __device__ inline void multiply_stage(floatx16 (&acc)[4][2], int wm, int wn, int
     }
 }
 
+// Work item i of the launch (a tile and a K split) for persistent workgroup
+// w of G: the items are cut into kXcds contiguous ranges, one per XCD
+// (workgroup w runs on XCD w % kXcds), and the XCD's workgroups take the
+// items of its range in turn, so the tiles in flight on one XCD are
+// neighbours (they share operand panels in that XCD's L2).
+__device__ inline int persistent_item(int w, int G, int total, int j) {
+    const int xcd = w % kXcds, lw = w / kXcds;
+    const int gx = G / kXcds + (xcd < G % kXcds ? 1 : 0);  // workgroups on this XCD
+    const int per = total / kXcds, rem = total % kXcds;
+    const int beg = xcd < rem ? xcd * (per + 1) : rem * (per + 1) + (xcd - rem) * per;
+    const int cnt = per + (xcd < rem ? 1 : 0);
+    const int k = lw + j * gx;
+    return k < cnt ? beg + k : -1;
+}
+
+// Persistent: gridDim.x workgroups (one per CU) loop over the work items.
+// The first k-tile of a workgroup's next item is copied into stage 0 before
+// the current item's results are stored (stage 0 was last read before the
+// barrier of the current item's final k-tile), so that latency overlaps the
+// stores.
 template <int MT>
 __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
-    int M, int N, int K, int k_chunk, int tiles_n, const uint16_t *__restrict__ A, int64_t lda,
-    const uint16_t *__restrict__ B, int64_t ldb, float *__restrict__ C, int64_t ldc,
-    int64_t split_stride, const float *__restrict__ bias, const float *__restrict__ c_div) {
-    const int item = xcd_local_item();
-    const int tiles = gridDim.x;
-    const int zk = item / tiles, tile = item % tiles;
-    const int m0 = (tile / tiles_n) * kTile, n0 = (tile % tiles_n) * kTile;
-    const int kbeg = zk * k_chunk;
-    const int kend = min(K, kbeg + k_chunk);
-    const int nk = (kend - kbeg + kKT - 1) / kKT;  // >= 1
+    int M, int N, int K, int k_chunk, int tiles_n, int tiles, int total,
+    const uint16_t *__restrict__ A, int64_t lda, const uint16_t *__restrict__ B, int64_t ldb,
+    float *__restrict__ C, int64_t ldc, int64_t split_stride, const float *__restrict__ bias,
+    const float *__restrict__ c_div) {
     const int wave = threadIdx.x >> 6, wm = wave & 1, wn = wave >> 1;
-
-    floatx16 acc[4][2];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
+    const int lane = threadIdx.x & 63;
+    const float inv = c_div ? 1.f / c_div[0] : 1.f;
+    int item = persistent_item(blockIdx.x, gridDim.x, total, 0);
+    if (item < 0) return;
     TileCopy ca, cb;
-    ca.init(A, lda, M, m0);
-    cb.init(B, ldb, N, n0);
-    // k-tile t of this split.  The loop runs an even number of tiles; a tile
-    // past the end re-copies the last one and is multiplied fully masked.
-    const int nk2 = (nk + 1) & ~1;
+    auto setup = [&](int it, int &m0, int &n0, int &zk, int &kbeg, int &kend, int &nk) {
+        zk = it / tiles;
+        const int tile = it % tiles;
+        m0 = (tile / tiles_n) * kTile;
+        n0 = (tile % tiles_n) * kTile;
+        kbeg = zk * k_chunk;
+        kend = min(K, kbeg + k_chunk);
+        nk = (kend - kbeg + kKT - 1) / kKT;  // >= 1
+        ca.init(A, lda, M, m0);
+        cb.init(B, ldb, N, n0);
+    };
+    int m0, n0, zk, kbeg, kend, nk;
+    setup(item, m0, n0, zk, kbeg, kend, nk);
+    ca.copy(kbeg, kend, stage_a<0>());
+    cb.copy(kbeg, kend, stage_b<0>());
+    for (int j = 0; item >= 0; ++j) {
+        floatx16 acc[4][2];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) acc[i][q][r] = 0.f;
+        // k-tile t of this item.  The loop runs an even number of tiles; a
+        // tile past the end re-copies the last one and is multiplied fully
+        // masked.
+        const int nk2 = (nk + 1) & ~1;
 #define SNN_KTILE(t) (kbeg + kKT * min((t), nk - 1))
-    ca.copy(SNN_KTILE(0), kend, stage_a<0>());
-    cb.copy(SNN_KTILE(0), kend, stage_b<0>());
-    for (int t = 0; t < nk2; t += 2) {
+        for (int t = 0; t < nk2; t += 2) {
 #define SNN_ASYNC_STEP(S, NEXT)                                                             \
     {                                                                                       \
         const int tt = t + (S);                                                             \
@@ -210,39 +239,37 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
         }                                                                                   \
         multiply_stage<MT, S>(acc, wm, wn, kend - (kbeg + kKT * tt));                       \
     }
-        SNN_ASYNC_STEP(0, 1)
-        SNN_ASYNC_STEP(1, 0)
+            SNN_ASYNC_STEP(0, 1)
+            SNN_ASYNC_STEP(1, 0)
 #undef SNN_ASYNC_STEP
-    }
+        }
 #undef SNN_KTILE
-
-    // 32x32 block: lane holds column (lane & 31); register r holds row
-    // 8*(r/4) + 4*(lane/32) + r%4.  A scaled operand's power of two is
-    // divided out exactly (multiplication by its exact reciprocal).
-    const int lane = threadIdx.x & 63;
-    float *Cz = C + (int64_t)zk * split_stride;
-    if (c_div) {
-        const float inv = 1.f / c_div[0];
+        // the next item's first k-tile, in flight during the stores below
+        const int m0c = m0, n0c = n0, zkc = zk;
+        item = persistent_item(blockIdx.x, gridDim.x, total, j + 1);
+        if (item >= 0) {
+            setup(item, m0, n0, zk, kbeg, kend, nk);
+            ca.copy(kbeg, kend, stage_a<0>());
+            cb.copy(kbeg, kend, stage_b<0>());
+        }
+        // 32x32 block: lane holds column (lane & 31); register r holds row
+        // 8*(r/4) + 4*(lane/32) + r%4.  A scaled operand's power of two is
+        // divided out exactly (multiplication by its exact reciprocal).
+        float *Cz = C + (int64_t)zkc * split_stride;
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
+            for (int q = 0; q < 2; ++q) {
+                const int n = n0c + wn * 64 + q * 32 + (lane & 31);
+                if (n >= N) continue;
+                const float bn = bias ? bias[n] : 0.f;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) acc[i][j][r] *= inv;
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int n = n0 + wn * 64 + j * 32 + (lane & 31);
-            if (n >= N) continue;
-            const float bn = bias ? bias[n] : 0.f;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int m = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                if (m < M) Cz[(int64_t)m * ldc + n] = acc[i][j][r] + bn;
+                for (int r = 0; r < 16; ++r) {
+                    const int m = m0c + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                    if (m < M) Cz[(int64_t)m * ldc + n] = acc[i][q][r] * inv + bn;
+                }
             }
-        }
+    }
 }
 
 // Spike bytes widened to the 16-bit MFMA type: dst[r][k] (ld K) from
@@ -362,13 +389,17 @@ hipError_t launch_gemm_async(const GemmArgs &g, void *ws, size_t ws_bytes, hipSt
         bias = nullptr;
         c_div = nullptr;  // divided in the reduction
     }
-    dim3 grid((unsigned)(p.tiles_m * p.tiles_n), 1, (unsigned)p.splits);
+    const int tiles = p.tiles_m * p.tiles_n, total = tiles * p.splits;
+    // one persistent workgroup per compute unit (128 KiB of LDS each)
+    const unsigned grid = (unsigned)min(total, device_cus());
     if (mt == MT_F16)
-        gemm_async_kernel<MT_F16><<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n, A,
-                                                            lda, B, ldb, out, ldo, ss, bias, c_div);
+        gemm_async_kernel<MT_F16><<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n,
+                                                            tiles, total, A, lda, B, ldb, out, ldo,
+                                                            ss, bias, c_div);
     else
-        gemm_async_kernel<MT_BF16><<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n, A,
-                                                             lda, B, ldb, out, ldo, ss, bias, c_div);
+        gemm_async_kernel<MT_BF16><<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n,
+                                                             tiles, total, A, lda, B, ldb, out, ldo,
+                                                             ss, bias, c_div);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (p.splits > 1)

@@ -904,10 +904,16 @@ namespace {
 // the LDS accesses of a wave fall on 64 distinct banks either way.  With
 // PLANES, an fp32 source is written as three bf16 planes (dst + p*plane) of
 // its exact split.
+// perm_T > 0: destination index k takes source row (k % perm_T) *
+// (rows / perm_T) + k / perm_T (rows = T B ordered [T][B] read as k = b T + t).
+__device__ inline int src_row(int k, int rows, int perm_T) {
+    return perm_T > 0 ? (k % perm_T) * (rows / perm_T) + k / perm_T : k;
+}
+
 template <typename T, bool PLANES>
 __global__ __launch_bounds__(256) void transpose_kernel(int rows, int cols, const T *__restrict__ src,
                                                         int64_t lds_, void *__restrict__ dst,
-                                                        int64_t ldd, int64_t plane) {
+                                                        int64_t ldd, int64_t plane, int perm_T) {
     __shared__ T tile[64][65];
     typedef uint16_t O;  // element type of the destination when PLANES
     const int r0 = blockIdx.y * 64, c0 = blockIdx.x * 64;
@@ -921,7 +927,7 @@ __global__ __launch_bounds__(256) void transpose_kernel(int rows, int cols, cons
             const int rl = g + 16 * j, r = r0 + rl;
             T v[4] = {T(0), T(0), T(0), T(0)};
             if (r < rows) {
-                const T *p = src + (int64_t)r * lds_ + c;
+                const T *p = src + (int64_t)src_row(r, rows, perm_T) * lds_ + c;
                 if (vec) {
                     if constexpr (sizeof(T) == 4) {
                         const uint4 u = *reinterpret_cast<const uint4 *>(p);
@@ -1006,7 +1012,7 @@ constexpr int kT8Row = 132;    // LDS row stride (bytes)
 __global__ __launch_bounds__(256) void transpose_u8_kernel(int rows, int cols,
                                                            const uint8_t *__restrict__ src,
                                                            int64_t lds_, uint8_t *__restrict__ dst,
-                                                           int64_t ldd) {
+                                                           int64_t ldd, int perm_T) {
     __shared__ __attribute__((aligned(16))) uint32_t tile[kT8 * kT8Row / 4];
     const int r0 = blockIdx.y * kT8, c0 = blockIdx.x * kT8;
     const int t = threadIdx.x;
@@ -1018,7 +1024,7 @@ __global__ __launch_bounds__(256) void transpose_u8_kernel(int rows, int cols,
             const int r = (t >> 3) + 32 * i, gr = r0 + r;
             uint32_t w[4] = {0u, 0u, 0u, 0u};
             if (gr < rows) {
-                const uint8_t *p = src + (int64_t)gr * lds_ + gc;
+                const uint8_t *p = src + (int64_t)src_row(gr, rows, perm_T) * lds_ + gc;
                 if (gc + 16 <= cols && (((uintptr_t)p) & 15) == 0) {
                     const uint4 v = *reinterpret_cast<const uint4 *>(p);
                     w[0] = v.x; w[1] = v.y; w[2] = v.z; w[3] = v.w;
@@ -1062,23 +1068,25 @@ __global__ __launch_bounds__(256) void transpose_u8_kernel(int rows, int cols,
 
 hipError_t launch_transpose(int rows, int cols, const void *src, int64_t ld_src, int elem_bytes,
                             void *dst, int64_t ld_dst, bool to_planes, int64_t plane,
-                            hipStream_t s) {
+                            hipStream_t s, int perm_T) {
     if (rows <= 0 || cols <= 0) return hipSuccess;
+    if (perm_T < 0 || (perm_T > 0 && rows % perm_T != 0)) return hipErrorInvalidValue;
     dim3 grid((unsigned)((cols + 63) / 64), (unsigned)((rows + 63) / 64));
     if (to_planes) {
         if (elem_bytes != 4) return hipErrorInvalidValue;
         transpose_kernel<float, true><<<grid, 256, 0, s>>>(
-            rows, cols, reinterpret_cast<const float *>(src), ld_src, dst, ld_dst, plane);
+            rows, cols, reinterpret_cast<const float *>(src), ld_src, dst, ld_dst, plane, perm_T);
     } else if (elem_bytes == 4) {
         transpose_kernel<float, false><<<grid, 256, 0, s>>>(
-            rows, cols, reinterpret_cast<const float *>(src), ld_src, dst, ld_dst, 0);
+            rows, cols, reinterpret_cast<const float *>(src), ld_src, dst, ld_dst, 0, perm_T);
     } else if (elem_bytes == 2) {
         transpose_kernel<uint16_t, false><<<grid, 256, 0, s>>>(
-            rows, cols, reinterpret_cast<const uint16_t *>(src), ld_src, dst, ld_dst, 0);
+            rows, cols, reinterpret_cast<const uint16_t *>(src), ld_src, dst, ld_dst, 0, perm_T);
     } else {
         const dim3 g8((unsigned)((cols + kT8 - 1) / kT8), (unsigned)((rows + kT8 - 1) / kT8));
         transpose_u8_kernel<<<g8, 256, 0, s>>>(rows, cols, reinterpret_cast<const uint8_t *>(src),
-                                                 ld_src, reinterpret_cast<uint8_t *>(dst), ld_dst);
+                                                 ld_src, reinterpret_cast<uint8_t *>(dst), ld_dst,
+                                                 perm_T);
     }
     return hipGetLastError();
 }

@@ -216,6 +216,27 @@ __device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC]
     }
 }
 
+// The 16-bit parts of dL/dI for the weight-gradient contraction: fp32 as
+// three exact bf16 parts (hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi
+// - mid), each subtraction exact), bf16 or fp16 (scaled) as one.
+__device__ inline uint32_t bf16_rne_bits(float x) { return f32_to_bf16_rne(x); }
+template <int GT>
+__device__ inline uint32_t grad_part(float x, int p, float scale) {
+    if constexpr (GT == SNN_F16) {
+        const _Float16 f = (_Float16)(x * scale);
+        return __builtin_bit_cast(uint16_t, f);
+    } else if constexpr (GT == SNN_BF16) {
+        return bf16_rne_bits(x);
+    } else {
+        const uint32_t hi = bf16_rne_bits(x);
+        if (p == 0) return hi;
+        const float r = x - __uint_as_float(hi << 16);
+        const uint32_t mid = bf16_rne_bits(r);
+        if (p == 1) return mid;
+        return bf16_rne_bits(r - __uint_as_float(mid << 16));
+    }
+}
+
 // Sources of the upstream gradient g_t = dL/dz_t of the reverse scan.
 constexpr int GM_FULL = 0;   // g [T, C]
 constexpr int GM_BCAST = 1;  // g [C], the same for every t
@@ -278,15 +299,26 @@ struct FoldStage {
 // For the recurrent neuron the spike z_t reaches u_{t+1} through
 // (v - r thr), so the carry is beta + (v - r thr) s_t, and the recurrent
 // weight's gradient collects lam_{t+1} z_t per column (dvcol, fp32).
-template <int NEURON, int VEC, int GM, bool RESET_SURR, int GT>
+//
+// With TR, dL/dI is also written as the weight gradient's operand: dcur_t
+// [P][N][B*T] (P = 3 bf16 parts of fp32, else 1 plane of the 16-bit type,
+// planes t_plane elements apart), row n holding column n of every sample,
+// K index b*T + t.  A lane's column is one row there and a chunk's steps are
+// consecutive in it, so each chunk's values are packed in registers as the
+// reverse loop produces them and stored together (the row-major dcur may be
+// skipped: nullptr).
+template <int NEURON, int VEC, int GM, bool RESET_SURR, int GT, bool TR>
 __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
     int T, int64_t C, int64_t N, float alpha, float beta, float thr, float slope,
     const float *__restrict__ vrec, const float *__restrict__ cur, const float *__restrict__ ckpt,
     const float *__restrict__ g, FoldIn fold, void *__restrict__ dcur,
+    uint16_t *__restrict__ dcur_t, int64_t t_plane,
     const float *__restrict__ dscale, float *__restrict__ colsum, float *__restrict__ dvcol) {
     constexpr bool BCAST = GM == GM_BCAST, FOLD = GM == GM_FOLD || GM == GM_FOLD12;
     constexpr bool FULL = GM == GM_FULL;
     constexpr int K = kCkpt;
+    constexpr int P = GT == SNN_F32 ? 3 : 1;  // 16-bit parts per value in dcur_t
+    uint32_t pk[TR ? P : 1][TR ? VEC : 1][TR ? K / 2 : 1];  // packed parts of a chunk
     const float scale = GT == SNN_F16 ? *dscale : 1.f;
     constexpr int KF = GM == GM_FOLD12 ? 12 : kFoldMax;  // dI_up values per row (padded)
     const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
@@ -378,6 +410,14 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
             }
         }
         const float *fr = FOLD ? frows[c & 1] : nullptr;
+        if constexpr (TR) {
+#pragma unroll
+            for (int p = 0; p < P; ++p)
+#pragma unroll
+                for (int v = 0; v < VEC; ++v)
+#pragma unroll
+                    for (int q = 0; q < K / 2; ++q) pk[p][v][q] = 0u;
+        }
 #pragma unroll
         for (int j = K - 1; j >= 0; --j) {
             const int t = t_lo + j;
@@ -425,7 +465,43 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
                     }
                     acc[v] += d[v];
                 }
-                store_grad<GT, VEC>(dcur, (int64_t)t * C + col, d, scale);
+                if (dcur) store_grad<GT, VEC>(dcur, (int64_t)t * C + col, d, scale);
+                if constexpr (TR) {
+#pragma unroll
+                    for (int p = 0; p < P; ++p)
+#pragma unroll
+                        for (int v = 0; v < VEC; ++v) {
+                            const uint32_t h = grad_part<GT>(d[v], p, scale);
+                            pk[p][v][j / 2] |= (j & 1) ? h << 16 : h;
+                        }
+                }
+            }
+        }
+        if constexpr (TR) {
+            // the chunk's steps of this lane's columns, row (col + v) % N,
+            // K index b*T + t
+            if (active) {
+                const int len = min(K, T - t_lo);
+#pragma unroll
+                for (int v = 0; v < VEC; ++v) {
+                    const int64_t n = (col + v) % N, b = (col + v) / N;
+                    const int64_t base = n * ((int64_t)T * (C / N)) + b * T + t_lo;
+#pragma unroll
+                    for (int p = 0; p < P; ++p) {
+                        uint16_t *row = dcur_t + p * t_plane + base;
+                        if (len == K && (T & 3) == 0) {
+#pragma unroll
+                            for (int q = 0; q < K / 4; ++q)
+                                *reinterpret_cast<uint2 *>(row + 4 * q) =
+                                    make_uint2(pk[p][v][2 * q], pk[p][v][2 * q + 1]);
+                        } else {
+#pragma unroll
+                            for (int jj = 0; jj < K; ++jj)
+                                if (jj < len)
+                                    row[jj] = (uint16_t)(pk[p][v][jj / 2] >> (16 * (jj & 1)));
+                        }
+                    }
+                }
             }
         }
         if constexpr (FOLD) {
@@ -616,6 +692,7 @@ struct BwdBuffers {
     const float *cur, *ckpt, *g;
     FoldIn fold;
     void *dcur;
+    uint16_t *dcur_t;
     const float *dscale;
     float *colsum, *dvcol;
 };
@@ -624,9 +701,15 @@ template <int NEURON, int VEC, int GM, bool RS, int GT>
 void bwd_launch(const ScanArgs &a, const BwdBuffers &b, hipStream_t s) {
     const int64_t lanes = (a.C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_bwd_kernel<NEURON, VEC, GM, RS, GT><<<grid, kThreads, 0, s>>>(
-        a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.cur, b.ckpt, b.g, b.fold,
-        b.dcur, b.dscale, b.colsum, b.dvcol);
+    const int64_t t_plane = (int64_t)a.T * a.C;
+    if (b.dcur_t)
+        neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, true><<<grid, kThreads, 0, s>>>(
+            a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.cur, b.ckpt, b.g, b.fold,
+            b.dcur, b.dcur_t, t_plane, b.dscale, b.colsum, b.dvcol);
+    else
+        neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, false><<<grid, kThreads, 0, s>>>(
+            a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.cur, b.ckpt, b.g, b.fold,
+            b.dcur, nullptr, 0, b.dscale, b.colsum, b.dvcol);
 }
 
 template <int NEURON, int VEC, int GM, bool RS>
@@ -698,8 +781,9 @@ bool neuron_fold_supported(int64_t N) { return N >= 64; }
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
                              const float *cur, const float *ckpt, const BwdGrad &grad, int B,
-                             void *dcur, int grad_dtype, const float *dscale, float *colsum,
-                             float *dvcol, hipStream_t s) {
+                             void *dcur, void *dcur_t, int grad_dtype, const float *dscale,
+                             float *colsum, float *dvcol, hipStream_t s) {
+    if (dcur == nullptr && dcur_t == nullptr) return hipErrorInvalidValue;
     if (grad_dtype == SNN_F16 && dscale == nullptr) return hipErrorInvalidValue;
     if (T <= 0 || C <= 0) return hipSuccess;
     if (neuron_ckpt_count(T) > 0 && ckpt == nullptr) return hipErrorInvalidValue;
@@ -721,7 +805,8 @@ hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, 
     }
     const ScanArgs a{T, C, N, alpha, beta, thr, slope, vrec};
     const FoldIn fold{grad.dup, grad.wup, grad.nup, grad.dt_up, grad.dt_w, B};
-    const BwdBuffers b{cur, ckpt, grad.g, fold, dcur, dscale, colsum, dvcol};
+    const BwdBuffers b{cur, ckpt, grad.g, fold, dcur, reinterpret_cast<uint16_t *>(dcur_t),
+                       dscale, colsum, dvcol};
     const int rs = reset_surrogate, gt = grad_dtype;
     switch (neuron) {
         case SNN_SYNAPTIC: bwd_dispatch<SNN_SYNAPTIC>(vec, rs, gm, gt, a, b, s); break;

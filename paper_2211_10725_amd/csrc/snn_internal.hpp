@@ -75,11 +75,14 @@ bool neuron_fold_supported(int64_t N);
 // may be NULL) and, for SNN_RLEAKY, dvcol [C] = sum_t lam_{t+1} z_t (fp32,
 // may be NULL).  C = B * N.  An SNN_F16 dcur holds dL/dI * S with the power
 // of two S read from dscale[0] (launch_grad_scale writes it).
+// dcur_t (nullable): dL/dI also written as the weight gradient's operand,
+// [P][N][B*T] 16-bit (P = 3 exact bf16 parts of fp32, else 1), K index b*T + t;
+// dcur may be NULL when dcur_t is given.
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
                              const float *cur, const float *ckpt, const BwdGrad &grad, int B,
-                             void *dcur, int grad_dtype, const float *dscale, float *colsum,
-                             float *dvcol, hipStream_t s);
+                             void *dcur, void *dcur_t, int grad_dtype, const float *dscale,
+                             float *colsum, float *dvcol, hipStream_t s);
 // scale[0] = S = 2^e, the largest power of two with G * growth * S <= 2^15,
 // G a bound on |g| over the upstream gradient (device reduction into
 // `scratch`, grad_scale_workspace_bytes()); growth bounds |dL/dI| / G.
@@ -159,11 +162,13 @@ bool gemm_async_applies(const GemmArgs &g);
 size_t gemm_async_workspace_bytes(const GemmArgs &g);
 hipError_t launch_gemm_async(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
 
-// dst[c*ld_dst + r] = src[r*ld_src + c] for r < rows, c < cols; to_planes
+// dst[c*ld_dst + k] = src[row(k)*ld_src + c] for k < rows, c < cols, with
+// row(k) = k, or, when perm_T > 0, row(k) = (k % perm_T) * (rows / perm_T) +
+// k / perm_T (a [T][B] row index read in the order k = b*T + t); to_planes
 // writes an fp32 source as three bf16 planes `plane` elements apart.
 hipError_t launch_transpose(int rows, int cols, const void *src, int64_t ld_src, int elem_bytes,
                             void *dst, int64_t ld_dst, bool to_planes, int64_t plane,
-                            hipStream_t s);
+                            hipStream_t s, int perm_T = 0);
 
 // ---- losses (loss.hip) -----------------------------------------------------
 size_t loss_workspace_bytes(int kind, int B, int K);

@@ -88,7 +88,7 @@ def test_fold_validation():
 
     def bwd(gi, desc=d):
         return L.snn_neuron_bwd(ctypes.byref(desc), ctypes.byref(gi), None, 64, 128, 80 + 1,
-                                None, None, None, None, 0, None)
+                                None, None, None, None, None, 0, None)
 
     F = snn.GRAD_FOLD
     assert bwd(snn.GradIn(F, 10, None, 96, 112, snn.F32, snn.F32)) == 4     # valid up to dcur

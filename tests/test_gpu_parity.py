@@ -226,6 +226,115 @@ def test_scan_bwd_fold_half_operands():
     assert_close(_np(gb), ref.sum(axis=(0, 1)), 1e-3, what="db (folded)")
 
 
+def _bf16_parts(x):
+    """The three exact bf16 parts of fp32 values, hi = bf16(x), mid =
+    bf16(x - hi), lo = bf16(x - hi - mid) (round to nearest even; every
+    subtraction exact), as uint16 bit patterns."""
+    x = torch.as_tensor(np.ascontiguousarray(x, np.float32))
+    hi = x.to(torch.bfloat16)
+    r = x - hi.float()
+    mid = r.to(torch.bfloat16)
+    lo = (r - mid.float()).to(torch.bfloat16)
+    return [t.view(torch.int16).numpy().view(np.uint16) for t in (hi, mid, lo)]
+
+
+@pytest.mark.parametrize("gkind", ["fold", "full", "bcast"])
+@pytest.mark.parametrize("gdt", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("T,B,N", [(37, 5, 300), (20, 3, 64), (16, 1100, 512), (7, 130, 4096)])
+def test_scan_bwd_transposed_operand(gkind, gdt, T, B, N):
+    """The reverse scan's transposed dL/dI (the weight gradient's operand,
+    [P][N][B*T] with K index b*T + t) holds exactly the row-major dL/dI's
+    16-bit parts: bf16 parts of fp32, or the bf16 / scaled fp16 value; one
+    and four column lanes, ragged chunks (T not a multiple of 16 or 4)."""
+    rng = np.random.default_rng(T * 7 + N + B)
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    gcode, tdt = GRAD_TYPES[gdt]
+    spec = dict(kind="dense", n_in=8, n_out=N, neuron="synaptic" if N == 300 else "leaky",
+                beta=0.8, alpha=0.5)
+    d = snn.layer_desc(spec, T, B, grad_dtype=gcode)
+    dn, _ = _none_desc(T, B, N, spec["neuron"], 0.8, 0.5)
+    x, ck = _t(I), snn.ckpt_buffer(dn)
+    spk = torch.empty((T, B, N), dtype=torch.uint8, device=DEV)
+    snn.snn_neuron_fwd(dn, x, None, spk, ck, None)
+    if gkind == "fold":
+        nup = 10
+        g = (_t(rng.normal(0, 0.1, (T, B, nup)).astype(np.float32)),
+             _t(rng.uniform(-1, 1, (nup, N)).astype(np.float32)))
+        kind = snn.GRAD_FOLD
+    elif gkind == "full":
+        g, kind = _t(rng.normal(0, 0.1, (T, B, N)).astype(np.float32)), snn.GRAD_FULL
+    else:
+        g, kind = _t(rng.normal(0, 0.1, (B, N)).astype(np.float32)), snn.GRAD_BCAST
+    P = 3 if gcode == snn.F32 else 1
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    sc = torch.empty(4, dtype=torch.float32, device=DEV)
+    dI = torch.empty((T, B, N), dtype=tdt, device=DEV)
+    snn.snn_neuron_bwd(d, kind, g, None, x, ck, dI, None, None, ws, dcur_scale=sc)
+    dt = torch.full((P, N, B * T), 0x7fff, dtype=torch.int16, device=DEV)
+    snn.snn_neuron_bwd(d, kind, g, None, x, ck, None, None, None, ws, dcur_scale=sc, dcur_t=dt)
+    got = _np(dt).view(np.uint16)
+    if gcode == snn.F32:
+        parts = _bf16_parts(_np(dI))
+    else:
+        parts = [_np(dI.view(torch.int16)).view(np.uint16)]
+    for p in range(P):
+        want = parts[p].reshape(T, B, N).transpose(2, 1, 0).reshape(N, B * T)
+        np.testing.assert_array_equal(got[p], want, err_msg=f"plane {p}")
+
+
+def test_synapse_bwd_transposed_operand_same_bytes():
+    """The weight gradient from the scan's transposed operand equals the one
+    from the row-major dL/dI (transposed inside the call): the same operand
+    bytes in the same contraction."""
+    T, B, N, K = 40, 240, 600, 784  # 9600 rows: the transposed path
+    rng = np.random.default_rng(3)
+    spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
+    for gdt in ("f32", "bf16"):
+        gcode, tdt = GRAD_TYPES[gdt]
+        d = snn.layer_desc(spec, T, B, grad_dtype=gcode)
+        assert snn.snn_layer_dcur_t_bytes(d) > 0
+        I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+        dn, _ = _none_desc(T, B, N, "leaky", 0.9)
+        xc, ck = _t(I), snn.ckpt_buffer(dn)
+        snn.snn_neuron_fwd(dn, xc, None, torch.empty((T, B, N), dtype=torch.uint8, device=DEV),
+                           ck, None)
+        g = _t(rng.normal(0, 0.1, (B, N)).astype(np.float32))
+        ws = _ws(snn.snn_layer_workspace_bytes(d))
+        dI = torch.empty((T, B, N), dtype=tdt, device=DEV)
+        dt = torch.empty(snn.snn_layer_dcur_t_bytes(d), dtype=torch.uint8, device=DEV)
+        snn.snn_neuron_bwd(d, snn.GRAD_BCAST, g, None, xc, ck, dI, None, None, ws, dcur_t=dt)
+        x = _t((rng.random((T, B, K)) < 0.3).astype(np.uint8))
+        W = _t(rng.uniform(-0.05, 0.05, (N, K)).astype(np.float32))
+        gW1 = torch.empty((N, K), dtype=torch.float32, device=DEV)
+        gW2 = torch.empty_like(gW1)
+        snn.snn_synapse_bwd(d, dI, None, x, W, gW1, None, ws)
+        snn.snn_synapse_bwd(d, None, None, x, W, gW2, None, ws, dcur_t=dt)
+        np.testing.assert_array_equal(_np(gW1), _np(gW2))
+        rW, _, _ = oracle.dense_bwd(_np(dI.float()).astype(np.float64).reshape(T * B, N),
+                                    _np(x).reshape(T * B, K), _np(W), want_db=False,
+                                    want_dx=False)
+        assert_close(_np(gW2), rW, 1e-3, what=f"dW from the transposed {gdt} operand")
+
+
+@pytest.mark.parametrize("name,T,B,width", [("dsnn_half_t100_b512", 20, 64, 512),
+                                            ("dsnn_synaptic_t50_b256", 40, 240, 600)])
+def test_step_with_scan_transposed_operand(name, T, B, width):
+    """A whole step whose reverse scans write the weight gradients' operands
+    transposed gives the layer calls' gradients bit for bit (the same operand
+    bytes in the same contractions)."""
+    wl = wls.scaled(wls.get(name), T=T, B=B, width=width)
+    inp = wls.make_inputs(wl, seed=2)
+    net = snn.Network(wl, inp["params"], device=DEV)
+    assert any(b > 0 for b in net.dcur_t_bytes)
+    x, lab = _t(inp["x"]), _t(inp["labels"])
+    net.step(x, labels=lab)
+    ref = [_np(t).copy() for t in net.gW + net.gb]
+    net.transposed_operand = True
+    net.step_stages(x, labels=lab)
+    for a, b in zip(ref, [_np(t) for t in net.gW + net.gb]):
+        np.testing.assert_array_equal(a, b)
+
+
 # recurrent neuron (eq. 7): one recurrent weight per neuron, column c of the
 # [T, B*N] layout is neuron c % N.  (8, 65538) takes the 4-column lanes with
 # groups that straddle two samples; (9, 65537) the 1-column lanes.
