@@ -448,7 +448,7 @@ def scan_wide_leg(args, stream):
     from paper_2211_10725_amd import workloads as wls
     wl = wls.get(SCAN_WORKLOAD)
     net = snn.Network(wl, wls.init_params(wl, args.seed), device="cuda")
-    steps, warm = max(2, min(args.steps, 10)), 2
+    steps, warm = max(2, min(args.steps, 10)), 5
     with torch.cuda.stream(stream):
         x, y, tgt = _inputs(wl, args.seed)
         for _ in range(warm):

@@ -4,7 +4,7 @@
 // Layout: every tensor is time-major [T, C] with C = B * n columns, column
 // fastest.  One lane owns VEC consecutive columns for all T steps and keeps
 // the neuron state in registers; a wave therefore streams 64*VEC contiguous
-// floats per step (1 KiB for VEC = 4), fully coalesced.  The inputs of the
+// floats per step (512 bytes for VEC = 2), fully coalesced.  The inputs of the
 // next D steps do not depend on the state, so each lane keeps a ring of D
 // prefetched steps in registers to keep enough HBM requests in flight while
 // the sequential recurrence runs.
@@ -24,28 +24,17 @@ namespace snn {
 namespace {
 
 constexpr int kThreads = 256;
-// Lanes own 4 columns and prefetch 6 steps when there are enough columns to
-// fill the chip (on the 65536 x 64-column layer 6 sustained at least the
-// bandwidth of 8 in every measurement, with fewer registers); otherwise 1
-// column and 16 steps, which gives 4x the waves and halves the number of
-// exposed memory round trips of the serial scan.
-constexpr int kWideColumns = 4 * 64 * 2048;  // 2048 waves of 4-column lanes
+// Lanes own 2 columns when there are enough columns to fill the chip (2^19:
+// 4096 waves of 2-column lanes; on the 65536 x 64-column layer 2 columns and
+// 16 steps ahead measured 4-7 % faster than 4 columns and 8 steps, and 1
+// column slower still), otherwise 1; the forward loads 16 steps ahead.
+constexpr int kWideColumns = 4 * 64 * 2048;
 constexpr int kCkpt = kCheckpointInterval;  // steps per recomputed chunk
 constexpr int kFoldMax = 16;   // most outputs of a dense layer whose input gradient is folded
 constexpr int kFoldRows = 5;   // batch rows one workgroup's columns can span when folding
 
 template <int VEC>
 struct Vec;
-template <>
-struct Vec<4> {
-    static __device__ inline void load(const float *p, float (&v)[4]) {
-        const float4 x = *reinterpret_cast<const float4 *>(p);
-        v[0] = x.x; v[1] = x.y; v[2] = x.z; v[3] = x.w;
-    }
-    static __device__ inline void store(float *p, const float (&v)[4]) {
-        *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
-    }
-};
 template <>
 struct Vec<2> {
     static __device__ inline void load(const float *p, float (&v)[2]) {
@@ -65,11 +54,7 @@ struct Vec<1> {
 // spikes as bytes 0/1
 template <int VEC>
 __device__ inline void store_spikes_u8(uint8_t *p, const float (&z)[VEC]) {
-    if constexpr (VEC == 4) {
-        const uint32_t w = (uint32_t)z[0] | ((uint32_t)z[1] << 8) | ((uint32_t)z[2] << 16) |
-                           ((uint32_t)z[3] << 24);
-        *reinterpret_cast<uint32_t *>(p) = w;
-    } else if constexpr (VEC == 2) {
+    if constexpr (VEC == 2) {
         *reinterpret_cast<uint16_t *>(p) = (uint16_t)((uint32_t)z[0] | ((uint32_t)z[1] << 8));
     } else {
         p[0] = (uint8_t)z[0];
@@ -79,11 +64,7 @@ __device__ inline void store_spikes_u8(uint8_t *p, const float (&z)[VEC]) {
 // spikes as fp16 0.0 / 1.0 (0x3c00)
 template <int VEC>
 __device__ inline void store_spikes_f16(uint16_t *p, const float (&z)[VEC]) {
-    if constexpr (VEC == 4) {
-        const uint32_t lo = (z[0] != 0.f ? 0x3c00u : 0u) | (z[1] != 0.f ? 0x3c000000u : 0u);
-        const uint32_t hi = (z[2] != 0.f ? 0x3c00u : 0u) | (z[3] != 0.f ? 0x3c000000u : 0u);
-        *reinterpret_cast<uint2 *>(p) = make_uint2(lo, hi);
-    } else if constexpr (VEC == 2) {
+    if constexpr (VEC == 2) {
         *reinterpret_cast<uint32_t *>(p) =
             (z[0] != 0.f ? 0x3c00u : 0u) | (z[1] != 0.f ? 0x3c000000u : 0u);
     } else {
@@ -206,10 +187,7 @@ __device__ inline void store_grad(void *base, int64_t off, const float (&v)[VEC]
             }
         }
         uint16_t *p = reinterpret_cast<uint16_t *>(base) + off;
-        if constexpr (VEC == 4)
-            *reinterpret_cast<uint2 *>(p) =
-                make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
-        else if constexpr (VEC == 2)
+        if constexpr (VEC == 2)
             *reinterpret_cast<uint32_t *>(p) = (uint32_t)h[0] | ((uint32_t)h[1] << 16);
         else
             p[0] = h[0];
@@ -678,7 +656,7 @@ template <int NEURON, int VEC, int OUT>
 void fwd_launch(const ScanArgs &a, const FwdBuffers &b, hipStream_t s) {
     const int64_t lanes = (a.C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
-    neuron_fwd_kernel<NEURON, VEC, OUT, VEC == 4 ? 8 : 16><<<grid, kThreads, 0, s>>>(
+    neuron_fwd_kernel<NEURON, VEC, OUT, 16><<<grid, kThreads, 0, s>>>(
         a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.vrec, b.cur, b.spk, b.u_out, b.ckpt, b.counts);
 }
 
@@ -725,15 +703,14 @@ void bwd_dispatch_rs(int rs, int gt, const ScanArgs &a, const BwdBuffers &b, hip
     else bwd_dispatch_gt<NEURON, VEC, GM, false>(gt, a, b, s);
 }
 
-// Lane widths: four columns for layers of at least kWideColumns columns
-// (two with a full upstream gradient, whose chunk also holds kCkpt steps of
-// g per column, and two with a folded one, whose lanes also hold their
-// columns of W_up), else one.
+// Lane widths: two columns for layers of at least kWideColumns columns
+// (measured on the 65536 x 64-column layer: 7.0 against 7.4 ms for four
+// columns per lane, whose chunk registers left two waves per SIMD), else one.
 template <int NEURON>
 void bwd_dispatch(int vec, int rs, int gm, int gt, const ScanArgs &a, const BwdBuffers &b,
                   hipStream_t s) {
     if (gm == GM_BCAST) {
-        if (vec == 4) bwd_dispatch_rs<NEURON, 4, GM_BCAST>(rs, gt, a, b, s);
+        if (vec == 2) bwd_dispatch_rs<NEURON, 2, GM_BCAST>(rs, gt, a, b, s);
         else bwd_dispatch_rs<NEURON, 1, GM_BCAST>(rs, gt, a, b, s);
     } else if (gm == GM_FOLD12) {
         if (vec == 2) bwd_dispatch_rs<NEURON, 2, GM_FOLD12>(rs, gt, a, b, s);
@@ -757,20 +734,20 @@ hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, int64_t N, float alph
                              hipStream_t s) {
     if (T <= 0 || C <= 0) return hipSuccess;
     if (neuron_ckpt_count(T) > 0 && ckpt == nullptr) return hipErrorInvalidValue;
-    const bool v4 = (C % 4) == 0 && C >= kWideColumns;
+    const bool v2 = (C % 2) == 0 && C >= kWideColumns;
     const ScanArgs a{T, C, N, alpha, beta, thr, 0.f, vrec};
     const FwdBuffers b{cur, spk, u_out, ckpt, counts};
     switch (neuron) {
         case SNN_SYNAPTIC:
-            if (v4) fwd_dispatch<SNN_SYNAPTIC, 4>(out_dtype, a, b, s);
+            if (v2) fwd_dispatch<SNN_SYNAPTIC, 2>(out_dtype, a, b, s);
             else fwd_dispatch<SNN_SYNAPTIC, 1>(out_dtype, a, b, s);
             break;
         case SNN_RLEAKY:
-            if (v4) fwd_dispatch<SNN_RLEAKY, 4>(out_dtype, a, b, s);
+            if (v2) fwd_dispatch<SNN_RLEAKY, 2>(out_dtype, a, b, s);
             else fwd_dispatch<SNN_RLEAKY, 1>(out_dtype, a, b, s);
             break;
         default:
-            if (v4) fwd_dispatch<SNN_LEAKY, 4>(out_dtype, a, b, s);
+            if (v2) fwd_dispatch<SNN_LEAKY, 2>(out_dtype, a, b, s);
             else fwd_dispatch<SNN_LEAKY, 1>(out_dtype, a, b, s);
     }
     return hipGetLastError();
@@ -797,7 +774,7 @@ hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, 
     if (gm == GM_FULL) {
         if (wide && C % 2 == 0) vec = 2;
     } else if (gm == GM_BCAST) {
-        if (wide && C % 4 == 0) vec = 4;
+        if (wide && C % 2 == 0) vec = 2;
     } else if (wide && N % 2 == 0 && N >= 128) {
         // a lane's two columns in one batch row, and the workgroup's 512
         // columns within kFoldRows batch rows

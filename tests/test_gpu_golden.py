@@ -10,9 +10,9 @@ reaches exactly 1.0) must not spike, and the surrogate of eq. (9) there is
 exactly 1.
 
 Each case runs on both lane layouts of the scans: one column per lane
-(a small layer) and four consecutive columns per lane (layers of at least
+(a small layer) and two consecutive columns per lane (layers of at least
 2^19 columns).  Every column holds one of the group's traces, interleaved so
-that the four columns of a wide lane hold different traces.
+that the columns of a wide lane hold different traces.
 """
 import json
 import os
@@ -28,7 +28,7 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 DEV = "cuda"
-# (B, N): 111 columns (one column per lane); 2^19 columns (four per lane)
+# (B, N): 111 columns (one column per lane); 2^19 columns (two per lane)
 LANES = {"narrow": (3, 37), "wide": (8, 65536)}
 
 

@@ -165,8 +165,8 @@ def test_scan_bwd_half_gradient_operand(gdt, tdt):
 # reverse scan of the layer below (SNN_GRAD_FOLD): the scan computes
 # g[t,b,n] = sum_j dI_up[t,b,j] W_up[j,n] itself.  N = 64: a workgroup's 256
 # columns span 5 batch rows; ragged column counts; n_up 1 and 16; N = 4096
-# (over 512k columns) the 4-column lanes; N = 1018 over 512k columns but not
-# a multiple of 4, the 1-column lanes.
+# (over 512k columns) the 2-column lanes; N = 1018 over 512k columns, also
+# 2-column lanes with ragged workgroups.
 FOLD_SHAPES = [(7, 5, 64, 10), (9, 3, 1000, 10), (5, 4, 100, 1), (6, 2, 130, 16),
                (40, 3, 257, 7), (3, 128, 4096, 10), (2, 516, 1018, 10)]
 
@@ -245,7 +245,7 @@ def test_scan_bwd_transposed_operand(gkind, gdt, T, B, N):
     """The reverse scan's transposed dL/dI (the weight gradient's operand,
     [P][N][B*T] with K index b*T + t) holds exactly the row-major dL/dI's
     16-bit parts: bf16 parts of fp32, or the bf16 / scaled fp16 value; one
-    and four column lanes, ragged chunks (T not a multiple of 16 or 4)."""
+    and two column lanes, ragged chunks (T not a multiple of 16 or 4)."""
     rng = np.random.default_rng(T * 7 + N + B)
     I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
     gcode, tdt = GRAD_TYPES[gdt]
@@ -316,7 +316,7 @@ def test_synapse_bwd_transposed_operand_same_bytes():
         assert_close(_np(gW2), rW, 1e-3, what=f"dW from the transposed {gdt} operand")
 
 
-@pytest.mark.parametrize("name,T,B,width", [("dsnn_half_t100_b512", 20, 64, 512),
+@pytest.mark.parametrize("name,T,B,width", [("dsnn_half_t100_b512", 32, 256, 1024),
                                             ("dsnn_synaptic_t50_b256", 40, 240, 600)])
 def test_step_with_scan_transposed_operand(name, T, B, width):
     """A whole step whose reverse scans write the weight gradients' operands
@@ -336,9 +336,9 @@ def test_step_with_scan_transposed_operand(name, T, B, width):
 
 
 # recurrent neuron (eq. 7): one recurrent weight per neuron, column c of the
-# [T, B*N] layout is neuron c % N.  (8, 65538) takes the 4-column lanes with
-# groups that straddle two samples; (9, 65537) the 1-column lanes.
-RLEAKY_SHAPES = [(1, 2, 8), (7, 3, 101), (33, 4, 256), (50, 5, 1001), (6, 8, 65538),
+# [T, B*N] layout is neuron c % N.  (8, 65537) takes the 2-column lanes with
+# pairs that straddle two samples; (9, 65537) the 1-column lanes (odd count).
+RLEAKY_SHAPES = [(1, 2, 8), (7, 3, 101), (33, 4, 256), (50, 5, 1001), (6, 8, 65537),
                  (3, 9, 65537)]
 
 
