@@ -366,7 +366,9 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const void
 
 /* Bytes of the transposed dL/dI operand (dcur_t of snn_neuron_bwd /
  * snn_synapse_bwd), or 0 when the layer's weight gradient does not take it
- * (conv layers, layers with at most 16 outputs, small products). */
+ * (conv layers, layers with at most 16 outputs, small products, and large
+ * products of a 16-bit dL/dI, which read dL/dI and x in their own
+ * layouts). */
 size_t snn_layer_dcur_t_bytes(const snn_layer_desc *d);
 
 #ifdef __cplusplus

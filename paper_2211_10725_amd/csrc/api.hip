@@ -191,7 +191,16 @@ DwPlan dw_plan(const snn_layer_desc *d) {
     // transposed fragments (measured: 42 against 34 + 17 us of contraction and
     // transposes at 3200 rows, 127 against 85 + 34 us at 12800 rows).
     const bool mn_direct = d->grad_dtype == SNN_F32 && d->in_dtype == SNN_U8 && M <= 8192;
-    p.transposed = split_ok(d) && gemm16_applies(kc) && d->n_out > 16 && !mn_direct &&
+    // A 16-bit dL/dI against 16-bit or spike x on the asynchronous pipeline:
+    // the tiles are staged M/N-contiguous as they are and read with
+    // transposing LDS loads, so no operand is transposed in global memory.
+    GemmArgs mn{};
+    mn.M = d->n_out; mn.N = d->n_in; mn.K = M;
+    mn.a_dtype = d->grad_dtype; mn.a_kc = false; mn.lda = d->n_out;
+    mn.b_dtype = d->in_dtype; mn.b_kc = false; mn.ldb = d->n_in;
+    mn.allow_split = split_ok(d);
+    const bool async_mn = gemm_async_applies(mn);
+    p.transposed = split_ok(d) && gemm16_applies(kc) && d->n_out > 16 && !mn_direct && !async_mn &&
                    2.0 * M * d->n_in * d->n_out >= kTransposeFlops;
     if (p.transposed) {
         p.a_dtype = kc.a_dtype;
@@ -629,12 +638,11 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     char *colsum = base + dcur_bytes(d);
     float *scale = scaled_grad(d) ? reinterpret_cast<float *>(colsum + neuron_ws(d)) : nullptr;
     char *gws = colsum + neuron_ws(d) + scale_slot_bytes(d);
-    // The reverse scan could write the weight gradient's transposed operand
-    // itself (dcur_t), but its rows are written in runs of one chunk (16
-    // steps, 32 bytes) per lane, which measured slower than the row-major
-    // write plus one transpose (fp16 net: 0.72 + 0.78 ms of scans against
-    // 0.41 + 0.47 ms and 0.31 ms of transposes), so the layer call keeps the
-    // transpose.
+    // Where the weight gradient takes a transposed operand (fp32 dL/dI as
+    // three bf16 parts), the reverse scan could write it itself (dcur_t), but
+    // its rows are written in runs of one chunk (16 steps, 32 bytes) per
+    // lane, which measured slower than the row-major write plus one
+    // transpose, so the layer call keeps the transpose.
     void *dcur_t = nullptr;
     void *dcur_rm = dcur;
     st = snn_neuron_bwd(d, grad, v, cur, ckpt, dcur_rm, dcur_t, scale, grad_b, grad_v, colsum,

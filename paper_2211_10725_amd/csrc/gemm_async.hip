@@ -29,6 +29,8 @@
 // K must be a multiple of 8 (a 16-byte chunk is all in range or all out); the
 // chunks past K of the last k-tile are loaded from column 0 and zeroed before
 // the multiply.  Rows past M (N) load row M-1 (N-1) and are not stored.
+#include <type_traits>
+
 #include "snn_internal.hpp"
 
 namespace snn {
@@ -77,7 +79,7 @@ __device__ inline floatx16 mfma32(const u32x4 &a, const u32x4 &b, const floatx16
 // read one row's 128 contiguous bytes.  The per-thread row pointers (row
 // clamped to the operand) and chunk offsets are fixed for the whole k loop; a
 // chunk past K reads column 0 instead (zeroed before use).
-struct TileCopy {
+struct TileCopyKC {
     const uint16_t *row[4];
     int c8[4];  // 8 * chunk
 
@@ -100,6 +102,45 @@ struct TileCopy {
         }
     }
 };
+
+// M/N-contiguous operand ([k][row] in memory: dL/dI and the spikes in the
+// weight gradient dW = dI^T x, K = T*B).  A stage holds [64 k-rows][256 rows]
+// (512 bytes per k-row); 16-byte chunk c (rows 8c .. 8c + 7) of k-row k is
+// stored at slot c ^ mn_swz(k).  Wave w, copy j fills stage bytes
+// [(4 w + j) KiB, +1 KiB): k-rows 8 w + 2 j + lane / 32, slot lane % 32; the
+// 32 lanes of a k-row read its 512 contiguous bytes.  k-rows past the end read
+// the last one (zeroed before use); chunks past the last row read the last
+// chunk (not stored).  Needs rows % 8 == 0.
+__device__ inline int mn_swz(int k) { return 2 * ((k & 3) | ((k & 1) << 2)); }
+
+struct TileCopyMN {
+    const uint16_t *X;
+    int64_t ld;
+    int col[2];  // first row of the chunk this thread copies, for j even / odd
+    int kr0;     // k-row of copy 0 within the tile
+
+    __device__ inline void init(const uint16_t *X_, int64_t ld_, int rows, int r0) {
+        const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+        X = X_;
+        ld = ld_;
+        kr0 = 8 * w + (lane >> 5);
+#pragma unroll
+        for (int jj = 0; jj < 2; ++jj)
+            col[jj] = min(r0 + 8 * ((lane & 31) ^ mn_swz(kr0 + 2 * jj)), rows - 8);
+    }
+    __device__ inline void copy(int k0, int K, uint16_t *stage) const {
+        const int w = threadIdx.x >> 6;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int k = min(k0 + kr0 + 2 * j, K - 1);
+            __builtin_amdgcn_global_load_lds(X + (int64_t)k * ld + col[j & 1],
+                                             (lds_void *)(stage + (4 * w + j) * 512), 16, 0, 0);
+        }
+    }
+};
+
+template <bool MN>
+using TileCopy = typename std::conditional<MN, TileCopyMN, TileCopyKC>::type;
 
 // Wait until this thread's copies of the stage to multiply have landed (the
 // only ones in flight), then the workgroup barrier: every wave's copies of
@@ -168,6 +209,170 @@ __device__ inline void multiply_stage(floatx16 (&acc)[4][2], int wm, int wn, int
     }
 }
 
+// M/N-contiguous stages: a fragment is two transposing reads.  Within each 16
+// lanes, ds_read_b64_tr_b16 hands lane i element e of lane 4 e + i / 4's
+// 4-element run (position i % 4).  Lane L of 16-lane group g points at k-row
+// kb + L / 4 and rows j0 + 4 (L % 4), j0 = fragment row + 16 (g & 1), kb =
+// 16 ks + 8 (g >> 1) + 4 r: lane i of the group receives k = kb .. kb + 3 of
+// row j0 + i, and reads r = 0, 1 make the 8 k-contiguous values of the MFMA
+// operand.  A read's 16-lane group covers 4 k-rows of 32 bytes each: with the
+// chunk slots XORed by mn_swz(k) (k mod 4 -> 32-byte slot XOR 0, 5, 2, 7),
+// the 4 k-rows of a group fall on distinct banks of a 128-byte line and the 8
+// of two groups on distinct banks of a 256-byte line.  k mod 4 is fixed per
+// lane, so step ks and read r are constant offsets from the lane's address.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ inline void lds_read_tr(u32x2 &v, uint32_t addr) {
+    asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(v) : "v"(addr));
+}
+
+template <int S>
+__device__ inline uint32_t frag_addr_mn(int wm, int wn, int i) {
+    const int lane = threadIdx.x & 63, g = lane >> 4, L = lane & 15;
+    const uint16_t *stage = i < 4 ? stage_a<S>() : stage_b<S>();
+    const int row = (i < 4 ? wm * 128 + i * 32 : wn * 64 + (i - 4) * 32) + 16 * (g & 1) + 4 * (L & 3);
+    const int kr = 8 * (g >> 1) + (L >> 2);
+    return lds_addr(stage + kr * kTile + ((row >> 3) ^ mn_swz(kr)) * 8 + (row & 7));
+}
+
+template <int MT, int S>
+__device__ inline void multiply_stage_mn(floatx16 (&acc)[4][2], int wm, int wn, int kvalid) {
+    const int half = (threadIdx.x & 63) >> 5;
+    uint32_t base[6];
+#pragma unroll
+    for (int i = 0; i < 6; ++i) base[i] = frag_addr_mn<S>(wm, wn, i);
+    u32x2 f[2][6][2];
+#pragma unroll
+    for (int i = 0; i < 6; ++i)
+#pragma unroll
+        for (int r = 0; r < 2; ++r) lds_read_tr(f[0][i][r], base[i] + r * 4 * kTile * 2);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+        u32x2(&cur)[6][2] = f[ks & 1];
+        u32x2(&nxt)[6][2] = f[(ks + 1) & 1];
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(cur[0][0]), "+v"(cur[0][1]), "+v"(cur[1][0]), "+v"(cur[1][1]),
+                       "+v"(cur[2][0]), "+v"(cur[2][1]), "+v"(cur[3][0]), "+v"(cur[3][1]),
+                       "+v"(cur[4][0]), "+v"(cur[4][1]), "+v"(cur[5][0]), "+v"(cur[5][1]));
+        if (kvalid < kKT) {
+            const uint32_t m = 8 * (2 * ks + half) < kvalid ? 0xffffffffu : 0u;
+#pragma unroll
+            for (int i = 0; i < 6; ++i) {
+                cur[i][0] &= m;
+                cur[i][1] &= m;
+            }
+        }
+        u32x4 op[6];
+#pragma unroll
+        for (int i = 0; i < 6; ++i) op[i] = __builtin_shufflevector(cur[i][0], cur[i][1], 0, 1, 2, 3);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int i = q >> 1, j = q & 1;
+            acc[i][j] = mfma32<MT>(op[i], op[4 + j], acc[i][j]);
+            __builtin_amdgcn_sched_barrier(0);
+            if (ks + 1 < 4 && q < 6) {
+#pragma unroll
+                for (int r = 0; r < 2; ++r)
+                    lds_read_tr(nxt[q][r], base[q] + ((ks + 1) * 16 + r * 4) * kTile * 2);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+}
+
+template <int MT, bool MN, int S>
+__device__ inline void multiply(floatx16 (&acc)[4][2], int wm, int wn, int kvalid) {
+    if constexpr (MN) multiply_stage_mn<MT, S>(acc, wm, wn, kvalid);
+    else multiply_stage<MT, S>(acc, wm, wn, kvalid);
+}
+
+// ---- storing a 256 x 256 fp32 result tile ------------------------------------
+// In the 32x32 MFMA block (i, q) of wave (wm, wn), a lane holds column
+// wn * 64 + 32 q + (lane & 31) and, in register r, row wm * 128 + 32 i +
+// 8 (r / 4) + 4 (lane / 32) + r % 4 of the tile.  A scaled operand's power of
+// two is divided out exactly (multiplication by its exact reciprocal).
+
+// Directly from the registers: every store instruction writes two 128-byte
+// row pieces (for C rows that are not 16-byte aligned).
+__device__ inline void store_tile_direct(const floatx16 (&acc)[4][2], float *Cz, int64_t ldc,
+                                         int M, int N, int m0, int n0, int wm, int wn, float inv,
+                                         const float (&bn)[2]) {
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const int n = n0 + wn * 64 + q * 32 + (lane & 31);
+            if (n >= N) continue;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int m = m0 + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                if (m < M) Cz[(int64_t)m * ldc + n] = acc[i][q][r] * inv + bn[q];
+            }
+        }
+}
+
+// Through LDS (the second stage, free once every wave is past its last
+// multiply): four passes of 64 tile rows.  In a pass the four waves that hold
+// those rows write them into a [64][256] fp32 tile (column c of row R at
+// c ^ 32 (R & 4 ? 1 : 0), so the two half-waves of a write fall on distinct
+// banks), then every thread stores 16 contiguous bytes of a row: each store
+// instruction writes one whole 1 KiB row of C.  Measured on the
+// 51200 x 4096 products: a quarter of the store instructions of the direct
+// epilogue and about a fifth of the kernel time at K = 784.
+__device__ inline void store_tile_lds(const floatx16 (&acc)[4][2], float *Cz, int64_t ldc, int M,
+                                      int N, int m0, int n0, int wm, int wn, float inv,
+                                      const float (&bn)[2]) {
+    float *t = reinterpret_cast<float *>(stage_a<1>());  // 64 KiB: [64][256]
+    const int lane = threadIdx.x & 63;
+    const bool full = m0 + kTile <= M && n0 + kTile <= N;
+#pragma unroll
+    for (int pass = 0; pass < 4; ++pass) {
+        __syncthreads();  // the stage (or the previous pass) is no longer read
+        if (wm == pass / 2) {
+#pragma unroll
+            for (int ii = 0; ii < 2; ++ii) {
+                const int i = 2 * (pass & 1) + ii;
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    const int c = wn * 64 + q * 32 + (lane & 31);
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int R = ii * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+                        t[R * 256 + (c ^ ((R & 4) << 3))] = acc[i][q][r] * inv + bn[q];
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        const int c = 4 * lane, n = n0 + c;
+        float4 v[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            const int R = (threadIdx.x >> 6) + 8 * k;  // one row per wave and k
+            v[k] = *reinterpret_cast<const float4 *>(&t[R * 256 + (c ^ ((R & 4) << 3))]);
+        }
+        float *row = Cz + (int64_t)(m0 + 64 * pass + (threadIdx.x >> 6)) * ldc + n;
+        if (full) {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) *reinterpret_cast<float4 *>(row + 8 * k * ldc) = v[k];
+        } else {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                if (m0 + 64 * pass + (threadIdx.x >> 6) + 8 * k >= M) continue;
+                float *dst = row + 8 * k * ldc;
+                if (n + 3 < N) {
+                    *reinterpret_cast<float4 *>(dst) = v[k];
+                } else {
+                    if (n < N) dst[0] = v[k].x;
+                    if (n + 1 < N) dst[1] = v[k].y;
+                    if (n + 2 < N) dst[2] = v[k].z;
+                }
+            }
+        }
+    }
+}
+
 // Work item i of the launch (a tile and a K split) for persistent workgroup
 // w of G: the items are cut into kXcds contiguous ranges, one per XCD
 // (workgroup w runs on XCD w % kXcds), and the XCD's workgroups take the
@@ -185,10 +390,10 @@ __device__ inline int persistent_item(int w, int G, int total, int j) {
 
 // Persistent: gridDim.x workgroups (one per CU) loop over the work items.
 // The first k-tile of a workgroup's next item is copied into stage 0 before
-// the current item's results are stored (stage 0 was last read before the
+// the current item's results are stored (through stage 1) (stage 0 was last read before the
 // barrier of the current item's final k-tile), so that latency overlaps the
 // stores.
-template <int MT>
+template <int MT, bool MN>
 __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
     int M, int N, int K, int k_chunk, int tiles_n, int tiles, int total,
     const uint16_t *__restrict__ A, int64_t lda, const uint16_t *__restrict__ B, int64_t ldb,
@@ -197,9 +402,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
     const int wave = threadIdx.x >> 6, wm = wave & 1, wn = wave >> 1;
     const int lane = threadIdx.x & 63;
     const float inv = c_div ? 1.f / c_div[0] : 1.f;
+    // rows of C (and of every split's partial sums) start on 16 bytes
+    const bool wide_stores = ((uintptr_t)C & 15) == 0 && (ldc & 3) == 0 && (split_stride & 3) == 0;
     int item = persistent_item(blockIdx.x, gridDim.x, total, 0);
     if (item < 0) return;
-    TileCopy ca, cb;
+    TileCopy<MN> ca, cb;
     auto setup = [&](int it, int &m0, int &n0, int &zk, int &kbeg, int &kend, int &nk) {
         zk = it / tiles;
         const int tile = it % tiles;
@@ -237,39 +444,35 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
             ca.copy(SNN_KTILE(tt + 1), kend, stage_a<NEXT>());                              \
             cb.copy(SNN_KTILE(tt + 1), kend, stage_b<NEXT>());                              \
         }                                                                                   \
-        multiply_stage<MT, S>(acc, wm, wn, kend - (kbeg + kKT * tt));                       \
+        multiply<MT, MN, S>(acc, wm, wn, kend - (kbeg + kKT * tt));                         \
     }
             SNN_ASYNC_STEP(0, 1)
             SNN_ASYNC_STEP(1, 0)
 #undef SNN_ASYNC_STEP
         }
 #undef SNN_KTILE
-        // the next item's first k-tile, in flight during the stores below
+        // This tile's bias values, loaded before the copies below.  The
+        // copies are issued on every path (after the last item they copy its
+        // first k-tile again, into the free stage 0), so the wait for the
+        // bias values is for all but the copies' 8 loads on every path.
         const int m0c = m0, n0c = n0, zkc = zk;
+        float bn[2];
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+            bn[q] = bias ? bias[min(n0c + wn * 64 + q * 32 + (lane & 31), N - 1)] : 0.f;
+        // the next item's first k-tile, in flight during the stores below
         item = persistent_item(blockIdx.x, gridDim.x, total, j + 1);
-        if (item >= 0) {
-            setup(item, m0, n0, zk, kbeg, kend, nk);
-            ca.copy(kbeg, kend, stage_a<0>());
-            cb.copy(kbeg, kend, stage_b<0>());
-        }
-        // 32x32 block: lane holds column (lane & 31); register r holds row
-        // 8*(r/4) + 4*(lane/32) + r%4.  A scaled operand's power of two is
-        // divided out exactly (multiplication by its exact reciprocal).
+        if (item >= 0) setup(item, m0, n0, zk, kbeg, kend, nk);
+        ca.copy(kbeg, kend, stage_a<0>());
+        cb.copy(kbeg, kend, stage_b<0>());
         float *Cz = C + (int64_t)zkc * split_stride;
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int q = 0; q < 2; ++q) {
-                const int n = n0c + wn * 64 + q * 32 + (lane & 31);
-                if (n >= N) continue;
-                const float bn = bias ? bias[n] : 0.f;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int m = m0c + wm * 128 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-                    if (m < M) Cz[(int64_t)m * ldc + n] = acc[i][q][r] * inv + bn;
-                }
-            }
+        if (wide_stores)
+            store_tile_lds(acc, Cz, ldc, M, N, m0c, n0c, wm, wn, inv, bn);
+        else
+            store_tile_direct(acc, Cz, ldc, M, N, m0c, n0c, wm, wn, inv, bn);
     }
+    // the workgroup's LDS must not be released with copies into it in flight
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 // Spike bytes widened to the 16-bit MFMA type: dst[r][k] (ld K) from
@@ -332,9 +535,11 @@ AsyncPlan plan_async(const GemmArgs &g) {
 }  // namespace
 
 bool gemm_async_applies(const GemmArgs &g) {
-    if (!g.allow_split || !g.a_kc || !g.b_kc) return false;
+    // both operands K-contiguous, or both M/N-contiguous
+    if (!g.allow_split || g.a_kc != g.b_kc) return false;
     if (mfma_type(g.a_dtype, g.b_dtype) < 0) return false;
     if (g.K % 8 != 0 || g.K < 256 || g.M < kTile || g.N < kTile) return false;
+    if (!g.a_kc && (g.M % 8 != 0 || g.N % 8 != 0)) return false;
     if (g.a_dtype != SNN_U8 && g.lda % 8 != 0) return false;
     if (g.b_dtype != SNN_U8 && g.ldb % 8 != 0) return false;
     // large enough to fill the device with 256 x 256 tiles (K split as needed)
@@ -357,25 +562,26 @@ hipError_t launch_gemm_async(const GemmArgs &g, void *ws, size_t ws_bytes, hipSt
     const uint16_t *A = reinterpret_cast<const uint16_t *>(g.A);
     const uint16_t *B = reinterpret_cast<const uint16_t *>(g.B);
     int64_t lda = g.lda, ldb = g.ldb;
+    const bool mn = !g.a_kc;
+    // a spike operand widened in its own layout: [rows][K] or [K][rows]
+    auto widen = [&](const void *src, int64_t ld, int rows, uint16_t *d) {
+        const int r = mn ? g.K : rows, c = mn ? rows : g.K;
+        const int64_t n = (int64_t)r * (c / 8);
+        if (mt == MT_F16)
+            widen_kernel<MT_F16><<<blocks(n), kThreads, 0, s>>>(r, c, reinterpret_cast<const uint8_t *>(src), ld, d);
+        else
+            widen_kernel<MT_BF16><<<blocks(n), kThreads, 0, s>>>(r, c, reinterpret_cast<const uint8_t *>(src), ld, d);
+        return (int64_t)c;
+    };
     if (p.a_bytes) {
         uint16_t *d = reinterpret_cast<uint16_t *>(w);
-        const int64_t n = (int64_t)g.M * (g.K / 8);
-        if (mt == MT_F16)
-            widen_kernel<MT_F16><<<blocks(n), kThreads, 0, s>>>(g.M, g.K, reinterpret_cast<const uint8_t *>(g.A), g.lda, d);
-        else
-            widen_kernel<MT_BF16><<<blocks(n), kThreads, 0, s>>>(g.M, g.K, reinterpret_cast<const uint8_t *>(g.A), g.lda, d);
+        lda = widen(g.A, g.lda, g.M, d);
         A = d;
-        lda = g.K;
     }
     if (p.b_bytes) {
         uint16_t *d = reinterpret_cast<uint16_t *>(w + p.a_bytes);
-        const int64_t n = (int64_t)g.N * (g.K / 8);
-        if (mt == MT_F16)
-            widen_kernel<MT_F16><<<blocks(n), kThreads, 0, s>>>(g.N, g.K, reinterpret_cast<const uint8_t *>(g.B), g.ldb, d);
-        else
-            widen_kernel<MT_BF16><<<blocks(n), kThreads, 0, s>>>(g.N, g.K, reinterpret_cast<const uint8_t *>(g.B), g.ldb, d);
+        ldb = widen(g.B, g.ldb, g.N, d);
         B = d;
-        ldb = g.K;
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -392,14 +598,10 @@ hipError_t launch_gemm_async(const GemmArgs &g, void *ws, size_t ws_bytes, hipSt
     const int tiles = p.tiles_m * p.tiles_n, total = tiles * p.splits;
     // one persistent workgroup per compute unit (128 KiB of LDS each)
     const unsigned grid = (unsigned)min(total, device_cus());
-    if (mt == MT_F16)
-        gemm_async_kernel<MT_F16><<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n,
-                                                            tiles, total, A, lda, B, ldb, out, ldo,
-                                                            ss, bias, c_div);
-    else
-        gemm_async_kernel<MT_BF16><<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n,
-                                                             tiles, total, A, lda, B, ldb, out, ldo,
-                                                             ss, bias, c_div);
+    auto kernel = mt == MT_F16 ? (mn ? gemm_async_kernel<MT_F16, true> : gemm_async_kernel<MT_F16, false>)
+                               : (mn ? gemm_async_kernel<MT_BF16, true> : gemm_async_kernel<MT_BF16, false>);
+    kernel<<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n, tiles, total, A, lda, B,
+                                     ldb, out, ldo, ss, bias, c_div);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (p.splits > 1)

@@ -286,10 +286,14 @@ def test_synapse_bwd_transposed_operand_same_bytes():
     """The weight gradient from the scan's transposed operand equals the one
     from the row-major dL/dI (transposed inside the call): the same operand
     bytes in the same contraction."""
-    T, B, N, K = 40, 240, 600, 784  # 9600 rows: the transposed path
+    T, B, N, K = 40, 240, 600, 784  # 9600 rows: the transposed path for fp32 dL/dI
     rng = np.random.default_rng(3)
     spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
-    for gdt in ("f32", "bf16"):
+    # a 16-bit dL/dI is contracted in its own layout: no transposed operand
+    for gdt in ("bf16", "f16"):
+        assert snn.snn_layer_dcur_t_bytes(snn.layer_desc(spec, T, B,
+                                                         grad_dtype=GRAD_TYPES[gdt][0])) == 0
+    for gdt in ("f32",):
         gcode, tdt = GRAD_TYPES[gdt]
         d = snn.layer_desc(spec, T, B, grad_dtype=gcode)
         assert snn.snn_layer_dcur_t_bytes(d) > 0
@@ -316,8 +320,7 @@ def test_synapse_bwd_transposed_operand_same_bytes():
         assert_close(_np(gW2), rW, 1e-3, what=f"dW from the transposed {gdt} operand")
 
 
-@pytest.mark.parametrize("name,T,B,width", [("dsnn_half_t100_b512", 32, 256, 1024),
-                                            ("dsnn_synaptic_t50_b256", 40, 240, 600)])
+@pytest.mark.parametrize("name,T,B,width", [("dsnn_synaptic_t50_b256", 40, 240, 600)])
 def test_step_with_scan_transposed_operand(name, T, B, width):
     """A whole step whose reverse scans write the weight gradients' operands
     transposed gives the layer calls' gradients bit for bit (the same operand
@@ -523,6 +526,47 @@ def test_synapse_bwd_operand_types(M, N, K, gdt, wdt):
     aI = np.abs(dI_used)
     _assert_fp32_sum(gotW - rW, aI.T @ x.astype(np.float64), M, "dW")
     _assert_fp32_sum(gotx - rx, aI @ np.abs(W).astype(np.float64), N, "dx")
+
+
+# (rows T*B, n_out, n_in, x dtype): weight gradients of a 16-bit dL/dI large
+# enough for the asynchronous pipeline, which stages dL/dI [T*B][n_out] and x
+# [T*B][n_in] tiles as they are stored; ragged 256-tiles on both sides, a
+# partial last k-tile (rows not a multiple of 64) and splits over K.
+MN_DW_SHAPES = [(9640, 600, 784, "u8"), (8200, 264, 520, "f16"), (12800, 1000, 784, "f16")]
+
+
+@pytest.mark.parametrize("M,N,K,xdt", MN_DW_SHAPES)
+@pytest.mark.parametrize("gdt", ["bf16", "f16"])
+def test_synapse_bwd_dw_own_layout(M, N, K, xdt, gdt):
+    """dW = dI^T x from the M/N-contiguous operands (no transpose in memory):
+    products of the 16-bit values are exact, so the result is their fp32 sum."""
+    if gdt == "bf16" and xdt == "f16":
+        pytest.skip("bf16 dL/dI against fp16 x has no common MFMA type")
+    rng = np.random.default_rng(M + N + K)
+    gcode, tdt = GRAD_TYPES[gdt]
+    if xdt == "u8":
+        x = (rng.random((M, K)) < 0.3).astype(np.uint8)
+        x_dev, in_dt = _t(x), snn.U8
+    else:
+        x = (rng.random((M, K)) < 0.3).astype(np.float16)
+        x_dev, in_dt = _t(x, torch.float16), snn.F16
+    dI = rng.normal(0, 1e-3, (M, N)).astype(np.float32)
+    S = pow2_scale(dI) if gcode == snn.F16 else 1.0
+    dI_h = torch.as_tensor(dI * np.float32(S)).to(tdt)
+    dI_used = dI_h.float().numpy().astype(np.float64) / S
+    sc = _t(np.full(4, S, np.float32)) if gcode == snn.F16 else None
+    spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
+    d = snn.layer_desc(spec, 1, M, grad_dtype=gcode, in_dtype=in_dt, w_dtype=snn.F16)
+    assert snn.snn_layer_dcur_t_bytes(d) == 0
+    gW = torch.empty((N, K), dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    W = _t(np.zeros((N, K), np.float16), torch.float16)
+    snn.snn_synapse_bwd(d, dI_h.to(DEV), None, x_dev, W, gW, None, ws, dcur_scale=sc)
+    xf = x.astype(np.float64)
+    rW = dI_used.T @ xf
+    got = _np(gW)
+    assert_close(got, rW, 1e-3, what="dW")
+    _assert_fp32_sum(got - rW, np.abs(dI_used).T @ xf, M, "dW")
 
 
 # ---------------------------------------------------------------------------
