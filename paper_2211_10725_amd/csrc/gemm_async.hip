@@ -178,12 +178,16 @@ __device__ inline uint32_t frag_addr(int wm, int wn, int ks, int i) {
 // step ks + 1 are issued one by one between the 8 MFMAs of step ks
 // (scheduling barriers keep that order), so the wave issues them while the
 // matrix core is busy instead of stalling on them between steps.
-template <int MT, int S>
-__device__ inline void multiply_stage(floatx16 (&acc)[4][2], int wm, int wn, int kvalid) {
+template <int MT, int S, typename Issue>
+__device__ inline void multiply_stage(floatx16 (&acc)[4][2], int wm, int wn, int kvalid,
+                                      const Issue &issue) {
     const int half = (threadIdx.x & 63) >> 5;
     u32x4 f[2][6];
 #pragma unroll
     for (int i = 0; i < 6; ++i) lds_read(f[0][i], frag_addr<S>(wm, wn, 0, i));
+    __builtin_amdgcn_sched_barrier(0);
+    issue();
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
         u32x4(&cur)[6] = f[ks & 1];
@@ -235,8 +239,9 @@ __device__ inline uint32_t frag_addr_mn(int wm, int wn, int i) {
     return lds_addr(stage + kr * kTile + ((row >> 3) ^ mn_swz(kr)) * 8 + (row & 7));
 }
 
-template <int MT, int S>
-__device__ inline void multiply_stage_mn(floatx16 (&acc)[4][2], int wm, int wn, int kvalid) {
+template <int MT, int S, typename Issue>
+__device__ inline void multiply_stage_mn(floatx16 (&acc)[4][2], int wm, int wn, int kvalid,
+                                         const Issue &issue) {
     const int half = (threadIdx.x & 63) >> 5;
     uint32_t base[6];
 #pragma unroll
@@ -246,6 +251,9 @@ __device__ inline void multiply_stage_mn(floatx16 (&acc)[4][2], int wm, int wn, 
     for (int i = 0; i < 6; ++i)
 #pragma unroll
         for (int r = 0; r < 2; ++r) lds_read_tr(f[0][i][r], base[i] + r * 4 * kTile * 2);
+    __builtin_amdgcn_sched_barrier(0);
+    issue();
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks) {
         u32x2(&cur)[6][2] = f[ks & 1];
@@ -280,10 +288,14 @@ __device__ inline void multiply_stage_mn(floatx16 (&acc)[4][2], int wm, int wn, 
     }
 }
 
-template <int MT, bool MN, int S>
-__device__ inline void multiply(floatx16 (&acc)[4][2], int wm, int wn, int kvalid) {
-    if constexpr (MN) multiply_stage_mn<MT, S>(acc, wm, wn, kvalid);
-    else multiply_stage<MT, S>(acc, wm, wn, kvalid);
+// The stage's first fragment reads go out before issue() (the copies of the
+// next k-tile into the other stage), so their latency covers the copies'
+// address arithmetic and issue.
+template <int MT, bool MN, int S, typename Issue>
+__device__ inline void multiply(floatx16 (&acc)[4][2], int wm, int wn, int kvalid,
+                                const Issue &issue) {
+    if constexpr (MN) multiply_stage_mn<MT, S>(acc, wm, wn, kvalid, issue);
+    else multiply_stage<MT, S>(acc, wm, wn, kvalid, issue);
 }
 
 // ---- storing a 256 x 256 fp32 result tile ------------------------------------
@@ -440,11 +452,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
     {                                                                                       \
         const int tt = t + (S);                                                             \
         stage_barrier();                                                                    \
-        if (tt + 1 < nk2) {                                                                 \
-            ca.copy(SNN_KTILE(tt + 1), kend, stage_a<NEXT>());                              \
-            cb.copy(SNN_KTILE(tt + 1), kend, stage_b<NEXT>());                              \
-        }                                                                                   \
-        multiply<MT, MN, S>(acc, wm, wn, kend - (kbeg + kKT * tt));                         \
+        multiply<MT, MN, S>(acc, wm, wn, kend - (kbeg + kKT * tt), [&] {                    \
+            if (tt + 1 < nk2) {                                                             \
+                ca.copy(SNN_KTILE(tt + 1), kend, stage_a<NEXT>());                          \
+                cb.copy(SNN_KTILE(tt + 1), kend, stage_b<NEXT>());                          \
+            }                                                                               \
+        });                                                                                 \
     }
             SNN_ASYNC_STEP(0, 1)
             SNN_ASYNC_STEP(1, 0)
