@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 7
+#define SNN_ABI_VERSION 8
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -261,6 +261,61 @@ snn_status snn_loss(int32_t kind, int32_t B, int32_t K, int32_t P, const float *
 snn_status snn_loss_noalloc(int32_t kind, int32_t B, int32_t K, int32_t P, const float *counts,
                             const int32_t *labels, const float *targets, float *loss,
                             float *grad_counts, hipStream_t stream);
+
+/* ---- whole step of a small two-layer network in one launch -----------------
+ * Forward, loss and BPTT backward of a dense hidden layer (spike input x
+ * [T,B,n_in] u8 0 / 1, a nonzero byte counting as 1; fp32 weights) and a
+ * dense readout whose spike counts feed the loss, as one kernel: for small batches (Sec. IV's small-batch
+ * results), where the step as separate calls is a chain of launch
+ * latencies.  The arithmetic is that of snn_layer_fwd / snn_loss /
+ * snn_layer_bwd on the same network with the readout's input gradient folded
+ * into the hidden layer's reverse scan: exact products of the spikes with
+ * the fp32 weights' three bf16 parts, fp32 accumulation (in another order
+ * than the layer calls, so a current may differ in its last bits), the same
+ * scans, adjoints and loss.  Workgroups own hidden neurons; grid-wide
+ * barriers separate packing the input to bits, the hidden forward, the
+ * readout with the loss, and the hidden backward.  The grid is at most one
+ * workgroup per compute unit (resident at once on an otherwise idle device);
+ * each barrier wait polls at most wait_limit times (0: a default of about
+ * 0.1 s or more), and a workgroup that gives up writes 1 to *status and
+ * skips the rest of the step, so the launch ends whatever happens (the
+ * outputs are then undefined; so it goes when another kernel holds compute
+ * units meanwhile).  *status is 0 after a step that
+ * completed.  The barrier counters are device state of the library, clear
+ * after every launch: calls that overlap on one device must not be made. */
+typedef struct snn_fused_desc {
+    snn_layer_desc hidden;   /* SNN_SYN_DENSE, in_dtype SNN_U8, w_dtype SNN_F32,
+                                SNN_LEAKY or SNN_SYNAPTIC, n_in and n_out
+                                multiples of 8 */
+    snn_layer_desc readout;  /* SNN_SYN_DENSE, n_in = hidden.n_out, n_out <= 16,
+                                w_dtype SNN_F32, same T (1..32) and B (>= 1),
+                                SNN_LEAKY or SNN_SYNAPTIC */
+    int32_t loss_kind;       /* SNN_LOSS_CE_COUNT | SNN_LOSS_MSE_COUNT */
+    int32_t pop;             /* population size P, readout.n_out = K * P */
+    uint32_t wait_limit;     /* polls per barrier wait before giving up; 0: default */
+    int32_t reserved;        /* 0 */
+} snn_fused_desc;
+
+/* SNN_OK if snn_fused_step runs this network on the current device, else the
+ * reason: SNN_ERR_UNSUPPORTED (layer kinds, neurons, sizes above, too many
+ * hidden neurons or too large T*B for one co-resident grid with its state in
+ * LDS), SNN_ERR_DTYPE, SNN_ERR_SHAPE, or the layer descriptors' own errors. */
+snn_status snn_fused_step_check(const snn_fused_desc *d);
+size_t snn_fused_step_workspace_bytes(const snn_fused_desc *d);
+
+/* x [T,B,n_in] u8; w0 [n_hid,n_in], b0 [n_hid] (nullable), w1 [n_out,n_hid],
+ * b1 [n_out] (nullable), fp32.  labels int32 [B] (cross-entropy) or targets
+ * fp32 [B,K] (MSE).  Outputs (each nullable except status): loss (fp32 [1],
+ * the batch mean as snn_loss), counts [B,n_out] (readout spike counts),
+ * spk_hidden u8 [T,B,n_hid] (the hidden layer's spikes), grad_w0, grad_b0,
+ * grad_w1, grad_b1 (fp32, shapes of the parameters); status int32 [1] on the
+ * device.  All device pointers 16-byte aligned. */
+snn_status snn_fused_step(const snn_fused_desc *d, const uint8_t *x, const float *w0,
+                          const float *b0, const float *w1, const float *b1,
+                          const int32_t *labels, const float *targets, float *loss,
+                          float *counts, uint8_t *spk_hidden, float *grad_w0, float *grad_b0,
+                          float *grad_w1, float *grad_b1, int32_t *status, void *ws,
+                          size_t ws_bytes, hipStream_t stream);
 
 /* ---- weight update ---------------------------------------------------------
  * AdamW, the optimizer the paper trains every network with (Sec. IV): for

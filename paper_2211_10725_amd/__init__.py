@@ -31,7 +31,7 @@ RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST, GRAD_FOLD = 0, 1, 2
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 7
+ABI_VERSION = 8
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
           4: "SNN_ERR_ALIGN", 5: "SNN_ERR_UNSUPPORTED", 6: "SNN_ERR_WORKSPACE",
@@ -41,7 +41,8 @@ EXPORTS = ["snn_abi_version", "snn_status_str", "snn_layer_saved_bytes",
            "snn_layer_workspace_bytes", "snn_layer_fwd", "snn_layer_bwd",
            "snn_loss_workspace_bytes", "snn_loss", "snn_synapse_fwd", "snn_neuron_fwd",
            "snn_neuron_bwd", "snn_synapse_bwd", "snn_adamw", "snn_loss_noalloc",
-           "snn_layer_saved_layout", "snn_layer_dcur_t_bytes"]
+           "snn_layer_saved_layout", "snn_layer_dcur_t_bytes", "snn_fused_step_check",
+           "snn_fused_step_workspace_bytes", "snn_fused_step"]
 
 
 class LayerDesc(ctypes.Structure):
@@ -68,6 +69,12 @@ class SavedLayout(ctypes.Structure):
                 ("ckpt_bytes", ctypes.c_size_t), ("pool_offset", ctypes.c_size_t),
                 ("pool_bytes", ctypes.c_size_t), ("ckpt_interval", ctypes.c_int32),
                 ("ckpt_count", ctypes.c_int32), ("ckpt_planes", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+class FusedDesc(ctypes.Structure):
+    _fields_ = [("hidden", LayerDesc), ("readout", LayerDesc), ("loss_kind", ctypes.c_int32),
+                ("pop", ctypes.c_int32), ("wait_limit", ctypes.c_uint32),
                 ("reserved", ctypes.c_int32)]
 
 
@@ -126,6 +133,9 @@ def lib():
         "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_layer_dcur_t_bytes": ([D], S),
+        "snn_fused_step_check": ([ctypes.POINTER(FusedDesc)], ctypes.c_int),
+        "snn_fused_step_workspace_bytes": ([ctypes.POINTER(FusedDesc)], S),
+        "snn_fused_step": ([ctypes.POINTER(FusedDesc)] + [P] * 16 + [S, P], ctypes.c_int),
         "snn_adamw": ([ctypes.POINTER(AdamwTensor), i32, ctypes.POINTER(AdamwHparams), P],
                       ctypes.c_int),
     }
@@ -184,7 +194,8 @@ def _grad_in(kind, g):
     return GradIn(kind, 0, _p(g), None, None, 0, 0)
 
 
-_ELEM = {F32: 4, F16: 2, BF16: 2, U8: 1}
+I32 = 100  # int32 arguments (labels, status): not a layer dtype
+_ELEM = {F32: 4, F16: 2, BF16: 2, U8: 1, I32: 4}
 
 
 def _need(fn, t, dtype_code, count, what):
@@ -279,6 +290,47 @@ def snn_loss_noalloc(kind, B, K, P, counts, labels, targets, loss, grad_counts, 
     _check("snn_loss_noalloc", lib().snn_loss_noalloc(kind, B, K, P, _p(counts), _p(labels),
                                                       _p(targets), _p(loss), _p(grad_counts),
                                                       _stream(stream)))
+
+
+def fused_desc(hidden, readout, loss_kind, pop=1, wait_limit=0) -> FusedDesc:
+    f = FusedDesc()
+    f.hidden, f.readout = hidden, readout
+    f.loss_kind, f.pop, f.wait_limit, f.reserved = loss_kind, pop, wait_limit, 0
+    return f
+
+
+def snn_fused_step_check(fd) -> int:
+    return lib().snn_fused_step_check(ctypes.byref(fd))
+
+
+def snn_fused_step_workspace_bytes(fd) -> int:
+    return lib().snn_fused_step_workspace_bytes(ctypes.byref(fd))
+
+
+def snn_fused_step(fd, x, w0, b0, w1, b1, labels, targets, loss, counts, gw0, gb0, gw1, gb1,
+                   status, ws, stream=None, spk_hidden=None):
+    h, r = fd.hidden, fd.readout
+    _need("snn_fused_step", x, U8, h.T * h.B * h.n_in, "x")
+    _need("snn_fused_step", w0, F32, h.n_out * h.n_in, "w0")
+    _need("snn_fused_step", w1, F32, r.n_out * r.n_in, "w1")
+    _need("snn_fused_step", gw0, F32, h.n_out * h.n_in, "grad_w0")
+    _need("snn_fused_step", gw1, F32, r.n_out * r.n_in, "grad_w1")
+    _need("snn_fused_step", counts, F32, h.B * r.n_out, "counts")
+    _need("snn_fused_step", b0, F32, h.n_out, "b0")
+    _need("snn_fused_step", b1, F32, r.n_out, "b1")
+    _need("snn_fused_step", gb0, F32, h.n_out, "grad_b0")
+    _need("snn_fused_step", gb1, F32, r.n_out, "grad_b1")
+    _need("snn_fused_step", loss, F32, 1, "loss")
+    _need("snn_fused_step", status, I32, 1, "status")
+    _need("snn_fused_step", spk_hidden, U8, h.T * h.B * h.n_out, "spk_hidden")
+    if fd.loss_kind == LOSS_CE_COUNT:
+        _need("snn_fused_step", labels, I32, h.B, "labels")
+    else:
+        _need("snn_fused_step", targets, F32, h.B * (r.n_out // max(fd.pop, 1)), "targets")
+    _check("snn_fused_step", lib().snn_fused_step(
+        ctypes.byref(fd), _p(x), _p(w0), _p(b0), _p(w1), _p(b1), _p(labels), _p(targets),
+        _p(loss), _p(counts), _p(spk_hidden), _p(gw0), _p(gb0), _p(gw1), _p(gb1), _p(status),
+        _p(ws), _nbytes(ws), _stream(stream)))
 
 
 def snn_synapse_fwd(desc, x, w, bias, cur, pool_arg, ws, stream=None):
@@ -486,6 +538,17 @@ class Network:
         self.dcur_t_bytes = [snn_layer_dcur_t_bytes(d) for d in self.descs]
         self.transposed_operand = False
         self.dcur_t = torch.empty(max(self.dcur_t_bytes + [256]), dtype=u8, device=device)
+        # The whole step as one cooperative launch (step_fused): two dense
+        # layers on spike input with fp32 weights, small enough for one
+        # co-resident grid; None where snn_fused_step_check refuses the net.
+        self.fdesc = None
+        if n == 2 and not half and all(d.synapse == SYN_DENSE for d in self.descs):
+            fd = fused_desc(self.descs[0].copy(), self.descs[1].copy(), self.loss_kind, self.P)
+            if snn_fused_step_check(fd) == 0:
+                self.fdesc = fd
+                self.fws = torch.empty(max(256, snn_fused_step_workspace_bytes(fd)), dtype=u8,
+                                       device=device)
+                self.fstatus = torch.zeros(4, dtype=torch.int32, device=device)
 
     def forward(self, x, stream=None):
         h = x
@@ -529,6 +592,17 @@ class Network:
         self.forward(x, stream)
         self.loss_and_grad(labels, targets, stream)
         self.backward(x, stream)
+
+    def step_fused(self, x, labels=None, targets=None, stream=None):
+        """The step as one snn_fused_step launch (needs ``fdesc``): the loss,
+        the readout's counts, the hidden spikes and the weight and bias
+        gradients land in the buffers ``step`` writes; ``fstatus[0]`` is 0
+        after a completed step."""
+        if self.fdesc is None:
+            raise RuntimeError("step_fused: the library's fused step does not run this network")
+        snn_fused_step(self.fdesc, x, self.W[0], self.b[0], self.W[1], self.b[1], labels, targets,
+                       self.loss, self.counts, self.gW[0], self.gb[0], self.gW[1], self.gb[1],
+                       self.fstatus, self.fws, stream, spk_hidden=self.spk[0])
 
     def capture_step(self, x, labels=None, targets=None, warmup=2):
         """Capture one forward + loss + BPTT step into a HIP graph (torch's

@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libsnn.so")
-SOURCES = ["api.hip", "scan.hip", "gemm.hip", "gemm_mfma16.hip", "gemm_async.hip", "skinny.hip", "conv.hip", "loss.hip", "optim.hip"]
+SOURCES = ["api.hip", "scan.hip", "gemm.hip", "gemm_mfma16.hip", "gemm_async.hip", "skinny.hip", "conv.hip", "loss.hip", "optim.hip", "fused.hip"]
 
 # No packed-fp32 instructions: some of their forms are not trusted on these
 # parts, so the feature is switched off for every device compilation.

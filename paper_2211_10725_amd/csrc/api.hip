@@ -314,6 +314,33 @@ BwdGrad bwd_grad(const snn_grad_in *g) {
 
 }  // namespace
 
+namespace {
+snn_status check_fused(const snn_fused_desc *f, FusedPlan *plan) {
+    if (!f) return SNN_ERR_NULL;
+    const snn_layer_desc &h = f->hidden, &r = f->readout;
+    snn_status st = check_desc(&h);
+    if (st != SNN_OK) return st;
+    st = check_desc(&r);
+    if (st != SNN_OK) return st;
+    if (h.synapse != SNN_SYN_DENSE || r.synapse != SNN_SYN_DENSE) return SNN_ERR_UNSUPPORTED;
+    if (h.in_dtype != SNN_U8 || r.in_dtype != SNN_U8 || h.w_dtype != SNN_F32 ||
+        r.w_dtype != SNN_F32)
+        return SNN_ERR_DTYPE;
+    auto plain = [](int n) { return n == SNN_LEAKY || n == SNN_SYNAPTIC; };
+    if (!plain(h.neuron) || !plain(r.neuron)) return SNN_ERR_UNSUPPORTED;
+    if (r.n_in != h.n_out || r.T != h.T || r.B != h.B || h.T < 1 || h.B < 1)
+        return SNN_ERR_SHAPE;
+    if (f->loss_kind != SNN_LOSS_CE_COUNT && f->loss_kind != SNN_LOSS_MSE_COUNT)
+        return SNN_ERR_UNSUPPORTED;
+    if (f->pop < 1 || r.n_out % f->pop != 0 || f->reserved != 0) return SNN_ERR_SHAPE;
+    if (r.n_out > kFusedMaxOut) return SNN_ERR_UNSUPPORTED;
+    const FusedPlan p = fused_plan(h.T, h.B, h.n_in, h.n_out, r.n_out);
+    if (!p.ok) return SNN_ERR_UNSUPPORTED;
+    if (plan) *plan = p;
+    return SNN_OK;
+}
+}  // namespace
+
 extern "C" {
 
 int snn_abi_version(void) { return SNN_ABI_VERSION; }
@@ -683,6 +710,52 @@ snn_status snn_loss_noalloc(int32_t kind, int32_t B, int32_t K, int32_t P, const
     (void)hipGetLastError();
     return hip_status(launch_loss(kind, B, K, P, counts, labels, targets, loss, grad_counts,
                                   scratch, stream));
+}
+
+
+snn_status snn_fused_step_check(const snn_fused_desc *d) { return check_fused(d, nullptr); }
+
+size_t snn_fused_step_workspace_bytes(const snn_fused_desc *d) {
+    FusedPlan p{};
+    return check_fused(d, &p) == SNN_OK ? p.ws_bytes : 0;
+}
+
+snn_status snn_fused_step(const snn_fused_desc *d, const uint8_t *x, const float *w0,
+                          const float *b0, const float *w1, const float *b1,
+                          const int32_t *labels, const float *targets, float *loss,
+                          float *counts, uint8_t *spk_hidden, float *grad_w0, float *grad_b0,
+                          float *grad_w1, float *grad_b1, int32_t *status, void *ws,
+                          size_t ws_bytes, hipStream_t stream) {
+    FusedPlan p{};
+    snn_status st = check_fused(d, &p);
+    if (st != SNN_OK) return st;
+    if (!x || !w0 || !w1 || !status) return SNN_ERR_NULL;
+    if (d->loss_kind == SNN_LOSS_CE_COUNT && !labels) return SNN_ERR_NULL;
+    if (d->loss_kind == SNN_LOSS_MSE_COUNT && !targets) return SNN_ERR_NULL;
+    for (const void *q : {(const void *)x, (const void *)w0, (const void *)b0, (const void *)w1,
+                          (const void *)b1, (const void *)labels, (const void *)targets,
+                          (const void *)loss, (const void *)counts, (const void *)spk_hidden,
+                          (const void *)grad_w0,
+                          (const void *)grad_b0, (const void *)grad_w1, (const void *)grad_b1,
+                          (const void *)status, (const void *)ws})
+        if (q && !aligned16(q)) return SNN_ERR_ALIGN;
+    if (!ws || ws_bytes < p.ws_bytes) return SNN_ERR_WORKSPACE;
+    const snn_layer_desc &h = d->hidden, &r = d->readout;
+    FusedStep f{};
+    f.T = h.T; f.B = h.B; f.n_in = h.n_in; f.n_hid = h.n_out; f.n_out = r.n_out; f.P = d->pop;
+    f.neuron0 = h.neuron; f.neuron1 = r.neuron;
+    f.rs0 = h.reset_grad == SNN_RESET_SURROGATE; f.rs1 = r.reset_grad == SNN_RESET_SURROGATE;
+    f.alpha0 = h.alpha; f.beta0 = h.beta; f.thr0 = h.threshold; f.slope0 = h.slope;
+    f.alpha1 = r.alpha; f.beta1 = r.beta; f.thr1 = r.threshold; f.slope1 = r.slope;
+    f.loss_kind = d->loss_kind;
+    f.wait_limit = d->wait_limit;
+    f.x = x; f.W0 = w0; f.b0 = b0; f.W1 = w1; f.b1 = b1;
+    f.labels = labels; f.targets = targets;
+    f.loss = loss; f.counts = counts; f.spk = spk_hidden;
+    f.gW0 = grad_w0; f.gb0 = grad_b0; f.gW1 = grad_w1; f.gb1 = grad_b1;
+    f.status = status;
+    (void)hipGetLastError();
+    return hip_status(launch_fused_step(f, ws, stream));
 }
 
 snn_status snn_adamw(const snn_adamw_tensor *tensors, int32_t count,

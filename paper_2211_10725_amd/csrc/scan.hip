@@ -18,7 +18,7 @@
 // running the chunk backwards.
 #include <atomic>
 
-#include "snn_internal.hpp"
+#include "neuron.hpp"
 
 namespace snn {
 namespace {
@@ -70,25 +70,6 @@ __device__ inline void store_spikes_f16(uint16_t *p, const float (&z)[VEC]) {
     } else {
         p[0] = z[0] != 0.f ? 0x3c00u : 0u;
     }
-}
-
-// One step of the forward recurrence for one column (eqs. 3-7), in the exact
-// fp32 operations both scans use: the decay-plus-input term as one fused
-// multiply-add, then the reset (eq. 7: plus the recurrent weight) if the
-// previous step spiked.  Returns the new membrane; the spike is u > thr.
-template <int NEURON>
-__device__ inline float neuron_step(float &u, float &syn, float zp, float in, float alpha,
-                                    float beta, float jump) {
-    float uu;
-    if constexpr (NEURON == SNN_SYNAPTIC) {
-        syn = __builtin_fmaf(alpha, syn, in);
-        uu = __builtin_fmaf(beta, u, syn);
-    } else {
-        uu = __builtin_fmaf(beta, u, in);
-    }
-    uu = (zp != 0.f) ? uu + jump : uu;
-    u = uu;
-    return uu;
 }
 
 // Forward scan.  Writes the spikes, the spike counts (nullable), the full
@@ -415,8 +396,7 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
 #pragma unroll
                 for (int v = 0; v < VEC; ++v) {
                     const float uu = ii[j][v];
-                    const float e = 1.f + slope * __builtin_fabsf(uu - thr);
-                    const float s = __builtin_amdgcn_rcpf(e * e);  // eq. (9) with slope
+                    const float s = surrogate(uu, thr, slope);
                     float gt;
                     if constexpr (BCAST) {
                         gt = gb[v];
@@ -427,19 +407,14 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
                     } else {
                         gt = gg[j][v];
                     }
-                    float carry = beta;
                     if constexpr (NEURON == SNN_RLEAKY) {
                         if (uu > thr) dv[v] += lam[v];  // lam_{t+1} z_t
-                        carry = __builtin_fmaf(vr[v], s, beta);
-                    } else if constexpr (RESET_SURR) {
-                        carry = beta - thr * s;
-                    }
-                    lam[v] = __builtin_fmaf(carry, lam[v], gt * s);
-                    if constexpr (NEURON == SNN_SYNAPTIC) {
-                        lami[v] = __builtin_fmaf(alpha, lami[v], lam[v]);
-                        d[v] = lami[v];
-                    } else {
+                        const float carry = __builtin_fmaf(vr[v], s, beta);
+                        lam[v] = __builtin_fmaf(carry, lam[v], gt * s);
                         d[v] = lam[v];
+                    } else {
+                        d[v] = adjoint_step<NEURON, RESET_SURR>(lam[v], lami[v], gt, s, alpha,
+                                                                beta, thr);
                     }
                     acc[v] += d[v];
                 }

@@ -215,4 +215,31 @@ hipError_t launch_conv_pool_bwd(const ConvGeom &g, const float *dI, const uint8_
                                 float *grad_w, float *grad_x, void *ws, size_t ws_bytes,
                                 hipStream_t s);
 
+// ---- fused small-batch step (fused.hip) ---------------------------------------
+constexpr int kFusedMaxNpw = 16;                 // hidden neurons per workgroup
+constexpr size_t kFusedMaxLds = 160 * 1024 - 4096;  // dynamic LDS per workgroup
+constexpr int kFusedMaxOut = 16;                 // readout neurons (one MFMA block)
+struct FusedPlan {
+    bool ok;
+    int npw, grid;
+    size_t lds, ws_bytes;
+};
+FusedPlan fused_plan(int T, int B, int n_in, int n_hid, int n_out);
+struct FusedStep {
+    int T, B, n_in, n_hid, n_out, P;
+    int neuron0, neuron1;
+    bool rs0, rs1;
+    float alpha0, beta0, thr0, slope0, alpha1, beta1, thr1, slope1;
+    int loss_kind;
+    unsigned wait_limit;
+    const uint8_t *x;
+    const float *W0, *b0, *W1, *b1;
+    const int32_t *labels;
+    const float *targets;
+    float *loss, *counts, *gW0, *gb0, *gW1, *gb1;
+    uint8_t *spk;
+    int32_t *status;
+};
+hipError_t launch_fused_step(const FusedStep &f, void *ws, hipStream_t s);
+
 }  // namespace snn
