@@ -442,9 +442,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
             for (int q = 0; q < 2; ++q)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[i][q][r] = 0.f;
-        // k-tile t of this item.  The loop runs an even number of tiles; a
-        // tile past the end re-copies the last one and is multiplied fully
-        // masked.
+        // k-tile t of this item.  The loop runs an even number of steps; with
+        // an odd number of tiles the last step only waits at the barrier.
         const int nk2 = (nk + 1) & ~1;
 #define SNN_KTILE(t) (kbeg + kKT * min((t), nk - 1))
         for (int t = 0; t < nk2; t += 2) {
@@ -452,12 +451,13 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
     {                                                                                       \
         const int tt = t + (S);                                                             \
         stage_barrier();                                                                    \
-        multiply<MT, MN, S>(acc, wm, wn, kend - (kbeg + kKT * tt), [&] {                    \
-            if (tt + 1 < nk2) {                                                             \
-                ca.copy(SNN_KTILE(tt + 1), kend, stage_a<NEXT>());                          \
-                cb.copy(SNN_KTILE(tt + 1), kend, stage_b<NEXT>());                          \
-            }                                                                               \
-        });                                                                                 \
+        if (tt < nk)                                                                        \
+            multiply<MT, MN, S>(acc, wm, wn, kend - (kbeg + kKT * tt), [&] {                \
+                if (tt + 1 < nk) {                                                          \
+                    ca.copy(SNN_KTILE(tt + 1), kend, stage_a<NEXT>());                      \
+                    cb.copy(SNN_KTILE(tt + 1), kend, stage_b<NEXT>());                      \
+                }                                                                           \
+            });                                                                             \
     }
             SNN_ASYNC_STEP(0, 1)
             SNN_ASYNC_STEP(1, 0)
