@@ -260,6 +260,54 @@ def _parse_key(key):
     return key.split("[L")[0], int(key.split("[L")[1].rstrip("]"))
 
 
+def fused_bench(args, wl, net, x, y, tgt, stream):
+    """The step as one snn_fused_step launch per step: the kernel is the whole
+    step, so its roofline is the step's contraction flops (hidden currents,
+    readout currents, dW0, as exact three-part bf16 MFMA passes) per launch."""
+    import torch
+    with torch.cuda.stream(stream):
+        for _ in range(args.warmup):
+            net.step_fused(x, labels=y, targets=tgt)
+        torch.cuda.synchronize()
+        marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
+        marks[0].record(stream)
+        for i in range(args.steps):
+            net.step_fused(x, labels=y, targets=tgt)
+            marks[i + 1].record(stream)
+        torch.cuda.synchronize()
+    if int(net.fstatus[0].item()) != 0:
+        print("snn_fused_step gave up at a grid barrier (status 1)", file=sys.stderr)
+        sys.exit(1)
+    total_ms = marks[0].elapsed_time(marks[-1])
+    per_step = sorted(marks[i].elapsed_time(marks[i + 1]) for i in range(args.steps))
+    ms = total_ms / args.steps
+    h, r = net.descs
+    rows = wl.T * wl.B
+    flops = 2.0 * rows * (2 * h.n_in * h.n_out + r.n_in * r.n_out)  # algorithmic
+    out = {
+        "metric": METRIC, "value": round(wl.B * args.steps / (total_ms / 1000.0), 1),
+        "unit": "samples/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "description": wl.description, "T": wl.T,
+                   "batch": wl.B, "layers": [_layer_str(s) for s in wl.layers],
+                   "precision": "fp32 weights, currents, state and gradients; products "
+                                "exact, fp32 accumulation",
+                   "includes": "forward + loss + BPTT backward, no optimizer update",
+                   "launch": "one snn_fused_step kernel per step"},
+        "step_ms": {"median": round(per_step[len(per_step) // 2], 5),
+                    "p10": round(per_step[len(per_step) // 10], 5),
+                    "p90": round(per_step[(9 * len(per_step)) // 10], 5)},
+        "roofline": {"bound": "mfma", "achieved": round(flops / (ms / 1000.0) / 1e12, 3),
+                     "peak": 2500.0, "unit": "TFLOP/s", "peak_basis": "bf16/fp16 dense MFMA",
+                     "mfma_passes": 3,
+                     "frac": round(flops / (ms / 1000.0) / 1e12 / 2500.0, 5),
+                     "traffic": None, "kernel": "fused_step_kernel (the whole step)",
+                     "avg_launch_ms": round(ms, 5), "share_of_step": 1.0},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -279,6 +327,9 @@ def main():
     ap.add_argument("--update", action="store_true",
                     help="end every step with the fused AdamW update (the paper's "
                          "training step); the default step is forward + BPTT")
+    ap.add_argument("--fused", action="store_true",
+                    help="run each step as one snn_fused_step launch (two dense layers on "
+                         "spike input with fp32 weights, small batches)")
     ap.add_argument("--fp32-mfma", action="store_true",
                     help="contract spike x fp32 with fp32 MFMA instead of the exact "
                          "three-pass bf16 split")
@@ -320,6 +371,15 @@ def main():
     if args.mode == "pmc":
         with torch.cuda.stream(stream):
             run_pmc_mode(net, x, y, tgt, max(1, args.steps))
+        return
+
+    if args.fused:
+        if net.fdesc is None or args.graph or upd:
+            print("--fused runs two dense layers on spike input with fp32 weights, small "
+                  "enough for one co-resident grid, without --graph or --update",
+                  file=sys.stderr)
+            sys.exit(2)
+        fused_bench(args, wl, net, x, y, tgt, stream)
         return
 
     with torch.cuda.stream(stream):
