@@ -47,7 +47,7 @@ SCAN_WORKLOAD = "scan_wide_t1000_b64"
 STAGE_SOURCES = {
     "synapse": ["snn_internal.hpp", "gemm.hip", "gemm_mfma16.hip", "gemm_async.hip", "skinny.hip",
                 "conv.hip"],
-    "neuron": ["snn_internal.hpp", "scan.hip"],
+    "neuron": ["snn_internal.hpp", "neuron.hpp", "scan.hip"],
 }
 
 
