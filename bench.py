@@ -657,10 +657,26 @@ def _narrow_contraction(net, li, fp32_mfma):
     return (d.in_dtype == 3 and d.w_dtype in (0, 1)) or (d.in_dtype == 1 and d.w_dtype == 1)
 
 
-def _async_ok(a, b, M, N, K):
-    """Mirrors gemm_async_applies in gemm_async.hip (both operands K-contiguous)."""
+def _async_passes(a, b, M, N, K, mn=False):
+    """Mirrors gemm_async_applies in gemm_async.hip: 0 when the asynchronous
+    256x256 kernel does not take the product, else its MFMA passes (3 for
+    spikes against an fp32 operand held as three bf16 planes).  mn: both
+    operands M/N-contiguous."""
+    if K % 8 or K < 256 or M < 256 or N < 256 or (mn and (M % 8 or N % 8)):
+        return 0
+    if (a, b) in ((0, 3), (3, 0)):
+        tiles = -(-M // 256) * -(-N // 256)
+        nk = -(-K // 64)
+        S = max(1, min(256 // tiles, 3 * nk // 16, 64)) if tiles < 256 else 1
+        k_chunk = -(-nk // S) * 64
+        splits = -(-K // k_chunk)
+        return 3 if tiles * splits >= 192 and M * N * K >= 2 ** 32 else 0
     ok_type = (a in (3, 1) and b in (3, 1)) or (a in (3, 2) and b in (3, 2))
-    return ok_type and K % 8 == 0 and K >= 256 and M >= 256 and N >= 256 and M * N * K >= 2 ** 30
+    return 1 if ok_type and M * N * K >= 2 ** 30 else 0
+
+
+def _async_ok(a, b, M, N, K, mn=False):
+    return _async_passes(a, b, M, N, K, mn) > 0
 
 
 def _async_contraction(net, li, fp32_mfma):
@@ -689,16 +705,24 @@ def _stage_kernels(net, name, li, fp32_mfma):
         if name == "synapse_bwd_dw":
             if d.n_out <= 16:
                 return ": few_rows_mfma_kernel / few_rows_kernel + splitk_reduce_kernel"
+            # mirrors dw_plan in api.hip
+            sfx = f" ({passes} pass{'es' if passes > 1 else ''}, + splitk_reduce_kernel when split over K)"
+            if (not fp32_mfma and d.synapse == 0 and
+                    _async_ok(d.grad_dtype, d.in_dtype, d.n_out, d.n_in, M, mn=True)):
+                what = ("dL/dI (the 3 bf16 planes the reverse scan writes)" if d.grad_dtype == 0
+                        else "dL/dI")
+                widen = "widen_kernel (x to 16 bits) + " if d.in_dtype == 3 else ""
+                return (f": {widen}gemm_async_kernel reading {what} and x in their own "
+                        f"layouts{sfx}")
             big = 2.0 * M * d.n_in * d.n_out >= 2 ** 30
             trans = big and not (d.grad_dtype == 0 and d.in_dtype == 3 and M <= 8192)
-            gemm = ("gemm_async_kernel" if trans and passes == 1 and
+            gemm = ("gemm_async_kernel" if trans and
                     _async_ok(d.grad_dtype, d.in_dtype, d.n_out, d.n_in, M) else
                     "gemm16_kernel" if kind == "mfma16" else "gemm_f32_kernel")
             pre = ("transpose_kernel (dL/dI^T" + (" as 3 bf16 planes" if d.grad_dtype == 0
                                                   else "") + ") + transpose_u8_kernel (x^T) + "
                    if trans else "")
-            return f": {pre}{gemm} ({passes} pass{'es' if passes > 1 else ''}, " \
-                   "+ splitk_reduce_kernel when split over K)"
+            return f": {pre}{gemm}{sfx}"
         big = 2.0 * M * d.n_in * K >= 2 ** 30
         gemm = ("gemm_async_kernel" if big and passes == 1 and
                 _async_ok(d.grad_dtype, d.w_dtype, M, d.n_in, K) else
@@ -710,6 +734,9 @@ def _stage_kernels(net, name, li, fp32_mfma):
         return ": unpool_t_kernel + im2col_t_kernel + contractions + col2im_kernel " \
                "(conv weight and input gradients)"
     if name == "synapse_fwd" and _async_contraction(net, li, fp32_mfma):
+        if d.w_dtype == 0:
+            return (": widen_kernel (spikes to bf16) + split_planes_kernel (weights as 3 bf16 "
+                    "planes) + gemm_async_kernel (3 passes)")
         widen = " widen_kernel (spikes to fp16) +" if d.in_dtype == 3 else ""
         return f":{widen} gemm_async_kernel"
     if name == "synapse_fwd" and _narrow_contraction(net, li, fp32_mfma):

@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 8
+#define SNN_ABI_VERSION 9
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -396,11 +396,14 @@ snn_status snn_neuron_fwd(const snn_layer_desc *d, const float *cur, const float
  * (SNN_ERR_UNSUPPORTED).  Ignored (may be NULL) for the other dtypes.
  * dcur_t (nullable, dense layers only, snn_layer_dcur_t_bytes(d) bytes): the
  * same dL/dI written as the weight gradient's operand, so that
- * snn_synapse_bwd needs no transpose: 16-bit [P][n_out][B*T], row n holding
- * neuron n of every sample, column b*T + t (sample-major), P = 3 exact bf16
- * parts (hi, mid, lo: hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi -
- * mid)) for SNN_F32, else 1 plane of d->grad_dtype (fp16 scaled as dcur).
- * dcur may be NULL when dcur_t is given. */
+ * snn_synapse_bwd needs no transpose or split, in the layout
+ * snn_layer_dcur_t_layout(d) names: SNN_DCUR_T_TRANSPOSED, 16-bit
+ * [P][n_out][B*T], row n holding neuron n of every sample, column b*T + t
+ * (sample-major), P = 3 exact bf16 parts (hi, mid, lo: hi = bf16(x), mid =
+ * bf16(x - hi), lo = bf16(x - hi - mid)) for SNN_F32, else 1 plane of
+ * d->grad_dtype (fp16 scaled as dcur); SNN_DCUR_T_PLANES, the same three
+ * parts of an fp32 dL/dI as [3][T*B][n_out].  dcur may be NULL when dcur_t
+ * is given. */
 snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const float *v,
                           const float *cur, const float *ckpt, void *dcur, void *dcur_t,
                           float *dcur_scale, float *grad_b, float *grad_v, void *ws,
@@ -408,8 +411,8 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
 
 /* Synapse backward from dcur (of d->grad_dtype): grad_w and/or grad_x
  * (dW = dI^T x and dx = dI W, BPTT through the w x_t term of eqs. (4)/(5)).
- * dcur_t (nullable): the transposed operand snn_neuron_bwd wrote; the weight
- * gradient contracts it instead of transposing dcur (used when
+ * dcur_t (nullable): the operand snn_neuron_bwd wrote; the weight gradient
+ * contracts it instead of transposing or splitting dcur (used when
  * snn_layer_dcur_t_bytes(d) > 0).  dcur may then be NULL unless grad_x is
  * requested.  dcur_scale: for SNN_F16, the scale snn_neuron_bwd wrote
  * (required); the contractions divide it out.  Ignored for the other
@@ -425,6 +428,20 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const void
  * products of a 16-bit dL/dI, which read dL/dI and x in their own
  * layouts). */
 size_t snn_layer_dcur_t_bytes(const snn_layer_desc *d);
+
+/* Layout of the dcur_t operand snn_neuron_bwd writes for this layer (-1 for
+ * an invalid descriptor):
+ * SNN_DCUR_T_TRANSPOSED: 16-bit [P][n_out][B*T] as described at
+ *   snn_neuron_bwd (P = 3 exact bf16 parts for SNN_F32, else 1);
+ * SNN_DCUR_T_PLANES: an fp32 dL/dI as its three exact bf16 parts (hi, mid,
+ *   lo, as above) in dL/dI's own layout, [3][T*B][n_out], for a weight
+ *   gradient that reads dL/dI untransposed (large dense fp32 layers whose
+ *   n_out and n_in are multiples of 8).  snn_layer_bwd has the scan write
+ *   these planes in place of the fp32 dL/dI when the layer has no input
+ *   gradient to compute. */
+#define SNN_DCUR_T_TRANSPOSED 1
+#define SNN_DCUR_T_PLANES 2
+int32_t snn_layer_dcur_t_layout(const snn_layer_desc *d);
 
 #ifdef __cplusplus
 }

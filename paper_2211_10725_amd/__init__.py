@@ -31,7 +31,8 @@ RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST, GRAD_FOLD = 0, 1, 2
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 8
+ABI_VERSION = 9
+DCUR_T_TRANSPOSED, DCUR_T_PLANES = 1, 2
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
           4: "SNN_ERR_ALIGN", 5: "SNN_ERR_UNSUPPORTED", 6: "SNN_ERR_WORKSPACE",
@@ -41,8 +42,8 @@ EXPORTS = ["snn_abi_version", "snn_status_str", "snn_layer_saved_bytes",
            "snn_layer_workspace_bytes", "snn_layer_fwd", "snn_layer_bwd",
            "snn_loss_workspace_bytes", "snn_loss", "snn_synapse_fwd", "snn_neuron_fwd",
            "snn_neuron_bwd", "snn_synapse_bwd", "snn_adamw", "snn_loss_noalloc",
-           "snn_layer_saved_layout", "snn_layer_dcur_t_bytes", "snn_fused_step_check",
-           "snn_fused_step_workspace_bytes", "snn_fused_step"]
+           "snn_layer_saved_layout", "snn_layer_dcur_t_bytes", "snn_layer_dcur_t_layout",
+           "snn_fused_step_check", "snn_fused_step_workspace_bytes", "snn_fused_step"]
 
 
 class LayerDesc(ctypes.Structure):
@@ -133,6 +134,7 @@ def lib():
         "snn_neuron_bwd": ([D, G, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_synapse_bwd": ([D, P, P, P, P, P, P, P, P, P, S, P], ctypes.c_int),
         "snn_layer_dcur_t_bytes": ([D], S),
+        "snn_layer_dcur_t_layout": ([D], i32),
         "snn_fused_step_check": ([ctypes.POINTER(FusedDesc)], ctypes.c_int),
         "snn_fused_step_workspace_bytes": ([ctypes.POINTER(FusedDesc)], S),
         "snn_fused_step": ([ctypes.POINTER(FusedDesc)] + [P] * 16 + [S, P], ctypes.c_int),
@@ -254,6 +256,12 @@ def ckpt_buffer(desc: LayerDesc, device="cuda"):
 
 def snn_layer_dcur_t_bytes(desc: LayerDesc) -> int:
     return int(lib().snn_layer_dcur_t_bytes(ctypes.byref(desc)))
+
+
+def snn_layer_dcur_t_layout(desc: LayerDesc) -> int:
+    """DCUR_T_TRANSPOSED or DCUR_T_PLANES: the layout of the dcur_t operand
+    snn_neuron_bwd writes for this layer."""
+    return int(lib().snn_layer_dcur_t_layout(ctypes.byref(desc)))
 
 
 def snn_layer_workspace_bytes(desc: LayerDesc) -> int:
@@ -536,6 +544,7 @@ class Network:
         # the reverse scan's transposed dL/dI for the weight gradient (stage
         # calls; the layer calls keep it in the workspace)
         self.dcur_t_bytes = [snn_layer_dcur_t_bytes(d) for d in self.descs]
+        self.dcur_t_layout = [snn_layer_dcur_t_layout(d) for d in self.descs]
         self.transposed_operand = False
         self.dcur_t = torch.empty(max(self.dcur_t_bytes + [256]), dtype=u8, device=device)
         # The whole step as one cooperative launch (step_fused): two dense
@@ -712,11 +721,14 @@ class Network:
                     dcur = dcur.view(torch.float32)
                 rest = self.ws[(dcur_bytes + 255) // 256 * 256:]
             sc = self.scale[li]
-            # the weight gradient's operand written transposed by the scan
-            # (transposed_operand=True); the row-major dL/dI only where the
-            # input gradient needs it.  Off by default: it measured slower
-            # than one transpose (as in the layer call).
-            dt = self.dcur_t if self.transposed_operand and self.dcur_t_bytes[li] > 0 and \
+            # the weight gradient's operand written by the scan: transposed
+            # (transposed_operand=True; off by default, it measured slower
+            # than one transpose, as in the layer call), or the three bf16
+            # planes of an fp32 dL/dI in its own layout (always, as in the
+            # layer call); the row-major dL/dI only where the input gradient
+            # needs it.
+            use_t = self.transposed_operand or self.dcur_t_layout[li] == DCUR_T_PLANES
+            dt = self.dcur_t if use_t and self.dcur_t_bytes[li] > 0 and \
                 self.dup[li] is None else None
             rm = dcur if dt is None or self.gx[li] is not None or self.dup[li] is not None \
                 else None

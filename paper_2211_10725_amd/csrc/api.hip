@@ -167,6 +167,7 @@ constexpr double kTransposeFlops = 1073741824.0;  // 2 M N K above which it pays
 
 struct DwPlan {
     bool transposed;
+    bool planes;       // fp32 dI as three bf16 planes in its own layout (asynchronous kernel)
     int a_dtype;       // dtype of the transposed dI operand
     size_t dit_bytes;  // dI^T (planes for fp32)
     size_t xt_bytes;   // x^T
@@ -200,6 +201,7 @@ DwPlan dw_plan(const snn_layer_desc *d) {
     mn.b_dtype = d->in_dtype; mn.b_kc = false; mn.ldb = d->n_in;
     mn.allow_split = split_ok(d);
     const bool async_mn = gemm_async_applies(mn);
+    p.planes = async_mn && d->grad_dtype == SNN_F32;
     p.transposed = split_ok(d) && gemm16_applies(kc) && d->n_out > 16 && !mn_direct && !async_mn &&
                    2.0 * M * d->n_in * d->n_out >= kTransposeFlops;
     if (p.transposed) {
@@ -214,13 +216,21 @@ DwPlan dw_plan(const snn_layer_desc *d) {
     return p;
 }
 
-// bytes of the transposed dL/dI operand of the weight gradient ([planes][n_out]
-// [T*B] 16-bit), 0 when the layer's weight gradient does not contract it
+// bytes of the weight gradient's dL/dI operand as the reverse scan can write
+// it: transposed ([planes][n_out][T*B] 16-bit) or, for an fp32 dL/dI read in
+// its own layout, its three bf16 planes [3][T*B][n_out]; 0 when the layer's
+// weight gradient contracts neither
 size_t dcur_t_bytes(const snn_layer_desc *d) {
     if (d->synapse != SNN_SYN_DENSE || rows(d) == 0) return 0;
     const DwPlan p = dw_plan(d);
+    if (p.planes) return align_up((size_t)3 * rows(d) * d->n_out * sizeof(uint16_t));
     return p.transposed ? p.dit_bytes : 0;
 }
+bool dcur_t_planes(const snn_layer_desc *d) {
+    return d->synapse == SNN_SYN_DENSE && rows(d) > 0 && dw_plan(d).planes;
+}
+// the layer call has the reverse scan write the planes (in its workspace)
+size_t layer_planes_bytes(const snn_layer_desc *d) { return dcur_t_planes(d) ? dcur_t_bytes(d) : 0; }
 
 struct DxPlan {
     bool transposed;
@@ -260,7 +270,8 @@ size_t bwd_gemm_ws(const snn_layer_desc *d) {
     return dw > dx ? dw : dx;
 }
 size_t bwd_ws(const snn_layer_desc *d) {
-    return dcur_bytes(d) + neuron_ws(d) + scale_slot_bytes(d) + bwd_gemm_ws(d);
+    return dcur_bytes(d) + neuron_ws(d) + scale_slot_bytes(d) + layer_planes_bytes(d) +
+           bwd_gemm_ws(d);
 }
 
 snn_status hip_status(hipError_t e) { return e == hipSuccess ? SNN_OK : SNN_ERR_HIP; }
@@ -367,6 +378,11 @@ size_t snn_layer_saved_bytes(const snn_layer_desc *d) {
 size_t snn_layer_dcur_t_bytes(const snn_layer_desc *d) {
     if (check_desc(d) != SNN_OK) return 0;
     return dcur_t_bytes(d);
+}
+
+int32_t snn_layer_dcur_t_layout(const snn_layer_desc *d) {
+    if (check_desc(d) != SNN_OK) return -1;
+    return dcur_t_planes(d) ? SNN_DCUR_T_PLANES : SNN_DCUR_T_TRANSPOSED;
 }
 
 snn_status snn_layer_saved_layout(const snn_layer_desc *d, snn_saved_layout *out) {
@@ -495,7 +511,7 @@ snn_status snn_neuron_bwd(const snn_layer_desc *d, const snn_grad_in *grad, cons
     }
     e = launch_neuron_bwd(d->neuron, d->reset_grad, d->T, C, d->n_out, d->alpha, d->beta,
                           d->threshold, d->slope, v, cur, ckpt, bg, d->B, dcur, dcur_t,
-                          d->grad_dtype, dcur_scale, colsum, dvcol, stream);
+                          dcur_t_planes(d), d->grad_dtype, dcur_scale, colsum, dvcol, stream);
     if (e != hipSuccess) return SNN_ERR_HIP;
     if (grad_b) {
         int F = d->n_out, P = 1;
@@ -579,8 +595,15 @@ snn_status snn_synapse_bwd(const snn_layer_desc *d, const void *dcur, const void
             g.B = xt; g.ldb = M; g.b_dtype = d->in_dtype; g.b_kc = true;
             e = launch_gemm(g, xt + pl.xt_bytes, ws_bytes - pl.dit_bytes - pl.xt_bytes, stream);
         } else {
-            // both operands stored with the output index contiguous
+            // both operands stored with the output index contiguous; an fp32
+            // dI as the three bf16 planes the reverse scan wrote, else split
+            // into planes in the workspace
             g.A = dcur; g.lda = d->n_out; g.a_dtype = d->grad_dtype; g.a_kc = false;
+            if (use_t && pl.planes) {
+                g.A = dcur_t;
+                g.a_dtype = kPlanes3;
+                g.a_ps = (int64_t)M * d->n_out;
+            }
             g.B = x; g.ldb = d->n_in; g.b_dtype = d->in_dtype; g.b_kc = false;
             e = launch_gemm(g, ws, ws_bytes, stream);
         }
@@ -664,14 +687,22 @@ snn_status snn_layer_bwd(const snn_layer_desc *d, const snn_grad_in *grad, const
     void *dcur = base;
     char *colsum = base + dcur_bytes(d);
     float *scale = scaled_grad(d) ? reinterpret_cast<float *>(colsum + neuron_ws(d)) : nullptr;
-    char *gws = colsum + neuron_ws(d) + scale_slot_bytes(d);
+    char *planes = colsum + neuron_ws(d) + scale_slot_bytes(d);
+    char *gws = planes + layer_planes_bytes(d);
     // Where the weight gradient takes a transposed operand (fp32 dL/dI as
     // three bf16 parts), the reverse scan could write it itself (dcur_t), but
     // its rows are written in runs of one chunk (16 steps, 32 bytes) per
     // lane, which measured slower than the row-major write plus one
-    // transpose, so the layer call keeps the transpose.
+    // transpose, so the layer call keeps the transpose.  Where it takes an
+    // fp32 dL/dI in its own layout, the scan writes the three bf16 planes
+    // (coalesced like dL/dI itself) instead of the fp32 values, which only
+    // the input gradient still needs.
     void *dcur_t = nullptr;
     void *dcur_rm = dcur;
+    if (grad_w && layer_planes_bytes(d) > 0) {
+        dcur_t = planes;
+        if (!grad_x) dcur_rm = nullptr;
+    }
     st = snn_neuron_bwd(d, grad, v, cur, ckpt, dcur_rm, dcur_t, scale, grad_b, grad_v, colsum,
                         neuron_ws(d), stream);
     if (st != SNN_OK) return st;

@@ -3,10 +3,15 @@
 //
 //   C[M,N] = sum_k A[m][k] B[n][k] (+ bias[n]),  fp32 accumulate,
 //
-// A and B 16-bit values of the MFMA type (fp16, or bf16), both K-contiguous.
-// Spike operands (bytes, exact in either type) are first widened into the
-// workspace.  Used for the big products of the half-precision network, where
-// every product is one MFMA pass.
+// A and B 16-bit values of the MFMA type (fp16, or bf16), both K-contiguous
+// or both M/N-contiguous.  Spike operands (bytes, exact in either type) are
+// first widened into the workspace.  Used for the big products of the
+// half-precision network, where every product is one MFMA pass, and for the
+// big products of spikes with an fp32 operand: that operand is held as three
+// exact bf16 planes (hi, mid, lo; split into the workspace if given as fp32),
+// and an item's k loop runs over the planes one after the other, the smallest
+// first, each against the same spike tiles, accumulating in fp32 (three
+// passes, every product exact).
 //
 // Tile 256 x 256 per workgroup of 8 wave64s (2 along M x 4 along N), 128 x 64
 // per wave with v_mfma_f32_32x32x16_{f16,bf16}: two waves per SIMD, so one
@@ -93,12 +98,13 @@ struct TileCopyKC {
             row[j] = X + (int64_t)min(r0 + r, rows - 1) * ld;
         }
     }
-    __device__ inline void copy(int k0, int K, uint16_t *stage) const {
+    // off: element offset of the plane to copy from (0 for a one-part operand)
+    __device__ inline void copy(int k0, int K, uint16_t *stage, int64_t off) const {
         const int w = threadIdx.x >> 6;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int k = k0 + c8[j];
-            __builtin_amdgcn_global_load_lds(row[j] + (k < K ? k : 0),
+            __builtin_amdgcn_global_load_lds(row[j] + off + (k < K ? k : 0),
                                              (lds_void *)(stage + (4 * w + j) * 512), 16, 0, 0);
         }
     }
@@ -129,12 +135,12 @@ struct TileCopyMN {
         for (int jj = 0; jj < 2; ++jj)
             col[jj] = min(r0 + 8 * ((lane & 31) ^ mn_swz(kr0 + 2 * jj)), rows - 8);
     }
-    __device__ inline void copy(int k0, int K, uint16_t *stage) const {
+    __device__ inline void copy(int k0, int K, uint16_t *stage, int64_t off) const {
         const int w = threadIdx.x >> 6;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int k = min(k0 + kr0 + 2 * j, K - 1);
-            __builtin_amdgcn_global_load_lds(X + (int64_t)k * ld + col[j & 1],
+            __builtin_amdgcn_global_load_lds(X + off + (int64_t)k * ld + col[j & 1],
                                              (lds_void *)(stage + (4 * w + j) * 512), 16, 0, 0);
         }
     }
@@ -405,13 +411,15 @@ __device__ inline int persistent_item(int w, int G, int total, int j) {
 // The first k-tile of a workgroup's next item is copied into stage 0 before
 // the current item's results are stored (through stage 1) (stage 0 was last read before the
 // barrier of the current item's final k-tile), so that latency overlaps the
-// stores.
-template <int MT, bool MN>
+// stores.  P = 3: one operand is three bf16 planes (a_ps / b_ps elements
+// apart, the other's stride 0); step v = p nk + kk of an item multiplies
+// k-tile kk of plane 2 - p (lo, then mid, then hi).
+template <int MT, bool MN, int P>
 __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
     int M, int N, int K, int k_chunk, int tiles_n, int tiles, int total,
     const uint16_t *__restrict__ A, int64_t lda, const uint16_t *__restrict__ B, int64_t ldb,
     float *__restrict__ C, int64_t ldc, int64_t split_stride, const float *__restrict__ bias,
-    const float *__restrict__ c_div) {
+    const float *__restrict__ c_div, int64_t a_ps, int64_t b_ps) {
     const int wave = threadIdx.x >> 6, wm = wave & 1, wn = wave >> 1;
     const int lane = threadIdx.x & 63;
     const float inv = c_div ? 1.f / c_div[0] : 1.f;
@@ -438,10 +446,12 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
         ca.init(A, lda, M, m0);
         cb.init(B, ldb, N, n0);
     };
+    // plane offsets of the first step (part 0: the last plane)
+    const int64_t a_off0 = (P - 1) * a_ps, b_off0 = (P - 1) * b_ps;
     int m0, n0, zk, kbeg, kend, nk;
     setup(item, m0, n0, zk, kbeg, kend, nk);
-    ca.copy(kbeg, kend, stage_a<0>());
-    cb.copy(kbeg, kend, stage_b<0>());
+    ca.copy(kbeg, kend, stage_a<0>(), a_off0);
+    cb.copy(kbeg, kend, stage_b<0>(), b_off0);
     for (int j = 0; item >= 0; ++j) {
         floatx16 acc[4][2];
 #pragma unroll
@@ -450,28 +460,43 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
             for (int q = 0; q < 2; ++q)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) acc[i][q][r] = 0.f;
-        // k-tile t of this item.  The loop runs an even number of steps; with
-        // an odd number of tiles the last step only waits at the barrier.
-        const int nk2 = (nk + 1) & ~1;
-#define SNN_KTILE(t) (kbeg + kKT * min((t), nk - 1))
-        for (int t = 0; t < nk2; t += 2) {
+        // Step tt of this item: part cp, k-tile ck (P = 1: k-tile tt).  The
+        // loop runs an even number of steps; with an odd number of steps the
+        // last one only waits at the barrier.
+        const int nv = P * nk, nv2 = (nv + 1) & ~1;
+        int cp = 0, ck = 0;
+        for (int t = 0; t < nv2; t += 2) {
 #define SNN_ASYNC_STEP(S, NEXT)                                                             \
     {                                                                                       \
         const int tt = t + (S);                                                             \
         stage_barrier();                                                                    \
-        if (tt < nk)                                                                        \
-            multiply<MT, MN, S>(acc, wm, wn, kend - (kbeg + kKT * tt), [&] {                \
-                if (tt + 1 < nk) {                                                          \
-                    ca.copy(SNN_KTILE(tt + 1), kend, stage_a<NEXT>());                      \
-                    cb.copy(SNN_KTILE(tt + 1), kend, stage_b<NEXT>());                      \
+        if (tt < nv) {                                                                      \
+            int np = 0, nkk = tt + 1, kc = tt;                                              \
+            if constexpr (P > 1) {                                                          \
+                kc = ck;                                                                    \
+                np = cp;                                                                    \
+                nkk = ck + 1;                                                               \
+                if (nkk == nk) {                                                            \
+                    nkk = 0;                                                                \
+                    ++np;                                                                   \
+                }                                                                           \
+            }                                                                               \
+            multiply<MT, MN, S>(acc, wm, wn, kend - (kbeg + kKT * kc), [&] {                \
+                if (tt + 1 < nv) {                                                          \
+                    ca.copy(kbeg + kKT * nkk, kend, stage_a<NEXT>(), (P - 1 - np) * a_ps);  \
+                    cb.copy(kbeg + kKT * nkk, kend, stage_b<NEXT>(), (P - 1 - np) * b_ps);  \
                 }                                                                           \
             });                                                                             \
+            if constexpr (P > 1) {                                                          \
+                cp = np;                                                                    \
+                ck = nkk;                                                                   \
+            }                                                                               \
+        }                                                                                   \
     }
             SNN_ASYNC_STEP(0, 1)
             SNN_ASYNC_STEP(1, 0)
 #undef SNN_ASYNC_STEP
         }
-#undef SNN_KTILE
         // This tile's bias values, loaded before the copies below.  The
         // copies are issued on every path (after the last item they copy its
         // first k-tile again, into the free stage 0), so the wait for the
@@ -484,8 +509,8 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
         // the next item's first k-tile, in flight during the stores below
         item = persistent_item(blockIdx.x, gridDim.x, total, j + 1);
         if (item >= 0) setup(item, m0, n0, zk, kbeg, kend, nk);
-        ca.copy(kbeg, kend, stage_a<0>());
-        cb.copy(kbeg, kend, stage_b<0>());
+        ca.copy(kbeg, kend, stage_a<0>(), a_off0);
+        cb.copy(kbeg, kend, stage_b<0>(), b_off0);
         float *Cz = C + (int64_t)zkc * split_stride;
         if (wide_stores)
             store_tile_lds(acc, Cz, ldc, M, N, m0c, n0c, wm, wn, inv, bn);
@@ -519,10 +544,16 @@ __global__ __launch_bounds__(kThreads) void widen_kernel(int64_t rows, int K, co
 
 unsigned blocks(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 
-// MFMA type of an operand pair, or -1: fp16 for spikes/fp16, bf16 for spikes/bf16.
+// bf16 planes of an operand: an fp32 array (split into the workspace) or
+// one already split into three planes
+bool planar(int t) { return t == SNN_F32 || t == kPlanes3; }
+
+// MFMA type of an operand pair, or -1: fp16 for spikes/fp16, bf16 for
+// spikes/bf16 and for spikes against three bf16 planes.
 int mfma_type(int a, int b) {
     auto f16ish = [](int t) { return t == SNN_U8 || t == SNN_F16; };
     auto bf16ish = [](int t) { return t == SNN_U8 || t == SNN_BF16; };
+    if ((planar(a) && b == SNN_U8) || (a == SNN_U8 && planar(b))) return MT_BF16;
     if (a == SNN_U8 && b == SNN_U8) return MT_F16;
     if (f16ish(a) && f16ish(b)) return MT_F16;
     if (bf16ish(a) && bf16ish(b)) return MT_BF16;
@@ -530,25 +561,36 @@ int mfma_type(int a, int b) {
 }
 
 struct AsyncPlan {
-    int tiles_m, tiles_n, splits, k_chunk;
-    size_t a_bytes, b_bytes;  // widened spike operands
+    int tiles_m, tiles_n, splits, k_chunk, parts;
+    size_t a_bytes, b_bytes;  // widened spike operands, or the planes of an fp32 operand
     size_t part_bytes;        // split-K partial sums
 };
+
+// 16-bit elements per plane row of an fp32 operand split in its own layout
+// ([rows][K] K-contiguous, [K][rows] M/N-contiguous): rows start on 16 bytes
+int64_t plane_ld(const GemmArgs &g, int rows) { return g.a_kc ? (g.K + 7) / 8 * 8 : (rows + 7) / 8 * 8; }
+int64_t plane_rows(const GemmArgs &g, int rows) { return g.a_kc ? rows : g.K; }
 
 AsyncPlan plan_async(const GemmArgs &g) {
     AsyncPlan p{};
     p.tiles_m = (g.M + kTile - 1) / kTile;
     p.tiles_n = (g.N + kTile - 1) / kTile;
+    p.parts = planar(g.a_dtype) || planar(g.b_dtype) ? 3 : 1;
     const int tiles = p.tiles_m * p.tiles_n;
     const int nk = (g.K + kKT - 1) / kKT;
     int S = 1;
     const int cus = 256;  // one workgroup per CU; MI355X has 256 CUs
-    if (tiles < cus) S = max(1, min(min(cus / tiles, nk / 16), 64));
+    if (tiles < cus) S = max(1, min(min(cus / tiles, p.parts * nk / 16), 64));
     const int per = (nk + S - 1) / S;
     p.k_chunk = per * kKT;
     p.splits = (g.K + p.k_chunk - 1) / p.k_chunk;
-    p.a_bytes = g.a_dtype == SNN_U8 ? align_up((size_t)g.M * g.K * 2) : 0;
-    p.b_bytes = g.b_dtype == SNN_U8 ? align_up((size_t)g.N * g.K * 2) : 0;
+    auto operand = [&](int t, int rows) -> size_t {
+        if (t == SNN_U8) return align_up((size_t)rows * g.K * 2);
+        if (t == SNN_F32) return align_up((size_t)3 * plane_rows(g, rows) * plane_ld(g, rows) * 2);
+        return 0;
+    };
+    p.a_bytes = operand(g.a_dtype, g.M);
+    p.b_bytes = operand(g.b_dtype, g.N);
     p.part_bytes = p.splits > 1 ? align_up((size_t)p.splits * g.M * g.N * sizeof(float)) : 0;
     return p;
 }
@@ -561,8 +603,18 @@ bool gemm_async_applies(const GemmArgs &g) {
     if (mfma_type(g.a_dtype, g.b_dtype) < 0) return false;
     if (g.K % 8 != 0 || g.K < 256 || g.M < kTile || g.N < kTile) return false;
     if (!g.a_kc && (g.M % 8 != 0 || g.N % 8 != 0)) return false;
-    if (g.a_dtype != SNN_U8 && g.lda % 8 != 0) return false;
-    if (g.b_dtype != SNN_U8 && g.ldb % 8 != 0) return false;
+    if (g.a_dtype != SNN_U8 && g.a_dtype != SNN_F32 && g.lda % 8 != 0) return false;
+    if (g.b_dtype != SNN_U8 && g.b_dtype != SNN_F32 && g.ldb % 8 != 0) return false;
+    if (g.a_dtype == kPlanes3 && g.a_ps % 8 != 0) return false;
+    if (g.b_dtype == kPlanes3 && g.b_ps % 8 != 0) return false;
+    if (planar(g.a_dtype) || planar(g.b_dtype)) {
+        // three passes: the pooling epilogue of a convolution stays with the
+        // kernels that have it; enough 256 x 256 tiles to fill the device
+        if (g.pool_hw > 0 || g.c_div) return false;
+        const AsyncPlan p = plan_async(g);
+        if (p.tiles_m * p.tiles_n * p.splits < 192) return false;
+        return (double)g.M * g.N * g.K >= 4294967296.0;
+    }
     // large enough to fill the device with 256 x 256 tiles (K split as needed)
     return (double)g.M * g.N * g.K >= 1073741824.0;
 }
@@ -582,7 +634,8 @@ hipError_t launch_gemm_async(const GemmArgs &g, void *ws, size_t ws_bytes, hipSt
     char *w = reinterpret_cast<char *>(ws);
     const uint16_t *A = reinterpret_cast<const uint16_t *>(g.A);
     const uint16_t *B = reinterpret_cast<const uint16_t *>(g.B);
-    int64_t lda = g.lda, ldb = g.ldb;
+    int64_t lda = g.lda, ldb = g.ldb, a_ps = g.a_dtype == kPlanes3 ? g.a_ps : 0,
+            b_ps = g.b_dtype == kPlanes3 ? g.b_ps : 0;
     const bool mn = !g.a_kc;
     // a spike operand widened in its own layout: [rows][K] or [K][rows]
     auto widen = [&](const void *src, int64_t ld, int rows, uint16_t *d) {
@@ -594,18 +647,26 @@ hipError_t launch_gemm_async(const GemmArgs &g, void *ws, size_t ws_bytes, hipSt
             widen_kernel<MT_BF16><<<blocks(n), kThreads, 0, s>>>(r, c, reinterpret_cast<const uint8_t *>(src), ld, d);
         return (int64_t)c;
     };
+    // an fp32 operand split into three bf16 planes in its own layout
+    auto split = [&](const void *src, int64_t ld, int rows, uint16_t *d, int64_t &ps) {
+        const int64_t pr = plane_rows(g, rows), pl = plane_ld(g, rows);
+        ps = pr * pl;
+        return launch_split_planes(reinterpret_cast<const float *>(src), ld, (int)pr,
+                                   mn ? rows : g.K, (int)pl, d, s) == hipSuccess ? pl : (int64_t)-1;
+    };
     if (p.a_bytes) {
         uint16_t *d = reinterpret_cast<uint16_t *>(w);
-        lda = widen(g.A, g.lda, g.M, d);
+        lda = g.a_dtype == SNN_F32 ? split(g.A, g.lda, g.M, d, a_ps) : widen(g.A, g.lda, g.M, d);
         A = d;
     }
     if (p.b_bytes) {
         uint16_t *d = reinterpret_cast<uint16_t *>(w + p.a_bytes);
-        ldb = widen(g.B, g.ldb, g.N, d);
+        ldb = g.b_dtype == SNN_F32 ? split(g.B, g.ldb, g.N, d, b_ps) : widen(g.B, g.ldb, g.N, d);
         B = d;
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (lda < 0 || ldb < 0) return hipErrorInvalidValue;
     float *out = g.C;
     int64_t ldo = g.ldc, ss = 0;
     const float *bias = g.bias, *c_div = g.c_div;
@@ -619,10 +680,15 @@ hipError_t launch_gemm_async(const GemmArgs &g, void *ws, size_t ws_bytes, hipSt
     const int tiles = p.tiles_m * p.tiles_n, total = tiles * p.splits;
     // one persistent workgroup per compute unit (128 KiB of LDS each)
     const unsigned grid = (unsigned)min(total, device_cus());
-    auto kernel = mt == MT_F16 ? (mn ? gemm_async_kernel<MT_F16, true> : gemm_async_kernel<MT_F16, false>)
-                               : (mn ? gemm_async_kernel<MT_BF16, true> : gemm_async_kernel<MT_BF16, false>);
+    decltype(&gemm_async_kernel<MT_F16, false, 1>) kernel;
+    if (p.parts == 3)
+        kernel = mn ? gemm_async_kernel<MT_BF16, true, 3> : gemm_async_kernel<MT_BF16, false, 3>;
+    else if (mt == MT_F16)
+        kernel = mn ? gemm_async_kernel<MT_F16, true, 1> : gemm_async_kernel<MT_F16, false, 1>;
+    else
+        kernel = mn ? gemm_async_kernel<MT_BF16, true, 1> : gemm_async_kernel<MT_BF16, false, 1>;
     kernel<<<grid, kThreads, 0, s>>>(g.M, g.N, g.K, p.k_chunk, p.tiles_n, tiles, total, A, lda, B,
-                                     ldb, out, ldo, ss, bias, c_div);
+                                     ldb, out, ldo, ss, bias, c_div, a_ps, b_ps);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     if (p.splits > 1)

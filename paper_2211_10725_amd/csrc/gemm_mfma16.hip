@@ -885,6 +885,15 @@ hipError_t launch_gemm16(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream
     return dispatch16(g, kd, ws, ws_bytes, s, true, &sup);
 }
 
+hipError_t launch_split_planes(const float *src, int64_t ld, int rows, int K, int ldp,
+                               uint16_t *dst, hipStream_t s) {
+    const int64_t n = (int64_t)rows * ldp;
+    if (n <= 0) return hipSuccess;
+    split_planes_kernel<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, s>>>(src, ld, K,
+                                                                                  ldp, n, dst);
+    return hipGetLastError();
+}
+
 int gemm16_passes(const GemmArgs &g) {
     if (!gemm16_applies(g)) return 0;
     const Kind kd = classify(g.a_dtype, g.b_dtype);

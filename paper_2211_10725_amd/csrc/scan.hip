@@ -259,14 +259,17 @@ struct FoldStage {
 // (v - r thr), so the carry is beta + (v - r thr) s_t, and the recurrent
 // weight's gradient collects lam_{t+1} z_t per column (dvcol, fp32).
 //
-// With TR, dL/dI is also written as the weight gradient's operand: dcur_t
-// [P][N][B*T] (P = 3 bf16 parts of fp32, else 1 plane of the 16-bit type,
-// planes t_plane elements apart), row n holding column n of every sample,
-// K index b*T + t.  A lane's column is one row there and a chunk's steps are
-// consecutive in it, so each chunk's values are packed in registers as the
-// reverse loop produces them and stored together (the row-major dcur may be
-// skipped: nullptr).
-template <int NEURON, int VEC, int GM, bool RESET_SURR, int GT, bool TR>
+// With TR = TR_TRANSPOSED, dL/dI is also written as the weight gradient's
+// operand: dcur_t [P][N][B*T] (P = 3 bf16 parts of fp32, else 1 plane of the
+// 16-bit type, planes t_plane elements apart), row n holding column n of
+// every sample, K index b*T + t.  A lane's column is one row there and a
+// chunk's steps are consecutive in it, so each chunk's values are packed in
+// registers as the reverse loop produces them and stored together.  With
+// TR = TR_PLANES (fp32 only), dcur_t holds the three bf16 parts in dcur's own
+// layout, [3][T][C], written at every step like dcur.  The row-major dcur
+// may be skipped (nullptr) in both cases.
+constexpr int TR_NONE = 0, TR_TRANSPOSED = 1, TR_PLANES = 2;
+template <int NEURON, int VEC, int GM, bool RESET_SURR, int GT, int TRM>
 __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
     int T, int64_t C, int64_t N, float alpha, float beta, float thr, float slope,
     const float *__restrict__ vrec, const float *__restrict__ cur, const float *__restrict__ ckpt,
@@ -277,6 +280,7 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
     constexpr bool FULL = GM == GM_FULL;
     constexpr int K = kCkpt;
     constexpr int P = GT == SNN_F32 ? 3 : 1;  // 16-bit parts per value in dcur_t
+    constexpr bool TR = TRM == TR_TRANSPOSED;
     uint32_t pk[TR ? P : 1][TR ? VEC : 1][TR ? K / 2 : 1];  // packed parts of a chunk
     const float scale = GT == SNN_F16 ? *dscale : 1.f;
     constexpr int KF = GM == GM_FOLD12 ? 12 : kFoldMax;  // dI_up values per row (padded)
@@ -419,6 +423,17 @@ __global__ __launch_bounds__(kThreads) void neuron_bwd_kernel(
                     acc[v] += d[v];
                 }
                 if (dcur) store_grad<GT, VEC>(dcur, (int64_t)t * C + col, d, scale);
+                if constexpr (TRM == TR_PLANES) {
+#pragma unroll
+                    for (int p = 0; p < 3; ++p) {
+                        uint16_t *q = dcur_t + p * t_plane + (int64_t)t * C + col;
+                        const uint32_t h0 = grad_part<SNN_F32>(d[0], p, 1.f);
+                        if constexpr (VEC == 2)
+                            *reinterpret_cast<uint32_t *>(q) = h0 | (grad_part<SNN_F32>(d[1], p, 1.f) << 16);
+                        else
+                            q[0] = (uint16_t)h0;
+                    }
+                }
                 if constexpr (TR) {
 #pragma unroll
                     for (int p = 0; p < P; ++p)
@@ -646,6 +661,7 @@ struct BwdBuffers {
     FoldIn fold;
     void *dcur;
     uint16_t *dcur_t;
+    bool planes;  // dcur_t holds the planes of an fp32 dL/dI in dcur's layout
     const float *dscale;
     float *colsum, *dvcol;
 };
@@ -655,14 +671,20 @@ void bwd_launch(const ScanArgs &a, const BwdBuffers &b, hipStream_t s) {
     const int64_t lanes = (a.C + VEC - 1) / VEC;
     const unsigned grid = (unsigned)((lanes + kThreads - 1) / kThreads);
     const int64_t t_plane = (int64_t)a.T * a.C;
-    if (b.dcur_t)
-        neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, true><<<grid, kThreads, 0, s>>>(
+    if (b.dcur_t && b.planes) {
+        if constexpr (GT == SNN_F32)
+            neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, TR_PLANES><<<grid, kThreads, 0, s>>>(
+                a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.cur, b.ckpt, b.g,
+                b.fold, b.dcur, b.dcur_t, t_plane, b.dscale, b.colsum, b.dvcol);
+    } else if (b.dcur_t) {
+        neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, TR_TRANSPOSED><<<grid, kThreads, 0, s>>>(
             a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.cur, b.ckpt, b.g, b.fold,
             b.dcur, b.dcur_t, t_plane, b.dscale, b.colsum, b.dvcol);
-    else
-        neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, false><<<grid, kThreads, 0, s>>>(
+    } else {
+        neuron_bwd_kernel<NEURON, VEC, GM, RS, GT, TR_NONE><<<grid, kThreads, 0, s>>>(
             a.T, a.C, a.N, a.alpha, a.beta, a.thr, a.slope, a.vrec, b.cur, b.ckpt, b.g, b.fold,
             b.dcur, nullptr, 0, b.dscale, b.colsum, b.dvcol);
+    }
 }
 
 template <int NEURON, int VEC, int GM, bool RS>
@@ -733,9 +755,10 @@ bool neuron_fold_supported(int64_t N) { return N >= 64; }
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
                              const float *cur, const float *ckpt, const BwdGrad &grad, int B,
-                             void *dcur, void *dcur_t, int grad_dtype, const float *dscale,
-                             float *colsum, float *dvcol, hipStream_t s) {
+                             void *dcur, void *dcur_t, bool dcur_t_planes, int grad_dtype,
+                             const float *dscale, float *colsum, float *dvcol, hipStream_t s) {
     if (dcur == nullptr && dcur_t == nullptr) return hipErrorInvalidValue;
+    if (dcur_t && dcur_t_planes && grad_dtype != SNN_F32) return hipErrorInvalidValue;
     if (grad_dtype == SNN_F16 && dscale == nullptr) return hipErrorInvalidValue;
     if (T <= 0 || C <= 0) return hipSuccess;
     if (neuron_ckpt_count(T) > 0 && ckpt == nullptr) return hipErrorInvalidValue;
@@ -757,8 +780,8 @@ hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, 
     }
     const ScanArgs a{T, C, N, alpha, beta, thr, slope, vrec};
     const FoldIn fold{grad.dup, grad.wup, grad.nup, grad.dt_up, grad.dt_w, B};
-    const BwdBuffers b{cur, ckpt, grad.g, fold, dcur, reinterpret_cast<uint16_t *>(dcur_t),
-                       dscale, colsum, dvcol};
+    const BwdBuffers b{cur,  ckpt, grad.g, fold, dcur, reinterpret_cast<uint16_t *>(dcur_t),
+                       dcur_t_planes, dscale, colsum, dvcol};
     const int rs = reset_surrogate, gt = grad_dtype;
     switch (neuron) {
         case SNN_SYNAPTIC: bwd_dispatch<SNN_SYNAPTIC>(vec, rs, gm, gt, a, b, s); break;

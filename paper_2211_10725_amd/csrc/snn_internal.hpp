@@ -77,12 +77,13 @@ bool neuron_fold_supported(int64_t N);
 // of two S read from dscale[0] (launch_grad_scale writes it).
 // dcur_t (nullable): dL/dI also written as the weight gradient's operand,
 // [P][N][B*T] 16-bit (P = 3 exact bf16 parts of fp32, else 1), K index b*T + t;
-// dcur may be NULL when dcur_t is given.
+// with dcur_t_planes (fp32 only) instead the three exact bf16 parts in dcur's
+// own layout, [3][T][C].  dcur may be NULL when dcur_t is given.
 hipError_t launch_neuron_bwd(int neuron, int reset_surrogate, int T, int64_t C, int64_t N,
                              float alpha, float beta, float thr, float slope, const float *vrec,
                              const float *cur, const float *ckpt, const BwdGrad &grad, int B,
-                             void *dcur, void *dcur_t, int grad_dtype, const float *dscale,
-                             float *colsum, float *dvcol, hipStream_t s);
+                             void *dcur, void *dcur_t, bool dcur_t_planes, int grad_dtype,
+                             const float *dscale, float *colsum, float *dvcol, hipStream_t s);
 // scale[0] = S = 2^e, the largest power of two with G * growth * S <= 2^15,
 // G a bound on |g| over the upstream gradient (device reduction into
 // `scratch`, grad_scale_workspace_bytes()); growth bounds |dL/dI| / G.
@@ -142,6 +143,10 @@ bool gemm16_applies(const GemmArgs &g);
 size_t gemm16_workspace_bytes(const GemmArgs &g);
 hipError_t launch_gemm16(const GemmArgs &g, void *ws, size_t ws_bytes, hipStream_t s);
 int gemm16_passes(const GemmArgs &g);  // MFMA passes per product, 0 if not applicable
+// dst[p][rows][ldp] = part p (hi, mid, lo) of the exact three-bf16 split of
+// src[r * ld + k], k < K; columns K .. ldp - 1 are 0
+hipError_t launch_split_planes(const float *src, int64_t ld, int rows, int K, int ldp,
+                               uint16_t *dst, hipStream_t s);
 // ---- contractions of layers with few outputs (skinny.hip) --------------------
 // short contraction: K <= 16, A K-contiguous, B N-contiguous
 bool short_k_applies(const GemmArgs &g);

@@ -5,6 +5,8 @@ checks run the oracle's chain on its own and feed each GPU stage the oracle's
 inputs to that stage, so that a legal spike flip in one stage cannot cascade
 into the next.  Scans given identical fp32 currents must be bit-identical.
 """
+import copy
+
 import numpy as np
 import pytest
 
@@ -286,13 +288,19 @@ def test_synapse_bwd_transposed_operand_same_bytes():
     """The weight gradient from the scan's transposed operand equals the one
     from the row-major dL/dI (transposed inside the call): the same operand
     bytes in the same contraction."""
-    T, B, N, K = 40, 240, 600, 784  # 9600 rows: the transposed path for fp32 dL/dI
+    # 9600 rows and 602 neurons (not a multiple of 8, which the M/N-contiguous
+    # asynchronous kernel needs): the transposed path for fp32 dL/dI
+    T, B, N, K = 40, 240, 602, 784
     rng = np.random.default_rng(3)
     spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
-    # a 16-bit dL/dI is contracted in its own layout: no transposed operand
+    # with 600 neurons a 16-bit or fp32 dL/dI is contracted in its own layout:
+    # no transposed operand (an fp32 one as the three planes of its values)
+    spec600 = dict(spec, n_out=600)
     for gdt in ("bf16", "f16"):
-        assert snn.snn_layer_dcur_t_bytes(snn.layer_desc(spec, T, B,
+        assert snn.snn_layer_dcur_t_bytes(snn.layer_desc(spec600, T, B,
                                                          grad_dtype=GRAD_TYPES[gdt][0])) == 0
+    assert snn.snn_layer_dcur_t_layout(snn.layer_desc(spec600, T, B)) == snn.DCUR_T_PLANES
+    assert snn.snn_layer_dcur_t_layout(snn.layer_desc(spec, T, B)) == snn.DCUR_T_TRANSPOSED
     for gdt in ("f32",):
         gcode, tdt = GRAD_TYPES[gdt]
         d = snn.layer_desc(spec, T, B, grad_dtype=gcode)
@@ -320,7 +328,93 @@ def test_synapse_bwd_transposed_operand_same_bytes():
         assert_close(_np(gW2), rW, 1e-3, what=f"dW from the transposed {gdt} operand")
 
 
-@pytest.mark.parametrize("name,T,B,width", [("dsnn_synaptic_t50_b256", 40, 240, 600)])
+def _bf16_rne(x):
+    """bf16 bits of fp32 values, round to nearest even (finite values)."""
+    b = np.ascontiguousarray(x, np.float32).view(np.uint32).astype(np.uint64)
+    return ((b + 0x7FFF + ((b >> 16) & 1)) >> 16).astype(np.uint16)
+
+
+def _bf16_val(h):
+    return (h.astype(np.uint32) << 16).view(np.float32)
+
+
+def _three_parts(x):
+    """hi = bf16(x), mid = bf16(x - hi), lo = bf16(x - hi - mid), each
+    difference exact in fp32."""
+    x = np.asarray(x, np.float32)
+    hi = _bf16_rne(x)
+    r = x - _bf16_val(hi)
+    mid = _bf16_rne(r)
+    lo = _bf16_rne(r - _bf16_val(mid))
+    return np.stack([hi, mid, lo])
+
+
+def test_synapse_bwd_planes_operand_same_bytes():
+    """An fp32 dL/dI that the weight gradient reads in its own layout: the
+    reverse scan writes its three exact bf16 parts as [3][T*B][n_out] (the
+    split of the fp32 values it writes beside them, bit for bit; the parts
+    add up to the value exactly), and the weight gradient from them equals
+    the one from the fp32 dL/dI (split inside the call)."""
+    T, B, N, K = 40, 240, 600, 784
+    rng = np.random.default_rng(5)
+    spec = dict(kind="dense", n_in=K, n_out=N, neuron="leaky", beta=0.9)
+    d = snn.layer_desc(spec, T, B)
+    assert snn.snn_layer_dcur_t_layout(d) == snn.DCUR_T_PLANES
+    nb = snn.snn_layer_dcur_t_bytes(d)
+    assert nb >= 3 * T * B * N * 2
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    dn, _ = _none_desc(T, B, N, "leaky", 0.9)
+    xc, ck = _t(I), snn.ckpt_buffer(dn)
+    snn.snn_neuron_fwd(dn, xc, None, torch.empty((T, B, N), dtype=torch.uint8, device=DEV), ck,
+                       None)
+    g = _t(rng.normal(0, 0.1, (B, N)).astype(np.float32))
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    dI = torch.empty((T, B, N), dtype=torch.float32, device=DEV)
+    dt = torch.zeros(nb, dtype=torch.uint8, device=DEV)
+    snn.snn_neuron_bwd(d, snn.GRAD_BCAST, g, None, xc, ck, dI, None, None, ws, dcur_t=dt)
+    dI_h = _np(dI)
+    planes = _np(dt[:3 * T * B * N * 2].view(torch.int16)).view(np.uint16).reshape(3, T * B, N)
+    want = _three_parts(dI_h.reshape(T * B, N))
+    np.testing.assert_array_equal(planes, want)
+    total = sum(_bf16_val(planes[p]).astype(np.float64) for p in range(3))
+    np.testing.assert_array_equal(total, dI_h.reshape(T * B, N).astype(np.float64))
+    x = _t((rng.random((T, B, K)) < 0.3).astype(np.uint8))
+    W = _t(rng.uniform(-0.05, 0.05, (N, K)).astype(np.float32))
+    gW1 = torch.empty((N, K), dtype=torch.float32, device=DEV)
+    gW2 = torch.empty_like(gW1)
+    snn.snn_synapse_bwd(d, dI, None, x, W, gW1, None, ws)
+    snn.snn_synapse_bwd(d, None, None, x, W, gW2, None, ws, dcur_t=dt)
+    np.testing.assert_array_equal(_np(gW1), _np(gW2))
+    rW, _, _ = oracle.dense_bwd(dI_h.astype(np.float64).reshape(T * B, N),
+                                _np(x).reshape(T * B, K), _np(W), want_db=False, want_dx=False)
+    assert_close(_np(gW2), rW, 1e-3, what="dW from the scan's planes")
+    _assert_fp32_sum(_np(gW2) - rW, np.abs(dI_h.reshape(T * B, N)).astype(np.float64).T @
+                     _np(x).reshape(T * B, K).astype(np.float64), T * B, "dW")
+
+
+@pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
+def test_step_fp32_planes_operand(reset):
+    """784-704-704-10 in fp32 over 9600 rows: both hidden layers' weight
+    gradients read dL/dI as the three bf16 planes the reverse scan writes,
+    the upper one beside the fp32 dL/dI its input gradient needs.  Stage by
+    stage against the oracle, and the layer calls give the stage calls'
+    bytes."""
+    wl = copy.deepcopy(wls.get("dsnn_half_t100_b512"))
+    wl.dtype = "f32"
+    wl = wls.scaled(wl, T=40, B=240, width=704)
+    inp = wls.make_inputs(wl, seed=6)
+    net = snn.Network(wl, inp["params"], device=DEV, reset_grad=reset)
+    assert [snn.snn_layer_dcur_t_layout(d) for d in net.descs[:2]] == [snn.DCUR_T_PLANES] * 2
+    _check_step_stagewise(wl, inp, reset)
+    x, lab = _t(inp["x"]), _t(inp["labels"])
+    net.step(x, labels=lab)
+    ref = [_np(t).copy() for t in net.gW + net.gb]
+    net.step_stages(x, labels=lab)
+    for a, b in zip(ref, [_np(t) for t in net.gW + net.gb]):
+        np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("name,T,B,width", [("dsnn_synaptic_t50_b256", 40, 240, 602)])
 def test_step_with_scan_transposed_operand(name, T, B, width):
     """A whole step whose reverse scans write the weight gradients' operands
     transposed gives the layer calls' gradients bit for bit (the same operand
