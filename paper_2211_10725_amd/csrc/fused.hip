@@ -402,9 +402,10 @@ __global__ __launch_bounds__(kThreads) void fused_step_kernel(FusedArgs a) {
                 }
         }
         __syncthreads();
-        // one thread per own column (q, b)
+        // one thread per own column (b, q), neurons fastest: consecutive
+        // threads read consecutive LDS words and store consecutive spikes
         for (int c = tid; c < nq * B; c += kThreads) {
-            const int q = c / B, b = c % B, o = o0 + q;
+            const int b = c / nq, q = c % nq, o = o0 + q;
             float u = 0.f, syn = 0.f, zp = 0.f;
             for (int t = 0; t < T; ++t) {
                 const int r = t * B + b;
@@ -544,7 +545,7 @@ __global__ __launch_bounds__(kThreads) void fused_step_kernel(FusedArgs a) {
         stage16(Xb, a.xb, nxb);
         __syncthreads();
         for (int c = tid; c < nq * B; c += kThreads) {
-            const int q = c / B, b = c % B;
+            const int b = c / nq, q = c % nq;
             float wcol[kFusedMaxOut];
 #pragma unroll
             for (int j = 0; j < kFusedMaxOut; ++j) wcol[j] = Wc[q * kFusedMaxOut + j];
