@@ -303,6 +303,33 @@ __global__ __launch_bounds__(kThreads) void fused_step_kernel(FusedArgs a) {
     const unsigned limit = a.wait_limit;
     const int nxb = (int)(xbits_bytes(T, B, n_in) / 16);  // 16-byte chunks of packed x
     if (w == 0 && tid == 0) __hip_atomic_store(a.status, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    // W1 rows [n_out][HS] for the readout phase (workgroups w < B)
+    float *W1l = reinterpret_cast<float *>(lds + L.bw);
+    auto stage_w1 = [&] {
+        if (w >= B) return;
+        // W1 rows at stride HS: 16-byte chunks when rows are whole chunks
+        if (n_hid % 4 == 0) {
+            const int cpr = n_hid / 4, nc = n_out * cpr;
+            const u32x4 *src = reinterpret_cast<const u32x4 *>(a.W1);
+            for (int i0 = tid; i0 < nc; i0 += 8 * kThreads) {
+                u32x4 v[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) v[k] = src[min(i0 + k * kThreads, nc - 1)];
+#pragma unroll
+                for (int k = 0; k < 8; ++k) {
+                    const int i = i0 + k * kThreads;
+                    if (i < nc)
+                        *reinterpret_cast<u32x4 *>(W1l + (i / cpr) * HS + 4 * (i % cpr)) = v[k];
+                }
+            }
+        } else {
+            for (int i = tid; i < n_out * n_hid; i += kThreads)
+                W1l[(i / n_hid) * HS + i % n_hid] = a.W1[i];
+        }
+    };
+    // W1 rows go in with the W0 parts when they do not overlap the packed
+    // input of phase A (region X: packed input, then phase B's sample)
+    const bool w1_early = xbits_bytes(T, B, n_in) <= L.bw;
 
     // ---- 0: the input spikes as bits, 4 packed bytes (32 inputs) per thread
     {
@@ -325,14 +352,12 @@ __global__ __launch_bounds__(kThreads) void fused_step_kernel(FusedArgs a) {
             put_shared(reinterpret_cast<uint32_t *>(a.xb) + i, word);
         }
     }
-    bool alive = grid_barrier(1, G, limit, a.status, &ok);
-
-    // ---- A: currents and forward scan of the own neurons ---------------------
-    if (alive) {
+    const int kp = round32(n_in);
+    uint16_t *Wp = reinterpret_cast<uint16_t *>(lds + L.y);  // [3][NPW][kp]
+    {
         // the bf16 parts of the own neurons' W0 rows (zero past n_in and past
-        // the last neuron), W1 columns of the own neurons, the packed input
-        const int kp = round32(n_in);
-        uint16_t *Wp = reinterpret_cast<uint16_t *>(lds + L.y);  // [3][NPW][kp]
+        // the last neuron) and W1 columns of the own neurons: LDS is free and
+        // W0 does not depend on phase 0, so their loads run before barrier 1
         for (int i0 = tid; i0 < kp; i0 += 4 * kThreads) {
             float v[NPW][4];
 #pragma unroll
@@ -361,6 +386,12 @@ __global__ __launch_bounds__(kThreads) void fused_step_kernel(FusedArgs a) {
             const int q = tid / kFusedMaxOut, j = tid % kFusedMaxOut;
             Wc[tid] = (q < nq && j < n_out) ? a.W1[(int64_t)j * n_hid + o0 + q] : 0.f;
         }
+        if (w1_early) stage_w1();
+    }
+    bool alive = grid_barrier(1, G, limit, a.status, &ok);
+
+    // ---- A: currents and forward scan of the own neurons ---------------------
+    if (alive) {
         stage16(Xb, a.xb, nxb);
         __syncthreads();
         // D[r][q] = sum_k x[r][k] W0[o0 + q][k]: wave wv takes row blocks wv,
@@ -423,32 +454,11 @@ __global__ __launch_bounds__(kThreads) void fused_step_kernel(FusedArgs a) {
     // ---- B: readout forward, loss, readout reverse scan (one sample each) ----
     if (alive) {
         uint8_t *Sb = lds;                                       // [T][HS]
-        float *W1l = reinterpret_cast<float *>(lds + L.bw);      // [n_out][HS]
         float *I1 = reinterpret_cast<float *>(lds + L.bi);       // [T][n_out]
         float *U1 = reinterpret_cast<float *>(lds + L.bu);       // [T][n_out]
         double *cls = reinterpret_cast<double *>(lds + L.bc);    // [64]
         float *part = reinterpret_cast<float *>(cls + 64);       // [4][32][16] k-quarter partials
-        if (w < B) {
-            // W1 rows at stride HS: 16-byte chunks when rows are whole chunks
-            if (n_hid % 4 == 0) {
-                const int cpr = n_hid / 4, nc = n_out * cpr;
-                const u32x4 *src = reinterpret_cast<const u32x4 *>(a.W1);
-                for (int i0 = tid; i0 < nc; i0 += 8 * kThreads) {
-                    u32x4 v[8];
-#pragma unroll
-                    for (int k = 0; k < 8; ++k) v[k] = src[min(i0 + k * kThreads, nc - 1)];
-#pragma unroll
-                    for (int k = 0; k < 8; ++k) {
-                        const int i = i0 + k * kThreads;
-                        if (i < nc)
-                            *reinterpret_cast<u32x4 *>(W1l + (i / cpr) * HS + 4 * (i % cpr)) = v[k];
-                    }
-                }
-            } else {
-                for (int i = tid; i < n_out * n_hid; i += kThreads)
-                    W1l[(i / n_hid) * HS + i % n_hid] = a.W1[i];
-            }
-        }
+        if (!w1_early) stage_w1();
         for (int b = w; b < B; b += G) {
             __syncthreads();
             stage16(Sb, a.s0 + (int64_t)b * T * HS, T * HS / 16);
