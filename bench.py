@@ -81,7 +81,7 @@ def stored_traffic(workload: str, stage_key: str):
 
 
 def _dtype_bytes(code):
-    return {0: 4, 1: 2, 2: 2, 3: 1}[code]
+    return {0: 4, 1: 2, 2: 2, 3: 1, 4: 0.125}[code]  # 4: spikes packed to bits
 
 
 def _macs(d):
@@ -101,7 +101,7 @@ def stage_work(net, name, li):
                    (K = T*B) and dx (K = n_out), each 2 M N K; a conv layer's
                    backward is one stage with both
       forward scan 4 B read current + s B write spike per (t, b, n) (s = 1
-                   for bytes, 2 for fp16 spikes), + 4 P B per (b, n) per
+                   for bytes, 2 for fp16 spikes, 1/8 packed to bits), + 4 P B per (b, n) per
                    checkpoint (P = 1 state plane, 2 for the current-based
                    neuron), + 4 B count per (b, n) of the layer that counts
       reverse scan 4 B read current (the membrane is recomputed from it) +
@@ -359,8 +359,10 @@ def main():
         sys.exit(2)
     stream = torch.cuda.Stream()  # default priority
     params = wls.init_params(wl, args.seed)
+    # a scan-only layer's spikes (read by nothing in the step) packed to bits
     net = snn.Network(wl, params, device="cuda",
-                      flags=snn.FLAG_FP32_MFMA if args.fp32_mfma else 0)
+                      flags=snn.FLAG_FP32_MFMA if args.fp32_mfma else 0,
+                      spike_bits=wl.layers[0]["kind"] == "none")
     if args.update:
         net.init_adamw(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2)
     upd = bool(args.update)
@@ -464,7 +466,9 @@ def main():
                    "includes": "forward + loss + BPTT backward + fused AdamW update"
                    if upd else "forward + loss + BPTT backward, no optimizer update",
                    "launch": "one HIP graph replay per step" if args.graph
-                   else "eager library calls"},
+                   else "eager library calls",
+                   "output_spikes": "packed bits" if net.descs[-1].out_dtype == snn.SPK_BITS
+                   else "bytes"},
         "step_ms": {"median": round(per_step[len(per_step) // 2], 5),
                     "p10": round(per_step[len(per_step) // 10], 5),
                     "p90": round(per_step[(9 * len(per_step)) // 10], 5)},
@@ -507,7 +511,7 @@ def scan_wide_leg(args, stream):
     import paper_2211_10725_amd as snn
     from paper_2211_10725_amd import workloads as wls
     wl = wls.get(SCAN_WORKLOAD)
-    net = snn.Network(wl, wls.init_params(wl, args.seed), device="cuda")
+    net = snn.Network(wl, wls.init_params(wl, args.seed), device="cuda", spike_bits=True)
     steps, warm = max(2, min(args.steps, 10)), 5
     with torch.cuda.stream(stream):
         x, y, tgt = _inputs(wl, args.seed)
@@ -535,7 +539,8 @@ def scan_wide_leg(args, stream):
     out = {"workload": wl.name, "description": wl.description, "steps": steps,
            "warmup": warm, "ms_per_step": round(total_ms / steps, 5),
            "value": round(wl.B * steps / (total_ms / 1000.0), 1), "unit": "samples/s",
-           "dtype": "f32", "stage_ms": {k: round(v, 5) for k, v in split.items()},
+           "dtype": "f32", "output_spikes": "packed bits",
+           "stage_ms": {k: round(v, 5) for k, v in split.items()},
            "scan_roofline": scans}
     del net, x
     torch.cuda.empty_cache()

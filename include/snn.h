@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 9
+#define SNN_ABI_VERSION 10
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -81,6 +81,10 @@ typedef enum snn_status {
 #define SNN_F16 1
 #define SNN_BF16 2
 #define SNN_U8 3 /* spikes stored as bytes 0 / 1 */
+#define SNN_SPK_BITS 4 /* spikes packed 64 to a 64-bit word: neuron n of row
+                          (t, b) is bit n % 64 of word n / 64 of that row's
+                          n / 64 words (little-endian: bit n % 8 of byte
+                          n / 8); an output type only, n_out a multiple of 64 */
 
 /* neuron models */
 #define SNN_LEAKY 0    /* eq. (4) */
@@ -135,7 +139,9 @@ typedef struct snn_layer_desc {
     int32_t c_in, h_in, w_in, c_out; /* conv geometry, else ignored */
     int32_t in_dtype;       /* x: SNN_U8 spikes, SNN_F32 (also SYN_NONE), SNN_F16 */
     int32_t w_dtype;        /* w: SNN_F32 | SNN_F16 */
-    int32_t out_dtype;      /* spikes written as SNN_U8 | SNN_F16 (0.0 / 1.0) */
+    int32_t out_dtype;      /* spikes written as SNN_U8 | SNN_F16 (0.0 / 1.0) |
+                               SNN_SPK_BITS ([T,B,n_out / 8] bytes; n_out a
+                               multiple of 64, else SNN_ERR_SHAPE) */
     int32_t grad_dtype;     /* dL/dI handed to the weight / input gradient
                                contractions: SNN_F32 | SNN_BF16 | SNN_F16.
                                SNN_F16 holds dL/dI * S, S a power of two

@@ -25,13 +25,14 @@ LIB_PATH = os.path.join(_HERE, "libsnn.so")
 
 # element types, neuron models, synapses, gradient kinds, losses (snn.h)
 F32, F16, BF16, U8 = 0, 1, 2, 3
+SPK_BITS = 4  # spikes packed 64 to a word (an output type only)
 LEAKY, SYNAPTIC, RLEAKY = 0, 1, 2
 SYN_DENSE, SYN_CONV5_POOL2, SYN_NONE = 0, 1, 2
 RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST, GRAD_FOLD = 0, 1, 2
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 9
+ABI_VERSION = 10
 DCUR_T_TRANSPOSED, DCUR_T_PLANES = 1, 2
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
@@ -215,7 +216,10 @@ def _need(fn, t, dtype_code, count, what):
 def _check_fwd_io(fn, d, x=None, spk=None):
     rows = d.T * d.B
     _need(fn, x, d.in_dtype, rows * d.n_in, "x")
-    _need(fn, spk, d.out_dtype, rows * d.n_out, "spk_out")
+    if d.out_dtype == SPK_BITS:
+        _need(fn, spk, U8, rows * d.n_out // 8, "spk_out (packed bits)")
+    else:
+        _need(fn, spk, d.out_dtype, rows * d.n_out, "spk_out")
 
 
 def snn_layer_saved_bytes(desc: LayerDesc) -> int:
@@ -439,7 +443,8 @@ class Network:
     All buffers are allocated once here (torch, device memory only); ``step``
     then only enqueues library calls on the current stream."""
 
-    def __init__(self, wl, params, device="cuda", reset_grad=RESET_DETACHED, flags=0, fold=True):
+    def __init__(self, wl, params, device="cuda", reset_grad=RESET_DETACHED, flags=0, fold=True,
+                 spike_bits=False):
         import torch
         self.torch = torch
         self.wl = wl
@@ -478,8 +483,13 @@ class Network:
             if half and up.synapse == SYN_DENSE and up.n_out >= 256 and up.n_in >= 256:
                 self.descs[li].out_dtype = F16
                 up.in_dtype = F16
-        self.spk = [torch.empty((T, B, d.n_out), dtype=torch.float16 if d.out_dtype == F16
-                                else u8, device=device) for d in self.descs]
+        # spike_bits: the last layer's spikes, which no contraction reads,
+        # packed 64 to a word (layers of a multiple of 64 neurons)
+        if spike_bits and self.descs[-1].n_out % 64 == 0:
+            self.descs[-1].out_dtype = SPK_BITS
+        self.spk = [torch.empty((T, B, d.n_out // 8 if d.out_dtype == SPK_BITS else d.n_out),
+                                dtype=torch.float16 if d.out_dtype == F16 else u8, device=device)
+                    for d in self.descs]
         self.in_shape = (T, B) + tuple(wl.in_shape)
         self.saved = [torch.empty(snn_layer_saved_bytes(d), dtype=u8, device=device)
                       for d in self.descs]

@@ -41,7 +41,9 @@ snn_status check_desc(const snn_layer_desc *d) {
     if (!finite(d->beta) || !finite(d->alpha) || !finite(d->threshold) || !finite(d->slope) ||
         d->slope < 0.f)
         return SNN_ERR_SHAPE;
-    if (d->out_dtype != SNN_U8 && d->out_dtype != SNN_F16) return SNN_ERR_DTYPE;
+    if (d->out_dtype != SNN_U8 && d->out_dtype != SNN_F16 && d->out_dtype != SNN_SPK_BITS)
+        return SNN_ERR_DTYPE;
+    if (d->out_dtype == SNN_SPK_BITS && d->n_out % 64 != 0) return SNN_ERR_SHAPE;
     if (d->grad_dtype != SNN_F32 && d->grad_dtype != SNN_F16 && d->grad_dtype != SNN_BF16)
         return SNN_ERR_DTYPE;
     const int64_t TB = (int64_t)d->T * d->B;
@@ -335,7 +337,7 @@ snn_status check_fused(const snn_fused_desc *f, FusedPlan *plan) {
     if (st != SNN_OK) return st;
     if (h.synapse != SNN_SYN_DENSE || r.synapse != SNN_SYN_DENSE) return SNN_ERR_UNSUPPORTED;
     if (h.in_dtype != SNN_U8 || r.in_dtype != SNN_U8 || h.w_dtype != SNN_F32 ||
-        r.w_dtype != SNN_F32)
+        r.w_dtype != SNN_F32 || h.out_dtype == SNN_SPK_BITS)
         return SNN_ERR_DTYPE;
     auto plain = [](int n) { return n == SNN_LEAKY || n == SNN_SYNAPTIC; };
     if (!plain(h.neuron) || !plain(r.neuron)) return SNN_ERR_UNSUPPORTED;

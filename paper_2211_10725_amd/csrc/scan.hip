@@ -72,6 +72,25 @@ __device__ inline void store_spikes_f16(uint16_t *p, const float (&z)[VEC]) {
     }
 }
 
+// Spikes packed to bits, one wave's columns per step: a ballot per column
+// slot of the lanes.  Lanes that pack bits own the columns w0 + lane + 64 v
+// of their wave's 64 VEC columns (w0 the wave's first column, a multiple of
+// 64 VEC: the launcher takes VEC = 2 only when C is a multiple of 128, and C
+// is a multiple of 64), so ballot v is the 64-bit word of columns
+// w0 + 64 v .. + 63.  Lane 0 stores the wave's VEC words.
+template <int VEC>
+__device__ inline void store_spikes_bits(uint64_t *words, int64_t wave_off, const float (&z)[VEC]) {
+    const int lane = threadIdx.x & 63;
+    const uint64_t w0 = __ballot(z[0] > 0.f);
+    if constexpr (VEC == 2) {
+        const uint64_t w1 = __ballot(z[1] > 0.f);
+        if (lane == 0)
+            *reinterpret_cast<ulonglong2 *>(words + wave_off / 64) = make_ulonglong2(w0, w1);
+    } else {
+        if (lane == 0) words[wave_off / 64] = w0;
+    }
+}
+
 // Forward scan.  Writes the spikes, the spike counts (nullable), the full
 // membrane (u_out, nullable; it may alias cur exactly: each lane reads step
 // t before it writes it) and the checkpoints: after step t with
@@ -89,26 +108,47 @@ __global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, 
                                                               float *__restrict__ ckpt,
                                                               float *__restrict__ counts) {
     static_assert(kCkpt % kDepth == 0, "checkpoints fall on block boundaries");
-    const int64_t col = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * VEC;
+    // packed-bit output with two columns per lane: the lane's columns are col
+    // and col + 64 (see store_spikes_bits), else col and col + 1
+    constexpr bool SPLIT = OUT == SNN_SPK_BITS && VEC == 2;
+    constexpr int CS = SPLIT ? 64 : 1;  // column stride within a lane
+    const int64_t gid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    const int64_t col = SPLIT ? (gid >> 6) * 128 + (gid & 63) : gid * VEC;
     if (col >= C) return;
+    auto ld = [&](const float *p, float (&v)[VEC]) {
+        if constexpr (SPLIT) {
+            v[0] = p[0];
+            v[1] = p[64];
+        } else {
+            Vec<VEC>::load(p, v);
+        }
+    };
+    auto st = [&](float *p, const float (&v)[VEC]) {
+        if constexpr (SPLIT) {
+            p[0] = v[0];
+            p[64] = v[1];
+        } else {
+            Vec<VEC>::store(p, v);
+        }
+    };
     const int nck = (T - 1) / kCkpt;
     float u[VEC], syn[VEC], zp[VEC], cnt[VEC], jump[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) {
         u[v] = syn[v] = zp[v] = cnt[v] = 0.f;
-        if constexpr (NEURON == SNN_RLEAKY) jump[v] = vrec[(col + v) % N] - thr;
+        if constexpr (NEURON == SNN_RLEAKY) jump[v] = vrec[(col + CS * v) % N] - thr;
         else jump[v] = -thr;
     }
 
     float in[kDepth][VEC], nx[kDepth][VEC];
 #pragma unroll
     for (int j = 0; j < kDepth; ++j)
-        if (j < T) Vec<VEC>::load(cur + (int64_t)j * C + col, in[j]);
+        if (j < T) ld(cur + (int64_t)j * C + col, in[j]);
 
     for (int t0 = 0; t0 < T; t0 += kDepth) {
 #pragma unroll
         for (int j = 0; j < kDepth; ++j)
-            if (t0 + kDepth + j < T) Vec<VEC>::load(cur + (int64_t)(t0 + kDepth + j) * C + col, nx[j]);
+            if (t0 + kDepth + j < T) ld(cur + (int64_t)(t0 + kDepth + j) * C + col, nx[j]);
 #pragma unroll
         for (int j = 0; j < kDepth; ++j) {
             const int t = t0 + j;
@@ -123,9 +163,12 @@ __global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, 
                     cnt[v] += z[v];
                 }
                 const int64_t off = (int64_t)t * C + col;
-                if (u_out) Vec<VEC>::store(u_out + off, u);
+                if (u_out) st(u_out + off, u);
                 if constexpr (OUT == SNN_U8)
                     store_spikes_u8<VEC>(reinterpret_cast<uint8_t *>(spk) + off, z);
+                else if constexpr (OUT == SNN_SPK_BITS)
+                    store_spikes_bits<VEC>(reinterpret_cast<uint64_t *>(spk),
+                                           off - (threadIdx.x & 63), z);
                 else
                     store_spikes_f16<VEC>(reinterpret_cast<uint16_t *>(spk) + off, z);
             }
@@ -133,15 +176,15 @@ __global__ __launch_bounds__(kThreads) void neuron_fwd_kernel(int T, int64_t C, 
         const int tn = t0 + kDepth;  // steps done
         if (tn % kCkpt == 0 && tn < T) {
             const int64_t slot = (int64_t)(tn / kCkpt - 1) * C + col;
-            Vec<VEC>::store(ckpt + slot, u);
-            if constexpr (NEURON == SNN_SYNAPTIC) Vec<VEC>::store(ckpt + (int64_t)nck * C + slot, syn);
+            st(ckpt + slot, u);
+            if constexpr (NEURON == SNN_SYNAPTIC) st(ckpt + (int64_t)nck * C + slot, syn);
         }
 #pragma unroll
         for (int j = 0; j < kDepth; ++j)
 #pragma unroll
             for (int v = 0; v < VEC; ++v) in[j][v] = nx[j][v];
     }
-    if (counts) Vec<VEC>::store(counts + col, cnt);
+    if (counts) st(counts + col, cnt);
 }
 
 __device__ inline uint16_t f32_to_bf16_rne(float x) {
@@ -653,6 +696,7 @@ void fwd_launch(const ScanArgs &a, const FwdBuffers &b, hipStream_t s) {
 template <int NEURON, int VEC>
 void fwd_dispatch(int out_dtype, const ScanArgs &a, const FwdBuffers &b, hipStream_t s) {
     if (out_dtype == SNN_U8) fwd_launch<NEURON, VEC, SNN_U8>(a, b, s);
+    else if (out_dtype == SNN_SPK_BITS) fwd_launch<NEURON, VEC, SNN_SPK_BITS>(a, b, s);
     else fwd_launch<NEURON, VEC, SNN_F16>(a, b, s);
 }
 
@@ -731,7 +775,9 @@ hipError_t launch_neuron_fwd(int neuron, int T, int64_t C, int64_t N, float alph
                              hipStream_t s) {
     if (T <= 0 || C <= 0) return hipSuccess;
     if (neuron_ckpt_count(T) > 0 && ckpt == nullptr) return hipErrorInvalidValue;
-    const bool v2 = (C % 2) == 0 && C >= kWideColumns;
+    // packed spikes: whole 64-bit words per wave (C a multiple of 64 * VEC)
+    if (out_dtype == SNN_SPK_BITS && C % 64 != 0) return hipErrorInvalidValue;
+    const bool v2 = (C % 2) == 0 && C >= kWideColumns && (out_dtype != SNN_SPK_BITS || C % 128 == 0);
     const ScanArgs a{T, C, N, alpha, beta, thr, 0.f, vrec};
     const FwdBuffers b{cur, spk, u_out, ckpt, counts};
     switch (neuron) {

@@ -65,6 +65,13 @@ def test_validation_errors_before_launch():
                                beta=0.5), 4, 3)
     bad = conv.copy(); bad.n_out = 5
     assert _fwd(bad) == 2
+    # packed spikes: an output type only, for layers of a multiple of 64 neurons
+    bits = d.copy(); bits.out_dtype = snn.SPK_BITS
+    assert _fwd(bits) == 2                                      # n_out = 7
+    bits = _dense(n_out=128); bits.out_dtype = snn.SPK_BITS
+    assert snn.lib().snn_layer_saved_bytes(ctypes.byref(bits)) > 0
+    bad = _dense(); bad.in_dtype = snn.SPK_BITS
+    assert _fwd(bad) == 3
     # the recurrent neuron (eq. 7) needs its recurrent weights
     rec = _dense(); rec.neuron = snn.RLEAKY
     assert _fwd(rec) == 1

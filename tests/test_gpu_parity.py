@@ -110,6 +110,48 @@ def test_scan_fwd_in_place_and_f16_spikes():
     np.testing.assert_array_equal(_np(spk).astype(np.uint8), z)
 
 
+# SNN_SPK_BITS: (5, 8, 65536) takes two-column lanes (the even and odd
+# columns' ballots interleaved), (3, 9, 65600) one-column lanes on a wide
+# layer (4.3M columns, not a multiple of 128), the others one-column lanes.
+@pytest.mark.parametrize("neuron,alpha,beta", [("leaky", 0.0, 0.95), ("synaptic", 0.9, 0.8)])
+@pytest.mark.parametrize("T,B,N", [(1, 1, 64), (7, 3, 128), (5, 8, 65536), (3, 9, 65600)])
+def test_scan_fwd_packed_bits(neuron, alpha, beta, T, B, N):
+    """Spikes packed 64 to a word: neuron n of row (t, b) is bit n % 8 of
+    byte n / 8 of the row, the oracle's spikes packed; counts and checkpoints
+    as with byte spikes."""
+    rng = np.random.default_rng(T * 1000 + N + 7)
+    I = rng.normal(0.3, 0.8, (T, B, N)).astype(np.float32)
+    d, _ = _none_desc(T, B, N, neuron, beta, alpha)
+    d.out_dtype = snn.SPK_BITS
+    bits = torch.full((T, B, N // 8), 0xA5, dtype=torch.uint8, device=DEV)
+    counts = torch.empty((B, N), dtype=torch.float32, device=DEV)
+    ck = snn.ckpt_buffer(d)
+    snn.snn_neuron_fwd(d, _t(I), None, bits, ck, counts)
+    z, u, c = oracle.scan_fwd(I, neuron, beta, 1.0, alpha)
+    want = np.packbits(np.asarray(z, np.uint8).reshape(T, B, N), axis=-1, bitorder="little")
+    np.testing.assert_array_equal(_np(bits), want)
+    np.testing.assert_array_equal(_np(counts), c)
+    _assert_checkpoints(d, ck, u)
+
+
+def test_network_packed_output_spikes():
+    """A scan-only network with its spikes packed gives the unpacked
+    network's spikes, counts, loss and gradients bit for bit."""
+    wl = wls.scaled(wls.get("scan_wide_t1000_b64"), T=40, B=16, width=65536)
+    inp = wls.make_inputs(wl, seed=3)
+    x, tgt = _t(inp["x"]), _t(inp["targets"])
+    nets = [snn.Network(wl, inp["params"], device=DEV, spike_bits=sb) for sb in (False, True)]
+    for net in nets:
+        net.step(x, targets=tgt)
+    assert nets[1].descs[0].out_dtype == snn.SPK_BITS
+    z = _np(nets[0].spk[0])
+    np.testing.assert_array_equal(_np(nets[1].spk[0]),
+                                  np.packbits(z, axis=-1, bitorder="little"))
+    for a, b in ((nets[0].counts, nets[1].counts), (nets[0].loss[:1], nets[1].loss[:1]),
+                 (nets[0].gx[0], nets[1].gx[0])):
+        np.testing.assert_array_equal(_np(a), _np(b))
+
+
 @pytest.mark.parametrize("neuron,alpha,beta", [("leaky", 0.0, 0.95), ("synaptic", 0.9, 0.8)])
 @pytest.mark.parametrize("reset", [snn.RESET_DETACHED, snn.RESET_SURROGATE])
 @pytest.mark.parametrize("bcast", [True, False])
