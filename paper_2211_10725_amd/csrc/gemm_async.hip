@@ -154,6 +154,14 @@ using TileCopy = typename std::conditional<MN, TileCopyMN, TileCopyKC>::type;
 // that stage are in LDS, and every wave has finished reading the other stage,
 // which the next copies overwrite.
 __device__ inline void stage_barrier() { asm volatile("s_waitcnt vmcnt(0)\n\ts_barrier" ::: "memory"); }
+// The first step of an item after a whole tile was stored through LDS: the
+// 32 row stores of that epilogue were issued after this item's first
+// copies, and vector memory operations complete in issue order, so waiting
+// until at most 32 are outstanding waits for the copies only and leaves the
+// stores draining under the first multiply.
+__device__ inline void stage_barrier_after_stores() {
+    asm volatile("s_waitcnt vmcnt(32)\n\ts_barrier" ::: "memory");
+}
 
 // LDS byte address of a stage element
 __device__ inline uint32_t lds_addr(const uint16_t *p) {
@@ -449,6 +457,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
     // plane offsets of the first step (part 0: the last plane)
     const int64_t a_off0 = (P - 1) * a_ps, b_off0 = (P - 1) * b_ps;
     int m0, n0, zk, kbeg, kend, nk;
+    bool stores_pending = false;  // the previous item stored a whole tile through LDS
     setup(item, m0, n0, zk, kbeg, kend, nk);
     ca.copy(kbeg, kend, stage_a<0>(), a_off0);
     cb.copy(kbeg, kend, stage_b<0>(), b_off0);
@@ -469,7 +478,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
 #define SNN_ASYNC_STEP(S, NEXT)                                                             \
     {                                                                                       \
         const int tt = t + (S);                                                             \
-        stage_barrier();                                                                    \
+        if (tt == 0 && stores_pending)                                                      \
+            stage_barrier_after_stores();                                                   \
+        else                                                                                \
+            stage_barrier();                                                                \
         if (tt < nv) {                                                                      \
             int np = 0, nkk = tt + 1, kc = tt;                                              \
             if constexpr (P > 1) {                                                          \
@@ -516,6 +528,7 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
             store_tile_lds(acc, Cz, ldc, M, N, m0c, n0c, wm, wn, inv, bn);
         else
             store_tile_direct(acc, Cz, ldc, M, N, m0c, n0c, wm, wn, inv, bn);
+        stores_pending = wide_stores && m0c + kTile <= M && n0c + kTile <= N;
     }
     // the workgroup's LDS must not be released with copies into it in flight
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
