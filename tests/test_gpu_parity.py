@@ -565,10 +565,13 @@ PATHS = {"split": 0, "fp32mfma": snn.FLAG_FP32_MFMA}
 
 
 # (1040, 1100, 1000): large enough for the 256 x 256 asynchronous kernel with
-# fp16 weights, ragged in M and N, and a last k-tile of 8 values.  Layers with
-# at most 16 outputs: (12800, 10, 1000) the readout, (5000, 7, 1003) rows not
-# 4-aligned, (777, 16, 1500) and (2000, 10, 4096) long contractions.
-@pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784), (1040, 1100, 1000),
+# fp16 weights, ragged in M and N, and a last k-tile of 8 values; with fp32
+# weights (12800, 1000, 784) and (12850, 1000, 1000) run its three-plane
+# mode, the latter ragged in M, N and K.  Layers with at most 16 outputs:
+# (12800, 10, 1000) the readout, (5000, 7, 1003) rows not 4-aligned,
+# (777, 16, 1500) and (2000, 10, 4096) long contractions.
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784), (12850, 1000, 1000),
+                                                 (1040, 1100, 1000),
                                                  (12800, 10, 1000), (5000, 7, 1003),
                                                  (777, 16, 1500), (2000, 10, 4096)])
 @pytest.mark.parametrize("wdt", ["f32", "f16"])
@@ -598,9 +601,13 @@ def test_synapse_fwd(M, N, K, wdt, path):
 # for the skinny kernels (short contraction for dx, few rows for dW); 1003
 # inputs give unaligned rows and a partial last group of 4 columns.
 # (8197, 130, 1003): the weight gradient's operands are transposed first, with
-# ragged rows and columns on both sides of every transpose
+# ragged rows and columns on both sides of every transpose.  (9640, 600, 784):
+# the weight gradient on the asynchronous kernel's three-plane mode in the
+# operands' own layouts, ragged in both tile dimensions, a partial last
+# k-tile and 19 splits over K.
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784), (12800, 10, 1000),
-                                                 (5000, 7, 1003), (8197, 130, 1003)])
+                                                 (5000, 7, 1003), (8197, 130, 1003),
+                                                 (9640, 600, 784)])
 @pytest.mark.parametrize("path", list(PATHS))
 def test_synapse_bwd(M, N, K, path):
     """dW = dI^T x (split over K = T*B) and dx = dI W."""
