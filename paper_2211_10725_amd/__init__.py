@@ -262,6 +262,16 @@ def snn_layer_dcur_t_bytes(desc: LayerDesc) -> int:
     return int(lib().snn_layer_dcur_t_bytes(ctypes.byref(desc)))
 
 
+def _dcur_t_written(desc: LayerDesc) -> int:
+    """Bytes snn_neuron_bwd writes to a dcur_t argument: the layer's operand
+    when its weight gradient takes one, else the transposed layout
+    ([P][n_out][T*B] 16-bit, P = 3 for an fp32 dL/dI)."""
+    n = snn_layer_dcur_t_bytes(desc)
+    if n > 0:
+        return n
+    return (3 if desc.grad_dtype == F32 else 1) * desc.n_out * desc.T * desc.B * 2
+
+
 def snn_layer_dcur_t_layout(desc: LayerDesc) -> int:
     """DCUR_T_TRANSPOSED or DCUR_T_PLANES: the layout of the dcur_t operand
     snn_neuron_bwd writes for this layer."""
@@ -366,11 +376,12 @@ def snn_neuron_bwd(desc, grad_kind, g, v, cur, ckpt, dcur, grad_b, grad_v, ws, s
                    dcur_scale=None, dcur_t=None):
     """cur, ckpt: the forward's currents and checkpoints.  dcur_scale: device
     fp32 scalar receiving the power of two an fp16 dcur is scaled by
-    (required for grad_dtype F16).  dcur_t: the transposed weight-gradient
-    operand (snn_layer_dcur_t_bytes), or None; dcur may then be None."""
-    if dcur_t is not None and dcur_t.numel() * dcur_t.element_size() < \
-            snn_layer_dcur_t_bytes(desc):
-        raise ValueError("snn_neuron_bwd: dcur_t smaller than snn_layer_dcur_t_bytes")
+    (required for grad_dtype F16).  dcur_t: the weight gradient's operand in
+    the layout snn_layer_dcur_t_layout names (transposed, or an fp32 dL/dI's
+    three bf16 planes; snn_layer_dcur_t_bytes), or None; dcur may then be
+    None."""
+    if dcur_t is not None and dcur_t.numel() * dcur_t.element_size() < _dcur_t_written(desc):
+        raise ValueError("snn_neuron_bwd: dcur_t smaller than the operand the scan writes")
     _need("snn_neuron_bwd", cur, F32, desc.T * desc.B * desc.n_out, "cur")
     _need("snn_neuron_bwd", ckpt, F32, snn_layer_saved_layout(desc).ckpt_bytes // 4, "ckpt")
     _need("snn_neuron_bwd", dcur, desc.grad_dtype if desc.synapse != SYN_NONE else F32,
