@@ -359,15 +359,22 @@ def main():
         sys.exit(2)
     stream = torch.cuda.Stream()  # default priority
     params = wls.init_params(wl, args.seed)
-    # a scan-only layer's spikes (read by nothing in the step) packed to bits
+    # a scan-only layer's spikes (read by nothing in the step) packed to bits;
+    # an fp32 net's input spikes stored as bf16 0/1 when its first product
+    # runs on the asynchronous kernel's three-plane mode (no widening passes)
+    l0 = wl.layers[0]
+    bf16_in = (wl.dtype == "f32" and l0["kind"] == "dense" and not args.fp32_mfma and
+               _async_ok(3, 0, wl.T * wl.B, l0["n_out"], l0["n_in"]))
     net = snn.Network(wl, params, device="cuda",
                       flags=snn.FLAG_FP32_MFMA if args.fp32_mfma else 0,
-                      spike_bits=wl.layers[0]["kind"] == "none")
+                      spike_bits=l0["kind"] == "none", input_bf16=bf16_in)
     if args.update:
         net.init_adamw(lr=1e-3, betas=(0.9, 0.999), eps=1e-8, weight_decay=1e-2)
     upd = bool(args.update)
     with torch.cuda.stream(stream):
         x, y, tgt = _inputs(wl, args.seed)
+        if bf16_in:
+            x = x.to(torch.bfloat16)
     torch.cuda.synchronize()
 
     if args.mode == "pmc":
@@ -461,7 +468,9 @@ def main():
                                  "backward contractions, fp32 weight gradients") if half else
                                 ("fp32 weights, currents, state and gradients; products "
                                  "exact, fp32 accumulation"),
-                   "surrogate_slope": wl.slope, "input": "Bernoulli rate-coded spikes"
+                   "surrogate_slope": wl.slope,
+                   "input": ("Bernoulli rate-coded spikes" +
+                             (", stored as bf16 0/1" if bf16_in else ""))
                    if wl.input == "spikes" else "normal currents",
                    "includes": "forward + loss + BPTT backward + fused AdamW update"
                    if upd else "forward + loss + BPTT backward, no optimizer update",
@@ -669,7 +678,7 @@ def _async_passes(a, b, M, N, K, mn=False):
     operands M/N-contiguous."""
     if K % 8 or K < 256 or M < 256 or N < 256 or (mn and (M % 8 or N % 8)):
         return 0
-    if (a, b) in ((0, 3), (3, 0)):
+    if (a, b) in ((0, 3), (3, 0), (0, 2), (2, 0)):  # fp32 against spikes or bf16
         tiles = -(-M // 256) * -(-N // 256)
         nk = -(-K // 64)
         S = max(1, min(256 // tiles, 3 * nk // 16, 64)) if tiles < 256 else 1
@@ -740,8 +749,9 @@ def _stage_kernels(net, name, li, fp32_mfma):
                "(conv weight and input gradients)"
     if name == "synapse_fwd" and _async_contraction(net, li, fp32_mfma):
         if d.w_dtype == 0:
-            return (": widen_kernel (spikes to bf16) + split_planes_kernel (weights as 3 bf16 "
-                    "planes) + gemm_async_kernel (3 passes)")
+            widen = "widen_kernel (spikes to bf16) + " if d.in_dtype == 3 else ""
+            return (f": {widen}split_planes_kernel (weights as 3 bf16 planes) + "
+                    "gemm_async_kernel (3 passes)")
         widen = " widen_kernel (spikes to fp16) +" if d.in_dtype == 3 else ""
         return f":{widen} gemm_async_kernel"
     if name == "synapse_fwd" and _narrow_contraction(net, li, fp32_mfma):

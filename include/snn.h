@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define SNN_ABI_VERSION 10
+#define SNN_ABI_VERSION 11
 
 typedef enum snn_status {
     SNN_OK = 0,
@@ -137,7 +137,10 @@ typedef struct snn_layer_desc {
                                conv: c_in*h_in*w_in and c_out*hp*wp;
                                SNN_SYN_NONE: n_in == n_out */
     int32_t c_in, h_in, w_in, c_out; /* conv geometry, else ignored */
-    int32_t in_dtype;       /* x: SNN_U8 spikes, SNN_F32 (also SYN_NONE), SNN_F16 */
+    int32_t in_dtype;       /* x: SNN_U8 spikes, SNN_F32 (also SYN_NONE), SNN_F16,
+                               or SNN_BF16 (dense layers with SNN_F32 weights:
+                               spikes in the operand type of the three-plane
+                               contractions, no widening per call) */
     int32_t w_dtype;        /* w: SNN_F32 | SNN_F16 */
     int32_t out_dtype;      /* spikes written as SNN_U8 | SNN_F16 (0.0 / 1.0) |
                                SNN_SPK_BITS ([T,B,n_out / 8] bytes; n_out a

@@ -32,7 +32,7 @@ RESET_DETACHED, RESET_SURROGATE = 0, 1
 GRAD_FULL, GRAD_BCAST, GRAD_FOLD = 0, 1, 2
 LOSS_CE_COUNT, LOSS_MSE_COUNT = 0, 1
 FLAG_FP32_MFMA = 1
-ABI_VERSION = 10
+ABI_VERSION = 11
 DCUR_T_TRANSPOSED, DCUR_T_PLANES = 1, 2
 
 STATUS = {0: "SNN_OK", 1: "SNN_ERR_NULL", 2: "SNN_ERR_SHAPE", 3: "SNN_ERR_DTYPE",
@@ -455,7 +455,7 @@ class Network:
     then only enqueues library calls on the current stream."""
 
     def __init__(self, wl, params, device="cuda", reset_grad=RESET_DETACHED, flags=0, fold=True,
-                 spike_bits=False):
+                 spike_bits=False, input_bf16=False):
         import torch
         self.torch = torch
         self.wl = wl
@@ -466,6 +466,11 @@ class Network:
         self.W, self.b, self.v = [], [], []
         for li, spec in enumerate(wl.layers):
             in_dt = F32 if spec["kind"] == "none" else U8
+            # input_bf16: an fp32 net's input spikes given as bf16 0/1, the
+            # operand type of its three-plane contractions (no widening pass
+            # before the first layer's forward and weight gradient)
+            if li == 0 and input_bf16 and not half and spec["kind"] == "dense":
+                in_dt = BF16
             # half-precision nets hand dL/dI to the contractions in bf16, which
             # keeps fp32's exponent range for the small BPTT gradients
             d = layer_desc(spec, T, B, in_dtype=in_dt, w_dtype=F16 if half else F32,

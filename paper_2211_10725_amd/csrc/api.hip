@@ -51,7 +51,8 @@ snn_status check_desc(const snn_layer_desc *d) {
     switch (d->synapse) {
         case SNN_SYN_DENSE:
             if (d->n_in < 1 || d->n_out < 1) return SNN_ERR_SHAPE;
-            if (d->in_dtype != SNN_U8 && d->in_dtype != SNN_F32 && d->in_dtype != SNN_F16)
+            if (d->in_dtype != SNN_U8 && d->in_dtype != SNN_F32 && d->in_dtype != SNN_F16 &&
+                !(d->in_dtype == SNN_BF16 && d->w_dtype == SNN_F32))
                 return SNN_ERR_DTYPE;
             if (d->w_dtype != SNN_F32 && d->w_dtype != SNN_F16) return SNN_ERR_DTYPE;
             break;

@@ -7,7 +7,7 @@
 // or both M/N-contiguous.  Spike operands (bytes, exact in either type) are
 // first widened into the workspace.  Used for the big products of the
 // half-precision network, where every product is one MFMA pass, and for the
-// big products of spikes with an fp32 operand: that operand is held as three
+// big products of spikes (or bf16 values) with an fp32 operand: that operand is held as three
 // exact bf16 planes (hi, mid, lo; split into the workspace if given as fp32),
 // and an item's k loop runs over the planes one after the other, the smallest
 // first, each against the same spike tiles, accumulating in fp32 (three
@@ -562,11 +562,12 @@ unsigned blocks(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 bool planar(int t) { return t == SNN_F32 || t == kPlanes3; }
 
 // MFMA type of an operand pair, or -1: fp16 for spikes/fp16, bf16 for
-// spikes/bf16 and for spikes against three bf16 planes.
+// spikes/bf16 and for spikes or bf16 values against three bf16 planes (a
+// product of two bf16 values is exact in fp32).
 int mfma_type(int a, int b) {
     auto f16ish = [](int t) { return t == SNN_U8 || t == SNN_F16; };
     auto bf16ish = [](int t) { return t == SNN_U8 || t == SNN_BF16; };
-    if ((planar(a) && b == SNN_U8) || (a == SNN_U8 && planar(b))) return MT_BF16;
+    if ((planar(a) && bf16ish(b)) || (bf16ish(a) && planar(b))) return MT_BF16;
     if (a == SNN_U8 && b == SNN_U8) return MT_F16;
     if (f16ish(a) && f16ish(b)) return MT_F16;
     if (bf16ish(a) && bf16ish(b)) return MT_BF16;

@@ -134,6 +134,33 @@ def test_scan_fwd_packed_bits(neuron, alpha, beta, T, B, N):
     _assert_checkpoints(d, ck, u)
 
 
+def test_network_bf16_input_spikes():
+    """An fp32 net given its input spikes as bf16 0/1 (the operand type of
+    the three-plane contractions: no widening of the spikes per call)
+    computes what it computes from byte spikes, bit for bit, through the
+    layer calls and through the stage calls: the 784-1000-10 synaptic net at
+    full size, whose first layer's forward and weight gradient run on the
+    asynchronous kernel."""
+    wl = wls.get("dsnn_synaptic_t50_b256")
+    inp = wls.make_inputs(wl, seed=5)
+    x, lab = _t(inp["x"]), _t(inp["labels"])
+    xb = x.to(torch.bfloat16)
+    nets = [snn.Network(wl, inp["params"], device=DEV, input_bf16=f) for f in (False, True)]
+    assert nets[1].descs[0].in_dtype == snn.BF16
+    nets[0].step(x, labels=lab)
+    want = [_np(t).copy() for t in nets[0].gW + nets[0].gb + nets[0].spk +
+            [nets[0].counts, nets[0].loss[:1]]]
+    for stages in (False, True):
+        if stages:
+            nets[1].step_stages(xb, labels=lab)
+        else:
+            nets[1].step(xb, labels=lab)
+        got = [_np(t) for t in nets[1].gW + nets[1].gb + nets[1].spk +
+               [nets[1].counts, nets[1].loss[:1]]]
+        for a, b in zip(want, got):
+            np.testing.assert_array_equal(a, b)
+
+
 def test_network_packed_output_spikes():
     """A scan-only network with its spikes packed gives the unpacked
     network's spikes, counts, loss and gradients bit for bit."""
