@@ -634,7 +634,7 @@ def _contraction_kind(net, li, fp32_mfma, stage="synapse_fwd"):
         else:
             rows, cols = d.T * d.B, d.n_out
         wide = rows >= 64 and cols >= 64
-        if fp32_mfma or not wide or d.in_dtype not in (1, 3):
+        if fp32_mfma or not wide or d.in_dtype not in (1, 2, 3):
             return "mfma32", 1
         return "mfma16", _parts(d.w_dtype, d.in_dtype)
     if stage == "synapse_bwd_dw":
