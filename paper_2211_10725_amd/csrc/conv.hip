@@ -29,7 +29,9 @@
 //
 // The contractions are the library's GEMMs (exact multi-part bf16 products
 // with fp32 accumulation on the 16-bit matrix cores where they apply, fp32
-// MFMA otherwise), so every sum is deterministic.  Spikes are staged as
+// MFMA otherwise), so every sum is deterministic.  Where one image's dx^T
+// fits a workgroup's LDS (the CSNN's second layer), conv_dx_kernel computes
+// it and the gather in one pass, without dx^T in HBM (see there).  Spikes are staged as
 // bytes; an fp32 dC^T is written directly as three exact bf16 planes when the
 // weight gradient runs on the 16-bit cores.  The bias gradient comes from the
 // neuron scan's per-column sums.
@@ -321,9 +323,9 @@ __device__ inline uint32_t bf16_rne(float x) {
     return (b + 0x7fffu + ((b >> 16) & 1u)) >> 16;
 }
 
-// dC^T[co][4q .. 4q + 3] from the pooled gradient and the saved choice; with
-// `planes`, also its three exact bf16 parts (hi, mid, lo), planes Co * ldm
-// elements apart.
+// dC^T[co][4q .. 4q + 3] from the pooled gradient and the saved choice
+// (unless `dct` is null); with `planes`, also its three exact bf16 parts
+// (hi, mid, lo), planes Co * ldm elements apart.
 __global__ __launch_bounds__(kThreads) void unpool_t_kernel(int Q, int Co, int HW, int ldm,
                                                             const float *__restrict__ dI,
                                                             const uint8_t *__restrict__ arg,
@@ -340,7 +342,7 @@ __global__ __launch_bounds__(kThreads) void unpool_t_kernel(int Q, int Co, int H
 #pragma unroll
     for (int d = 0; d < 4; ++d) v[d] = (d == a) ? g : 0.f;
     const int o = co * ldm + 4 * q;
-    *reinterpret_cast<float4 *>(dct + o) = make_float4(v[0], v[1], v[2], v[3]);
+    if (dct) *reinterpret_cast<float4 *>(dct + o) = make_float4(v[0], v[1], v[2], v[3]);
     if (planes) {
         uint32_t p[3][4];
 #pragma unroll
@@ -402,6 +404,214 @@ __global__ __launch_bounds__(kThreads) void col2im_kernel(int total, int Ci, int
     dx[(img * H + yy) * W + xx] = acc;
 }
 
+// ---- input gradient in one pass ----------------------------------------------
+// When one image's product fits a workgroup (Ci * 25 <= 320, Co <= 64, at most
+// 16 pooled cells per channel, so at most 64 window rows), dx^T never reaches
+// HBM.  A workgroup takes one image at a time:
+//   dcol[m][k] = sum_co dC[m][co] w[co][k]      (16 x 16 x 32 bf16 MFMA tiles)
+// with dC[m][co] = dI[co][q] if the saved choice of (co, q) is d (m = 4 q + d),
+// else 0; dcol goes to LDS as [k][m], and dx is gathered from it as
+// col2im_kernel does (fixed order ky, kx over the window rows that exist).
+// The weights stay in registers for the whole launch as three exact bf16
+// parts (hi, mid, lo); dC is staged in LDS split the same way, and six of the
+// nine part products are summed, the smallest first.  The three left out
+// (mid lo, lo mid, lo lo) are below 2^-26 of |dC w| (|mid| <= 2^-9 |x|,
+// |lo| <= 2^-18 |x|), a quarter of an fp32 rounding, so every product is
+// fp32-accurate before the fp32 accumulation.  Eight waves: wave v takes
+// every row tile and the column tiles v, v + 8, v + 16.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kDxThreads = 512;
+constexpr int kDxMaxK = 320;                  // Ci * 25: 20 column tiles
+constexpr int kDxTileRows = 24 * 16;          // dcol^T rows the eight waves store
+constexpr int kDxMaxCo = 64;                  // two k-steps of 32
+constexpr int kDxMaxCells = 16;               // pooled cells per channel
+constexpr int kDxRows = 4 * kDxMaxCells;      // window rows: four row tiles
+constexpr int kDxLdm = kDxRows + 4;           // dcol^T row stride (floats): the
+                                              // 16-byte stores of 16 lanes, k
+                                              // apart, hit distinct bank groups
+constexpr int kDxLdc = kDxMaxCo + 8;          // dC part row stride (bf16): the
+                                              // 16-byte reads of 16 lanes, m
+                                              // apart, hit distinct bank groups
+constexpr int kDxPer = kDxMaxCo * kDxMaxCells / kDxThreads;  // (co, q) per thread
+
+// A workgroup barrier that waits for the wave's LDS accesses only: the loads
+// of the next image and the stores of dx stay in flight across it (nothing
+// in this kernel reads global memory that another wave writes).
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+__device__ inline floatx4 mfma_bf16(const u32x4 &a, const u32x4 &b, const floatx4 &c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__global__ __launch_bounds__(kDxThreads) void conv_dx_kernel(
+    int NB, int Ci, int H, int W, int Co, int Hp, int Wp, const float *__restrict__ dI,
+    const uint8_t *__restrict__ arg, const float *__restrict__ w, float *__restrict__ dx) {
+    __shared__ __attribute__((aligned(16))) float dcol[kDxTileRows * kDxLdm];
+    __shared__ __attribute__((aligned(16))) uint16_t dcp[2][3][kDxRows * kDxLdc];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int col = lane & 15, kg = lane >> 4;
+    const int HW = Hp * Wp, Kc = Ci * KS * KS, CHW = Co * HW;
+    const bool two_k = Co > 32;
+
+    // rows past 4 HW and columns past Co stay zero for the whole launch
+    for (int i = tid; i < 2 * 3 * kDxRows * kDxLdc / 2; i += kDxThreads)
+        reinterpret_cast<uint32_t *>(&dcp[0][0][0])[i] = 0u;
+
+    // B fragments of the weights: lane (col, kg) holds w[32 ks + 8 kg + e][16 nt + col]
+    // (zero past Kc and Co: the tiles there multiply zeros)
+    u32x4 bw[3][2][3];
+#pragma unroll
+    for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int n = (wv + 8 * j) * 16 + col;
+            uint32_t h[3][8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int co = ks * 32 + 8 * kg + e;
+                const float x = (n < Kc && co < Co) ? w[co * Kc + n] : 0.f;
+                h[0][e] = bf16_rne(x);
+                const float r = x - __uint_as_float(h[0][e] << 16);
+                h[1][e] = bf16_rne(r);
+                h[2][e] = bf16_rne(r - __uint_as_float(h[1][e] << 16));
+            }
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+                bw[j][ks][p] = u32x4{h[p][0] | (h[p][1] << 16), h[p][2] | (h[p][3] << 16),
+                                     h[p][4] | (h[p][5] << 16), h[p][6] | (h[p][7] << 16)};
+        }
+
+    float gnext[kDxPer];
+    int anext[kDxPer];
+    // Loads and LDS stores without branches (clamped addresses; a thread past
+    // the image writes a padding column), so the wait for the loaded values
+    // sits at their one use on every path and covers nothing issued later.
+    auto fetch = [&](int nb) {
+#pragma unroll
+        for (int r = 0; r < kDxPer; ++r) {
+            const int i = tid + r * kDxThreads;
+            const bool in = nb < NB && i < CHW;
+            const int o = min(nb, NB - 1) * CHW + min(i, CHW - 1);
+            const float g = dI[o];
+            const int a = arg[o];
+            gnext[r] = in ? g : 0.f;
+            anext[r] = in ? a : 0;
+        }
+    };
+    // dC of an image as three bf16 parts, [part][m][co]
+    auto stage = [&](uint16_t (*dst)[kDxRows * kDxLdc]) {
+#pragma unroll
+        for (int r = 0; r < kDxPer; ++r) {
+            const int i = tid + r * kDxThreads;
+            const float g = gnext[r];
+            const int a = anext[r];
+            const uint32_t hi = bf16_rne(g);
+            const float rr = g - __uint_as_float(hi << 16);
+            const uint32_t mid = bf16_rne(rr);
+            const uint32_t lo = bf16_rne(rr - __uint_as_float(mid << 16));
+            const bool in = i < CHW;
+            const int co = i / HW, q = i - co * HW;
+#pragma unroll
+            for (int d = 0; d < 4; ++d) {
+                const bool on = a == d;
+                const int o = in ? (4 * q + d) * kDxLdc + co : kDxMaxCo;  // padding of row 0
+                dst[0][o] = on ? (uint16_t)hi : (uint16_t)0;
+                dst[1][o] = on ? (uint16_t)mid : (uint16_t)0;
+                dst[2][o] = on ? (uint16_t)lo : (uint16_t)0;
+            }
+        }
+    };
+
+    // Per image n: products from dcp[n & 1]; barrier (the gather of n - 1 is
+    // done with dcol); dcol stored; image n + 1 staged into the other buffer;
+    // barrier; gather.  The loads of n + 1 are issued before the products of
+    // n and the stores of dx drain under the next products, so no wait for
+    // global memory lands between two barriers.
+    fetch(blockIdx.x);
+    lds_barrier();  // the zeroed buffers
+    stage(dcp[0]);
+    lds_barrier();
+    const int HWi = H * W, npix = Ci * HWi;
+    int buf = 0;
+    for (int nb = blockIdx.x; nb < NB; nb += gridDim.x, buf ^= 1) {
+        fetch(nb + gridDim.x);
+
+        floatx4 acc[4][3];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 3; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+        const uint16_t(*src)[kDxRows * kDxLdc] = dcp[buf];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            if (ks == 1 && !two_k) break;
+            // A fragments: lane (col, kg) holds dC[16 mt + col][32 ks + 8 kg + e]
+            u32x4 ap[4][3];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int p = 0; p < 3; ++p)
+                    ap[i][p] = *reinterpret_cast<const u32x4 *>(
+                        &src[p][(16 * i + col) * kDxLdc + 32 * ks + 8 * kg]);
+            // part products smallest first (mid mid, lo hi, hi lo, mid hi, hi mid,
+            // hi hi); the twelve tiles interleave
+            constexpr int pa[6] = {1, 2, 0, 1, 0, 0}, pb[6] = {1, 0, 2, 0, 1, 0};
+#pragma unroll
+            for (int t = 0; t < 6; ++t)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 3; ++j)
+                        acc[i][j] = mfma_bf16(ap[i][pa[t]], bw[j][ks][pb[t]], acc[i][j]);
+        }
+        lds_barrier();  // the gather of the previous image is done with dcol
+        // D fragment: lane (col, kg) holds dcol[16 mt + 4 kg + r][16 nt + col], r = 0..3,
+        // stored as dcol^T[k][m], four consecutive m in one 16-byte store
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 3; ++j)
+                *reinterpret_cast<floatx4 *>(dcol + ((wv + 8 * j) * 16 + col) * kDxLdm + 16 * i +
+                                             4 * kg) = acc[i][j];
+        stage(dcp[buf ^ 1]);
+        lds_barrier();
+        // every load of an output's 25 taps is issued before the first add (a
+        // tap outside the windows reads a valid element that is not added)
+        float *dxi = dx + (int64_t)nb * npix;
+        for (int idx = tid; idx < npix; idx += kDxThreads) {
+            const int c = idx / HWi, rr = idx - c * HWi, y = rr / W, xx = rr - y * W;
+            const float *dc = dcol + c * KS * KS * kDxLdm;
+            int ry[KS], cx[KS];
+            bool vy[KS], vx[KS];
+#pragma unroll
+            for (int k = 0; k < KS; ++k) {
+                const int oy = y - k, ox = xx - k;
+                vy[k] = oy >= 0 && oy < 2 * Hp;
+                vx[k] = ox >= 0 && ox < 2 * Wp;
+                ry[k] = vy[k] ? 4 * (oy >> 1) * Wp + 2 * (oy & 1) : 0;
+                cx[k] = vx[k] ? 4 * (ox >> 1) + (ox & 1) : 0;
+            }
+            float v[KS * KS];
+#pragma unroll
+            for (int ky = 0; ky < KS; ++ky)
+#pragma unroll
+                for (int kx = 0; kx < KS; ++kx)
+                    v[ky * KS + kx] = dc[(ky * KS + kx) * kDxLdm + ry[ky] + cx[kx]];
+            float s = 0.f;
+#pragma unroll
+            for (int ky = 0; ky < KS; ++ky)
+#pragma unroll
+                for (int kx = 0; kx < KS; ++kx)
+                    if (vy[ky] && vx[kx]) s += v[ky * KS + kx];
+            dxi[idx] = s;
+        }
+    }
+}
+
 // Weight gradient of a layer with few inputs per channel (Kc = Ci * 25 = KC
 // <= 50: the network's input layer), straight from the pool's selection:
 //   dW[co][k] = sum over pooled cells of dI times x under the selected output.
@@ -457,6 +667,12 @@ int small_dw_chunks(const ConvGeom &g, int64_t Q) {
 }
 
 bool small_dw(const ConvGeom &g) { return g.Ci * KS * KS <= 50; }
+
+// the input gradient by conv_dx_kernel (16-bit cores: not under fp32-only MFMA)
+bool dx_one_pass(const ConvGeom &g, bool allow_split) {
+    return allow_split && g.Ci * KS * KS <= kDxMaxK && g.Co <= kDxMaxCo &&
+           g.Hp * g.Wp <= kDxMaxCells;
+}
 
 unsigned blocks(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 
@@ -644,10 +860,13 @@ hipError_t launch_conv_pool_bwd(const ConvGeom &g, const float *dI, const uint8_
     char *rest = base + l.dct;
     const size_t rest_bytes = ws_bytes - l.dct;
     hipError_t e;
-    if (grad_x || (grad_w && !l.small)) {
+    const bool dx1 = grad_x && dx_one_pass(g, allow_split);
+    // dC^T in fp32 feeds the two-pass input gradient and an fp32 weight gradient
+    const bool need_dct = (grad_x && !dx1) || (grad_w && !l.small && l.planes == 0);
+    if ((grad_x && !dx1) || (grad_w && !l.small)) {
         uint16_t *planes = (grad_w && l.planes > 0) ? reinterpret_cast<uint16_t *>(rest) : nullptr;
-        unpool_t_kernel<<<blocks(v.Q * g.Co), kThreads, 0, s>>>((int)v.Q, g.Co, g.Hp * g.Wp,
-                                                                (int)v.ldm, dI, arg, dct, planes);
+        unpool_t_kernel<<<blocks(v.Q * g.Co), kThreads, 0, s>>>(
+            (int)v.Q, g.Co, g.Hp * g.Wp, (int)v.ldm, dI, arg, need_dct ? dct : nullptr, planes);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -670,6 +889,12 @@ hipError_t launch_conv_pool_bwd(const ConvGeom &g, const float *dI, const uint8_
         a.B = colt; a.C = grad_w; a.bias = nullptr;
         e = launch_gemm(a, colt + l.colt, rest_bytes - l.planes - l.colt, s);
         if (e != hipSuccess) return e;
+    }
+    if (dx1) {
+        const unsigned grid = (unsigned)min(g.NB, device_cus());
+        conv_dx_kernel<<<grid, kDxThreads, 0, s>>>(g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, dI, arg,
+                                                   reinterpret_cast<const float *>(w), grad_x);
+        return hipGetLastError();
     }
     if (grad_x) {
         float *dxt = reinterpret_cast<float *>(rest);

@@ -826,9 +826,18 @@ def test_conv_pool_ties_first_maximum():
     assert (a[0] == 0).all()
 
 
-# (3, 8, 11, 12, 16): an odd conv row outside every window
+# (3, 8, 11, 12, 16): an odd conv row outside every window.  The input
+# gradient runs in one pass when Ci * 25 <= 320, Co <= 64 and at most 16
+# pooled cells per channel: (4, 12, 12, 12, 64) and (300, ...) at the limits
+# (more images than compute units: a workgroup takes several), (2, 3, 9, 11,
+# 5) and (3, 8, 11, 12, 16) ragged, (5, 7, 12, 12, 33) half of the second
+# k-step; past each limit the gather-and-contraction path: 144 cells (one
+# input channel), 25 cells (2, 4, 14, 14, 8), 70 output channels and
+# 13 * 25 = 325 inputs per channel.
 @pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (4, 12, 12, 12, 64), (2, 3, 9, 11, 5),
-                                          (3, 8, 11, 12, 16), (300, 12, 12, 12, 64)])
+                                          (3, 8, 11, 12, 16), (300, 12, 12, 12, 64),
+                                          (5, 7, 12, 12, 33), (2, 4, 14, 14, 8), (2, 2, 8, 8, 70),
+                                          (2, 13, 9, 9, 8)])
 def test_conv_pool_bwd(NB, Ci, H, W, Co):
     """Backward given the oracle's pool selection (one byte per pooled current)."""
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=7 * NB + Co)
@@ -846,6 +855,11 @@ def test_conv_pool_bwd(NB, Ci, H, W, Co):
     rW, _, rx = oracle.conv_bwd(dY, x, w)
     assert_close(_np(gW), rW, 1e-3, what="conv dW")
     assert_close(_np(gx), rx, 1e-3, what="conv dx")
+    # fp32 accuracy: dx^T sums at most six part products per output channel
+    # (each within 2^-26 of the exact product), col2im at most 25 of those
+    terms = oracle.conv_bwd(np.abs(dY), x, np.abs(w))[2]
+    bound = ((6 * Co + 27) * 2.0 ** -24 + 2.0 ** -26) * terms
+    assert (np.abs(_np(gx) - rx) <= bound + 1e-30).all()
 
 
 # ---------------------------------------------------------------------------
