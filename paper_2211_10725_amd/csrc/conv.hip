@@ -447,6 +447,7 @@ __device__ inline floatx4 mfma_bf16(const u32x4 &a, const u32x4 &b, const floatx
                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+template <int G>
 __global__ __launch_bounds__(kDxThreads) void conv_dx_kernel(
     int NB, int Ci, int H, int W, int Co, int Hp, int Wp, const float *__restrict__ dI,
     const uint8_t *__restrict__ arg, const float *__restrict__ w, float *__restrict__ dx) {
@@ -457,9 +458,34 @@ __global__ __launch_bounds__(kDxThreads) void conv_dx_kernel(
     const int HW = Hp * Wp, Kc = Ci * KS * KS, CHW = Co * HW;
     const bool two_k = Co > 32;
 
-    // rows past 4 HW and columns past Co stay zero for the whole launch
+    // rows past 4 HW and columns past Co stay zero for the whole launch, and
+    // so do the padding columns m = 64..67 of dcol^T, which the gather reads
+    // for a tap outside the windows
     for (int i = tid; i < 2 * 3 * kDxRows * kDxLdc / 2; i += kDxThreads)
         reinterpret_cast<uint32_t *>(&dcp[0][0][0])[i] = 0u;
+    for (int i = tid; i < kDxTileRows * (kDxLdm - kDxRows); i += kDxThreads)
+        dcol[(i >> 2) * kDxLdm + kDxRows + (i & 3)] = 0.f;
+
+    // Gather: thread (cg, p) < (G, H * W) takes pixel p of channels cg + G j.
+    // Its 25 taps read dcol^T[(c * 25 + t)][m_t] for the window row m_t under
+    // the tap, or the zero padding; tap[t] holds the offset for c = cg.
+    const int HWi = H * W, npix = Ci * HWi;
+    const bool gact = tid < G * HWi;
+    const int cg = gact ? tid / HWi : 0, pix = gact ? tid - cg * HWi : 0;
+    int tap[KS * KS];
+    {
+        const int y = pix / W, xx = pix - (pix / W) * W;
+#pragma unroll
+        for (int ky = 0; ky < KS; ++ky)
+#pragma unroll
+            for (int kx = 0; kx < KS; ++kx) {
+                const int oy = y - ky, ox = xx - kx;
+                const bool ok = oy >= 0 && oy < 2 * Hp && ox >= 0 && ox < 2 * Wp;
+                const int m = ok ? 4 * ((oy >> 1) * Wp + (ox >> 1)) + 2 * (oy & 1) + (ox & 1)
+                                 : kDxRows;
+                tap[ky * KS + kx] = (cg * KS * KS + ky * KS + kx) * kDxLdm + m;
+            }
+    }
 
     // B fragments of the weights: lane (col, kg) holds w[32 ks + 8 kg + e][16 nt + col]
     // (zero past Kc and Co: the tiles there multiply zeros)
@@ -535,7 +561,6 @@ __global__ __launch_bounds__(kDxThreads) void conv_dx_kernel(
     lds_barrier();  // the zeroed buffers
     stage(dcp[0]);
     lds_barrier();
-    const int HWi = H * W, npix = Ci * HWi;
     int buf = 0;
     for (int nb = blockIdx.x; nb < NB; nb += gridDim.x, buf ^= 1) {
         fetch(nb + gridDim.x);
@@ -579,35 +604,22 @@ __global__ __launch_bounds__(kDxThreads) void conv_dx_kernel(
                                              4 * kg) = acc[i][j];
         stage(dcp[buf ^ 1]);
         lds_barrier();
-        // every load of an output's 25 taps is issued before the first add (a
-        // tap outside the windows reads a valid element that is not added)
-        float *dxi = dx + (int64_t)nb * npix;
-        for (int idx = tid; idx < npix; idx += kDxThreads) {
-            const int c = idx / HWi, rr = idx - c * HWi, y = rr / W, xx = rr - y * W;
-            const float *dc = dcol + c * KS * KS * kDxLdm;
-            int ry[KS], cx[KS];
-            bool vy[KS], vx[KS];
+        // fixed order t = 5 ky + kx; a tap outside the windows adds the zero padding
+        if (gact) {
+            float *dxi = dx + (int64_t)nb * npix + pix;
 #pragma unroll
-            for (int k = 0; k < KS; ++k) {
-                const int oy = y - k, ox = xx - k;
-                vy[k] = oy >= 0 && oy < 2 * Hp;
-                vx[k] = ox >= 0 && ox < 2 * Wp;
-                ry[k] = vy[k] ? 4 * (oy >> 1) * Wp + 2 * (oy & 1) : 0;
-                cx[k] = vx[k] ? 4 * (ox >> 1) + (ox & 1) : 0;
+            for (int j = 0; j < (kDxMaxK / (KS * KS) + G - 1) / G; ++j) {
+                const int c = cg + G * j;
+                if (c >= Ci) break;
+                const float *dc = dcol + G * j * KS * KS * kDxLdm;
+                float v[KS * KS];
+#pragma unroll
+                for (int t = 0; t < KS * KS; ++t) v[t] = dc[tap[t]];
+                float acc = 0.f;
+#pragma unroll
+                for (int t = 0; t < KS * KS; ++t) acc += v[t];
+                dxi[c * HWi] = acc;
             }
-            float v[KS * KS];
-#pragma unroll
-            for (int ky = 0; ky < KS; ++ky)
-#pragma unroll
-                for (int kx = 0; kx < KS; ++kx)
-                    v[ky * KS + kx] = dc[(ky * KS + kx) * kDxLdm + ry[ky] + cx[kx]];
-            float s = 0.f;
-#pragma unroll
-            for (int ky = 0; ky < KS; ++ky)
-#pragma unroll
-                for (int kx = 0; kx < KS; ++kx)
-                    if (vy[ky] && vx[kx]) s += v[ky * KS + kx];
-            dxi[idx] = s;
         }
     }
 }
@@ -671,7 +683,7 @@ bool small_dw(const ConvGeom &g) { return g.Ci * KS * KS <= 50; }
 // the input gradient by conv_dx_kernel (16-bit cores: not under fp32-only MFMA)
 bool dx_one_pass(const ConvGeom &g, bool allow_split) {
     return allow_split && g.Ci * KS * KS <= kDxMaxK && g.Co <= kDxMaxCo &&
-           g.Hp * g.Wp <= kDxMaxCells;
+           g.Hp * g.Wp <= kDxMaxCells && g.H * g.W <= kDxThreads;
 }
 
 unsigned blocks(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
@@ -892,8 +904,17 @@ hipError_t launch_conv_pool_bwd(const ConvGeom &g, const float *dI, const uint8_
     }
     if (dx1) {
         const unsigned grid = (unsigned)min(g.NB, device_cus());
-        conv_dx_kernel<<<grid, kDxThreads, 0, s>>>(g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, dI, arg,
-                                                   reinterpret_cast<const float *>(w), grad_x);
+        const int hw = g.H * g.W;  // at most 259 under dx_one_pass
+        const float *wf = reinterpret_cast<const float *>(w);
+        if (3 * hw <= kDxThreads)
+            conv_dx_kernel<3><<<grid, kDxThreads, 0, s>>>(g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp,
+                                                          dI, arg, wf, grad_x);
+        else if (2 * hw <= kDxThreads)
+            conv_dx_kernel<2><<<grid, kDxThreads, 0, s>>>(g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp,
+                                                          dI, arg, wf, grad_x);
+        else
+            conv_dx_kernel<1><<<grid, kDxThreads, 0, s>>>(g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp,
+                                                          dI, arg, wf, grad_x);
         return hipGetLastError();
     }
     if (grad_x) {
