@@ -624,6 +624,170 @@ __global__ __launch_bounds__(kDxThreads) void conv_dx_kernel(
     }
 }
 
+// ---- weight gradient in one pass ---------------------------------------------
+// For the same layers, on spike input: a workgroup takes one image at a time
+// and accumulates, over all its images,
+//   dW[co][k] = sum_m dC^T[co][m] col[m][k]       (16 x 16 x 32 bf16 MFMA tiles)
+// with dC^T staged in LDS as three exact bf16 parts ([part][co][m]: four
+// window rows of a pooled cell are one 8-byte store) and col[m][k] read
+// straight from the image, staged in LDS as bf16 0 / 1: lane (n, g) of a
+// B fragment takes the 8 window rows 32 s + 8 g .. + 7, two pooled cells of
+// four positions (x offsets 0, 1, W, W + 1 from the cell's corner under tap
+// k).  The three part products per tile are exact and summed smallest first
+// in fp32; each workgroup writes its partial sums, which splitk_reduce adds
+// in a fixed order.  Eight waves: wave v takes every output-channel tile and
+// the k tiles v, v + 8, v + 16.  The image and the parts of the next image
+// are loaded during the products and staged after a barrier.
+constexpr int kDwMaxGrid = 256;                   // partial sums written
+constexpr int kDwLdm = kDxRows + 8;               // dC^T part row stride (bf16): the
+                                                  // 16-byte reads of 16 lanes, co
+                                                  // apart, hit distinct bank groups
+constexpr int kDwMaxX = kDxMaxK / (KS * KS) * kDxThreads;  // image elements staged
+constexpr int kDwXPer = kDwMaxX / kDxThreads;     // image bytes loaded per thread
+
+__global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
+    int NB, int Ci, int H, int W, int Co, int Hp, int Wp, const float *__restrict__ dI,
+    const uint8_t *__restrict__ arg, const uint8_t *__restrict__ x, float *__restrict__ partial) {
+    __shared__ __attribute__((aligned(16))) uint16_t dct[3][kDxMaxCo * kDwLdm];
+    __shared__ __attribute__((aligned(16))) uint16_t xs[kDwMaxX];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int col = lane & 15, kg = lane >> 4;
+    const int HW = Hp * Wp, Kc = Ci * KS * KS, CHW = Co * HW, HWi = H * W, npx = Ci * HWi;
+    const bool two_m = HW > 8;  // window rows past 32
+
+    // window rows past 4 HW and channels past Co stay zero for the whole launch
+    for (int i = tid; i < 3 * kDxMaxCo * kDwLdm / 2; i += kDxThreads)
+        reinterpret_cast<uint32_t *>(&dct[0][0])[i] = 0u;
+
+    // per lane: the image offset of its k under each of its k tiles (k past Kc
+    // reads a valid element; those output columns are not stored), and the
+    // corner of its two pooled cells per 32 window rows (cells past HW read
+    // element 0: their dC^T rows are zero)
+    int koff[3], cb[2][2];
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+        const int k = (wv + 8 * j) * 16 + col;
+        const int c = k / (KS * KS), t = k - c * KS * KS, ky = t / KS, kx = t - ky * KS;
+        koff[j] = k < Kc ? c * HWi + ky * W + kx : 0;
+    }
+#pragma unroll
+    for (int ms = 0; ms < 2; ++ms)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int q = 8 * ms + 2 * kg + h, py = q / Wp, px = q - py * Wp;
+            cb[ms][h] = q < HW ? 2 * py * W + 2 * px : 0;
+        }
+
+    float gnext[kDxPer];
+    int anext[kDxPer];
+    uint32_t xnext[kDwXPer];
+    auto fetch = [&](int nb) {
+        const int b = min(nb, NB - 1);
+#pragma unroll
+        for (int r = 0; r < kDxPer; ++r) {
+            const int i = tid + r * kDxThreads;
+            const int o = b * CHW + min(i, CHW - 1);
+            const float g = dI[o];
+            const int a = arg[o];
+            gnext[r] = (nb < NB && i < CHW) ? g : 0.f;
+            anext[r] = a;
+        }
+#pragma unroll
+        for (int r = 0; r < kDwXPer; ++r) {
+            const int i = tid + r * kDxThreads;
+            if (r * kDxThreads < npx) xnext[r] = x[(int64_t)b * npx + min(i, npx - 1)];
+        }
+    };
+    auto stage = [&]() {
+#pragma unroll
+        for (int r = 0; r < kDxPer; ++r) {
+            const int i = tid + r * kDxThreads;
+            const float g = gnext[r];
+            const uint32_t hi = bf16_rne(g);
+            const float rr = g - __uint_as_float(hi << 16);
+            const uint32_t mid = bf16_rne(rr);
+            const uint32_t lo = bf16_rne(rr - __uint_as_float(mid << 16));
+            const uint32_t pv[3] = {hi, mid, lo};
+            if (i < CHW) {
+                const int co = i / HW, q = i - co * HW, a = anext[r];
+#pragma unroll
+                for (int p = 0; p < 3; ++p) {
+                    const uint32_t v = pv[p];
+                    const uint2 w2 = make_uint2((a == 0 ? v : 0u) | ((a == 1 ? v : 0u) << 16),
+                                                (a == 2 ? v : 0u) | ((a == 3 ? v : 0u) << 16));
+                    *reinterpret_cast<uint2 *>(&dct[p][co * kDwLdm + 4 * q]) = w2;
+                }
+            }
+        }
+#pragma unroll
+        for (int r = 0; r < kDwXPer; ++r) {
+            const int i = tid + r * kDxThreads;
+            if (r * kDxThreads < npx && i < npx) xs[i] = (uint16_t)(__float_as_uint((float)xnext[r]) >> 16);  // exact
+        }
+    };
+
+    floatx4 acc[4][3];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 3; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    fetch(blockIdx.x);
+    lds_barrier();  // the zeroed parts
+    stage();
+    lds_barrier();
+    for (int nb = blockIdx.x; nb < NB; nb += gridDim.x) {
+        fetch(nb + gridDim.x);
+#pragma unroll
+        for (int ms = 0; ms < 2; ++ms) {
+            if (ms == 1 && !two_m) break;
+            // B fragments: lane (col, kg) holds col[32 ms + 8 kg + e][16 kt + col]
+            u32x4 bx[3];
+#pragma unroll
+            for (int j = 0; j < 3; ++j) {
+                uint32_t h4[4];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const uint16_t *p = xs + koff[j] + cb[ms][h];
+                    h4[2 * h] = (uint32_t)p[0] | ((uint32_t)p[1] << 16);
+                    h4[2 * h + 1] = (uint32_t)p[W] | ((uint32_t)p[W + 1] << 16);
+                }
+                bx[j] = u32x4{h4[0], h4[1], h4[2], h4[3]};
+            }
+            // A fragments: lane (col, kg) holds dC^T[16 ct + col][32 ms + 8 kg + e]
+#pragma unroll
+            for (int p = 2; p >= 0; --p) {
+                u32x4 ap[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    ap[i] = *reinterpret_cast<const u32x4 *>(
+                        &dct[p][(16 * i + col) * kDwLdm + 32 * ms + 8 * kg]);
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 3; ++j) acc[i][j] = mfma_bf16(ap[i], bx[j], acc[i][j]);
+            }
+        }
+        lds_barrier();  // every wave is done with the parts and the image
+        stage();
+        lds_barrier();
+    }
+    // D fragment: lane (col, kg) holds dW[16 ct + 4 kg + r][16 kt + col]
+    float *out = partial + (int64_t)blockIdx.x * Co * Kc;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+        const int k = (wv + 8 * j) * 16 + col;
+        if (k >= Kc) continue;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int co = 16 * i + 4 * kg + r;
+                if (co < Co) out[co * Kc + k] = acc[i][j][r];
+            }
+    }
+}
+
 // Weight gradient of a layer with few inputs per channel (Kc = Ci * 25 = KC
 // <= 50: the network's input layer), straight from the pool's selection:
 //   dW[co][k] = sum over pooled cells of dI times x under the selected output.
@@ -686,6 +850,11 @@ bool dx_one_pass(const ConvGeom &g, bool allow_split) {
            g.Hp * g.Wp <= kDxMaxCells && g.H * g.W <= kDxThreads;
 }
 
+// the weight gradient by conv_dw_kernel (spike input, exact in bf16)
+bool dw_one_pass(const ConvGeom &g, int in_dtype, bool allow_split) {
+    return in_dtype == SNN_U8 && dx_one_pass(g, allow_split);
+}
+
 unsigned blocks(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
 
 // ---- plans and workspace ----------------------------------------------------
@@ -730,18 +899,23 @@ size_t gemm_ws(const GemmArgs &a) {
 }
 
 struct BwdLayout {
-    bool small;  // weight gradient by conv_dw_small_kernel
-    int chunks;  // its cell chunks per channel
+    bool one_pass;  // weight gradient by conv_dw_kernel
+    bool small;     // weight gradient by conv_dw_small_kernel
+    int chunks;     // the partial sums of either
     size_t dct, partial, planes, colt, dw_gemm, dxt, dx_gemm;
-    size_t dw_phase() const { return small ? partial : planes + colt + dw_gemm; }
+    size_t dw_phase() const { return one_pass || small ? partial : planes + colt + dw_gemm; }
     size_t dx_phase() const { return dxt + dx_gemm; }
 };
 
 BwdLayout bwd_layout(const ConvGeom &g, const ConvDims &v, int in_dtype, bool allow_split) {
     BwdLayout l{};
-    l.small = small_dw(g);
+    l.one_pass = dw_one_pass(g, in_dtype, allow_split);
+    l.small = !l.one_pass && small_dw(g);
     l.dct = align_up((size_t)g.Co * v.ldm * sizeof(float));
-    if (l.small) {
+    if (l.one_pass) {
+        l.chunks = min(g.NB, kDwMaxGrid);
+        l.partial = align_up((size_t)l.chunks * g.Co * v.Kc * sizeof(float));
+    } else if (l.small) {
         l.chunks = small_dw_chunks(g, v.Q);
         l.partial = align_up((size_t)l.chunks * g.Co * v.Kc * sizeof(float));
     } else {
@@ -873,16 +1047,26 @@ hipError_t launch_conv_pool_bwd(const ConvGeom &g, const float *dI, const uint8_
     const size_t rest_bytes = ws_bytes - l.dct;
     hipError_t e;
     const bool dx1 = grad_x && dx_one_pass(g, allow_split);
+    const bool dw_gemm = grad_w && !l.one_pass && !l.small;
     // dC^T in fp32 feeds the two-pass input gradient and an fp32 weight gradient
-    const bool need_dct = (grad_x && !dx1) || (grad_w && !l.small && l.planes == 0);
-    if ((grad_x && !dx1) || (grad_w && !l.small)) {
-        uint16_t *planes = (grad_w && l.planes > 0) ? reinterpret_cast<uint16_t *>(rest) : nullptr;
+    const bool need_dct = (grad_x && !dx1) || (dw_gemm && l.planes == 0);
+    if ((grad_x && !dx1) || dw_gemm) {
+        uint16_t *planes = (dw_gemm && l.planes > 0) ? reinterpret_cast<uint16_t *>(rest) : nullptr;
         unpool_t_kernel<<<blocks(v.Q * g.Co), kThreads, 0, s>>>(
             (int)v.Q, g.Co, g.Hp * g.Wp, (int)v.ldm, dI, arg, need_dct ? dct : nullptr, planes);
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (grad_w && l.small) {
+    if (grad_w && l.one_pass) {
+        float *partial = reinterpret_cast<float *>(rest);
+        conv_dw_kernel<<<(unsigned)l.chunks, kDxThreads, 0, s>>>(
+            g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, dI, arg, reinterpret_cast<const uint8_t *>(x),
+            partial);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        e = launch_splitk_reduce(g.Co, v.Kc, l.chunks, partial, grad_w, v.Kc, nullptr, s);
+        if (e != hipSuccess) return e;
+    } else if (grad_w && l.small) {
         float *partial = reinterpret_cast<float *>(rest);
         if (in_dtype == SNN_U8) launch_dw_small<uint8_t>(g, v, l.chunks, dI, arg, x, partial, s);
         else launch_dw_small<float>(g, v, l.chunks, dI, arg, x, partial, s);

@@ -826,18 +826,20 @@ def test_conv_pool_ties_first_maximum():
     assert (a[0] == 0).all()
 
 
-# (3, 8, 11, 12, 16): an odd conv row outside every window.  The input
-# gradient runs in one pass when Ci * 25 <= 320, Co <= 64 and at most 16
-# pooled cells per channel: (4, 12, 12, 12, 64) and (300, ...) at the limits
-# (more images than compute units: a workgroup takes several), (2, 3, 9, 11,
-# 5) and (3, 8, 11, 12, 16) ragged, (5, 7, 12, 12, 33) half of the second
-# k-step; past each limit the gather-and-contraction path: 144 cells (one
-# input channel), 25 cells (2, 4, 14, 14, 8), 70 output channels and
-# 13 * 25 = 325 inputs per channel.
+# (3, 8, 11, 12, 16): an odd conv row outside every window.  Both gradients
+# run in one pass each when Ci * 25 <= 320, Co <= 64 and at most 16 pooled
+# cells per channel: (4, 12, 12, 12, 64) and (300, ...) at the limits (more
+# images than compute units: a workgroup takes several), (2, 3, 9, 11, 5)
+# and (3, 8, 11, 12, 16) ragged (6 cells: one 32-row step), (5, 7, 12, 12,
+# 33) half of the second k-step, (3, 5, 9, 21, 24) and (2, 4, 7, 37, 40)
+# images of 189 and 259 pixels (two and one channel groups in the gather);
+# past each limit the gather-and-contraction path: 144 cells (one input
+# channel), 25 cells (2, 4, 14, 14, 8), 70 output channels and 13 * 25 = 325
+# inputs per channel.
 @pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (4, 12, 12, 12, 64), (2, 3, 9, 11, 5),
                                           (3, 8, 11, 12, 16), (300, 12, 12, 12, 64),
-                                          (5, 7, 12, 12, 33), (2, 4, 14, 14, 8), (2, 2, 8, 8, 70),
-                                          (2, 13, 9, 9, 8)])
+                                          (5, 7, 12, 12, 33), (3, 5, 9, 21, 24), (2, 4, 7, 37, 40),
+                                          (2, 4, 14, 14, 8), (2, 2, 8, 8, 70), (2, 13, 9, 9, 8)])
 def test_conv_pool_bwd(NB, Ci, H, W, Co):
     """Backward given the oracle's pool selection (one byte per pooled current)."""
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=7 * NB + Co)
@@ -856,10 +858,35 @@ def test_conv_pool_bwd(NB, Ci, H, W, Co):
     assert_close(_np(gW), rW, 1e-3, what="conv dW")
     assert_close(_np(gx), rx, 1e-3, what="conv dx")
     # fp32 accuracy: dx^T sums at most six part products per output channel
-    # (each within 2^-26 of the exact product), col2im at most 25 of those
-    terms = oracle.conv_bwd(np.abs(dY), x, np.abs(w))[2]
-    bound = ((6 * Co + 27) * 2.0 ** -24 + 2.0 ** -26) * terms
+    # (each within 2^-26 of the exact product), col2im at most 25 of those;
+    # dW sums three exact part products per window row
+    tW, _, tx = oracle.conv_bwd(np.abs(dY), x, np.abs(w))
+    bound = ((6 * Co + 27) * 2.0 ** -24 + 2.0 ** -26) * tx
     assert (np.abs(_np(gx) - rx) <= bound + 1e-30).all()
+    Mw = 4 * NB * (Ho // 2) * (Wo // 2)
+    assert (np.abs(_np(gW) - rW) <= (3 * Mw + 2) * 2.0 ** -24 * tW + 1e-30).all()
+
+
+@pytest.mark.parametrize("NB,Ci,H,W,Co", [(4, 6, 12, 12, 20), (3, 2, 28, 28, 12)])
+def test_conv_pool_bwd_real_input(NB, Ci, H, W, Co):
+    """Real-valued input: the weight gradient runs on the contraction path
+    (the one-pass kernel takes spikes only), the input gradient in one pass
+    where the image fits."""
+    x, w, b, _ = _conv_case(NB, Ci, H, W, Co, seed=5 * NB + Ci)
+    x = np.random.default_rng(Co).uniform(-1, 1, x.shape).astype(np.float32)
+    spec = dict(kind="conv", c_in=Ci, h=H, w=W, c_out=Co, neuron="leaky", beta=0.5)
+    d = snn.layer_desc(spec, 1, NB, in_dtype=snn.F32)
+    y32 = oracle.conv_fwd(x, w, b).astype(np.float32).astype(np.float64)
+    _, arg = oracle.maxpool2_fwd(y32)
+    dI = np.random.default_rng(2).normal(0, 1, arg.shape).astype(np.float32)
+    gW = torch.empty(w.shape, dtype=torch.float32, device=DEV)
+    gx = torch.empty(x.shape, dtype=torch.float32, device=DEV)
+    ws = _ws(snn.snn_layer_workspace_bytes(d))
+    snn.snn_synapse_bwd(d, _t(dI), _t(arg.astype(np.uint8)), _t(x), _t(w), gW, gx, ws)
+    dY = oracle.maxpool2_bwd(dI, arg, H - 4, W - 4)
+    rW, _, rx = oracle.conv_bwd(dY, x, w)
+    assert_close(_np(gW), rW, 1e-3, what="conv dW")
+    assert_close(_np(gx), rx, 1e-3, what="conv dx")
 
 
 # ---------------------------------------------------------------------------
