@@ -650,8 +650,21 @@ def _contraction_kind(net, li, fp32_mfma, stage="synapse_fwd"):
         a, b = d.grad_dtype, d.w_dtype
         p = _parts(a, b) * _parts(b, a)
         return ("mfma16", p) if p <= 6 else ("mfma32", 1)
-    # conv backward: dW on the 16-bit cores (three planes of dC), dx on fp32 MFMA
+    # conv backward: one-pass kernels on the 16-bit cores (dW 3 exact passes,
+    # dx 6 part products) where the image fits, else the fp32 contractions
+    if _conv_one_pass(net, li, fp32_mfma) and d.in_dtype == 3:
+        return "mfma16", (4.5 if li > 0 and net.gx[li] is not None else 3)
     return "mfma32", 1
+
+
+def _conv_one_pass(net, li, fp32_mfma):
+    """Whether layer li's conv backward runs as conv_dx_kernel (and, on spike
+    input, conv_dw_kernel): mirrors dx_one_pass in conv.hip (at most 12 input
+    and 64 output channels, 16 pooled cells per channel, 512 pixels)."""
+    d = net.descs[li]
+    hp, wp = (d.h_in - 4) // 2, (d.w_in - 4) // 2
+    return (d.synapse == 1 and not fp32_mfma and d.c_in * 25 <= 320 and d.c_out <= 64
+            and hp * wp <= 16 and d.h_in * d.w_in <= 512)
 
 
 def _direct_conv(net, li):
@@ -745,8 +758,19 @@ def _stage_kernels(net, name, li, fp32_mfma):
         return f": {pre}{gemm} ({passes} pass{'es' if passes > 1 else ''}, " \
                "+ splitk_reduce_kernel when split over K)"
     if name == "synapse_bwd":
-        return ": unpool_t_kernel + im2col_t_kernel + contractions + col2im_kernel " \
-               "(conv weight and input gradients)"
+        one = _conv_one_pass(net, li, fp32_mfma)
+        if one and d.in_dtype == 3:
+            dw = "conv_dw_kernel + splitk_reduce_wide_kernel"
+        elif d.c_in * 25 <= 50:
+            dw = "conv_dw_small_kernel + splitk_reduce_wide_kernel"
+        else:
+            dw = "unpool_t_kernel + im2col_t_kernel + contraction"
+        if not (li > 0 and net.gx[li] is not None):
+            return f": {dw} (conv weight gradient)"
+        if not one:
+            return (": unpool_t_kernel + im2col_t_kernel + contractions + col2im_kernel "
+                    "(conv weight and input gradients)")
+        return f": {dw} + conv_dx_kernel (conv weight and input gradients)"
     if name == "synapse_fwd" and _async_contraction(net, li, fp32_mfma):
         if d.w_dtype == 0:
             widen = "widen_kernel (spikes to bf16) + " if d.in_dtype == 3 else ""
