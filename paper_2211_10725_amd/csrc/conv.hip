@@ -678,51 +678,55 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
             cb[ms][h] = q < HW ? 2 * py * W + 2 * px : 0;
         }
 
-    float gnext[kDxPer];
-    int anext[kDxPer];
-    uint32_t xnext[kDwXPer];
-    auto fetch = [&](int nb) {
+    // The loads of an image are issued two images ahead, into one of two
+    // register sets, so a whole image's products hide their latency.
+    struct Next {
+        float g[kDxPer];
+        int a[kDxPer];
+        uint32_t x[kDwXPer];
+    };
+    auto fetch = [&](Next &n, int nb) {
         const int b = min(nb, NB - 1);
 #pragma unroll
         for (int r = 0; r < kDxPer; ++r) {
             const int i = tid + r * kDxThreads;
             const int o = b * CHW + min(i, CHW - 1);
             const float g = dI[o];
-            const int a = arg[o];
-            gnext[r] = (nb < NB && i < CHW) ? g : 0.f;
-            anext[r] = a;
+            n.a[r] = arg[o];
+            n.g[r] = (nb < NB && i < CHW) ? g : 0.f;
         }
 #pragma unroll
         for (int r = 0; r < kDwXPer; ++r) {
             const int i = tid + r * kDxThreads;
-            if (r * kDxThreads < npx) xnext[r] = x[(int64_t)b * npx + min(i, npx - 1)];
+            if (r * kDxThreads < npx) n.x[r] = x[(int64_t)b * npx + min(i, npx - 1)];
         }
     };
-    auto stage = [&]() {
+    auto stage = [&](const Next &n) {
 #pragma unroll
         for (int r = 0; r < kDxPer; ++r) {
             const int i = tid + r * kDxThreads;
-            const float g = gnext[r];
+            const float g = n.g[r];
             const uint32_t hi = bf16_rne(g);
             const float rr = g - __uint_as_float(hi << 16);
             const uint32_t mid = bf16_rne(rr);
             const uint32_t lo = bf16_rne(rr - __uint_as_float(mid << 16));
             const uint32_t pv[3] = {hi, mid, lo};
             if (i < CHW) {
-                const int co = i / HW, q = i - co * HW, a = anext[r];
+                const int co = i / HW, q = i - co * HW, a = n.a[r];
 #pragma unroll
-                for (int p = 0; p < 3; ++p) {
-                    const uint32_t v = pv[p];
+                for (int pp = 0; pp < 3; ++pp) {
+                    const uint32_t v = pv[pp];
                     const uint2 w2 = make_uint2((a == 0 ? v : 0u) | ((a == 1 ? v : 0u) << 16),
                                                 (a == 2 ? v : 0u) | ((a == 3 ? v : 0u) << 16));
-                    *reinterpret_cast<uint2 *>(&dct[p][co * kDwLdm + 4 * q]) = w2;
+                    *reinterpret_cast<uint2 *>(&dct[pp][co * kDwLdm + 4 * q]) = w2;
                 }
             }
         }
 #pragma unroll
         for (int r = 0; r < kDwXPer; ++r) {
             const int i = tid + r * kDxThreads;
-            if (r * kDxThreads < npx && i < npx) xs[i] = (uint16_t)(__float_as_uint((float)xnext[r]) >> 16);  // exact
+            if (r * kDxThreads < npx && i < npx)
+                xs[i] = (uint16_t)(__float_as_uint((float)n.x[r]) >> 16);  // exact
         }
     };
 
@@ -731,16 +735,18 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
     for (int i = 0; i < 4; ++i)
 #pragma unroll
         for (int j = 0; j < 3; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-    fetch(blockIdx.x);
-    lds_barrier();  // the zeroed parts
-    stage();
-    lds_barrier();
-    for (int nb = blockIdx.x; nb < NB; nb += gridDim.x) {
-        fetch(nb + gridDim.x);
+    auto products = [&]() {
 #pragma unroll
         for (int ms = 0; ms < 2; ++ms) {
             if (ms == 1 && !two_m) break;
+            // A fragments, all parts: lane (col, kg) holds dC^T[16 ct + col][32 ms + 8 kg + e]
+            u32x4 ap[3][4];
+#pragma unroll
+            for (int pp = 0; pp < 3; ++pp)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    ap[pp][i] = *reinterpret_cast<const u32x4 *>(
+                        &dct[pp][(16 * i + col) * kDwLdm + 32 * ms + 8 * kg]);
             // B fragments: lane (col, kg) holds col[32 ms + 8 kg + e][16 kt + col]
             u32x4 bx[3];
 #pragma unroll
@@ -748,28 +754,44 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
                 uint32_t h4[4];
 #pragma unroll
                 for (int h = 0; h < 2; ++h) {
-                    const uint16_t *p = xs + koff[j] + cb[ms][h];
-                    h4[2 * h] = (uint32_t)p[0] | ((uint32_t)p[1] << 16);
-                    h4[2 * h + 1] = (uint32_t)p[W] | ((uint32_t)p[W + 1] << 16);
+                    const uint16_t *q = xs + koff[j] + cb[ms][h];
+                    h4[2 * h] = (uint32_t)q[0] | ((uint32_t)q[1] << 16);
+                    h4[2 * h + 1] = (uint32_t)q[W] | ((uint32_t)q[W + 1] << 16);
                 }
                 bx[j] = u32x4{h4[0], h4[1], h4[2], h4[3]};
             }
-            // A fragments: lane (col, kg) holds dC^T[16 ct + col][32 ms + 8 kg + e]
+            // parts smallest first
 #pragma unroll
-            for (int p = 2; p >= 0; --p) {
-                u32x4 ap[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    ap[i] = *reinterpret_cast<const u32x4 *>(
-                        &dct[p][(16 * i + col) * kDwLdm + 32 * ms + 8 * kg]);
+            for (int pp = 2; pp >= 0; --pp)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
 #pragma unroll
-                    for (int j = 0; j < 3; ++j) acc[i][j] = mfma_bf16(ap[i], bx[j], acc[i][j]);
-            }
+                    for (int j = 0; j < 3; ++j) acc[i][j] = mfma_bf16(ap[pp][i], bx[j], acc[i][j]);
         }
+    };
+
+    Next n0, n1;
+    const int G = gridDim.x;
+    int nb = blockIdx.x;
+    fetch(n0, nb);
+    fetch(n1, nb + G);
+    lds_barrier();  // the zeroed parts
+    stage(n0);
+    lds_barrier();
+    while (true) {
+        fetch(n0, nb + 2 * G);
+        products();
         lds_barrier();  // every wave is done with the parts and the image
-        stage();
+        nb += G;
+        if (nb >= NB) break;
+        stage(n1);
+        lds_barrier();
+        fetch(n1, nb + 2 * G);
+        products();
+        lds_barrier();
+        nb += G;
+        if (nb >= NB) break;
+        stage(n0);
         lds_barrier();
     }
     // D fragment: lane (col, kg) holds dW[16 ct + 4 kg + r][16 kt + col]
