@@ -29,9 +29,12 @@
 //
 // The contractions are the library's GEMMs (exact multi-part bf16 products
 // with fp32 accumulation on the 16-bit matrix cores where they apply, fp32
-// MFMA otherwise), so every sum is deterministic.  Where one image's dx^T
-// fits a workgroup's LDS (the CSNN's second layer), conv_dx_kernel computes
-// it and the gather in one pass, without dx^T in HBM (see there).  Spikes are staged as
+// MFMA otherwise), so every sum is deterministic.  Where one image's window
+// rows fit a workgroup (the CSNN's second layer: at most 16 pooled cells per
+// channel, Ci * 25 <= 320, Co <= 64), each direction is one kernel that takes
+// an image at a time with its tiles in LDS and registers: conv_fwd_kernel
+// (contraction and pool, spike input), conv_dw_kernel (spike input) and
+// conv_dx_kernel; col, C, dC^T and dx^T never reach HBM (see there).  Spikes are staged as
 // bytes; an fp32 dC^T is written directly as three exact bf16 planes when the
 // weight gradient runs on the 16-bit cores.  The bias gradient comes from the
 // neuron scan's per-column sums.
@@ -810,6 +813,170 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
     }
 }
 
+// ---- forward in one pass --------------------------------------------------------
+// For the same layers on spike input, without col or C in HBM: a workgroup
+// takes one image at a time, gathers col[m][k] for its window rows into LDS
+// (bf16 0 / 1, from the image staged there), and computes
+//   C[m][co] = sum_k col[m][k] w[co][k] + bias[co]  (16 x 16 x 32 bf16 MFMA tiles)
+// with the weights held in registers as three exact bf16 parts: exact
+// products, summed smallest part first in fp32 (two accumulators per tile,
+// even and odd k-steps, added at the end).  The pool needs no exchange: the
+// four window rows of a pooled cell are the four accumulator rows of one lane,
+// so each lane adds the bias, keeps the first maximum and stores cur and the
+// choice.  Eight waves: wave v takes row tiles 2 (v & 1) + {0, 1} and output
+// channels 16 (v >> 1) .. + 15.  Threads t < 480 gather col: the 8 columns
+// 8 (t % 40) .. + 7 of rows t / 40 + 12 j.
+constexpr int kFwLdk = kDxMaxK + 8;  // col row stride (bf16): 656-byte rows, so the
+                                     // 16-byte reads of 16 lanes, rows apart, hit
+                                     // distinct bank groups
+constexpr int kFwChunks = kDxMaxK / 8;
+constexpr int kFwRowGroups = kDxThreads / kFwChunks;  // 12
+
+__global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
+    int NB, int Ci, int H, int W, int Co, int Hp, int Wp, const uint8_t *__restrict__ x,
+    const float *__restrict__ w, const float *__restrict__ bias, float *__restrict__ cur,
+    uint8_t *__restrict__ arg) {
+    __shared__ __attribute__((aligned(16))) uint16_t colb[kDxRows * kFwLdk];
+    __shared__ __attribute__((aligned(16))) uint16_t xs[2][kDwMaxX];
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int col = lane & 15, kg = lane >> 4;
+    const int wm = wv & 1, wn = wv >> 1;
+    const int HW = Hp * Wp, Kc = Ci * KS * KS, HWi = H * W, npx = Ci * HWi, Mi = 4 * HW;
+    const int KT = (Kc + 31) / 32, MT = (Mi + 15) / 16;
+
+    // B fragments: lane (col, kg) holds w[16 wn + col][32 ks + 8 kg + e] as three parts
+    const int co = 16 * wn + col;
+    u32x4 bw[kDxMaxK / 32][3];
+#pragma unroll
+    for (int ks = 0; ks < kDxMaxK / 32; ++ks) {
+        uint32_t h[3][8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int k = ks * 32 + 8 * kg + e;
+            const float v = (co < Co && k < Kc) ? w[co * Kc + k] : 0.f;
+            h[0][e] = bf16_rne(v);
+            const float r = v - __uint_as_float(h[0][e] << 16);
+            h[1][e] = bf16_rne(r);
+            h[2][e] = bf16_rne(r - __uint_as_float(h[1][e] << 16));
+        }
+#pragma unroll
+        for (int pp = 0; pp < 3; ++pp)
+            bw[ks][pp] = u32x4{h[pp][0] | (h[pp][1] << 16), h[pp][2] | (h[pp][3] << 16),
+                               h[pp][4] | (h[pp][5] << 16), h[pp][6] | (h[pp][7] << 16)};
+    }
+    const float bco = (bias && co < Co) ? bias[co] : 0.f;
+
+    // the gather: image offsets of the thread's 8 columns (a column past Kc
+    // reads element 0: its weights are zero)
+    const bool builder = tid < kFwChunks * kFwRowGroups;
+    const int ch = tid % kFwChunks, m0 = tid / kFwChunks;
+    int koff[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const int k = 8 * ch + e;
+        const int c = k / (KS * KS), t = k - c * KS * KS, ky = t / KS, kx = t - ky * KS;
+        koff[e] = k < Kc ? c * HWi + ky * W + kx : 0;
+    }
+    const bool build_chunk = builder && ch < 4 * KT;
+
+    struct Next {
+        uint32_t x[kDwXPer];
+    };
+    auto fetch = [&](Next &n, int nb) {
+        const int b = min(nb, NB - 1);
+#pragma unroll
+        for (int r = 0; r < kDwXPer; ++r) {
+            const int i = tid + r * kDxThreads;
+            if (r * kDxThreads < npx) n.x[r] = x[(int64_t)b * npx + min(i, npx - 1)];
+        }
+    };
+    auto stage = [&](const Next &n, uint16_t *dst) {
+#pragma unroll
+        for (int r = 0; r < kDwXPer; ++r) {
+            const int i = tid + r * kDxThreads;
+            if (r * kDxThreads < npx && i < npx)
+                dst[i] = (uint16_t)(__float_as_uint((float)n.x[r]) >> 16);  // exact
+        }
+    };
+    auto build = [&](const uint16_t *src) {
+        if (!build_chunk) return;
+        for (int m = m0; m < 16 * MT; m += kFwRowGroups) {
+            const int q = m >> 2, d = m & 3;
+            const int py = q / Wp, px = q - py * Wp;
+            // a row past the windows reads the image corner: its outputs are not stored
+            const int mo = m < Mi ? (2 * py + (d >> 1)) * W + 2 * px + (d & 1) : 0;
+            uint32_t hv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) hv[e] = src[mo + koff[e]];
+            *reinterpret_cast<u32x4 *>(&colb[m * kFwLdk + 8 * ch]) =
+                u32x4{hv[0] | (hv[1] << 16), hv[2] | (hv[3] << 16), hv[4] | (hv[5] << 16),
+                      hv[6] | (hv[7] << 16)};
+        }
+    };
+
+    // The registers hold the image after the one being multiplied: it is
+    // staged into the other buffer during the products, and the loads of the
+    // one after it are issued there.
+    Next n;
+    const int G = gridDim.x;
+    int nb = blockIdx.x, buf = 0;
+    fetch(n, nb);
+    stage(n, xs[0]);
+    fetch(n, nb + G);
+    lds_barrier();
+    while (true) {
+        build(xs[buf]);
+        lds_barrier();  // col complete
+        // (the other buffer's last reader, the previous gather, finished
+        // before the barrier above)
+        stage(n, xs[buf ^ 1]);
+        fetch(n, nb + 2 * G);
+        floatx4 acc[2][2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < kDxMaxK / 32; ++ks) {
+            if (ks < KT) {
+                u32x4 a[2];
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+                    a[i] = *reinterpret_cast<const u32x4 *>(
+                        &colb[(16 * (2 * wm + i) + col) * kFwLdk + 32 * ks + 8 * kg]);
+#pragma unroll
+                for (int pp = 2; pp >= 0; --pp)
+#pragma unroll
+                    for (int i = 0; i < 2; ++i)
+                        acc[i][ks & 1] = mfma_bf16(a[i], bw[ks][pp], acc[i][ks & 1]);
+            }
+        }
+        // pool: lane (col, kg) holds C rows 16 mt + 4 kg + r, r = 0..3 = the
+        // window positions of pooled cell q = 4 mt + kg, for output channel co
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int q = 4 * (2 * wm + i) + kg;
+            if (q < HW && co < Co) {
+                float best = (acc[i][0][0] + acc[i][1][0]) + bco;
+                int sel = 0;
+#pragma unroll
+                for (int r = 1; r < 4; ++r) {
+                    const float v = (acc[i][0][r] + acc[i][1][r]) + bco;
+                    if (v > best) {
+                        best = v;
+                        sel = r;
+                    }
+                }
+                const int o = (nb * Co + co) * HW + q;
+                cur[o] = best;
+                arg[o] = (uint8_t)sel;
+            }
+        }
+        lds_barrier();  // done with col; the next image is staged
+        nb += G;
+        if (nb >= NB) break;
+        buf ^= 1;
+    }
+}
+
 // Weight gradient of a layer with few inputs per channel (Kc = Ci * 25 = KC
 // <= 50: the network's input layer), straight from the pool's selection:
 //   dW[co][k] = sum over pooled cells of dI times x under the selected output.
@@ -1019,6 +1186,13 @@ hipError_t launch_conv_pool_fwd(const ConvGeom &g, const void *x, int in_dtype, 
     if (v.Mw == 0) return hipSuccess;
     if (ws == nullptr || ws_bytes < conv_fwd_workspace_bytes(g, in_dtype, allow_split))
         return hipErrorInvalidValue;
+    if (!(g.Ci == 1 && g.H * g.W <= kDirectMaxHW && g.Co <= kDirectMaxCo) &&
+        dw_one_pass(g, in_dtype, allow_split)) {
+        conv_fwd_kernel<<<(unsigned)min(g.NB, device_cus()), kDxThreads, 0, s>>>(
+            g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, reinterpret_cast<const uint8_t *>(x),
+            reinterpret_cast<const float *>(w), bias, cur, arg);
+        return hipGetLastError();
+    }
     if (g.Ci == 1 && g.H * g.W <= kDirectMaxHW && g.Co <= kDirectMaxCo) {
         if (in_dtype == SNN_U8)
             conv1_pool_kernel<uint8_t><<<(unsigned)g.NB, kThreads, 0, s>>>(

@@ -759,11 +759,17 @@ def _conv_fwd_gpu(d, x, w, b):
     return _np(cur), _np(arg)
 
 
-# (800, 12, 12, 12, 64): 51200 conv rows, one pass over K, so the contraction
-# pools its own output; (5, 12, 12, 12, 64) is split over K and pooled after
+# Spike input with Ci * 25 <= 320, Co <= 64 and at most 16 pooled cells per
+# channel runs the one-pass kernel: (5, 12, 12, 12, 64) and (800, ...) at the
+# limits, (2, 3, 9, 11, 5) ragged, (1, 2, 6, 6, 2) one cell, (5, 7, 12, 12,
+# 33) part of a channel tile, (2, 4, 7, 37, 40) a 259-pixel image; past them
+# the gather and the contraction, which pools its own output when it makes one
+# pass over K ((300, 3, 15, 13, 70), 70 channels) or pools after it
+# ((4, 13, 9, 9, 8), 325 columns split over K).
 @pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (5, 12, 12, 12, 64), (2, 3, 9, 11, 5),
                                           (1, 2, 6, 6, 2), (800, 12, 12, 12, 64),
-                                          (300, 3, 15, 13, 70)])
+                                          (5, 7, 12, 12, 33), (2, 4, 7, 37, 40),
+                                          (300, 3, 15, 13, 70), (4, 13, 9, 9, 8)])
 def test_conv_pool_fwd(NB, Ci, H, W, Co):
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=NB * 100 + Co)
     _check_conv_fwd(x, w, b, d)
