@@ -782,6 +782,8 @@ def _stage_kernels(net, name, li, fp32_mfma):
         return ": narrow_fwd_kernel (16 outputs per MFMA tile, weights staged in LDS)"
     if name == "synapse_fwd" and _direct_conv(net, li):
         return ": conv1_pool_kernel (convolution and pool in one kernel)"
+    if name == "synapse_fwd" and _conv_one_pass(net, li, fp32_mfma) and d.in_dtype == 3:
+        return ": conv_fwd_kernel (gather, contraction in 3 exact bf16 passes and pool in one kernel)"
     if name == "loss":
         return ": loss kernels"
     kind, passes = _contraction_kind(net, li, fp32_mfma)
