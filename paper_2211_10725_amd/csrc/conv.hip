@@ -824,13 +824,11 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
 // four window rows of a pooled cell are the four accumulator rows of one lane,
 // so each lane adds the bias, keeps the first maximum and stores cur and the
 // choice.  Eight waves: wave v takes row tiles 2 (v & 1) + {0, 1} and output
-// channels 16 (v >> 1) .. + 15.  Threads t < 480 gather col: the 8 columns
-// 8 (t % 40) .. + 7 of rows t / 40 + 12 j.
+// channels 16 (v >> 1) .. + 15.
 constexpr int kFwLdk = kDxMaxK + 8;  // col row stride (bf16): 656-byte rows, so the
                                      // 16-byte reads of 16 lanes, rows apart, hit
                                      // distinct bank groups
-constexpr int kFwChunks = kDxMaxK / 8;
-constexpr int kFwRowGroups = kDxThreads / kFwChunks;  // 12
+constexpr int kFwChunks = kDxMaxK / 8;  // 8-column chunks of col
 
 __global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
     int NB, int Ci, int H, int W, int Co, int Hp, int Wp, const uint8_t *__restrict__ x,
@@ -842,7 +840,7 @@ __global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
     const int col = lane & 15, kg = lane >> 4;
     const int wm = wv & 1, wn = wv >> 1;
     const int HW = Hp * Wp, Kc = Ci * KS * KS, HWi = H * W, npx = Ci * HWi, Mi = 4 * HW;
-    const int KT = (Kc + 31) / 32, MT = (Mi + 15) / 16;
+    const int KT = (Kc + 31) / 32;
 
     // B fragments: lane (col, kg) holds w[16 wn + col][32 ks + 8 kg + e] as three parts
     const int co = 16 * wn + col;
@@ -866,19 +864,19 @@ __global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
     }
     const float bco = (bias && co < Co) ? bias[co] : 0.f;
 
-    // the gather: image offsets of the thread's 8 columns (a column past Kc
-    // reads element 0: its weights are zero)
-    const bool builder = tid < kFwChunks * kFwRowGroups;
-    const int ch = tid % kFwChunks, m0 = tid / kFwChunks;
-    int koff[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-        const int k = 8 * ch + e;
-        const int c = k / (KS * KS), t = k - c * KS * KS, ky = t / KS, kx = t - ky * KS;
-        koff[e] = k < Kc ? c * HWi + ky * W + kx : 0;
+    // The gather: lane l of wave v writes row m = l of col, columns 8 ch ..
+    // + 7 for ch = v, v + 8, ..; the image offset of a row (mo) is the lane's,
+    // that of a column (koff) is the same for the whole wave.  Lanes, 64
+    // window rows of an 8 x 8 block of conv outputs, read 32 distinct words:
+    // no bank conflicts.  A row past the windows reads the image corner (its
+    // outputs are not stored); a column past Kc reads its channel's corner
+    // (its weights are zero).
+    const int wvs = __builtin_amdgcn_readfirstlane(wv);
+    int mo;
+    {
+        const int m = lane, q = m >> 2, d = m & 3, py = q / Wp, px = q - py * Wp;
+        mo = m < Mi ? (2 * py + (d >> 1)) * W + 2 * px + (d & 1) : 0;
     }
-    const bool build_chunk = builder && ch < 4 * KT;
-
     struct Next {
         uint32_t x[kDwXPer];
     };
@@ -899,18 +897,22 @@ __global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
         }
     };
     auto build = [&](const uint16_t *src) {
-        if (!build_chunk) return;
-        for (int m = m0; m < 16 * MT; m += kFwRowGroups) {
-            const int q = m >> 2, d = m & 3;
-            const int py = q / Wp, px = q - py * Wp;
-            // a row past the windows reads the image corner: its outputs are not stored
-            const int mo = m < Mi ? (2 * py + (d >> 1)) * W + 2 * px + (d & 1) : 0;
-            uint32_t hv[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) hv[e] = src[mo + koff[e]];
-            *reinterpret_cast<u32x4 *>(&colb[m * kFwLdk + 8 * ch]) =
-                u32x4{hv[0] | (hv[1] << 16), hv[2] | (hv[3] << 16), hv[4] | (hv[5] << 16),
-                      hv[6] | (hv[7] << 16)};
+        for (int j = 0; j < kFwChunks / 8; ++j) {
+            const int ch = wvs + 8 * j;
+            if (ch < 4 * KT) {
+                uint32_t hv[8];
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int k = 8 * ch + e;
+                    const int c = k / (KS * KS), t = k - c * KS * KS, ky = t / KS, kx = t - ky * KS;
+                    const int ko = k < Kc ? c * HWi + ky * W + kx : 0;
+                    hv[e] = src[mo + ko];
+                }
+                *reinterpret_cast<u32x4 *>(&colb[lane * kFwLdk + 8 * ch]) =
+                    u32x4{hv[0] | (hv[1] << 16), hv[2] | (hv[3] << 16), hv[4] | (hv[5] << 16),
+                          hv[6] | (hv[7] << 16)};
+            }
         }
     };
 
