@@ -45,8 +45,9 @@ SCAN_WORKLOAD = "scan_wide_t1000_b64"
 # kernel sources behind each kind of stage (a stored counter profile of a
 # stage stays valid while these files are unchanged)
 STAGE_SOURCES = {
-    "synapse": ["snn_internal.hpp", "gemm.hip", "gemm_mfma16.hip", "gemm_async.hip", "skinny.hip",
-                "conv.hip"],
+    "synapse": ["snn_internal.hpp", "gemm.hip", "gemm_mfma16.hip", "gemm_async.hip", "skinny.hip"],
+    "conv": ["snn_internal.hpp", "gemm.hip", "gemm_mfma16.hip", "gemm_async.hip", "skinny.hip",
+             "conv.hip"],
     "neuron": ["snn_internal.hpp", "neuron.hpp", "scan.hip"],
 }
 
@@ -61,8 +62,17 @@ def csrc_hash(files=None) -> str:
     return h.hexdigest()[:16]
 
 
-def stage_sources(stage_key: str):
-    return STAGE_SOURCES["synapse" if stage_key.startswith("synapse") else "neuron"]
+def stage_sources(stage_key: str, workload: str):
+    """Kernel sources a stage of a workload runs: a conv layer's synapse
+    stages also depend on conv.hip."""
+    if not stage_key.startswith("synapse"):
+        return STAGE_SOURCES["neuron"]
+    from paper_2211_10725_amd import workloads as wls
+    m = re.search(r"\[L(\d+)\]", stage_key)
+    layers = wls.get(workload).layers if workload in wls.WORKLOADS else []
+    conv = m is not None and int(m.group(1)) < len(layers) and \
+        layers[int(m.group(1))].get("kind") == "conv"
+    return STAGE_SOURCES["conv" if conv else "synapse"]
 
 
 def stored_traffic(workload: str, stage_key: str):
@@ -75,7 +85,7 @@ def stored_traffic(workload: str, stage_key: str):
     txt = open(path).read()
     m = re.search(rf"^\|\s*{re.escape(stage_key)}\s*\|[^|]*\|[^|]*\|[^|]*\|\s*([0-9.eE+]+)\s*\|"
                   rf"\s*([0-9a-f]+)\s*\|", txt, re.M)
-    if not m or m.group(2) != csrc_hash(stage_sources(stage_key)):
+    if not m or m.group(2) != csrc_hash(stage_sources(stage_key, workload)):
         return None
     return float(m.group(1))
 
