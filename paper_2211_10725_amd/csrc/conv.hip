@@ -1027,8 +1027,8 @@ __global__ __launch_bounds__(kThreads) void conv_dw_small_kernel(
 }
 
 // chunks of pooled cells per output channel for conv_dw_small_kernel: about
-// 1024 workgroups (4 per compute unit); 4096 measured 12 % slower on the
-// CSNN's first layer (more block reductions), 256 18 % slower
+// 1024 workgroups in all (4 per compute unit); 4096 measured 12 % slower on
+// the CSNN's first layer (more block reductions), 512 20 % slower
 int small_dw_chunks(const ConvGeom &g, int64_t Q) {
     const int64_t by_cells = (Q + kThreads - 1) / kThreads;
     const int64_t by_grid = max(1, 1024 / g.Co);
