@@ -662,19 +662,31 @@ def _contraction_kind(net, li, fp32_mfma, stage="synapse_fwd"):
         return ("mfma16", p) if p <= 6 else ("mfma32", 1)
     # conv backward: one-pass kernels on the 16-bit cores (dW 3 exact passes,
     # dx 6 part products) where the image fits, else the fp32 contractions
-    if _conv_one_pass(net, li, fp32_mfma) and d.in_dtype == 3:
-        return "mfma16", (4.5 if li > 0 and net.gx[li] is not None else 3)
+    dx = li > 0 and net.gx[li] is not None
+    if _conv_one_pass_fw(net, li, fp32_mfma) and (not dx or _conv_one_pass(net, li, fp32_mfma)):
+        return "mfma16", (4.5 if dx else 3)
     return "mfma32", 1
 
 
 def _conv_one_pass(net, li, fp32_mfma):
-    """Whether layer li's conv backward runs as conv_dx_kernel (and, on spike
-    input, conv_dw_kernel): mirrors dx_one_pass in conv.hip (at most 12 input
-    and 64 output channels, 16 pooled cells per channel, 512 pixels)."""
+    """Whether layer li's conv input gradient runs as conv_dx_kernel: mirrors
+    dx_one_pass in conv.hip (at most 12 input and 64 output channels, 16
+    pooled cells per channel, 512 pixels)."""
     d = net.descs[li]
     hp, wp = (d.h_in - 4) // 2, (d.w_in - 4) // 2
     return (d.synapse == 1 and not fp32_mfma and d.c_in * 25 <= 320 and d.c_out <= 64
             and hp * wp <= 16 and d.h_in * d.w_in <= 512)
+
+
+def _conv_one_pass_fw(net, li, fp32_mfma):
+    """Whether layer li's conv forward and weight gradient run as
+    conv_fwd_kernel and conv_dw_kernel: mirrors dw_one_pass in conv.hip
+    (spike input, up to 32 pooled cells, images of whole 4-byte words)."""
+    d = net.descs[li]
+    hp, wp = (d.h_in - 4) // 2, (d.w_in - 4) // 2
+    return (d.synapse == 1 and not fp32_mfma and d.in_dtype == 3 and d.c_in * 25 <= 320
+            and d.c_out <= 64 and hp * wp <= 32 and d.h_in * d.w_in <= 512
+            and d.c_in * d.h_in * d.w_in % 4 == 0)
 
 
 def _direct_conv(net, li):
@@ -768,8 +780,8 @@ def _stage_kernels(net, name, li, fp32_mfma):
         return f": {pre}{gemm} ({passes} pass{'es' if passes > 1 else ''}, " \
                "+ splitk_reduce_kernel when split over K)"
     if name == "synapse_bwd":
-        one = _conv_one_pass(net, li, fp32_mfma)
-        if one and d.in_dtype == 3:
+        one, one_w = _conv_one_pass(net, li, fp32_mfma), _conv_one_pass_fw(net, li, fp32_mfma)
+        if one_w:
             dw = "conv_dw_kernel + splitk_reduce_wide_kernel"
         elif d.c_in * 25 <= 50:
             dw = "conv_dw_small_kernel + splitk_reduce_wide_kernel"
@@ -777,10 +789,13 @@ def _stage_kernels(net, name, li, fp32_mfma):
             dw = "unpool_t_kernel + im2col_t_kernel + contraction"
         if not (li > 0 and net.gx[li] is not None):
             return f": {dw} (conv weight gradient)"
-        if not one:
-            return (": unpool_t_kernel + im2col_t_kernel + contractions + col2im_kernel "
+        if one:
+            return f": {dw} + conv_dx_kernel (conv weight and input gradients)"
+        if one_w:
+            return (f": {dw} + unpool_t_kernel + contraction + col2im_kernel "
                     "(conv weight and input gradients)")
-        return f": {dw} + conv_dx_kernel (conv weight and input gradients)"
+        return (": unpool_t_kernel + im2col_t_kernel + contractions + col2im_kernel "
+                "(conv weight and input gradients)")
     if name == "synapse_fwd" and _async_contraction(net, li, fp32_mfma):
         if d.w_dtype == 0:
             widen = "widen_kernel (spikes to bf16) + " if d.in_dtype == 3 else ""
@@ -792,7 +807,7 @@ def _stage_kernels(net, name, li, fp32_mfma):
         return ": narrow_fwd_kernel (16 outputs per MFMA tile, weights staged in LDS)"
     if name == "synapse_fwd" and _direct_conv(net, li):
         return ": conv1_pool_kernel (convolution and pool in one kernel)"
-    if name == "synapse_fwd" and _conv_one_pass(net, li, fp32_mfma) and d.in_dtype == 3:
+    if name == "synapse_fwd" and _conv_one_pass_fw(net, li, fp32_mfma):
         return ": conv_fwd_kernel (gather, contraction in 3 exact bf16 passes and pool in one kernel)"
     if name == "loss":
         return ": loss kernels"

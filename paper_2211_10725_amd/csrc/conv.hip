@@ -642,11 +642,24 @@ __global__ __launch_bounds__(kDxThreads) void conv_dx_kernel(
 // the k tiles v, v + 8, v + 16.  The image and the parts of the next image
 // are loaded during the products and staged after a barrier.
 constexpr int kDwMaxGrid = 256;                   // partial sums written
-constexpr int kDwLdm = kDxRows + 8;               // dC^T part row stride (bf16): the
-                                                  // 16-byte reads of 16 lanes, co
-                                                  // apart, hit distinct bank groups
+constexpr int kFwMaxCells = 32;                   // pooled cells per channel for the
+                                                  // forward and the weight gradient
+constexpr int kFwRows = 4 * kFwMaxCells;          // window rows: up to 8 row tiles
+constexpr int kDwLdm = kFwRows + 8;               // dC^T part row stride (bf16): 272-byte
+                                                  // rows, so the 16-byte reads of 16
+                                                  // lanes, co apart, hit distinct
+                                                  // bank groups
 constexpr int kDwMaxX = kDxMaxK / (KS * KS) * kDxThreads;  // image elements staged
-constexpr int kDwXPer = kDwMaxX / kDxThreads;     // image bytes loaded per thread
+constexpr int kDwXPer = kDwMaxX / 4 / kDxThreads; // 4-byte image words loaded per thread
+constexpr int kDwPer = kDxMaxCo * kFwMaxCells / kDxThreads;  // (co, q) per thread
+
+// bf16 of four spike bytes (every byte value is exact), as two words
+__device__ inline uint2 bytes4_bf16(uint32_t w) {
+    uint32_t h[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) h[e] = __float_as_uint((float)((w >> (8 * e)) & 0xffu)) >> 16;
+    return make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+}
 
 __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
     int NB, int Ci, int H, int W, int Co, int Hp, int Wp, const float *__restrict__ dI,
@@ -656,7 +669,8 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int col = lane & 15, kg = lane >> 4;
     const int HW = Hp * Wp, Kc = Ci * KS * KS, CHW = Co * HW, HWi = H * W, npx = Ci * HWi;
-    const bool two_m = HW > 8;  // window rows past 32
+    const int nxw = npx / 4;  // image words (npx is a multiple of 4)
+    const int nms = (4 * HW + 31) / 32;  // 32-row steps of the window rows
 
     // window rows past 4 HW and channels past Co stay zero for the whole launch
     for (int i = tid; i < 3 * kDxMaxCo * kDwLdm / 2; i += kDxThreads)
@@ -666,7 +680,7 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
     // reads a valid element; those output columns are not stored), and the
     // corner of its two pooled cells per 32 window rows (cells past HW read
     // element 0: their dC^T rows are zero)
-    int koff[3], cb[2][2];
+    int koff[3], cb[kFwRows / 32][2];
 #pragma unroll
     for (int j = 0; j < 3; ++j) {
         const int k = (wv + 8 * j) * 16 + col;
@@ -674,7 +688,7 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
         koff[j] = k < Kc ? c * HWi + ky * W + kx : 0;
     }
 #pragma unroll
-    for (int ms = 0; ms < 2; ++ms)
+    for (int ms = 0; ms < kFwRows / 32; ++ms)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int q = 8 * ms + 2 * kg + h, py = q / Wp, px = q - py * Wp;
@@ -684,29 +698,30 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
     // The loads of an image are issued two images ahead, into one of two
     // register sets, so a whole image's products hide their latency.
     struct Next {
-        float g[kDxPer];
-        int a[kDxPer];
+        float g[kDwPer];
+        int a[kDwPer];
         uint32_t x[kDwXPer];
     };
     auto fetch = [&](Next &n, int nb) {
         const int b = min(nb, NB - 1);
 #pragma unroll
-        for (int r = 0; r < kDxPer; ++r) {
+        for (int r = 0; r < kDwPer; ++r) {
             const int i = tid + r * kDxThreads;
             const int o = b * CHW + min(i, CHW - 1);
             const float g = dI[o];
             n.a[r] = arg[o];
             n.g[r] = (nb < NB && i < CHW) ? g : 0.f;
         }
+        const uint32_t *xw = reinterpret_cast<const uint32_t *>(x) + (int64_t)b * nxw;
 #pragma unroll
         for (int r = 0; r < kDwXPer; ++r) {
             const int i = tid + r * kDxThreads;
-            if (r * kDxThreads < npx) n.x[r] = x[(int64_t)b * npx + min(i, npx - 1)];
+            if (r * kDxThreads < nxw) n.x[r] = xw[min(i, nxw - 1)];
         }
     };
     auto stage = [&](const Next &n) {
 #pragma unroll
-        for (int r = 0; r < kDxPer; ++r) {
+        for (int r = 0; r < kDwPer; ++r) {
             const int i = tid + r * kDxThreads;
             const float g = n.g[r];
             const uint32_t hi = bf16_rne(g);
@@ -728,8 +743,8 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
 #pragma unroll
         for (int r = 0; r < kDwXPer; ++r) {
             const int i = tid + r * kDxThreads;
-            if (r * kDxThreads < npx && i < npx)
-                xs[i] = (uint16_t)(__float_as_uint((float)n.x[r]) >> 16);  // exact
+            if (r * kDxThreads < nxw && i < nxw)
+                *reinterpret_cast<uint2 *>(&xs[4 * i]) = bytes4_bf16(n.x[r]);
         }
     };
 
@@ -740,36 +755,38 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
         for (int j = 0; j < 3; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
     auto products = [&]() {
 #pragma unroll
-        for (int ms = 0; ms < 2; ++ms) {
-            if (ms == 1 && !two_m) break;
-            // A fragments, all parts: lane (col, kg) holds dC^T[16 ct + col][32 ms + 8 kg + e]
-            u32x4 ap[3][4];
+        for (int ms = 0; ms < kFwRows / 32; ++ms) {
+            if (ms < nms) {
+                // A fragments, all parts: lane (col, kg) holds dC^T[16 ct + col][32 ms + 8 kg + e]
+                u32x4 ap[3][4];
 #pragma unroll
-            for (int pp = 0; pp < 3; ++pp)
+                for (int pp = 0; pp < 3; ++pp)
 #pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    ap[pp][i] = *reinterpret_cast<const u32x4 *>(
-                        &dct[pp][(16 * i + col) * kDwLdm + 32 * ms + 8 * kg]);
-            // B fragments: lane (col, kg) holds col[32 ms + 8 kg + e][16 kt + col]
-            u32x4 bx[3];
+                    for (int i = 0; i < 4; ++i)
+                        ap[pp][i] = *reinterpret_cast<const u32x4 *>(
+                            &dct[pp][(16 * i + col) * kDwLdm + 32 * ms + 8 * kg]);
+                // B fragments: lane (col, kg) holds col[32 ms + 8 kg + e][16 kt + col]
+                u32x4 bx[3];
 #pragma unroll
-            for (int j = 0; j < 3; ++j) {
-                uint32_t h4[4];
+                for (int j = 0; j < 3; ++j) {
+                    uint32_t h4[4];
 #pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    const uint16_t *q = xs + koff[j] + cb[ms][h];
-                    h4[2 * h] = (uint32_t)q[0] | ((uint32_t)q[1] << 16);
-                    h4[2 * h + 1] = (uint32_t)q[W] | ((uint32_t)q[W + 1] << 16);
+                    for (int h = 0; h < 2; ++h) {
+                        const uint16_t *q = xs + koff[j] + cb[ms][h];
+                        h4[2 * h] = (uint32_t)q[0] | ((uint32_t)q[1] << 16);
+                        h4[2 * h + 1] = (uint32_t)q[W] | ((uint32_t)q[W + 1] << 16);
+                    }
+                    bx[j] = u32x4{h4[0], h4[1], h4[2], h4[3]};
                 }
-                bx[j] = u32x4{h4[0], h4[1], h4[2], h4[3]};
+                // parts smallest first
+#pragma unroll
+                for (int pp = 2; pp >= 0; --pp)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+#pragma unroll
+                        for (int j = 0; j < 3; ++j)
+                            acc[i][j] = mfma_bf16(ap[pp][i], bx[j], acc[i][j]);
             }
-            // parts smallest first
-#pragma unroll
-            for (int pp = 2; pp >= 0; --pp)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-#pragma unroll
-                    for (int j = 0; j < 3; ++j) acc[i][j] = mfma_bf16(ap[pp][i], bx[j], acc[i][j]);
         }
     };
 
@@ -819,28 +836,32 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
 // (bf16 0 / 1, from the image staged there), and computes
 //   C[m][co] = sum_k col[m][k] w[co][k] + bias[co]  (16 x 16 x 32 bf16 MFMA tiles)
 // with the weights held in registers as three exact bf16 parts: exact
-// products, summed smallest part first in fp32 (two accumulators per tile,
-// even and odd k-steps, added at the end).  The pool needs no exchange: the
+// products, summed smallest part first in fp32.  The pool needs no exchange: the
 // four window rows of a pooled cell are the four accumulator rows of one lane,
 // so each lane adds the bias, keeps the first maximum and stores cur and the
-// choice.  Eight waves: wave v takes row tiles 2 (v & 1) + {0, 1} and output
-// channels 16 (v >> 1) .. + 15.
+// choice.  Eight waves: wave v takes row tiles (v & 1) + {0, 2} (+ {4, 6}
+// past 16 pooled cells) and output channels 16 (v >> 1) .. + 15.
 constexpr int kFwLdk = kDxMaxK + 8;  // col row stride (bf16): 656-byte rows, so the
                                      // 16-byte reads of 16 lanes, rows apart, hit
                                      // distinct bank groups
 constexpr int kFwChunks = kDxMaxK / 8;  // 8-column chunks of col
 
+template <int MPW>  // row tiles per wave: 2 (at most 16 pooled cells) or 4
 __global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
     int NB, int Ci, int H, int W, int Co, int Hp, int Wp, const uint8_t *__restrict__ x,
     const float *__restrict__ w, const float *__restrict__ bias, float *__restrict__ cur,
     uint8_t *__restrict__ arg) {
-    __shared__ __attribute__((aligned(16))) uint16_t colb[kDxRows * kFwLdk];
+    constexpr int ROWS = 32 * MPW;
+    __shared__ __attribute__((aligned(16))) uint16_t colb[ROWS * kFwLdk];
     __shared__ __attribute__((aligned(16))) uint16_t xs[2][kDwMaxX];
+    __shared__ __attribute__((aligned(16))) int kot[kDxMaxK];  // image offset of column k
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
     const int col = lane & 15, kg = lane >> 4;
-    const int wm = wv & 1, wn = wv >> 1;
+    const int wvu = __builtin_amdgcn_readfirstlane(wv);  // uniform across the wave
+    const int wm = wvu & 1, wn = wvu >> 1;
     const int HW = Hp * Wp, Kc = Ci * KS * KS, HWi = H * W, npx = Ci * HWi, Mi = 4 * HW;
-    const int KT = (Kc + 31) / 32;
+    const int nxw = npx / 4;  // image words (npx is a multiple of 4)
+    const int KT = (Kc + 31) / 32, MT = (Mi + 15) / 16;
 
     // B fragments: lane (col, kg) holds w[16 wn + col][32 ks + 8 kg + e] as three parts
     const int co = 16 * wn + col;
@@ -864,36 +885,42 @@ __global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
     }
     const float bco = (bias && co < Co) ? bias[co] : 0.f;
 
-    // The gather: lane l of wave v writes row m = l of col, columns 8 ch ..
-    // + 7 for ch = v, v + 8, ..; the image offset of a row (mo) is the lane's,
-    // that of a column (koff) is the same for the whole wave.  Lanes, 64
-    // window rows of an 8 x 8 block of conv outputs, read 32 distinct words:
-    // no bank conflicts.  A row past the windows reads the image corner (its
+    // The gather: lane l of wave v writes rows m = l and l + 64 of col,
+    // columns 8 ch .. + 7 for ch = v, v + 8, ..; the image offset of a row
+    // (mo) is the lane's, that of a column (kot, read as a broadcast) is the
+    // same for the whole wave.  Lanes, 64 window rows (16 pooled cells), read distinct words: no
+    // bank conflicts.  A row past the windows reads the image corner (its
     // outputs are not stored); a column past Kc reads its channel's corner
     // (its weights are zero).
-    const int wvs = __builtin_amdgcn_readfirstlane(wv);
-    int mo;
-    {
-        const int m = lane, q = m >> 2, d = m & 3, py = q / Wp, px = q - py * Wp;
-        mo = m < Mi ? (2 * py + (d >> 1)) * W + 2 * px + (d & 1) : 0;
+    const int wvs = wvu;
+    for (int k = tid; k < kDxMaxK; k += kDxThreads) {
+        const int c = k / (KS * KS), t = k - c * KS * KS, ky = t / KS, kx = t - ky * KS;
+        kot[k] = k < Kc ? c * HWi + ky * W + kx : 0;
+    }
+    int mo[MPW / 2];
+#pragma unroll
+    for (int r = 0; r < MPW / 2; ++r) {
+        const int m = lane + 64 * r, q = m >> 2, d = m & 3, py = q / Wp, px = q - py * Wp;
+        mo[r] = m < Mi ? (2 * py + (d >> 1)) * W + 2 * px + (d & 1) : 0;
     }
     struct Next {
         uint32_t x[kDwXPer];
     };
     auto fetch = [&](Next &n, int nb) {
         const int b = min(nb, NB - 1);
+        const uint32_t *xw = reinterpret_cast<const uint32_t *>(x) + (int64_t)b * nxw;
 #pragma unroll
         for (int r = 0; r < kDwXPer; ++r) {
             const int i = tid + r * kDxThreads;
-            if (r * kDxThreads < npx) n.x[r] = x[(int64_t)b * npx + min(i, npx - 1)];
+            if (r * kDxThreads < nxw) n.x[r] = xw[min(i, nxw - 1)];
         }
     };
     auto stage = [&](const Next &n, uint16_t *dst) {
 #pragma unroll
         for (int r = 0; r < kDwXPer; ++r) {
             const int i = tid + r * kDxThreads;
-            if (r * kDxThreads < npx && i < npx)
-                dst[i] = (uint16_t)(__float_as_uint((float)n.x[r]) >> 16);  // exact
+            if (r * kDxThreads < nxw && i < nxw)
+                *reinterpret_cast<uint2 *>(&dst[4 * i]) = bytes4_bf16(n.x[r]);
         }
     };
     auto build = [&](const uint16_t *src) {
@@ -901,17 +928,21 @@ __global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
         for (int j = 0; j < kFwChunks / 8; ++j) {
             const int ch = wvs + 8 * j;
             if (ch < 4 * KT) {
-                uint32_t hv[8];
+                const int4 k0 = *reinterpret_cast<const int4 *>(&kot[8 * ch]);
+                const int4 k1 = *reinterpret_cast<const int4 *>(&kot[8 * ch + 4]);
+                const int ko[8] = {k0.x, k0.y, k0.z, k0.w, k1.x, k1.y, k1.z, k1.w};
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int k = 8 * ch + e;
-                    const int c = k / (KS * KS), t = k - c * KS * KS, ky = t / KS, kx = t - ky * KS;
-                    const int ko = k < Kc ? c * HWi + ky * W + kx : 0;
-                    hv[e] = src[mo + ko];
+                for (int r = 0; r < MPW / 2; ++r) {
+                    const int m = lane + 64 * r;
+                    if (m < 16 * MT) {
+                        uint32_t hv[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) hv[e] = src[mo[r] + ko[e]];
+                        *reinterpret_cast<u32x4 *>(&colb[m * kFwLdk + 8 * ch]) =
+                            u32x4{hv[0] | (hv[1] << 16), hv[2] | (hv[3] << 16),
+                                  hv[4] | (hv[5] << 16), hv[6] | (hv[7] << 16)};
+                    }
                 }
-                *reinterpret_cast<u32x4 *>(&colb[lane * kFwLdk + 8 * ch]) =
-                    u32x4{hv[0] | (hv[1] << 16), hv[2] | (hv[3] << 16), hv[4] | (hv[5] << 16),
-                          hv[6] | (hv[7] << 16)};
             }
         }
     };
@@ -933,35 +964,35 @@ __global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
         // before the barrier above)
         stage(n, xs[buf ^ 1]);
         fetch(n, nb + 2 * G);
-        floatx4 acc[2][2];
+        floatx4 acc[MPW];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) acc[i][0] = acc[i][1] = floatx4{0.f, 0.f, 0.f, 0.f};
+        for (int i = 0; i < MPW; ++i) acc[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+        // (tiles past the window rows multiply stale rows; they are not stored)
 #pragma unroll
         for (int ks = 0; ks < kDxMaxK / 32; ++ks) {
             if (ks < KT) {
-                u32x4 a[2];
+                u32x4 a[MPW];
 #pragma unroll
-                for (int i = 0; i < 2; ++i)
+                for (int i = 0; i < MPW; ++i)
                     a[i] = *reinterpret_cast<const u32x4 *>(
-                        &colb[(16 * (2 * wm + i) + col) * kFwLdk + 32 * ks + 8 * kg]);
+                        &colb[(16 * (wm + 2 * i) + col) * kFwLdk + 32 * ks + 8 * kg]);
 #pragma unroll
                 for (int pp = 2; pp >= 0; --pp)
 #pragma unroll
-                    for (int i = 0; i < 2; ++i)
-                        acc[i][ks & 1] = mfma_bf16(a[i], bw[ks][pp], acc[i][ks & 1]);
+                    for (int i = 0; i < MPW; ++i) acc[i] = mfma_bf16(a[i], bw[ks][pp], acc[i]);
             }
         }
         // pool: lane (col, kg) holds C rows 16 mt + 4 kg + r, r = 0..3 = the
         // window positions of pooled cell q = 4 mt + kg, for output channel co
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int q = 4 * (2 * wm + i) + kg;
+        for (int i = 0; i < MPW; ++i) {
+            const int q = 4 * (wm + 2 * i) + kg;
             if (q < HW && co < Co) {
-                float best = (acc[i][0][0] + acc[i][1][0]) + bco;
+                float best = acc[i][0] + bco;
                 int sel = 0;
 #pragma unroll
                 for (int r = 1; r < 4; ++r) {
-                    const float v = (acc[i][0][r] + acc[i][1][r]) + bco;
+                    const float v = acc[i][r] + bco;
                     if (v > best) {
                         best = v;
                         sel = r;
@@ -1043,9 +1074,12 @@ bool dx_one_pass(const ConvGeom &g, bool allow_split) {
            g.Hp * g.Wp <= kDxMaxCells && g.H * g.W <= kDxThreads;
 }
 
-// the weight gradient by conv_dw_kernel (spike input, exact in bf16)
+// the forward by conv_fwd_kernel and the weight gradient by conv_dw_kernel
+// (spike input, exact in bf16; up to 32 pooled cells per channel)
 bool dw_one_pass(const ConvGeom &g, int in_dtype, bool allow_split) {
-    return in_dtype == SNN_U8 && dx_one_pass(g, allow_split);
+    return in_dtype == SNN_U8 && allow_split && g.Ci * KS * KS <= kDxMaxK &&
+           g.Co <= kDxMaxCo && g.Hp * g.Wp <= kFwMaxCells && g.H * g.W <= kDxThreads &&
+           g.Ci * g.H * g.W % 4 == 0;  // images staged as 4-byte words
 }
 
 unsigned blocks(int64_t n) { return (unsigned)((n + kThreads - 1) / kThreads); }
@@ -1192,9 +1226,15 @@ hipError_t launch_conv_pool_fwd(const ConvGeom &g, const void *x, int in_dtype, 
         return hipErrorInvalidValue;
     if (!(g.Ci == 1 && g.H * g.W <= kDirectMaxHW && g.Co <= kDirectMaxCo) &&
         dw_one_pass(g, in_dtype, allow_split)) {
-        conv_fwd_kernel<<<(unsigned)min(g.NB, device_cus()), kDxThreads, 0, s>>>(
-            g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, reinterpret_cast<const uint8_t *>(x),
-            reinterpret_cast<const float *>(w), bias, cur, arg);
+        const unsigned grid = (unsigned)min(g.NB, device_cus());
+        const uint8_t *xb = reinterpret_cast<const uint8_t *>(x);
+        const float *wf = reinterpret_cast<const float *>(w);
+        if (g.Hp * g.Wp <= kDxMaxCells)
+            conv_fwd_kernel<2><<<grid, kDxThreads, 0, s>>>(g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp,
+                                                           xb, wf, bias, cur, arg);
+        else
+            conv_fwd_kernel<4><<<grid, kDxThreads, 0, s>>>(g.NB, g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp,
+                                                           xb, wf, bias, cur, arg);
         return hipGetLastError();
     }
     if (g.Ci == 1 && g.H * g.W <= kDirectMaxHW && g.Co <= kDirectMaxCo) {

@@ -759,17 +759,21 @@ def _conv_fwd_gpu(d, x, w, b):
     return _np(cur), _np(arg)
 
 
-# Spike input with Ci * 25 <= 320, Co <= 64 and at most 16 pooled cells per
-# channel runs the one-pass kernel: (5, 12, 12, 12, 64) and (800, ...) at the
-# limits, (2, 3, 9, 11, 5) ragged, (1, 2, 6, 6, 2) one cell, (5, 7, 12, 12,
-# 33) part of a channel tile, (2, 4, 7, 37, 40) a 259-pixel image; past them
-# the gather and the contraction, which pools its own output when it makes one
-# pass over K ((300, 3, 15, 13, 70), 70 channels) or pools after it
-# ((4, 13, 9, 9, 8), 325 columns split over K).
-@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (5, 12, 12, 12, 64), (2, 3, 9, 11, 5),
+# Spike input with Ci * 25 <= 320, Co <= 64, at most 32 pooled cells per
+# channel and images of a whole number of 4-byte words runs the one-pass
+# kernel: (5, 12, 12, 12, 64) and (800, ...) two row tiles per wave at 16
+# cells, (2, 4, 9, 11, 5) ragged, (1, 2, 6, 6, 2) one cell, (5, 7, 12, 12,
+# 33) part of a channel tile, (2, 4, 7, 37, 40) a 259-pixel image, (3, 12,
+# 14, 14, 64) 25 cells and (2, 3, 20, 12, 8) 32 (four row tiles per wave);
+# past them the gather and the contraction, which pools its own output when
+# it makes one pass over K ((300, 3, 15, 13, 70), 70 channels; (2, 3, 9, 11,
+# 5), 297-byte images) or pools after it ((4, 13, 9, 9, 8), 325 columns
+# split over K).
+@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (5, 12, 12, 12, 64), (2, 4, 9, 11, 5),
                                           (1, 2, 6, 6, 2), (800, 12, 12, 12, 64),
                                           (5, 7, 12, 12, 33), (2, 4, 7, 37, 40),
-                                          (300, 3, 15, 13, 70), (4, 13, 9, 9, 8)])
+                                          (3, 12, 14, 14, 64), (2, 3, 20, 12, 8),
+                                          (300, 3, 15, 13, 70), (2, 3, 9, 11, 5), (4, 13, 9, 9, 8)])
 def test_conv_pool_fwd(NB, Ci, H, W, Co):
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=NB * 100 + Co)
     _check_conv_fwd(x, w, b, d)
@@ -834,18 +838,23 @@ def test_conv_pool_ties_first_maximum():
 
 # (3, 8, 11, 12, 16): an odd conv row outside every window.  Both gradients
 # run in one pass each when Ci * 25 <= 320, Co <= 64 and at most 16 pooled
-# cells per channel: (4, 12, 12, 12, 64) and (300, ...) at the limits (more
-# images than compute units: a workgroup takes several), (2, 3, 9, 11, 5)
-# and (3, 8, 11, 12, 16) ragged (6 cells: one 32-row step), (5, 7, 12, 12,
-# 33) half of the second k-step, (3, 5, 9, 21, 24) and (2, 4, 7, 37, 40)
-# images of 189 and 259 pixels (two and one channel groups in the gather);
-# past each limit the gather-and-contraction path: 144 cells (one input
-# channel), 25 cells (2, 4, 14, 14, 8), 70 output channels and 13 * 25 = 325
-# inputs per channel.
-@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (4, 12, 12, 12, 64), (2, 3, 9, 11, 5),
+# cells per channel (the weight gradient up to 32 cells, on images of a
+# whole number of 4-byte words): (4, 12, 12, 12, 64) and (300, ...) at the
+# 16-cell limit (more images than compute units: a workgroup takes
+# several), (2, 4, 9, 11, 5) and (3, 8, 11, 12, 16) ragged (6 and 12 cells),
+# (5, 7, 12, 12, 33) half of the second k-step, (3, 5, 9, 21, 24) and (2, 4,
+# 7, 37, 40) images of 189 and 259 pixels (two and one channel groups in the
+# gather); (3, 12, 14, 14, 64) 25 cells and (2, 3, 20, 12, 8) 32: the weight
+# gradient in one pass, the input gradient on the contraction; past each
+# limit the gather-and-contraction path for both: 144 cells (one input
+# channel), 36 cells (2, 4, 16, 16, 8), 70 output channels, 13 * 25 = 325
+# inputs per channel and 297-byte images (2, 3, 9, 11, 5).
+@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (4, 12, 12, 12, 64), (2, 4, 9, 11, 5),
                                           (3, 8, 11, 12, 16), (300, 12, 12, 12, 64),
                                           (5, 7, 12, 12, 33), (3, 5, 9, 21, 24), (2, 4, 7, 37, 40),
-                                          (2, 4, 14, 14, 8), (2, 2, 8, 8, 70), (2, 13, 9, 9, 8)])
+                                          (3, 12, 14, 14, 64), (2, 3, 20, 12, 8),
+                                          (2, 4, 16, 16, 8), (2, 2, 8, 8, 70), (2, 13, 9, 9, 8),
+                                          (2, 3, 9, 11, 5)])
 def test_conv_pool_bwd(NB, Ci, H, W, Co):
     """Backward given the oracle's pool selection (one byte per pooled current)."""
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=7 * NB + Co)
