@@ -691,10 +691,11 @@ def _conv_one_pass_fw(net, li, fp32_mfma):
 
 def _direct_conv(net, li):
     """Whether layer li's forward runs as the one-kernel convolution and pool
-    on the vector ALUs (mirrors the routing in conv.hip: one input channel,
-    at most 4096 pixels, at most 128 output channels)."""
+    on the vector ALUs (mirrors the routing in conv.hip: at most 4 input
+    channels of 4096 pixels in all, at most 128 output channels)."""
     d = net.descs[li]
-    return d.synapse == 1 and d.c_in == 1 and d.h_in * d.w_in <= 4096 and d.c_out <= 128
+    return (d.synapse == 1 and d.c_in <= 4 and d.c_in * d.h_in * d.w_in <= 4096
+            and d.c_out <= 128)
 
 
 def _narrow_contraction(net, li, fp32_mfma):
@@ -783,7 +784,7 @@ def _stage_kernels(net, name, li, fp32_mfma):
         one, one_w = _conv_one_pass(net, li, fp32_mfma), _conv_one_pass_fw(net, li, fp32_mfma)
         if one_w:
             dw = "conv_dw_kernel + splitk_reduce_wide_kernel"
-        elif d.c_in * 25 <= 50:
+        elif d.c_in * 25 <= 75:
             dw = "conv_dw_small_kernel + splitk_reduce_wide_kernel"
         else:
             dw = "unpool_t_kernel + im2col_t_kernel + contraction"

@@ -18,7 +18,8 @@
 //                order; its d (0..3) is saved for the backward  (pool; the
 //                16-bit contraction does it in its epilogue when it makes one
 //                pass over K, a window being four rows of one lane's tile)
-// One input channel: conv1_pool_kernel computes the pooled currents directly.
+// At most four input channels (the input layer): conv1_pool_kernel computes
+// the pooled currents directly.
 //
 // Backward, given dI = dL/dcur:
 //   dC^T[co][m] = dI[nb, co, py, px] if d is the saved choice, else 0
@@ -236,33 +237,39 @@ __global__ __launch_bounds__(kThreads) void pool_kernel(int Q, int Co, int HW, i
     }
 }
 
-// One input channel (the first layer): the convolution and the pool in one
-// kernel, without the gathered matrix or the unpooled currents.  A workgroup
-// per image stages the image (as fp32) and the weights in LDS; a thread takes
-// pooled currents (co, py, px), pooled column fastest, holds the 6x6 input
-// patch of the window in registers and accumulates the window's four conv
-// outputs tap by tap (ky, kx ascending) with fp32 fma, then adds the bias and
-// keeps the first maximum in window order, as the pool after the contraction.
-constexpr int kDirectMaxHW = 4096;  // image pixels staged in LDS
-constexpr int kDirectMaxCo = 128;  // 14 KiB of padded weights
+// At most four input channels (the input layer): the convolution and the pool
+// in one kernel, without the gathered matrix or the unpooled currents.  A
+// workgroup per image stages the image (as fp32) and the weights in LDS; a
+// thread takes pooled currents (co, py, px), pooled column fastest, holds the
+// 6x6 input patch of the window of one channel at a time in registers and
+// accumulates the window's four conv outputs tap by tap (c, ky, kx ascending)
+// with fp32 fma, then adds the bias and keeps the first maximum in window
+// order, as the pool after the contraction.
+constexpr int kDirectMaxHW = 4096;  // image pixels (all channels) staged in LDS
+constexpr int kDirectMaxCo = 128;
+constexpr int kDirectMaxCi = 4;    // 56 KiB of padded weights at most
 
-template <typename T>
-__global__ __launch_bounds__(kThreads) void conv1_pool_kernel(int H, int W, int Co, int Hp, int Wp,
-                                                              const T *__restrict__ x,
+bool direct_conv(const ConvGeom &g) {
+    return g.Ci <= kDirectMaxCi && g.Ci * g.H * g.W <= kDirectMaxHW && g.Co <= kDirectMaxCo;
+}
+
+template <typename T, int CIM>  // CIM: most input channels (1, or up to kDirectMaxCi)
+__global__ __launch_bounds__(kThreads) void conv1_pool_kernel(int Ci, int H, int W, int Co, int Hp,
+                                                              int Wp, const T *__restrict__ x,
                                                               const float *__restrict__ w,
                                                               const float *__restrict__ bias,
                                                               float *__restrict__ cur,
                                                               uint8_t *__restrict__ arg) {
-    constexpr int WS = 28;  // weights of one output channel, padded to 16 bytes
+    constexpr int WS = 28;  // weights of one (output, input) channel pair, padded to 16 bytes
     __shared__ __attribute__((aligned(16))) float xs[kDirectMaxHW];
-    __shared__ __attribute__((aligned(16))) float wsh[kDirectMaxCo * WS];
+    __shared__ __attribute__((aligned(16))) float wsh[kDirectMaxCo * CIM * WS];
     const int64_t nb = blockIdx.x;
     const int hw = H * W;
-    const T *xi = x + nb * hw;
-    for (int i = threadIdx.x; i < hw; i += kThreads) xs[i] = (float)xi[i];
-    for (int i = threadIdx.x; i < Co * WS; i += kThreads) {
-        const int co = i / WS, t = i - co * WS;
-        wsh[i] = t < KS * KS ? w[co * KS * KS + t] : 0.f;
+    const T *xi = x + nb * Ci * hw;
+    for (int i = threadIdx.x; i < Ci * hw; i += kThreads) xs[i] = (float)xi[i];
+    for (int i = threadIdx.x; i < Co * Ci * WS; i += kThreads) {
+        const int cc = i / WS, t = i - cc * WS;  // cc = co * Ci + c
+        wsh[i] = t < KS * KS ? w[cc * KS * KS + t] : 0.f;
     }
     __syncthreads();
     const bool pairs = (W & 1) == 0;  // patch rows start at even offsets: 8-byte reads
@@ -272,39 +279,41 @@ __global__ __launch_bounds__(kThreads) void conv1_pool_kernel(int H, int W, int 
     for (int o = threadIdx.x; o < total; o += kThreads) {
         const int co = o / cells, p = o - co * cells;
         const int py = p / Wp, px = p - py * Wp;
-        const float *xp = xs + 2 * py * W + 2 * px;
-        float patch[KS + 1][KS + 1];
-        if (pairs) {
-#pragma unroll
-            for (int r = 0; r <= KS; ++r)
-#pragma unroll
-                for (int c = 0; c <= KS; c += 2) {
-                    const float2 v = *reinterpret_cast<const float2 *>(xp + r * W + c);
-                    patch[r][c] = v.x;
-                    patch[r][c + 1] = v.y;
-                }
-        } else {
-#pragma unroll
-            for (int r = 0; r <= KS; ++r)
-#pragma unroll
-                for (int c = 0; c <= KS; ++c) patch[r][c] = xp[r * W + c];
-        }
-        float wv[WS];
-#pragma unroll
-        for (int q = 0; q < WS / 4; ++q) {
-            const float4 v = *reinterpret_cast<const float4 *>(wsh + co * WS + 4 * q);
-            wv[4 * q] = v.x; wv[4 * q + 1] = v.y; wv[4 * q + 2] = v.z; wv[4 * q + 3] = v.w;
-        }
         float acc[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int ci = 0; ci < (CIM == 1 ? 1 : Ci); ++ci) {  // k = (ci, ky, kx) ascending
+            const float *xp = xs + ci * hw + 2 * py * W + 2 * px;
+            float patch[KS + 1][KS + 1];
+            if (pairs) {
 #pragma unroll
-        for (int ky = 0; ky < KS; ++ky)
+                for (int r = 0; r <= KS; ++r)
 #pragma unroll
-            for (int kx = 0; kx < KS; ++kx) {
-                const float wv1 = wv[ky * KS + kx];
+                    for (int c = 0; c <= KS; c += 2) {
+                        const float2 v = *reinterpret_cast<const float2 *>(xp + r * W + c);
+                        patch[r][c] = v.x;
+                        patch[r][c + 1] = v.y;
+                    }
+            } else {
 #pragma unroll
-                for (int d = 0; d < 4; ++d)
-                    acc[d] = __builtin_fmaf(patch[(d >> 1) + ky][(d & 1) + kx], wv1, acc[d]);
+                for (int r = 0; r <= KS; ++r)
+#pragma unroll
+                    for (int c = 0; c <= KS; ++c) patch[r][c] = xp[r * W + c];
             }
+            float wv[WS];
+#pragma unroll
+            for (int q = 0; q < WS / 4; ++q) {
+                const float4 v = *reinterpret_cast<const float4 *>(wsh + (co * Ci + ci) * WS + 4 * q);
+                wv[4 * q] = v.x; wv[4 * q + 1] = v.y; wv[4 * q + 2] = v.z; wv[4 * q + 3] = v.w;
+            }
+#pragma unroll
+            for (int ky = 0; ky < KS; ++ky)
+#pragma unroll
+                for (int kx = 0; kx < KS; ++kx) {
+                    const float wv1 = wv[ky * KS + kx];
+#pragma unroll
+                    for (int d = 0; d < 4; ++d)
+                        acc[d] = __builtin_fmaf(patch[(d >> 1) + ky][(d & 1) + kx], wv1, acc[d]);
+                }
+        }
         const float bco = bias ? bias[co] : 0.f;
         float best = acc[0] + bco;
         int a = 0;
@@ -1011,7 +1020,7 @@ __global__ __launch_bounds__(kDxThreads) void conv_fwd_kernel(
 }
 
 // Weight gradient of a layer with few inputs per channel (Kc = Ci * 25 = KC
-// <= 50: the network's input layer), straight from the pool's selection:
+// <= 75: the network's input layer), straight from the pool's selection:
 //   dW[co][k] = sum over pooled cells of dI times x under the selected output.
 // Block (chunk, co) takes a fixed range of cells; each thread sums its cells
 // in fp32, then a fixed-order tree over the block gives partial[chunk][co][k].
@@ -1066,7 +1075,7 @@ int small_dw_chunks(const ConvGeom &g, int64_t Q) {
     return (int)max((int64_t)1, min(by_cells, by_grid));
 }
 
-bool small_dw(const ConvGeom &g) { return g.Ci * KS * KS <= 50; }
+bool small_dw(const ConvGeom &g) { return g.Ci * KS * KS <= 75; }
 
 // the input gradient by conv_dx_kernel (16-bit cores: not under fp32-only MFMA)
 bool dx_one_pass(const ConvGeom &g, bool allow_split) {
@@ -1188,8 +1197,11 @@ void launch_dw_small(const ConvGeom &g, const ConvDims &v, int chunks, const flo
     if (g.Ci == 1)
         conv_dw_small_kernel<T, 25><<<grid, kThreads, 0, s>>>((int)v.Q, cells, g.Co, g.H, g.W,
                                                               g.Hp, g.Wp, dI, arg, xt, partial);
-    else
+    else if (g.Ci == 2)
         conv_dw_small_kernel<T, 50><<<grid, kThreads, 0, s>>>((int)v.Q, cells, g.Co, g.H, g.W,
+                                                              g.Hp, g.Wp, dI, arg, xt, partial);
+    else
+        conv_dw_small_kernel<T, 75><<<grid, kThreads, 0, s>>>((int)v.Q, cells, g.Co, g.H, g.W,
                                                               g.Hp, g.Wp, dI, arg, xt, partial);
 }
 
@@ -1224,7 +1236,7 @@ hipError_t launch_conv_pool_fwd(const ConvGeom &g, const void *x, int in_dtype, 
     if (v.Mw == 0) return hipSuccess;
     if (ws == nullptr || ws_bytes < conv_fwd_workspace_bytes(g, in_dtype, allow_split))
         return hipErrorInvalidValue;
-    if (!(g.Ci == 1 && g.H * g.W <= kDirectMaxHW && g.Co <= kDirectMaxCo) &&
+    if (!direct_conv(g) &&
         dw_one_pass(g, in_dtype, allow_split)) {
         const unsigned grid = (unsigned)min(g.NB, device_cus());
         const uint8_t *xb = reinterpret_cast<const uint8_t *>(x);
@@ -1237,15 +1249,23 @@ hipError_t launch_conv_pool_fwd(const ConvGeom &g, const void *x, int in_dtype, 
                                                            xb, wf, bias, cur, arg);
         return hipGetLastError();
     }
-    if (g.Ci == 1 && g.H * g.W <= kDirectMaxHW && g.Co <= kDirectMaxCo) {
-        if (in_dtype == SNN_U8)
-            conv1_pool_kernel<uint8_t><<<(unsigned)g.NB, kThreads, 0, s>>>(
-                g.H, g.W, g.Co, g.Hp, g.Wp, reinterpret_cast<const uint8_t *>(x),
-                reinterpret_cast<const float *>(w), bias, cur, arg);
+    if (direct_conv(g)) {
+        const float *wf = reinterpret_cast<const float *>(w);
+        const uint8_t *xu = reinterpret_cast<const uint8_t *>(x);
+        const float *xf = reinterpret_cast<const float *>(x);
+        const unsigned grid = (unsigned)g.NB;
+        if (in_dtype == SNN_U8 && g.Ci == 1)
+            conv1_pool_kernel<uint8_t, 1><<<grid, kThreads, 0, s>>>(g.Ci, g.H, g.W, g.Co, g.Hp,
+                                                                    g.Wp, xu, wf, bias, cur, arg);
+        else if (in_dtype == SNN_U8)
+            conv1_pool_kernel<uint8_t, kDirectMaxCi><<<grid, kThreads, 0, s>>>(
+                g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, xu, wf, bias, cur, arg);
+        else if (g.Ci == 1)
+            conv1_pool_kernel<float, 1><<<grid, kThreads, 0, s>>>(g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp,
+                                                                  xf, wf, bias, cur, arg);
         else
-            conv1_pool_kernel<float><<<(unsigned)g.NB, kThreads, 0, s>>>(
-                g.H, g.W, g.Co, g.Hp, g.Wp, reinterpret_cast<const float *>(x),
-                reinterpret_cast<const float *>(w), bias, cur, arg);
+            conv1_pool_kernel<float, kDirectMaxCi><<<grid, kThreads, 0, s>>>(
+                g.Ci, g.H, g.W, g.Co, g.Hp, g.Wp, xf, wf, bias, cur, arg);
         return hipGetLastError();
     }
     char *p = reinterpret_cast<char *>(ws);

@@ -759,21 +759,25 @@ def _conv_fwd_gpu(d, x, w, b):
     return _np(cur), _np(arg)
 
 
-# Spike input with Ci * 25 <= 320, Co <= 64, at most 32 pooled cells per
-# channel and images of a whole number of 4-byte words runs the one-pass
-# kernel: (5, 12, 12, 12, 64) and (800, ...) two row tiles per wave at 16
-# cells, (2, 4, 9, 11, 5) ragged, (1, 2, 6, 6, 2) one cell, (5, 7, 12, 12,
-# 33) part of a channel tile, (2, 4, 7, 37, 40) a 259-pixel image, (3, 12,
-# 14, 14, 64) 25 cells and (2, 3, 20, 12, 8) 32 (four row tiles per wave);
-# past them the gather and the contraction, which pools its own output when
-# it makes one pass over K ((300, 3, 15, 13, 70), 70 channels; (2, 3, 9, 11,
-# 5), 297-byte images) or pools after it ((4, 13, 9, 9, 8), 325 columns
-# split over K).
-@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (5, 12, 12, 12, 64), (2, 4, 9, 11, 5),
-                                          (1, 2, 6, 6, 2), (800, 12, 12, 12, 64),
-                                          (5, 7, 12, 12, 33), (2, 4, 7, 37, 40),
-                                          (3, 12, 14, 14, 64), (2, 3, 20, 12, 8),
-                                          (300, 3, 15, 13, 70), (2, 3, 9, 11, 5), (4, 13, 9, 9, 8)])
+# Up to 4 input channels of at most 4096 pixels in all, and at most 128
+# output channels, take the direct convolution-and-pool kernel ((3, 1, 28,
+# 28, 12); (1, 2, 6, 6, 2) one cell; (2, 4, 9, 11, 5), (2, 3, 9, 11, 5) and
+# (300, 3, 15, 13, 70) several channels).  Spike input with Ci * 25 <= 320,
+# Co <= 64, at most 32 pooled cells per channel and images of a whole number
+# of 4-byte words runs the one-pass kernel: (5, 12, 12, 12, 64) and (800,
+# ...) two row tiles per wave at 16 cells, (2, 8, 9, 11, 5) ragged, (1, 8, 6,
+# 6, 2) one cell, (5, 7, 12, 12, 33) part of a channel tile, (2, 8, 7, 37,
+# 40) a 259-pixel image, (3, 12, 14, 14, 64) 25 cells and (2, 6, 20, 12, 8)
+# 32 (four row tiles per wave); past them the gather and the contraction,
+# which pools its own output when it makes one pass over K ((300, 5, 15, 13,
+# 70), 70 channels; (2, 5, 9, 11, 5), 495-byte images) or pools after it
+# ((4, 13, 9, 9, 8), 325 columns split over K).
+@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (1, 2, 6, 6, 2), (2, 4, 9, 11, 5),
+                                          (2, 3, 9, 11, 5), (300, 3, 15, 13, 70),
+                                          (5, 12, 12, 12, 64), (2, 8, 9, 11, 5), (1, 8, 6, 6, 2),
+                                          (800, 12, 12, 12, 64), (5, 7, 12, 12, 33),
+                                          (2, 8, 7, 37, 40), (3, 12, 14, 14, 64), (2, 6, 20, 12, 8),
+                                          (300, 5, 15, 13, 70), (2, 5, 9, 11, 5), (4, 13, 9, 9, 8)])
 def test_conv_pool_fwd(NB, Ci, H, W, Co):
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=NB * 100 + Co)
     _check_conv_fwd(x, w, b, d)
@@ -791,6 +795,17 @@ def test_conv_pool_fwd_one_channel(NB, H, W, Co, real):
         x = np.random.default_rng(H).uniform(-1, 1, x.shape).astype(np.float32)
         spec = dict(kind="conv", c_in=1, h=H, w=W, c_out=Co, neuron="leaky", beta=0.5)
         d = snn.layer_desc(spec, 1, NB, in_dtype=snn.F32)
+    _check_conv_fwd(x, w, b, d)
+
+
+@pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 3, 16, 16, 20), (2, 4, 32, 32, 12)])
+def test_conv_pool_fwd_direct_channels_real(NB, Ci, H, W, Co):
+    """Real-valued input to the direct kernel with several input channels
+    (the largest image it stages: 4 x 32 x 32)."""
+    x, w, b, _ = _conv_case(NB, Ci, H, W, Co, seed=NB + Ci + H)
+    x = np.random.default_rng(W).uniform(-1, 1, x.shape).astype(np.float32)
+    spec = dict(kind="conv", c_in=Ci, h=H, w=W, c_out=Co, neuron="leaky", beta=0.5)
+    d = snn.layer_desc(spec, 1, NB, in_dtype=snn.F32)
     _check_conv_fwd(x, w, b, d)
 
 
