@@ -863,13 +863,15 @@ def test_conv_pool_ties_first_maximum():
 # gradient in one pass, the input gradient on the contraction; past each
 # limit the gather-and-contraction path for both: 144 cells (one input
 # channel), 36 cells (2, 4, 16, 16, 8), 70 output channels, 13 * 25 = 325
-# inputs per channel and 297-byte images (2, 3, 9, 11, 5).
+# inputs per channel and 297-byte images (2, 3, 9, 11, 5).  (1100, 12, 12,
+# 12, 64): four or five images per workgroup, through every register set and
+# buffer the kernels alternate.
 @pytest.mark.parametrize("NB,Ci,H,W,Co", [(3, 1, 28, 28, 12), (4, 12, 12, 12, 64), (2, 4, 9, 11, 5),
                                           (3, 8, 11, 12, 16), (300, 12, 12, 12, 64),
                                           (5, 7, 12, 12, 33), (3, 5, 9, 21, 24), (2, 4, 7, 37, 40),
                                           (3, 12, 14, 14, 64), (2, 3, 20, 12, 8),
                                           (2, 4, 16, 16, 8), (2, 2, 8, 8, 70), (2, 13, 9, 9, 8),
-                                          (2, 3, 9, 11, 5)])
+                                          (2, 3, 9, 11, 5), (1100, 12, 12, 12, 64)])
 def test_conv_pool_bwd(NB, Ci, H, W, Co):
     """Backward given the oracle's pool selection (one byte per pooled current)."""
     x, w, b, d = _conv_case(NB, Ci, H, W, Co, seed=7 * NB + Co)
