@@ -637,7 +637,8 @@ __global__ __launch_bounds__(kDxThreads) void conv_dx_kernel(
 }
 
 // ---- weight gradient in one pass ---------------------------------------------
-// For the same layers, on spike input: a workgroup takes one image at a time
+// For the same layers up to 32 pooled cells per channel (128 window rows), on
+// spike images of whole 4-byte words: a workgroup takes one image at a time
 // and accumulates, over all its images,
 //   dW[co][k] = sum_m dC^T[co][m] col[m][k]       (16 x 16 x 32 bf16 MFMA tiles)
 // with dC^T staged in LDS as three exact bf16 parts ([part][co][m]: four
@@ -649,7 +650,8 @@ __global__ __launch_bounds__(kDxThreads) void conv_dx_kernel(
 // in fp32; each workgroup writes its partial sums, which splitk_reduce adds
 // in a fixed order.  Eight waves: wave v takes every output-channel tile and
 // the k tiles v, v + 8, v + 16.  The image and the parts of the next image
-// are loaded during the products and staged after a barrier.
+// are loaded during the products (two images ahead) and staged after a
+// barrier.
 constexpr int kDwMaxGrid = 256;                   // partial sums written
 constexpr int kFwMaxCells = 32;                   // pooled cells per channel for the
                                                   // forward and the weight gradient
@@ -840,7 +842,8 @@ __global__ __launch_bounds__(kDxThreads) void conv_dw_kernel(
 }
 
 // ---- forward in one pass --------------------------------------------------------
-// For the same layers on spike input, without col or C in HBM: a workgroup
+// For the same layers as the weight gradient above (spike images of whole
+// 4-byte words, up to 32 pooled cells), without col or C in HBM: a workgroup
 // takes one image at a time, gathers col[m][k] for its window rows into LDS
 // (bf16 0 / 1, from the image staged there), and computes
 //   C[m][co] = sum_k col[m][k] w[co][k] + bias[co]  (16 x 16 x 32 bf16 MFMA tiles)
