@@ -61,6 +61,14 @@ constexpr int MT_F16 = 1;
 // one LDS object per stage: A tile, then B tile
 __shared__ __attribute__((aligned(1024))) uint16_t g_s0[2 * kStage], g_s1[2 * kStage];
 
+// The bias vector, staged once per workgroup: the epilogue reads its values
+// from LDS, so no global load is pending when the next item starts (a global
+// load there made the compiler wait for every store of the previous tile
+// before the next item's first copies).  Layers with bias take this kernel
+// only up to kBiasLds outputs.
+constexpr int kBiasLds = 8192;
+__shared__ float g_bias[kBiasLds];
+
 template <int S>
 __device__ inline uint16_t *stage_a() {
     if constexpr (S == 0) return g_s0;
@@ -100,7 +108,8 @@ struct TileCopyKC {
     }
     // off: element offset of the plane to copy from (0 for a one-part operand)
     __device__ inline void copy(int k0, int K, uint16_t *stage, int64_t off) const {
-        const int w = threadIdx.x >> 6;
+        // wave-uniform, so the LDS destinations are scalar (M0 set from SGPRs)
+        const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int k = k0 + c8[j];
@@ -136,7 +145,8 @@ struct TileCopyMN {
             col[jj] = min(r0 + 8 * ((lane & 31) ^ mn_swz(kr0 + 2 * jj)), rows - 8);
     }
     __device__ inline void copy(int k0, int K, uint16_t *stage, int64_t off) const {
-        const int w = threadIdx.x >> 6;
+        // wave-uniform, so the LDS destinations are scalar (M0 set from SGPRs)
+        const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int k = min(k0 + kr0 + 2 * j, K - 1);
@@ -435,6 +445,10 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
     const bool wide_stores = ((uintptr_t)C & 15) == 0 && (ldc & 3) == 0 && (split_stride & 3) == 0;
     int item = persistent_item(blockIdx.x, gridDim.x, total, 0);
     if (item < 0) return;
+    if (bias) {
+        for (int i = threadIdx.x; i < N; i += kThreads) g_bias[i] = bias[i];
+        __syncthreads();
+    }
     TileCopy<MN> ca, cb;
     auto setup = [&](int it, int &m0, int &n0, int &zk, int &kbeg, int &kend, int &nk) {
         zk = it / tiles;
@@ -509,15 +523,11 @@ __global__ __launch_bounds__(kThreads, 1) void gemm_async_kernel(
             SNN_ASYNC_STEP(1, 0)
 #undef SNN_ASYNC_STEP
         }
-        // This tile's bias values, loaded before the copies below.  The
-        // copies are issued on every path (after the last item they copy its
-        // first k-tile again, into the free stage 0), so the wait for the
-        // bias values is for all but the copies' 8 loads on every path.
         const int m0c = m0, n0c = n0, zkc = zk;
         float bn[2];
 #pragma unroll
         for (int q = 0; q < 2; ++q)
-            bn[q] = bias ? bias[min(n0c + wn * 64 + q * 32 + (lane & 31), N - 1)] : 0.f;
+            bn[q] = bias ? g_bias[min(n0c + wn * 64 + q * 32 + (lane & 31), N - 1)] : 0.f;
         // the next item's first k-tile, in flight during the stores below
         item = persistent_item(blockIdx.x, gridDim.x, total, j + 1);
         if (item >= 0) setup(item, m0, n0, zk, kbeg, kend, nk);
@@ -616,6 +626,7 @@ bool gemm_async_applies(const GemmArgs &g) {
     if (!g.allow_split || g.a_kc != g.b_kc) return false;
     if (mfma_type(g.a_dtype, g.b_dtype) < 0) return false;
     if (g.K % 8 != 0 || g.K < 256 || g.M < kTile || g.N < kTile) return false;
+    if (g.bias && g.N > kBiasLds) return false;
     if (!g.a_kc && (g.M % 8 != 0 || g.N % 8 != 0)) return false;
     if (g.a_dtype != SNN_U8 && g.a_dtype != SNN_F32 && g.lda % 8 != 0) return false;
     if (g.b_dtype != SNN_U8 && g.b_dtype != SNN_F32 && g.ldb % 8 != 0) return false;

@@ -596,9 +596,12 @@ PATHS = {"split": 0, "fp32mfma": snn.FLAG_FP32_MFMA}
 # weights (12800, 1000, 784) and (12850, 1000, 1000) run its three-plane
 # mode, the latter ragged in M, N and K.  Layers with at most 16 outputs:
 # (12800, 10, 1000) the readout, (5000, 7, 1003) rows not 4-aligned,
-# (777, 16, 1500) and (2000, 10, 4096) long contractions.
+# (777, 16, 1500) and (2000, 10, 4096) long contractions; (600, 8192, 256)
+# the widest layer whose bias the asynchronous kernel stages in LDS, and
+# (520, 8200, 256) one that goes to another kernel for that reason.
 @pytest.mark.parametrize("M,N,K", GEMM_SHAPES + [(12800, 1000, 784), (12850, 1000, 1000),
-                                                 (1040, 1100, 1000),
+                                                 (1040, 1100, 1000), (600, 8192, 256),
+                                                 (520, 8200, 256),
                                                  (12800, 10, 1000), (5000, 7, 1003),
                                                  (777, 16, 1500), (2000, 10, 4096)])
 @pytest.mark.parametrize("wdt", ["f32", "f16"])
